@@ -1,0 +1,169 @@
+"""fp64 CPU oracle for the selective-SSM primal + tangent (JVP) scan.
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, by the smoke check and by
+the benchmark's CPU-baseline leg, never by the product path.  It shares no
+code with the HIP path; both consume arrays from the seeded input module.
+
+Layers
+------
+* ``core``: the per-lane recurrence of Lemma 3.1 (Eq. 3) and the output map,
+  given explicit per-step coefficients (C, fp64, in ``pgf_oracle.c``).
+* ``discretize``: Delta = softplus(x*w_delta + b_delta) and its tangent
+  dDelta_k = sigmoid(z)*w_delta*dx_k (softplus' = sigmoid), per (b,t,d).  The
+  selective step size follows the Mamba parameterisation the paper studies
+  (Sec. 3; Lemma 3.1 makes Delta a function of the input).
+* ``project``: B_t = x_t W_B (+ b_B), C_t = x_t W_C (+ b_C) and their tangents
+  dB_k = dx_k W_B, dC_k = dx_k W_C (selective input/output maps, Sec. 3).
+* ``scan_jvp``: the three above over L-chunks with the state carried between
+  chunks (the block hand-off of Alg. 1), optionally for a subset of channels.
+
+Precision: everything in fp64 from the exact fp32 / bf16 input values.
+Library routines used as steps: numpy.logaddexp (softplus), scipy expit
+(sigmoid), numpy matmul (projections), libm exp (transition).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+from scipy.special import expit
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "pgf_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(verbose: bool = False) -> str:
+    """Compile the C core into oracle/liboracle.so (always recompiles)."""
+    cmd = ["gcc", "-O2", "-fno-fast-math", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
+           "-std=c11", "-Wall", "-Wextra", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    dp = ctypes.POINTER(ctypes.c_double)
+    i64 = ctypes.c_int64
+    lib.pgf_oracle_core.restype = ctypes.c_int
+    lib.pgf_oracle_core.argtypes = [i64] * 5 + [dp] * 13 + [ctypes.c_int]
+    _lib = lib
+    return lib
+
+
+def _dp(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _threads() -> int:
+    return int(os.environ.get("PGF_ORACLE_THREADS", "0"))
+
+
+def core(A, x, dx, delta, ddelta, Bm, Cm, dBm, dCm, h=None, dh=None, nthreads=None):
+    """Run the recurrence.  Shapes: A [D,N]; x, delta [B,L,D]; dx, ddelta
+    [K,B,L,D]; Bm, Cm [B,L,N]; dBm, dCm [K,B,L,N]; h [B,D,N]; dh [K,B,D,N].
+    Returns (y [B,L,D], dy [K,B,L,D], h_out, dh_out), all fp64."""
+    lib = _load()
+    A = _f64(A)
+    x, dx, delta, ddelta = _f64(x), _f64(dx), _f64(delta), _f64(ddelta)
+    Bm, Cm, dBm, dCm = _f64(Bm), _f64(Cm), _f64(dBm), _f64(dCm)
+    K, B, L, D = dx.shape
+    N = A.shape[1]
+    assert A.shape == (D, N) and x.shape == (B, L, D) and delta.shape == (B, L, D)
+    assert ddelta.shape == (K, B, L, D) and Bm.shape == (B, L, N) and Cm.shape == (B, L, N)
+    assert dBm.shape == (K, B, L, N) and dCm.shape == (K, B, L, N)
+    h = np.zeros((B, D, N)) if h is None else np.array(h, dtype=np.float64, copy=True, order="C")
+    dh = np.zeros((K, B, D, N)) if dh is None else np.array(dh, dtype=np.float64, copy=True, order="C")
+    assert h.shape == (B, D, N) and dh.shape == (K, B, D, N)
+    y = np.empty((B, L, D))
+    dy = np.empty((K, B, L, D))
+    rc = lib.pgf_oracle_core(B, L, D, N, K, _dp(A), _dp(x), _dp(dx), _dp(delta), _dp(ddelta),
+                             _dp(Bm), _dp(Cm), _dp(dBm), _dp(dCm), _dp(h), _dp(dh), _dp(y), _dp(dy),
+                             _threads() if nthreads is None else nthreads)
+    if rc != 0:
+        raise RuntimeError("pgf_oracle_core failed")
+    return y, dy, h, dh
+
+
+def discretize(x, dx, w_delta, b_delta):
+    """Delta = softplus(z), dDelta_k = sigmoid(z) * w_delta * dx_k with
+    z = x*w_delta + b_delta, per (b,t,d).  x [B,L,D], dx [K,B,L,D]."""
+    x = _f64(x)
+    w = _f64(w_delta)
+    z = x * w + _f64(b_delta)
+    delta = np.logaddexp(0.0, z)
+    sw = expit(z) * w
+    ddelta = sw[None] * _f64(dx)
+    return delta, ddelta
+
+
+def project(x, dx, W_B, W_C, b_B=None, b_C=None):
+    """B = x W_B (+b_B), C = x W_C (+b_C), dB_k = dx_k W_B, dC_k = dx_k W_C.
+    x [B,L,D] -> [B,L,N]; dx [K,B,L,D] -> [K,B,L,N]."""
+    x, dx = _f64(x), _f64(dx)
+    WB, WC = _f64(W_B), _f64(W_C)
+    Bm = x @ WB
+    Cm = x @ WC
+    if b_B is not None:
+        Bm = Bm + _f64(b_B)
+    if b_C is not None:
+        Cm = Cm + _f64(b_C)
+    return Bm, Cm, dx @ WB, dx @ WC
+
+
+def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nthreads=None):
+    """Full model: discretization, projections, recurrence, over L-chunks.
+
+    x [B,L,D], dx [K,B,L,D] (any float dtype; converted exactly to fp64).
+    params: dict with A, w_delta, b_delta, W_B, W_C and optional b_B, b_C.
+    channels: optional 1-D index array of channels d to compute (the
+    projections still use every channel).  h_in [B,D,N] / dh_in [K,B,D,N]
+    are over all D channels (or only the selected ones if shaped so).
+    Returns (y [B,L,Dsel], dy [K,B,L,Dsel], h_out [B,Dsel,N], dh_out).
+    """
+    K, B, L, D = dx.shape
+    A = _f64(params["A"])
+    N = A.shape[1]
+    sel = np.arange(D) if channels is None else np.asarray(channels, dtype=np.int64)
+    Ds = len(sel)
+    h = np.zeros((B, Ds, N)) if h_in is None else _f64(h_in)
+    dh = np.zeros((K, B, Ds, N)) if dh_in is None else _f64(dh_in)
+    if h.shape[1] == D and Ds != D:
+        h = h[:, sel]
+    if dh.shape[2] == D and Ds != D:
+        dh = dh[:, :, sel]
+    y = np.empty((B, L, Ds))
+    dy = np.empty((K, B, L, Ds))
+    step = L if not chunk else int(chunk)
+    step = max(step, 1)
+    w = _f64(params["w_delta"])[sel]
+    bd = _f64(params["b_delta"])[sel]
+    As = A[sel]
+    for t0 in range(0, L, step):
+        t1 = min(L, t0 + step)
+        xc = _f64(x[:, t0:t1])
+        dxc = _f64(dx[:, :, t0:t1])
+        Bm, Cm, dBm, dCm = project(xc, dxc, params["W_B"], params["W_C"],
+                                   params.get("b_B"), params.get("b_C"))
+        xs = np.ascontiguousarray(xc[..., sel])
+        dxs = np.ascontiguousarray(dxc[..., sel])
+        delta, ddelta = discretize(xs, dxs, w, bd)
+        yc, dyc, h, dh = core(As, xs, dxs, delta, ddelta, Bm, Cm, dBm, dCm, h, dh, nthreads)
+        y[:, t0:t1] = yc
+        dy[:, :, t0:t1] = dyc
+    return y, dy, h, dh

@@ -1,0 +1,124 @@
+/*
+ * Plain, slow, sequential fp64 oracle for the primal + tangent (forward-mode
+ * JVP) scan of a selective diagonal SSM.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the tests, the smoke check and the CPU-baseline leg of
+ * the benchmark do.  It shares no code with the HIP path.
+ *
+ * What it computes (paper Sec. 3, Lemma 3.1 "Selectivity Jacobian", Eq. 3,
+ * and the chain-rule terms of the equivalence proof in Sec. 4.1):
+ *
+ *   for every lane (b, d, n), sequentially in t = 0 .. L-1:
+ *     Abar   = exp(Delta[t] * A[d,n])                 zero-order-hold transition
+ *     b_t    = Delta[t] * B[t,n] * x[t]               input drive
+ *     K_t,k  = Abar * A[d,n] * dDelta_k[t]            derivative of Abar along dx_k
+ *     j_t,k  = dDelta_k[t]*B[t,n]*x[t]                derivative of b_t along dx_k
+ *            + Delta[t]*dB_k[t,n]*x[t]
+ *            + Delta[t]*B[t,n]*dx_k[t]
+ *     h'     = Abar*h + b_t                           primal recurrence
+ *     dh'_k  = Abar*dh_k + K_t,k*h + j_t,k            tangent recurrence (Eq. 3)
+ *   and per (b, t, d), summing n = 0 .. N-1 in order:
+ *     y      = sum_n C[t,n] * h'[n]                   output map with identity
+ *                                                     activation, no residual
+ *     dy_k   = sum_n dC_k[t,n]*h'[n] + C[t,n]*dh'_k[n]
+ *
+ * dC_k*h' is the derivative of the output map through C; the paper's output
+ * variation (Eq. 2) omits it, but the map y = C(x) h is differentiated here in
+ * full.  The per-step coefficients Delta, dDelta_k, B, C, dB_k, dC_k are
+ * inputs: the caller derives them from x and the model parameters.
+ *
+ * Build: -O2 -fno-fast-math -ffp-contract=off -fopenmp.  Parallel over lanes
+ * (b, d) only; t stays sequential.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/*
+ * Shapes (all row-major, double):
+ *   A [D,N]; x, delta [B,L,D]; dx, ddelta [K,B,L,D];
+ *   Bm, Cm [B,L,N]; dBm, dCm [K,B,L,N];
+ *   h [B,D,N] and dh [K,B,D,N]: entry state on input, exit state on output;
+ *   y [B,L,D]; dy [K,B,L,D].
+ * Returns 0, or -1 on a bad argument or allocation failure.
+ */
+int pgf_oracle_core(int64_t B, int64_t L, int64_t D, int64_t N, int64_t K,
+                    const double *A, const double *x, const double *dx,
+                    const double *delta, const double *ddelta,
+                    const double *Bm, const double *Cm,
+                    const double *dBm, const double *dCm,
+                    double *h, double *dh, double *y, double *dy,
+                    int nthreads)
+{
+    if (B < 0 || L < 0 || D < 0 || N <= 0 || K <= 0) return -1;
+    if (!A || !h || !dh) return -1;
+    if (L > 0 && (!x || !dx || !delta || !ddelta || !Bm || !Cm || !dBm || !dCm || !y || !dy))
+        return -1;
+    int bad = 0;
+    const int64_t lanes = B * D;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t lane = 0; lane < lanes; ++lane) {
+        const int64_t b = lane / D, d = lane % D;
+        double *hs = (double *)malloc(sizeof(double) * (size_t)N);
+        double *dhs = (double *)malloc(sizeof(double) * (size_t)(N * K));
+        double *dyk = (double *)malloc(sizeof(double) * (size_t)K);
+        if (!hs || !dhs || !dyk) {
+#pragma omp atomic write
+            bad = 1;
+            free(hs); free(dhs); free(dyk);
+            continue;
+        }
+        /* entry state */
+        for (int64_t n = 0; n < N; ++n) hs[n] = h[(b * D + d) * N + n];
+        for (int64_t k = 0; k < K; ++k)
+            for (int64_t n = 0; n < N; ++n) dhs[k * N + n] = dh[((k * B + b) * D + d) * N + n];
+
+        for (int64_t t = 0; t < L; ++t) {
+            const int64_t btd = (b * L + t) * D + d;
+            const double xt = x[btd], dl = delta[btd];
+            const double *Bt = Bm + (b * L + t) * N;
+            const double *Ct = Cm + (b * L + t) * N;
+            double yt = 0.0;
+            for (int64_t k = 0; k < K; ++k) dyk[k] = 0.0;
+            for (int64_t n = 0; n < N; ++n) {
+                const double a = A[d * N + n];
+                const double abar = exp(dl * a);
+                const double bt = dl * Bt[n] * xt;
+                const double hprev = hs[n];
+                const double hnew = abar * hprev + bt;
+                for (int64_t k = 0; k < K; ++k) {
+                    const int64_t kbtd = ((k * B + b) * L + t) * D + d;
+                    const int64_t kbtn = ((k * B + b) * L + t) * N + n;
+                    const double ddl = ddelta[kbtd], dxt = dx[kbtd];
+                    const double Kt = abar * a * ddl;
+                    const double jt = ddl * Bt[n] * xt + dl * dBm[kbtn] * xt + dl * Bt[n] * dxt;
+                    const double dhnew = abar * dhs[k * N + n] + Kt * hprev + jt;
+                    dhs[k * N + n] = dhnew;
+                    dyk[k] += dCm[kbtn] * hnew + Ct[n] * dhnew;
+                }
+                hs[n] = hnew;
+                yt += Ct[n] * hnew;
+            }
+            y[btd] = yt;
+            for (int64_t k = 0; k < K; ++k) dy[((k * B + b) * L + t) * D + d] = dyk[k];
+        }
+        /* exit state */
+        for (int64_t n = 0; n < N; ++n) h[(b * D + d) * N + n] = hs[n];
+        for (int64_t k = 0; k < K; ++k)
+            for (int64_t n = 0; n < N; ++n) dh[((k * B + b) * D + d) * N + n] = dhs[k * N + n];
+        free(hs); free(dhs); free(dyk);
+    }
+    return bad ? -1 : 0;
+}

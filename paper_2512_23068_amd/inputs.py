@@ -1,0 +1,182 @@
+"""Seeded synthetic inputs for the selective-SSM primal + tangent scan.
+
+This module holds no arithmetic of the method itself: only random draws,
+the parameter recipes of the five benchmark workloads and the fp32 -> bf16
+rounding of inputs.  Both the HIP path and the CPU oracle consume the arrays
+it returns, so it must stay free of anything either side computes.
+
+Workloads (all synthetic; the paper's experiments are synthetic L- and
+D-sweeps, a 128k-step impulse ("ghost pulse") probe and a stiffness sweep,
+Sec. 5 and App. A-B):
+
+  tiny      B=1  L=1024    D=16    N=16 K=1  f32   dx = unit impulse at t=0, d=0
+  mamba130m B=1  L=8192    D=1536  N=16 K=1  f32   dx ~ N(0,1)
+  pulse128k B=1  L=131072  D=1536  N=16 K=1  f32   dx = unit impulse at t=0, all d
+  stiff128k B=1  L=131072  D=5120  N=16 K=1  bf16  dx ~ N(0,1)   (stiff A, wide Delta)
+  multidir  B=4  L=32768   D=2048  N=64 K=8  f32   dx_k ~ N(0,1)
+
+Parameter recipe (per workload index i, rng = default_rng([23068, i]),
+drawn in this order):
+  1. A[d,n]: stiff128k only, A = -exp(U(0,7)), shape [D,N].  Otherwise the
+     S4D-real pattern A[d,n] = -(n+1) (multidir: -(n+1)/8), broadcast over d.
+  2. w_delta ~ N(0,1), shape [D].
+  3. v = exp(U(ln lo, ln hi)), shape [D]; b_delta = log(expm1(v)) so that
+     softplus(b_delta) = v is log-uniform in [lo, hi].
+  4. W_B, W_C ~ N(0,1)/sqrt(D), shape [D,N].
+Sequences x [B,L,D] and dx [K,B,L,D] are drawn in blocks of ROWS_PER_BLOCK
+time rows, each block from default_rng([23068, i, stream, b, block]) with
+stream 0 for x and 1+k for dx_k, so the values do not depend on how many
+threads generate them.  bf16 workloads round the fp32 draws to bf16 with
+round-to-nearest-even; the oracle then reads those exact bf16 values.
+"""
+from __future__ import annotations
+
+import dataclasses
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+SEED_ROOT = 23068
+ROWS_PER_BLOCK = 256
+
+
+@dataclasses.dataclass(frozen=True)
+class ScanConfig:
+    name: str
+    index: int          # seed index of the workload
+    batch: int
+    seqlen: int
+    d_inner: int
+    d_state: int
+    n_dirs: int
+    delta_lo: float
+    delta_hi: float
+    a_kind: str         # "s4d" | "s4d_over8" | "stiff"
+    dx_kind: str        # "impulse_t0_d0" | "impulse_t0_all" | "normal" | "zero"
+    in_dtype: str       # "f32" | "bf16"
+
+    def with_(self, **kw) -> "ScanConfig":
+        return dataclasses.replace(self, **kw)
+
+    @property
+    def tok_ch(self) -> int:
+        return self.batch * self.seqlen * self.d_inner
+
+
+CONFIGS = [
+    ScanConfig("tiny", 0, 1, 1024, 16, 16, 1, 1e-3, 1e-1, "s4d", "impulse_t0_d0", "f32"),
+    ScanConfig("mamba130m", 1, 1, 8192, 1536, 16, 1, 1e-3, 1e-1, "s4d", "normal", "f32"),
+    ScanConfig("pulse128k", 2, 1, 131072, 1536, 16, 1, 1e-4, 1e-2, "s4d", "impulse_t0_all", "f32"),
+    ScanConfig("stiff128k", 3, 1, 131072, 5120, 16, 1, 1e-3, 10.0, "stiff", "normal", "bf16"),
+    ScanConfig("multidir", 4, 4, 32768, 2048, 64, 8, 1e-3, 1e-1, "s4d_over8", "normal", "f32"),
+]
+BY_NAME = {c.name: c for c in CONFIGS}
+
+
+def get_config(key) -> ScanConfig:
+    if isinstance(key, ScanConfig):
+        return key
+    if isinstance(key, int):
+        return CONFIGS[key]
+    return BY_NAME[key]
+
+
+def make_params(cfg: ScanConfig) -> dict:
+    """Model parameters of a workload as float32 numpy arrays."""
+    D, N = cfg.d_inner, cfg.d_state
+    rng = np.random.default_rng([SEED_ROOT, cfg.index])
+    if cfg.a_kind == "stiff":
+        A = -np.exp(rng.uniform(0.0, 7.0, size=(D, N)))
+    elif cfg.a_kind == "s4d":
+        A = -np.broadcast_to(np.arange(1, N + 1, dtype=np.float64), (D, N))
+    elif cfg.a_kind == "s4d_over8":
+        A = -np.broadcast_to(np.arange(1, N + 1, dtype=np.float64) / 8.0, (D, N))
+    else:
+        raise ValueError(cfg.a_kind)
+    w_delta = rng.standard_normal(D)
+    v = np.exp(rng.uniform(np.log(cfg.delta_lo), np.log(cfg.delta_hi), size=D))
+    b_delta = np.log(np.expm1(v))
+    W_B = rng.standard_normal((D, N)) / np.sqrt(D)
+    W_C = rng.standard_normal((D, N)) / np.sqrt(D)
+    f = lambda a: np.ascontiguousarray(a, dtype=np.float32)
+    return dict(A=f(A), w_delta=f(w_delta), b_delta=f(b_delta), W_B=f(W_B), W_C=f(W_C))
+
+
+def round_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bit patterns (uint16), round to nearest even (finite inputs)."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    return (bits.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _normal_rows(out: np.ndarray, cfg: ScanConfig, stream: int, b: int, threads: int) -> None:
+    """Fill out[L, D] (float32) with N(0,1) draws, block-seeded."""
+    L = out.shape[0]
+    nblk = (L + ROWS_PER_BLOCK - 1) // ROWS_PER_BLOCK
+
+    def work(blk):
+        r0 = blk * ROWS_PER_BLOCK
+        r1 = min(L, r0 + ROWS_PER_BLOCK)
+        g = np.random.default_rng([SEED_ROOT, cfg.index, stream, b, blk])
+        g.standard_normal(out=out[r0:r1], dtype=np.float32)
+
+    if threads <= 1 or nblk == 1:
+        for blk in range(nblk):
+            work(blk)
+    else:
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            list(ex.map(work, range(nblk)))
+
+
+def _threads() -> int:
+    return max(1, min(16, int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))))
+
+
+def make_x(cfg: ScanConfig, threads: int | None = None) -> np.ndarray:
+    """x [B,L,D] float32 (values already rounded to bf16 for bf16 workloads)."""
+    threads = threads or _threads()
+    x = np.empty((cfg.batch, cfg.seqlen, cfg.d_inner), dtype=np.float32)
+    for b in range(cfg.batch):
+        _normal_rows(x[b], cfg, 0, b, threads)
+    if cfg.in_dtype == "bf16":
+        x = bf16_bits_to_f32(round_to_bf16_bits(x)).reshape(x.shape)
+    return x
+
+
+def make_dx(cfg: ScanConfig, threads: int | None = None) -> np.ndarray:
+    """dx [K,B,L,D] float32 (bf16-rounded values for bf16 workloads)."""
+    threads = threads or _threads()
+    K, B, L, D = cfg.n_dirs, cfg.batch, cfg.seqlen, cfg.d_inner
+    dx = np.zeros((K, B, L, D), dtype=np.float32)
+    if cfg.dx_kind == "normal":
+        for k in range(K):
+            for b in range(B):
+                _normal_rows(dx[k, b], cfg, 1 + k, b, threads)
+        if cfg.in_dtype == "bf16":
+            dx = bf16_bits_to_f32(round_to_bf16_bits(dx)).reshape(dx.shape)
+    elif cfg.dx_kind == "impulse_t0_d0":
+        if L > 0:
+            dx[:, :, 0, 0] = 1.0
+    elif cfg.dx_kind == "impulse_t0_all":
+        if L > 0:
+            dx[:, :, 0, :] = 1.0
+    elif cfg.dx_kind == "zero":
+        pass
+    else:
+        raise ValueError(cfg.dx_kind)
+    return dx
+
+
+def make_inputs(key, threads: int | None = None) -> dict:
+    """All inputs of a workload: params plus x, dx (float32 numpy arrays)."""
+    cfg = get_config(key)
+    out = make_params(cfg)
+    out["x"] = make_x(cfg, threads)
+    out["dx"] = make_dx(cfg, threads)
+    out["cfg"] = cfg
+    return out

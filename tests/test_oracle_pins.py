@@ -1,0 +1,322 @@
+"""Pins of the fp64 oracle against facts that do not come from the oracle.
+
+Each test fixes part of the oracle with something independent of its own
+formula: closed forms (LTI impulse response), a different formula for the same
+quantity (the materialised quadratic kernel), finite differences, torch
+autograd in forward and reverse mode, linearity, the semigroup composition of
+the augmented operator (Prop. 3.2, Eq. 4-5) and exact causality (Sec. 5.3).
+A dropped chain-rule term, a wrong sign or index, or a transposed operand in
+the oracle fails at least one of them.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+
+torch.set_default_dtype(torch.float64)
+
+
+def rand_problem(seed, B=1, L=10, D=3, N=4, K=2, stiff=False, bias=False, zscale=1.0):
+    g = np.random.default_rng(seed)
+    if stiff:
+        A = -np.exp(g.uniform(0, 7, size=(D, N)))
+    else:
+        A = -g.uniform(0.1, 2.0, size=(D, N))
+    p = dict(A=A,
+             w_delta=g.standard_normal(D) * zscale,
+             b_delta=g.uniform(-3, 1, size=D),
+             W_B=g.standard_normal((D, N)) / np.sqrt(D),
+             W_C=g.standard_normal((D, N)) / np.sqrt(D))
+    if bias:
+        p["b_B"] = g.standard_normal(N)
+        p["b_C"] = g.standard_normal(N)
+    x = g.standard_normal((B, L, D))
+    dx = g.standard_normal((K, B, L, D))
+    return p, x, dx
+
+
+def relerr(a, b):
+    return np.linalg.norm((a - b).ravel()) / max(np.linalg.norm(np.ravel(b)), 1e-300)
+
+
+# ---------------------------------------------------------------- primal pins
+
+def test_lti_impulse_closed_form():
+    """Constant Delta, B, C (w_delta = 0, W = 0, biases set) and x an impulse
+    at t=0: y_t = sum_n C_n exp(t*Delta*A_n) Delta B_n, the impulse response of
+    the discretised LTI system (Lemma 3.1 with constant coefficients)."""
+    D, N, L = 3, 5, 40
+    g = np.random.default_rng(1)
+    A = -g.uniform(0.05, 3.0, size=(D, N))
+    bd = g.uniform(-2, 1, size=D)
+    p = dict(A=A, w_delta=np.zeros(D), b_delta=bd, W_B=np.zeros((D, N)), W_C=np.zeros((D, N)),
+             b_B=g.standard_normal(N), b_C=g.standard_normal(N))
+    x = np.zeros((1, L, D)); x[0, 0, :] = 1.0
+    s = 7  # tangent impulse at t = s
+    dx = np.zeros((1, 1, L, D)); dx[0, 0, s, :] = 1.0
+    y, dy, _, _ = oracle.scan_jvp(x, dx, p)
+    delta = np.log1p(np.exp(bd))  # softplus of the constant pre-activation
+    t = np.arange(L)[:, None, None]
+    resp = (p["b_C"][None, None, :] * np.exp(t * delta[None, :, None] * A[None]) *
+            delta[None, :, None] * p["b_B"][None, None, :]).sum(-1)      # [L, D]
+    assert relerr(y[0], resp) < 1e-13
+    # Tangent: with w_delta = 0 and W = 0 only the drive term Delta*B*dx
+    # survives, so dy is the same system's response to dx (the tangent flow
+    # is a copy of the primal dynamics): dy_t = resp_{t-s} for t >= s.
+    exp_dy = np.zeros((L, D)); exp_dy[s:] = resp[:L - s]
+    assert relerr(dy[0, 0], exp_dy) < 1e-13
+    assert np.all(dy[0, 0, :s] == 0.0)
+
+
+def _quadratic_primal(p, x):
+    """y_t = sum_{s<=t} sum_n C_{t,n} exp(A_n (S_t - S_s)) Delta_s B_{s,n} x_s,
+    S_t = sum_{tau<=t} Delta_tau: the recurrence unrolled into its kernel."""
+    xt = torch.tensor(x)
+    z = xt * torch.tensor(p["w_delta"]) + torch.tensor(p["b_delta"])
+    delta = torch.logaddexp(z, torch.zeros(()))
+    Bm = xt @ torch.tensor(p["W_B"])
+    Cm = xt @ torch.tensor(p["W_C"])
+    if "b_B" in p:
+        Bm = Bm + torch.tensor(p["b_B"])
+        Cm = Cm + torch.tensor(p["b_C"])
+    S = torch.cumsum(delta, dim=1)                        # [B, L, D]
+    A = torch.tensor(p["A"])                              # [D, N]
+    diff = S[:, :, None, :] - S[:, None, :, :]            # [B, t, s, D]
+    L = x.shape[1]
+    mask = torch.tril(torch.ones(L, L, dtype=torch.bool))[None, :, :, None, None]
+    decay = torch.exp(diff[..., None] * A)                # [B, t, s, D, N]
+    decay = torch.where(mask, decay, torch.zeros(()))
+    drive = (delta * xt)[:, None, :, :, None] * Bm[:, None, :, None, :]  # [B,1,s,1,N]
+    y = (Cm[:, :, None, None, :] * decay * drive).sum(dim=(2, 4))
+    return y
+
+
+@pytest.mark.parametrize("seed,bias", [(2, False), (3, True)])
+def test_quadratic_kernel_form(seed, bias):
+    p, x, dx = rand_problem(seed, B=2, L=14, D=3, N=4, K=1, bias=bias)
+    y, _, _, _ = oracle.scan_jvp(x, dx, p)
+    yq = _quadratic_primal(p, x).numpy()
+    assert relerr(y, yq) < 1e-12
+
+
+def test_softplus_identities():
+    """Delta = softplus(z): softplus(z) - softplus(-z) = z, softplus(0) = ln 2,
+    and dDelta = sigmoid(z) * w * dx is the derivative of Delta (central
+    differences)."""
+    z = np.linspace(-30, 30, 601)
+    x = z[None, :, None]
+    one = np.ones(1)
+    d_pos, _ = oracle.discretize(x, np.zeros((1,) + x.shape), one, np.zeros(1))
+    d_neg, _ = oracle.discretize(-x, np.zeros((1,) + x.shape), one, np.zeros(1))
+    assert np.allclose(d_pos - d_neg, x, rtol=0, atol=1e-13)
+    d0, _ = oracle.discretize(np.zeros((1, 1, 1)), np.zeros((1, 1, 1, 1)), one, np.zeros(1))
+    assert abs(d0[0, 0, 0] - np.log(2.0)) < 1e-16
+    g = np.random.default_rng(4)
+    w, bd = g.standard_normal(3), g.standard_normal(3)
+    x = g.standard_normal((1, 5, 3)) * 3
+    dx = g.standard_normal((1, 1, 5, 3))
+    eps = 1e-6
+    dp, _ = oracle.discretize(x + eps * dx[0], dx, w, bd)
+    dm, _ = oracle.discretize(x - eps * dx[0], dx, w, bd)
+    _, dd = oracle.discretize(x, dx, w, bd)
+    assert relerr(dd[0], (dp - dm) / (2 * eps)) < 1e-8
+
+
+def test_projection_bruteforce():
+    """B_t[n] = sum_d x_t[d] W_B[d,n] (+ b_B[n]) by an explicit double loop."""
+    g = np.random.default_rng(5)
+    x = g.standard_normal((2, 3, 4)); dx = g.standard_normal((2, 2, 3, 4))
+    WB, WC = g.standard_normal((4, 5)), g.standard_normal((4, 5))
+    bB, bC = g.standard_normal(5), g.standard_normal(5)
+    Bm, Cm, dBm, dCm = oracle.project(x, dx, WB, WC, bB, bC)
+    for b in range(2):
+        for t in range(3):
+            for n in range(5):
+                sB = bB[n] + sum(x[b, t, d] * WB[d, n] for d in range(4))
+                sC = bC[n] + sum(x[b, t, d] * WC[d, n] for d in range(4))
+                assert abs(Bm[b, t, n] - sB) < 1e-13 and abs(Cm[b, t, n] - sC) < 1e-13
+                for k in range(2):
+                    sdB = sum(dx[k, b, t, d] * WB[d, n] for d in range(4))
+                    sdC = sum(dx[k, b, t, d] * WC[d, n] for d in range(4))
+                    assert abs(dBm[k, b, t, n] - sdB) < 1e-13 and abs(dCm[k, b, t, n] - sdC) < 1e-13
+
+
+# ---------------------------------------------------------------- tangent pins
+
+@pytest.mark.parametrize("seed,stiff", [(6, False), (7, True)])
+def test_tangent_central_differences(seed, stiff):
+    """dy_k equals the central difference of the primal along dx_k."""
+    p, x, dx = rand_problem(seed, B=2, L=24, D=3, N=4, K=2, stiff=stiff, bias=True)
+    _, dy, _, _ = oracle.scan_jvp(x, dx, p)
+    eps = 1e-6
+    for k in range(2):
+        yp, _, _, _ = oracle.scan_jvp(x + eps * dx[k], dx, p)
+        ym, _, _, _ = oracle.scan_jvp(x - eps * dx[k], dx, p)
+        fd = (yp - ym) / (2 * eps)
+        assert relerr(dy[k], fd) < 2e-8, k
+
+
+def _torch_primal(p, xt):
+    """The selective scan written as a plain torch loop (for autograd)."""
+    w = torch.tensor(p["w_delta"]); bd = torch.tensor(p["b_delta"])
+    A = torch.tensor(p["A"])
+    z = xt * w + bd
+    delta = torch.logaddexp(z, torch.zeros(()))
+    Bm = xt @ torch.tensor(p["W_B"])
+    Cm = xt @ torch.tensor(p["W_C"])
+    if "b_B" in p:
+        Bm = Bm + torch.tensor(p["b_B"]); Cm = Cm + torch.tensor(p["b_C"])
+    Bsz, L, D = xt.shape
+    h = torch.zeros(Bsz, D, A.shape[1])
+    ys = []
+    for t in range(L):
+        dl = delta[:, t, :, None]
+        h = torch.exp(dl * A) * h + dl * Bm[:, t, None, :] * xt[:, t, :, None]
+        ys.append((h * Cm[:, t, None, :]).sum(-1))
+    return torch.stack(ys, 1)
+
+
+def test_tangent_forward_mode_autograd():
+    """Prop. 4.1: the tangent flow equals the autograd JVP."""
+    p, x, dx = rand_problem(8, B=2, L=9, D=3, N=3, K=3, bias=True)
+    _, dy, _, _ = oracle.scan_jvp(x, dx, p)
+    f = lambda xt: _torch_primal(p, xt)
+    for k in range(3):
+        _, jv = torch.func.jvp(f, (torch.tensor(x),), (torch.tensor(dx[k]),))
+        assert relerr(dy[k], jv.numpy()) < 1e-12
+
+
+def test_tangent_reverse_mode_jacobian_and_adjoint():
+    """Full Jacobian by reverse mode on a tiny case: J dx equals dy, and the
+    adjoint identity <w, J dx> = <J^T w, dx> holds."""
+    p, x, dx = rand_problem(9, B=1, L=6, D=3, N=2, K=1)
+    _, dy, _, _ = oracle.scan_jvp(x, dx, p)
+    J = torch.autograd.functional.jacobian(lambda xt: _torch_primal(p, xt), torch.tensor(x))
+    J = J.reshape(6 * 3, 6 * 3).numpy()
+    jdx = (J @ dx[0].reshape(-1)).reshape(1, 6, 3)
+    assert relerr(dy[0], jdx) < 1e-12
+    wv = np.random.default_rng(10).standard_normal(18)
+    assert abs(wv @ dy[0].reshape(-1) - (J.T @ wv) @ dx[0].reshape(-1)) < 1e-12 * np.abs(wv).sum() * np.abs(dy).max()
+    # causality: the Jacobian is block lower-triangular in time
+    Jb = J.reshape(6, 3, 6, 3)
+    for t in range(6):
+        assert np.all(Jb[t, :, t + 1:, :] == 0.0)
+
+
+def test_linearity_and_direction_independence():
+    p, x, dx = rand_problem(11, B=1, L=20, D=4, N=3, K=2)
+    _, dy2, _, _ = oracle.scan_jvp(x, dx, p)
+    a, b = 0.7, -1.9
+    comb = (a * dx[0] + b * dx[1])[None]
+    _, dyc, _, _ = oracle.scan_jvp(x, comb, p)
+    assert relerr(dyc[0], a * dy2[0] + b * dy2[1]) < 1e-13
+    for k in range(2):
+        y1, dy1, _, _ = oracle.scan_jvp(x, dx[k:k + 1], p)
+        assert np.array_equal(dy1[0], dy2[k])
+
+
+# ------------------------------------------------- state, blocks, composition
+
+def test_entry_state_composition_eq5():
+    """Over a block of steps the augmented operator composes (Prop. 3.2):
+    exit h = P h_in + h0_end and exit dh = P dh_in + Q h_in + dh0_end, with the
+    closed forms P = exp(A sum Delta) and Q = P A sum dDelta (the lower-left
+    block of the composed operator, Eq. 5, summed over the block)."""
+    p, x, dx = rand_problem(12, B=2, L=17, D=3, N=4, K=2)
+    g = np.random.default_rng(13)
+    h0 = g.standard_normal((2, 3, 4)); dh0 = g.standard_normal((2, 2, 3, 4))
+    _, _, hz, dhz = oracle.scan_jvp(x, dx, p)
+    _, _, hh, dhh = oracle.scan_jvp(x, dx, p, h_in=h0, dh_in=dh0)
+    delta, ddelta = oracle.discretize(x, dx, p["w_delta"], p["b_delta"])
+    P = np.exp(p["A"][None] * delta.sum(1)[:, :, None])                         # [B, D, N]
+    Q = P[None] * p["A"][None, None] * ddelta.sum(2)[:, :, :, None]              # [K, B, D, N]
+    assert relerr(hh, P * h0 + hz) < 1e-13
+    assert relerr(dhh, P[None] * dh0 + Q * h0[None] + dhz) < 1e-13
+
+
+def test_augmented_matrix_product():
+    """The product of the per-step 3x3 operators M_t (Eq. 4) over the sequence
+    maps (h_in, dh_in, 1) to the oracle's exit state."""
+    p, x, dx = rand_problem(14, B=1, L=11, D=2, N=3, K=1)
+    g = np.random.default_rng(15)
+    h0 = g.standard_normal((1, 2, 3)); dh0 = g.standard_normal((1, 1, 2, 3))
+    _, _, hh, dhh = oracle.scan_jvp(x, dx, p, h_in=h0, dh_in=dh0)
+    delta, ddelta = oracle.discretize(x, dx, p["w_delta"], p["b_delta"])
+    Bm, _, dBm, _ = oracle.project(x, dx, p["W_B"], p["W_C"])
+    for d in range(2):
+        for n in range(3):
+            M = np.eye(3)
+            for t in range(11):
+                a = np.exp(delta[0, t, d] * p["A"][d, n])
+                bt = delta[0, t, d] * Bm[0, t, n] * x[0, t, d]
+                Kt = a * p["A"][d, n] * ddelta[0, 0, t, d]
+                jt = (ddelta[0, 0, t, d] * Bm[0, t, n] * x[0, t, d] + delta[0, t, d] * dBm[0, 0, t, n] * x[0, t, d]
+                      + delta[0, t, d] * Bm[0, t, n] * dx[0, 0, t, d])
+                Mt = np.array([[a, 0, bt], [Kt, a, jt], [0, 0, 1.0]])
+                M = Mt @ M
+            v = M @ np.array([h0[0, d, n], dh0[0, 0, d, n], 1.0])
+            assert abs(v[0] - hh[0, d, n]) < 1e-12 * max(1, abs(v[0]))
+            assert abs(v[1] - dhh[0, 0, d, n]) < 1e-12 * max(1, abs(v[1]))
+            assert abs(v[2] - 1.0) == 0.0
+
+
+def test_chunked_equals_whole_and_channel_subset():
+    p, x, dx = rand_problem(16, B=2, L=33, D=5, N=4, K=2, bias=True)
+    y, dy, h, dh = oracle.scan_jvp(x, dx, p)
+    yc, dyc, hc, dhc = oracle.scan_jvp(x, dx, p, chunk=7)
+    assert relerr(yc, y) < 1e-15 and relerr(dyc, dy) < 1e-15 and relerr(hc, h) < 1e-15
+    sel = np.array([4, 1])
+    ys, dys, hs, dhs = oracle.scan_jvp(x, dx, p, channels=sel)
+    assert np.array_equal(ys, y[..., sel]) and np.array_equal(dys, dy[..., sel])
+    assert np.array_equal(hs, h[:, sel]) and np.array_equal(dhs, dh[:, :, sel])
+
+
+# ---------------------------------------------------------- exact properties
+
+def test_causality_prefix_and_ghost_pulse_zeros():
+    p, x, dx = rand_problem(17, B=1, L=30, D=3, N=4, K=1)
+    y, dy, _, _ = oracle.scan_jvp(x, dx, p)
+    yp, dyp, _, _ = oracle.scan_jvp(x[:, :12], dx[:, :, :12], p)
+    assert np.array_equal(yp, y[:, :12]) and np.array_equal(dyp, dy[:, :, :12])
+    t0 = 19
+    dxp = np.zeros_like(dx); dxp[:, :, t0, 1] = 1e-3      # a small pulse at t0 in one channel
+    _, dyg, _, _ = oracle.scan_jvp(x, dxp, p)
+    assert np.all(dyg[:, :, :t0] == 0.0)                  # no leakage before the pulse
+    assert np.all(np.abs(dyg[:, :, t0:]).sum(-1) > 0)     # and a response after it
+    _, dy0, _, _ = oracle.scan_jvp(x, np.zeros_like(dx), p)
+    assert np.all(dy0 == 0.0)
+
+
+def test_stiff_underflow_is_exact_drive():
+    """Where exp(Delta*A) underflows to 0 the state is the drive alone:
+    h' = Delta*B*x (and dh' = j_t), with no NaN or Inf."""
+    D, N, L = 2, 3, 8
+    p = dict(A=np.full((D, N), -1e4), w_delta=np.zeros(D), b_delta=np.full(D, 3.0),
+             W_B=np.zeros((D, N)), W_C=np.zeros((D, N)), b_B=np.array([1.0, -2.0, 0.5]),
+             b_C=np.array([0.3, 0.1, -1.0]))
+    g = np.random.default_rng(18)
+    x = g.standard_normal((1, L, D)); dx = g.standard_normal((1, 1, L, D))
+    y, dy, h, dh = oracle.scan_jvp(x, dx, p)
+    delta = np.log1p(np.exp(3.0))
+    assert np.exp(delta * -1e4) == 0.0
+    exp_y = (p["b_C"] * p["b_B"]).sum() * delta * x[0]
+    assert relerr(y[0], exp_y) < 1e-15
+    exp_dy = (p["b_C"] * p["b_B"]).sum() * delta * dx[0, 0]
+    assert relerr(dy[0, 0], exp_dy) < 1e-15
+    assert np.all(np.isfinite(y)) and np.all(np.isfinite(dy))
+
+
+def test_golden_fixture_regression():
+    """The tiny workload's oracle outputs at fixed sample points match the
+    committed fixture written by tests/golden/make_golden.py (oracle only)."""
+    import json, os
+    from paper_2512_23068_amd import inputs
+    path = os.path.join(os.path.dirname(__file__), "golden", "tiny_oracle.json")
+    with open(path) as f:
+        gold = json.load(f)
+    inp = inputs.make_inputs("tiny")
+    y, dy, h, dh = oracle.scan_jvp(inp["x"], inp["dx"], inp)
+    for (t, d, vy, vdy) in gold["samples"]:
+        assert abs(y[0, t, d] - vy) <= 1e-12 * max(1.0, abs(vy))
+        assert abs(dy[0, 0, t, d] - vdy) <= 1e-12 * max(1e-30, abs(vdy))
