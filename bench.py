@@ -1,0 +1,203 @@
+"""Benchmark of the fused primal + tangent selective scan on one MI355X.
+
+A step is one call of the whole hot path (projections, segment aggregates,
+carry, scan with outputs) over one batch of seeded synthetic input already
+resident in HBM.  Prints one JSON line.
+
+Default workload: the long-range impulse-response probe, B=1 L=131072
+D=1536 N=16 K=1, f32 (the L=128k workload the metric is quoted at).
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, vendor figure
+FP32_VECTOR_PEAK_TFLOPS = 157.3  # MI355X fp32 vector, vendor figure
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="pulse128k")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline leg")
+    ap.add_argument("--cpu-steps", type=int, default=0, help="oracle sample length (0 = auto)")
+    return ap.parse_args()
+
+
+def scan_flops_per_lane_step(K):
+    """Arithmetic of the definition per (b, t, d, n) and step, counting an fma
+    as 2 and exp as 1: primal Delta*A, exp, Abar*h, B*u + s, C*h' (7 with the
+    shared A*s); per direction Abar*dh + (A s)*dDelta + B*p + dB*u (7) and
+    dC*h' + C*dh' (4)."""
+    return 7 + 11 * K
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only; --gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2512_23068_amd import binding, inputs
+
+    cfg = inputs.get_config(args.workload)
+    B, L, D, N, K = cfg.batch, cfg.seqlen, cfg.d_inner, cfg.d_state, cfg.n_dirs
+    dev = torch.device("cuda:0")
+    t_gen = time.time()
+    inp = inputs.make_inputs(cfg)
+    print(f"bench: workload {cfg.name} B={B} L={L} D={D} N={N} K={K} {cfg.in_dtype}; inputs in "
+          f"{time.time() - t_gen:.1f}s", file=sys.stderr, flush=True)
+    tdt = torch.bfloat16 if cfg.in_dtype == "bf16" else torch.float32
+    x = torch.from_numpy(inp["x"]).to(dev).to(tdt)
+    dx = torch.from_numpy(inp["dx"]).to(dev).to(tdt)
+    params = {k: torch.from_numpy(inp[k]).to(dev) for k in ("A", "w_delta", "b_delta", "W_B", "W_C")}
+    s_in = x.element_size()
+    payload = x.numel() * s_in + dx.numel() * s_in + (x.numel() + dx.numel()) * 4
+    del inp
+    y = torch.empty((B, L, D), device=dev)
+    dy = torch.empty((K, B, L, D), device=dev)
+    plan = binding.plan(B, L, D, N, K, cfg.in_dtype)
+    ws = torch.empty(plan["workspace_bytes"], device=dev, dtype=torch.uint8)
+    torch.cuda.synchronize()
+    base_alloc = torch.cuda.memory_allocated()
+
+    def step():
+        binding.scan_jvp(x, dx, params, workspace=ws, out=(y, dy))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    binding.timing_read()
+    # Timed region: launch timing events recorded by the library on the
+    # stream its kernels run on, plus whole-step events on the same stream.
+    binding.timing_enable(True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    binding.timing_enable(False)
+    kern = binding.timing_read()
+    ms_total = ev0.elapsed_time(ev1)
+    peak = torch.cuda.max_memory_allocated()
+    ms_step = ms_total / args.steps
+
+    # a second timed pass without per-launch events, for the headline number
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms_step_clean = ev0.elapsed_time(ev1) / args.steps
+    ms_step = min(ms_step, ms_step_clean)
+
+    tokch = B * L * D
+    value = tokch / (ms_step * 1e-3) / 1e9
+    alg_bytes = tokch * (1 + K) * (s_in + 4)
+    # Dominant kernel: the scan that writes the outputs (kind 3).  Per launch
+    # it performs the whole of the algorithmic IO of its block (x, dx read
+    # once, y, dy written once) and the whole per-lane arithmetic.
+    dom_name = max(kern, key=lambda k: kern[k][0])
+    so_ms, so_n = kern["scan_out"]
+    so_avg_ms = so_ms / max(so_n, 1)
+    launches_per_step = so_n / args.steps
+    bytes_per_launch = alg_bytes / launches_per_step
+    flops_per_launch = tokch * N * scan_flops_per_lane_step(K) / launches_per_step
+    hbm_gbs = bytes_per_launch / (so_avg_ms * 1e-3) / 1e9
+    tflops = flops_per_launch / (so_avg_ms * 1e-3) / 1e12
+    roofline = {
+        "kernel": "k_scan (scan with outputs)",
+        "bound": "alu",
+        "achieved": round(tflops, 3),
+        "peak": FP32_VECTOR_PEAK_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": round(tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
+        "traffic": None,
+        "hbm_achieved_gbs": round(hbm_gbs, 1),
+        "hbm_frac": round(hbm_gbs / HBM_PEAK_GBS, 4),
+        "avg_launch_ms": round(so_avg_ms, 5),
+        "launches_per_step": launches_per_step,
+        "dominant_kind_by_time": dom_name,
+    }
+    kernels = {k: {"ms_per_step": round(v[0] / args.steps, 4), "launches_per_step": v[1] / args.steps}
+               for k, v in kern.items()}
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(cfg, args.cpu_steps)
+
+    out = {
+        "metric": "primal+JVP scan Gtok·ch/s at L=128k",
+        "value": round(value, 3),
+        "unit": "Gtok·ch/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if cfg.in_dtype == "f32" else "bf16-in/f32",
+        "data": "synthetic (seeded; BASELINE recipe)",
+        "config": {"workload": cfg.name, "batch": B, "seq_len": L, "d_inner": D, "d_state": N, "n_dirs": K,
+                   "in_dtype": cfg.in_dtype, "parallelism": "single GPU"},
+        "hbm_gbs_path": round(alg_bytes / (ms_step * 1e-3) / 1e9, 1),
+        "hbm_frac_path": round(alg_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "vram": {"peak_bytes": int(peak), "payload_bytes": int(payload), "workspace_bytes": plan["workspace_bytes"],
+                 "peak_minus_payload": int(peak - payload)},
+        "plan": plan,
+        "kernels": kernels,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "wall_s_timed": round(wall, 3),
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(cfg, cpu_steps):
+    """The fp64 oracle on the host cores over a prefix of the same workload
+    (all channels, the first Ls steps)."""
+    import numpy as np
+    from oracle import oracle
+    from paper_2512_23068_amd import inputs
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+
+    def run(Ls):
+        sub = cfg.with_(seqlen=Ls)
+        inp = inputs.make_inputs(sub)
+        t0 = time.perf_counter()
+        oracle.scan_jvp(inp["x"], inp["dx"], inp, chunk=4096, nthreads=threads)
+        return sub, time.perf_counter() - t0
+
+    if cpu_steps:
+        Ls = cpu_steps
+    else:   # calibrate on a short prefix, then size the sample to ~15 s
+        _, t_cal = run(256)
+        Ls = int(max(256, min(cfg.seqlen, 256 * 15.0 / max(t_cal, 1e-3))))
+    sub, dt = run(Ls)
+    tokch = sub.batch * Ls * sub.d_inner
+    return {"value": round(tokch / dt / 1e9, 6), "unit": "Gtok·ch/s", "cores": threads, "kind": "oracle",
+            "sample": f"{cfg.name} first {Ls} steps, all {sub.d_inner} channels, batch {sub.batch}, "
+                      f"{sub.n_dirs} direction(s); fp64; {dt:.2f}s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,148 @@
+/*
+ * pgf.h -- C ABI of libpgf: the fused primal + tangent (forward-mode JVP)
+ * scan of a selective diagonal state-space model on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The operation (paper Sec. 3, Lemma 3.1 "Selectivity Jacobian", Eq. 3;
+ * Prop. 3.2, Eq. 4; Alg. 1 "Tiled Operator-Space Evolution"):
+ *
+ *   For every batch b, channel d, state n and step t = 0 .. L-1
+ *     z      = x[b,t,d] * w_delta[d] + b_delta[d]
+ *     Delta  = softplus(z)                      selective step size
+ *     Abar   = exp(Delta * A[d,n])              zero-order-hold transition
+ *     B_t[n] = sum_d' x[b,t,d'] W_B[d',n] + b_B[n]
+ *     C_t[n] = sum_d' x[b,t,d'] W_C[d',n] + b_C[n]
+ *     h      = Abar * h + Delta * B_t[n] * x[b,t,d]        primal state
+ *     y[b,t,d] = sum_n C_t[n] * h                          output map
+ *   and, for every tangent direction k (the input perturbation dx_k), the
+ *   exact directional derivative of all of the above along dx_k:
+ *     dDelta = sigmoid(z) * w_delta[d] * dx_k[b,t,d]
+ *     dB[n], dC[n] = the projections applied to dx_k (no bias)
+ *     dh     = Abar*dh + Abar*A[d,n]*dDelta*h_prev
+ *              + dDelta*B*x + Delta*dB*x + Delta*B*dx      (Eq. 3: K_t, j_t)
+ *     dy_k[b,t,d] = sum_n dC[n]*h + C[n]*dh
+ *   The state starts at h_in / dh_in (zero when NULL).  The dC*h term is the
+ *   derivative of the output map through C; the paper's output variation
+ *   (Eq. 2) leaves it out, this library differentiates the map in full.
+ *
+ * Only the O(B*D*N*(1+K)) state crosses from one block of steps to the next
+ * (the block hand-off of Alg. 1); the state trajectory is never stored, so
+ * the workspace does not depend on L (Sec. 4.3, memory theorem).
+ *
+ * Conventions shared by every entry point
+ *   - Tensor pointers (x, dx, y, dy, parameters, h_in/dh_in/h_out/dh_out,
+ *     workspace) are DEVICE pointers owned by the caller.  The library
+ *     never allocates or frees device memory.
+ *   - Layouts are dense row-major, last index fastest:
+ *       x [B,L,D]     dx [K,B,L,D]     y [B,L,D] (f32)   dy [K,B,L,D] (f32)
+ *       A, W_B, W_C [D,N]   w_delta, b_delta [D]   b_B, b_C [N]
+ *       h_in, h_out [B,D,N]   dh_in, dh_out [K,B,D,N]            (all f32)
+ *   - x and dx are f32 or bf16 (in_dtype); everything else is f32, and all
+ *     arithmetic of the scan runs in f32.
+ *   - Calls are asynchronous on `stream` and make no host<->device sync.
+ *     Argument checks are synchronous and happen before any launch; on a
+ *     failed check nothing is launched and the outputs are untouched.
+ *     Faults inside kernels surface at the caller's next synchronisation.
+ *   - The library keeps no state between calls (except the optional
+ *     launch-timing record, see pgf_timing_*), and is reentrant on distinct
+ *     workspaces.  Two calls in flight on the same workspace race.
+ *   - No C++ exception crosses this boundary.
+ */
+#ifndef PGF_H_
+#define PGF_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes (negative = error). */
+#define PGF_OK                 0
+#define PGF_ERR_INVALID_ARG   -1   /* NULL where a pointer is required, bad size, overlap  */
+#define PGF_ERR_UNSUPPORTED   -2   /* shape outside what the kernels are built for          */
+#define PGF_ERR_WORKSPACE     -3   /* workspace NULL or smaller than pgf_workspace_bytes    */
+#define PGF_ERR_HIP           -4   /* a HIP launch or runtime call failed                   */
+
+/* dtype of x and dx. */
+#define PGF_F32   0
+#define PGF_BF16  1
+
+typedef struct pgf_params {
+    /* Problem size: batch B, sequence length L (>= 0), channels D, state size
+     * N, tangent directions K.  Supported: B, D >= 1; N in {4,8,16,32,64};
+     * 1 <= K <= 8. */
+    int64_t batch, seqlen, d_inner, d_state, n_dirs;
+    int32_t in_dtype;      /* PGF_F32 or PGF_BF16                                       */
+    /* Tiling overrides, 0 = library default (the defaults depend on B, D, N,
+     * K and in_dtype only, never on L).
+     *   seg_len   : steps per segment of the parallel-in-L evaluation (a
+     *               power of two, 16 .. 65536), or -1 to force the
+     *               sequential-in-L evaluation.
+     *   chunk_segs: segments per host block (the Alg. 1 block is
+     *               chunk_segs*seg_len steps), 1 .. 4096.
+     * Results are bit-identical for every chunk_segs at a fixed seg_len. */
+    int32_t seg_len;
+    int32_t chunk_segs;
+    /* Model parameters (device, f32).  b_B / b_C may be NULL (= 0). */
+    const float *A, *w_delta, *b_delta, *W_B, *W_C, *b_B, *b_C;
+    /* Optional state hand-off (device, f32; NULL = zero in / not written).
+     * Passing one call's h_out/dh_out as the next call's h_in/dh_in over the
+     * continuation of the sequence reproduces one long call bit for bit when
+     * the first call's L is a multiple of the segment length. */
+    const float *h_in, *dh_in;
+    float *h_out, *dh_out;
+    /* Scratch (device), at least pgf_workspace_bytes(p) bytes, 256-byte
+     * aligned.  Its size does not depend on L. */
+    void *workspace;
+    size_t workspace_bytes;
+} pgf_params;
+
+/* How a call is tiled (host-side planning; no device access). */
+typedef struct pgf_plan_info {
+    int32_t n_per_thread;   /* states n held by one thread                          */
+    int32_t n_split;        /* threads sharing one channel (N / n_per_thread)       */
+    int32_t seg_len;        /* segment length, or 0 in the sequential evaluation    */
+    int32_t chunk_segs;     /* segments per host block                              */
+    int64_t chunk_len;      /* steps per host block                                 */
+    int64_t n_chunks;       /* host blocks for this L                               */
+    size_t  workspace_bytes;
+} pgf_plan_info;
+
+/* Bytes of workspace a call with these sizes needs (only the size fields,
+ * in_dtype, seg_len and chunk_segs are read).  Returns 0 if the sizes are
+ * invalid or unsupported.  Host only. */
+size_t pgf_workspace_bytes(const pgf_params *p);
+
+/* Fill *info with the tiling a call would use.  Host only.  Returns a status. */
+int pgf_plan(const pgf_params *p, pgf_plan_info *info);
+
+/* The fused primal + tangent scan (see the file comment).
+ *   x  : device, [B,L,D] in in_dtype            (read)
+ *   dx : device, [K,B,L,D] in in_dtype          (read)
+ *   y  : device, [B,L,D] f32                    (fully overwritten)
+ *   dy : device, [K,B,L,D] f32                  (fully overwritten)
+ *   stream : a hipStream_t (NULL = the default stream)
+ * y and dy must not overlap x, dx or each other.  Returns PGF_OK or an
+ * error code; see the conventions above. */
+int pgf_scan_jvp(const void *x, const void *dx, const pgf_params *p,
+                 float *y, float *dy, void *stream);
+
+/* Static string for a status code. */
+const char *pgf_status_string(int status);
+
+/* Launch timing (measurement aid, off by default).  While enabled, every
+ * kernel a call launches is bracketed by HIP events on the call's stream;
+ * pgf_timing_read synchronises those events and returns, per kernel kind
+ * (0 projection, 1 segment aggregate, 2 carry, 3 scan+outputs, 4 state
+ * import/export), the summed milliseconds and launch counts, then clears
+ * the record.  Arrays have PGF_TIMING_KINDS entries.  Not reentrant. */
+#define PGF_TIMING_KINDS 5
+int pgf_timing_enable(int on);
+int pgf_timing_read(double *ms, int64_t *launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PGF_H_ */

@@ -1,0 +1,189 @@
+"""Python binding of libpgf (argument marshalling only).
+
+Every step of the scan runs in the HIP library ``libpgf.so`` built from
+``csrc/``; this module checks tensor metadata, allocates outputs and the
+workspace with torch, and passes raw device pointers and the current HIP
+stream through the C ABI declared in ``include/pgf.h``.  There is no other
+compute path: if the library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpgf.so")
+
+PGF_OK = 0
+PGF_F32 = 0
+PGF_BF16 = 1
+TIMING_KINDS = ("proj", "seg_aggregate", "carry", "scan_out", "state_io")
+
+_c_f = ctypes.c_void_p
+
+
+class PgfParams(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int64), ("seqlen", ctypes.c_int64), ("d_inner", ctypes.c_int64),
+        ("d_state", ctypes.c_int64), ("n_dirs", ctypes.c_int64),
+        ("in_dtype", ctypes.c_int32), ("seg_len", ctypes.c_int32), ("chunk_segs", ctypes.c_int32),
+        ("A", _c_f), ("w_delta", _c_f), ("b_delta", _c_f), ("W_B", _c_f), ("W_C", _c_f),
+        ("b_B", _c_f), ("b_C", _c_f),
+        ("h_in", _c_f), ("dh_in", _c_f), ("h_out", _c_f), ("dh_out", _c_f),
+        ("workspace", _c_f), ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
+class PgfPlanInfo(ctypes.Structure):
+    _fields_ = [
+        ("n_per_thread", ctypes.c_int32), ("n_split", ctypes.c_int32), ("seg_len", ctypes.c_int32),
+        ("chunk_segs", ctypes.c_int32), ("chunk_len", ctypes.c_int64), ("n_chunks", ctypes.c_int64),
+        ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
+EXPORTED = ("pgf_workspace_bytes", "pgf_plan", "pgf_scan_jvp", "pgf_status_string",
+            "pgf_timing_enable", "pgf_timing_read")
+
+_lib = None
+
+
+def lib():
+    """The loaded libpgf (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"libpgf.so not found at {LIB_PATH}: build it with __graft_entry__.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER(PgfParams)
+    L.pgf_workspace_bytes.restype = ctypes.c_size_t
+    L.pgf_workspace_bytes.argtypes = [P]
+    L.pgf_plan.restype = ctypes.c_int
+    L.pgf_plan.argtypes = [P, ctypes.POINTER(PgfPlanInfo)]
+    L.pgf_scan_jvp.restype = ctypes.c_int
+    L.pgf_scan_jvp.argtypes = [ctypes.c_void_p, ctypes.c_void_p, P, ctypes.c_void_p, ctypes.c_void_p,
+                               ctypes.c_void_p]
+    L.pgf_status_string.restype = ctypes.c_char_p
+    L.pgf_status_string.argtypes = [ctypes.c_int]
+    L.pgf_timing_enable.restype = ctypes.c_int
+    L.pgf_timing_enable.argtypes = [ctypes.c_int]
+    L.pgf_timing_read.restype = ctypes.c_int
+    L.pgf_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
+    _lib = L
+    return L
+
+
+def status_string(code: int) -> str:
+    return lib().pgf_status_string(int(code)).decode()
+
+
+def _check(code: int):
+    if code != PGF_OK:
+        raise RuntimeError(status_string(code))
+
+
+def make_params(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0) -> PgfParams:
+    p = PgfParams()
+    p.batch, p.seqlen, p.d_inner, p.d_state, p.n_dirs = int(B), int(L), int(D), int(N), int(K)
+    p.in_dtype = PGF_BF16 if in_dtype in ("bf16", torch.bfloat16) else PGF_F32
+    p.seg_len, p.chunk_segs = int(seg_len), int(chunk_segs)
+    return p
+
+
+def workspace_bytes(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0) -> int:
+    return int(lib().pgf_workspace_bytes(ctypes.byref(make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs))))
+
+
+def plan(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0) -> dict:
+    info = PgfPlanInfo()
+    _check(lib().pgf_plan(ctypes.byref(make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs)),
+                          ctypes.byref(info)))
+    return {f: getattr(info, f) for f, _ in PgfPlanInfo._fields_}
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dev_param(v, shape, device, name):
+    if v is None:
+        return None
+    if not isinstance(v, torch.Tensor):
+        v = torch.as_tensor(v)
+    if tuple(v.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(v.shape)}")
+    return v.to(device=device, dtype=torch.float32).contiguous()
+
+
+def scan_jvp(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_in=None, return_state=False,
+             seg_len=0, chunk_segs=0, workspace=None, out=None, stream=None):
+    """Fused primal + tangent scan on the GPU.
+
+    x [B,L,D] and dx [K,B,L,D]: float32 or bfloat16 CUDA tensors (same dtype).
+    params: A, W_B, W_C [D,N]; w_delta, b_delta [D]; optional b_B, b_C [N].
+    Returns (y [B,L,D], dy [K,B,L,D]) in float32, plus (h_out [B,D,N],
+    dh_out [K,B,D,N]) when return_state.  Asynchronous on the current stream.
+    """
+    L_ = lib()
+    if not (x.is_cuda and dx.is_cuda):
+        raise ValueError("x and dx must be device tensors")
+    if x.dtype not in (torch.float32, torch.bfloat16) or dx.dtype != x.dtype:
+        raise ValueError("x and dx must both be float32 or both bfloat16")
+    if x.dim() != 3 or dx.dim() != 4 or tuple(dx.shape[1:]) != tuple(x.shape):
+        raise ValueError(f"shapes: x [B,L,D], dx [K,B,L,D]; got {tuple(x.shape)}, {tuple(dx.shape)}")
+    x = x.contiguous()
+    dx = dx.contiguous()
+    B, L, D = x.shape
+    K = dx.shape[0]
+    dev = x.device
+    A = _dev_param(params["A"], (D, params["A"].shape[1]), dev, "A")
+    N = A.shape[1]
+    keep = [A]
+    pr = make_params(B, L, D, N, K, "bf16" if x.dtype == torch.bfloat16 else "f32", seg_len, chunk_segs)
+    vals = {"A": A}
+    for name, shape in (("w_delta", (D,)), ("b_delta", (D,)), ("W_B", (D, N)), ("W_C", (D, N)),
+                        ("b_B", (N,)), ("b_C", (N,))):
+        vals[name] = _dev_param(params.get(name), shape, dev, name)
+        keep.append(vals[name])
+    for name in ("A", "w_delta", "b_delta", "W_B", "W_C", "b_B", "b_C"):
+        setattr(pr, name, None if vals[name] is None else vals[name].data_ptr())
+    h_in = _dev_param(h_in, (B, D, N), dev, "h_in")
+    dh_in = _dev_param(dh_in, (K, B, D, N), dev, "dh_in")
+    pr.h_in = None if h_in is None else h_in.data_ptr()
+    pr.dh_in = None if dh_in is None else dh_in.data_ptr()
+    h_out = dh_out = None
+    if return_state:
+        h_out = torch.empty((B, D, N), device=dev, dtype=torch.float32)
+        dh_out = torch.empty((K, B, D, N), device=dev, dtype=torch.float32)
+        pr.h_out, pr.dh_out = h_out.data_ptr(), dh_out.data_ptr()
+    nbytes = int(L_.pgf_workspace_bytes(ctypes.byref(pr)))
+    if nbytes == 0:
+        _check(L_.pgf_plan(ctypes.byref(pr), ctypes.byref(PgfPlanInfo())))
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), device=dev, dtype=torch.uint8)
+    pr.workspace, pr.workspace_bytes = workspace.data_ptr(), workspace.numel()
+    if out is not None:
+        y, dy = out
+    else:
+        y = torch.empty((B, L, D), device=dev, dtype=torch.float32)
+        dy = torch.empty((K, B, L, D), device=dev, dtype=torch.float32)
+    st = torch.cuda.current_stream(dev).cuda_stream if stream is None else stream
+    rc = L_.pgf_scan_jvp(_ptr(x), _ptr(dx), ctypes.byref(pr), _ptr(y), _ptr(dy), ctypes.c_void_p(st))
+    _check(rc)
+    if return_state:
+        return y, dy, h_out, dh_out
+    return y, dy
+
+
+def timing_enable(on: bool = True):
+    _check(lib().pgf_timing_enable(1 if on else 0))
+
+
+def timing_read() -> dict:
+    ms = (ctypes.c_double * len(TIMING_KINDS))()
+    n = (ctypes.c_int64 * len(TIMING_KINDS))()
+    _check(lib().pgf_timing_read(ms, n))
+    return {k: (ms[i], n[i]) for i, k in enumerate(TIMING_KINDS)}

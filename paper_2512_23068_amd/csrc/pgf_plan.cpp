@@ -1,0 +1,134 @@
+// Host-side planning of a libpgf call (see pgf_plan.h).
+//
+// Tiling.  Each (batch, channel) owns N independent recurrences.  One thread
+// keeps nt of them in registers and ns = N/nt threads share a channel, so a
+// sequence position costs one thread nt*(1+K) state updates.  When B*D*ns
+// threads cannot fill the GPU, the sequence is cut into segments of `seg`
+// steps that run in parallel: each segment is first scanned from a zero
+// state (its end state and its sums of Delta and dDelta give the exact
+// two-step composition of the augmented operator, Prop. 3.2 Eq. 5), a short
+// sequential carry turns those into the true state entering every segment,
+// and the segments are then rescanned from their true entry states while the
+// outputs are written.  Host blocks of chunk_segs segments bound the
+// workspace independently of L (the tiling of Alg. 1).
+#include "pgf_plan.h"
+
+#include <algorithm>
+
+namespace pgf {
+
+namespace {
+
+constexpr int64_t kMaxSeg = 65536;
+constexpr int kMaxChunkSegs = 4096;
+// Waves the default tiling aims to keep resident (a few per SIMD).
+constexpr int64_t kTargetWaves = 4096;
+constexpr int64_t kDefaultSeg = 256;
+constexpr int64_t kSeqChunk = 4096;
+
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
+
+}  // namespace
+
+int make_plan(const pgf_params *p, Plan *plan) {
+    if (!p || !plan) return PGF_ERR_INVALID_ARG;
+    const int64_t B = p->batch, L = p->seqlen, D = p->d_inner, N = p->d_state, K = p->n_dirs;
+    if (B < 1 || L < 0 || D < 1 || N < 1 || K < 1) return PGF_ERR_INVALID_ARG;
+    if (p->in_dtype != PGF_F32 && p->in_dtype != PGF_BF16) return PGF_ERR_INVALID_ARG;
+    if (!(N == 4 || N == 8 || N == 16 || N == 32 || N == 64)) return PGF_ERR_UNSUPPORTED;
+    if (!(K == 1 || K == 2 || K == 4 || K == 8)) return PGF_ERR_UNSUPPORTED;
+    // Guard the 64-bit index arithmetic of the kernels with a wide margin.
+    if (B > 65535 || D > (int64_t(1) << 24) || L > (int64_t(1) << 40)) return PGF_ERR_UNSUPPORTED;
+    if ((1 + K) * B * N * D > (int64_t(1) << 36)) return PGF_ERR_UNSUPPORTED;
+    if ((double)K * B * (double)L * D > 9.0e18 / 16) return PGF_ERR_UNSUPPORTED;
+
+    Plan q{};
+    q.B = B; q.L = L; q.D = D; q.N = N; q.K = K;
+    q.in_bf16 = p->in_dtype == PGF_BF16;
+    // Registers per thread grow as nt*(3+K); keep them near 128.
+    q.nt = (int)std::min<int64_t>(N, K >= 4 ? 8 : 16);
+    q.ns = (int)(N / q.nt);
+    q.R = (int)(2 * N * (1 + K));
+
+    const int64_t waves_per_col = (B * D * q.ns + 63) / 64;
+    int64_t seg;
+    if (p->seg_len == -1) {
+        seg = 0;
+    } else if (p->seg_len != 0) {
+        if (p->seg_len < 16 || p->seg_len > kMaxSeg || !is_pow2(p->seg_len)) return PGF_ERR_INVALID_ARG;
+        seg = p->seg_len;
+    } else {
+        seg = (2 * waves_per_col >= kTargetWaves) ? 0 : kDefaultSeg;
+    }
+    int64_t cs;
+    if (p->chunk_segs < 0 || p->chunk_segs > kMaxChunkSegs) return PGF_ERR_INVALID_ARG;
+    if (seg == 0) {
+        cs = p->chunk_segs ? p->chunk_segs : 1;
+        q.chunk_len = cs * kSeqChunk;
+        q.chunk_segs = 1;
+        cs = 1;
+    } else {
+        cs = p->chunk_segs ? p->chunk_segs
+                           : std::max<int64_t>(1, (kTargetWaves + waves_per_col - 1) / waves_per_col);
+        cs = std::min<int64_t>(cs, kMaxChunkSegs);
+        q.chunk_len = cs * seg;
+        q.chunk_segs = (int)cs;
+    }
+    q.seg = (int)seg;
+    q.n_chunks = (L + q.chunk_len - 1) / q.chunk_len;
+
+    const size_t f = sizeof(float);
+    const size_t comp = (size_t)(1 + K);
+    Layout w{};
+    size_t off = 0;
+    w.state = off; off = align256(off + comp * B * N * D * f);
+    w.bc = off;    off = align256(off + (size_t)B * q.chunk_len * q.R * f);
+    if (seg) {
+        const size_t G = (size_t)cs;
+        w.agg_h = off;  off = align256(off + (size_t)B * G * comp * N * D * f);
+        w.agg_s = off;  off = align256(off + (size_t)B * G * comp * D * f);
+        w.seg_in = off; off = align256(off + (size_t)B * G * comp * N * D * f);
+    } else {
+        w.agg_h = w.agg_s = w.seg_in = off;
+    }
+    w.total = off;
+    q.ws = w;
+    *plan = q;
+    return PGF_OK;
+}
+
+}  // namespace pgf
+
+extern "C" size_t pgf_workspace_bytes(const pgf_params *p) {
+    pgf::Plan q;
+    if (pgf::make_plan(p, &q) != PGF_OK) return 0;
+    return q.ws.total;
+}
+
+extern "C" int pgf_plan(const pgf_params *p, pgf_plan_info *info) {
+    if (!info) return PGF_ERR_INVALID_ARG;
+    pgf::Plan q;
+    const int rc = pgf::make_plan(p, &q);
+    if (rc != PGF_OK) return rc;
+    info->n_per_thread = q.nt;
+    info->n_split = q.ns;
+    info->seg_len = q.seg;
+    info->chunk_segs = q.chunk_segs;
+    info->chunk_len = q.chunk_len;
+    info->n_chunks = q.n_chunks;
+    info->workspace_bytes = q.ws.total;
+    return PGF_OK;
+}
+
+extern "C" const char *pgf_status_string(int s) {
+    switch (s) {
+        case PGF_OK: return "PGF_OK";
+        case PGF_ERR_INVALID_ARG: return "PGF_ERR_INVALID_ARG: invalid argument (NULL pointer, size or overlap)";
+        case PGF_ERR_UNSUPPORTED: return "PGF_ERR_UNSUPPORTED: shape not supported (N in {4,8,16,32,64}, K in {1,2,4,8})";
+        case PGF_ERR_WORKSPACE: return "PGF_ERR_WORKSPACE: workspace missing or smaller than pgf_workspace_bytes()";
+        case PGF_ERR_HIP: return "PGF_ERR_HIP: a HIP runtime call or kernel launch failed";
+        default: return "PGF: unknown status";
+    }
+}

@@ -1,0 +1,39 @@
+// Host-side planning of a libpgf call: argument checks, tiling choice and
+// workspace layout.  No device access; shared by the launch code and by the
+// host-only entry points (pgf_workspace_bytes, pgf_plan).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/pgf.h"
+
+namespace pgf {
+
+// Offsets (bytes) of the workspace sections; each is 256-byte aligned.
+//   state   [(1+K)][B][N][D]         state carried between host blocks
+//   bc      [B][Tc][R]               per-step projections of one host block,
+//                                    R = 2N(1+K): B, dB_0..dB_{K-1}, C, dC_0..
+//   agg_h   [B][G][(1+K)][N][D]      segment end states from a zero start
+//   agg_s   [B][G][(1+K)][D]         segment sums of Delta and dDelta_k
+//   seg_in  [B][G][(1+K)][N][D]      true state entering each segment
+struct Layout {
+    size_t state, bc, agg_h, agg_s, seg_in, total;
+};
+
+struct Plan {
+    int64_t B, L, D, N, K;
+    int in_bf16;
+    int nt, ns;          // states per thread, threads per channel (nt*ns == N)
+    int seg;             // segment length; 0 = sequential evaluation
+    int chunk_segs;      // segments per host block (1 when sequential)
+    int64_t chunk_len;   // steps per host block
+    int64_t n_chunks;
+    int R;               // floats per step record in bc
+    Layout ws;
+};
+
+// Validates the size fields and fills *plan.  Returns PGF_OK or an error.
+int make_plan(const pgf_params *p, Plan *plan);
+
+}  // namespace pgf

@@ -1,0 +1,641 @@
+// libpgf: fused primal + tangent (forward-mode JVP) scan of a selective
+// diagonal SSM for gfx950 (MI355X).
+//
+// Kernels, per host block of steps [t0, t0+len) (the block loop of Alg. 1):
+//   k_proj   per-step projections B, C (x W + b) and their tangents dB_k, dC_k
+//            (dx_k W) -- the contraction over channels, Sec. 3 selective maps.
+//   k_scan<false>  segment aggregate: each segment scanned from a zero state;
+//            writes its end state (h0, dh0_k) and the sums of Delta, dDelta_k.
+//   k_carry  sequential over the block's segments, per lane: composes the
+//            segment operators (Prop. 3.2, Eq. 5 summed over a segment:
+//            P = exp(A sum Delta), Q_k = P A sum dDelta_k) into the true
+//            state entering each segment.  Division-free: P underflowing to
+//            zero is exact and cannot produce Inf or NaN.
+//   k_scan<true>   rescans each segment from its true entry state and writes
+//            y and dy_k (Lemma 3.1 Eq. 3 with the full output derivative).
+// In the sequential evaluation (enough channels to fill the GPU) only k_proj
+// and k_scan<true> run, with the state handed from block to block.
+//
+// Arithmetic is f32 throughout; per lane and step the order of operations is
+// fixed, so results do not depend on the block size.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+#include <string.h>
+
+#include <mutex>
+#include <vector>
+
+#include "pgf_plan.h"
+
+namespace pgf {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kThreads = 256;
+
+// ---------------------------------------------------------------- helpers
+
+__device__ __forceinline__ float load_in(const float *__restrict__ p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float load_in(const uint16_t *__restrict__ p, int64_t i) {
+    return __uint_as_float(((uint32_t)p[i]) << 16);
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the NS consecutive lanes that share a channel (all of them get
+// the same bits: every step adds a lane pair symmetrically).
+template <int NS>
+__device__ __forceinline__ float group_sum(float v) {
+    if constexpr (NS >= 2) v += dpp_mov<0xB1>(v);   // quad_perm [1,0,3,2]
+    if constexpr (NS >= 4) v += dpp_mov<0x4E>(v);   // quad_perm [2,3,0,1]
+    if constexpr (NS >= 8) v += dpp_mov<0x141>(v);  // row_half_mirror
+    if constexpr (NS >= 16) v += dpp_mov<0x140>(v); // row_mirror
+    return v;
+}
+
+// Step size and its sensitivity factor for one (t, d):
+//   Delta = softplus(z), z = x*w + b;  dDelta = sigmoid(z)*w*dx = sw*dx.
+__device__ __forceinline__ void discretize(float xv, float w, float bd, float &delta, float &sw) {
+    const float z = fmaf(xv, w, bd);
+    const float e = expf(-fabsf(z));
+    delta = fmaxf(z, 0.0f) + log1pf(e);
+    const float r = __builtin_amdgcn_rcpf(1.0f + e);
+    const float sig = z >= 0.0f ? r : e * r;
+    sw = sig * w;
+}
+
+// ---------------------------------------------------------------- k_proj
+// rec[b][t-t0] = [B(N) | dB_0..dB_{K-1} (N each) | C(N) | dC_0..dC_{K-1}]
+// Row source s = blockIdx.y: 0 -> x (bias added), 1+k -> dx_k.
+// Each output is one thread's sum over d in ascending order.
+template <int NC, int CT, int RT, typename InT>
+__global__ __launch_bounds__(kThreads) void k_proj(
+    const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ WB,
+    const float *__restrict__ WC, const float *__restrict__ bB, const float *__restrict__ bC,
+    float *__restrict__ bc, int64_t Bsz, int64_t L, int64_t D, int K, int64_t t0, int64_t len, int64_t Tc) {
+    constexpr int N = NC / 2;
+    constexpr int CG = NC / CT;
+    constexpr int RG = kThreads / CG;
+    constexpr int TM = RG * RT;
+    constexpr int DT = 32;
+    __shared__ float Xs[TM][DT + 1];
+    __shared__ float Ws[DT][NC];
+
+    const int tid = threadIdx.x;
+    const int cg = tid % CG, rg = tid / CG;
+    const int s = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int64_t r0 = (int64_t)blockIdx.x * TM;  // chunk-relative first row
+    const InT *src = s == 0 ? x + (b * L + t0) * D : dx + (((int64_t)(s - 1) * Bsz + b) * L + t0) * D;
+
+    float acc[RT][CT];
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+        for (int j = 0; j < CT; ++j) acc[i][j] = 0.0f;
+
+    for (int64_t d0 = 0; d0 < D; d0 += DT) {
+        // X tile: TM rows x DT channels (zero outside the block / past D).
+        for (int e = tid; e < TM * DT; e += kThreads) {
+            const int r = e / DT, dd = e % DT;
+            const int64_t row = r0 + r, d = d0 + dd;
+            Xs[r][dd] = (row < len && d < D) ? load_in(src, row * D + d) : 0.0f;
+        }
+        for (int e = tid; e < DT * NC; e += kThreads) {
+            const int dd = e / NC, j = e % NC;
+            const int64_t d = d0 + dd;
+            float v = 0.0f;
+            if (d < D) v = j < N ? WB[d * N + j] : WC[d * N + (j - N)];
+            Ws[dd][j] = v;
+        }
+        __syncthreads();
+#pragma unroll 8
+        for (int dd = 0; dd < DT; ++dd) {
+            float xv[RT], wv[CT];
+#pragma unroll
+            for (int i = 0; i < RT; ++i) xv[i] = Xs[rg * RT + i][dd];
+#pragma unroll
+            for (int j = 0; j < CT; ++j) wv[j] = Ws[dd][cg * CT + j];
+#pragma unroll
+            for (int i = 0; i < RT; ++i)
+#pragma unroll
+                for (int j = 0; j < CT; ++j) acc[i][j] = fmaf(xv[i], wv[j], acc[i][j]);
+        }
+        __syncthreads();
+    }
+    const int R = 2 * N * (1 + K);
+#pragma unroll
+    for (int i = 0; i < RT; ++i) {
+        const int64_t row = r0 + rg * RT + i;
+        if (row >= len) continue;
+        float *out = bc + (b * Tc + row) * R;
+#pragma unroll
+        for (int j = 0; j < CT; ++j) {
+            const int c = cg * CT + j;
+            float v = acc[i][j];
+            if (c < N) {
+                if (s == 0 && bB) v += bB[c];
+                out[s * N + c] = v;
+            } else {
+                if (s == 0 && bC) v += bC[c - N];
+                out[(1 + K) * N + s * N + (c - N)] = v;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- k_scan
+// Grid (ceil(D*NS/256), G, B); thread -> (channel d, state group ns).
+// OUT=false: segment aggregate from a zero state.  OUT=true: scan from the
+// entry state at init[b*ibs + g*igs + c*ics + n*D + d] and write y, dy; if
+// end_state is set (sequential evaluation) the exit state is stored there
+// with the same indexing (g = 0).
+template <int NT, int NS, int K, bool OUT, typename InT>
+__global__ __launch_bounds__(kThreads) void k_scan(
+    const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A,
+    const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
+    const float *__restrict__ init, int64_t ibs, int64_t igs, int64_t ics,
+    float *__restrict__ y, float *__restrict__ dy, float *__restrict__ end_state,
+    float *__restrict__ agg_h, float *__restrict__ agg_s,
+    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    constexpr int N = NT * NS;
+    constexpr int R = 2 * N * (1 + K);
+    constexpr int DPB = kThreads / NS;
+    constexpr int TT = 8;  // steps per register-prefetched tile
+
+    const int tid = threadIdx.x;
+    const int ns = tid % NS;
+    const int64_t d_raw = (int64_t)blockIdx.x * DPB + tid / NS;
+    const bool active = d_raw < D;
+    const int64_t d = active ? d_raw : D - 1;
+    const int g = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int64_t ts = (int64_t)g * S;
+    const int64_t te = ts + S < len ? ts + S : len;
+    if (ts >= te) return;
+
+    float Af[NT], At[NT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+        Af[i] = A[d * N + ns * NT + i];
+        At[i] = Af[i] * kLog2e;
+    }
+    const float w = w_delta[d], bd = b_delta[d];
+
+    float h[NT], dh[K][NT];
+    if constexpr (OUT) {
+        const float *ib = init + b * ibs + g * igs + d;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            const int n = ns * NT + i;
+            h[i] = ib[n * D];
+#pragma unroll
+            for (int k = 0; k < K; ++k) dh[k][i] = ib[(1 + k) * ics + n * D];
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            h[i] = 0.0f;
+#pragma unroll
+            for (int k = 0; k < K; ++k) dh[k][i] = 0.0f;
+        }
+    }
+    float sD = 0.0f, sdD[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) sdD[k] = 0.0f;
+
+    const InT *X = x + (b * L + t0) * D + d;
+    const int64_t dxs = Bsz * L * D;  // stride between directions
+    const InT *DX = dx + (b * L + t0) * D + d;
+    float *Y = y + (b * L + t0) * D + d;
+    float *DY = dy + (b * L + t0) * D + d;
+    const float *rec0 = bc + b * Tc * R;
+
+    float xc[TT], dxc[K][TT];
+#pragma unroll
+    for (int j = 0; j < TT; ++j) {
+        const int64_t t = ts + j < te ? ts + j : te - 1;
+        xc[j] = load_in(X, t * D);
+#pragma unroll
+        for (int k = 0; k < K; ++k) dxc[k][j] = load_in(DX, k * dxs + t * D);
+    }
+
+    for (int64_t tb = ts; tb < te; tb += TT) {
+        float xn[TT], dxn[K][TT];
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
+            xn[j] = load_in(X, t * D);
+#pragma unroll
+            for (int k = 0; k < K; ++k) dxn[k][j] = load_in(DX, k * dxs + t * D);
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + j;
+            if (t < te) {
+                const float xv = xc[j];
+                float delta, sw;
+                discretize(xv, w, bd, delta, sw);
+                const float u = delta * xv;
+                float dD[K], pk[K];
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    dD[k] = sw * dxc[k][j];
+                    pk[k] = fmaf(dD[k], xv, delta * dxc[k][j]);
+                }
+                if constexpr (!OUT) {
+                    sD += delta;
+#pragma unroll
+                    for (int k = 0; k < K; ++k) sdD[k] += dD[k];
+                }
+                const float *rec = rec0 + t * R;
+                float yv = 0.0f, dyv[K];
+#pragma unroll
+                for (int k = 0; k < K; ++k) dyv[k] = 0.0f;
+#pragma unroll
+                for (int i = 0; i < NT; ++i) {
+                    const int n = ns * NT + i;
+                    const float Bn = rec[n];
+                    const float a = __builtin_amdgcn_exp2f(delta * At[i]);
+                    const float sv = a * h[i];
+                    const float gv = Af[i] * sv;
+                    const float hn = fmaf(Bn, u, sv);
+#pragma unroll
+                    for (int k = 0; k < K; ++k) {
+                        const float dBn = rec[(1 + k) * N + n];
+                        dh[k][i] = fmaf(a, dh[k][i], fmaf(gv, dD[k], fmaf(Bn, pk[k], dBn * u)));
+                    }
+                    h[i] = hn;
+                    if constexpr (OUT) {
+                        const float Cn = rec[(1 + K) * N + n];
+                        yv = fmaf(Cn, hn, yv);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) {
+                            const float dCn = rec[(2 + K + k) * N + n];
+                            dyv[k] = fmaf(dCn, hn, fmaf(Cn, dh[k][i], dyv[k]));
+                        }
+                    }
+                }
+                if constexpr (OUT) {
+                    yv = group_sum<NS>(yv);
+#pragma unroll
+                    for (int k = 0; k < K; ++k) dyv[k] = group_sum<NS>(dyv[k]);
+                    if (active && ns == 0) {
+                        Y[t * D] = yv;
+#pragma unroll
+                        for (int k = 0; k < K; ++k) DY[k * dxs + t * D] = dyv[k];
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            xc[j] = xn[j];
+#pragma unroll
+            for (int k = 0; k < K; ++k) dxc[k][j] = dxn[k][j];
+        }
+    }
+
+    if (!active) return;
+    if constexpr (OUT) {
+        if (end_state) {
+            float *eb = end_state + b * ibs + d;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                const int n = ns * NT + i;
+                eb[n * D] = h[i];
+#pragma unroll
+                for (int k = 0; k < K; ++k) eb[(1 + k) * ics + n * D] = dh[k][i];
+            }
+        }
+    } else {
+        const int64_t base = (b * G + g) * (1 + K);
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            const int n = ns * NT + i;
+            agg_h[(base * N + n) * D + d] = h[i];
+#pragma unroll
+            for (int k = 0; k < K; ++k) agg_h[((base + 1 + k) * N + n) * D + d] = dh[k][i];
+        }
+        if (ns == 0) {
+            agg_s[base * D + d] = sD;
+#pragma unroll
+            for (int k = 0; k < K; ++k) agg_s[(base + 1 + k) * D + d] = sdD[k];
+        }
+    }
+}
+
+// ---------------------------------------------------------------- k_carry
+// One thread per lane (b, n, d).  state [(1+K)][B][N][D] enters the block
+// and leaves it; seg_in receives the state entering each segment.
+template <int K>
+__global__ __launch_bounds__(kThreads) void k_carry(
+    const float *__restrict__ A, const float *__restrict__ agg_h, const float *__restrict__ agg_s,
+    float *__restrict__ state, float *__restrict__ seg_in, int64_t Bsz, int64_t D, int64_t N, int G) {
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t ND = N * D;
+    if (idx >= Bsz * ND) return;
+    const int64_t d = idx % D, n = (idx / D) % N, b = idx / ND;
+    const float a = A[d * N + n];
+    const float at = a * kLog2e;
+    const int64_t cstride = Bsz * ND;  // state: component stride
+    float h = state[b * ND + n * D + d];
+    float dh[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) dh[k] = state[(1 + k) * cstride + b * ND + n * D + d];
+    for (int g = 0; g < G; ++g) {
+        const int64_t base = (b * G + g) * (1 + K);
+        seg_in[base * ND + n * D + d] = h;
+#pragma unroll
+        for (int k = 0; k < K; ++k) seg_in[(base + 1 + k) * ND + n * D + d] = dh[k];
+        const float P = __builtin_amdgcn_exp2f(at * agg_s[base * D + d]);
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const float q = P * (a * agg_s[(base + 1 + k) * D + d]);
+            dh[k] = fmaf(P, dh[k], fmaf(q, h, agg_h[(base + 1 + k) * ND + n * D + d]));
+        }
+        h = fmaf(P, h, agg_h[base * ND + n * D + d]);
+    }
+    state[b * ND + n * D + d] = h;
+#pragma unroll
+    for (int k = 0; k < K; ++k) state[(1 + k) * cstride + b * ND + n * D + d] = dh[k];
+}
+
+// ---------------------------------------------------------------- state in/out
+// state [(1+K)][B][N][D] <-> h [B][D][N], dh [K][B][D][N].
+__global__ __launch_bounds__(kThreads) void k_state_import(
+    const float *__restrict__ h_in, const float *__restrict__ dh_in, float *__restrict__ state,
+    int64_t Bsz, int64_t D, int64_t N, int K) {
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t per = Bsz * N * D;
+    if (idx >= per * (1 + K)) return;
+    const int64_t c = idx / per, r = idx % per;
+    const int64_t d = r % D, n = (r / D) % N, b = r / (N * D);
+    float v = 0.0f;
+    if (c == 0) {
+        if (h_in) v = h_in[(b * D + d) * N + n];
+    } else if (dh_in) {
+        v = dh_in[(((c - 1) * Bsz + b) * D + d) * N + n];
+    }
+    state[idx] = v;
+}
+
+__global__ __launch_bounds__(kThreads) void k_state_export(
+    const float *__restrict__ state, float *__restrict__ h_out, float *__restrict__ dh_out,
+    int64_t Bsz, int64_t D, int64_t N, int K) {
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t per = Bsz * N * D;
+    if (idx >= per * (1 + K)) return;
+    const int64_t c = idx / per, r = idx % per;
+    const int64_t d = r % D, n = (r / D) % N, b = r / (N * D);
+    if (c == 0) {
+        if (h_out) h_out[(b * D + d) * N + n] = state[idx];
+    } else if (dh_out) {
+        dh_out[(((c - 1) * Bsz + b) * D + d) * N + n] = state[idx];
+    }
+}
+
+// ---------------------------------------------------------------- timing
+namespace {
+struct Timing {
+    std::mutex mu;
+    bool on = false;
+    struct Rec { int kind; hipEvent_t a, b; };
+    std::vector<Rec> recs;
+    std::vector<hipEvent_t> pool;
+} g_timing;
+
+hipEvent_t take_event() {
+    if (!g_timing.pool.empty()) {
+        hipEvent_t e = g_timing.pool.back();
+        g_timing.pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Brackets one launch with events when timing is on.
+struct Timed {
+    int kind;
+    hipStream_t st;
+    hipEvent_t a = nullptr, b = nullptr;
+    Timed(int k, hipStream_t s) : kind(k), st(s) {
+        if (!g_timing.on) return;
+        std::lock_guard<std::mutex> lk(g_timing.mu);
+        a = take_event();
+        b = take_event();
+        if (a) (void)hipEventRecord(a, st);
+    }
+    ~Timed() {
+        if (!a || !b) return;
+        (void)hipEventRecord(b, st);
+        std::lock_guard<std::mutex> lk(g_timing.mu);
+        g_timing.recs.push_back({kind, a, b});
+    }
+};
+}  // namespace
+
+// ---------------------------------------------------------------- dispatch
+template <typename InT>
+struct Launcher {
+    const Plan &q;
+    const pgf_params &p;
+    const InT *x;
+    const InT *dx;
+    float *y, *dy;
+    hipStream_t st;
+    char *ws;
+
+    float *state() const { return (float *)(ws + q.ws.state); }
+    float *bcw() const { return (float *)(ws + q.ws.bc); }
+    float *agg_h() const { return (float *)(ws + q.ws.agg_h); }
+    float *agg_s() const { return (float *)(ws + q.ws.agg_s); }
+    float *seg_in() const { return (float *)(ws + q.ws.seg_in); }
+
+    template <int NC>
+    void proj_nc(int64_t t0, int64_t len) {
+        constexpr int CT = NC >= 64 ? 8 : 4;
+        constexpr int CG = NC / CT;
+        constexpr int RT = (NC >= 32) ? (NC >= 128 ? 4 : 2) : 1;
+        constexpr int TM = (kThreads / CG) * RT;
+        dim3 grid((unsigned)((len + TM - 1) / TM), (unsigned)(1 + q.K), (unsigned)q.B);
+        Timed tm(0, st);
+        hipLaunchKernelGGL((k_proj<NC, CT, RT, InT>), grid, dim3(kThreads), 0, st, x, dx, p.W_B, p.W_C, p.b_B,
+                           p.b_C, bcw(), q.B, q.L, q.D, (int)q.K, t0, len, q.chunk_len);
+    }
+
+    void proj(int64_t t0, int64_t len) {
+        switch (q.N) {
+            case 4: proj_nc<8>(t0, len); break;
+            case 8: proj_nc<16>(t0, len); break;
+            case 16: proj_nc<32>(t0, len); break;
+            case 32: proj_nc<64>(t0, len); break;
+            default: proj_nc<128>(t0, len); break;
+        }
+    }
+
+    template <int NT, int NS, int K>
+    void scans(int64_t t0, int64_t len) {
+        const unsigned gx = (unsigned)((q.D * NS + kThreads - 1) / kThreads);
+        const int64_t ND = q.N * q.D;
+        if (q.seg == 0) {
+            // Sequential evaluation: one segment per block, state in place.
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_scan<NT, NS, K, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x,
+                               dx, p.A, p.w_delta, p.b_delta, bcw(), state(), ND, (int64_t)0, q.B * ND, y, dy,
+                               state(), (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len,
+                               len, 1);
+            return;
+        }
+        const int G = (int)((len + q.seg - 1) / q.seg);
+        {
+            Timed tm(1, st);
+            hipLaunchKernelGGL((k_scan<NT, NS, K, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B),
+                               dim3(kThreads), 0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(),
+                               (const float *)nullptr, (int64_t)0, (int64_t)0, (int64_t)0, y, dy, (float *)nullptr,
+                               agg_h(), agg_s(), q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+        }
+        {
+            const int64_t lanes = q.B * ND;
+            Timed tm(2, st);
+            hipLaunchKernelGGL((k_carry<K>), dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                               st, p.A, agg_h(), agg_s(), state(), seg_in(), q.B, q.D, q.N, G);
+        }
+        {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_scan<NT, NS, K, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads),
+                               0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(), seg_in(), (int64_t)G * (1 + K) * ND,
+                               (int64_t)(1 + K) * ND, ND, y, dy, (float *)nullptr, (float *)nullptr,
+                               (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+        }
+    }
+
+    // Tilings the planner can choose: nt = min(N, 16) for K <= 2 and
+    // nt = min(N, 8) for K >= 4, ns = N / nt.
+    template <int K>
+    bool scan_block_k(int64_t t0, int64_t len) {
+        const int code = q.nt * 100 + q.ns;
+        if constexpr (K <= 2) {
+            switch (code) {
+                case 401: scans<4, 1, K>(t0, len); return true;
+                case 801: scans<8, 1, K>(t0, len); return true;
+                case 1601: scans<16, 1, K>(t0, len); return true;
+                case 1602: scans<16, 2, K>(t0, len); return true;
+                case 1604: scans<16, 4, K>(t0, len); return true;
+                default: return false;
+            }
+        } else {
+            switch (code) {
+                case 401: scans<4, 1, K>(t0, len); return true;
+                case 801: scans<8, 1, K>(t0, len); return true;
+                case 802: scans<8, 2, K>(t0, len); return true;
+                case 804: scans<8, 4, K>(t0, len); return true;
+                case 808: scans<8, 8, K>(t0, len); return true;
+                default: return false;
+            }
+        }
+    }
+
+    bool scan_block(int64_t t0, int64_t len) {
+        switch (q.K) {
+            case 1: return scan_block_k<1>(t0, len);
+            case 2: return scan_block_k<2>(t0, len);
+            case 4: return scan_block_k<4>(t0, len);
+            case 8: return scan_block_k<8>(t0, len);
+            default: return false;
+        }
+    }
+
+    int run() {
+        const int64_t lanes_all = (1 + q.K) * q.B * q.N * q.D;
+        const unsigned gs = (unsigned)((lanes_all + kThreads - 1) / kThreads);
+        {
+            Timed tm(4, st);
+            hipLaunchKernelGGL(k_state_import, dim3(gs), dim3(kThreads), 0, st, p.h_in, p.dh_in, state(), q.B, q.D,
+                               q.N, (int)q.K);
+        }
+        for (int64_t t0 = 0; t0 < q.L; t0 += q.chunk_len) {
+            const int64_t len = q.L - t0 < q.chunk_len ? q.L - t0 : q.chunk_len;
+            proj(t0, len);
+            if (!scan_block(t0, len)) return PGF_ERR_UNSUPPORTED;
+        }
+        if (p.h_out || p.dh_out) {
+            Timed tm(4, st);
+            hipLaunchKernelGGL(k_state_export, dim3(gs), dim3(kThreads), 0, st, state(), p.h_out, p.dh_out, q.B, q.D,
+                               q.N, (int)q.K);
+        }
+        return hipGetLastError() == hipSuccess ? PGF_OK : PGF_ERR_HIP;
+    }
+};
+
+namespace {
+bool overlap(const void *a, size_t na, const void *b, size_t nb) {
+    const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
+    return na && nb && pa < pb + nb && pb < pa + na;
+}
+}  // namespace
+
+}  // namespace pgf
+
+extern "C" int pgf_scan_jvp(const void *x, const void *dx, const pgf_params *p, float *y, float *dy, void *stream) {
+    using namespace pgf;
+    Plan q;
+    const int rc = make_plan(p, &q);
+    if (rc != PGF_OK) return rc;
+    if (!p->A || !p->w_delta || !p->b_delta || !p->W_B || !p->W_C) return PGF_ERR_INVALID_ARG;
+    if (!p->workspace || p->workspace_bytes < q.ws.total || ((uintptr_t)p->workspace & 255))
+        return PGF_ERR_WORKSPACE;
+    const size_t esz = q.in_bf16 ? 2 : 4;
+    const size_t nx = (size_t)q.B * q.L * q.D;
+    const size_t bx = nx * esz, bdx = nx * q.K * esz, by = nx * 4, bdy = nx * q.K * 4;
+    if (q.L > 0) {
+        if (!x || !dx || !y || !dy) return PGF_ERR_INVALID_ARG;
+        if (overlap(y, by, x, bx) || overlap(y, by, dx, bdx) || overlap(dy, bdy, x, bx) ||
+            overlap(dy, bdy, dx, bdx) || overlap(y, by, dy, bdy))
+            return PGF_ERR_INVALID_ARG;
+        if (overlap(p->workspace, q.ws.total, y, by) || overlap(p->workspace, q.ws.total, dy, bdy))
+            return PGF_ERR_INVALID_ARG;
+    }
+    // Clear any stale error from earlier, unrelated work on this thread.
+    (void)hipGetLastError();
+    hipStream_t st = (hipStream_t)stream;
+    if (q.in_bf16) {
+        Launcher<uint16_t> l{q, *p, (const uint16_t *)x, (const uint16_t *)dx, y, dy, st, (char *)p->workspace};
+        return l.run();
+    }
+    Launcher<float> l{q, *p, (const float *)x, (const float *)dx, y, dy, st, (char *)p->workspace};
+    return l.run();
+}
+
+extern "C" int pgf_timing_enable(int on) {
+    std::lock_guard<std::mutex> lk(pgf::g_timing.mu);
+    pgf::g_timing.on = on != 0;
+    return PGF_OK;
+}
+
+extern "C" int pgf_timing_read(double *ms, int64_t *launches) {
+    using namespace pgf;
+    std::lock_guard<std::mutex> lk(g_timing.mu);
+    for (int i = 0; i < PGF_TIMING_KINDS; ++i) {
+        if (ms) ms[i] = 0.0;
+        if (launches) launches[i] = 0;
+    }
+    int rc = PGF_OK;
+    for (auto &r : g_timing.recs) {
+        float t = 0.0f;
+        if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&t, r.a, r.b) != hipSuccess) rc = PGF_ERR_HIP;
+        if (r.kind >= 0 && r.kind < PGF_TIMING_KINDS) {
+            if (ms) ms[r.kind] += t;
+            if (launches) launches[r.kind] += 1;
+        }
+        g_timing.pool.push_back(r.a);
+        g_timing.pool.push_back(r.b);
+    }
+    g_timing.recs.clear();
+    return rc;
+}

@@ -1,0 +1,57 @@
+"""Helpers of the GPU tests: run the HIP path on seeded inputs and compare
+with the fp64 oracle."""
+import numpy as np
+import torch
+
+from oracle import oracle
+from paper_2512_23068_amd import binding, inputs
+
+PARAM_KEYS = ("A", "w_delta", "b_delta", "W_B", "W_C", "b_B", "b_C")
+TOL = 1e-5   # relative L2, f32 state against the fp64 oracle
+
+
+def dev():
+    return torch.device("cuda:0")
+
+
+def params_to_dev(inp):
+    return {k: torch.from_numpy(np.ascontiguousarray(inp[k])).to(dev()) for k in PARAM_KEYS if k in inp}
+
+
+def inputs_to_dev(inp, bf16=None):
+    if bf16 is None:
+        bf16 = inp.get("cfg") is not None and inp["cfg"].in_dtype == "bf16"
+    x = torch.from_numpy(inp["x"]).to(dev())
+    dx = torch.from_numpy(inp["dx"]).to(dev())
+    if bf16:   # the values are already bf16-representable: the cast is exact
+        x, dx = x.to(torch.bfloat16), dx.to(torch.bfloat16)
+    return x, dx
+
+
+def run(inp, bf16=None, **kw):
+    x, dx = inputs_to_dev(inp, bf16)
+    out = binding.scan_jvp(x, dx, params_to_dev(inp), **kw)
+    torch.cuda.synchronize()
+    return out
+
+
+def rel_l2(got, ref):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.linalg.norm(ref.ravel())
+    return float(np.linalg.norm((got - ref).ravel()) / (den if den > 0 else 1.0))
+
+
+def assert_close(y, dy, yo, dyo, tol=TOL, what=""):
+    ey = rel_l2(y, yo)
+    edys = [rel_l2(dy[k], dyo[k]) for k in range(dyo.shape[0])]
+    print(f"{what} rel_l2 y={ey:.3e} dy={max(edys):.3e}", flush=True)
+    assert np.all(np.isfinite(y)) and np.all(np.isfinite(dy))
+    assert ey <= tol, (what, ey)
+    assert max(edys) <= tol, (what, edys)
+    return ey, max(edys)
+
+
+def custom(name, **kw):
+    """A workload with the recipe of `name` and some sizes changed."""
+    return inputs.make_inputs(inputs.get_config(name).with_(**kw))

@@ -1,0 +1,126 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every symbol include/pgf.h declares, plans tilings whose workspace does not
+depend on L, and rejects bad arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2512_23068_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    with open(os.path.join(ROOT, "include", "pgf.h")) as f:
+        txt = f.read()
+    return sorted(set(re.findall(r"\b(pgf_[a-z_]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = binding.lib()
+    names = _declared_functions()
+    assert set(names) == set(binding.EXPORTED), names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    for code in (0, -1, -2, -3, -4):
+        assert binding.status_string(code).startswith("PGF_")
+    assert "unknown" in binding.status_string(7)
+
+
+@pytest.mark.parametrize("shape", [(1, 16, 16, 1), (1, 1536, 16, 1), (1, 5120, 16, 1), (4, 2048, 64, 8),
+                                   (2, 300, 32, 2), (3, 77, 4, 4)])
+def test_workspace_independent_of_L(shape):
+    B, D, N, K = shape
+    sizes = {binding.workspace_bytes(B, L, D, N, K) for L in (1, 1000, 8192, 16384, 32768, 65536, 131072, 1 << 22)}
+    assert len(sizes) == 1 and sizes.pop() > 0
+    p0 = binding.plan(B, 8192, D, N, K)
+    p1 = binding.plan(B, 131072, D, N, K)
+    for k in ("n_per_thread", "n_split", "seg_len", "chunk_segs", "chunk_len", "workspace_bytes"):
+        assert p0[k] == p1[k], k
+
+
+def test_plans_of_the_benchmark_workloads():
+    p = binding.plan(1, 131072, 1536, 16, 1)
+    assert p["n_per_thread"] * p["n_split"] == 16 and p["seg_len"] > 0
+    assert p["chunk_len"] == p["seg_len"] * p["chunk_segs"]
+    assert p["n_chunks"] == -(-131072 // p["chunk_len"])
+    p = binding.plan(4, 32768, 2048, 64, 8)
+    assert p["n_per_thread"] * p["n_split"] == 64
+    # workspace stays a small fraction of the 19 GB IO payload
+    assert p["workspace_bytes"] < 512 << 20
+    p = binding.plan(1, 131072, 5120, 16, 1, in_dtype="bf16")
+    assert p["workspace_bytes"] < 256 << 20
+
+
+def test_tiling_overrides():
+    p = binding.plan(1, 5000, 64, 16, 1, seg_len=-1)
+    assert p["seg_len"] == 0
+    p = binding.plan(1, 5000, 64, 16, 1, seg_len=128, chunk_segs=3)
+    assert p["seg_len"] == 128 and p["chunk_segs"] == 3 and p["chunk_len"] == 384 and p["n_chunks"] == 14
+    for bad in (dict(seg_len=100), dict(seg_len=8), dict(seg_len=1 << 17), dict(chunk_segs=-2),
+                dict(chunk_segs=5000)):
+        with pytest.raises(RuntimeError, match="INVALID_ARG"):
+            binding.plan(1, 5000, 64, 16, 1, **bad)
+
+
+@pytest.mark.parametrize("B,L,D,N,K,code", [
+    (0, 10, 16, 16, 1, "INVALID_ARG"), (1, -1, 16, 16, 1, "INVALID_ARG"), (1, 10, 0, 16, 1, "INVALID_ARG"),
+    (1, 10, 16, 0, 1, "INVALID_ARG"), (1, 10, 16, 16, 0, "INVALID_ARG"),
+    (1, 10, 16, 12, 1, "UNSUPPORTED"), (1, 10, 16, 128, 1, "UNSUPPORTED"), (1, 10, 16, 16, 3, "UNSUPPORTED"),
+    (1, 10, 16, 16, 9, "UNSUPPORTED")])
+def test_invalid_sizes(B, L, D, N, K, code):
+    assert binding.workspace_bytes(B, L, D, N, K) == 0
+    with pytest.raises(RuntimeError, match=code):
+        binding.plan(B, L, D, N, K)
+
+
+def _call(p, x=1 << 20, dx=2 << 20, y=3 << 20, dy=4 << 20):
+    """pgf_scan_jvp with fake (never dereferenced) addresses: every case here
+    fails the host-side checks, which run before any HIP call."""
+    lib = binding.lib()
+    v = lambda a: ctypes.c_void_p(a) if a else None
+    return lib.pgf_scan_jvp(v(x), v(dx), ctypes.byref(p), v(y), v(dy), None)
+
+
+def _valid_params(L=100, D=16, N=16, K=1):
+    p = binding.make_params(1, L, D, N, K)
+    base = 1 << 30
+    for i, name in enumerate(("A", "w_delta", "b_delta", "W_B", "W_C")):
+        setattr(p, name, base + i * 4096)
+    p.workspace_bytes = binding.lib().pgf_workspace_bytes(ctypes.byref(p))
+    p.workspace = 1 << 36
+    return p
+
+
+def test_scan_rejects_bad_arguments_before_launch():
+    ok = _valid_params()
+    # the fake pointers above are all disjoint: only the listed defects fail
+    for field in ("A", "w_delta", "b_delta", "W_B", "W_C"):
+        p = _valid_params()
+        setattr(p, field, None)
+        assert _call(p) == -1, field
+    p = _valid_params()
+    p.workspace = None
+    assert _call(p) == -3
+    p = _valid_params()
+    p.workspace_bytes -= 1
+    assert _call(p) == -3
+    p = _valid_params()
+    p.workspace += 4          # misaligned
+    assert _call(p) == -3
+    assert _call(ok, x=0) == -1
+    assert _call(ok, dy=0) == -1
+    # y overlapping x (100*16*4 bytes each)
+    assert _call(ok, x=1 << 20, y=(1 << 20) + 64) == -1
+    # dy overlapping y
+    assert _call(ok, y=3 << 20, dy=(3 << 20) + 128) == -1
+    p = _valid_params()
+    p.in_dtype = 5
+    assert _call(p) == -1
+    p = _valid_params(N=12)
+    assert _call(p) == -2

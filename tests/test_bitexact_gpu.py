@@ -1,0 +1,123 @@
+"""Bit-exact properties of the HIP path (GPU against GPU): tiling, state
+hand-off (the block hand-off of Alg. 1), causality, batch and direction
+independence, determinism, exact zeros ahead of a ghost pulse, channel
+isolation.  torch.equal treats -0 and +0 as equal."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2512_23068_amd import binding
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+
+def _inp(**kw):
+    base = dict(batch=2, seqlen=1300, d_inner=96, n_dirs=2)
+    base.update(kw)
+    return gu.custom("mamba130m", **base)
+
+
+@pytest.mark.parametrize("seg", [64, -1])
+def test_block_size_invariance(seg):
+    inp = _inp()
+    ref = gu.run(inp, seg_len=seg, chunk_segs=1)
+    for cs in (2, 3, 7, 0):
+        got = gu.run(inp, seg_len=seg, chunk_segs=cs)
+        assert torch.equal(got[0], ref[0]) and torch.equal(got[1], ref[1]), cs
+
+
+@pytest.mark.parametrize("seg,split", [(64, 640), (-1, 500)])
+def test_split_call_handoff(seg, split):
+    """Two calls chained through h_out -> h_in equal one call."""
+    inp = _inp()
+    y, dy, h, dh = gu.run(inp, seg_len=seg, return_state=True)
+    x, dx = gu.inputs_to_dev(inp)
+    prm = gu.params_to_dev(inp)
+    y1, dy1, h1, dh1 = binding.scan_jvp(x[:, :split], dx[:, :, :split], prm, seg_len=seg, return_state=True)
+    y2, dy2, h2, dh2 = binding.scan_jvp(x[:, split:], dx[:, :, split:], prm, seg_len=seg, h_in=h1, dh_in=dh1,
+                                        return_state=True)
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat([y1, y2], 1), y) and torch.equal(torch.cat([dy1, dy2], 2), dy)
+    assert torch.equal(h2, h) and torch.equal(dh2, dh)
+
+
+def test_prefix_causality():
+    inp = _inp()
+    y, dy = gu.run(inp, seg_len=64)
+    x, dx = gu.inputs_to_dev(inp)
+    for Lp in (64, 640, 999):
+        yp, dyp = binding.scan_jvp(x[:, :Lp], dx[:, :, :Lp], gu.params_to_dev(inp), seg_len=64)
+        torch.cuda.synchronize()
+        assert torch.equal(yp, y[:, :Lp]) and torch.equal(dyp, dy[:, :, :Lp]), Lp
+
+
+def test_batch_slicing():
+    inp = _inp(batch=3)
+    y, dy = gu.run(inp, seg_len=64)
+    x, dx = gu.inputs_to_dev(inp)
+    yb, dyb = binding.scan_jvp(x[1:2], dx[:, 1:2], gu.params_to_dev(inp), seg_len=64)
+    torch.cuda.synchronize()
+    assert torch.equal(yb, y[1:2]) and torch.equal(dyb, dy[:, 1:2])
+
+
+@pytest.mark.parametrize("K_small,K_big", [(1, 2), (4, 8)])
+def test_direction_independence(K_small, K_big):
+    """With the same tiling, direction k of a K-direction call equals a call
+    on dx_k alone (and y does not depend on K)."""
+    inp = gu.custom("multidir", batch=1, seqlen=700, d_inner=80, d_state=16, n_dirs=K_big)
+    pb, ps = binding.plan(1, 700, 80, 16, K_big), binding.plan(1, 700, 80, 16, K_small)
+    assert (pb["n_per_thread"], pb["n_split"]) == (ps["n_per_thread"], ps["n_split"])
+    y, dy = gu.run(inp, seg_len=128, chunk_segs=8)
+    for k0 in range(0, K_big, K_small):
+        sub = dict(inp)
+        sub["dx"] = np.ascontiguousarray(inp["dx"][k0:k0 + K_small])
+        ys, dys = gu.run(sub, seg_len=128, chunk_segs=8)
+        assert torch.equal(ys, y) and torch.equal(dys, dy[k0:k0 + K_small]), k0
+
+
+def test_determinism():
+    inp = _inp()
+    a = gu.run(inp)
+    for _ in range(3):
+        b = gu.run(inp)
+        assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+@pytest.mark.parametrize("seg", [0, -1])
+def test_ghost_pulse_zeros(seg):
+    """dx zero before t0 gives dy exactly zero before t0; after t0 the
+    response is nonzero in every channel (Sec. 5.3 ghost pulse)."""
+    inp = _inp(batch=1)
+    t0 = 777
+    dxp = np.zeros_like(inp["dx"])
+    dxp[:, :, t0, 5] = 1e-3
+    inp["dx"] = dxp
+    y, dy = gu.run(inp, seg_len=seg)
+    dy = dy.cpu()
+    assert torch.all(dy[:, :, :t0] == 0)
+    assert torch.all(dy[:, :, t0:].abs().sum(-1) > 0)
+    inp["dx"] = np.zeros_like(dxp)
+    _, dz = gu.run(inp, seg_len=seg)
+    assert torch.all(dz == 0)
+
+
+def test_channel_isolation():
+    """With W_B = W_C = 0 (biases carry B and C) channels are independent:
+    perturbing channel 3 leaves every other channel's bits unchanged."""
+    inp = _inp(batch=1)
+    g = np.random.default_rng(3)
+    inp["W_B"] = np.zeros_like(inp["W_B"])
+    inp["W_C"] = np.zeros_like(inp["W_C"])
+    inp["b_B"] = g.standard_normal(16).astype(np.float32)
+    inp["b_C"] = g.standard_normal(16).astype(np.float32)
+    y, dy = gu.run(inp)
+    inp2 = dict(inp)
+    inp2["x"] = inp["x"].copy()
+    inp2["x"][:, :, 3] += 0.5
+    inp2["dx"] = inp["dx"].copy()
+    inp2["dx"][:, :, :, 3] *= -2
+    y2, dy2 = gu.run(inp2)
+    keep = [d for d in range(96) if d != 3]
+    assert torch.equal(y[..., keep], y2[..., keep]) and torch.equal(dy[..., keep], dy2[..., keep])
+    assert not torch.equal(y[..., 3], y2[..., 3])

@@ -1,0 +1,116 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle on seeded
+inputs: element-by-element at sizes the oracle finishes in seconds, across
+every tiling the planner can choose, ragged tiles, both evaluations
+(sequential and segmented), both input dtypes and the stiff regime.  The
+gate is a relative L2 error of 1e-5 per output (y and every dy_k)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2512_23068_amd import binding, inputs
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(inp, what, **kw):
+    print(f"case {what}", flush=True)
+    y, dy = gu.run(inp, **kw)
+    yo, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp)
+    return gu.assert_close(y.cpu().numpy(), dy.cpu().numpy(), yo, dyo, what=what)
+
+
+def test_tiny_workload_full():
+    """B=1 L=1024 D=16 N=16 K=1, unit impulse tangent at t=0, d=0."""
+    _check(inputs.make_inputs("tiny"), "tiny")
+
+
+@pytest.mark.parametrize("seg", [0, -1, 64])
+def test_multi_tile_ragged(seg):
+    """Several channel blocks, segments and prefetch tiles, all ragged."""
+    inp = gu.custom("mamba130m", batch=2, seqlen=1500, d_inner=300, n_dirs=2)
+    _check(inp, f"ragged seg={seg}", seg_len=seg)
+
+
+# Every (n_per_thread, n_split) the planner can choose, for K <= 2 and K >= 4.
+@pytest.mark.parametrize("N,K", [(4, 1), (8, 2), (16, 1), (32, 2), (64, 1),
+                                 (4, 4), (8, 8), (16, 4), (32, 8), (64, 8)])
+def test_tilings(N, K):
+    inp = gu.custom("multidir", batch=1, seqlen=600, d_inner=72, d_state=N, n_dirs=K)
+    p = binding.plan(1, 600, 72, N, K)
+    _check(inp, f"N={N} K={K} nt={p['n_per_thread']} ns={p['n_split']}")
+
+
+@pytest.mark.parametrize("N,K", [(16, 1), (64, 8)])
+def test_sequential_evaluation(N, K):
+    inp = gu.custom("multidir", batch=2, seqlen=700, d_inner=130, d_state=N, n_dirs=K)
+    _check(inp, f"sequential N={N} K={K}", seg_len=-1, chunk_segs=0)
+
+
+def test_bf16_stiff_regime():
+    """bf16 inputs, A = -exp(U(0,7)), Delta in [1e-3, 10]: Abar underflows to
+    zero in many lanes; no Inf/NaN and the same tolerance."""
+    inp = gu.custom("stiff128k", seqlen=3000, d_inner=96)
+    a = np.exp(np.log(np.logaddexp(0, inp["b_delta"].astype(np.float64)))[:, None] * inp["A"])
+    assert (a == 0).mean() > 0.05          # the regime really underflows
+    _check(inp, "stiff bf16")
+    _check(inp, "stiff bf16 sequential", seg_len=-1)
+
+
+def test_biases_and_entry_state():
+    inp = gu.custom("mamba130m", batch=2, seqlen=900, d_inner=64, n_dirs=2)
+    g = np.random.default_rng(5)
+    inp["b_B"] = g.standard_normal(16).astype(np.float32)
+    inp["b_C"] = g.standard_normal(16).astype(np.float32)
+    h0 = g.standard_normal((2, 64, 16)).astype(np.float32)
+    dh0 = g.standard_normal((2, 2, 64, 16)).astype(np.float32)
+    y, dy, h, dh = gu.run(inp, h_in=torch.from_numpy(h0), dh_in=torch.from_numpy(dh0), return_state=True)
+    yo, dyo, ho, dho = oracle.scan_jvp(inp["x"], inp["dx"], inp, h_in=h0, dh_in=dh0)
+    gu.assert_close(y.cpu().numpy(), dy.cpu().numpy(), yo, dyo, what="bias+state")
+    assert gu.rel_l2(h.cpu().numpy(), ho) < 1e-5 and gu.rel_l2(dh.cpu().numpy(), dho) < 1e-5
+
+
+@pytest.mark.parametrize("L", [1, 7, 255, 256, 257])
+def test_short_sequences(L):
+    inp = gu.custom("mamba130m", seqlen=L, d_inner=40, n_dirs=1)
+    _check(inp, f"L={L}")
+
+
+def test_empty_sequence_passes_state_through():
+    inp = gu.custom("tiny", seqlen=0)
+    g = np.random.default_rng(9)
+    h0 = torch.from_numpy(g.standard_normal((1, 16, 16)).astype(np.float32))
+    dh0 = torch.from_numpy(g.standard_normal((1, 1, 16, 16)).astype(np.float32))
+    y, dy, h, dh = gu.run(inp, h_in=h0, dh_in=dh0, return_state=True)
+    assert y.shape == (1, 0, 16) and dy.shape == (1, 1, 0, 16)
+    assert torch.equal(h.cpu(), h0) and torch.equal(dh.cpu(), dh0)
+
+
+def test_single_channel():
+    inp = gu.custom("tiny", d_inner=1, seqlen=500, dx_kind="normal")
+    _check(inp, "D=1")
+
+
+def test_workspace_too_small_is_rejected():
+    inp = gu.custom("tiny", seqlen=64)
+    x, dx = gu.inputs_to_dev(inp)
+    ws = torch.empty(16, device=gu.dev(), dtype=torch.uint8)
+    nbytes = binding.workspace_bytes(1, 64, 16, 16, 1)
+    assert nbytes > 16
+    y = torch.full((1, 64, 16), 7.0, device=gu.dev())
+    dy = torch.full((1, 1, 64, 16), 7.0, device=gu.dev())
+    # a workspace tensor smaller than needed is replaced by the binding, so
+    # call the ABI with a too-small size directly
+    import ctypes
+    pr = binding.make_params(1, 64, 16, 16, 1)
+    prm = gu.params_to_dev(inp)
+    for k in ("A", "w_delta", "b_delta", "W_B", "W_C"):
+        setattr(pr, k, prm[k].data_ptr())
+    pr.workspace, pr.workspace_bytes = ws.data_ptr(), 16
+    rc = binding.lib().pgf_scan_jvp(ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(dx.data_ptr()),
+                                    ctypes.byref(pr), ctypes.c_void_p(y.data_ptr()),
+                                    ctypes.c_void_p(dy.data_ptr()), None)
+    assert rc == -3
+    torch.cuda.synchronize()
+    assert torch.all(y == 7.0) and torch.all(dy == 7.0)   # outputs untouched
