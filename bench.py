@@ -30,6 +30,8 @@ def parse():
     ap.add_argument("--workload", default="pulse128k")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline leg")
     ap.add_argument("--cpu-steps", type=int, default=0, help="oracle sample length (0 = auto)")
+    ap.add_argument("--seg-len", type=int, default=0, help="tiling override (0 = library default)")
+    ap.add_argument("--chunk-segs", type=int, default=0, help="tiling override (0 = library default)")
     return ap.parse_args()
 
 
@@ -67,13 +69,14 @@ def main():
     del inp
     y = torch.empty((B, L, D), device=dev)
     dy = torch.empty((K, B, L, D), device=dev)
-    plan = binding.plan(B, L, D, N, K, cfg.in_dtype)
+    plan = binding.plan(B, L, D, N, K, cfg.in_dtype, args.seg_len, args.chunk_segs)
     ws = torch.empty(plan["workspace_bytes"], device=dev, dtype=torch.uint8)
     torch.cuda.synchronize()
     base_alloc = torch.cuda.memory_allocated()
 
     def step():
-        binding.scan_jvp(x, dx, params, workspace=ws, out=(y, dy))
+        binding.scan_jvp(x, dx, params, workspace=ws, out=(y, dy), seg_len=args.seg_len,
+                         chunk_segs=args.chunk_segs)
 
     for _ in range(args.warmup):
         step()

@@ -21,10 +21,24 @@ namespace {
 
 constexpr int64_t kMaxSeg = 65536;
 constexpr int kMaxChunkSegs = 4096;
-// Waves the default tiling aims to keep resident (a few per SIMD).
-constexpr int64_t kTargetWaves = 4096;
+// Scan blocks (256 threads) resident at once on an MI355X: 256 compute units
+// x 4 blocks at the scan kernels' register use.  A launch whose block count
+// is a multiple of this has no partly filled last round.
+constexpr int64_t kResidentBlocks = 1024;
+constexpr int64_t kSimds = 1024;
 constexpr int64_t kDefaultSeg = 256;
 constexpr int64_t kSeqChunk = 4096;
+constexpr int64_t kMaxChunkLen = int64_t(1) << 18;
+constexpr size_t kWorkspaceCap = size_t(256) << 20;
+
+int64_t gcd64(int64_t a, int64_t b) {
+    while (b) {
+        const int64_t t = a % b;
+        a = b;
+        b = t;
+    }
+    return a;
+}
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
@@ -52,7 +66,8 @@ int make_plan(const pgf_params *p, Plan *plan) {
     q.ns = (int)(N / q.nt);
     q.R = (int)(2 * N * (1 + K));
 
-    const int64_t waves_per_col = (B * D * q.ns + 63) / 64;
+    // Blocks of one segment column (every channel, one segment).
+    const int64_t nblk = B * ((D * q.ns + 255) / 256);
     int64_t seg;
     if (p->seg_len == -1) {
         seg = 0;
@@ -60,19 +75,40 @@ int make_plan(const pgf_params *p, Plan *plan) {
         if (p->seg_len < 16 || p->seg_len > kMaxSeg || !is_pow2(p->seg_len)) return PGF_ERR_INVALID_ARG;
         seg = p->seg_len;
     } else {
-        seg = (2 * waves_per_col >= kTargetWaves) ? 0 : kDefaultSeg;
+        // Sequential when one segment column already gives every SIMD a wave
+        // (a block is 4 waves; an MI355X has 1024 SIMDs).
+        seg = (nblk * 4 >= kSimds) ? 0 : kDefaultSeg;
     }
+    // Kernels address one host block with 32-bit element offsets.
+    constexpr int64_t kMaxBlockElems = int64_t(1) << 30;
     int64_t cs;
     if (p->chunk_segs < 0 || p->chunk_segs > kMaxChunkSegs) return PGF_ERR_INVALID_ARG;
+    const int64_t unit = seg ? seg : kSeqChunk;
+    if (unit * D > kMaxBlockElems) return PGF_ERR_UNSUPPORTED;
+    const int64_t cs_max = kMaxBlockElems / (unit * D);
+    if (p->chunk_segs > cs_max) return PGF_ERR_INVALID_ARG;
     if (seg == 0) {
         cs = p->chunk_segs ? p->chunk_segs : 1;
         q.chunk_len = cs * kSeqChunk;
         q.chunk_segs = 1;
         cs = 1;
+    } else if (p->chunk_segs) {
+        cs = p->chunk_segs;
+        q.chunk_len = cs * seg;
+        q.chunk_segs = (int)cs;
     } else {
-        cs = p->chunk_segs ? p->chunk_segs
-                           : std::max<int64_t>(1, (kTargetWaves + waves_per_col - 1) / waves_per_col);
-        cs = std::min<int64_t>(cs, kMaxChunkSegs);
+        // At least three rounds of resident blocks per launch, rounded to a
+        // whole number of rounds when the workspace allows it.
+        const size_t per_seg = (size_t)B * (1 + K) * (size_t)(N * D + D) * sizeof(float) +
+                               (size_t)B * seg * q.R * sizeof(float);
+        const int64_t cap = std::max<int64_t>(1, (int64_t)(kWorkspaceCap / per_seg));
+        const int64_t period = kResidentBlocks / gcd64(nblk, kResidentBlocks);
+        const int64_t want = (3 * kResidentBlocks + nblk - 1) / nblk;
+        cs = (want + period - 1) / period * period;
+        if (cs > cap) cs = cap >= period ? cap / period * period : cap;
+        cs = std::min<int64_t>(cs, kMaxChunkLen / seg);
+        cs = std::min<int64_t>(std::min<int64_t>(cs, kMaxChunkSegs), cs_max);
+        cs = std::max<int64_t>(cs, 1);
         q.chunk_len = cs * seg;
         q.chunk_segs = (int)cs;
     }
@@ -89,9 +125,8 @@ int make_plan(const pgf_params *p, Plan *plan) {
         const size_t G = (size_t)cs;
         w.agg_h = off;  off = align256(off + (size_t)B * G * comp * N * D * f);
         w.agg_s = off;  off = align256(off + (size_t)B * G * comp * D * f);
-        w.seg_in = off; off = align256(off + (size_t)B * G * comp * N * D * f);
     } else {
-        w.agg_h = w.agg_s = w.seg_in = off;
+        w.agg_h = w.agg_s = off;
     }
     w.total = off;
     q.ws = w;

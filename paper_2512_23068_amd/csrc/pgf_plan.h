@@ -14,11 +14,12 @@ namespace pgf {
 //   state   [(1+K)][B][N][D]         state carried between host blocks
 //   bc      [B][Tc][R]               per-step projections of one host block,
 //                                    R = 2N(1+K): B, dB_0..dB_{K-1}, C, dC_0..
-//   agg_h   [B][G][(1+K)][N][D]      segment end states from a zero start
+//   agg_h   [B][G][(1+K)][N][D]      segment end states from a zero start,
+//                                    then (in place) the true state
+//                                    entering each segment
 //   agg_s   [B][G][(1+K)][D]         segment sums of Delta and dDelta_k
-//   seg_in  [B][G][(1+K)][N][D]      true state entering each segment
 struct Layout {
-    size_t state, bc, agg_h, agg_s, seg_in, total;
+    size_t state, bc, agg_h, agg_s, total;
 };
 
 struct Plan {

@@ -35,9 +35,18 @@ constexpr int kThreads = 256;
 
 // ---------------------------------------------------------------- helpers
 
-__device__ __forceinline__ float load_in(const float *__restrict__ p, int64_t i) { return p[i]; }
-__device__ __forceinline__ float load_in(const uint16_t *__restrict__ p, int64_t i) {
-    return __uint_as_float(((uint32_t)p[i]) << 16);
+// Loads of the input sequences at a 32-bit element offset from a base
+// pointer that is the same for the whole wave: the address is formed from a
+// scalar base and a 32-bit vector offset, with no 64-bit arithmetic per step.
+__device__ __forceinline__ float load_in(const float *__restrict__ base, uint32_t i) {
+    return *(const float *)((const char *)base + (size_t)(i * 4u));
+}
+__device__ __forceinline__ float load_in(const uint16_t *__restrict__ base, uint32_t i) {
+    const uint16_t v = *(const uint16_t *)((const char *)base + (size_t)(i * 2u));
+    return __uint_as_float(((uint32_t)v) << 16);
+}
+__device__ __forceinline__ void store_out(float *__restrict__ base, uint32_t i, float v) {
+    *(float *)((char *)base + (size_t)(i * 4u)) = v;
 }
 
 template <int CTRL>
@@ -56,92 +65,186 @@ __device__ __forceinline__ float group_sum(float v) {
     return v;
 }
 
+constexpr float kLog2eHi = 1.44269502162933349609375f;  // log2(e) rounded to f32
+constexpr float kLog2eLo = 1.925963033500011079e-08f;   // log2(e) - kLog2eHi
+constexpr float kLn2 = 0.693147180559945309f;
+
+// e^v for v <= 0 within ~2 ulp: v*log2(e) = p + lo exactly to f32 working
+// precision (an fma recovers the rounding error of p), 2^p from the
+// hardware exponential, and 2^lo ~ 1 + lo*ln2 applied as a correction.
+__device__ __forceinline__ float exp_nonpos(float v) {
+    const float p = v * kLog2eHi;
+    const float lo = fmaf(v, kLog2eHi, -p) + v * kLog2eLo;
+    const float e = __builtin_amdgcn_exp2f(p);
+    return fmaf(e, lo * kLn2, e);
+}
+
 // Step size and its sensitivity factor for one (t, d):
-//   Delta = softplus(z), z = x*w + b;  dDelta = sigmoid(z)*w*dx = sw*dx.
+//   Delta = softplus(z) = max(z, 0) + log1p(e),  e = exp(-|z|),  z = x*w + b
+//   dDelta = sigmoid(z) * w * dx = sw * dx.
+// log1p(e) for e in (0, 1] is 2 atanh(s) with s = e/(2+e) <= 1/3, summed as
+// 2s(1 + s^2/3 + ... + s^12/13): the first omitted term is below 2e-8
+// relative, and no 1+e is ever rounded, so small steps keep full precision.
 __device__ __forceinline__ void discretize(float xv, float w, float bd, float &delta, float &sw) {
     const float z = fmaf(xv, w, bd);
-    const float e = expf(-fabsf(z));
-    delta = fmaxf(z, 0.0f) + log1pf(e);
+    const float e = exp_nonpos(-fabsf(z));
+    const float sv = e * __builtin_amdgcn_rcpf(2.0f + e);
+    const float q = sv * sv;
+    float poly = fmaf(q, 1.0f / 13.0f, 1.0f / 11.0f);
+    poly = fmaf(q, poly, 1.0f / 9.0f);
+    poly = fmaf(q, poly, 1.0f / 7.0f);
+    poly = fmaf(q, poly, 1.0f / 5.0f);
+    poly = fmaf(q, poly, 1.0f / 3.0f);
+    poly = fmaf(q, poly, 1.0f);
+    delta = fmaxf(z, 0.0f) + 2.0f * sv * poly;
     const float r = __builtin_amdgcn_rcpf(1.0f + e);
-    const float sig = z >= 0.0f ? r : e * r;
-    sw = sig * w;
+    sw = (z >= 0.0f ? r : e * r) * w;
 }
 
 // ---------------------------------------------------------------- k_proj
 // rec[b][t-t0] = [B(N) | dB_0..dB_{K-1} (N each) | C(N) | dC_0..dC_{K-1}]
 // Row source s = blockIdx.y: 0 -> x (bias added), 1+k -> dx_k.
-// Each output is one thread's sum over d in ascending order.
-template <int NC, int CT, int RT, typename InT>
+// out[row][j] = sum_d X[row][d] * W[d][j], W = [W_B | W_C], on the matrix
+// cores: v_mfma_f32_16x16x4f32 computes D(16x16) += A(16x4) B(4x16) with,
+// for lane l, A[l%16][l/16], B[l/16][l%16] and D[4(l/16)+r][l%16] in
+// accumulator r.  Each wave owns 16 rows and every column; the channel
+// order of the sum is fixed (ascending blocks of 4), whatever the block of
+// rows, so outputs do not depend on how the sequence is tiled.
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// Loads 4 consecutive input values of one row (zero past D) as f32.
+template <typename InT>
+__device__ __forceinline__ floatx4 load4(const InT *__restrict__ row, int64_t d, int64_t D);
+template <>
+__device__ __forceinline__ floatx4 load4<float>(const float *__restrict__ row, int64_t d, int64_t D) {
+    if (d + 4 <= D && ((D & 3) == 0)) return *(const floatx4 *)(row + d);
+    floatx4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = d + i < D ? row[d + i] : 0.0f;
+    return v;
+}
+template <>
+__device__ __forceinline__ floatx4 load4<uint16_t>(const uint16_t *__restrict__ row, int64_t d, int64_t D) {
+    floatx4 v;
+    if (d + 4 <= D && ((D & 3) == 0)) {
+        const uint2 u = *(const uint2 *)(row + d);
+        v[0] = __uint_as_float(u.x << 16);
+        v[1] = __uint_as_float(u.x & 0xffff0000u);
+        v[2] = __uint_as_float(u.y << 16);
+        v[3] = __uint_as_float(u.y & 0xffff0000u);
+        return v;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = d + i < D ? __uint_as_float(((uint32_t)row[d + i]) << 16) : 0.0f;
+    return v;
+}
+
+template <int NC, typename InT>
 __global__ __launch_bounds__(kThreads) void k_proj(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ WB,
     const float *__restrict__ WC, const float *__restrict__ bB, const float *__restrict__ bC,
     float *__restrict__ bc, int64_t Bsz, int64_t L, int64_t D, int K, int64_t t0, int64_t len, int64_t Tc) {
     constexpr int N = NC / 2;
-    constexpr int CG = NC / CT;
-    constexpr int RG = kThreads / CG;
-    constexpr int TM = RG * RT;
-    constexpr int DT = 32;
-    __shared__ float Xs[TM][DT + 1];
-    __shared__ float Ws[DT][NC];
+    constexpr int CT = (NC + 15) / 16;  // 16-column tiles (zero-padded)
+    constexpr int NCP = CT * 16;
+    constexpr int RT = 2;               // 16-row tiles per wave
+    constexpr int TM = 4 * 16 * RT;     // rows per block
+    constexpr int DT = 32;              // channels per stage
+    constexpr int XP = DT + 4;          // padded LDS row pitch
+    constexpr int XV = TM * DT / 4 / kThreads;   // float4 of X per thread per stage
+    constexpr int WE = (DT * NCP + kThreads - 1) / kThreads;
+    __shared__ float Xs[2][TM][XP];
+    __shared__ float Ws[2][DT][NCP + 4];
 
     const int tid = threadIdx.x;
-    const int cg = tid % CG, rg = tid / CG;
+    const int wave = tid / 64, lane = tid % 64;
     const int s = blockIdx.y;
     const int64_t b = blockIdx.z;
     const int64_t r0 = (int64_t)blockIdx.x * TM;  // chunk-relative first row
     const InT *src = s == 0 ? x + (b * L + t0) * D : dx + (((int64_t)(s - 1) * Bsz + b) * L + t0) * D;
 
-    float acc[RT][CT];
+    floatx4 xr[XV];
+    float wr[WE];
+    auto fetch = [&](int64_t d0) {
 #pragma unroll
-    for (int i = 0; i < RT; ++i)
-#pragma unroll
-        for (int j = 0; j < CT; ++j) acc[i][j] = 0.0f;
-
-    for (int64_t d0 = 0; d0 < D; d0 += DT) {
-        // X tile: TM rows x DT channels (zero outside the block / past D).
-        for (int e = tid; e < TM * DT; e += kThreads) {
-            const int r = e / DT, dd = e % DT;
-            const int64_t row = r0 + r, d = d0 + dd;
-            Xs[r][dd] = (row < len && d < D) ? load_in(src, row * D + d) : 0.0f;
+        for (int i = 0; i < XV; ++i) {
+            const int e = tid + i * kThreads;          // float4 index in the tile
+            const int r = e / (DT / 4), c4 = e % (DT / 4);
+            const int64_t row = r0 + r;
+            xr[i] = row < len ? load4<InT>(src + row * D, d0 + 4 * c4, D) : floatx4{0.0f, 0.0f, 0.0f, 0.0f};
         }
-        for (int e = tid; e < DT * NC; e += kThreads) {
-            const int dd = e / NC, j = e % NC;
+#pragma unroll
+        for (int i = 0; i < WE; ++i) {
+            const int e = tid + i * kThreads;
+            const int dd = e / NCP, j = e % NCP;
             const int64_t d = d0 + dd;
             float v = 0.0f;
-            if (d < D) v = j < N ? WB[d * N + j] : WC[d * N + (j - N)];
-            Ws[dd][j] = v;
+            if (e < DT * NCP && d < D && j < NC) v = j < N ? WB[d * N + j] : WC[d * N + (j - N)];
+            wr[i] = v;
         }
-        __syncthreads();
-#pragma unroll 8
-        for (int dd = 0; dd < DT; ++dd) {
-            float xv[RT], wv[CT];
+    };
+    auto stash = [&](int buf) {
 #pragma unroll
-            for (int i = 0; i < RT; ++i) xv[i] = Xs[rg * RT + i][dd];
-#pragma unroll
-            for (int j = 0; j < CT; ++j) wv[j] = Ws[dd][cg * CT + j];
-#pragma unroll
-            for (int i = 0; i < RT; ++i)
-#pragma unroll
-                for (int j = 0; j < CT; ++j) acc[i][j] = fmaf(xv[i], wv[j], acc[i][j]);
+        for (int i = 0; i < XV; ++i) {
+            const int e = tid + i * kThreads;
+            const int r = e / (DT / 4), c4 = e % (DT / 4);
+            *(floatx4 *)&Xs[buf][r][4 * c4] = xr[i];
         }
+#pragma unroll
+        for (int i = 0; i < WE; ++i) {
+            const int e = tid + i * kThreads;
+            if (e < DT * NCP) Ws[buf][e / NCP][e % NCP] = wr[i];
+        }
+    };
+
+    floatx4 acc[RT][CT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int c = 0; c < CT; ++c) acc[rt][c] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    const int64_t nst = (D + DT - 1) / DT;
+    fetch(0);
+    stash(0);
+    __syncthreads();
+    for (int64_t st = 0; st < nst; ++st) {
+        const int buf = (int)(st & 1);
+        if (st + 1 < nst) fetch((st + 1) * DT);
+#pragma unroll
+        for (int kk = 0; kk < DT / 4; ++kk) {
+            float bv[CT];
+#pragma unroll
+            for (int c = 0; c < CT; ++c) bv[c] = Ws[buf][kk * 4 + lane / 16][c * 16 + lane % 16];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                const float a = Xs[buf][wave * 16 * RT + rt * 16 + lane % 16][kk * 4 + lane / 16];
+#pragma unroll
+                for (int c = 0; c < CT; ++c)
+                    acc[rt][c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[c], acc[rt][c], 0, 0, 0);
+            }
+        }
+        if (st + 1 < nst) stash(buf ^ 1);
         __syncthreads();
     }
     const int R = 2 * N * (1 + K);
 #pragma unroll
-    for (int i = 0; i < RT; ++i) {
-        const int64_t row = r0 + rg * RT + i;
-        if (row >= len) continue;
-        float *out = bc + (b * Tc + row) * R;
+    for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
-        for (int j = 0; j < CT; ++j) {
-            const int c = cg * CT + j;
-            float v = acc[i][j];
-            if (c < N) {
-                if (s == 0 && bB) v += bB[c];
-                out[s * N + c] = v;
-            } else {
-                if (s == 0 && bC) v += bC[c - N];
-                out[(1 + K) * N + s * N + (c - N)] = v;
+        for (int c = 0; c < CT; ++c) {
+            const int col = c * 16 + lane % 16;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int64_t row = r0 + wave * 16 * RT + rt * 16 + 4 * (lane / 16) + r;
+                if (row >= len || col >= NC) continue;
+                float *out = bc + (b * Tc + row) * R;
+                float v = acc[rt][c][r];
+                if (col < N) {
+                    if (s == 0 && bB) v += bB[col];
+                    out[s * N + col] = v;
+                } else {
+                    if (s == 0 && bC) v += bC[col - N];
+                    out[(1 + K) * N + s * N + (col - N)] = v;
+                }
             }
         }
     }
@@ -207,20 +310,23 @@ __global__ __launch_bounds__(kThreads) void k_scan(
 #pragma unroll
     for (int k = 0; k < K; ++k) sdD[k] = 0.0f;
 
-    const InT *X = x + (b * L + t0) * D + d;
+    // Wave-uniform bases of this block of steps; per-lane offsets t*D + d
+    // stay below 2^30 elements (checked by the planner).
     const int64_t dxs = Bsz * L * D;  // stride between directions
-    const InT *DX = dx + (b * L + t0) * D + d;
-    float *Y = y + (b * L + t0) * D + d;
-    float *DY = dy + (b * L + t0) * D + d;
+    const InT *Xb = x + (b * L + t0) * D;
+    const InT *DXb = dx + (b * L + t0) * D;
+    float *Yb = y + (b * L + t0) * D;
+    float *DYb = dy + (b * L + t0) * D;
+    const uint32_t Du = (uint32_t)D, du = (uint32_t)d;
     const float *rec0 = bc + b * Tc * R;
 
     float xc[TT], dxc[K][TT];
 #pragma unroll
     for (int j = 0; j < TT; ++j) {
         const int64_t t = ts + j < te ? ts + j : te - 1;
-        xc[j] = load_in(X, t * D);
+        xc[j] = load_in(Xb, (uint32_t)t * Du + du);
 #pragma unroll
-        for (int k = 0; k < K; ++k) dxc[k][j] = load_in(DX, k * dxs + t * D);
+        for (int k = 0; k < K; ++k) dxc[k][j] = load_in(DXb + k * dxs, (uint32_t)t * Du + du);
     }
 
     for (int64_t tb = ts; tb < te; tb += TT) {
@@ -228,9 +334,9 @@ __global__ __launch_bounds__(kThreads) void k_scan(
 #pragma unroll
         for (int j = 0; j < TT; ++j) {
             const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
-            xn[j] = load_in(X, t * D);
+            xn[j] = load_in(Xb, (uint32_t)t * Du + du);
 #pragma unroll
-            for (int k = 0; k < K; ++k) dxn[k][j] = load_in(DX, k * dxs + t * D);
+            for (int k = 0; k < K; ++k) dxn[k][j] = load_in(DXb + k * dxs, (uint32_t)t * Du + du);
         }
 #pragma unroll
         for (int j = 0; j < TT; ++j) {
@@ -284,9 +390,9 @@ __global__ __launch_bounds__(kThreads) void k_scan(
 #pragma unroll
                     for (int k = 0; k < K; ++k) dyv[k] = group_sum<NS>(dyv[k]);
                     if (active && ns == 0) {
-                        Y[t * D] = yv;
+                        store_out(Yb, (uint32_t)t * Du + du, yv);
 #pragma unroll
-                        for (int k = 0; k < K; ++k) DY[k * dxs + t * D] = dyv[k];
+                        for (int k = 0; k < K; ++k) store_out(DYb + k * dxs, (uint32_t)t * Du + du, dyv[k]);
                     }
                 }
             }
@@ -328,13 +434,255 @@ __global__ __launch_bounds__(kThreads) void k_scan(
     }
 }
 
+// ---------------------------------------------------------------- k_scan_sh
+// The same scan for NS >= 2 threads per channel.  Per tile of TT steps the
+// block stages in LDS (double-buffered through registers, so the global
+// loads of tile i+1 overlap the arithmetic of tile i):
+//   s_rec  the TT step records (B, dB_k, C, dC_k), read by every channel;
+//   s_sc   per (t, d): Delta, u = Delta*x, dDelta_k, p_k = dDelta_k*x +
+//          Delta*dx_k, each computed once per channel instead of once per
+//          thread sharing it.
+template <int NT, int NS, int K, bool OUT, typename InT>
+__global__ __launch_bounds__(kThreads) void k_scan_sh(
+    const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A,
+    const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
+    const float *__restrict__ init, int64_t ibs, int64_t igs, int64_t ics,
+    float *__restrict__ y, float *__restrict__ dy, float *__restrict__ end_state,
+    float *__restrict__ agg_h, float *__restrict__ agg_s,
+    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    static_assert(NS >= 2, "one thread per channel uses k_scan");
+    constexpr int N = NT * NS;
+    constexpr int R = 2 * N * (1 + K);
+    constexpr int DPB = kThreads / NS;       // channels per block
+    constexpr int TT = 8;                    // steps per tile
+    constexpr int SCW = 2 + 2 * K;           // Delta, u, dDelta_k, p_k
+    constexpr int SCP = SCW | 1;             // odd pitch against bank conflicts
+    constexpr int RV = (TT * R + kThreads - 1) / kThreads;       // record floats per thread
+    constexpr int TQ = (TT * DPB + kThreads - 1) / kThreads;     // (t, d) tasks per thread
+    __shared__ float s_rec[TT * R];
+    __shared__ float s_sc[TT][DPB][SCP];
+
+    const int tid = threadIdx.x;
+    const int ns = tid % NS;
+    const int dl = tid / NS;
+    const int64_t d0 = (int64_t)blockIdx.x * DPB;
+    const bool active = d0 + dl < D;
+    const int64_t d = active ? d0 + dl : D - 1;
+    const int g = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int64_t ts = (int64_t)g * S;
+    const int64_t te = ts + S < len ? ts + S : len;
+    if (ts >= te) return;
+
+    float Af[NT], At[NT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+        Af[i] = A[d * N + ns * NT + i];
+        At[i] = Af[i] * kLog2e;
+    }
+    float h[NT], dh[K][NT];
+    if constexpr (OUT) {
+        const float *ib = init + b * ibs + g * igs + d;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            const int n = ns * NT + i;
+            h[i] = ib[n * D];
+#pragma unroll
+            for (int k = 0; k < K; ++k) dh[k][i] = ib[(1 + k) * ics + n * D];
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            h[i] = 0.0f;
+#pragma unroll
+            for (int k = 0; k < K; ++k) dh[k][i] = 0.0f;
+        }
+    }
+    float sD = 0.0f, sdD[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) sdD[k] = 0.0f;
+
+    const int64_t dxs = Bsz * L * D;
+    const InT *Xb = x + (b * L + t0) * D;
+    const InT *DXb = dx + (b * L + t0) * D;
+    float *Yb = y + (b * L + t0) * D;
+    float *DYb = dy + (b * L + t0) * D;
+    const uint32_t Du = (uint32_t)D;
+    const float *rec0 = bc + b * Tc * R;
+
+    // Registers holding the next tile while the current one is computed.
+    // Thread tid always owns the same tasks (channel d0 + j of step slot tt).
+    float rr[RV];
+    float xq[TQ], dxq[TQ][K], wq[TQ], bq[TQ];
+#pragma unroll
+    for (int i = 0; i < TQ; ++i) {
+        const int j = (tid + i * kThreads) % DPB;
+        const int64_t dj = d0 + j < D ? d0 + j : D - 1;
+        wq[i] = w_delta[dj];
+        bq[i] = b_delta[dj];
+    }
+    auto fetch = [&](int64_t tb) {
+        const int64_t nrow = te - tb < TT ? te - tb : TT;
+#pragma unroll
+        for (int i = 0; i < RV; ++i) {
+            const int e = tid + i * kThreads;
+            rr[i] = (e < TT * R && e / R < nrow) ? rec0[tb * R + e] : 0.0f;
+        }
+#pragma unroll
+        for (int i = 0; i < TQ; ++i) {
+            const int qi = tid + i * kThreads;
+            const int tt = qi / DPB, j = qi % DPB;
+            const bool ok = qi < TT * DPB && tt < nrow && d0 + j < D;
+            const uint32_t o = ok ? (uint32_t)(tb + tt) * Du + (uint32_t)(d0 + j) : 0u;
+            xq[i] = ok ? load_in(Xb, o) : 0.0f;
+#pragma unroll
+            for (int k = 0; k < K; ++k) dxq[i][k] = ok ? load_in(DXb + k * dxs, o) : 0.0f;
+        }
+    };
+    auto stash = [&]() {
+#pragma unroll
+        for (int i = 0; i < RV; ++i) {
+            const int e = tid + i * kThreads;
+            if (e < TT * R) s_rec[e] = rr[i];
+        }
+#pragma unroll
+        for (int i = 0; i < TQ; ++i) {
+            const int qi = tid + i * kThreads;
+            if (qi >= TT * DPB) break;
+            const int tt = qi / DPB, j = qi % DPB;
+            float delta, sw;
+            discretize(xq[i], wq[i], bq[i], delta, sw);
+            float *o = &s_sc[tt][j][0];
+            o[0] = delta;
+            o[1] = delta * xq[i];
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const float ddl = sw * dxq[i][k];
+                o[2 + k] = ddl;
+                o[2 + K + k] = fmaf(ddl, xq[i], delta * dxq[i][k]);
+            }
+        }
+    };
+
+    fetch(ts);
+    stash();
+    __syncthreads();
+    for (int64_t tb = ts; tb < te; tb += TT) {
+        const bool more = tb + TT < te;
+        if (more) fetch(tb + TT);
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt) {
+            const int64_t t = tb + tt;
+            if (t >= te) break;
+            const float *sc = &s_sc[tt][dl][0];
+            const float delta = sc[0], u = sc[1];
+            float dD[K], pk[K];
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                dD[k] = sc[2 + k];
+                pk[k] = sc[2 + K + k];
+            }
+            if constexpr (!OUT) {
+                sD += delta;
+#pragma unroll
+                for (int k = 0; k < K; ++k) sdD[k] += dD[k];
+            }
+            const float *rec = s_rec + tt * R;
+            float yv = 0.0f, dyv[K];
+#pragma unroll
+            for (int k = 0; k < K; ++k) dyv[k] = 0.0f;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                const int n = ns * NT + i;
+                const float Bn = rec[n];
+                const float a = __builtin_amdgcn_exp2f(delta * At[i]);
+                const float sv = a * h[i];
+                const float gv = Af[i] * sv;
+                const float hn = fmaf(Bn, u, sv);
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    const float dBn = rec[(1 + k) * N + n];
+                    dh[k][i] = fmaf(a, dh[k][i], fmaf(gv, dD[k], fmaf(Bn, pk[k], dBn * u)));
+                }
+                h[i] = hn;
+                if constexpr (OUT) {
+                    const float Cn = rec[(1 + K) * N + n];
+                    yv = fmaf(Cn, hn, yv);
+#pragma unroll
+                    for (int k = 0; k < K; ++k) {
+                        const float dCn = rec[(2 + K + k) * N + n];
+                        dyv[k] = fmaf(dCn, hn, fmaf(Cn, dh[k][i], dyv[k]));
+                    }
+                }
+            }
+            if constexpr (OUT) {
+                yv = group_sum<NS>(yv);
+#pragma unroll
+                for (int k = 0; k < K; ++k) dyv[k] = group_sum<NS>(dyv[k]);
+                if (active) {
+                    const uint32_t o = (uint32_t)t * Du + (uint32_t)d;
+                    // the NS lanes of a channel share its K+1 stores
+                    if (ns == 0) store_out(Yb, o, yv);
+#pragma unroll
+                    for (int k = 0; k < K; ++k)
+                        if (ns == (1 + k) % NS) store_out(DYb + k * dxs, o, dyv[k]);
+                }
+            }
+        }
+        __syncthreads();
+        if (more) {
+            stash();
+            __syncthreads();
+        }
+    }
+
+    if (!active) return;
+    if constexpr (OUT) {
+        if (end_state) {
+            float *eb = end_state + b * ibs + d;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                const int n = ns * NT + i;
+                eb[n * D] = h[i];
+#pragma unroll
+                for (int k = 0; k < K; ++k) eb[(1 + k) * ics + n * D] = dh[k][i];
+            }
+        }
+    } else {
+        const int64_t base = (b * G + g) * (1 + K);
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            const int n = ns * NT + i;
+            agg_h[(base * N + n) * D + d] = h[i];
+#pragma unroll
+            for (int k = 0; k < K; ++k) agg_h[((base + 1 + k) * N + n) * D + d] = dh[k][i];
+        }
+        if (ns == 0) {
+            agg_s[base * D + d] = sD;
+#pragma unroll
+            for (int k = 0; k < K; ++k) agg_s[(base + 1 + k) * D + d] = sdD[k];
+        }
+    }
+}
+
+// Kernel for a tiling: one thread per channel, or several sharing one.
+template <int NT, int NS, int K, bool OUT, typename InT>
+constexpr auto scan_kernel() {
+    if constexpr (NS == 1) return &k_scan<NT, NS, K, OUT, InT>;
+    else return &k_scan_sh<NT, NS, K, OUT, InT>;
+}
+
 // ---------------------------------------------------------------- k_carry
-// One thread per lane (b, n, d).  state [(1+K)][B][N][D] enters the block
-// and leaves it; seg_in receives the state entering each segment.
+// One thread per lane (b, n, d), sequential over the block's segments.
+// state [(1+K)][B][N][D] enters the block and leaves it.  seg [B][G][(1+K)]
+// [N][D] holds each segment's end state from a zero start on entry and is
+// overwritten, segment by segment, with the true state entering it.  Loads
+// for GB segments are issued together so their latencies overlap.
 template <int K>
 __global__ __launch_bounds__(kThreads) void k_carry(
-    const float *__restrict__ A, const float *__restrict__ agg_h, const float *__restrict__ agg_s,
-    float *__restrict__ state, float *__restrict__ seg_in, int64_t Bsz, int64_t D, int64_t N, int G) {
+    const float *__restrict__ A, float *__restrict__ seg, const float *__restrict__ agg_s,
+    float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int G) {
+    constexpr int GB = K == 1 ? 32 : (K == 2 ? 16 : (K == 4 ? 8 : 4));
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int64_t ND = N * D;
     if (idx >= Bsz * ND) return;
@@ -342,26 +690,44 @@ __global__ __launch_bounds__(kThreads) void k_carry(
     const float a = A[d * N + n];
     const float at = a * kLog2e;
     const int64_t cstride = Bsz * ND;  // state: component stride
-    float h = state[b * ND + n * D + d];
+    const int64_t lane = n * D + d;
+    float h = state[b * ND + lane];
     float dh[K];
 #pragma unroll
-    for (int k = 0; k < K; ++k) dh[k] = state[(1 + k) * cstride + b * ND + n * D + d];
-    for (int g = 0; g < G; ++g) {
-        const int64_t base = (b * G + g) * (1 + K);
-        seg_in[base * ND + n * D + d] = h;
+    for (int k = 0; k < K; ++k) dh[k] = state[(1 + k) * cstride + b * ND + lane];
+    for (int g0 = 0; g0 < G; g0 += GB) {
+        float h0[GB], dh0[GB][K], sD[GB], sdD[GB][K];
 #pragma unroll
-        for (int k = 0; k < K; ++k) seg_in[(base + 1 + k) * ND + n * D + d] = dh[k];
-        const float P = __builtin_amdgcn_exp2f(at * agg_s[base * D + d]);
+        for (int j = 0; j < GB; ++j) {
+            const int g = g0 + j < G ? g0 + j : G - 1;
+            const int64_t base = (b * G + g) * (1 + K);
+            h0[j] = seg[base * ND + lane];
+            sD[j] = agg_s[base * D + d];
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-            const float q = P * (a * agg_s[(base + 1 + k) * D + d]);
-            dh[k] = fmaf(P, dh[k], fmaf(q, h, agg_h[(base + 1 + k) * ND + n * D + d]));
+            for (int k = 0; k < K; ++k) {
+                dh0[j][k] = seg[(base + 1 + k) * ND + lane];
+                sdD[j][k] = agg_s[(base + 1 + k) * D + d];
+            }
         }
-        h = fmaf(P, h, agg_h[base * ND + n * D + d]);
-    }
-    state[b * ND + n * D + d] = h;
 #pragma unroll
-    for (int k = 0; k < K; ++k) state[(1 + k) * cstride + b * ND + n * D + d] = dh[k];
+        for (int j = 0; j < GB; ++j) {
+            if (g0 + j >= G) break;
+            const int64_t base = (b * G + g0 + j) * (1 + K);
+            seg[base * ND + lane] = h;
+#pragma unroll
+            for (int k = 0; k < K; ++k) seg[(base + 1 + k) * ND + lane] = dh[k];
+            const float P = __builtin_amdgcn_exp2f(at * sD[j]);
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const float q = P * (a * sdD[j][k]);
+                dh[k] = fmaf(P, dh[k], fmaf(q, h, dh0[j][k]));
+            }
+            h = fmaf(P, h, h0[j]);
+        }
+    }
+    state[b * ND + lane] = h;
+#pragma unroll
+    for (int k = 0; k < K; ++k) state[(1 + k) * cstride + b * ND + lane] = dh[k];
 }
 
 // ---------------------------------------------------------------- state in/out
@@ -455,18 +821,15 @@ struct Launcher {
     float *bcw() const { return (float *)(ws + q.ws.bc); }
     float *agg_h() const { return (float *)(ws + q.ws.agg_h); }
     float *agg_s() const { return (float *)(ws + q.ws.agg_s); }
-    float *seg_in() const { return (float *)(ws + q.ws.seg_in); }
+    float *seg_in() const { return (float *)(ws + q.ws.agg_h); }  // overwritten in place by k_carry
 
     template <int NC>
     void proj_nc(int64_t t0, int64_t len) {
-        constexpr int CT = NC >= 64 ? 8 : 4;
-        constexpr int CG = NC / CT;
-        constexpr int RT = (NC >= 32) ? (NC >= 128 ? 4 : 2) : 1;
-        constexpr int TM = (kThreads / CG) * RT;
+        constexpr int TM = 128;
         dim3 grid((unsigned)((len + TM - 1) / TM), (unsigned)(1 + q.K), (unsigned)q.B);
         Timed tm(0, st);
-        hipLaunchKernelGGL((k_proj<NC, CT, RT, InT>), grid, dim3(kThreads), 0, st, x, dx, p.W_B, p.W_C, p.b_B,
-                           p.b_C, bcw(), q.B, q.L, q.D, (int)q.K, t0, len, q.chunk_len);
+        hipLaunchKernelGGL((k_proj<NC, InT>), grid, dim3(kThreads), 0, st, x, dx, p.W_B, p.W_C, p.b_B, p.b_C,
+                           bcw(), q.B, q.L, q.D, (int)q.K, t0, len, q.chunk_len);
     }
 
     void proj(int64_t t0, int64_t len) {
@@ -486,7 +849,7 @@ struct Launcher {
         if (q.seg == 0) {
             // Sequential evaluation: one segment per block, state in place.
             Timed tm(3, st);
-            hipLaunchKernelGGL((k_scan<NT, NS, K, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x,
+            hipLaunchKernelGGL((scan_kernel<NT, NS, K, true, InT>()), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x,
                                dx, p.A, p.w_delta, p.b_delta, bcw(), state(), ND, (int64_t)0, q.B * ND, y, dy,
                                state(), (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len,
                                len, 1);
@@ -495,7 +858,7 @@ struct Launcher {
         const int G = (int)((len + q.seg - 1) / q.seg);
         {
             Timed tm(1, st);
-            hipLaunchKernelGGL((k_scan<NT, NS, K, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B),
+            hipLaunchKernelGGL((scan_kernel<NT, NS, K, false, InT>()), dim3(gx, (unsigned)G, (unsigned)q.B),
                                dim3(kThreads), 0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(),
                                (const float *)nullptr, (int64_t)0, (int64_t)0, (int64_t)0, y, dy, (float *)nullptr,
                                agg_h(), agg_s(), q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
@@ -504,11 +867,11 @@ struct Launcher {
             const int64_t lanes = q.B * ND;
             Timed tm(2, st);
             hipLaunchKernelGGL((k_carry<K>), dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0,
-                               st, p.A, agg_h(), agg_s(), state(), seg_in(), q.B, q.D, q.N, G);
+                               st, p.A, agg_h(), agg_s(), state(), q.B, q.D, q.N, G);
         }
         {
             Timed tm(3, st);
-            hipLaunchKernelGGL((k_scan<NT, NS, K, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads),
+            hipLaunchKernelGGL((scan_kernel<NT, NS, K, true, InT>()), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads),
                                0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(), seg_in(), (int64_t)G * (1 + K) * ND,
                                (int64_t)(1 + K) * ND, ND, y, dy, (float *)nullptr, (float *)nullptr,
                                (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);

@@ -14,7 +14,16 @@ import torch
 
 from oracle import oracle
 
-torch.set_default_dtype(torch.float64)
+
+
+@pytest.fixture(autouse=True)
+def _float64_default():
+    """Tensors built from Python scalars in this module are fp64; the
+    default is restored so other test modules are unaffected."""
+    old = torch.get_default_dtype()
+    torch.set_default_dtype(torch.float64)
+    yield
+    torch.set_default_dtype(old)
 
 
 def rand_problem(seed, B=1, L=10, D=3, N=4, K=2, stiff=False, bias=False, zscale=1.0):
