@@ -30,6 +30,12 @@ def parse():
     ap.add_argument("--workload", default="pulse128k")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline leg")
     ap.add_argument("--cpu-steps", type=int, default=0, help="oracle sample length (0 = auto)")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="after the timed steps, copy 1 GiB device-to-device once (counter calibration)")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="condense two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; made with "
+                         "--calib-copy) into profiles/traffic_<workload>.json and exit")
+    ap.add_argument("--traffic-out", default=None, help="output path of --summarize-counters")
     ap.add_argument("--seg-len", type=int, default=0, help="tiling override (0 = library default)")
     ap.add_argument("--chunk-segs", type=int, default=0, help="tiling override (0 = library default)")
     return ap.parse_args()
@@ -43,8 +49,92 @@ def scan_flops_per_lane_step(K):
     return 7 + 11 * K
 
 
+COPY_BYTES = 1 << 30
+KERNEL_KIND = {"k_proj": "proj", "k_scan<": None, "k_carry": "carry", "k_state": "state_io"}
+TRAFFIC_SOURCES = ("paper_2512_23068_amd/csrc/pgf_scan.hip", "paper_2512_23068_amd/csrc/pgf_plan.cpp")
+
+
+def source_digest():
+    """Digest of the kernel and planner sources the counters were taken on."""
+    import hashlib
+    h = hashlib.sha256()
+    for rel in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def _kernel_label(name):
+    base = name.split("(")[0].replace("void ", "").strip()
+    if "k_scan" in base:
+        # template args <NT, NS, K, OUT, InT>: OUT=true is the scan with outputs
+        return "scan_out" if ", true," in base else "seg_aggregate"
+    for key, lab in KERNEL_KIND.items():
+        if key in base and lab:
+            return lab
+    return "copy" if "copyBuffer" in base else base
+
+
+def summarize_counters(workload, fetch_csv, write_csv, out_path=None):
+    import csv
+    import statistics
+    per = {}
+    calib = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            lab = _kernel_label(r["Kernel_Name"])
+            v = float(r["Counter_Value"])
+            if lab == "copy":
+                if v > calib.get(counter, 0.0):
+                    calib[counter] = v        # the 1 GiB copy is the largest copy dispatch
+                continue
+            per.setdefault(lab, {}).setdefault(counter, []).append(v)
+    out = {"workload": workload, "source_sha256": source_digest(),
+           "calibration": {"copy_bytes": COPY_BYTES, "FETCH_SIZE_KiB": calib.get("FETCH_SIZE"),
+                           "WRITE_SIZE_KiB": calib.get("WRITE_SIZE"),
+                           "fetch_factor": calib.get("FETCH_SIZE", 0) * 1024 / COPY_BYTES,
+                           "write_factor": calib.get("WRITE_SIZE", 0) * 1024 / COPY_BYTES},
+           "kernels": {}}
+    for lab, c in per.items():
+        f = statistics.mean(c.get("FETCH_SIZE", [0.0]))
+        w = statistics.mean(c.get("WRITE_SIZE", [0.0]))
+        ff = out["calibration"]["fetch_factor"] or 1.0
+        wf = out["calibration"]["write_factor"] or 1.0
+        out["kernels"][lab] = {"FETCH_SIZE_KiB_per_dispatch": round(f, 1), "WRITE_SIZE_KiB_per_dispatch": round(w, 1),
+                               "dispatches": len(c.get("FETCH_SIZE", [])),
+                               "hbm_bytes_per_dispatch": int(f * 1024 / ff + w * 1024 / wf)}
+    out["commands"] = [
+        f"rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pmc_{workload}_{c} -o pmc -- "
+        f"python3 -u bench.py --workload {workload} --steps 2 --warmup 1 --no-cpu --calib-copy"
+        for c in ("FETCH_SIZE", "WRITE_SIZE")]
+    path = out_path or os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(path)
+
+
+def committed_traffic(workload, kind):
+    """HBM bytes per dispatch of `kind` from the committed counter summary,
+    or None when it is missing or was taken on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    try:
+        with open(path) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha256") != source_digest():
+        return None
+    k = t.get("kernels", {}).get(kind)
+    return None if k is None else k["hbm_bytes_per_dispatch"]
+
+
 def main():
     args = parse()
+    if args.summarize_counters:
+        summarize_counters(args.workload, *args.summarize_counters, out_path=args.traffic_out)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on one GPU only; --gpus must be 1", file=sys.stderr)
         sys.exit(2)
@@ -132,7 +222,7 @@ def main():
         "peak": FP32_VECTOR_PEAK_TFLOPS,
         "unit": "TFLOP/s",
         "frac": round(tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
-        "traffic": None,
+        "traffic": committed_traffic(cfg.name, "scan_out"),
         "hbm_achieved_gbs": round(hbm_gbs, 1),
         "hbm_frac": round(hbm_gbs / HBM_PEAK_GBS, 4),
         "avg_launch_ms": round(so_avg_ms, 5),
@@ -141,6 +231,18 @@ def main():
     }
     kernels = {k: {"ms_per_step": round(v[0] / args.steps, 4), "launches_per_step": v[1] / args.steps}
                for k, v in kern.items()}
+
+    if args.calib_copy:
+        # A plain copy of known size: what the HBM counters read for it
+        # calibrates FETCH_SIZE / WRITE_SIZE against true bytes.
+        del y, dy, ws
+        torch.cuda.empty_cache()
+        src = torch.ones(1 << 28, device=dev, dtype=torch.float32)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     cpu = None
     if not args.no_cpu:

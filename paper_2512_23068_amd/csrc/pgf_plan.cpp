@@ -62,7 +62,7 @@ int make_plan(const pgf_params *p, Plan *plan) {
     q.B = B; q.L = L; q.D = D; q.N = N; q.K = K;
     q.in_bf16 = p->in_dtype == PGF_BF16;
     // Registers per thread grow as nt*(3+K); keep them near 128.
-    q.nt = (int)std::min<int64_t>(N, K >= 4 ? 8 : 16);
+    q.nt = (int)std::min<int64_t>(N, K >= 8 ? 4 : (K >= 4 ? 8 : 16));
     q.ns = (int)(N / q.nt);
     q.R = (int)(2 * N * (1 + K));
 

@@ -457,10 +457,11 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
     constexpr int TT = 8;                    // steps per tile
     constexpr int SCW = 2 + 2 * K;           // Delta, u, dDelta_k, p_k
     constexpr int SCP = SCW | 1;             // odd pitch against bank conflicts
-    constexpr int RV = (TT * R + kThreads - 1) / kThreads;       // record floats per thread
+    constexpr int RV4 = (TT * R / 4 + kThreads - 1) / kThreads;  // record float4s per thread
     constexpr int TQ = (TT * DPB + kThreads - 1) / kThreads;     // (t, d) tasks per thread
-    __shared__ float s_rec[TT * R];
+    __shared__ floatx4 s_rec4[TT * R / 4];
     __shared__ float s_sc[TT][DPB][SCP];
+    const float *s_rec = (const float *)s_rec4;
 
     const int tid = threadIdx.x;
     const int ns = tid % NS;
@@ -512,38 +513,45 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
 
     // Registers holding the next tile while the current one is computed.
     // Thread tid always owns the same tasks (channel d0 + j of step slot tt).
-    float rr[RV];
+    // Indices past the tile or past D are clamped to valid ones (their
+    // values are never used), so the loads need no branches.
+    floatx4 rr[RV4];
     float xq[TQ], dxq[TQ][K], wq[TQ], bq[TQ];
+    int qt[TQ];          // step slot of task i
+    uint32_t qd[TQ];     // channel of task i
 #pragma unroll
     for (int i = 0; i < TQ; ++i) {
-        const int j = (tid + i * kThreads) % DPB;
+        const int qi = tid + i * kThreads;
+        const int j = qi % DPB;
         const int64_t dj = d0 + j < D ? d0 + j : D - 1;
         wq[i] = w_delta[dj];
         bq[i] = b_delta[dj];
+        qt[i] = qi / DPB;
+        qd[i] = (uint32_t)dj;
     }
     auto fetch = [&](int64_t tb) {
-        const int64_t nrow = te - tb < TT ? te - tb : TT;
+        const int nrow = (int)(te - tb < TT ? te - tb : TT);
+        const int lim4 = nrow * (R / 4) - 1;
+        const floatx4 *src4 = (const floatx4 *)(rec0 + tb * R);
 #pragma unroll
-        for (int i = 0; i < RV; ++i) {
-            const int e = tid + i * kThreads;
-            rr[i] = (e < TT * R && e / R < nrow) ? rec0[tb * R + e] : 0.0f;
+        for (int i = 0; i < RV4; ++i) {
+            const int e4 = tid + i * kThreads;
+            rr[i] = src4[e4 < lim4 ? e4 : lim4];
         }
 #pragma unroll
         for (int i = 0; i < TQ; ++i) {
-            const int qi = tid + i * kThreads;
-            const int tt = qi / DPB, j = qi % DPB;
-            const bool ok = qi < TT * DPB && tt < nrow && d0 + j < D;
-            const uint32_t o = ok ? (uint32_t)(tb + tt) * Du + (uint32_t)(d0 + j) : 0u;
-            xq[i] = ok ? load_in(Xb, o) : 0.0f;
+            const int tt = qt[i] < nrow ? qt[i] : nrow - 1;
+            const uint32_t o = (uint32_t)(tb + tt) * Du + qd[i];
+            xq[i] = load_in(Xb, o);
 #pragma unroll
-            for (int k = 0; k < K; ++k) dxq[i][k] = ok ? load_in(DXb + k * dxs, o) : 0.0f;
+            for (int k = 0; k < K; ++k) dxq[i][k] = load_in(DXb + k * dxs, o);
         }
     };
     auto stash = [&]() {
 #pragma unroll
-        for (int i = 0; i < RV; ++i) {
-            const int e = tid + i * kThreads;
-            if (e < TT * R) s_rec[e] = rr[i];
+        for (int i = 0; i < RV4; ++i) {
+            const int e4 = tid + i * kThreads;
+            if (e4 < TT * R / 4) s_rec4[e4] = rr[i];
         }
 #pragma unroll
         for (int i = 0; i < TQ; ++i) {
@@ -570,7 +578,9 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
     for (int64_t tb = ts; tb < te; tb += TT) {
         const bool more = tb + TT < te;
         if (more) fetch(tb + TT);
-#pragma unroll
+        // Not unrolled: keeps the scheduler from hoisting the LDS reads of
+        // later steps, which would multiply the live registers.
+#pragma unroll 1
         for (int tt = 0; tt < TT; ++tt) {
             const int64_t t = tb + tt;
             if (t >= te) break;
@@ -878,8 +888,8 @@ struct Launcher {
         }
     }
 
-    // Tilings the planner can choose: nt = min(N, 16) for K <= 2 and
-    // nt = min(N, 8) for K >= 4, ns = N / nt.
+    // Tilings the planner can choose: nt = min(N, 16) for K <= 2,
+    // nt = min(N, 8) for K = 4 and nt = min(N, 4) for K = 8; ns = N / nt.
     template <int K>
     bool scan_block_k(int64_t t0, int64_t len) {
         const int code = q.nt * 100 + q.ns;
@@ -892,13 +902,22 @@ struct Launcher {
                 case 1604: scans<16, 4, K>(t0, len); return true;
                 default: return false;
             }
-        } else {
+        } else if constexpr (K == 4) {
             switch (code) {
                 case 401: scans<4, 1, K>(t0, len); return true;
                 case 801: scans<8, 1, K>(t0, len); return true;
                 case 802: scans<8, 2, K>(t0, len); return true;
                 case 804: scans<8, 4, K>(t0, len); return true;
                 case 808: scans<8, 8, K>(t0, len); return true;
+                default: return false;
+            }
+        } else {
+            switch (code) {
+                case 401: scans<4, 1, K>(t0, len); return true;
+                case 402: scans<4, 2, K>(t0, len); return true;
+                case 404: scans<4, 4, K>(t0, len); return true;
+                case 408: scans<4, 8, K>(t0, len); return true;
+                case 416: scans<4, 16, K>(t0, len); return true;
                 default: return false;
             }
         }

@@ -61,12 +61,12 @@ def test_batch_slicing():
     assert torch.equal(yb, y[1:2]) and torch.equal(dyb, dy[:, 1:2])
 
 
-@pytest.mark.parametrize("K_small,K_big", [(1, 2), (4, 8)])
-def test_direction_independence(K_small, K_big):
-    """With the same tiling, direction k of a K-direction call equals a call
-    on dx_k alone (and y does not depend on K)."""
-    inp = gu.custom("multidir", batch=1, seqlen=700, d_inner=80, d_state=16, n_dirs=K_big)
-    pb, ps = binding.plan(1, 700, 80, 16, K_big), binding.plan(1, 700, 80, 16, K_small)
+@pytest.mark.parametrize("N,K_small,K_big", [(16, 1, 2), (4, 1, 8), (4, 2, 8), (4, 4, 8)])
+def test_direction_independence(N, K_small, K_big):
+    """With the same tiling, directions k0..k0+K_small-1 of a K_big-direction
+    call equal a call on those directions alone (and y does not depend on K)."""
+    inp = gu.custom("multidir", batch=1, seqlen=700, d_inner=80, d_state=N, n_dirs=K_big)
+    pb, ps = binding.plan(1, 700, 80, N, K_big), binding.plan(1, 700, 80, N, K_small)
     assert (pb["n_per_thread"], pb["n_split"]) == (ps["n_per_thread"], ps["n_split"])
     y, dy = gu.run(inp, seg_len=128, chunk_segs=8)
     for k0 in range(0, K_big, K_small):
