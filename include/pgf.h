@@ -43,6 +43,8 @@
  *     Argument checks are synchronous and happen before any launch; on a
  *     failed check nothing is launched and the outputs are untouched.
  *     Faults inside kernels surface at the caller's next synchronisation.
+ *   - Launches go to the device that is current on the calling thread; the
+ *     stream must belong to it.
  *   - The library keeps no state between calls (except the optional
  *     launch-timing record, see pgf_timing_*), and is reentrant on distinct
  *     workspaces.  Two calls in flight on the same workspace race.

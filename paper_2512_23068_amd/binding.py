@@ -171,7 +171,8 @@ def scan_jvp(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_i
         y = torch.empty((B, L, D), device=dev, dtype=torch.float32)
         dy = torch.empty((K, B, L, D), device=dev, dtype=torch.float32)
     st = torch.cuda.current_stream(dev).cuda_stream if stream is None else stream
-    rc = L_.pgf_scan_jvp(_ptr(x), _ptr(dx), ctypes.byref(pr), _ptr(y), _ptr(dy), ctypes.c_void_p(st))
+    with torch.cuda.device(dev):   # the library launches on the current device
+        rc = L_.pgf_scan_jvp(_ptr(x), _ptr(dx), ctypes.byref(pr), _ptr(y), _ptr(dy), ctypes.c_void_p(st))
     _check(rc)
     if return_state:
         return y, dy, h_out, dh_out

@@ -124,3 +124,15 @@ def test_scan_rejects_bad_arguments_before_launch():
     assert _call(p) == -1
     p = _valid_params(N=12)
     assert _call(p) == -2
+
+
+def test_binding_refuses_host_tensors_and_missing_library(monkeypatch):
+    import torch
+    x = torch.zeros(1, 4, 16)
+    dx = torch.zeros(1, 1, 4, 16)
+    with pytest.raises(ValueError, match="device tensors"):
+        binding.scan_jvp(x, dx, {"A": torch.zeros(16, 16)})
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "LIB_PATH", "/nonexistent/libpgf.so")
+    with pytest.raises(RuntimeError, match="not found"):
+        binding.lib()

@@ -114,3 +114,28 @@ def test_workspace_too_small_is_rejected():
     assert rc == -3
     torch.cuda.synchronize()
     assert torch.all(y == 7.0) and torch.all(dy == 7.0)   # outputs untouched
+
+
+@pytest.mark.parametrize("N,K,D", [(64, 8, 40), (32, 2, 98), (16, 4, 70)])
+def test_bf16_multi_thread_channels(N, K, D):
+    """bf16 inputs through the tilings where several threads share a channel,
+    with channel counts that are not multiples of 4 (scalar load paths)."""
+    inp = gu.custom("stiff128k", seqlen=900, d_inner=D, d_state=N, n_dirs=K)
+    _check(inp, f"bf16 N={N} K={K} D={D}")
+
+
+def test_timing_api_counts_launches():
+    inp = gu.custom("mamba130m", seqlen=2000, d_inner=64, n_dirs=1)
+    binding.timing_read()
+    binding.timing_enable(True)
+    try:
+        gu.run(inp, seg_len=256, chunk_segs=3)
+    finally:
+        binding.timing_enable(False)
+    t = binding.timing_read()
+    # ceil(2000 / 768) = 3 host blocks: 3 x (projection, aggregate, carry,
+    # output scan) plus the state import
+    assert t["proj"][1] == 3 and t["seg_aggregate"][1] == 3 and t["carry"][1] == 3
+    assert t["scan_out"][1] == 3 and t["state_io"][1] == 1
+    assert all(ms >= 0 for ms, _ in t.values()) and t["scan_out"][0] > 0
+    assert binding.timing_read()["scan_out"] == (0.0, 0)      # read clears
