@@ -462,6 +462,10 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
     __shared__ floatx4 s_rec4[TT * R / 4];
     __shared__ float s_sc[TT][DPB][SCP];
     const float *s_rec = (const float *)s_rec4;
+    constexpr int O = 1 + K;                 // outputs per channel
+    constexpr int OP = O | 1;                // odd pitch of one lane's partials
+    constexpr int CW = 64 / NS;              // channels per wave
+    __shared__ float s_out[OUT ? 4 * CW * NS * OP : 1];
 
     const int tid = threadIdx.x;
     const int ns = tid % NS;
@@ -626,17 +630,32 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
                 }
             }
             if constexpr (OUT) {
-                yv = group_sum<NS>(yv);
+                // Sum the NS partial outputs of each channel through this
+                // wave's LDS slice: every lane writes its K+1 partials, then
+                // lane j adds the NS partials of output j (channel j / O,
+                // output j % O) in ascending order and stores it.  A wave's
+                // LDS operations complete in order, so no barrier is needed.
+                float *wo = s_out + (tid / 64) * (CW * NS * OP);
+                const int lw = tid % 64;
+                float *mine = wo + ((lw / NS) * NS + ns) * OP;
+                mine[0] = yv;
 #pragma unroll
-                for (int k = 0; k < K; ++k) dyv[k] = group_sum<NS>(dyv[k]);
-                if (active) {
-                    const uint32_t o = (uint32_t)t * Du + (uint32_t)d;
-                    // the NS lanes of a channel share its K+1 stores
-                    if (ns == 0) store_out(Yb, o, yv);
+                for (int k = 0; k < K; ++k) mine[1 + k] = dyv[k];
+                __builtin_amdgcn_wave_barrier();
 #pragma unroll
-                    for (int k = 0; k < K; ++k)
-                        if (ns == (1 + k) % NS) store_out(DYb + k * dxs, o, dyv[k]);
+                for (int j = lw; j < CW * O; j += 64) {
+                    const int c = j / O, oi = j % O;
+                    const float *src = wo + c * NS * OP + oi;
+                    float v = src[0];
+#pragma unroll
+                    for (int q = 1; q < NS; ++q) v += src[q * OP];
+                    const int64_t dc = d0 + (tid / 64) * CW + c;
+                    if (dc < D) {
+                        float *base = oi == 0 ? Yb : DYb + (int64_t)(oi - 1) * dxs;
+                        store_out(base, (uint32_t)t * Du + (uint32_t)dc, v);
+                    }
                 }
+                __builtin_amdgcn_wave_barrier();
             }
         }
         __syncthreads();
