@@ -16,6 +16,9 @@ Layers
   dB_k = dx_k W_B, dC_k = dx_k W_C (selective input/output maps, Sec. 3).
 * ``scan_jvp``: the three above over L-chunks with the state carried between
   chunks (the block hand-off of Alg. 1), optionally for a subset of channels.
+* ``core2`` / ``discretize2`` / ``scan_jvp2``: the second-order flow of
+  App. G (mixed second directional derivative along two input directions
+  v, w, with both first-order flows), same layering.
 
 Precision: everything in fp64 from the exact fp32 / bf16 input values.
 Library routines used as steps: numpy.logaddexp (softplus), scipy expit
@@ -58,6 +61,8 @@ def _load():
     i64 = ctypes.c_int64
     lib.pgf_oracle_core.restype = ctypes.c_int
     lib.pgf_oracle_core.argtypes = [i64] * 5 + [dp] * 13 + [ctypes.c_int]
+    lib.pgf_oracle_core2.restype = ctypes.c_int
+    lib.pgf_oracle_core2.argtypes = [i64] * 4 + [dp] * 22 + [ctypes.c_int]
     _lib = lib
     return lib
 
@@ -167,3 +172,77 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
         y[:, t0:t1] = yc
         dy[:, :, t0:t1] = dyc
     return y, dy, h, dh
+
+
+# ------------------------------------------------------------------ second order
+
+def core2(A, x, xv, xw, delta, dv, dw, dvw, Bm, Cm, Bv, Cv, Bw, Cw, state=None, nthreads=None):
+    """Second-order recurrence (see pgf_oracle_core2).  Shapes: A [D,N];
+    x, xv, xw, delta, dv, dw, dvw [B,L,D]; Bm, Cm, Bv, Cv, Bw, Cw [B,L,N];
+    state = (h, hv, hw, hvw), each [B,D,N] (zero when None).
+    Returns (y, yv, yw, yvw) [B,L,D] and the exit state tuple."""
+    lib = _load()
+    A = _f64(A)
+    arrs = [_f64(a) for a in (x, xv, xw, delta, dv, dw, dvw, Bm, Cm, Bv, Cv, Bw, Cw)]
+    B, L, D = arrs[0].shape
+    N = A.shape[1]
+    for a in arrs[:7]:
+        assert a.shape == (B, L, D)
+    for a in arrs[7:]:
+        assert a.shape == (B, L, N)
+    if state is None:
+        st = [np.zeros((B, D, N)) for _ in range(4)]
+    else:
+        st = [np.array(s, dtype=np.float64, copy=True, order="C") for s in state]
+    for s_ in st:
+        assert s_.shape == (B, D, N)
+    outs = [np.empty((B, L, D)) for _ in range(4)]
+    rc = lib.pgf_oracle_core2(B, L, D, N, _dp(A), *[_dp(a) for a in arrs], *[_dp(s_) for s_ in st],
+                              *[_dp(o) for o in outs], _threads() if nthreads is None else nthreads)
+    if rc != 0:
+        raise RuntimeError("pgf_oracle_core2 failed")
+    return tuple(outs), tuple(st)
+
+
+def discretize2(x, xv, xw, w_delta, b_delta):
+    """Delta = softplus(z) and its derivatives along v and w, z = x*w_delta
+    + b_delta:  dv = s*w*xv, dw = s*w*xw, dvw = s*(1-s)*w^2*xv*xw with
+    s = sigmoid(z) = softplus'(z) and s*(1-s) = softplus''(z)."""
+    x = _f64(x)
+    w = _f64(w_delta)
+    z = x * w + _f64(b_delta)
+    delta = np.logaddexp(0.0, z)
+    s = expit(z)
+    xv, xw = _f64(xv), _f64(xw)
+    return delta, s * w * xv, s * w * xw, s * (1.0 - s) * w * w * xv * xw
+
+
+def scan_jvp2(x, dxv, dxw, params, state=None, channels=None, chunk=None, nthreads=None):
+    """Primal, both first-order flows and the mixed second-order flow of the
+    full model over L-chunks.  x, dxv, dxw [B,L,D]; params as scan_jvp.
+    Returns ((y, yv, yw, yvw) each [B,L,Dsel], exit state tuple)."""
+    B, L, D = np.shape(x)
+    A = _f64(params["A"])
+    N = A.shape[1]
+    sel = np.arange(D) if channels is None else np.asarray(channels, dtype=np.int64)
+    Ds = len(sel)
+    st = None if state is None else tuple(_f64(s_)[:, sel] if _f64(s_).shape[1] == D and Ds != D else _f64(s_)
+                                          for s_ in state)
+    outs = [np.empty((B, L, Ds)) for _ in range(4)]
+    step = max(1, L if not chunk else int(chunk))
+    w = _f64(params["w_delta"])[sel]
+    bd = _f64(params["b_delta"])[sel]
+    As = A[sel]
+    for t0 in range(0, L, step):
+        t1 = min(L, t0 + step)
+        xc = _f64(x[:, t0:t1])
+        vc = _f64(dxv[:, t0:t1])
+        wc = _f64(dxw[:, t0:t1])
+        Bm, Cm, dB, dC = project(xc, np.stack([vc, wc]), params["W_B"], params["W_C"],
+                                 params.get("b_B"), params.get("b_C"))
+        xs, vs, ws = (np.ascontiguousarray(a[..., sel]) for a in (xc, vc, wc))
+        delta, dv, dw, dvw = discretize2(xs, vs, ws, w, bd)
+        o, st = core2(As, xs, vs, ws, delta, dv, dw, dvw, Bm, Cm, dB[0], dC[0], dB[1], dC[1], st, nthreads)
+        for i in range(4):
+            outs[i][:, t0:t1] = o[i]
+    return tuple(outs), st

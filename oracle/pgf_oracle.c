@@ -122,3 +122,92 @@ int pgf_oracle_core(int64_t B, int64_t L, int64_t D, int64_t N, int64_t K,
     }
     return bad ? -1 : 0;
 }
+
+/*
+ * Second-order flow (App. G "Hessian flow"): for two input directions v and
+ * w, the mixed second directional derivative of the scan, alongside the
+ * primal and both first-order flows.  Everything is the chain rule applied
+ * twice to the same recurrence (Leibniz rule on h = Abar*h_prev + b):
+ *
+ *   Abar_v  = Abar*A*dv                      (d/dv of exp(Delta*A))
+ *   Abar_w  = Abar*A*dw
+ *   Abar_vw = Abar*A*A*dv*dw + Abar*A*dvw    (d2/dvdw of exp(Delta*A))
+ *   b    = Delta*B*x
+ *   b_v  = dv*B*x + Delta*Bv*x + Delta*B*xv
+ *   b_w  = dw*B*x + Delta*Bw*x + Delta*B*xw
+ *   b_vw = dvw*B*x + dv*Bw*x + dv*B*xw + dw*Bv*x + dw*B*xv
+ *          + Delta*Bv*xw + Delta*Bw*xv      (B is linear in x: no B_vw)
+ *   h'    = Abar*h + b
+ *   hv'   = Abar*hv + Abar_v*h + b_v
+ *   hw'   = Abar*hw + Abar_w*h + b_w
+ *   hvw'  = Abar*hvw + Abar_w*hv + Abar_v*hw + Abar_vw*h + b_vw
+ *   y     = sum_n C h'
+ *   yv    = sum_n Cv h' + C hv'
+ *   yw    = sum_n Cw h' + C hw'
+ *   yvw   = sum_n Cv hw' + Cw hv' + C hvw'  (C is linear in x: no C_vw)
+ *
+ * dv, dw, dvw are the first and second directional derivatives of Delta;
+ * Bv, Bw, Cv, Cw those of B and C.  Shapes (double, row-major): A [D,N];
+ * x, xv, xw, delta, dv, dw, dvw [B,L,D]; Bm, Cm, Bv, Cv, Bw, Cw [B,L,N];
+ * h, hv, hw, hvw [B,D,N] (entry state in, exit state out);
+ * y, yv, yw, yvw [B,L,D].  Returns 0, or -1 on a bad argument.
+ */
+int pgf_oracle_core2(int64_t B, int64_t L, int64_t D, int64_t N,
+                     const double *A, const double *x, const double *xv, const double *xw,
+                     const double *delta, const double *dv, const double *dw, const double *dvw,
+                     const double *Bm, const double *Cm, const double *Bv, const double *Cv,
+                     const double *Bw, const double *Cw,
+                     double *h, double *hv, double *hw, double *hvw,
+                     double *y, double *yv, double *yw, double *yvw, int nthreads)
+{
+    if (B < 0 || L < 0 || D < 0 || N <= 0) return -1;
+    if (!A || !h || !hv || !hw || !hvw) return -1;
+    if (L > 0 && (!x || !xv || !xw || !delta || !dv || !dw || !dvw || !Bm || !Cm || !Bv || !Cv ||
+                  !Bw || !Cw || !y || !yv || !yw || !yvw))
+        return -1;
+    const int64_t lanes = B * D;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t lane = 0; lane < lanes; ++lane) {
+        const int64_t b = lane / D, d = lane % D;
+        for (int64_t t = 0; t < L; ++t) {
+            const int64_t btd = (b * L + t) * D + d;
+            const int64_t btn = (b * L + t) * N;
+            const double xt = x[btd], xvt = xv[btd], xwt = xw[btd];
+            const double dl = delta[btd], dlv = dv[btd], dlw = dw[btd], dlvw = dvw[btd];
+            double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+            for (int64_t n = 0; n < N; ++n) {
+                const int64_t i = (b * D + d) * N + n;
+                const double a = A[d * N + n];
+                const double ab = exp(dl * a);
+                const double ab_v = ab * a * dlv;
+                const double ab_w = ab * a * dlw;
+                const double ab_vw = ab * a * a * dlv * dlw + ab * a * dlvw;
+                const double Bt = Bm[btn + n], Bvt = Bv[btn + n], Bwt = Bw[btn + n];
+                const double bt = dl * Bt * xt;
+                const double bt_v = dlv * Bt * xt + dl * Bvt * xt + dl * Bt * xvt;
+                const double bt_w = dlw * Bt * xt + dl * Bwt * xt + dl * Bt * xwt;
+                const double bt_vw = dlvw * Bt * xt + dlv * Bwt * xt + dlv * Bt * xwt + dlw * Bvt * xt +
+                                     dlw * Bt * xvt + dl * Bvt * xwt + dl * Bwt * xvt;
+                const double h0 = h[i], hv0 = hv[i], hw0 = hw[i], hvw0 = hvw[i];
+                const double h1 = ab * h0 + bt;
+                const double hv1 = ab * hv0 + ab_v * h0 + bt_v;
+                const double hw1 = ab * hw0 + ab_w * h0 + bt_w;
+                const double hvw1 = ab * hvw0 + ab_w * hv0 + ab_v * hw0 + ab_vw * h0 + bt_vw;
+                h[i] = h1; hv[i] = hv1; hw[i] = hw1; hvw[i] = hvw1;
+                const double Ct = Cm[btn + n], Cvt = Cv[btn + n], Cwt = Cw[btn + n];
+                s0 += Ct * h1;
+                s1 += Cvt * h1 + Ct * hv1;
+                s2 += Cwt * h1 + Ct * hw1;
+                s3 += Cvt * hw1 + Cwt * hv1 + Ct * hvw1;
+            }
+            y[btd] = s0; yv[btd] = s1; yw[btd] = s2; yvw[btd] = s3;
+        }
+    }
+    return 0;
+}
