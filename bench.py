@@ -36,17 +36,22 @@ def parse():
                     help="condense two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; made with "
                          "--calib-copy) into profiles/traffic_<workload>.json and exit")
     ap.add_argument("--traffic-out", default=None, help="output path of --summarize-counters")
+    ap.add_argument("--order", type=int, default=1, choices=(1, 2),
+                    help="2: second-order flow (two directions, pgf_scan_jvp2)")
     ap.add_argument("--seg-len", type=int, default=0, help="tiling override (0 = library default)")
     ap.add_argument("--chunk-segs", type=int, default=0, help="tiling override (0 = library default)")
     return ap.parse_args()
 
 
-def scan_flops_per_lane_step(K):
+def scan_flops_per_lane_step(K, order=1):
     """Arithmetic of the definition per (b, t, d, n) and step, counting an fma
     as 2 and exp as 1: primal Delta*A, exp, Abar*h, B*u + s, C*h' (7 with the
     shared A*s); per direction Abar*dh + (A s)*dDelta + B*p + dB*u (7) and
-    dC*h' + C*dh' (4)."""
-    return 7 + 11 * K
+    dC*h' + C*dh' (4).  The mixed second-order flow adds Abar*hvw, the two
+    cross-talk products A*(Abar*h_v)*dw and A*(Abar*h_w)*dv, the curvature
+    (A s)*(A*dv*dw + dvw), the drive B*q + dBv*pw + dBw*pv (19) and its
+    output dCv*hw + dCw*hv + C*hvw (6)."""
+    return 7 + 11 * K + (25 if order == 2 else 0)
 
 
 COPY_BYTES = 1 << 30
@@ -75,7 +80,7 @@ def _kernel_label(name):
     return "copy" if "copyBuffer" in base else base
 
 
-def summarize_counters(workload, fetch_csv, write_csv, out_path=None):
+def summarize_counters(workload, order, fetch_csv, write_csv, out_path=None):
     import csv
     import statistics
     per = {}
@@ -91,7 +96,9 @@ def summarize_counters(workload, fetch_csv, write_csv, out_path=None):
                     calib[counter] = v        # the 1 GiB copy is the largest copy dispatch
                 continue
             per.setdefault(lab, {}).setdefault(counter, []).append(v)
-    out = {"workload": workload, "source_sha256": source_digest(),
+    label = workload + ("-order2" if order == 2 else "")
+    opt = " --order 2" if order == 2 else ""
+    out = {"workload": label, "source_sha256": source_digest(),
            "calibration": {"copy_bytes": COPY_BYTES, "FETCH_SIZE_KiB": calib.get("FETCH_SIZE"),
                            "WRITE_SIZE_KiB": calib.get("WRITE_SIZE"),
                            "fetch_factor": calib.get("FETCH_SIZE", 0) * 1024 / COPY_BYTES,
@@ -107,9 +114,9 @@ def summarize_counters(workload, fetch_csv, write_csv, out_path=None):
                                "hbm_bytes_per_dispatch": int(f * 1024 / ff + w * 1024 / wf)}
     out["commands"] = [
         f"rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pmc_{workload}_{c} -o pmc -- "
-        f"python3 -u bench.py --workload {workload} --steps 2 --warmup 1 --no-cpu --calib-copy"
+        f"python3 -u bench.py --workload {workload}{opt} --steps 2 --warmup 1 --no-cpu --calib-copy"
         for c in ("FETCH_SIZE", "WRITE_SIZE")]
-    path = out_path or os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    path = out_path or os.path.join(ROOT, "profiles", f"traffic_{label}.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
     print(path)
@@ -133,7 +140,7 @@ def committed_traffic(workload, kind):
 def main():
     args = parse()
     if args.summarize_counters:
-        summarize_counters(args.workload, *args.summarize_counters, out_path=args.traffic_out)
+        summarize_counters(args.workload, args.order, *args.summarize_counters, out_path=args.traffic_out)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on one GPU only; --gpus must be 1", file=sys.stderr)
@@ -144,6 +151,9 @@ def main():
     from paper_2512_23068_amd import binding, inputs
 
     cfg = inputs.get_config(args.workload)
+    if args.order == 2:
+        # two independent N(0,1) directions on the same workload shape
+        cfg = cfg.with_(n_dirs=2, dx_kind="normal")
     B, L, D, N, K = cfg.batch, cfg.seqlen, cfg.d_inner, cfg.d_state, cfg.n_dirs
     dev = torch.device("cuda:0")
     t_gen = time.time()
@@ -159,14 +169,19 @@ def main():
     del inp
     y = torch.empty((B, L, D), device=dev)
     dy = torch.empty((K, B, L, D), device=dev)
-    plan = binding.plan(B, L, D, N, K, cfg.in_dtype, args.seg_len, args.chunk_segs)
+    outs = (y, dy)
+    if args.order == 2:
+        outs = outs + (torch.empty((B, L, D), device=dev),)
+        payload += x.numel() * 4
+    plan = binding.plan(B, L, D, N, K, cfg.in_dtype, args.seg_len, args.chunk_segs, args.order)
     ws = torch.empty(plan["workspace_bytes"], device=dev, dtype=torch.uint8)
     torch.cuda.synchronize()
     base_alloc = torch.cuda.memory_allocated()
 
+    fn = binding.scan_jvp2 if args.order == 2 else binding.scan_jvp
+
     def step():
-        binding.scan_jvp(x, dx, params, workspace=ws, out=(y, dy), seg_len=args.seg_len,
-                         chunk_segs=args.chunk_segs)
+        fn(x, dx, params, workspace=ws, out=outs, seg_len=args.seg_len, chunk_segs=args.chunk_segs)
 
     for _ in range(args.warmup):
         step()
@@ -203,7 +218,7 @@ def main():
 
     tokch = B * L * D
     value = tokch / (ms_step * 1e-3) / 1e9
-    alg_bytes = tokch * (1 + K) * (s_in + 4)
+    alg_bytes = tokch * ((1 + K) * (s_in + 4) + (4 if args.order == 2 else 0))
     # Dominant kernel: the scan that writes the outputs (kind 3).  Per launch
     # it performs the whole of the algorithmic IO of its block (x, dx read
     # once, y, dy written once) and the whole per-lane arithmetic.
@@ -212,7 +227,7 @@ def main():
     so_avg_ms = so_ms / max(so_n, 1)
     launches_per_step = so_n / args.steps
     bytes_per_launch = alg_bytes / launches_per_step
-    flops_per_launch = tokch * N * scan_flops_per_lane_step(K) / launches_per_step
+    flops_per_launch = tokch * N * scan_flops_per_lane_step(K, args.order) / launches_per_step
     hbm_gbs = bytes_per_launch / (so_avg_ms * 1e-3) / 1e9
     tflops = flops_per_launch / (so_avg_ms * 1e-3) / 1e12
     roofline = {
@@ -222,7 +237,7 @@ def main():
         "peak": FP32_VECTOR_PEAK_TFLOPS,
         "unit": "TFLOP/s",
         "frac": round(tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
-        "traffic": committed_traffic(cfg.name, "scan_out"),
+        "traffic": committed_traffic(cfg.name + ("-order2" if args.order == 2 else ""), "scan_out"),
         "hbm_achieved_gbs": round(hbm_gbs, 1),
         "hbm_frac": round(hbm_gbs / HBM_PEAK_GBS, 4),
         "avg_launch_ms": round(so_avg_ms, 5),
@@ -245,11 +260,12 @@ def main():
         del src, dst
 
     cpu = None
-    if not args.no_cpu:
+    if not args.no_cpu and args.order == 1:
         cpu = cpu_baseline(cfg, args.cpu_steps)
 
     out = {
-        "metric": "primal+JVP scan Gtok·ch/s at L=128k",
+        "metric": "primal+JVP scan Gtok·ch/s at L=128k" if args.order == 1
+                  else "primal+JVP+second-order scan Gtok·ch/s",
         "value": round(value, 3),
         "unit": "Gtok·ch/s",
         "n_gpus": 1,
@@ -261,7 +277,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32" if cfg.in_dtype == "f32" else "bf16-in/f32",
         "data": "synthetic (seeded; BASELINE recipe)",
-        "config": {"workload": cfg.name, "batch": B, "seq_len": L, "d_inner": D, "d_state": N, "n_dirs": K,
+        "config": {"workload": cfg.name + ("-order2" if args.order == 2 else ""), "batch": B, "seq_len": L, "d_inner": D, "d_state": N, "n_dirs": K,
                    "in_dtype": cfg.in_dtype, "parallelism": "single GPU"},
         "hbm_gbs_path": round(alg_bytes / (ms_step * 1e-3) / 1e9, 1),
         "hbm_frac_path": round(alg_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),

@@ -87,6 +87,10 @@ typedef struct pgf_params {
      * Results are bit-identical for every chunk_segs at a fixed seg_len. */
     int32_t seg_len;
     int32_t chunk_segs;
+    /* 0 or 1: first order (pgf_scan_jvp).  2: second order (pgf_scan_jvp2,
+     * which needs n_dirs == 2 and N <= 16).  Read by the planning calls too:
+     * the second order carries one more state per lane. */
+    int32_t order;
     /* Model parameters (device, f32).  b_B / b_C may be NULL (= 0). */
     const float *A, *w_delta, *b_delta, *W_B, *W_C, *b_B, *b_C;
     /* Optional state hand-off (device, f32; NULL = zero in / not written).
@@ -99,6 +103,10 @@ typedef struct pgf_params {
      * aligned.  Its size does not depend on L. */
     void *workspace;
     size_t workspace_bytes;
+    /* Second order only: state of the mixed flow, [B,D,N] (NULL = zero in /
+     * not written). */
+    const float *d2h_in;
+    float *d2h_out;
 } pgf_params;
 
 /* How a call is tiled (host-side planning; no device access). */
@@ -130,6 +138,24 @@ int pgf_plan(const pgf_params *p, pgf_plan_info *info);
  * error code; see the conventions above. */
 int pgf_scan_jvp(const void *x, const void *dx, const pgf_params *p,
                  float *y, float *dy, void *stream);
+
+/* Second-order flow (App. G, the Hessian flow): along the two input
+ * directions v = dx[0] and w = dx[1], the primal, both first-order flows and
+ * the mixed second directional derivative, with the curvature of
+ * Delta = softplus(z) (softplus'' = sigmoid*(1-sigmoid)) and the
+ * cross-talk terms of the transition:
+ *   h_vw = Abar*h_vw + Abar_w*h_v + Abar_v*h_w + Abar_vw*h + b_vw,
+ *   Abar_vw = Abar*A^2*dDelta_v*dDelta_w + Abar*A*d2Delta_vw,
+ *   d2y[b,t,d] = sum_n dC_v h_w + dC_w h_v + C h_vw.
+ *   x   : device, [B,L,D] in in_dtype      dx : device, [2,B,L,D] (v, w)
+ *   y   : device, [B,L,D] f32              dy : device, [2,B,L,D] f32
+ *   d2y : device, [B,L,D] f32 (the mixed flow's output)
+ * p->order must be 2 and p->n_dirs 2; h_in/dh_in/h_out/dh_out and
+ * d2h_in/d2h_out carry the state as in pgf_scan_jvp.  y and dy equal what
+ * pgf_scan_jvp returns for the same two directions up to rounding.  Other
+ * conventions as pgf_scan_jvp; d2y must not overlap any other array. */
+int pgf_scan_jvp2(const void *x, const void *dx, const pgf_params *p,
+                  float *y, float *dy, float *d2y, void *stream);
 
 /* Static string for a status code. */
 const char *pgf_status_string(int status);

@@ -29,10 +29,12 @@ class PgfParams(ctypes.Structure):
         ("batch", ctypes.c_int64), ("seqlen", ctypes.c_int64), ("d_inner", ctypes.c_int64),
         ("d_state", ctypes.c_int64), ("n_dirs", ctypes.c_int64),
         ("in_dtype", ctypes.c_int32), ("seg_len", ctypes.c_int32), ("chunk_segs", ctypes.c_int32),
+        ("order", ctypes.c_int32),
         ("A", _c_f), ("w_delta", _c_f), ("b_delta", _c_f), ("W_B", _c_f), ("W_C", _c_f),
         ("b_B", _c_f), ("b_C", _c_f),
         ("h_in", _c_f), ("dh_in", _c_f), ("h_out", _c_f), ("dh_out", _c_f),
         ("workspace", _c_f), ("workspace_bytes", ctypes.c_size_t),
+        ("d2h_in", _c_f), ("d2h_out", _c_f),
     ]
 
 
@@ -44,7 +46,7 @@ class PgfPlanInfo(ctypes.Structure):
     ]
 
 
-EXPORTED = ("pgf_workspace_bytes", "pgf_plan", "pgf_scan_jvp", "pgf_status_string",
+EXPORTED = ("pgf_workspace_bytes", "pgf_plan", "pgf_scan_jvp", "pgf_scan_jvp2", "pgf_status_string",
             "pgf_timing_enable", "pgf_timing_read")
 
 _lib = None
@@ -66,6 +68,9 @@ def lib():
     L.pgf_scan_jvp.restype = ctypes.c_int
     L.pgf_scan_jvp.argtypes = [ctypes.c_void_p, ctypes.c_void_p, P, ctypes.c_void_p, ctypes.c_void_p,
                                ctypes.c_void_p]
+    L.pgf_scan_jvp2.restype = ctypes.c_int
+    L.pgf_scan_jvp2.argtypes = [ctypes.c_void_p, ctypes.c_void_p, P, ctypes.c_void_p, ctypes.c_void_p,
+                                ctypes.c_void_p, ctypes.c_void_p]
     L.pgf_status_string.restype = ctypes.c_char_p
     L.pgf_status_string.argtypes = [ctypes.c_int]
     L.pgf_timing_enable.restype = ctypes.c_int
@@ -85,21 +90,22 @@ def _check(code: int):
         raise RuntimeError(status_string(code))
 
 
-def make_params(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0) -> PgfParams:
+def make_params(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1) -> PgfParams:
     p = PgfParams()
     p.batch, p.seqlen, p.d_inner, p.d_state, p.n_dirs = int(B), int(L), int(D), int(N), int(K)
     p.in_dtype = PGF_BF16 if in_dtype in ("bf16", torch.bfloat16) else PGF_F32
-    p.seg_len, p.chunk_segs = int(seg_len), int(chunk_segs)
+    p.seg_len, p.chunk_segs, p.order = int(seg_len), int(chunk_segs), int(order)
     return p
 
 
-def workspace_bytes(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0) -> int:
-    return int(lib().pgf_workspace_bytes(ctypes.byref(make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs))))
+def workspace_bytes(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1) -> int:
+    return int(lib().pgf_workspace_bytes(ctypes.byref(make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs,
+                                                                  order))))
 
 
-def plan(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0) -> dict:
+def plan(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1) -> dict:
     info = PgfPlanInfo()
-    _check(lib().pgf_plan(ctypes.byref(make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs)),
+    _check(lib().pgf_plan(ctypes.byref(make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs, order)),
                           ctypes.byref(info)))
     return {f: getattr(info, f) for f, _ in PgfPlanInfo._fields_}
 
@@ -118,15 +124,7 @@ def _dev_param(v, shape, device, name):
     return v.to(device=device, dtype=torch.float32).contiguous()
 
 
-def scan_jvp(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_in=None, return_state=False,
-             seg_len=0, chunk_segs=0, workspace=None, out=None, stream=None):
-    """Fused primal + tangent scan on the GPU.
-
-    x [B,L,D] and dx [K,B,L,D]: float32 or bfloat16 CUDA tensors (same dtype).
-    params: A, W_B, W_C [D,N]; w_delta, b_delta [D]; optional b_B, b_C [N].
-    Returns (y [B,L,D], dy [K,B,L,D]) in float32, plus (h_out [B,D,N],
-    dh_out [K,B,D,N]) when return_state.  Asynchronous on the current stream.
-    """
+def _scan(x, dx, params, order, h_in, dh_in, d2h_in, return_state, seg_len, chunk_segs, workspace, out, stream):
     L_ = lib()
     if not (x.is_cuda and dx.is_cuda):
         raise ValueError("x and dx must be device tensors")
@@ -138,11 +136,13 @@ def scan_jvp(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_i
     dx = dx.contiguous()
     B, L, D = x.shape
     K = dx.shape[0]
+    if order == 2 and K != 2:
+        raise ValueError("the second-order scan takes exactly two directions (dx of shape [2,B,L,D])")
     dev = x.device
     A = _dev_param(params["A"], (D, params["A"].shape[1]), dev, "A")
     N = A.shape[1]
     keep = [A]
-    pr = make_params(B, L, D, N, K, "bf16" if x.dtype == torch.bfloat16 else "f32", seg_len, chunk_segs)
+    pr = make_params(B, L, D, N, K, "bf16" if x.dtype == torch.bfloat16 else "f32", seg_len, chunk_segs, order)
     vals = {"A": A}
     for name, shape in (("w_delta", (D,)), ("b_delta", (D,)), ("W_B", (D, N)), ("W_C", (D, N)),
                         ("b_B", (N,)), ("b_C", (N,))):
@@ -152,13 +152,20 @@ def scan_jvp(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_i
         setattr(pr, name, None if vals[name] is None else vals[name].data_ptr())
     h_in = _dev_param(h_in, (B, D, N), dev, "h_in")
     dh_in = _dev_param(dh_in, (K, B, D, N), dev, "dh_in")
+    d2h_in = _dev_param(d2h_in, (B, D, N), dev, "d2h_in")
     pr.h_in = None if h_in is None else h_in.data_ptr()
     pr.dh_in = None if dh_in is None else dh_in.data_ptr()
-    h_out = dh_out = None
+    pr.d2h_in = None if d2h_in is None else d2h_in.data_ptr()
+    states = ()
     if return_state:
         h_out = torch.empty((B, D, N), device=dev, dtype=torch.float32)
         dh_out = torch.empty((K, B, D, N), device=dev, dtype=torch.float32)
         pr.h_out, pr.dh_out = h_out.data_ptr(), dh_out.data_ptr()
+        states = (h_out, dh_out)
+        if order == 2:
+            d2h_out = torch.empty((B, D, N), device=dev, dtype=torch.float32)
+            pr.d2h_out = d2h_out.data_ptr()
+            states = states + (d2h_out,)
     nbytes = int(L_.pgf_workspace_bytes(ctypes.byref(pr)))
     if nbytes == 0:
         _check(L_.pgf_plan(ctypes.byref(pr), ctypes.byref(PgfPlanInfo())))
@@ -166,17 +173,46 @@ def scan_jvp(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_i
         workspace = torch.empty(max(nbytes, 1), device=dev, dtype=torch.uint8)
     pr.workspace, pr.workspace_bytes = workspace.data_ptr(), workspace.numel()
     if out is not None:
-        y, dy = out
+        outs = tuple(out)
     else:
-        y = torch.empty((B, L, D), device=dev, dtype=torch.float32)
-        dy = torch.empty((K, B, L, D), device=dev, dtype=torch.float32)
+        outs = (torch.empty((B, L, D), device=dev, dtype=torch.float32),
+                torch.empty((K, B, L, D), device=dev, dtype=torch.float32))
+        if order == 2:
+            outs = outs + (torch.empty((B, L, D), device=dev, dtype=torch.float32),)
     st = torch.cuda.current_stream(dev).cuda_stream if stream is None else stream
     with torch.cuda.device(dev):   # the library launches on the current device
-        rc = L_.pgf_scan_jvp(_ptr(x), _ptr(dx), ctypes.byref(pr), _ptr(y), _ptr(dy), ctypes.c_void_p(st))
+        if order == 2:
+            rc = L_.pgf_scan_jvp2(_ptr(x), _ptr(dx), ctypes.byref(pr), _ptr(outs[0]), _ptr(outs[1]),
+                                  _ptr(outs[2]), ctypes.c_void_p(st))
+        else:
+            rc = L_.pgf_scan_jvp(_ptr(x), _ptr(dx), ctypes.byref(pr), _ptr(outs[0]), _ptr(outs[1]),
+                                 ctypes.c_void_p(st))
     _check(rc)
-    if return_state:
-        return y, dy, h_out, dh_out
-    return y, dy
+    return outs + states
+
+
+def scan_jvp(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_in=None, return_state=False,
+             seg_len=0, chunk_segs=0, workspace=None, out=None, stream=None):
+    """Fused primal + tangent scan on the GPU.
+
+    x [B,L,D] and dx [K,B,L,D]: float32 or bfloat16 CUDA tensors (same dtype).
+    params: A, W_B, W_C [D,N]; w_delta, b_delta [D]; optional b_B, b_C [N].
+    Returns (y [B,L,D], dy [K,B,L,D]) in float32, plus (h_out [B,D,N],
+    dh_out [K,B,D,N]) when return_state.  Asynchronous on the current stream.
+    """
+    return _scan(x, dx, params, 1, h_in, dh_in, None, return_state, seg_len, chunk_segs, workspace, out, stream)
+
+
+def scan_jvp2(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_in=None, d2h_in=None,
+              return_state=False, seg_len=0, chunk_segs=0, workspace=None, out=None, stream=None):
+    """Second-order flow on the GPU along v = dx[0], w = dx[1] (dx [2,B,L,D]).
+
+    Returns (y [B,L,D], dy [2,B,L,D], d2y [B,L,D]) in float32: the primal,
+    both first-order directional derivatives and the mixed second
+    directional derivative; plus (h_out, dh_out, d2h_out) when return_state.
+    """
+    return _scan(x, dx, params, 2, h_in, dh_in, d2h_in, return_state, seg_len, chunk_segs, workspace, out,
+                 stream)
 
 
 def timing_enable(on: bool = True):

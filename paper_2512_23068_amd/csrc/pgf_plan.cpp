@@ -58,8 +58,15 @@ int make_plan(const pgf_params *p, Plan *plan) {
     if ((1 + K) * B * N * D > (int64_t(1) << 36)) return PGF_ERR_UNSUPPORTED;
     if ((double)K * B * (double)L * D > 9.0e18 / 16) return PGF_ERR_UNSUPPORTED;
 
+    if (p->order < 0 || p->order > 2) return PGF_ERR_INVALID_ARG;
+    const int order = p->order == 2 ? 2 : 1;
+    if (order == 2 && K != 2) return PGF_ERR_INVALID_ARG;
+    if (order == 2 && N > 16) return PGF_ERR_UNSUPPORTED;
+
     Plan q{};
     q.B = B; q.L = L; q.D = D; q.N = N; q.K = K;
+    q.order = order;
+    q.comp = (int)(1 + K + (order == 2 ? 1 : 0));
     q.in_bf16 = p->in_dtype == PGF_BF16;
     // Registers per thread grow as nt*(3+K); keep them near 128.
     q.nt = (int)std::min<int64_t>(N, K >= 8 ? 4 : (K >= 4 ? 8 : 16));
@@ -99,7 +106,7 @@ int make_plan(const pgf_params *p, Plan *plan) {
     } else {
         // At least three rounds of resident blocks per launch, rounded to a
         // whole number of rounds when the workspace allows it.
-        const size_t per_seg = (size_t)B * (1 + K) * (size_t)(N * D + D) * sizeof(float) +
+        const size_t per_seg = (size_t)B * q.comp * (size_t)(N * D + D) * sizeof(float) +
                                (size_t)B * seg * q.R * sizeof(float);
         const int64_t cap = std::max<int64_t>(1, (int64_t)(kWorkspaceCap / per_seg));
         const int64_t period = kResidentBlocks / gcd64(nblk, kResidentBlocks);
@@ -116,7 +123,7 @@ int make_plan(const pgf_params *p, Plan *plan) {
     q.n_chunks = (L + q.chunk_len - 1) / q.chunk_len;
 
     const size_t f = sizeof(float);
-    const size_t comp = (size_t)(1 + K);
+    const size_t comp = (size_t)q.comp;
     Layout w{};
     size_t off = 0;
     w.state = off; off = align256(off + comp * B * N * D * f);

@@ -24,6 +24,8 @@ struct Layout {
 
 struct Plan {
     int64_t B, L, D, N, K;
+    int order;           // 1 or 2
+    int comp;            // states per lane: 1 + K (+ 1 for the mixed flow)
     int in_bf16;
     int nt, ns;          // states per thread, threads per channel (nt*ns == N)
     int seg;             // segment length; 0 = sequential evaluation

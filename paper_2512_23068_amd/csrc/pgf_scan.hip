@@ -101,6 +101,25 @@ __device__ __forceinline__ void discretize(float xv, float w, float bd, float &d
     sw = (z >= 0.0f ? r : e * r) * w;
 }
 
+// Also returns s2 = softplus''(z) * w^2 = sigmoid(z)(1 - sigmoid(z)) w^2,
+// which is e/(1+e)^2 * w^2 on both sides of z = 0.
+__device__ __forceinline__ void discretize2(float xv, float w, float bd, float &delta, float &sw, float &s2) {
+    const float z = fmaf(xv, w, bd);
+    const float e = exp_nonpos(-fabsf(z));
+    const float sv = e * __builtin_amdgcn_rcpf(2.0f + e);
+    const float q = sv * sv;
+    float poly = fmaf(q, 1.0f / 13.0f, 1.0f / 11.0f);
+    poly = fmaf(q, poly, 1.0f / 9.0f);
+    poly = fmaf(q, poly, 1.0f / 7.0f);
+    poly = fmaf(q, poly, 1.0f / 5.0f);
+    poly = fmaf(q, poly, 1.0f / 3.0f);
+    poly = fmaf(q, poly, 1.0f);
+    delta = fmaxf(z, 0.0f) + 2.0f * sv * poly;
+    const float r = __builtin_amdgcn_rcpf(1.0f + e);
+    sw = (z >= 0.0f ? r : e * r) * w;
+    s2 = (e * r) * r * (w * w);
+}
+
 // ---------------------------------------------------------------- k_proj
 // rec[b][t-t0] = [B(N) | dB_0..dB_{K-1} (N each) | C(N) | dC_0..dC_{K-1}]
 // Row source s = blockIdx.y: 0 -> x (bias added), 1+k -> dx_k.
@@ -701,6 +720,245 @@ constexpr auto scan_kernel() {
     else return &k_scan_sh<NT, NS, K, OUT, InT>;
 }
 
+// ---------------------------------------------------------------- k_scan2
+// Second-order flow, one thread per channel with all NT = N states: the
+// primal h, the first-order flows hv, hw along v = dx[0] and w = dx[1]
+// (same operation order as k_scan, so y, dy match the first-order kernel)
+// and the mixed flow (App. G):
+//   hvw' = Abar hvw + Abar_w hv + Abar_v hw + Abar_vw h + b_vw
+// with Abar_v h = (A Abar h) dv, Abar_vw h = (A Abar h)(A dv dw + dvw) and
+// b_vw = B q + dBv pw + dBw pv,  q = dvw x + dv xw + dw xv,
+// pv = dv x + Delta xv, pw = dw x + Delta xw.  Layouts and grid as k_scan
+// with 4 state components (h, hv, hw, hvw).
+template <int NT, bool OUT, typename InT>
+__global__ __launch_bounds__(kThreads) void k_scan2(
+    const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A,
+    const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
+    const float *__restrict__ init, int64_t ibs, int64_t igs, int64_t ics,
+    float *__restrict__ y, float *__restrict__ dy, float *__restrict__ d2y, float *__restrict__ end_state,
+    float *__restrict__ agg_h, float *__restrict__ agg_s,
+    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    constexpr int N = NT;
+    constexpr int R = 6 * N;          // B, dBv, dBw, C, dCv, dCw
+    constexpr int TT = 8;
+
+    const int tid = threadIdx.x;
+    const int64_t d_raw = (int64_t)blockIdx.x * kThreads + tid;
+    const bool active = d_raw < D;
+    const int64_t d = active ? d_raw : D - 1;
+    const int g = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int64_t ts = (int64_t)g * S;
+    const int64_t te = ts + S < len ? ts + S : len;
+    if (ts >= te) return;
+
+    float Af[NT], At[NT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+        Af[i] = A[d * N + i];
+        At[i] = Af[i] * kLog2e;
+    }
+    const float w = w_delta[d], bd = b_delta[d];
+
+    float h[NT], hv[NT], hw[NT], hvw[NT];
+    if constexpr (OUT) {
+        const float *ib = init + b * ibs + g * igs + d;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            h[i] = ib[i * D];
+            hv[i] = ib[ics + i * D];
+            hw[i] = ib[2 * ics + i * D];
+            hvw[i] = ib[3 * ics + i * D];
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NT; ++i) h[i] = hv[i] = hw[i] = hvw[i] = 0.0f;
+    }
+    float sD = 0.0f, sDv = 0.0f, sDw = 0.0f, sDvw = 0.0f;
+
+    const int64_t dxs = Bsz * L * D;
+    const InT *Xb = x + (b * L + t0) * D;
+    const InT *Vb = dx + (b * L + t0) * D;
+    const InT *Wb = Vb + dxs;
+    float *Yb = y + (b * L + t0) * D;
+    float *DVb = dy + (b * L + t0) * D;
+    float *DWb = DVb + dxs;
+    float *D2b = d2y + (b * L + t0) * D;
+    const uint32_t Du = (uint32_t)D, du = (uint32_t)d;
+    const float *rec0 = bc + b * Tc * R;
+
+    float xc[TT], vc[TT], wc[TT];
+#pragma unroll
+    for (int j = 0; j < TT; ++j) {
+        const int64_t t = ts + j < te ? ts + j : te - 1;
+        const uint32_t o = (uint32_t)t * Du + du;
+        xc[j] = load_in(Xb, o);
+        vc[j] = load_in(Vb, o);
+        wc[j] = load_in(Wb, o);
+    }
+    for (int64_t tb = ts; tb < te; tb += TT) {
+        float xn[TT], vn[TT], wn[TT];
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
+            const uint32_t o = (uint32_t)t * Du + du;
+            xn[j] = load_in(Xb, o);
+            vn[j] = load_in(Vb, o);
+            wn[j] = load_in(Wb, o);
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + j;
+            if (t < te) {
+                const float xv = xc[j], vv = vc[j], wv = wc[j];
+                float delta, sw, s2;
+                discretize2(xv, w, bd, delta, sw, s2);
+                const float dv = sw * vv, dw = sw * wv;
+                const float dvw = s2 * vv * wv;
+                const float u = delta * xv;
+                const float pv = fmaf(dv, xv, delta * vv);
+                const float pw = fmaf(dw, xv, delta * wv);
+                const float q = fmaf(dvw, xv, fmaf(dv, wv, dw * vv));
+                const float c1 = dv * dw;
+                if constexpr (!OUT) {
+                    sD += delta;
+                    sDv += dv;
+                    sDw += dw;
+                    sDvw += dvw;
+                }
+                const float *rec = rec0 + t * R;
+                float yv = 0.0f, y1 = 0.0f, y2 = 0.0f, y3 = 0.0f;
+#pragma unroll
+                for (int i = 0; i < NT; ++i) {
+                    const float Bn = rec[i], dBv = rec[N + i], dBw = rec[2 * N + i];
+                    const float a = __builtin_amdgcn_exp2f(delta * At[i]);
+                    const float sv = a * h[i];
+                    const float gv = Af[i] * sv;
+                    const float hn = fmaf(Bn, u, sv);
+                    const float g1 = Af[i] * (a * hv[i]);
+                    const float g2 = Af[i] * (a * hw[i]);
+                    const float hvn = fmaf(a, hv[i], fmaf(gv, dv, fmaf(Bn, pv, dBv * u)));
+                    const float hwn = fmaf(a, hw[i], fmaf(gv, dw, fmaf(Bn, pw, dBw * u)));
+                    const float cvw = fmaf(Af[i], c1, dvw);
+                    const float hvwn = fmaf(a, hvw[i],
+                                            fmaf(g1, dw, fmaf(g2, dv, fmaf(gv, cvw, fmaf(Bn, q, fmaf(dBv, pw, dBw * pv))))));
+                    h[i] = hn;
+                    hv[i] = hvn;
+                    hw[i] = hwn;
+                    hvw[i] = hvwn;
+                    if constexpr (OUT) {
+                        const float Cn = rec[3 * N + i], dCv = rec[4 * N + i], dCw = rec[5 * N + i];
+                        yv = fmaf(Cn, hn, yv);
+                        y1 = fmaf(dCv, hn, fmaf(Cn, hvn, y1));
+                        y2 = fmaf(dCw, hn, fmaf(Cn, hwn, y2));
+                        y3 = fmaf(Cn, hvwn, fmaf(dCw, hvn, fmaf(dCv, hwn, y3)));
+                    }
+                }
+                if constexpr (OUT) {
+                    if (active) {
+                        const uint32_t o = (uint32_t)t * Du + du;
+                        store_out(Yb, o, yv);
+                        store_out(DVb, o, y1);
+                        store_out(DWb, o, y2);
+                        store_out(D2b, o, y3);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            xc[j] = xn[j];
+            vc[j] = vn[j];
+            wc[j] = wn[j];
+        }
+    }
+
+    if (!active) return;
+    if constexpr (OUT) {
+        if (end_state) {
+            float *eb = end_state + b * ibs + d;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                eb[i * D] = h[i];
+                eb[ics + i * D] = hv[i];
+                eb[2 * ics + i * D] = hw[i];
+                eb[3 * ics + i * D] = hvw[i];
+            }
+        }
+    } else {
+        const int64_t base = (b * G + g) * 4;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            agg_h[(base * N + i) * D + d] = h[i];
+            agg_h[((base + 1) * N + i) * D + d] = hv[i];
+            agg_h[((base + 2) * N + i) * D + d] = hw[i];
+            agg_h[((base + 3) * N + i) * D + d] = hvw[i];
+        }
+        agg_s[base * D + d] = sD;
+        agg_s[(base + 1) * D + d] = sDv;
+        agg_s[(base + 2) * D + d] = sDw;
+        agg_s[(base + 3) * D + d] = sDvw;
+    }
+}
+
+// Carry of the second-order flow: each segment acts on (h, hv, hw, hvw) as
+//   h' = P h + h0, hv' = P hv + Pv h + hv0, hw' = P hw + Pw h + hw0,
+//   hvw' = P hvw + Pw hv + Pv hw + Pvw h + hvw0,
+// P = 2^(At S), Pv = P (A Sv), Pw = P (A Sw), Pvw = P ((A Sv)(A Sw) + A Svw):
+// the derivatives of the segment's map h_in -> P h_in + h0 along v, w.
+__global__ __launch_bounds__(kThreads) void k_carry2(
+    const float *__restrict__ A, float *__restrict__ seg, const float *__restrict__ agg_s,
+    float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int G) {
+    constexpr int GB = 8;
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t ND = N * D;
+    if (idx >= Bsz * ND) return;
+    const int64_t d = idx % D, n = (idx / D) % N, b = idx / ND;
+    const float a = A[d * N + n];
+    const float at = a * kLog2e;
+    const int64_t cs = Bsz * ND;
+    const int64_t lane = n * D + d;
+    float h = state[b * ND + lane], hv = state[cs + b * ND + lane];
+    float hw = state[2 * cs + b * ND + lane], hvw = state[3 * cs + b * ND + lane];
+    for (int g0 = 0; g0 < G; g0 += GB) {
+        float e[GB][4], sm[GB][4];
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            const int g = g0 + j < G ? g0 + j : G - 1;
+            const int64_t base = (b * G + g) * 4;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                e[j][c] = seg[(base + c) * ND + lane];
+                sm[j][c] = agg_s[(base + c) * D + d];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            if (g0 + j >= G) break;
+            const int64_t base = (b * G + g0 + j) * 4;
+            seg[base * ND + lane] = h;
+            seg[(base + 1) * ND + lane] = hv;
+            seg[(base + 2) * ND + lane] = hw;
+            seg[(base + 3) * ND + lane] = hvw;
+            const float P = __builtin_amdgcn_exp2f(at * sm[j][0]);
+            const float asv = a * sm[j][1], asw = a * sm[j][2];
+            const float Pv = P * asv, Pw = P * asw;
+            const float Pvw = P * fmaf(asv, asw, a * sm[j][3]);
+            const float hvw1 = fmaf(P, hvw, fmaf(Pw, hv, fmaf(Pv, hw, fmaf(Pvw, h, e[j][3]))));
+            const float hv1 = fmaf(P, hv, fmaf(Pv, h, e[j][1]));
+            const float hw1 = fmaf(P, hw, fmaf(Pw, h, e[j][2]));
+            h = fmaf(P, h, e[j][0]);
+            hv = hv1;
+            hw = hw1;
+            hvw = hvw1;
+        }
+    }
+    state[b * ND + lane] = h;
+    state[cs + b * ND + lane] = hv;
+    state[2 * cs + b * ND + lane] = hw;
+    state[3 * cs + b * ND + lane] = hvw;
+}
+
 // ---------------------------------------------------------------- k_carry
 // One thread per lane (b, n, d), sequential over the block's segments.
 // state [(1+K)][B][N][D] enters the block and leaves it.  seg [B][G][(1+K)]
@@ -761,35 +1019,41 @@ __global__ __launch_bounds__(kThreads) void k_carry(
 
 // ---------------------------------------------------------------- state in/out
 // state [(1+K)][B][N][D] <-> h [B][D][N], dh [K][B][D][N].
+// Component c of the state: 0 -> h, 1..K -> dh_{c-1}, 1+K -> d2h (second
+// order only; comp = number of components).
 __global__ __launch_bounds__(kThreads) void k_state_import(
-    const float *__restrict__ h_in, const float *__restrict__ dh_in, float *__restrict__ state,
-    int64_t Bsz, int64_t D, int64_t N, int K) {
+    const float *__restrict__ h_in, const float *__restrict__ dh_in, const float *__restrict__ d2h_in,
+    float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int K, int comp) {
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int64_t per = Bsz * N * D;
-    if (idx >= per * (1 + K)) return;
+    if (idx >= per * comp) return;
     const int64_t c = idx / per, r = idx % per;
     const int64_t d = r % D, n = (r / D) % N, b = r / (N * D);
     float v = 0.0f;
     if (c == 0) {
         if (h_in) v = h_in[(b * D + d) * N + n];
-    } else if (dh_in) {
-        v = dh_in[(((c - 1) * Bsz + b) * D + d) * N + n];
+    } else if (c <= K) {
+        if (dh_in) v = dh_in[(((c - 1) * Bsz + b) * D + d) * N + n];
+    } else if (d2h_in) {
+        v = d2h_in[(b * D + d) * N + n];
     }
     state[idx] = v;
 }
 
 __global__ __launch_bounds__(kThreads) void k_state_export(
     const float *__restrict__ state, float *__restrict__ h_out, float *__restrict__ dh_out,
-    int64_t Bsz, int64_t D, int64_t N, int K) {
+    float *__restrict__ d2h_out, int64_t Bsz, int64_t D, int64_t N, int K, int comp) {
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int64_t per = Bsz * N * D;
-    if (idx >= per * (1 + K)) return;
+    if (idx >= per * comp) return;
     const int64_t c = idx / per, r = idx % per;
     const int64_t d = r % D, n = (r / D) % N, b = r / (N * D);
     if (c == 0) {
         if (h_out) h_out[(b * D + d) * N + n] = state[idx];
-    } else if (dh_out) {
-        dh_out[(((c - 1) * Bsz + b) * D + d) * N + n] = state[idx];
+    } else if (c <= K) {
+        if (dh_out) dh_out[(((c - 1) * Bsz + b) * D + d) * N + n] = state[idx];
+    } else if (d2h_out) {
+        d2h_out[(b * D + d) * N + n] = state[idx];
     }
 }
 
@@ -843,6 +1107,7 @@ struct Launcher {
     const InT *x;
     const InT *dx;
     float *y, *dy;
+    float *d2y;        // second order only
     hipStream_t st;
     char *ws;
 
@@ -942,7 +1207,51 @@ struct Launcher {
         }
     }
 
+    // Second order: one thread per channel with all N <= 16 states.
+    template <int NT>
+    void scans2(int64_t t0, int64_t len) {
+        const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
+        const int64_t ND = q.N * q.D;
+        if (q.seg == 0) {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_scan2<NT, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, dx, p.A,
+                               p.w_delta, p.b_delta, bcw(), state(), ND, (int64_t)0, q.B * ND, y, dy, d2y, state(),
+                               (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, len, 1);
+            return;
+        }
+        const int G = (int)((len + q.seg - 1) / q.seg);
+        {
+            Timed tm(1, st);
+            hipLaunchKernelGGL((k_scan2<NT, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
+                               x, dx, p.A, p.w_delta, p.b_delta, bcw(), (const float *)nullptr, (int64_t)0, (int64_t)0,
+                               (int64_t)0, y, dy, d2y, (float *)nullptr, agg_h(), agg_s(), q.B, q.L, q.D, t0, len,
+                               q.chunk_len, (int64_t)q.seg, G);
+        }
+        {
+            const int64_t lanes = q.B * ND;
+            Timed tm(2, st);
+            hipLaunchKernelGGL(k_carry2, dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
+                               p.A, agg_h(), agg_s(), state(), q.B, q.D, q.N, G);
+        }
+        {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_scan2<NT, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
+                               x, dx, p.A, p.w_delta, p.b_delta, bcw(), seg_in(), (int64_t)G * 4 * ND, (int64_t)4 * ND,
+                               ND, y, dy, d2y, (float *)nullptr, (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0,
+                               len, q.chunk_len, (int64_t)q.seg, G);
+        }
+    }
+
     bool scan_block(int64_t t0, int64_t len) {
+        if (q.order == 2) {
+            if (q.ns != 1) return false;
+            switch (q.nt) {
+                case 4: scans2<4>(t0, len); return true;
+                case 8: scans2<8>(t0, len); return true;
+                case 16: scans2<16>(t0, len); return true;
+                default: return false;
+            }
+        }
         switch (q.K) {
             case 1: return scan_block_k<1>(t0, len);
             case 2: return scan_block_k<2>(t0, len);
@@ -953,22 +1262,24 @@ struct Launcher {
     }
 
     int run() {
-        const int64_t lanes_all = (1 + q.K) * q.B * q.N * q.D;
+        const int64_t lanes_all = (int64_t)q.comp * q.B * q.N * q.D;
         const unsigned gs = (unsigned)((lanes_all + kThreads - 1) / kThreads);
+        const float *d2h_in = q.order == 2 ? p.d2h_in : nullptr;
+        float *d2h_out = q.order == 2 ? p.d2h_out : nullptr;
         {
             Timed tm(4, st);
-            hipLaunchKernelGGL(k_state_import, dim3(gs), dim3(kThreads), 0, st, p.h_in, p.dh_in, state(), q.B, q.D,
-                               q.N, (int)q.K);
+            hipLaunchKernelGGL(k_state_import, dim3(gs), dim3(kThreads), 0, st, p.h_in, p.dh_in, d2h_in, state(), q.B,
+                               q.D, q.N, (int)q.K, q.comp);
         }
         for (int64_t t0 = 0; t0 < q.L; t0 += q.chunk_len) {
             const int64_t len = q.L - t0 < q.chunk_len ? q.L - t0 : q.chunk_len;
             proj(t0, len);
             if (!scan_block(t0, len)) return PGF_ERR_UNSUPPORTED;
         }
-        if (p.h_out || p.dh_out) {
+        if (p.h_out || p.dh_out || d2h_out) {
             Timed tm(4, st);
-            hipLaunchKernelGGL(k_state_export, dim3(gs), dim3(kThreads), 0, st, state(), p.h_out, p.dh_out, q.B, q.D,
-                               q.N, (int)q.K);
+            hipLaunchKernelGGL(k_state_export, dim3(gs), dim3(kThreads), 0, st, state(), p.h_out, p.dh_out, d2h_out,
+                               q.B, q.D, q.N, (int)q.K, q.comp);
         }
         return hipGetLastError() == hipSuccess ? PGF_OK : PGF_ERR_HIP;
     }
@@ -983,11 +1294,14 @@ bool overlap(const void *a, size_t na, const void *b, size_t nb) {
 
 }  // namespace pgf
 
-extern "C" int pgf_scan_jvp(const void *x, const void *dx, const pgf_params *p, float *y, float *dy, void *stream) {
-    using namespace pgf;
+namespace pgf {
+namespace {
+int scan_common(const void *x, const void *dx, const pgf_params *p, float *y, float *dy, float *d2y,
+                void *stream, int order) {
     Plan q;
     const int rc = make_plan(p, &q);
     if (rc != PGF_OK) return rc;
+    if (q.order != order) return PGF_ERR_INVALID_ARG;
     if (!p->A || !p->w_delta || !p->b_delta || !p->W_B || !p->W_C) return PGF_ERR_INVALID_ARG;
     if (!p->workspace || p->workspace_bytes < q.ws.total || ((uintptr_t)p->workspace & 255))
         return PGF_ERR_WORKSPACE;
@@ -995,22 +1309,36 @@ extern "C" int pgf_scan_jvp(const void *x, const void *dx, const pgf_params *p, 
     const size_t nx = (size_t)q.B * q.L * q.D;
     const size_t bx = nx * esz, bdx = nx * q.K * esz, by = nx * 4, bdy = nx * q.K * 4;
     if (q.L > 0) {
-        if (!x || !dx || !y || !dy) return PGF_ERR_INVALID_ARG;
+        if (!x || !dx || !y || !dy || (order == 2 && !d2y)) return PGF_ERR_INVALID_ARG;
         if (overlap(y, by, x, bx) || overlap(y, by, dx, bdx) || overlap(dy, bdy, x, bx) ||
             overlap(dy, bdy, dx, bdx) || overlap(y, by, dy, bdy))
             return PGF_ERR_INVALID_ARG;
         if (overlap(p->workspace, q.ws.total, y, by) || overlap(p->workspace, q.ws.total, dy, bdy))
+            return PGF_ERR_INVALID_ARG;
+        if (order == 2 && (overlap(d2y, by, x, bx) || overlap(d2y, by, dx, bdx) || overlap(d2y, by, y, by) ||
+                           overlap(d2y, by, dy, bdy) || overlap(d2y, by, p->workspace, q.ws.total)))
             return PGF_ERR_INVALID_ARG;
     }
     // Clear any stale error from earlier, unrelated work on this thread.
     (void)hipGetLastError();
     hipStream_t st = (hipStream_t)stream;
     if (q.in_bf16) {
-        Launcher<uint16_t> l{q, *p, (const uint16_t *)x, (const uint16_t *)dx, y, dy, st, (char *)p->workspace};
+        Launcher<uint16_t> l{q, *p, (const uint16_t *)x, (const uint16_t *)dx, y, dy, d2y, st, (char *)p->workspace};
         return l.run();
     }
-    Launcher<float> l{q, *p, (const float *)x, (const float *)dx, y, dy, st, (char *)p->workspace};
+    Launcher<float> l{q, *p, (const float *)x, (const float *)dx, y, dy, d2y, st, (char *)p->workspace};
     return l.run();
+}
+}  // namespace
+}  // namespace pgf
+
+extern "C" int pgf_scan_jvp(const void *x, const void *dx, const pgf_params *p, float *y, float *dy, void *stream) {
+    return pgf::scan_common(x, dx, p, y, dy, nullptr, stream, 1);
+}
+
+extern "C" int pgf_scan_jvp2(const void *x, const void *dx, const pgf_params *p, float *y, float *dy, float *d2y,
+                             void *stream) {
+    return pgf::scan_common(x, dx, p, y, dy, d2y, stream, 2);
 }
 
 extern "C" int pgf_timing_enable(int on) {

@@ -15,7 +15,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def _declared_functions():
     with open(os.path.join(ROOT, "include", "pgf.h")) as f:
         txt = f.read()
-    return sorted(set(re.findall(r"\b(pgf_[a-z_]+)\s*\(", txt)))
+    return sorted(set(re.findall(r"\b(pgf_[a-z0-9_]+)\s*\(", txt)))
 
 
 def test_library_exports_every_declared_symbol():
