@@ -95,7 +95,8 @@ def summarize_counters(workload, order, fetch_csv, write_csv, out_path=None):
                 if v > calib.get(counter, 0.0):
                     calib[counter] = v        # the 1 GiB copy is the largest copy dispatch
                 continue
-            per.setdefault(lab, {}).setdefault(counter, []).append(v)
+            if lab in ("proj", "seg_aggregate", "carry", "scan_out", "state_io"):
+                per.setdefault(lab, {}).setdefault(counter, []).append(v)
     label = workload + ("-order2" if order == 2 else "")
     opt = " --order 2" if order == 2 else ""
     out = {"workload": label, "source_sha256": source_digest(),
@@ -113,7 +114,7 @@ def summarize_counters(workload, order, fetch_csv, write_csv, out_path=None):
                                "dispatches": len(c.get("FETCH_SIZE", [])),
                                "hbm_bytes_per_dispatch": int(f * 1024 / ff + w * 1024 / wf)}
     out["commands"] = [
-        f"rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pmc_{workload}_{c} -o pmc -- "
+        f"rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pmc_{label}_{c} -o pmc -- "
         f"python3 -u bench.py --workload {workload}{opt} --steps 2 --warmup 1 --no-cpu --calib-copy"
         for c in ("FETCH_SIZE", "WRITE_SIZE")]
     path = out_path or os.path.join(ROOT, "profiles", f"traffic_{label}.json")

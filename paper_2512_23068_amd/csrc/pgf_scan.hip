@@ -726,7 +726,7 @@ constexpr auto scan_kernel() {
 // (same operation order as k_scan, so y, dy match the first-order kernel)
 // and the mixed flow (App. G):
 //   hvw' = Abar hvw + Abar_w hv + Abar_v hw + Abar_vw h + b_vw
-// with Abar_v h = (A Abar h) dv, Abar_vw h = (A Abar h)(A dv dw + dvw) and
+// with Abar_v = A Abar dv, Abar_vw = A Abar (A dv dw + dvw) and
 // b_vw = B q + dBv pw + dBw pv,  q = dvw x + dv xw + dw xv,
 // pv = dv x + Delta xv, pw = dw x + Delta xw.  Layouts and grid as k_scan
 // with 4 state components (h, hv, hw, hvw).
@@ -740,7 +740,7 @@ __global__ __launch_bounds__(kThreads) void k_scan2(
     int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
     constexpr int N = NT;
     constexpr int R = 6 * N;          // B, dBv, dBw, C, dCv, dCw
-    constexpr int TT = 8;
+    constexpr int TT = NT >= 16 ? 4 : 8;   // prefetch depth, bounded by the VGPR budget
 
     const int tid = threadIdx.x;
     const int64_t d_raw = (int64_t)blockIdx.x * kThreads + tid;
@@ -835,13 +835,12 @@ __global__ __launch_bounds__(kThreads) void k_scan2(
                     const float sv = a * h[i];
                     const float gv = Af[i] * sv;
                     const float hn = fmaf(Bn, u, sv);
-                    const float g1 = Af[i] * (a * hv[i]);
-                    const float g2 = Af[i] * (a * hw[i]);
+                    // Abar_w hv + Abar_v hw + Abar_vw h = (A Abar)(dw hv + dv hw + cvw h)
+                    const float cvw = fmaf(Af[i], c1, dvw);
+                    const float cross = fmaf(dw, hv[i], fmaf(dv, hw[i], cvw * h[i]));
+                    const float hvwn = fmaf(a, hvw[i], fmaf(Af[i] * a, cross, fmaf(Bn, q, fmaf(dBv, pw, dBw * pv))));
                     const float hvn = fmaf(a, hv[i], fmaf(gv, dv, fmaf(Bn, pv, dBv * u)));
                     const float hwn = fmaf(a, hw[i], fmaf(gv, dw, fmaf(Bn, pw, dBw * u)));
-                    const float cvw = fmaf(Af[i], c1, dvw);
-                    const float hvwn = fmaf(a, hvw[i],
-                                            fmaf(g1, dw, fmaf(g2, dv, fmaf(gv, cvw, fmaf(Bn, q, fmaf(dBv, pw, dBw * pv))))));
                     h[i] = hn;
                     hv[i] = hvn;
                     hw[i] = hwn;
@@ -909,7 +908,7 @@ __global__ __launch_bounds__(kThreads) void k_scan2(
 __global__ __launch_bounds__(kThreads) void k_carry2(
     const float *__restrict__ A, float *__restrict__ seg, const float *__restrict__ agg_s,
     float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int G) {
-    constexpr int GB = 8;
+    constexpr int GB = 16;
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int64_t ND = N * D;
     if (idx >= Bsz * ND) return;
@@ -921,16 +920,19 @@ __global__ __launch_bounds__(kThreads) void k_carry2(
     float h = state[b * ND + lane], hv = state[cs + b * ND + lane];
     float hw = state[2 * cs + b * ND + lane], hvw = state[3 * cs + b * ND + lane];
     for (int g0 = 0; g0 < G; g0 += GB) {
-        float e[GB][4], sm[GB][4];
+        float e0[GB], e1[GB], e2[GB], e3[GB], s0[GB], s1[GB], s2[GB], s3[GB];
 #pragma unroll
         for (int j = 0; j < GB; ++j) {
             const int g = g0 + j < G ? g0 + j : G - 1;
             const int64_t base = (b * G + g) * 4;
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                e[j][c] = seg[(base + c) * ND + lane];
-                sm[j][c] = agg_s[(base + c) * D + d];
-            }
+            e0[j] = seg[base * ND + lane];
+            e1[j] = seg[(base + 1) * ND + lane];
+            e2[j] = seg[(base + 2) * ND + lane];
+            e3[j] = seg[(base + 3) * ND + lane];
+            s0[j] = agg_s[base * D + d];
+            s1[j] = agg_s[(base + 1) * D + d];
+            s2[j] = agg_s[(base + 2) * D + d];
+            s3[j] = agg_s[(base + 3) * D + d];
         }
 #pragma unroll
         for (int j = 0; j < GB; ++j) {
@@ -940,14 +942,14 @@ __global__ __launch_bounds__(kThreads) void k_carry2(
             seg[(base + 1) * ND + lane] = hv;
             seg[(base + 2) * ND + lane] = hw;
             seg[(base + 3) * ND + lane] = hvw;
-            const float P = __builtin_amdgcn_exp2f(at * sm[j][0]);
-            const float asv = a * sm[j][1], asw = a * sm[j][2];
+            const float P = __builtin_amdgcn_exp2f(at * s0[j]);
+            const float asv = a * s1[j], asw = a * s2[j];
             const float Pv = P * asv, Pw = P * asw;
-            const float Pvw = P * fmaf(asv, asw, a * sm[j][3]);
-            const float hvw1 = fmaf(P, hvw, fmaf(Pw, hv, fmaf(Pv, hw, fmaf(Pvw, h, e[j][3]))));
-            const float hv1 = fmaf(P, hv, fmaf(Pv, h, e[j][1]));
-            const float hw1 = fmaf(P, hw, fmaf(Pw, h, e[j][2]));
-            h = fmaf(P, h, e[j][0]);
+            const float Pvw = P * fmaf(asv, asw, a * s3[j]);
+            const float hvw1 = fmaf(P, hvw, fmaf(Pw, hv, fmaf(Pv, hw, fmaf(Pvw, h, e3[j]))));
+            const float hv1 = fmaf(P, hv, fmaf(Pv, h, e1[j]));
+            const float hw1 = fmaf(P, hw, fmaf(Pw, h, e2[j]));
+            h = fmaf(P, h, e0[j]);
             hv = hv1;
             hw = hw1;
             hvw = hvw1;
