@@ -19,6 +19,9 @@ Layers
 * ``core2`` / ``discretize2`` / ``scan_jvp2``: the second-order flow of
   App. G (mixed second directional derivative along two input directions
   v, w, with both first-order flows), same layering.
+* ``core_param`` / ``param_grads``: the parameter-sensitivity flows and the
+  online gradient accumulation of App. E (Alg. 2) for a given adjoint
+  signal dl/dy, same layering.
 
 Precision: everything in fp64 from the exact fp32 / bf16 input values.
 Library routines used as steps: numpy.logaddexp (softplus), scipy expit
@@ -63,6 +66,8 @@ def _load():
     lib.pgf_oracle_core.argtypes = [i64] * 5 + [dp] * 13 + [ctypes.c_int]
     lib.pgf_oracle_core2.restype = ctypes.c_int
     lib.pgf_oracle_core2.argtypes = [i64] * 4 + [dp] * 22 + [ctypes.c_int]
+    lib.pgf_oracle_param.restype = ctypes.c_int
+    lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 13 + [ctypes.c_int]
     _lib = lib
     return lib
 
@@ -246,3 +251,62 @@ def scan_jvp2(x, dxv, dxw, params, state=None, channels=None, chunk=None, nthrea
         for i in range(4):
             outs[i][:, t0:t1] = o[i]
     return tuple(outs), st
+
+
+# ------------------------------------------------------------------ parameter flows
+
+def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None):
+    """Parameter-sensitivity flows (see pgf_oracle_param).  Shapes: A [D,N];
+    x, delta, gy [B,L,D]; Bm, Cm [B,L,N]; state = (h, GammaA, GammaB), each
+    [B,D,N] (zero when None).  Returns y [B,L,D], (GA, GB, GC) each [B,D,N]
+    (this call's contributions per batch row) and the exit state tuple."""
+    lib = _load()
+    A = _f64(A)
+    x, delta, gy, Bm, Cm = (_f64(a) for a in (x, delta, gy, Bm, Cm))
+    B, L, D = x.shape
+    N = A.shape[1]
+    assert delta.shape == (B, L, D) and gy.shape == (B, L, D)
+    assert Bm.shape == (B, L, N) and Cm.shape == (B, L, N)
+    if state is None:
+        st = [np.zeros((B, D, N)) for _ in range(3)]
+    else:
+        st = [np.array(s, dtype=np.float64, copy=True, order="C") for s in state]
+    for s_ in st:
+        assert s_.shape == (B, D, N)
+    y = np.empty((B, L, D))
+    G = [np.zeros((B, D, N)) for _ in range(3)]
+    rc = lib.pgf_oracle_param(B, L, D, N, _dp(A), _dp(x), _dp(delta), _dp(gy), _dp(Bm), _dp(Cm),
+                              *[_dp(s_) for s_ in st], _dp(y), *[_dp(g) for g in G],
+                              _threads() if nthreads is None else nthreads)
+    if rc != 0:
+        raise RuntimeError("pgf_oracle_param failed")
+    return y, tuple(G), tuple(st)
+
+
+def param_grads(x, gy, params, state=None, chunk=None, nthreads=None):
+    """Primal output and online parameter gradients of the full model over
+    L-chunks (App. E, Alg. 2).  x, gy [B,L,D]; params as scan_jvp.
+
+    Returns (y [B,L,D], (G_A, G_B, G_C) each [D,N] summed over the batch,
+    exit state (h, GammaA, GammaB) each [B,D,N]).  G_A = dl/dA; G_B and G_C
+    are the gradients with respect to per-lane offsets of B and C, so that
+    dl/db_B = G_B.sum(0) and dl/db_C = G_C.sum(0)."""
+    B, L, D = np.shape(x)
+    A = _f64(params["A"])
+    N = A.shape[1]
+    y = np.empty((B, L, D))
+    tot = [np.zeros((B, D, N)) for _ in range(3)]
+    st = state
+    step = max(1, L if not chunk else int(chunk))
+    for t0 in range(0, L, step):
+        t1 = min(L, t0 + step)
+        xc = _f64(x[:, t0:t1])
+        Bm, Cm, _, _ = project(xc, xc[None], params["W_B"], params["W_C"], params.get("b_B"), params.get("b_C"))
+        delta, _ = discretize(xc, xc[None], params["w_delta"], params["b_delta"])
+        yc, G, st = core_param(A, xc, delta, _f64(gy[:, t0:t1]), Bm, Cm, st, nthreads)
+        y[:, t0:t1] = yc
+        for i in range(3):
+            tot[i] += G[i]
+    if st is None:
+        st = tuple(np.zeros((B, D, N)) for _ in range(3))
+    return y, tuple(g.sum(0) for g in tot), st

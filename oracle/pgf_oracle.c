@@ -211,3 +211,72 @@ int pgf_oracle_core2(int64_t B, int64_t L, int64_t D, int64_t N,
     }
     return 0;
 }
+
+/*
+ * Parameter-sensitivity flows with online gradient accumulation (App. E,
+ * Alg. 2): for a scalar loss l whose adjoint signal gy[t] = dl/dy[t] is
+ * given, the gradients of l with respect to the transition parameter A and
+ * to per-lane, time-invariant offsets of the input and output maps B and C
+ * are accumulated in the same forward pass as the primal, keeping only the
+ * current state.  Per lane (b, d, n), sequentially in t:
+ *
+ *   Abar    = exp(Delta*A)
+ *   GammaA' = Abar*GammaA + Delta*Abar*h        dh/dA: d(Abar)/dA = Delta*Abar;
+ *                                              the Euler drive Delta*B*x has
+ *                                              no A in it
+ *   GammaB' = Abar*GammaB + Delta*x             dh/dB: d(Delta*B*x)/dB
+ *   h'      = Abar*h + Delta*B*x
+ *   y       = sum_n C*h'                        (identity activation)
+ *   GA     += gy*C*GammaA'                      dy/dh' = C, chain rule into A
+ *   GB     += gy*C*GammaB'
+ *   GC     += gy*h'                             dy/dC = h' (outer product)
+ *
+ * GammaA and GammaB use the state before the step (h), h' the state after.
+ * Shapes (double, row-major): A [D,N]; x, delta, gy [B,L,D];
+ * Bm, Cm [B,L,N]; h, gA, gB [B,D,N] (entry state in, exit state out);
+ * y [B,L,D] (written); GA, GB, GC [B,D,N] (added to, per batch row).
+ * Returns 0, or -1 on a bad argument.
+ */
+int pgf_oracle_param(int64_t B, int64_t L, int64_t D, int64_t N,
+                     const double *A, const double *x, const double *delta, const double *gy,
+                     const double *Bm, const double *Cm,
+                     double *h, double *gA, double *gB,
+                     double *y, double *GA, double *GB, double *GC, int nthreads)
+{
+    if (B < 0 || L < 0 || D < 0 || N <= 0) return -1;
+    if (!A || !h || !gA || !gB || !GA || !GB || !GC) return -1;
+    if (L > 0 && (!x || !delta || !gy || !Bm || !Cm || !y)) return -1;
+    const int64_t lanes = B * D;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t lane = 0; lane < lanes; ++lane) {
+        const int64_t b = lane / D, d = lane % D;
+        for (int64_t t = 0; t < L; ++t) {
+            const int64_t btd = (b * L + t) * D + d;
+            const int64_t btn = (b * L + t) * N;
+            const double xt = x[btd], dl = delta[btd], g = gy[btd];
+            double yt = 0.0;
+            for (int64_t n = 0; n < N; ++n) {
+                const int64_t i = (b * D + d) * N + n;
+                const double abar = exp(dl * A[d * N + n]);
+                const double hprev = h[i];
+                const double ga = abar * gA[i] + dl * abar * hprev;
+                const double gb = abar * gB[i] + dl * xt;
+                const double hnew = abar * hprev + dl * Bm[btn + n] * xt;
+                h[i] = hnew; gA[i] = ga; gB[i] = gb;
+                const double Ct = Cm[btn + n];
+                yt += Ct * hnew;
+                GA[i] += g * Ct * ga;
+                GB[i] += g * Ct * gb;
+                GC[i] += g * hnew;
+            }
+            y[btd] = yt;
+        }
+    }
+    return 0;
+}

@@ -1,0 +1,83 @@
+"""Plants plausible mistakes in the parameter-flow oracle (on the CPU) and
+checks that the pins of test_oracle_param_pins.py catch each one."""
+import ctypes
+import os
+import subprocess
+import tempfile
+
+import pytest
+
+from oracle import oracle
+import tests.test_oracle_param_pins as pins
+
+PIN_TESTS = [
+    lambda: pins.test_reverse_mode_autograd(40, False),
+    lambda: pins.test_central_differences_of_the_primal(),
+    lambda: pins.test_time_invariant_closed_form(),
+    lambda: pins.test_one_step_adjoint_is_the_outer_product(),
+    lambda: pins.test_segment_composition_closed_forms(),
+]
+
+C_MUTANTS = {
+    "GammaA without its drive": ("const double ga = abar * gA[i] + dl * abar * hprev;",
+                                 "const double ga = abar * gA[i];"),
+    "GammaA drive without Abar": ("const double ga = abar * gA[i] + dl * abar * hprev;",
+                                  "const double ga = abar * gA[i] + dl * hprev;"),
+    "GammaA drive from the new state": ("const double ga = abar * gA[i] + dl * abar * hprev;",
+                                        "const double ga = abar * gA[i] + dl * (abar * hprev + dl * Bm[btn + n] * xt);"),
+    "GammaB drive carries B": ("const double gb = abar * gB[i] + dl * xt;",
+                               "const double gb = abar * gB[i] + dl * Bm[btn + n] * xt;"),
+    "GammaB without decay": ("const double gb = abar * gB[i] + dl * xt;", "const double gb = gB[i] + dl * xt;"),
+    "G_C from the old state": ("GC[i] += g * hnew;", "GC[i] += g * hprev;"),
+    "G_A without C": ("GA[i] += g * Ct * ga;", "GA[i] += g * ga;"),
+    "G_B from GammaA": ("GB[i] += g * Ct * gb;", "GB[i] += g * Ct * ga;"),
+}
+
+
+def _caught():
+    for t in PIN_TESTS:
+        try:
+            t()
+        except AssertionError:
+            return True
+    return False
+
+
+def test_unmutated_oracle_passes_all_pins():
+    assert not _caught()
+
+
+@pytest.mark.parametrize("name", sorted(C_MUTANTS))
+def test_c_mutant_is_caught(name, monkeypatch):
+    with open(oracle._SRC) as f:
+        src = f.read()
+    old, new = C_MUTANTS[name]
+    assert src.count(old) == 1, name
+    with tempfile.TemporaryDirectory() as td:
+        c, so = os.path.join(td, "m.c"), os.path.join(td, "m.so")
+        with open(c, "w") as f:
+            f.write(src.replace(old, new))
+        subprocess.run(["gcc", "-O2", "-fno-fast-math", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
+                        "-o", so, c, "-lm"], check=True)
+        lib = ctypes.CDLL(so)
+        dp = ctypes.POINTER(ctypes.c_double)
+        i64 = ctypes.c_int64
+        lib.pgf_oracle_core.restype = ctypes.c_int
+        lib.pgf_oracle_core.argtypes = [i64] * 5 + [dp] * 13 + [ctypes.c_int]
+        lib.pgf_oracle_core2.restype = ctypes.c_int
+        lib.pgf_oracle_core2.argtypes = [i64] * 4 + [dp] * 22 + [ctypes.c_int]
+        lib.pgf_oracle_param.restype = ctypes.c_int
+        lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 13 + [ctypes.c_int]
+        monkeypatch.setattr(oracle, "_lib", lib)
+        assert _caught(), name
+
+
+def test_python_mutant_is_caught(monkeypatch):
+    """The projections of the parameter path without the bias of B."""
+    orig = oracle.project
+
+    def no_bias(x, dx, W_B, W_C, b_B=None, b_C=None):
+        return orig(x, dx, W_B, W_C, None, b_C)
+
+    monkeypatch.setattr(oracle, "project", no_bias)
+    assert _caught()

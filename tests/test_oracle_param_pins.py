@@ -1,0 +1,167 @@
+"""Pins of the parameter-flow oracle (App. E, Alg. 2: sensitivity flows of
+A and of per-lane offsets of B and C, accumulated against an adjoint
+signal) against facts that do not come from its own formula: reverse-mode
+autograd of an independent torch loop, central differences of the
+separately pinned primal, a closed form for a time-invariant system, the
+outer-product form of G_C at a one-step adjoint, and the segment
+composition the GPU carry uses."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from tests.test_oracle_pins import rand_problem, relerr
+
+
+@pytest.fixture(autouse=True)
+def _float64_default():
+    old = torch.get_default_dtype()
+    torch.set_default_dtype(torch.float64)
+    yield
+    torch.set_default_dtype(old)
+
+
+def problem(seed, B=2, L=14, D=3, N=4, stiff=False):
+    p, x, _ = rand_problem(seed, B=B, L=L, D=D, N=N, K=1, stiff=stiff, bias=True)
+    gy = np.random.default_rng(seed + 1000).standard_normal(x.shape)
+    return p, x, gy
+
+
+def _torch_loss(p, x, gy, A, beta_B, beta_C):
+    """l = sum gy*y of the selective scan as a plain torch loop, with the
+    per-lane offsets beta_B, beta_C [D,N] added to B_t and C_t."""
+    xt = torch.tensor(x)
+    z = xt * torch.tensor(p["w_delta"]) + torch.tensor(p["b_delta"])
+    delta = torch.logaddexp(z, torch.zeros((), dtype=torch.float64))
+    Bm = xt @ torch.tensor(p["W_B"]) + torch.tensor(p["b_B"])
+    Cm = xt @ torch.tensor(p["W_C"]) + torch.tensor(p["b_C"])
+    Bsz, L, D = xt.shape
+    h = torch.zeros(Bsz, D, A.shape[1], dtype=torch.float64)
+    loss = torch.zeros((), dtype=torch.float64)
+    for t in range(L):
+        dl = delta[:, t, :, None]
+        Bt = Bm[:, t, None, :] + beta_B
+        Ct = Cm[:, t, None, :] + beta_C
+        h = torch.exp(dl * A) * h + dl * Bt * xt[:, t, :, None]
+        loss = loss + (torch.tensor(gy[:, t]) * (h * Ct).sum(-1)).sum()
+    return loss
+
+
+@pytest.mark.parametrize("seed,stiff", [(40, False), (41, True)])
+def test_reverse_mode_autograd(seed, stiff):
+    p, x, gy = problem(seed, stiff=stiff)
+    y, (GA, GB, GC), _ = oracle.param_grads(x, gy, p)
+    A = torch.tensor(p["A"], requires_grad=True)
+    bB = torch.zeros(p["A"].shape, dtype=torch.float64, requires_grad=True)
+    bC = torch.zeros(p["A"].shape, dtype=torch.float64, requires_grad=True)
+    _torch_loss(p, x, gy, A, bB, bC).backward()
+    assert relerr(GA, A.grad.numpy()) < 1e-12
+    assert relerr(GB, bB.grad.numpy()) < 1e-12
+    assert relerr(GC, bC.grad.numpy()) < 1e-12
+
+
+def _loss_np(p, x, gy):
+    y, _, _, _ = oracle.scan_jvp(x, x[None] * 0.0, p)
+    return float((gy * y).sum())
+
+
+def test_central_differences_of_the_primal():
+    """Directional derivatives of l along A, b_B and b_C from the pinned
+    first-order oracle's primal: <G_A, dA>, <sum_d G_B, db_B>, <sum_d G_C, db_C>."""
+    p, x, gy = problem(42, L=18)
+    _, (GA, GB, GC), _ = oracle.param_grads(x, gy, p)
+    g = np.random.default_rng(43)
+    eps = 1e-6
+    dA = g.standard_normal(p["A"].shape)
+    fd = (_loss_np(dict(p, A=p["A"] + eps * dA), x, gy) - _loss_np(dict(p, A=p["A"] - eps * dA), x, gy)) / (2 * eps)
+    assert abs(fd - (GA * dA).sum()) < 1e-7 * max(1.0, abs(fd))
+    for key, G in (("b_B", GB), ("b_C", GC)):
+        db = g.standard_normal(p[key].shape)
+        fd = (_loss_np(dict(p, **{key: p[key] + eps * db}), x, gy)
+              - _loss_np(dict(p, **{key: p[key] - eps * db}), x, gy)) / (2 * eps)
+        assert abs(fd - (G.sum(0) * db).sum()) < 1e-7 * max(1.0, abs(fd)), key
+
+
+def test_time_invariant_closed_form():
+    """w_delta = 0, W_B = W_C = 0: Delta, B, C constant, h_t = sum_{s<=t}
+    a^(t-s) Delta B x_s with a = exp(Delta A), so dh_t/dA = sum_s (t-s) Delta
+    a^(t-s) Delta B x_s, dh_t/dB = sum_s a^(t-s) Delta x_s."""
+    g = np.random.default_rng(44)
+    D, N, L = 3, 4, 16
+    p = dict(A=-g.uniform(0.1, 2, (D, N)), w_delta=np.zeros(D), b_delta=g.uniform(-2, 1, D),
+             W_B=np.zeros((D, N)), W_C=np.zeros((D, N)), b_B=g.standard_normal(N), b_C=g.standard_normal(N))
+    x = g.standard_normal((1, L, D))
+    gy = g.standard_normal((1, L, D))
+    _, (GA, GB, GC), _ = oracle.param_grads(x, gy, p)
+    dl = np.log1p(np.exp(p["b_delta"]))[:, None]
+    a = np.exp(dl * p["A"])
+    rA = np.zeros((D, N)); rB = np.zeros((D, N)); rC = np.zeros((D, N))
+    for t in range(L):
+        h = np.zeros((D, N)); hA = np.zeros((D, N)); hB = np.zeros((D, N))
+        for s in range(t + 1):
+            k = t - s
+            h += a ** k * dl * p["b_B"] * x[0, s][:, None]
+            hA += k * dl * a ** k * dl * p["b_B"] * x[0, s][:, None]
+            hB += a ** k * dl * x[0, s][:, None]
+        gt = gy[0, t][:, None]
+        rA += gt * p["b_C"] * hA
+        rB += gt * p["b_C"] * hB
+        rC += gt * h
+    assert relerr(GA, rA) < 1e-12 and relerr(GB, rB) < 1e-12 and relerr(GC, rC) < 1e-12
+
+
+def test_one_step_adjoint_is_the_outer_product():
+    """An adjoint at a single (b, t0, d) gives G_C[d] = gy * h_t0[b, d] with
+    h_t0 the state after step t0 from the first-order oracle."""
+    p, x, _ = problem(45, B=2, L=20)
+    t0, b, d = 11, 1, 2
+    gy = np.zeros_like(x)
+    gy[b, t0, d] = 1.7
+    _, (GA, GB, GC), _ = oracle.param_grads(x, gy, p)
+    _, _, h, _ = oracle.scan_jvp(x[:, :t0 + 1], np.zeros((1,) + x[:, :t0 + 1].shape), p)
+    ref = np.zeros_like(GC)
+    ref[d] = 1.7 * h[b, d]
+    assert relerr(GC, ref) < 1e-15
+    assert np.all(GA[np.arange(3) != d] == 0) and np.all(GB[np.arange(3) != d] == 0)
+
+
+def test_linear_in_the_adjoint_and_primal_unchanged():
+    p, x, gy = problem(46)
+    y, G1, _ = oracle.param_grads(x, gy, p)
+    g2 = np.random.default_rng(47).standard_normal(x.shape)
+    _, G2, _ = oracle.param_grads(x, g2, p)
+    _, G12, _ = oracle.param_grads(x, 2.0 * gy - 0.5 * g2, p)
+    for a, b, c in zip(G1, G2, G12):
+        assert relerr(c, 2.0 * a - 0.5 * b) < 1e-13
+    y1, _, _, _ = oracle.scan_jvp(x, np.zeros((1,) + x.shape), p)
+    assert np.array_equal(y, y1)
+    _, G0, _ = oracle.param_grads(x, np.zeros_like(x), p)
+    assert all(np.all(g == 0) for g in G0)
+
+
+def test_segment_composition_closed_forms():
+    """Over a block with S = sum Delta and P = exp(A S), the exit state from
+    entry (h, GA, GB) is (P h + h0, P GA + S P h + GA0, P GB + GB0), with
+    *0 the exit state from a zero start: what the L-parallel carry uses."""
+    p, x, gy = problem(48, L=17)
+    g = np.random.default_rng(49)
+    ent = tuple(g.standard_normal((2, 3, 4)) for _ in range(3))
+    _, _, z = oracle.param_grads(x, gy, p)
+    _, _, e = oracle.param_grads(x, gy, p, state=ent)
+    delta, _ = oracle.discretize(x, x[None], p["w_delta"], p["b_delta"])
+    S = delta.sum(1)[:, :, None]
+    P = np.exp(p["A"][None] * S)
+    assert relerr(e[0], P * ent[0] + z[0]) < 1e-13
+    assert relerr(e[1], P * ent[1] + S * P * ent[0] + z[1]) < 1e-13
+    assert relerr(e[2], P * ent[2] + z[2]) < 1e-13
+
+
+def test_chunked_equals_whole():
+    p, x, gy = problem(50, L=31)
+    y, G, st = oracle.param_grads(x, gy, p)
+    y2, G2, st2 = oracle.param_grads(x, gy, p, chunk=6)
+    assert relerr(y2, y) < 1e-15
+    for a, b in zip(G, G2):
+        assert relerr(b, a) < 1e-14
+    for a, b in zip(st, st2):
+        assert relerr(b, a) < 1e-15
