@@ -36,8 +36,9 @@ def parse():
                     help="condense two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; made with "
                          "--calib-copy) into profiles/traffic_<workload>.json and exit")
     ap.add_argument("--traffic-out", default=None, help="output path of --summarize-counters")
-    ap.add_argument("--order", type=int, default=1, choices=(1, 2),
-                    help="2: second-order flow (two directions, pgf_scan_jvp2)")
+    ap.add_argument("--order", type=int, default=1, choices=(1, 2, 3),
+                    help="2: second-order flow (two directions, pgf_scan_jvp2); "
+                         "3: parameter flows with gradient accumulation (pgf_param_grads)")
     ap.add_argument("--seg-len", type=int, default=0, help="tiling override (0 = library default)")
     ap.add_argument("--chunk-segs", type=int, default=0, help="tiling override (0 = library default)")
     return ap.parse_args()
@@ -50,12 +51,22 @@ def scan_flops_per_lane_step(K, order=1):
     dC*h' + C*dh' (4).  The mixed second-order flow adds Abar*hvw, the two
     cross-talk products A*(Abar*h_v)*dw and A*(Abar*h_w)*dv, the curvature
     (A s)*(A*dv*dw + dvw), the drive B*q + dBv*pw + dBw*pv (19) and its
-    output dCv*hw + dCw*hv + C*hvw (6)."""
+    output dCv*hw + dCw*hv + C*hvw (6).  The parameter flows (order 3, no
+    tangent directions) add Abar*GA + Delta*s (3), Abar*GB + u (2), gy*C (1)
+    and the three accumulations (6)."""
+    if order == 3:
+        return 7 + 12
     return 7 + 11 * K + (25 if order == 2 else 0)
 
 
+SUFFIX = {1: "", 2: "-order2", 3: "-param"}
+METRIC = {1: "primal+JVP scan Gtok·ch/s at L=128k", 2: "primal+JVP+second-order scan Gtok·ch/s",
+          3: "primal+parameter-gradient flows Gtok·ch/s"}
+
+
 COPY_BYTES = 1 << 30
-KERNEL_KIND = {"k_proj": "proj", "k_scan<": None, "k_carry": "carry", "k_state": "state_io"}
+KERNEL_KIND = {"k_proj": "proj", "k_carry": "carry", "k_pcarry": "carry", "k_gsum": "gsum", "k_state": "state_io",
+               "k_gout": "state_io", "k_fill0": "state_io"}
 TRAFFIC_SOURCES = ("paper_2512_23068_amd/csrc/pgf_scan.hip", "paper_2512_23068_amd/csrc/pgf_plan.cpp")
 
 
@@ -71,8 +82,8 @@ def source_digest():
 
 def _kernel_label(name):
     base = name.split("(")[0].replace("void ", "").strip()
-    if "k_scan" in base:
-        # template args <NT, NS, K, OUT, InT>: OUT=true is the scan with outputs
+    if "k_scan" in base or "k_pscan" in base:
+        # the OUT template argument true marks the scan with outputs
         return "scan_out" if ", true," in base else "seg_aggregate"
     for key, lab in KERNEL_KIND.items():
         if key in base and lab:
@@ -95,10 +106,10 @@ def summarize_counters(workload, order, fetch_csv, write_csv, out_path=None):
                 if v > calib.get(counter, 0.0):
                     calib[counter] = v        # the 1 GiB copy is the largest copy dispatch
                 continue
-            if lab in ("proj", "seg_aggregate", "carry", "scan_out", "state_io"):
+            if lab in ("proj", "seg_aggregate", "carry", "gsum", "scan_out", "state_io"):
                 per.setdefault(lab, {}).setdefault(counter, []).append(v)
-    label = workload + ("-order2" if order == 2 else "")
-    opt = " --order 2" if order == 2 else ""
+    label = workload + SUFFIX[order]
+    opt = f" --order {order}" if order != 1 else ""
     out = {"workload": label, "source_sha256": source_digest(),
            "calibration": {"copy_bytes": COPY_BYTES, "FETCH_SIZE_KiB": calib.get("FETCH_SIZE"),
                            "WRITE_SIZE_KiB": calib.get("WRITE_SIZE"),
@@ -155,6 +166,9 @@ def main():
     if args.order == 2:
         # two independent N(0,1) directions on the same workload shape
         cfg = cfg.with_(n_dirs=2, dx_kind="normal")
+    if args.order == 3:
+        # no tangent directions: an N(0,1) adjoint signal instead
+        cfg = cfg.with_(n_dirs=1, dx_kind="zero")
     B, L, D, N, K = cfg.batch, cfg.seqlen, cfg.d_inner, cfg.d_state, cfg.n_dirs
     dev = torch.device("cuda:0")
     t_gen = time.time()
@@ -163,26 +177,35 @@ def main():
           f"{time.time() - t_gen:.1f}s", file=sys.stderr, flush=True)
     tdt = torch.bfloat16 if cfg.in_dtype == "bf16" else torch.float32
     x = torch.from_numpy(inp["x"]).to(dev).to(tdt)
-    dx = torch.from_numpy(inp["dx"]).to(dev).to(tdt)
     params = {k: torch.from_numpy(inp[k]).to(dev) for k in ("A", "w_delta", "b_delta", "W_B", "W_C")}
     s_in = x.element_size()
-    payload = x.numel() * s_in + dx.numel() * s_in + (x.numel() + dx.numel()) * 4
-    del inp
     y = torch.empty((B, L, D), device=dev)
-    dy = torch.empty((K, B, L, D), device=dev)
-    outs = (y, dy)
-    if args.order == 2:
-        outs = outs + (torch.empty((B, L, D), device=dev),)
-        payload += x.numel() * 4
+    if args.order == 3:
+        gy = torch.from_numpy(inputs.make_adjoint(cfg)).to(dev)
+        grads = tuple(torch.zeros((D, N), device=dev) for _ in range(3))
+        payload = x.numel() * s_in + gy.numel() * 4 + y.numel() * 4 + 3 * D * N * 4
+    else:
+        dx = torch.from_numpy(inp["dx"]).to(dev).to(tdt)
+        payload = x.numel() * s_in + dx.numel() * s_in + (x.numel() + dx.numel()) * 4
+        dy = torch.empty((K, B, L, D), device=dev)
+        outs = (y, dy)
+        if args.order == 2:
+            outs = outs + (torch.empty((B, L, D), device=dev),)
+            payload += x.numel() * 4
+    del inp
     plan = binding.plan(B, L, D, N, K, cfg.in_dtype, args.seg_len, args.chunk_segs, args.order)
     ws = torch.empty(plan["workspace_bytes"], device=dev, dtype=torch.uint8)
     torch.cuda.synchronize()
-    base_alloc = torch.cuda.memory_allocated()
 
-    fn = binding.scan_jvp2 if args.order == 2 else binding.scan_jvp
+    if args.order == 3:
+        def step():
+            binding.param_grads(x, gy, params, grads=grads, workspace=ws, out=y, seg_len=args.seg_len,
+                                chunk_segs=args.chunk_segs)
+    else:
+        fn = binding.scan_jvp2 if args.order == 2 else binding.scan_jvp
 
-    def step():
-        fn(x, dx, params, workspace=ws, out=outs, seg_len=args.seg_len, chunk_segs=args.chunk_segs)
+        def step():
+            fn(x, dx, params, workspace=ws, out=outs, seg_len=args.seg_len, chunk_segs=args.chunk_segs)
 
     for _ in range(args.warmup):
         step()
@@ -219,7 +242,10 @@ def main():
 
     tokch = B * L * D
     value = tokch / (ms_step * 1e-3) / 1e9
-    alg_bytes = tokch * ((1 + K) * (s_in + 4) + (4 if args.order == 2 else 0))
+    if args.order == 3:
+        alg_bytes = tokch * (s_in + 4 + 4)    # read x and gy, write y
+    else:
+        alg_bytes = tokch * ((1 + K) * (s_in + 4) + (4 if args.order == 2 else 0))
     # Dominant kernel: the scan that writes the outputs (kind 3).  Per launch
     # it performs the whole of the algorithmic IO of its block (x, dx read
     # once, y, dy written once) and the whole per-lane arithmetic.
@@ -238,7 +264,7 @@ def main():
         "peak": FP32_VECTOR_PEAK_TFLOPS,
         "unit": "TFLOP/s",
         "frac": round(tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
-        "traffic": committed_traffic(cfg.name + ("-order2" if args.order == 2 else ""), "scan_out"),
+        "traffic": committed_traffic(cfg.name + SUFFIX[args.order], "scan_out"),
         "hbm_achieved_gbs": round(hbm_gbs, 1),
         "hbm_frac": round(hbm_gbs / HBM_PEAK_GBS, 4),
         "avg_launch_ms": round(so_avg_ms, 5),
@@ -251,7 +277,7 @@ def main():
     if args.calib_copy:
         # A plain copy of known size: what the HBM counters read for it
         # calibrates FETCH_SIZE / WRITE_SIZE against true bytes.
-        del y, dy, ws
+        del y, ws
         torch.cuda.empty_cache()
         src = torch.ones(1 << 28, device=dev, dtype=torch.float32)
         dst = torch.empty_like(src)
@@ -265,8 +291,7 @@ def main():
         cpu = cpu_baseline(cfg, args.cpu_steps)
 
     out = {
-        "metric": "primal+JVP scan Gtok·ch/s at L=128k" if args.order == 1
-                  else "primal+JVP+second-order scan Gtok·ch/s",
+        "metric": METRIC[args.order],
         "value": round(value, 3),
         "unit": "Gtok·ch/s",
         "n_gpus": 1,
@@ -277,9 +302,10 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32" if cfg.in_dtype == "f32" else "bf16-in/f32",
-        "data": "synthetic (seeded; BASELINE recipe)",
-        "config": {"workload": cfg.name + ("-order2" if args.order == 2 else ""), "batch": B, "seq_len": L, "d_inner": D, "d_state": N, "n_dirs": K,
-                   "in_dtype": cfg.in_dtype, "parallelism": "single GPU"},
+        "data": "synthetic (seeded workload recipe)",
+        "config": {"workload": cfg.name + SUFFIX[args.order], "batch": B, "seq_len": L, "d_inner": D,
+                   "d_state": N, "n_dirs": 0 if args.order == 3 else K, "in_dtype": cfg.in_dtype,
+                   "parallelism": "single GPU"},
         "hbm_gbs_path": round(alg_bytes / (ms_step * 1e-3) / 1e9, 1),
         "hbm_frac_path": round(alg_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "vram": {"peak_bytes": int(peak), "payload_bytes": int(payload), "workspace_bytes": plan["workspace_bytes"],

@@ -87,9 +87,10 @@ typedef struct pgf_params {
      * Results are bit-identical for every chunk_segs at a fixed seg_len. */
     int32_t seg_len;
     int32_t chunk_segs;
-    /* 0 or 1: first order (pgf_scan_jvp).  2: second order (pgf_scan_jvp2,
-     * which needs n_dirs == 2 and N <= 16).  Read by the planning calls too:
-     * the second order carries one more state per lane. */
+    /* Which flows a call carries; read by the planning calls too.
+     *   0 or 1: first order (pgf_scan_jvp).
+     *   2: second order (pgf_scan_jvp2; needs n_dirs == 2 and N <= 16).
+     *   3: parameter flows (pgf_param_grads; N <= 16; n_dirs is not read). */
     int32_t order;
     /* Model parameters (device, f32).  b_B / b_C may be NULL (= 0). */
     const float *A, *w_delta, *b_delta, *W_B, *W_C, *b_B, *b_C;
@@ -156,6 +157,36 @@ int pgf_scan_jvp(const void *x, const void *dx, const pgf_params *p,
  * conventions as pgf_scan_jvp; d2y must not overlap any other array. */
 int pgf_scan_jvp2(const void *x, const void *dx, const pgf_params *p,
                   float *y, float *dy, float *d2y, void *stream);
+
+/* Parameter-sensitivity flows with online gradient accumulation (App. E,
+ * Alg. 2 "online parameter gradient accumulation").  Given the adjoint
+ * signal gy = dl/dy of a scalar loss l, runs the primal scan and, in the
+ * same pass, the flows of the state's sensitivity to the parameters, per
+ * lane (b, d, n):
+ *   GammaA' = Abar*GammaA + Delta*Abar*h       (dh/dA[d,n]; the Euler drive
+ *                                              Delta*B*x has no A in it)
+ *   GammaB' = Abar*GammaB + Delta*x            (dh/dB for a per-lane offset)
+ *   h'      = Abar*h + Delta*B_t[n]*x,  y = sum_n C_t[n]*h'
+ * and accumulates, over b and t,
+ *   grad_A[d,n] += gy*C_t[n]*GammaA'     = dl/dA
+ *   grad_B[d,n] += gy*C_t[n]*GammaB'     = dl/d(offset of B_t[n] in lane d,n)
+ *   grad_C[d,n] += gy*h'                 = dl/d(offset of C_t[n] in lane d,n)
+ * (the outer product of the adjoint and the state).  Summing grad_B and
+ * grad_C over d gives dl/db_B and dl/db_C.  No trajectory is stored.
+ *   x      : device, [B,L,D] in in_dtype            (read)
+ *   gy     : device, [B,L,D] f32, the adjoint signal (read)
+ *   y      : device, [B,L,D] f32                    (fully overwritten)
+ *   grad_A, grad_B, grad_C : device, [D,N] f32, ADDED to (the caller zeroes
+ *            them before the first call of a sequence)
+ *   stream : a hipStream_t (NULL = the default stream)
+ * p->order must be 3.  State hand-off: h_in/h_out as in pgf_scan_jvp;
+ * dh_in/dh_out hold [GammaA; GammaB] as [2,B,D,N].  Chaining calls through
+ * the state and adding into the same gradients gives the gradients of the
+ * whole sequence (up to the rounding of the additions).  y must not overlap
+ * x or gy; the gradients must not overlap any other array or each other.
+ * Other conventions as pgf_scan_jvp. */
+int pgf_param_grads(const void *x, const float *gy, const pgf_params *p,
+                    float *y, float *grad_A, float *grad_B, float *grad_C, void *stream);
 
 /* Static string for a status code. */
 const char *pgf_status_string(int status);

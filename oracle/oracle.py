@@ -283,30 +283,40 @@ def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None):
     return y, tuple(G), tuple(st)
 
 
-def param_grads(x, gy, params, state=None, chunk=None, nthreads=None):
+def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=None):
     """Primal output and online parameter gradients of the full model over
-    L-chunks (App. E, Alg. 2).  x, gy [B,L,D]; params as scan_jvp.
+    L-chunks (App. E, Alg. 2).  x, gy [B,L,D]; params as scan_jvp; channels:
+    optional 1-D index array of the channels d to compute (the projections
+    still use every channel; state and outputs cover only those).
 
-    Returns (y [B,L,D], (G_A, G_B, G_C) each [D,N] summed over the batch,
-    exit state (h, GammaA, GammaB) each [B,D,N]).  G_A = dl/dA; G_B and G_C
-    are the gradients with respect to per-lane offsets of B and C, so that
-    dl/db_B = G_B.sum(0) and dl/db_C = G_C.sum(0)."""
+    Returns (y [B,L,Dsel], (G_A, G_B, G_C) each [Dsel,N] summed over the
+    batch, exit state (h, GammaA, GammaB) each [B,Dsel,N]).  G_A = dl/dA;
+    G_B and G_C are the gradients with respect to per-lane offsets of B and
+    C, so that dl/db_B = G_B.sum(0) and dl/db_C = G_C.sum(0)."""
     B, L, D = np.shape(x)
     A = _f64(params["A"])
     N = A.shape[1]
-    y = np.empty((B, L, D))
-    tot = [np.zeros((B, D, N)) for _ in range(3)]
+    sel = np.arange(D) if channels is None else np.asarray(channels, dtype=np.int64)
+    Ds = len(sel)
+    w = _f64(params["w_delta"])[sel]
+    bd = _f64(params["b_delta"])[sel]
+    As = A[sel]
+    y = np.empty((B, L, Ds))
+    tot = [np.zeros((B, Ds, N)) for _ in range(3)]
     st = state
     step = max(1, L if not chunk else int(chunk))
     for t0 in range(0, L, step):
         t1 = min(L, t0 + step)
         xc = _f64(x[:, t0:t1])
-        Bm, Cm, _, _ = project(xc, xc[None], params["W_B"], params["W_C"], params.get("b_B"), params.get("b_C"))
-        delta, _ = discretize(xc, xc[None], params["w_delta"], params["b_delta"])
-        yc, G, st = core_param(A, xc, delta, _f64(gy[:, t0:t1]), Bm, Cm, st, nthreads)
+        Bm, Cm, _, _ = project(xc, xc[None, :, :1], params["W_B"], params["W_C"], params.get("b_B"),
+                               params.get("b_C"))
+        xs = np.ascontiguousarray(xc[..., sel])
+        delta, _ = discretize(xs, xs[None], w, bd)
+        gs = np.ascontiguousarray(_f64(gy[:, t0:t1])[..., sel])
+        yc, G, st = core_param(As, xs, delta, gs, Bm, Cm, st, nthreads)
         y[:, t0:t1] = yc
         for i in range(3):
             tot[i] += G[i]
     if st is None:
-        st = tuple(np.zeros((B, D, N)) for _ in range(3))
+        st = tuple(np.zeros((B, Ds, N)) for _ in range(3))
     return y, tuple(g.sum(0) for g in tot), st

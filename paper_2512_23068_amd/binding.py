@@ -46,8 +46,8 @@ class PgfPlanInfo(ctypes.Structure):
     ]
 
 
-EXPORTED = ("pgf_workspace_bytes", "pgf_plan", "pgf_scan_jvp", "pgf_scan_jvp2", "pgf_status_string",
-            "pgf_timing_enable", "pgf_timing_read")
+EXPORTED = ("pgf_workspace_bytes", "pgf_plan", "pgf_scan_jvp", "pgf_scan_jvp2", "pgf_param_grads",
+            "pgf_status_string", "pgf_timing_enable", "pgf_timing_read")
 
 _lib = None
 
@@ -71,6 +71,9 @@ def lib():
     L.pgf_scan_jvp2.restype = ctypes.c_int
     L.pgf_scan_jvp2.argtypes = [ctypes.c_void_p, ctypes.c_void_p, P, ctypes.c_void_p, ctypes.c_void_p,
                                 ctypes.c_void_p, ctypes.c_void_p]
+    L.pgf_param_grads.restype = ctypes.c_int
+    L.pgf_param_grads.argtypes = [ctypes.c_void_p, ctypes.c_void_p, P, ctypes.c_void_p, ctypes.c_void_p,
+                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     L.pgf_status_string.restype = ctypes.c_char_p
     L.pgf_status_string.argtypes = [ctypes.c_int]
     L.pgf_timing_enable.restype = ctypes.c_int
@@ -124,6 +127,31 @@ def _dev_param(v, shape, device, name):
     return v.to(device=device, dtype=torch.float32).contiguous()
 
 
+def _model_params(pr, params, D, dev, keep):
+    """Moves the model parameters to the device as f32 and stores their
+    pointers in pr; returns N."""
+    A = _dev_param(params["A"], (D, params["A"].shape[1]), dev, "A")
+    N = A.shape[1]
+    vals = {"A": A}
+    for name, shape in (("w_delta", (D,)), ("b_delta", (D,)), ("W_B", (D, N)), ("W_C", (D, N)),
+                        ("b_B", (N,)), ("b_C", (N,))):
+        vals[name] = _dev_param(params.get(name), shape, dev, name)
+    for name, v in vals.items():
+        keep.append(v)
+        setattr(pr, name, None if v is None else v.data_ptr())
+    return N
+
+
+def _workspace(L_, pr, workspace, dev):
+    nbytes = int(L_.pgf_workspace_bytes(ctypes.byref(pr)))
+    if nbytes == 0:
+        _check(L_.pgf_plan(ctypes.byref(pr), ctypes.byref(PgfPlanInfo())))
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), device=dev, dtype=torch.uint8)
+    pr.workspace, pr.workspace_bytes = workspace.data_ptr(), workspace.numel()
+    return workspace
+
+
 def _scan(x, dx, params, order, h_in, dh_in, d2h_in, return_state, seg_len, chunk_segs, workspace, out, stream):
     L_ = lib()
     if not (x.is_cuda and dx.is_cuda):
@@ -139,17 +167,10 @@ def _scan(x, dx, params, order, h_in, dh_in, d2h_in, return_state, seg_len, chun
     if order == 2 and K != 2:
         raise ValueError("the second-order scan takes exactly two directions (dx of shape [2,B,L,D])")
     dev = x.device
-    A = _dev_param(params["A"], (D, params["A"].shape[1]), dev, "A")
-    N = A.shape[1]
-    keep = [A]
-    pr = make_params(B, L, D, N, K, "bf16" if x.dtype == torch.bfloat16 else "f32", seg_len, chunk_segs, order)
-    vals = {"A": A}
-    for name, shape in (("w_delta", (D,)), ("b_delta", (D,)), ("W_B", (D, N)), ("W_C", (D, N)),
-                        ("b_B", (N,)), ("b_C", (N,))):
-        vals[name] = _dev_param(params.get(name), shape, dev, name)
-        keep.append(vals[name])
-    for name in ("A", "w_delta", "b_delta", "W_B", "W_C", "b_B", "b_C"):
-        setattr(pr, name, None if vals[name] is None else vals[name].data_ptr())
+    pr = make_params(B, L, D, params["A"].shape[1], K, "bf16" if x.dtype == torch.bfloat16 else "f32", seg_len,
+                     chunk_segs, order)
+    keep = []
+    N = _model_params(pr, params, D, dev, keep)
     h_in = _dev_param(h_in, (B, D, N), dev, "h_in")
     dh_in = _dev_param(dh_in, (K, B, D, N), dev, "dh_in")
     d2h_in = _dev_param(d2h_in, (B, D, N), dev, "d2h_in")
@@ -166,12 +187,7 @@ def _scan(x, dx, params, order, h_in, dh_in, d2h_in, return_state, seg_len, chun
             d2h_out = torch.empty((B, D, N), device=dev, dtype=torch.float32)
             pr.d2h_out = d2h_out.data_ptr()
             states = states + (d2h_out,)
-    nbytes = int(L_.pgf_workspace_bytes(ctypes.byref(pr)))
-    if nbytes == 0:
-        _check(L_.pgf_plan(ctypes.byref(pr), ctypes.byref(PgfPlanInfo())))
-    if workspace is None or workspace.numel() < nbytes:
-        workspace = torch.empty(max(nbytes, 1), device=dev, dtype=torch.uint8)
-    pr.workspace, pr.workspace_bytes = workspace.data_ptr(), workspace.numel()
+    workspace = _workspace(L_, pr, workspace, dev)
     if out is not None:
         outs = tuple(out)
     else:
@@ -213,6 +229,62 @@ def scan_jvp2(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_
     """
     return _scan(x, dx, params, 2, h_in, dh_in, d2h_in, return_state, seg_len, chunk_segs, workspace, out,
                  stream)
+
+
+def param_grads(x: torch.Tensor, gy: torch.Tensor, params: dict, *, h_in=None, gamma_in=None, grads=None,
+                return_state=False, seg_len=0, chunk_segs=0, workspace=None, out=None, stream=None):
+    """Primal scan with the parameter-sensitivity flows and online gradient
+    accumulation against the adjoint signal gy = dl/dy, on the GPU.
+
+    x [B,L,D] float32 or bfloat16 and gy [B,L,D] float32, CUDA tensors.
+    grads: optional (grad_A, grad_B, grad_C), each [D,N] float32 on the
+    device, which are ADDED to in place (zeros are allocated when None).
+    gamma_in: optional [2,B,D,N] entry state of the flows (dh/dA, dh/dB).
+    Returns (y [B,L,D], grad_A, grad_B, grad_C), plus (h_out [B,D,N],
+    gamma_out [2,B,D,N]) when return_state.  grad_B and grad_C are the
+    gradients of per-lane offsets of B and C; their sums over d are
+    dl/db_B and dl/db_C.  Asynchronous on the current stream.
+    """
+    L_ = lib()
+    if not (x.is_cuda and gy.is_cuda):
+        raise ValueError("x and gy must be device tensors")
+    if x.dtype not in (torch.float32, torch.bfloat16) or gy.dtype != torch.float32:
+        raise ValueError("x must be float32 or bfloat16 and gy float32")
+    if x.dim() != 3 or tuple(gy.shape) != tuple(x.shape):
+        raise ValueError(f"shapes: x and gy [B,L,D]; got {tuple(x.shape)}, {tuple(gy.shape)}")
+    x = x.contiguous()
+    gy = gy.contiguous()
+    B, L, D = x.shape
+    dev = x.device
+    pr = make_params(B, L, D, params["A"].shape[1], 2, "bf16" if x.dtype == torch.bfloat16 else "f32", seg_len,
+                     chunk_segs, 3)
+    keep = []
+    N = _model_params(pr, params, D, dev, keep)
+    h_in = _dev_param(h_in, (B, D, N), dev, "h_in")
+    gamma_in = _dev_param(gamma_in, (2, B, D, N), dev, "gamma_in")
+    pr.h_in = None if h_in is None else h_in.data_ptr()
+    pr.dh_in = None if gamma_in is None else gamma_in.data_ptr()
+    states = ()
+    if return_state:
+        h_out = torch.empty((B, D, N), device=dev, dtype=torch.float32)
+        g_out = torch.empty((2, B, D, N), device=dev, dtype=torch.float32)
+        pr.h_out, pr.dh_out = h_out.data_ptr(), g_out.data_ptr()
+        states = (h_out, g_out)
+    if grads is None:
+        grads = tuple(torch.zeros((D, N), device=dev, dtype=torch.float32) for _ in range(3))
+    else:
+        grads = tuple(grads)
+        for g in grads:
+            if not (g.is_cuda and g.dtype == torch.float32 and tuple(g.shape) == (D, N) and g.is_contiguous()):
+                raise ValueError("grads: three contiguous float32 device tensors of shape [D,N]")
+    workspace = _workspace(L_, pr, workspace, dev)
+    y = out if out is not None else torch.empty((B, L, D), device=dev, dtype=torch.float32)
+    st = torch.cuda.current_stream(dev).cuda_stream if stream is None else stream
+    with torch.cuda.device(dev):
+        rc = L_.pgf_param_grads(_ptr(x), _ptr(gy), ctypes.byref(pr), _ptr(y), _ptr(grads[0]), _ptr(grads[1]),
+                                _ptr(grads[2]), ctypes.c_void_p(st))
+    _check(rc)
+    return (y,) + grads + states
 
 
 def timing_enable(on: bool = True):

@@ -48,7 +48,12 @@ bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
 
 int make_plan(const pgf_params *p, Plan *plan) {
     if (!p || !plan) return PGF_ERR_INVALID_ARG;
-    const int64_t B = p->batch, L = p->seqlen, D = p->d_inner, N = p->d_state, K = p->n_dirs;
+    if (p->order < 0 || p->order > 3) return PGF_ERR_INVALID_ARG;
+    const int order = p->order == 0 ? 1 : p->order;
+    // The parameter flows carry two sensitivity states (dh/dA, dh/dB) and
+    // need no tangent projections; n_dirs is not read.
+    const int64_t B = p->batch, L = p->seqlen, D = p->d_inner, N = p->d_state;
+    const int64_t K = order == 3 ? 2 : p->n_dirs;
     if (B < 1 || L < 0 || D < 1 || N < 1 || K < 1) return PGF_ERR_INVALID_ARG;
     if (p->in_dtype != PGF_F32 && p->in_dtype != PGF_BF16) return PGF_ERR_INVALID_ARG;
     if (!(N == 4 || N == 8 || N == 16 || N == 32 || N == 64)) return PGF_ERR_UNSUPPORTED;
@@ -58,20 +63,19 @@ int make_plan(const pgf_params *p, Plan *plan) {
     if ((1 + K) * B * N * D > (int64_t(1) << 36)) return PGF_ERR_UNSUPPORTED;
     if ((double)K * B * (double)L * D > 9.0e18 / 16) return PGF_ERR_UNSUPPORTED;
 
-    if (p->order < 0 || p->order > 2) return PGF_ERR_INVALID_ARG;
-    const int order = p->order == 2 ? 2 : 1;
     if (order == 2 && K != 2) return PGF_ERR_INVALID_ARG;
-    if (order == 2 && N > 16) return PGF_ERR_UNSUPPORTED;
+    if (order >= 2 && N > 16) return PGF_ERR_UNSUPPORTED;
 
     Plan q{};
     q.B = B; q.L = L; q.D = D; q.N = N; q.K = K;
     q.order = order;
+    q.KP = order == 3 ? 0 : K;
     q.comp = (int)(1 + K + (order == 2 ? 1 : 0));
     q.in_bf16 = p->in_dtype == PGF_BF16;
     // Registers per thread grow as nt*(3+K); keep them near 128.
     q.nt = (int)std::min<int64_t>(N, K >= 8 ? 4 : (K >= 4 ? 8 : 16));
     q.ns = (int)(N / q.nt);
-    q.R = (int)(2 * N * (1 + K));
+    q.R = (int)(2 * N * (1 + q.KP));
 
     // Blocks of one segment column (every channel, one segment).
     const int64_t nblk = B * ((D * q.ns + 255) / 256);
@@ -135,6 +139,8 @@ int make_plan(const pgf_params *p, Plan *plan) {
     } else {
         w.agg_h = w.agg_s = off;
     }
+    w.gacc = off;
+    if (order == 3) off = align256(off + 3 * (size_t)B * N * D * f);
     w.total = off;
     q.ws = w;
     *plan = q;

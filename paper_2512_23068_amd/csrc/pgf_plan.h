@@ -13,18 +13,23 @@ namespace pgf {
 // Offsets (bytes) of the workspace sections; each is 256-byte aligned.
 //   state   [(1+K)][B][N][D]         state carried between host blocks
 //   bc      [B][Tc][R]               per-step projections of one host block,
-//                                    R = 2N(1+K): B, dB_0..dB_{K-1}, C, dC_0..
+//                                    R = 2N(1+KP): B, dB_0..dB_{KP-1}, C, dC_0..
 //   agg_h   [B][G][(1+K)][N][D]      segment end states from a zero start,
 //                                    then (in place) the true state
 //                                    entering each segment
 //   agg_s   [B][G][(1+K)][D]         segment sums of Delta and dDelta_k
+//   gacc    [3][B][N][D]             parameter flows only: running gradient
+//                                    sums (A, B offset, C offset) of the call
+// In the parameter flows K = 2 (the states dh/dA and dh/dB) and agg_h also
+// receives each segment's gradient partials after its rescan.
 struct Layout {
-    size_t state, bc, agg_h, agg_s, total;
+    size_t state, bc, agg_h, agg_s, gacc, total;
 };
 
 struct Plan {
     int64_t B, L, D, N, K;
-    int order;           // 1 or 2
+    int order;           // 1, 2, or 3 (parameter flows)
+    int64_t KP;          // directions projected by k_proj (K, or 0 for order 3)
     int comp;            // states per lane: 1 + K (+ 1 for the mixed flow)
     int in_bf16;
     int nt, ns;          // states per thread, threads per channel (nt*ns == N)
@@ -32,7 +37,7 @@ struct Plan {
     int chunk_segs;      // segments per host block (1 when sequential)
     int64_t chunk_len;   // steps per host block
     int64_t n_chunks;
-    int R;               // floats per step record in bc
+    int R;               // floats per step record in bc: 2N(1+KP)
     Layout ws;
 };
 

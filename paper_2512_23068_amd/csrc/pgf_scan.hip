@@ -1019,6 +1019,261 @@ __global__ __launch_bounds__(kThreads) void k_carry(
     for (int k = 0; k < K; ++k) state[(1 + k) * cstride + b * ND + lane] = dh[k];
 }
 
+// ---------------------------------------------------------------- parameter flows
+// Sensitivity flows of the parameters with online gradient accumulation
+// against an adjoint signal gy = dl/dy (App. E, Alg. 2).  One thread per
+// channel with all NT = N states; per lane the state is (h, GA, GB):
+//   GA' = Abar GA + Delta Abar h     (dh/dA; the Euler drive has no A)
+//   GB' = Abar GB + Delta x          (dh/d offset of B)
+//   h'  = Abar h + Delta B x,        y = sum_n C h'
+// and the rescan (OUT) accumulates, per lane, over its segment
+//   gradA += gy C GA',  gradB += gy C GB',  gradC += gy h'.
+// Records are [B(N) | C(N)].  OUT=false: zero-start segment aggregates
+// (end state in agg_h [B][G][3][N][D], sum of Delta in agg_s [B][G][3][D],
+// component 0).  OUT=true: scan from the entry state in init (as k_scan) and
+// write y; the three gradient sums go to gout at the same place as the
+// entry state (the entry slot is read before it is overwritten, by the same
+// thread), or are added to gout when gadd is set (sequential evaluation:
+// gout is the running sum of the call, and end_state receives the state).
+template <int NT, bool OUT, typename InT>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_pscan(
+    const InT *__restrict__ x, const float *__restrict__ gy, const float *__restrict__ A,
+    const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
+    const float *init, int64_t ibs, int64_t igs, int64_t ics,
+    float *__restrict__ y, float *end_state, float *gout, int gadd,
+    float *__restrict__ agg_h, float *__restrict__ agg_s,
+    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    constexpr int N = NT;
+    constexpr int R = 2 * N;          // B, C
+    constexpr int TT = OUT && NT >= 16 ? 4 : 8;   // prefetch depth, bounded by the VGPR budget
+
+    const int tid = threadIdx.x;
+    const int64_t d_raw = (int64_t)blockIdx.x * kThreads + tid;
+    const bool active = d_raw < D;
+    const int64_t d = active ? d_raw : D - 1;
+    const int g = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int64_t ts = (int64_t)g * S;
+    const int64_t te = ts + S < len ? ts + S : len;
+    if (ts >= te) return;
+
+    float At[NT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i) At[i] = A[d * N + i] * kLog2e;
+    const float w = w_delta[d], bd = b_delta[d];
+
+    float h[NT], ga[NT], gb[NT];
+    float sA[NT], sB[NT], sC[NT];
+    if constexpr (OUT) {
+        const float *ib = init + b * ibs + g * igs + d;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            h[i] = ib[i * D];
+            ga[i] = ib[ics + i * D];
+            gb[i] = ib[2 * ics + i * D];
+            sA[i] = sB[i] = sC[i] = 0.0f;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NT; ++i) h[i] = ga[i] = gb[i] = 0.0f;
+    }
+    float sD = 0.0f;
+
+    const InT *Xb = x + (b * L + t0) * D;
+    const float *Gb = gy + (b * L + t0) * D;
+    float *Yb = y + (b * L + t0) * D;
+    const uint32_t Du = (uint32_t)D, du = (uint32_t)d;
+    const float *rec0 = bc + b * Tc * R;
+
+    float xc[TT], gc[TT];
+#pragma unroll
+    for (int j = 0; j < TT; ++j) {
+        const int64_t t = ts + j < te ? ts + j : te - 1;
+        const uint32_t o = (uint32_t)t * Du + du;
+        xc[j] = load_in(Xb, o);
+        if constexpr (OUT) gc[j] = load_in(Gb, o);
+    }
+    for (int64_t tb = ts; tb < te; tb += TT) {
+        float xn[TT], gn[TT];
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
+            const uint32_t o = (uint32_t)t * Du + du;
+            xn[j] = load_in(Xb, o);
+            if constexpr (OUT) gn[j] = load_in(Gb, o);
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + j;
+            if (t < te) {
+                const float xv = xc[j];
+                float delta, sw;
+                discretize(xv, w, bd, delta, sw);
+                const float u = delta * xv;
+                if constexpr (!OUT) sD += delta;
+                const float *rec = rec0 + t * R;
+                float yv = 0.0f;
+#pragma unroll
+                for (int i = 0; i < NT; ++i) {
+                    const float Bn = rec[i];
+                    const float a = __builtin_amdgcn_exp2f(delta * At[i]);
+                    const float sv = a * h[i];
+                    ga[i] = fmaf(a, ga[i], delta * sv);
+                    gb[i] = fmaf(a, gb[i], u);
+                    h[i] = fmaf(Bn, u, sv);
+                    if constexpr (OUT) {
+                        const float Cn = rec[N + i];
+                        const float gC = gc[j] * Cn;
+                        yv = fmaf(Cn, h[i], yv);
+                        sA[i] = fmaf(gC, ga[i], sA[i]);
+                        sB[i] = fmaf(gC, gb[i], sB[i]);
+                        sC[i] = fmaf(gc[j], h[i], sC[i]);
+                    }
+                }
+                if constexpr (OUT) {
+                    if (active) store_out(Yb, (uint32_t)t * Du + du, yv);
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            xc[j] = xn[j];
+            if constexpr (OUT) gc[j] = gn[j];
+        }
+    }
+
+    if (!active) return;
+    if constexpr (OUT) {
+        if (end_state) {
+            float *eb = end_state + b * ibs + d;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                eb[i * D] = h[i];
+                eb[ics + i * D] = ga[i];
+                eb[2 * ics + i * D] = gb[i];
+            }
+        }
+        float *ob = gout + b * ibs + g * igs + d;
+        if (gadd) {
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                ob[i * D] += sA[i];
+                ob[ics + i * D] += sB[i];
+                ob[2 * ics + i * D] += sC[i];
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                ob[i * D] = sA[i];
+                ob[ics + i * D] = sB[i];
+                ob[2 * ics + i * D] = sC[i];
+            }
+        }
+    } else {
+        const int64_t base = (b * G + g) * 3;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            agg_h[(base * N + i) * D + d] = h[i];
+            agg_h[((base + 1) * N + i) * D + d] = ga[i];
+            agg_h[((base + 2) * N + i) * D + d] = gb[i];
+        }
+        agg_s[base * D + d] = sD;
+    }
+}
+
+// Carry of the parameter flows: a segment maps its entry state to
+//   h' = P h + h0,  GA' = P GA + S P h + GA0,  GB' = P GB + GB0,
+// P = exp(A S), S = the segment's sum of Delta (dP/dA = S P).  Same layout
+// and in-place convention as k_carry.
+__global__ __launch_bounds__(kThreads) void k_pcarry(
+    const float *__restrict__ A, float *__restrict__ seg, const float *__restrict__ agg_s,
+    float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int G) {
+    constexpr int GB = 16;
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t ND = N * D;
+    if (idx >= Bsz * ND) return;
+    const int64_t d = idx % D, n = (idx / D) % N, b = idx / ND;
+    const float a = A[d * N + n];
+    const float at = a * kLog2e;
+    const int64_t cs = Bsz * ND;
+    const int64_t lane = n * D + d;
+    float h = state[b * ND + lane], ga = state[cs + b * ND + lane], gb = state[2 * cs + b * ND + lane];
+    for (int g0 = 0; g0 < G; g0 += GB) {
+        float e0[GB], e1[GB], e2[GB], s0[GB];
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            const int g = g0 + j < G ? g0 + j : G - 1;
+            const int64_t base = (b * G + g) * 3;
+            e0[j] = seg[base * ND + lane];
+            e1[j] = seg[(base + 1) * ND + lane];
+            e2[j] = seg[(base + 2) * ND + lane];
+            s0[j] = agg_s[base * D + d];
+        }
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            if (g0 + j >= G) break;
+            const int64_t base = (b * G + g0 + j) * 3;
+            seg[base * ND + lane] = h;
+            seg[(base + 1) * ND + lane] = ga;
+            seg[(base + 2) * ND + lane] = gb;
+            const float P = __builtin_amdgcn_exp2f(at * s0[j]);
+            ga = fmaf(P, ga, fmaf(P * s0[j], h, e1[j]));
+            gb = fmaf(P, gb, e2[j]);
+            h = fmaf(P, h, e0[j]);
+        }
+    }
+    state[b * ND + lane] = h;
+    state[cs + b * ND + lane] = ga;
+    state[2 * cs + b * ND + lane] = gb;
+}
+
+// Adds the block's per-segment gradient partials part [B][G][3][N][D] to the
+// running sums acc [3][B][N][D] (the state layout), one segment after the
+// other in order, so the sums do not depend on how the call is split into
+// host blocks.
+__global__ __launch_bounds__(kThreads) void k_gsum(
+    const float *__restrict__ part, float *__restrict__ acc, int64_t Bsz, int64_t ND, int G) {
+    constexpr int GB = 16;
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= 3 * Bsz * ND) return;
+    const int64_t c = idx / (Bsz * ND), b = (idx / ND) % Bsz, r = idx % ND;
+    float s = acc[idx];
+    for (int g0 = 0; g0 < G; g0 += GB) {
+        float v[GB];
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            const int g = g0 + j < G ? g0 + j : G - 1;
+            v[j] = part[((b * G + g) * 3 + c) * ND + r];
+        }
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            if (g0 + j >= G) break;
+            s += v[j];
+        }
+    }
+    acc[idx] = s;
+}
+
+__global__ __launch_bounds__(kThreads) void k_fill0(float *__restrict__ p, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < n) p[i] = 0.0f;
+}
+
+// grad_c[d][n] += sum over b (in order) of acc[c][b][n][d], c = A, B, C.
+__global__ __launch_bounds__(kThreads) void k_gout(
+    const float *__restrict__ acc, float *__restrict__ gA, float *__restrict__ gB, float *__restrict__ gC,
+    int64_t Bsz, int64_t D, int64_t N) {
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t ND = N * D;
+    if (idx >= 3 * ND) return;
+    const int64_t c = idx / ND, r = idx % ND;
+    const int64_t d = r % D, n = r / D;
+    float s = 0.0f;
+    for (int64_t b = 0; b < Bsz; ++b) s += acc[(c * Bsz + b) * ND + r];
+    float *out = c == 0 ? gA : (c == 1 ? gB : gC);
+    out[d * N + n] += s;
+}
+
 // ---------------------------------------------------------------- state in/out
 // state [(1+K)][B][N][D] <-> h [B][D][N], dh [K][B][D][N].
 // Component c of the state: 0 -> h, 1..K -> dh_{c-1}, 1+K -> d2h (second
@@ -1112,20 +1367,23 @@ struct Launcher {
     float *d2y;        // second order only
     hipStream_t st;
     char *ws;
+    const float *gy = nullptr;                          // parameter flows only
+    float *gA = nullptr, *gB = nullptr, *gC = nullptr;  // parameter flows only
 
     float *state() const { return (float *)(ws + q.ws.state); }
     float *bcw() const { return (float *)(ws + q.ws.bc); }
     float *agg_h() const { return (float *)(ws + q.ws.agg_h); }
     float *agg_s() const { return (float *)(ws + q.ws.agg_s); }
     float *seg_in() const { return (float *)(ws + q.ws.agg_h); }  // overwritten in place by k_carry
+    float *gacc() const { return (float *)(ws + q.ws.gacc); }
 
     template <int NC>
     void proj_nc(int64_t t0, int64_t len) {
         constexpr int TM = 128;
-        dim3 grid((unsigned)((len + TM - 1) / TM), (unsigned)(1 + q.K), (unsigned)q.B);
+        dim3 grid((unsigned)((len + TM - 1) / TM), (unsigned)(1 + q.KP), (unsigned)q.B);
         Timed tm(0, st);
         hipLaunchKernelGGL((k_proj<NC, InT>), grid, dim3(kThreads), 0, st, x, dx, p.W_B, p.W_C, p.b_B, p.b_C,
-                           bcw(), q.B, q.L, q.D, (int)q.K, t0, len, q.chunk_len);
+                           bcw(), q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len);
     }
 
     void proj(int64_t t0, int64_t len) {
@@ -1244,7 +1502,57 @@ struct Launcher {
         }
     }
 
+    // Parameter flows: one thread per channel with all N <= 16 states.
+    template <int NT>
+    void pscans(int64_t t0, int64_t len) {
+        const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
+        const int64_t ND = q.N * q.D;
+        if (q.seg == 0) {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_pscan<NT, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, gy, p.A,
+                               p.w_delta, p.b_delta, bcw(), (const float *)state(), ND, (int64_t)0, q.B * ND, y,
+                               state(), gacc(), 1, (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len,
+                               q.chunk_len, len, 1);
+            return;
+        }
+        const int G = (int)((len + q.seg - 1) / q.seg);
+        {
+            Timed tm(1, st);
+            hipLaunchKernelGGL((k_pscan<NT, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
+                               x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)nullptr, (int64_t)0,
+                               (int64_t)0, (int64_t)0, y, (float *)nullptr, (float *)nullptr, 0, agg_h(), agg_s(),
+                               q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+        }
+        const int64_t lanes = q.B * ND;
+        {
+            Timed tm(2, st);
+            hipLaunchKernelGGL(k_pcarry, dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
+                               p.A, agg_h(), agg_s(), state(), q.B, q.D, q.N, G);
+        }
+        {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_pscan<NT, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
+                               x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(), (int64_t)G * 3 * ND,
+                               (int64_t)3 * ND, ND, y, (float *)nullptr, seg_in(), 0, (float *)nullptr,
+                               (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+        }
+        {
+            Timed tm(2, st);
+            hipLaunchKernelGGL(k_gsum, dim3((unsigned)((3 * lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
+                               (const float *)seg_in(), gacc(), q.B, ND, G);
+        }
+    }
+
     bool scan_block(int64_t t0, int64_t len) {
+        if (q.order == 3) {
+            if (q.ns != 1) return false;
+            switch (q.nt) {
+                case 4: pscans<4>(t0, len); return true;
+                case 8: pscans<8>(t0, len); return true;
+                case 16: pscans<16>(t0, len); return true;
+                default: return false;
+            }
+        }
         if (q.order == 2) {
             if (q.ns != 1) return false;
             switch (q.nt) {
@@ -1268,15 +1576,25 @@ struct Launcher {
         const unsigned gs = (unsigned)((lanes_all + kThreads - 1) / kThreads);
         const float *d2h_in = q.order == 2 ? p.d2h_in : nullptr;
         float *d2h_out = q.order == 2 ? p.d2h_out : nullptr;
+        const int64_t nacc = 3 * q.B * q.N * q.D;
         {
             Timed tm(4, st);
             hipLaunchKernelGGL(k_state_import, dim3(gs), dim3(kThreads), 0, st, p.h_in, p.dh_in, d2h_in, state(), q.B,
                                q.D, q.N, (int)q.K, q.comp);
+            if (q.order == 3)
+                hipLaunchKernelGGL(k_fill0, dim3((unsigned)((nacc + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                                   st, gacc(), nacc);
         }
         for (int64_t t0 = 0; t0 < q.L; t0 += q.chunk_len) {
             const int64_t len = q.L - t0 < q.chunk_len ? q.L - t0 : q.chunk_len;
             proj(t0, len);
             if (!scan_block(t0, len)) return PGF_ERR_UNSUPPORTED;
+        }
+        if (q.order == 3) {
+            Timed tm(4, st);
+            const int64_t nd3 = 3 * q.N * q.D;
+            hipLaunchKernelGGL(k_gout, dim3((unsigned)((nd3 + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
+                               (const float *)gacc(), gA, gB, gC, q.B, q.D, q.N);
         }
         if (p.h_out || p.dh_out || d2h_out) {
             Timed tm(4, st);
@@ -1331,8 +1649,52 @@ int scan_common(const void *x, const void *dx, const pgf_params *p, float *y, fl
     Launcher<float> l{q, *p, (const float *)x, (const float *)dx, y, dy, d2y, st, (char *)p->workspace};
     return l.run();
 }
+
+int param_common(const void *x, const float *gy, const pgf_params *p, float *y, float *gA, float *gB, float *gC,
+                 void *stream) {
+    Plan q;
+    const int rc = make_plan(p, &q);
+    if (rc != PGF_OK) return rc;
+    if (q.order != 3) return PGF_ERR_INVALID_ARG;
+    if (!p->A || !p->w_delta || !p->b_delta || !p->W_B || !p->W_C) return PGF_ERR_INVALID_ARG;
+    if (!gA || !gB || !gC) return PGF_ERR_INVALID_ARG;
+    if (!p->workspace || p->workspace_bytes < q.ws.total || ((uintptr_t)p->workspace & 255))
+        return PGF_ERR_WORKSPACE;
+    const size_t esz = q.in_bf16 ? 2 : 4;
+    const size_t nx = (size_t)q.B * q.L * q.D;
+    const size_t bx = nx * esz, bg = nx * 4, by = nx * 4, bw = q.ws.total;
+    const size_t bp = (size_t)q.N * q.D * 4;
+    const float *grads[3] = {gA, gB, gC};
+    for (int i = 0; i < 3; ++i) {
+        for (int j = i + 1; j < 3; ++j)
+            if (overlap(grads[i], bp, grads[j], bp)) return PGF_ERR_INVALID_ARG;
+        if (overlap(grads[i], bp, p->workspace, bw)) return PGF_ERR_INVALID_ARG;
+    }
+    if (q.L > 0) {
+        if (!x || !gy || !y) return PGF_ERR_INVALID_ARG;
+        if (overlap(y, by, x, bx) || overlap(y, by, gy, bg) || overlap(y, by, p->workspace, bw))
+            return PGF_ERR_INVALID_ARG;
+        for (int i = 0; i < 3; ++i)
+            if (overlap(grads[i], bp, x, bx) || overlap(grads[i], bp, gy, bg) || overlap(grads[i], bp, y, by))
+                return PGF_ERR_INVALID_ARG;
+    }
+    (void)hipGetLastError();
+    hipStream_t st = (hipStream_t)stream;
+    if (q.in_bf16) {
+        Launcher<uint16_t> l{q, *p, (const uint16_t *)x, nullptr, y, nullptr, nullptr, st, (char *)p->workspace,
+                             gy, gA, gB, gC};
+        return l.run();
+    }
+    Launcher<float> l{q, *p, (const float *)x, nullptr, y, nullptr, nullptr, st, (char *)p->workspace, gy, gA, gB, gC};
+    return l.run();
+}
 }  // namespace
 }  // namespace pgf
+
+extern "C" int pgf_param_grads(const void *x, const float *gy, const pgf_params *p, float *y, float *grad_A,
+                               float *grad_B, float *grad_C, void *stream) {
+    return pgf::param_common(x, gy, p, y, grad_A, grad_B, grad_C, stream);
+}
 
 extern "C" int pgf_scan_jvp(const void *x, const void *dx, const pgf_params *p, float *y, float *dy, void *stream) {
     return pgf::scan_common(x, dx, p, y, dy, nullptr, stream, 1);

@@ -27,7 +27,9 @@ Sequences x [B,L,D] and dx [K,B,L,D] are drawn in blocks of ROWS_PER_BLOCK
 time rows, each block from default_rng([23068, i, stream, b, block]) with
 stream 0 for x and 1+k for dx_k, so the values do not depend on how many
 threads generate them.  bf16 workloads round the fp32 draws to bf16 with
-round-to-nearest-even; the oracle then reads those exact bf16 values.
+round-to-nearest-even; the oracle then reads those exact bf16 values.  The
+adjoint signal gy [B,L,D] of the parameter flows (an upstream dl/dy) is
+N(0,1) from stream 100, always float32.
 """
 from __future__ import annotations
 
@@ -170,6 +172,19 @@ def make_dx(cfg: ScanConfig, threads: int | None = None) -> np.ndarray:
     else:
         raise ValueError(cfg.dx_kind)
     return dx
+
+
+ADJOINT_STREAM = 100
+
+
+def make_adjoint(cfg: ScanConfig, threads: int | None = None) -> np.ndarray:
+    """gy [B,L,D] float32 ~ N(0,1): the adjoint signal of the parameter flows."""
+    cfg = get_config(cfg)
+    threads = threads or _threads()
+    gy = np.empty((cfg.batch, cfg.seqlen, cfg.d_inner), dtype=np.float32)
+    for b in range(cfg.batch):
+        _normal_rows(gy[b], cfg, ADJOINT_STREAM, b, threads)
+    return gy
 
 
 def make_inputs(key, threads: int | None = None) -> dict:

@@ -136,3 +136,20 @@ def test_binding_refuses_host_tensors_and_missing_library(monkeypatch):
     monkeypatch.setattr(binding, "LIB_PATH", "/nonexistent/libpgf.so")
     with pytest.raises(RuntimeError, match="not found"):
         binding.lib()
+
+
+def test_parameter_flow_plans():
+    """order 3 carries two sensitivity states and ignores n_dirs; the first
+    and second-order entry points refuse it."""
+    p1 = binding.plan(1, 131072, 1536, 16, 1, order=3)
+    p8 = binding.plan(1, 131072, 1536, 16, 8, order=3)
+    assert p1 == p8 and p1["n_per_thread"] == 16
+    assert len({binding.workspace_bytes(1, L, 1536, 16, 1, order=3) for L in (1, 8192, 131072)}) == 1
+    with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+        binding.plan(1, 100, 16, 64, 1, order=3)
+    with pytest.raises(RuntimeError, match="INVALID_ARG"):
+        binding.plan(1, 100, 16, 16, 1, order=4)
+    p = _valid_params()
+    p.order = 3
+    p.workspace_bytes = binding.lib().pgf_workspace_bytes(ctypes.byref(p))
+    assert _call(p) == -1

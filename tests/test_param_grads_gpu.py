@@ -1,0 +1,144 @@
+"""Parameter flows (App. E, Alg. 2) on the GPU against the fp64 oracle: the
+primal y and the accumulated gradients dl/dA and of the per-lane offsets of
+B and C for a seeded adjoint signal; y bit-identical to pgf_scan_jvp;
+gradients bit-identical for every host block size; split calls chained
+through the state; accumulation into caller buffers; argument checks."""
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2512_23068_amd import binding, inputs
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(name, **kw):
+    inp = gu.custom(name, **kw)
+    inp["gy"] = inputs.make_adjoint(inp["cfg"])
+    return inp
+
+
+def _run(inp, **kw):
+    x, _ = gu.inputs_to_dev(inp)
+    gy = torch.from_numpy(inp["gy"]).to(gu.dev())
+    out = binding.param_grads(x, gy, gu.params_to_dev(inp), **kw)
+    torch.cuda.synchronize()
+    return out
+
+
+def _check(inp, what, channels=None, **kw):
+    print(f"case {what}", flush=True)
+    y, gA, gB, gC = _run(inp, **kw)[:4]
+    yo, (GA, GB, GC), _ = oracle.param_grads(inp["x"], inp["gy"], inp, channels=channels,
+                                             chunk=None if channels is None else 8192)
+    if channels is not None:
+        idx = torch.from_numpy(np.asarray(channels)).to(gu.dev())
+        y = y.index_select(-1, idx)
+        gA, gB, gC = (g.index_select(0, idx) for g in (gA, gB, gC))
+    errs = [gu.rel_l2(a.cpu().numpy(), b) for a, b in ((y, yo), (gA, GA), (gB, GB), (gC, GC))]
+    print(f"{what} rel_l2 y={errs[0]:.3e} gA={errs[1]:.3e} gB={errs[2]:.3e} gC={errs[3]:.3e}", flush=True)
+    for a in (y, gA, gB, gC):
+        assert torch.all(torch.isfinite(a))
+    assert max(errs) <= gu.TOL, (what, errs)
+
+
+@pytest.mark.parametrize("N,seg", [(16, 0), (8, 0), (4, 0), (16, -1), (16, 64)])
+def test_param_grads_parity(N, seg):
+    inp = _case("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N)
+    _check(inp, f"param N={N} seg={seg}", seg_len=seg)
+
+
+def test_param_grads_bf16_stiff():
+    _check(_case("stiff128k", seqlen=1500, d_inner=64), "param stiff bf16")
+
+
+def test_param_grads_full_size_sampled_channels():
+    """pulse128k's sizes (B=1, L=131072, D=1536, N=16) in the default plan,
+    against the oracle on sampled channels over the whole sequence."""
+    inp = _case("pulse128k")
+    g = np.random.default_rng(5)
+    ch = np.unique(np.concatenate([[0, 1535], g.choice(np.arange(1, 1535), 4, replace=False)]))
+    _check(inp, "param pulse128k full", channels=ch)
+
+
+def test_primal_matches_pgf_scan_jvp():
+    inp = _case("mamba130m", batch=1, seqlen=900, d_inner=96)
+    for seg in (128, -1):
+        y = _run(inp, seg_len=seg, chunk_segs=4)[0]
+        y1, _ = gu.run(inp, seg_len=seg, chunk_segs=4)
+        assert torch.equal(y, y1), seg
+
+
+def test_block_invariance_and_handoff():
+    inp = _case("mamba130m", batch=2, seqlen=1000, d_inner=48)
+    ref = _run(inp, seg_len=64, chunk_segs=1, return_state=True)
+    for cs in (3, 0):
+        got = _run(inp, seg_len=64, chunk_segs=cs, return_state=True)
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), cs
+    x, _ = gu.inputs_to_dev(inp)
+    gy = torch.from_numpy(inp["gy"]).to(gu.dev())
+    prm = gu.params_to_dev(inp)
+    s = 384
+    a = binding.param_grads(x[:, :s], gy[:, :s], prm, seg_len=64, return_state=True)
+    b = binding.param_grads(x[:, s:], gy[:, s:], prm, seg_len=64, h_in=a[4], gamma_in=a[5], grads=a[1:4],
+                            return_state=True)
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat([a[0], b[0]], 1), ref[0])
+    assert torch.equal(b[4], ref[4]) and torch.equal(b[5], ref[5])
+    for i in (1, 2, 3):   # the split adds the two halves' sums: rounding only
+        assert gu.rel_l2(b[i].cpu().numpy(), ref[i].cpu().numpy()) < 1e-6, i
+
+
+def test_entry_state_matches_oracle():
+    inp = _case("mamba130m", batch=1, seqlen=700, d_inner=40)
+    g = np.random.default_rng(41)
+    st = [g.standard_normal((1, 40, 16)).astype(np.float32) for _ in range(3)]
+    y, gA, gB, gC, h, gam = _run(inp, h_in=torch.from_numpy(st[0]), gamma_in=torch.from_numpy(np.stack(st[1:])),
+                                 return_state=True)
+    yo, G, so = oracle.param_grads(inp["x"], inp["gy"], inp, state=tuple(st))
+    for got, ref in ((y, yo), (gA, G[0]), (gB, G[1]), (gC, G[2]), (h, so[0]), (gam[0], so[1]), (gam[1], so[2])):
+        assert gu.rel_l2(got.cpu().numpy(), ref) < gu.TOL
+
+
+def test_gradients_are_added_to_the_callers_buffers():
+    inp = _case("mamba130m", batch=1, seqlen=500, d_inner=32)
+    _, gA, gB, gC = _run(inp)
+    pre = tuple(torch.full_like(g, 0.25) for g in (gA, gB, gC))
+    _, hA, hB, hC = _run(inp, grads=pre)
+    for g, h in ((gA, hA), (gB, hB), (gC, hC)):
+        assert torch.allclose(h, g + 0.25, rtol=1e-6, atol=1e-6)
+    # an empty sequence adds nothing and passes the state through
+    x, _ = gu.inputs_to_dev(inp)
+    gy = torch.from_numpy(inp["gy"]).to(gu.dev())
+    h0 = torch.randn(1, 32, 16, device=gu.dev())
+    out = binding.param_grads(x[:, :0], gy[:, :0], gu.params_to_dev(inp), h_in=h0, grads=pre, return_state=True)
+    torch.cuda.synchronize()
+    assert torch.equal(out[1], pre[0]) and torch.equal(out[4], h0) and torch.all(out[5] == 0)
+
+
+def test_zero_adjoint_gives_zero_gradients():
+    inp = _case("mamba130m", batch=1, seqlen=300, d_inner=32)
+    inp["gy"][:] = 0.0
+    _, gA, gB, gC = _run(inp)
+    assert all(torch.all(g == 0) for g in (gA, gB, gC))
+
+
+def test_argument_checks():
+    inp = _case("tiny", seqlen=64)
+    with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+        binding.plan(1, 64, 16, 32, 1, order=3)
+    pr = binding.make_params(1, 64, 16, 16, 1, order=1)
+    lib = binding.lib()
+    assert lib.pgf_param_grads(None, None, ctypes.byref(pr), None, None, None, None, None) == -1
+    x, _ = gu.inputs_to_dev(inp)
+    with pytest.raises(ValueError, match="float32"):
+        binding.param_grads(x, torch.zeros_like(x, dtype=torch.bfloat16), gu.params_to_dev(inp))
+    gy = torch.zeros_like(x)
+    with pytest.raises(ValueError, match="grads"):
+        binding.param_grads(x, gy, gu.params_to_dev(inp), grads=(torch.zeros(16, 16, device=gu.dev()),) * 2
+                            + (torch.zeros(16, 8, device=gu.dev()),))
