@@ -67,16 +67,40 @@ METRIC = {1: "primal+JVP scan Gtok·ch/s at L=128k", 2: "primal+JVP+second-order
 COPY_BYTES = 1 << 30
 KERNEL_KIND = {"k_proj": "proj", "k_carry": "carry", "k_pcarry": "carry", "k_gsum": "gsum", "k_state": "state_io",
                "k_gout": "state_io", "k_fill0": "state_io"}
-TRAFFIC_SOURCES = ("paper_2512_23068_amd/csrc/pgf_scan.hip", "paper_2512_23068_amd/csrc/pgf_plan.cpp")
+SCAN_SRC = "paper_2512_23068_amd/csrc/pgf_scan.hip"
+PLAN_SRC = "paper_2512_23068_amd/csrc/pgf_plan.cpp"
+# Sections of the kernel source (delimited by "// ----...---- name" lines)
+# whose code a run of each order executes.
+TRAFFIC_SECTIONS = {
+    1: ("helpers", "k_proj", "k_scan", "k_scan_sh", "k_carry", "state in/out", "dispatch"),
+    2: ("helpers", "k_proj", "k_scan2", "state in/out", "dispatch"),
+    3: ("helpers", "k_proj", "parameter flows", "state in/out", "dispatch"),
+}
 
 
-def source_digest():
-    """Digest of the kernel and planner sources the counters were taken on."""
+def _sections(text):
+    out, name = {}, None
+    for line in text.splitlines(keepends=True):
+        if line.startswith("// ------"):
+            name = line.strip("/- \n")
+            out[name] = ""
+        elif name is not None:
+            out[name] += line
+    return out
+
+
+def source_digest(order=1):
+    """Digest of the kernel sections and the planner the counters of an
+    order were taken on."""
     import hashlib
     h = hashlib.sha256()
-    for rel in TRAFFIC_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+    with open(os.path.join(ROOT, SCAN_SRC)) as f:
+        sec = _sections(f.read())
+    for name in TRAFFIC_SECTIONS[order]:
+        h.update(name.encode())
+        h.update(sec[name].encode())
+    with open(os.path.join(ROOT, PLAN_SRC), "rb") as f:
+        h.update(f.read())
     return h.hexdigest()
 
 
@@ -110,7 +134,7 @@ def summarize_counters(workload, order, fetch_csv, write_csv, out_path=None):
                 per.setdefault(lab, {}).setdefault(counter, []).append(v)
     label = workload + SUFFIX[order]
     opt = f" --order {order}" if order != 1 else ""
-    out = {"workload": label, "source_sha256": source_digest(),
+    out = {"workload": label, "source_sha256": source_digest(order),
            "calibration": {"copy_bytes": COPY_BYTES, "FETCH_SIZE_KiB": calib.get("FETCH_SIZE"),
                            "WRITE_SIZE_KiB": calib.get("WRITE_SIZE"),
                            "fetch_factor": calib.get("FETCH_SIZE", 0) * 1024 / COPY_BYTES,
@@ -134,7 +158,7 @@ def summarize_counters(workload, order, fetch_csv, write_csv, out_path=None):
     print(path)
 
 
-def committed_traffic(workload, kind):
+def committed_traffic(workload, kind, order=1):
     """HBM bytes per dispatch of `kind` from the committed counter summary,
     or None when it is missing or was taken on other kernel sources."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
@@ -143,7 +167,7 @@ def committed_traffic(workload, kind):
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("source_sha256") != source_digest():
+    if t.get("source_sha256") != source_digest(order):
         return None
     k = t.get("kernels", {}).get(kind)
     return None if k is None else k["hbm_bytes_per_dispatch"]
@@ -264,7 +288,7 @@ def main():
         "peak": FP32_VECTOR_PEAK_TFLOPS,
         "unit": "TFLOP/s",
         "frac": round(tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
-        "traffic": committed_traffic(cfg.name + SUFFIX[args.order], "scan_out"),
+        "traffic": committed_traffic(cfg.name + SUFFIX[args.order], "scan_out", args.order),
         "hbm_achieved_gbs": round(hbm_gbs, 1),
         "hbm_frac": round(hbm_gbs / HBM_PEAK_GBS, 4),
         "avg_launch_ms": round(so_avg_ms, 5),
