@@ -53,23 +53,28 @@ def build(verbose: bool = False) -> str:
     return _LIB_PATH
 
 
+def declare(lib):
+    """Declares the C signatures on a loaded oracle library (also used by
+    the tests that load mutated copies of it)."""
+    dp = ctypes.POINTER(ctypes.c_double)
+    i64 = ctypes.c_int64
+    lib.pgf_oracle_core.restype = ctypes.c_int
+    lib.pgf_oracle_core.argtypes = [i64] * 5 + [dp] * 13 + [ctypes.c_int, ctypes.c_int]
+    lib.pgf_oracle_core2.restype = ctypes.c_int
+    lib.pgf_oracle_core2.argtypes = [i64] * 4 + [dp] * 22 + [ctypes.c_int]
+    lib.pgf_oracle_param.restype = ctypes.c_int
+    lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 13 + [ctypes.c_int]
+    return lib
+
+
 def _load():
     global _lib
     if _lib is not None:
         return _lib
     if not os.path.exists(_LIB_PATH):
         build()
-    lib = ctypes.CDLL(_LIB_PATH)
-    dp = ctypes.POINTER(ctypes.c_double)
-    i64 = ctypes.c_int64
-    lib.pgf_oracle_core.restype = ctypes.c_int
-    lib.pgf_oracle_core.argtypes = [i64] * 5 + [dp] * 13 + [ctypes.c_int]
-    lib.pgf_oracle_core2.restype = ctypes.c_int
-    lib.pgf_oracle_core2.argtypes = [i64] * 4 + [dp] * 22 + [ctypes.c_int]
-    lib.pgf_oracle_param.restype = ctypes.c_int
-    lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 13 + [ctypes.c_int]
-    _lib = lib
-    return lib
+    _lib = declare(ctypes.CDLL(_LIB_PATH))
+    return _lib
 
 
 def _dp(a):
@@ -84,10 +89,15 @@ def _threads() -> int:
     return int(os.environ.get("PGF_ORACLE_THREADS", "0"))
 
 
-def core(A, x, dx, delta, ddelta, Bm, Cm, dBm, dCm, h=None, dh=None, nthreads=None):
+DRIVES = {"euler": 0, "zoh": 1}
+
+
+def core(A, x, dx, delta, ddelta, Bm, Cm, dBm, dCm, h=None, dh=None, nthreads=None, drive="euler"):
     """Run the recurrence.  Shapes: A [D,N]; x, delta [B,L,D]; dx, ddelta
     [K,B,L,D]; Bm, Cm [B,L,N]; dBm, dCm [K,B,L,N]; h [B,D,N]; dh [K,B,D,N].
-    Returns (y [B,L,D], dy [K,B,L,D], h_out, dh_out), all fp64."""
+    drive: "euler" (Delta*B*x) or "zoh" (A^-1 (Abar - 1) B x).
+    Returns (y [B,L,D], dy [K,B,L,D], h_out, dh_out), all fp64; y and dy
+    are the state read-out sum_n C h (before any activation)."""
     lib = _load()
     A = _f64(A)
     x, dx, delta, ddelta = _f64(x), _f64(dx), _f64(delta), _f64(ddelta)
@@ -104,7 +114,7 @@ def core(A, x, dx, delta, ddelta, Bm, Cm, dBm, dCm, h=None, dh=None, nthreads=No
     dy = np.empty((K, B, L, D))
     rc = lib.pgf_oracle_core(B, L, D, N, K, _dp(A), _dp(x), _dp(dx), _dp(delta), _dp(ddelta),
                              _dp(Bm), _dp(Cm), _dp(dBm), _dp(dCm), _dp(h), _dp(dh), _dp(y), _dp(dy),
-                             _threads() if nthreads is None else nthreads)
+                             DRIVES[drive], _threads() if nthreads is None else nthreads)
     if rc != 0:
         raise RuntimeError("pgf_oracle_core failed")
     return y, dy, h, dh
@@ -136,11 +146,37 @@ def project(x, dx, W_B, W_C, b_B=None, b_C=None):
     return Bm, Cm, dx @ WB, dx @ WC
 
 
-def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nthreads=None):
-    """Full model: discretization, projections, recurrence, over L-chunks.
+ACTIVATIONS = ("identity", "silu")
+
+
+def output_map(yr, dyr, x, dx, D_res=None, act="identity"):
+    """The output map of Sec. 3 applied to the state read-out yr = sum_n C h
+    and its tangents dyr [K,...]: y_hat = yr + D_res*x, y = act(y_hat),
+    dy_k = act'(y_hat) * (dyr_k + D_res*dx_k).  act: identity or SiLU
+    (z*sigmoid(z), derivative s + z*s*(1-s))."""
+    yh, dyh = _f64(yr), _f64(dyr)
+    if D_res is not None:
+        Dr = _f64(D_res)
+        yh = yh + Dr * _f64(x)
+        dyh = dyh + Dr * _f64(dx)
+    if act == "identity":
+        return yh, dyh
+    if act == "silu":
+        s = expit(yh)
+        return yh * s, (s + yh * s * (1.0 - s))[None] * dyh
+    raise ValueError(act)
+
+
+def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nthreads=None, drive="euler",
+             act="identity"):
+    """Full model: discretization, projections, recurrence, output map, over
+    L-chunks.
 
     x [B,L,D], dx [K,B,L,D] (any float dtype; converted exactly to fp64).
-    params: dict with A, w_delta, b_delta, W_B, W_C and optional b_B, b_C.
+    params: dict with A, w_delta, b_delta, W_B, W_C and optional b_B, b_C,
+    D_res [D] (residual weight of the output map).
+    drive: "euler" or "zoh" (the input drive, see core); act: "identity" or
+    "silu" (the output activation, see output_map).
     channels: optional 1-D index array of channels d to compute (the
     projections still use every channel).  h_in [B,D,N] / dh_in [K,B,D,N]
     are over all D channels (or only the selected ones if shaped so).
@@ -163,6 +199,7 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
     step = max(step, 1)
     w = _f64(params["w_delta"])[sel]
     bd = _f64(params["b_delta"])[sel]
+    Dr = None if params.get("D_res") is None else _f64(params["D_res"])[sel]
     As = A[sel]
     for t0 in range(0, L, step):
         t1 = min(L, t0 + step)
@@ -173,9 +210,8 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
         xs = np.ascontiguousarray(xc[..., sel])
         dxs = np.ascontiguousarray(dxc[..., sel])
         delta, ddelta = discretize(xs, dxs, w, bd)
-        yc, dyc, h, dh = core(As, xs, dxs, delta, ddelta, Bm, Cm, dBm, dCm, h, dh, nthreads)
-        y[:, t0:t1] = yc
-        dy[:, :, t0:t1] = dyc
+        yc, dyc, h, dh = core(As, xs, dxs, delta, ddelta, Bm, Cm, dBm, dCm, h, dh, nthreads, drive)
+        y[:, t0:t1], dy[:, :, t0:t1] = output_map(yc, dyc, xs, dxs, Dr, act)
     return y, dy, h, dh
 
 

@@ -28,6 +28,12 @@
  * full.  The per-step coefficients Delta, dDelta_k, B, C, dB_k, dC_k are
  * inputs: the caller derives them from x and the model parameters.
  *
+ * drive = 1 replaces the Euler drive Delta*B*x with the zero-order-hold
+ * drive of the appendix (the exact solution over the step for an input
+ * held constant): b_t = A^{-1}(Abar - 1)*B*x = e*B*x with
+ * e = expm1(Delta*A)/A (= Delta at A = 0), whose derivative in Delta is
+ * Abar, so j_t,k = Abar*dDelta_k*B*x + e*dB_k*x + e*B*dx_k.
+ *
  * Build: -O2 -fno-fast-math -ffp-contract=off -fopenmp.  Parallel over lanes
  * (b, d) only; t stays sequential.
  */
@@ -45,7 +51,7 @@
  *   A [D,N]; x, delta [B,L,D]; dx, ddelta [K,B,L,D];
  *   Bm, Cm [B,L,N]; dBm, dCm [K,B,L,N];
  *   h [B,D,N] and dh [K,B,D,N]: entry state on input, exit state on output;
- *   y [B,L,D]; dy [K,B,L,D].
+ *   y [B,L,D]; dy [K,B,L,D]; drive 0 (Euler) or 1 (zero-order hold).
  * Returns 0, or -1 on a bad argument or allocation failure.
  */
 int pgf_oracle_core(int64_t B, int64_t L, int64_t D, int64_t N, int64_t K,
@@ -54,9 +60,9 @@ int pgf_oracle_core(int64_t B, int64_t L, int64_t D, int64_t N, int64_t K,
                     const double *Bm, const double *Cm,
                     const double *dBm, const double *dCm,
                     double *h, double *dh, double *y, double *dy,
-                    int nthreads)
+                    int drive, int nthreads)
 {
-    if (B < 0 || L < 0 || D < 0 || N <= 0 || K <= 0) return -1;
+    if (B < 0 || L < 0 || D < 0 || N <= 0 || K <= 0 || drive < 0 || drive > 1) return -1;
     if (!A || !h || !dh) return -1;
     if (L > 0 && (!x || !dx || !delta || !ddelta || !Bm || !Cm || !dBm || !dCm || !y || !dy))
         return -1;
@@ -95,7 +101,10 @@ int pgf_oracle_core(int64_t B, int64_t L, int64_t D, int64_t N, int64_t K,
             for (int64_t n = 0; n < N; ++n) {
                 const double a = A[d * N + n];
                 const double abar = exp(dl * a);
-                const double bt = dl * Bt[n] * xt;
+                /* drive coefficient and its derivative in Delta */
+                const double ec = drive ? (a != 0.0 ? expm1(dl * a) / a : dl) : dl;
+                const double dec = drive ? abar : 1.0;
+                const double bt = ec * Bt[n] * xt;
                 const double hprev = hs[n];
                 const double hnew = abar * hprev + bt;
                 for (int64_t k = 0; k < K; ++k) {
@@ -103,7 +112,7 @@ int pgf_oracle_core(int64_t B, int64_t L, int64_t D, int64_t N, int64_t K,
                     const int64_t kbtn = ((k * B + b) * L + t) * N + n;
                     const double ddl = ddelta[kbtd], dxt = dx[kbtd];
                     const double Kt = abar * a * ddl;
-                    const double jt = ddl * Bt[n] * xt + dl * dBm[kbtn] * xt + dl * Bt[n] * dxt;
+                    const double jt = dec * ddl * Bt[n] * xt + ec * dBm[kbtn] * xt + ec * Bt[n] * dxt;
                     const double dhnew = abar * dhs[k * N + n] + Kt * hprev + jt;
                     dhs[k * N + n] = dhnew;
                     dyk[k] += dCm[kbtn] * hnew + Ct[n] * dhnew;

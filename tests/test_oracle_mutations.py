@@ -32,9 +32,9 @@ C_MUTANTS = {
     "drop K_t (dDelta through Abar)": ("const double Kt = abar * a * ddl;", "const double Kt = 0.0 * abar * a * ddl;"),
     "K_t sign": ("const double Kt = abar * a * ddl;", "const double Kt = -abar * a * ddl;"),
     "K_t without A": ("const double Kt = abar * a * ddl;", "const double Kt = abar * ddl;"),
-    "drop dDelta*B*x": ("const double jt = ddl * Bt[n] * xt + ", "const double jt = "),
-    "drop Delta*dB*x": ("+ dl * dBm[kbtn] * xt ", ""),
-    "drop Delta*B*dx": ("+ dl * Bt[n] * dxt;", ";"),
+    "drop dDelta*B*x": ("const double jt = dec * ddl * Bt[n] * xt + ", "const double jt = "),
+    "drop Delta*dB*x": ("+ ec * dBm[kbtn] * xt ", ""),
+    "drop Delta*B*dx": ("+ ec * Bt[n] * dxt;", ";"),
     "drop dC*h (paper's Eq. 2)": ("dyk[k] += dCm[kbtn] * hnew + Ct[n] * dhnew;", "dyk[k] += Ct[n] * dhnew;"),
     "output uses previous state": ("yt += Ct[n] * hnew;", "yt += Ct[n] * hprev;"),
     "tangent uses new state": ("Kt * hprev + jt", "Kt * hnew + jt"),
@@ -51,11 +51,7 @@ def _build_mutant(src_text, tmpdir, name):
         f.write(src_text)
     subprocess.run(["gcc", "-O2", "-fno-fast-math", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
                     "-o", so, c, "-lm"], check=True)
-    lib = ctypes.CDLL(so)
-    dp = ctypes.POINTER(ctypes.c_double)
-    lib.pgf_oracle_core.restype = ctypes.c_int
-    lib.pgf_oracle_core.argtypes = [ctypes.c_int64] * 5 + [dp] * 13 + [ctypes.c_int]
-    return lib
+    return oracle.declare(ctypes.CDLL(so))
 
 
 def _caught():

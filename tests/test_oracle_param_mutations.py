@@ -59,15 +59,7 @@ def test_c_mutant_is_caught(name, monkeypatch):
             f.write(src.replace(old, new))
         subprocess.run(["gcc", "-O2", "-fno-fast-math", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
                         "-o", so, c, "-lm"], check=True)
-        lib = ctypes.CDLL(so)
-        dp = ctypes.POINTER(ctypes.c_double)
-        i64 = ctypes.c_int64
-        lib.pgf_oracle_core.restype = ctypes.c_int
-        lib.pgf_oracle_core.argtypes = [i64] * 5 + [dp] * 13 + [ctypes.c_int]
-        lib.pgf_oracle_core2.restype = ctypes.c_int
-        lib.pgf_oracle_core2.argtypes = [i64] * 4 + [dp] * 22 + [ctypes.c_int]
-        lib.pgf_oracle_param.restype = ctypes.c_int
-        lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 13 + [ctypes.c_int]
+        lib = oracle.declare(ctypes.CDLL(so))
         monkeypatch.setattr(oracle, "_lib", lib)
         assert _caught(), name
 
