@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--order", type=int, default=1, choices=(1, 2, 3),
                     help="2: second-order flow (two directions, pgf_scan_jvp2); "
                          "3: parameter flows with gradient accumulation (pgf_param_grads)")
+    ap.add_argument("--drive", default="euler", choices=("euler", "zoh"), help="input drive (first order)")
+    ap.add_argument("--act", default="identity", choices=("identity", "silu"), help="output activation (first order)")
+    ap.add_argument("--dres", action="store_true", help="add a residual weight D_res ~ N(0,1) to the output map")
     ap.add_argument("--seg-len", type=int, default=0, help="tiling override (0 = library default)")
     ap.add_argument("--chunk-segs", type=int, default=0, help="tiling override (0 = library default)")
     return ap.parse_args()
@@ -72,7 +75,7 @@ PLAN_SRC = "paper_2512_23068_amd/csrc/pgf_plan.cpp"
 # Sections of the kernel source (delimited by "// ----...---- name" lines)
 # whose code a run of each order executes.
 TRAFFIC_SECTIONS = {
-    1: ("helpers", "k_proj", "k_scan", "k_scan_sh", "k_carry", "state in/out", "dispatch"),
+    1: ("helpers", "variants", "k_proj", "k_scan", "k_scan_sh", "k_carry", "state in/out", "dispatch"),
     2: ("helpers", "k_proj", "k_scan2", "state in/out", "dispatch"),
     3: ("helpers", "k_proj", "parameter flows", "state in/out", "dispatch"),
 }
@@ -187,6 +190,10 @@ def main():
     from paper_2512_23068_amd import binding, inputs
 
     cfg = inputs.get_config(args.workload)
+    variant = args.drive != "euler" or args.act != "identity" or args.dres
+    if variant and args.order != 1:
+        print("bench.py: --drive/--act/--dres apply to the first order only", file=sys.stderr)
+        sys.exit(2)
     if args.order == 2:
         # two independent N(0,1) directions on the same workload shape
         cfg = cfg.with_(n_dirs=2, dx_kind="normal")
@@ -202,6 +209,8 @@ def main():
     tdt = torch.bfloat16 if cfg.in_dtype == "bf16" else torch.float32
     x = torch.from_numpy(inp["x"]).to(dev).to(tdt)
     params = {k: torch.from_numpy(inp[k]).to(dev) for k in ("A", "w_delta", "b_delta", "W_B", "W_C")}
+    if args.dres:
+        params["D_res"] = torch.from_numpy(np.random.default_rng([23068, 7]).standard_normal(D).astype(np.float32)).to(dev)
     s_in = x.element_size()
     y = torch.empty((B, L, D), device=dev)
     if args.order == 3:
@@ -217,7 +226,7 @@ def main():
             outs = outs + (torch.empty((B, L, D), device=dev),)
             payload += x.numel() * 4
     del inp
-    plan = binding.plan(B, L, D, N, K, cfg.in_dtype, args.seg_len, args.chunk_segs, args.order)
+    plan = binding.plan(B, L, D, N, K, cfg.in_dtype, args.seg_len, args.chunk_segs, args.order, args.drive, args.act)
     ws = torch.empty(plan["workspace_bytes"], device=dev, dtype=torch.uint8)
     torch.cuda.synchronize()
 
@@ -228,8 +237,10 @@ def main():
     else:
         fn = binding.scan_jvp2 if args.order == 2 else binding.scan_jvp
 
+        vkw = dict(drive=args.drive, act=args.act) if args.order == 1 else {}
+
         def step():
-            fn(x, dx, params, workspace=ws, out=outs, seg_len=args.seg_len, chunk_segs=args.chunk_segs)
+            fn(x, dx, params, workspace=ws, out=outs, seg_len=args.seg_len, chunk_segs=args.chunk_segs, **vkw)
 
     for _ in range(args.warmup):
         step()
@@ -288,7 +299,7 @@ def main():
         "peak": FP32_VECTOR_PEAK_TFLOPS,
         "unit": "TFLOP/s",
         "frac": round(tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
-        "traffic": committed_traffic(cfg.name + SUFFIX[args.order], "scan_out", args.order),
+        "traffic": None if variant else committed_traffic(cfg.name + SUFFIX[args.order], "scan_out", args.order),
         "hbm_achieved_gbs": round(hbm_gbs, 1),
         "hbm_frac": round(hbm_gbs / HBM_PEAK_GBS, 4),
         "avg_launch_ms": round(so_avg_ms, 5),
@@ -311,7 +322,7 @@ def main():
         del src, dst
 
     cpu = None
-    if not args.no_cpu and args.order == 1:
+    if not args.no_cpu and args.order == 1 and not variant:
         cpu = cpu_baseline(cfg, args.cpu_steps)
 
     out = {
@@ -327,7 +338,8 @@ def main():
         "vs_baseline": None,
         "dtype": "f32" if cfg.in_dtype == "f32" else "bf16-in/f32",
         "data": "synthetic (seeded workload recipe)",
-        "config": {"workload": cfg.name + SUFFIX[args.order], "batch": B, "seq_len": L, "d_inner": D,
+        "config": {"workload": cfg.name + SUFFIX[args.order] + variant_suffix(args), "batch": B, "seq_len": L,
+                   "d_inner": D,
                    "d_state": N, "n_dirs": 0 if args.order == 3 else K, "in_dtype": cfg.in_dtype,
                    "parallelism": "single GPU"},
         "hbm_gbs_path": round(alg_bytes / (ms_step * 1e-3) / 1e9, 1),
@@ -341,6 +353,12 @@ def main():
         "wall_s_timed": round(wall, 3),
     }
     print(json.dumps(out), flush=True)
+
+
+def variant_suffix(args):
+    parts = ([args.drive] if args.drive != "euler" else []) + ([args.act] if args.act != "identity" else []) + \
+        (["dres"] if args.dres else [])
+    return "".join("-" + p for p in parts)
 
 
 def cpu_baseline(cfg, cpu_steps):

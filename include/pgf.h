@@ -71,6 +71,14 @@ extern "C" {
 #define PGF_F32   0
 #define PGF_BF16  1
 
+/* Input drive of the discretised recurrence (pgf_params.drive). */
+#define PGF_DRIVE_EULER  0   /* b = Delta * B * x                                  */
+#define PGF_DRIVE_ZOH    1   /* b = A^-1 (Abar - 1) * B * x (zero-order hold)      */
+
+/* Output activation (pgf_params.activation). */
+#define PGF_ACT_IDENTITY 0
+#define PGF_ACT_SILU     1   /* act(v) = v * sigmoid(v)                            */
+
 typedef struct pgf_params {
     /* Problem size: batch B, sequence length L (>= 0), channels D, state size
      * N, tangent directions K.  Supported: B, D >= 1; N in {4,8,16,32,64};
@@ -108,6 +116,17 @@ typedef struct pgf_params {
      * not written). */
     const float *d2h_in;
     float *d2h_out;
+    /* Model variants of the first-order scan (Sec. 3 output map, the
+     * appendix's zero-order-hold drive); zero for the others.  With any of
+     * them set, pgf_scan_jvp supports N <= 16 and K <= 2.
+     *   drive      : PGF_DRIVE_EULER or PGF_DRIVE_ZOH
+     *   activation : PGF_ACT_IDENTITY or PGF_ACT_SILU
+     *   D_res      : device, [D] f32 residual weight, or NULL (= 0)
+     * The output becomes y = act(sum_n C h + D_res x) and
+     * dy_k = act'(.) * (sum_n dC_k h + C dh_k + D_res dx_k). */
+    int32_t drive;
+    int32_t activation;
+    const float *D_res;
 } pgf_params;
 
 /* How a call is tiled (host-side planning; no device access). */

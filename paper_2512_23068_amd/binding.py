@@ -19,6 +19,8 @@ LIB_PATH = os.path.join(_HERE, "libpgf.so")
 PGF_OK = 0
 PGF_F32 = 0
 PGF_BF16 = 1
+DRIVES = {"euler": 0, "zoh": 1}
+ACTIVATIONS = {"identity": 0, "silu": 1}
 TIMING_KINDS = ("proj", "seg_aggregate", "carry", "scan_out", "state_io")
 
 _c_f = ctypes.c_void_p
@@ -35,6 +37,7 @@ class PgfParams(ctypes.Structure):
         ("h_in", _c_f), ("dh_in", _c_f), ("h_out", _c_f), ("dh_out", _c_f),
         ("workspace", _c_f), ("workspace_bytes", ctypes.c_size_t),
         ("d2h_in", _c_f), ("d2h_out", _c_f),
+        ("drive", ctypes.c_int32), ("activation", ctypes.c_int32), ("D_res", _c_f),
     ]
 
 
@@ -93,23 +96,26 @@ def _check(code: int):
         raise RuntimeError(status_string(code))
 
 
-def make_params(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1) -> PgfParams:
+def make_params(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1, drive="euler",
+                act="identity") -> PgfParams:
     p = PgfParams()
     p.batch, p.seqlen, p.d_inner, p.d_state, p.n_dirs = int(B), int(L), int(D), int(N), int(K)
     p.in_dtype = PGF_BF16 if in_dtype in ("bf16", torch.bfloat16) else PGF_F32
     p.seg_len, p.chunk_segs, p.order = int(seg_len), int(chunk_segs), int(order)
+    p.drive, p.activation = DRIVES[drive], ACTIVATIONS[act]
     return p
 
 
-def workspace_bytes(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1) -> int:
+def workspace_bytes(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1, drive="euler",
+                    act="identity") -> int:
     return int(lib().pgf_workspace_bytes(ctypes.byref(make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs,
-                                                                  order))))
+                                                                  order, drive, act))))
 
 
-def plan(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1) -> dict:
+def plan(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1, drive="euler", act="identity") -> dict:
     info = PgfPlanInfo()
-    _check(lib().pgf_plan(ctypes.byref(make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs, order)),
-                          ctypes.byref(info)))
+    _check(lib().pgf_plan(ctypes.byref(make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs, order, drive,
+                                                   act)), ctypes.byref(info)))
     return {f: getattr(info, f) for f, _ in PgfPlanInfo._fields_}
 
 
@@ -152,7 +158,8 @@ def _workspace(L_, pr, workspace, dev):
     return workspace
 
 
-def _scan(x, dx, params, order, h_in, dh_in, d2h_in, return_state, seg_len, chunk_segs, workspace, out, stream):
+def _scan(x, dx, params, order, h_in, dh_in, d2h_in, return_state, seg_len, chunk_segs, workspace, out, stream,
+          drive="euler", act="identity"):
     L_ = lib()
     if not (x.is_cuda and dx.is_cuda):
         raise ValueError("x and dx must be device tensors")
@@ -168,9 +175,12 @@ def _scan(x, dx, params, order, h_in, dh_in, d2h_in, return_state, seg_len, chun
         raise ValueError("the second-order scan takes exactly two directions (dx of shape [2,B,L,D])")
     dev = x.device
     pr = make_params(B, L, D, params["A"].shape[1], K, "bf16" if x.dtype == torch.bfloat16 else "f32", seg_len,
-                     chunk_segs, order)
+                     chunk_segs, order, drive, act)
     keep = []
     N = _model_params(pr, params, D, dev, keep)
+    D_res = _dev_param(params.get("D_res"), (D,), dev, "D_res")
+    keep.append(D_res)
+    pr.D_res = None if D_res is None else D_res.data_ptr()
     h_in = _dev_param(h_in, (B, D, N), dev, "h_in")
     dh_in = _dev_param(dh_in, (K, B, D, N), dev, "dh_in")
     d2h_in = _dev_param(d2h_in, (B, D, N), dev, "d2h_in")
@@ -208,15 +218,19 @@ def _scan(x, dx, params, order, h_in, dh_in, d2h_in, return_state, seg_len, chun
 
 
 def scan_jvp(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_in=None, return_state=False,
-             seg_len=0, chunk_segs=0, workspace=None, out=None, stream=None):
+             seg_len=0, chunk_segs=0, workspace=None, out=None, stream=None, drive="euler", act="identity"):
     """Fused primal + tangent scan on the GPU.
 
     x [B,L,D] and dx [K,B,L,D]: float32 or bfloat16 CUDA tensors (same dtype).
-    params: A, W_B, W_C [D,N]; w_delta, b_delta [D]; optional b_B, b_C [N].
+    params: A, W_B, W_C [D,N]; w_delta, b_delta [D]; optional b_B, b_C [N]
+    and D_res [D] (residual weight of the output map).
+    drive: "euler" or "zoh"; act: "identity" or "silu" (the variants need
+    N <= 16 and K <= 2).
     Returns (y [B,L,D], dy [K,B,L,D]) in float32, plus (h_out [B,D,N],
     dh_out [K,B,D,N]) when return_state.  Asynchronous on the current stream.
     """
-    return _scan(x, dx, params, 1, h_in, dh_in, None, return_state, seg_len, chunk_segs, workspace, out, stream)
+    return _scan(x, dx, params, 1, h_in, dh_in, None, return_state, seg_len, chunk_segs, workspace, out, stream,
+                 drive, act)
 
 
 def scan_jvp2(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_in=None, d2h_in=None,

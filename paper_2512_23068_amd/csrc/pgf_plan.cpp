@@ -65,10 +65,16 @@ int make_plan(const pgf_params *p, Plan *plan) {
 
     if (order == 2 && K != 2) return PGF_ERR_INVALID_ARG;
     if (order >= 2 && N > 16) return PGF_ERR_UNSUPPORTED;
+    if (p->drive < 0 || p->drive > 1 || p->activation < 0 || p->activation > 1) return PGF_ERR_INVALID_ARG;
+    const int var = (p->drive == PGF_DRIVE_ZOH ? 1 : 0) |
+                    ((p->activation != PGF_ACT_IDENTITY || p->D_res) ? 2 : 0);
+    if (var && order != 1) return PGF_ERR_UNSUPPORTED;
+    if (var && (K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
 
     Plan q{};
     q.B = B; q.L = L; q.D = D; q.N = N; q.K = K;
     q.order = order;
+    q.var = var;
     q.KP = order == 3 ? 0 : K;
     q.comp = (int)(1 + K + (order == 2 ? 1 : 0));
     q.in_bf16 = p->in_dtype == PGF_BF16;

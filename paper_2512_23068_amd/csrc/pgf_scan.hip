@@ -120,6 +120,46 @@ __device__ __forceinline__ void discretize2(float xv, float w, float bd, float &
     s2 = (e * r) * r * (w * w);
 }
 
+// ---------------------------------------------------------------- variants
+// Model variants of the first-order scan, selected by the VAR template
+// argument of k_scan: bit 0 (kZoh) replaces the Euler drive Delta*B*x with
+// the zero-order-hold drive (Abar - 1)/A * B*x; bit 1 (kOutMap) applies the
+// output map y = act(sum_n C h + D_res x) with its derivative.
+constexpr int kZoh = 1;
+constexpr int kOutMap = 2;
+struct Variant {
+    const float *D_res;   // [D] residual weight, or NULL (= 0)
+    int act;              // PGF_ACT_IDENTITY or PGF_ACT_SILU
+};
+
+// The ZOH drive coefficient e = (Abar - 1)/A of one lane, z = Delta*A,
+// Abar = exp(z) as computed by the caller.  For |z| < 1/4, e = Delta * phi(z) with
+// phi(z) = expm1(z)/z = sum_k z^k/(k+1)! summed to z^6 (the first omitted
+// term is below 2e-9 relative); otherwise (Abar - 1) * (1/A), where the
+// subtraction loses less than 3 bits.  A = 0 takes the first branch (e = Delta).
+__device__ __forceinline__ float zoh_coef(float delta, float a_n, float inv_a, float abar) {
+    const float z = delta * a_n;
+    float ph = fmaf(z, 1.0f / 5040.0f, 1.0f / 720.0f);
+    ph = fmaf(z, ph, 1.0f / 120.0f);
+    ph = fmaf(z, ph, 1.0f / 24.0f);
+    ph = fmaf(z, ph, 1.0f / 6.0f);
+    ph = fmaf(z, ph, 0.5f);
+    ph = fmaf(z, ph, 1.0f);
+    return fabsf(z) < 0.25f ? delta * ph : (abar - 1.0f) * inv_a;
+}
+
+// SiLU and its derivative at v: s = sigmoid(v) and 1 - s from one
+// e = exp(-|v|) (no cancellation on either side), silu = v s,
+// silu' = s + v s (1 - s).
+__device__ __forceinline__ void silu_and_slope(float v, float &f, float &df) {
+    const float e = exp_nonpos(-fabsf(v));
+    const float r = __builtin_amdgcn_rcpf(1.0f + e);
+    const float s = v >= 0.0f ? r : e * r;
+    const float sc = v >= 0.0f ? e * r : r;
+    f = v * s;
+    df = fmaf(v * s, sc, s);
+}
+
 // ---------------------------------------------------------------- k_proj
 // rec[b][t-t0] = [B(N) | dB_0..dB_{K-1} (N each) | C(N) | dC_0..dC_{K-1}]
 // Row source s = blockIdx.y: 0 -> x (bias added), 1+k -> dx_k.
@@ -275,14 +315,15 @@ __global__ __launch_bounds__(kThreads) void k_proj(
 // entry state at init[b*ibs + g*igs + c*ics + n*D + d] and write y, dy; if
 // end_state is set (sequential evaluation) the exit state is stored there
 // with the same indexing (g = 0).
-template <int NT, int NS, int K, bool OUT, typename InT>
+template <int NT, int NS, int K, bool OUT, typename InT, int VAR = 0>
 __global__ __launch_bounds__(kThreads) void k_scan(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *__restrict__ init, int64_t ibs, int64_t igs, int64_t ics,
     float *__restrict__ y, float *__restrict__ dy, float *__restrict__ end_state,
     float *__restrict__ agg_h, float *__restrict__ agg_s,
-    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G, Variant vr) {
+    static_assert(VAR == 0 || NS == 1, "model variants run one thread per channel");
     constexpr int N = NT * NS;
     constexpr int R = 2 * N * (1 + K);
     constexpr int DPB = kThreads / NS;
@@ -299,13 +340,16 @@ __global__ __launch_bounds__(kThreads) void k_scan(
     const int64_t te = ts + S < len ? ts + S : len;
     if (ts >= te) return;
 
-    float Af[NT], At[NT];
+    float Af[NT], At[NT], Ai[NT];
 #pragma unroll
     for (int i = 0; i < NT; ++i) {
         Af[i] = A[d * N + ns * NT + i];
         At[i] = Af[i] * kLog2e;
+        if constexpr ((VAR & kZoh) != 0) Ai[i] = 1.0f / Af[i];
     }
     const float w = w_delta[d], bd = b_delta[d];
+    float Dr = 0.0f;
+    if constexpr ((VAR & kOutMap) != 0 && OUT) Dr = vr.D_res ? vr.D_res[d] : 0.0f;
 
     float h[NT], dh[K][NT];
     if constexpr (OUT) {
@@ -387,11 +431,25 @@ __global__ __launch_bounds__(kThreads) void k_scan(
                     const float a = __builtin_amdgcn_exp2f(delta * At[i]);
                     const float sv = a * h[i];
                     const float gv = Af[i] * sv;
-                    const float hn = fmaf(Bn, u, sv);
+                    float hn;
+                    if constexpr ((VAR & kZoh) != 0) {
+                        // b = e B x, db_k = Abar dDelta_k B x + e (dB_k x + B dx_k)
+                        const float e = zoh_coef(delta, Af[i], Ai[i], a);
+                        const float Bx = Bn * xv;
+                        hn = fmaf(e, Bx, sv);
 #pragma unroll
-                    for (int k = 0; k < K; ++k) {
-                        const float dBn = rec[(1 + k) * N + n];
-                        dh[k][i] = fmaf(a, dh[k][i], fmaf(gv, dD[k], fmaf(Bn, pk[k], dBn * u)));
+                        for (int k = 0; k < K; ++k) {
+                            const float dBn = rec[(1 + k) * N + n];
+                            const float jk = fmaf(a * dD[k], Bx, e * fmaf(dBn, xv, Bn * dxc[k][j]));
+                            dh[k][i] = fmaf(a, dh[k][i], fmaf(gv, dD[k], jk));
+                        }
+                    } else {
+                        hn = fmaf(Bn, u, sv);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) {
+                            const float dBn = rec[(1 + k) * N + n];
+                            dh[k][i] = fmaf(a, dh[k][i], fmaf(gv, dD[k], fmaf(Bn, pk[k], dBn * u)));
+                        }
                     }
                     h[i] = hn;
                     if constexpr (OUT) {
@@ -408,6 +466,18 @@ __global__ __launch_bounds__(kThreads) void k_scan(
                     yv = group_sum<NS>(yv);
 #pragma unroll
                     for (int k = 0; k < K; ++k) dyv[k] = group_sum<NS>(dyv[k]);
+                    if constexpr ((VAR & kOutMap) != 0) {
+                        yv = fmaf(Dr, xv, yv);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) dyv[k] = fmaf(Dr, dxc[k][j], dyv[k]);
+                        if (vr.act == PGF_ACT_SILU) {
+                            float f, df;
+                            silu_and_slope(yv, f, df);
+                            yv = f;
+#pragma unroll
+                            for (int k = 0; k < K; ++k) dyv[k] *= df;
+                        }
+                    }
                     if (active && ns == 0) {
                         store_out(Yb, (uint32_t)t * Du + du, yv);
 #pragma unroll
@@ -468,7 +538,7 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
     const float *__restrict__ init, int64_t ibs, int64_t igs, int64_t ics,
     float *__restrict__ y, float *__restrict__ dy, float *__restrict__ end_state,
     float *__restrict__ agg_h, float *__restrict__ agg_s,
-    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G, Variant) {
     static_assert(NS >= 2, "one thread per channel uses k_scan");
     constexpr int N = NT * NS;
     constexpr int R = 2 * N * (1 + K);
@@ -714,9 +784,11 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
 }
 
 // Kernel for a tiling: one thread per channel, or several sharing one.
-template <int NT, int NS, int K, bool OUT, typename InT>
+// The aggregate pass (OUT = false) writes no outputs, so it only needs the
+// drive bit of a variant.
+template <int NT, int NS, int K, bool OUT, typename InT, int VAR>
 constexpr auto scan_kernel() {
-    if constexpr (NS == 1) return &k_scan<NT, NS, K, OUT, InT>;
+    if constexpr (NS == 1) return &k_scan<NT, NS, K, OUT, InT, OUT ? VAR : (VAR & kZoh)>;
     else return &k_scan_sh<NT, NS, K, OUT, InT>;
 }
 
@@ -1396,26 +1468,27 @@ struct Launcher {
         }
     }
 
-    template <int NT, int NS, int K>
+    template <int NT, int NS, int K, int VAR = 0>
     void scans(int64_t t0, int64_t len) {
         const unsigned gx = (unsigned)((q.D * NS + kThreads - 1) / kThreads);
         const int64_t ND = q.N * q.D;
+        const Variant vr{p.D_res, p.activation};
         if (q.seg == 0) {
             // Sequential evaluation: one segment per block, state in place.
             Timed tm(3, st);
-            hipLaunchKernelGGL((scan_kernel<NT, NS, K, true, InT>()), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x,
-                               dx, p.A, p.w_delta, p.b_delta, bcw(), state(), ND, (int64_t)0, q.B * ND, y, dy,
-                               state(), (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len,
-                               len, 1);
+            hipLaunchKernelGGL((scan_kernel<NT, NS, K, true, InT, VAR>()), dim3(gx, 1, (unsigned)q.B), dim3(kThreads),
+                               0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(), state(), ND, (int64_t)0, q.B * ND, y,
+                               dy, state(), (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len,
+                               len, 1, vr);
             return;
         }
         const int G = (int)((len + q.seg - 1) / q.seg);
         {
             Timed tm(1, st);
-            hipLaunchKernelGGL((scan_kernel<NT, NS, K, false, InT>()), dim3(gx, (unsigned)G, (unsigned)q.B),
+            hipLaunchKernelGGL((scan_kernel<NT, NS, K, false, InT, VAR>()), dim3(gx, (unsigned)G, (unsigned)q.B),
                                dim3(kThreads), 0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(),
                                (const float *)nullptr, (int64_t)0, (int64_t)0, (int64_t)0, y, dy, (float *)nullptr,
-                               agg_h(), agg_s(), q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+                               agg_h(), agg_s(), q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G, vr);
         }
         {
             const int64_t lanes = q.B * ND;
@@ -1425,17 +1498,41 @@ struct Launcher {
         }
         {
             Timed tm(3, st);
-            hipLaunchKernelGGL((scan_kernel<NT, NS, K, true, InT>()), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads),
-                               0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(), seg_in(), (int64_t)G * (1 + K) * ND,
-                               (int64_t)(1 + K) * ND, ND, y, dy, (float *)nullptr, (float *)nullptr,
-                               (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+            hipLaunchKernelGGL((scan_kernel<NT, NS, K, true, InT, VAR>()), dim3(gx, (unsigned)G, (unsigned)q.B),
+                               dim3(kThreads), 0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(), seg_in(),
+                               (int64_t)G * (1 + K) * ND, (int64_t)(1 + K) * ND, ND, y, dy, (float *)nullptr,
+                               (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg,
+                               G, vr);
         }
     }
 
     // Tilings the planner can choose: nt = min(N, 16) for K <= 2,
     // nt = min(N, 8) for K = 4 and nt = min(N, 4) for K = 8; ns = N / nt.
+    // Model variants: one thread per channel, N <= 16, K <= 2.
+    template <int K, int VAR>
+    bool variant_block(int64_t t0, int64_t len) {
+        if (q.ns != 1) return false;
+        switch (q.nt) {
+            case 4: scans<4, 1, K, VAR>(t0, len); return true;
+            case 8: scans<8, 1, K, VAR>(t0, len); return true;
+            case 16: scans<16, 1, K, VAR>(t0, len); return true;
+            default: return false;
+        }
+    }
+
     template <int K>
     bool scan_block_k(int64_t t0, int64_t len) {
+        if constexpr (K <= 2) {
+            switch (q.var) {
+                case 0: break;
+                case kZoh: return variant_block<K, kZoh>(t0, len);
+                case kOutMap: return variant_block<K, kOutMap>(t0, len);
+                case kZoh | kOutMap: return variant_block<K, kZoh | kOutMap>(t0, len);
+                default: return false;
+            }
+        } else if (q.var != 0) {
+            return false;
+        }
         const int code = q.nt * 100 + q.ns;
         if constexpr (K <= 2) {
             switch (code) {

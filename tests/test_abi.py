@@ -153,3 +153,18 @@ def test_parameter_flow_plans():
     p.order = 3
     p.workspace_bytes = binding.lib().pgf_workspace_bytes(ctypes.byref(p))
     assert _call(p) == -1
+
+
+def test_variant_plans_and_bad_variant_fields():
+    p = binding.plan(1, 131072, 1536, 16, 1, drive="zoh", act="silu")
+    assert p == binding.plan(1, 131072, 1536, 16, 1)
+    for kw in (dict(K=4), dict(N=32)):
+        args = dict(B=1, L=100, D=64, N=16, K=1)
+        args.update(kw)
+        with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+            binding.plan(*args.values(), drive="zoh")
+    pr = binding.make_params(1, 100, 16, 16, 1)
+    pr.drive = 2
+    assert binding.lib().pgf_workspace_bytes(ctypes.byref(pr)) == 0
+    pr.drive, pr.activation = 0, 5
+    assert binding.lib().pgf_workspace_bytes(ctypes.byref(pr)) == 0

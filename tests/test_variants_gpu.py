@@ -1,0 +1,83 @@
+"""Model variants of the first-order scan on the GPU against the fp64
+oracle: the zero-order-hold drive (small and large Delta*A, both branches
+of the drive coefficient), the output map act(C h + D_res x) with identity
+and SiLU, and both together; bit-identical results for every host block
+size; the plain path unchanged when no variant is set."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2512_23068_amd import binding
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+
+def _with_dres(inp, seed=7):
+    inp["D_res"] = np.random.default_rng(seed).standard_normal(inp["x"].shape[-1]).astype(np.float32)
+    return inp
+
+
+def _check(inp, what, drive="euler", act="identity", **kw):
+    print(f"case {what}", flush=True)
+    y, dy = gu.run(inp, drive=drive, act=act, **kw)
+    yo, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp, drive=drive, act=act)
+    gu.assert_close(y.cpu().numpy(), dy.cpu().numpy(), yo, dyo, what=what)
+
+
+@pytest.mark.parametrize("N,K,seg", [(16, 1, 0), (16, 2, 0), (8, 1, -1), (4, 2, 64), (16, 1, -1)])
+def test_zoh_parity(N, K, seg):
+    inp = gu.custom("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N, n_dirs=K)
+    _check(inp, f"zoh N={N} K={K} seg={seg}", drive="zoh", seg_len=seg)
+
+
+def test_zoh_small_steps_and_stiff():
+    """Delta*A spans both branches of the drive coefficient: tiny steps
+    (pulse128k's Delta in [1e-4, 1e-2]) and the stiff bf16 workload."""
+    _check(gu.custom("pulse128k", seqlen=2000, d_inner=64, dx_kind="normal"), "zoh small steps", drive="zoh")
+    _check(gu.custom("stiff128k", seqlen=1500, d_inner=64), "zoh stiff bf16", drive="zoh")
+
+
+@pytest.mark.parametrize("act,dres", [("silu", False), ("silu", True), ("identity", True)])
+def test_output_map_parity(act, dres):
+    inp = gu.custom("mamba130m", batch=2, seqlen=900, d_inner=70, n_dirs=2)
+    if dres:
+        _with_dres(inp)
+    _check(inp, f"output map act={act} D_res={dres}", act=act)
+
+
+def test_zoh_with_output_map():
+    inp = _with_dres(gu.custom("mamba130m", batch=1, seqlen=1300, d_inner=96, n_dirs=1))
+    _check(inp, "zoh + silu + D_res", drive="zoh", act="silu")
+
+
+def test_variant_block_invariance():
+    inp = _with_dres(gu.custom("mamba130m", batch=2, seqlen=1000, d_inner=48, n_dirs=2))
+    ref = gu.run(inp, drive="zoh", act="silu", seg_len=64, chunk_segs=1, return_state=True)
+    for cs in (3, 0):
+        got = gu.run(inp, drive="zoh", act="silu", seg_len=64, chunk_segs=cs, return_state=True)
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), cs
+
+
+def test_plain_path_unchanged_and_residual_is_additive():
+    inp = gu.custom("mamba130m", batch=1, seqlen=700, d_inner=64, n_dirs=1)
+    y0, dy0 = gu.run(inp)
+    y1, dy1 = gu.run(inp, drive="euler", act="identity")
+    assert torch.equal(y0, y1) and torch.equal(dy0, dy1)
+    _with_dres(inp)
+    y2, dy2 = gu.run(inp)
+    Dr = torch.from_numpy(inp["D_res"]).to(gu.dev())
+    x, dx = gu.inputs_to_dev(inp)
+    assert torch.allclose(y2, y0 + Dr * x, rtol=1e-6, atol=1e-6)
+    assert torch.allclose(dy2, dy0 + Dr * dx, rtol=1e-6, atol=1e-6)
+
+
+def test_variant_limits():
+    with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+        binding.plan(1, 100, 64, 16, 4, drive="zoh")
+    with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+        binding.plan(1, 100, 64, 32, 1, act="silu")
+    with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+        binding.plan(1, 100, 64, 16, 2, order=2, drive="zoh")
