@@ -22,6 +22,8 @@ Layers
 * ``core_param`` / ``param_grads``: the parameter-sensitivity flows and the
   online gradient accumulation of App. E (Alg. 2) for a given adjoint
   signal dl/dy, same layering.
+* ``la_scan_jvp``: decaying linear attention (App. F: RetNet, RWKV-6,
+  linear transformers) with its tangent flow, over L-chunks.
 
 Precision: everything in fp64 from the exact fp32 / bf16 input values.
 Library routines used as steps: numpy.logaddexp (softplus), scipy expit
@@ -64,6 +66,8 @@ def declare(lib):
     lib.pgf_oracle_core2.argtypes = [i64] * 4 + [dp] * 22 + [ctypes.c_int]
     lib.pgf_oracle_param.restype = ctypes.c_int
     lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 13 + [ctypes.c_int]
+    lib.pgf_oracle_la.restype = ctypes.c_int
+    lib.pgf_oracle_la.argtypes = [i64] * 6 + [dp] * 12 + [ctypes.c_int]
     return lib
 
 
@@ -356,3 +360,38 @@ def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=N
     if st is None:
         st = tuple(np.zeros((B, Ds, N)) for _ in range(3))
     return y, tuple(g.sum(0) for g in tot), st
+
+
+# ------------------------------------------------------------------ linear attention
+
+def la_scan_jvp(q, k, v, g, dq, dk, dv, dg, state=None, chunk=None, nthreads=None):
+    """Decaying linear attention and its tangent flow (see pgf_oracle_la).
+    q, k, g [B,H,L,dk]; v [B,H,L,dv]; dq, dk, dg [K,B,H,L,dk];
+    dv [K,B,H,L,dv]; state = (S [B,H,dk,dv], dS [K,B,H,dk,dv]) or None.
+    Returns (o [B,H,L,dv], do [K,B,H,L,dv], S_out, dS_out)."""
+    lib = _load()
+    B, H, L, DK = np.shape(q)
+    DV = np.shape(v)[-1]
+    K = np.shape(dq)[0]
+    if state is None:
+        S = np.zeros((B, H, DK, DV))
+        dS = np.zeros((K, B, H, DK, DV))
+    else:
+        S = np.array(state[0], dtype=np.float64, copy=True, order="C")
+        dS = np.array(state[1], dtype=np.float64, copy=True, order="C")
+    assert S.shape == (B, H, DK, DV) and dS.shape == (K, B, H, DK, DV)
+    o = np.empty((B, H, L, DV))
+    do = np.empty((K, B, H, L, DV))
+    step = max(1, L if not chunk else int(chunk))
+    for t0 in range(0, L, step):
+        t1 = min(L, t0 + step)
+        a = [_f64(np.asarray(u)[..., t0:t1, :]) for u in (q, k, v, g, dq, dk, dv, dg)]
+        oc = np.empty((B, H, t1 - t0, DV))
+        doc = np.empty((K, B, H, t1 - t0, DV))
+        rc = lib.pgf_oracle_la(B, H, t1 - t0, DK, DV, K, *[_dp(u) for u in a], _dp(S), _dp(dS), _dp(oc), _dp(doc),
+                               _threads() if nthreads is None else nthreads)
+        if rc != 0:
+            raise RuntimeError("pgf_oracle_la failed")
+        o[:, :, t0:t1] = oc
+        do[:, :, :, t0:t1] = doc
+    return o, do, S, dS

@@ -289,3 +289,70 @@ int pgf_oracle_param(int64_t B, int64_t L, int64_t D, int64_t N,
     }
     return 0;
 }
+
+/*
+ * Decaying linear attention with its tangent flow (App. F: linear
+ * transformers, RetNet, RWKV-6 as general linear recurrences).  Per batch
+ * b and head h the state is a d_k x d_v matrix S with a per-key-dimension
+ * decay alpha_t = exp(g_t) (g_t <= 0 is the log-decay, an input):
+ *
+ *   S_t[i,j]  = alpha_t[i]*S_{t-1}[i,j] + k_t[i]*v_t[j]
+ *   o_t[j]    = sum_i q_t[i]*S_t[i,j]
+ *
+ * and, for every tangent direction (dq, dk, dv, dg) of the four input
+ * sequences, the total differential (App. F "total differential"):
+ *
+ *   dS_t[i,j] = alpha*dS_{t-1} + (alpha*dg)*S_{t-1} + dk*v + k*dv
+ *   do_t[j]   = sum_i dq_t[i]*S_t[i,j] + q_t[i]*dS_t[i,j]
+ *
+ * (d alpha = alpha*dg).  RetNet is the case of a constant scalar decay, a
+ * linear transformer without normaliser the case g = 0.
+ * Shapes (double, row-major): q, k, g [B,H,L,dk]; v [B,H,L,dv];
+ * dq, dk_, dg [K,B,H,L,dk]; dv [K,B,H,L,dv]; S [B,H,dk,dv] and
+ * dS [K,B,H,dk,dv] (entry state in, exit state out); o [B,H,L,dv];
+ * do_ [K,B,H,L,dv].  Returns 0, or -1 on a bad argument.
+ */
+int pgf_oracle_la(int64_t B, int64_t H, int64_t L, int64_t DK, int64_t DV, int64_t K,
+                  const double *q, const double *k, const double *v, const double *g,
+                  const double *dq, const double *dk, const double *dv, const double *dg,
+                  double *S, double *dS, double *o, double *do_, int nthreads)
+{
+    if (B < 0 || H < 0 || L < 0 || DK <= 0 || DV <= 0 || K <= 0) return -1;
+    if (!S || !dS) return -1;
+    if (L > 0 && (!q || !k || !v || !g || !dq || !dk || !dv || !dg || !o || !do_)) return -1;
+    const int64_t lanes = B * H * DV;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t lane = 0; lane < lanes; ++lane) {
+        const int64_t bh = lane / DV, j = lane % DV;
+        for (int64_t t = 0; t < L; ++t) {
+            const int64_t rk = (bh * L + t) * DK;       /* row of q, k, g */
+            const int64_t rv = (bh * L + t) * DV + j;   /* element of v, o */
+            double ot = 0.0;
+            for (int64_t kk = 0; kk < K; ++kk) do_[(kk * B * H * L) * DV + rv] = 0.0;
+            for (int64_t i = 0; i < DK; ++i) {
+                const int64_t si = (bh * DK + i) * DV + j;
+                const double alpha = exp(g[rk + i]);
+                const double sprev = S[si];
+                const double snew = alpha * sprev + k[rk + i] * v[rv];
+                for (int64_t kk = 0; kk < K; ++kk) {
+                    const int64_t tk = kk * B * H * L * DK + rk + i;
+                    const int64_t tv = kk * B * H * L * DV + rv;
+                    const int64_t ts = kk * B * H * DK * DV + si;
+                    const double dsnew = alpha * dS[ts] + alpha * dg[tk] * sprev + dk[tk] * v[rv] + k[rk + i] * dv[tv];
+                    dS[ts] = dsnew;
+                    do_[tv] += dq[tk] * snew + q[rk + i] * dsnew;
+                }
+                S[si] = snew;
+                ot += q[rk + i] * snew;
+            }
+            o[rv] = ot;
+        }
+    }
+    return 0;
+}
