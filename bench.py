@@ -68,10 +68,12 @@ METRIC = {1: "primal+JVP scan Gtok·ch/s at L=128k", 2: "primal+JVP+second-order
 
 
 COPY_BYTES = 1 << 30
-KERNEL_KIND = {"k_proj": "proj", "k_carry": "carry", "k_pcarry": "carry", "k_gsum": "gsum", "k_state": "state_io",
-               "k_gout": "state_io", "k_fill0": "state_io"}
+KERNEL_KIND = {"k_proj": "proj", "k_la_prep": "proj", "k_carry": "carry", "k_pcarry": "carry", "k_la_carry": "carry",
+               "k_gsum": "gsum", "k_state": "state_io", "k_gout": "state_io", "k_fill0": "state_io",
+               "k_la_copy": "state_io"}
 SCAN_SRC = "paper_2512_23068_amd/csrc/pgf_scan.hip"
 PLAN_SRC = "paper_2512_23068_amd/csrc/pgf_plan.cpp"
+LA_SRC = "paper_2512_23068_amd/csrc/pgf_la.hip"
 # Sections of the kernel source (delimited by "// ----...---- name" lines)
 # whose code a run of each order executes.
 TRAFFIC_SECTIONS = {
@@ -94,24 +96,29 @@ def _sections(text):
 
 def source_digest(order=1):
     """Digest of the kernel sections and the planner the counters of an
-    order were taken on."""
+    order (1, 2, 3, or "la" for linear attention) were taken on."""
     import hashlib
     h = hashlib.sha256()
-    with open(os.path.join(ROOT, SCAN_SRC)) as f:
-        sec = _sections(f.read())
-    for name in TRAFFIC_SECTIONS[order]:
-        h.update(name.encode())
-        h.update(sec[name].encode())
+    if order == "la":
+        with open(os.path.join(ROOT, LA_SRC), "rb") as f:
+            h.update(f.read())
+    else:
+        with open(os.path.join(ROOT, SCAN_SRC)) as f:
+            sec = _sections(f.read())
+        for name in TRAFFIC_SECTIONS[order]:
+            h.update(name.encode())
+            h.update(sec[name].encode())
     with open(os.path.join(ROOT, PLAN_SRC), "rb") as f:
         h.update(f.read())
     return h.hexdigest()
 
 
 def _kernel_label(name):
+    import re
     base = name.split("(")[0].replace("void ", "").strip()
-    if "k_scan" in base or "k_pscan" in base:
+    if "k_scan" in base or "k_pscan" in base or "k_la_scan" in base:
         # the OUT template argument true marks the scan with outputs
-        return "scan_out" if ", true," in base else "seg_aggregate"
+        return "scan_out" if re.search(r"[<,]\s*true\s*[,>]", base) else "seg_aggregate"
     for key, lab in KERNEL_KIND.items():
         if key in base and lab:
             return lab
@@ -135,9 +142,10 @@ def summarize_counters(workload, order, fetch_csv, write_csv, out_path=None):
                 continue
             if lab in ("proj", "seg_aggregate", "carry", "gsum", "scan_out", "state_io"):
                 per.setdefault(lab, {}).setdefault(counter, []).append(v)
-    label = workload + SUFFIX[order]
+    la = workload.startswith(("la_", "rwkv"))
+    label = workload if la else workload + SUFFIX[order]
     opt = f" --order {order}" if order != 1 else ""
-    out = {"workload": label, "source_sha256": source_digest(order),
+    out = {"workload": label, "source_sha256": source_digest("la" if la else order),
            "calibration": {"copy_bytes": COPY_BYTES, "FETCH_SIZE_KiB": calib.get("FETCH_SIZE"),
                            "WRITE_SIZE_KiB": calib.get("WRITE_SIZE"),
                            "fetch_factor": calib.get("FETCH_SIZE", 0) * 1024 / COPY_BYTES,
@@ -176,19 +184,14 @@ def committed_traffic(workload, kind, order=1):
     return None if k is None else k["hbm_bytes_per_dispatch"]
 
 
-def main():
-    args = parse()
-    if args.summarize_counters:
-        summarize_counters(args.workload, args.order, *args.summarize_counters, out_path=args.traffic_out)
-        return
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on one GPU only; --gpus must be 1", file=sys.stderr)
-        sys.exit(2)
-    import numpy as np
-    import torch
+class Workload:
+    """What a bench run times: one step of the hot path and its accounting."""
 
-    from paper_2512_23068_amd import binding, inputs
+    def __init__(self, **kw):
+        self.__dict__.update(kw)
 
+
+def setup_ssm(args, np, torch, binding, inputs):
     cfg = inputs.get_config(args.workload)
     variant = args.drive != "euler" or args.act != "identity" or args.dres
     if variant and args.order != 1:
@@ -210,7 +213,8 @@ def main():
     x = torch.from_numpy(inp["x"]).to(dev).to(tdt)
     params = {k: torch.from_numpy(inp[k]).to(dev) for k in ("A", "w_delta", "b_delta", "W_B", "W_C")}
     if args.dres:
-        params["D_res"] = torch.from_numpy(np.random.default_rng([23068, 7]).standard_normal(D).astype(np.float32)).to(dev)
+        params["D_res"] = torch.from_numpy(
+            np.random.default_rng([23068, 7]).standard_normal(D).astype(np.float32)).to(dev)
     s_in = x.element_size()
     y = torch.empty((B, L, D), device=dev)
     if args.order == 3:
@@ -228,7 +232,6 @@ def main():
     del inp
     plan = binding.plan(B, L, D, N, K, cfg.in_dtype, args.seg_len, args.chunk_segs, args.order, args.drive, args.act)
     ws = torch.empty(plan["workspace_bytes"], device=dev, dtype=torch.uint8)
-    torch.cuda.synchronize()
 
     if args.order == 3:
         def step():
@@ -236,14 +239,88 @@ def main():
                                 chunk_segs=args.chunk_segs)
     else:
         fn = binding.scan_jvp2 if args.order == 2 else binding.scan_jvp
-
         vkw = dict(drive=args.drive, act=args.act) if args.order == 1 else {}
 
         def step():
             fn(x, dx, params, workspace=ws, out=outs, seg_len=args.seg_len, chunk_segs=args.chunk_segs, **vkw)
 
+    tokch = B * L * D
+    if args.order == 3:
+        alg_bytes = tokch * (s_in + 4 + 4)    # read x and gy, write y
+    else:
+        alg_bytes = tokch * ((1 + K) * (s_in + 4) + (4 if args.order == 2 else 0))
+    name = cfg.name + SUFFIX[args.order]
+    return Workload(
+        step=step, tokch=tokch, alg_bytes=alg_bytes, flops=tokch * N * scan_flops_per_lane_step(K, args.order),
+        payload=payload, plan=plan, metric=METRIC[args.order], kernel="k_scan (scan with outputs)",
+        traffic=None if variant else committed_traffic(name, "scan_out", args.order),
+        dtype="f32" if cfg.in_dtype == "f32" else "bf16-in/f32",
+        config={"workload": name + variant_suffix(args), "batch": B, "seq_len": L, "d_inner": D, "d_state": N,
+                "n_dirs": 0 if args.order == 3 else K, "in_dtype": cfg.in_dtype, "parallelism": "single GPU"},
+        cpu=(lambda: cpu_baseline(cfg, args.cpu_steps)) if args.order == 1 and not variant else None)
+
+
+def la_flops_per_lane_step(K):
+    """Arithmetic of the definition per (b, h, t, i, j): alpha*S + k*v and
+    q*S' (5 counting an fma as 2); per direction alpha*dS + (alpha dg)*S +
+    dk*v + k*dv (7) and dq*S' + q*dS' (4)."""
+    return 5 + 11 * K
+
+
+def setup_la(args, np, torch, binding, inputs):
+    cfg = inputs.LA_BY_NAME[args.workload]
+    if args.order != 1 or args.drive != "euler" or args.act != "identity" or args.dres:
+        print("bench.py: the linear-attention workloads take no --order/--drive/--act/--dres", file=sys.stderr)
+        sys.exit(2)
+    B, H, L, DK, DV, K = cfg.batch, cfg.heads, cfg.seqlen, cfg.d_key, cfg.d_value, cfg.n_dirs
+    dev = torch.device("cuda:0")
+    t_gen = time.time()
+    inp = inputs.make_la_inputs(cfg)
+    print(f"bench: workload {cfg.name} B={B} H={H} L={L} dk={DK} dv={DV} K={K}; inputs in "
+          f"{time.time() - t_gen:.1f}s", file=sys.stderr, flush=True)
+    ts = [torch.from_numpy(inp[n]).to(dev) for n in ("q", "k", "v", "g", "dq", "dk", "dv", "dg")]
+    del inp
+    o = torch.empty((B, H, L, DV), device=dev)
+    do = torch.empty((K, B, H, L, DV), device=dev)
+    payload = sum(t.numel() for t in ts) * 4 + (o.numel() + do.numel()) * 4
+    plan = binding.la_plan(B, H, L, DK, DV, K, args.seg_len, args.chunk_segs)
+    ws = torch.empty(plan["workspace_bytes"], device=dev, dtype=torch.uint8)
+
+    def step():
+        binding.la_scan_jvp(*ts, workspace=ws, out=(o, do), seg_len=args.seg_len, chunk_segs=args.chunk_segs)
+
+    tokch = B * L * H * DV
+    # read v, dv_k and the key-side q, k, g and tangents once, write o, do_k
+    alg_bytes = tokch * 4 * (2 * (1 + K)) + B * H * L * DK * 4 * (3 + 3 * K)
+    return Workload(
+        step=step, tokch=tokch, alg_bytes=alg_bytes, flops=tokch * DK * la_flops_per_lane_step(K),
+        payload=payload, plan=plan, metric="decaying linear attention primal+JVP Gtok·ch/s",
+        kernel="k_la_scan (scan with outputs)", traffic=committed_traffic(cfg.name, "scan_out", "la"), dtype="f32",
+        config={"workload": cfg.name, "batch": B, "heads": H, "seq_len": L, "d_key": DK, "d_value": DV,
+                "n_dirs": K, "parallelism": "single GPU"},
+        cpu=(lambda: la_cpu_baseline(cfg, args.cpu_steps)))
+
+
+def main():
+    args = parse()
+    if args.summarize_counters:
+        summarize_counters(args.workload, args.order, *args.summarize_counters, out_path=args.traffic_out)
+        return
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only; --gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2512_23068_amd import binding, inputs
+
+    setup = setup_la if args.workload in inputs.LA_BY_NAME else setup_ssm
+    w = setup(args, np, torch, binding, inputs)
+    dev = torch.device("cuda:0")
+    torch.cuda.synchronize()
+
     for _ in range(args.warmup):
-        step()
+        w.step()
     torch.cuda.synchronize()
     torch.cuda.reset_peak_memory_stats()
     binding.timing_read()
@@ -255,7 +332,7 @@ def main():
     ev0.record()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step()
+        w.step()
     ev1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -269,37 +346,32 @@ def main():
     torch.cuda.synchronize()
     ev0.record()
     for _ in range(args.steps):
-        step()
+        w.step()
     ev1.record()
     torch.cuda.synchronize()
     ms_step_clean = ev0.elapsed_time(ev1) / args.steps
     ms_step = min(ms_step, ms_step_clean)
 
-    tokch = B * L * D
-    value = tokch / (ms_step * 1e-3) / 1e9
-    if args.order == 3:
-        alg_bytes = tokch * (s_in + 4 + 4)    # read x and gy, write y
-    else:
-        alg_bytes = tokch * ((1 + K) * (s_in + 4) + (4 if args.order == 2 else 0))
+    value = w.tokch / (ms_step * 1e-3) / 1e9
     # Dominant kernel: the scan that writes the outputs (kind 3).  Per launch
-    # it performs the whole of the algorithmic IO of its block (x, dx read
-    # once, y, dy written once) and the whole per-lane arithmetic.
+    # it performs the whole of the algorithmic IO of its block (inputs read
+    # once, outputs written once) and the whole per-lane arithmetic.
     dom_name = max(kern, key=lambda k: kern[k][0])
     so_ms, so_n = kern["scan_out"]
     so_avg_ms = so_ms / max(so_n, 1)
     launches_per_step = so_n / args.steps
-    bytes_per_launch = alg_bytes / launches_per_step
-    flops_per_launch = tokch * N * scan_flops_per_lane_step(K, args.order) / launches_per_step
+    bytes_per_launch = w.alg_bytes / launches_per_step
+    flops_per_launch = w.flops / launches_per_step
     hbm_gbs = bytes_per_launch / (so_avg_ms * 1e-3) / 1e9
     tflops = flops_per_launch / (so_avg_ms * 1e-3) / 1e12
     roofline = {
-        "kernel": "k_scan (scan with outputs)",
+        "kernel": w.kernel,
         "bound": "alu",
         "achieved": round(tflops, 3),
         "peak": FP32_VECTOR_PEAK_TFLOPS,
         "unit": "TFLOP/s",
         "frac": round(tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
-        "traffic": None if variant else committed_traffic(cfg.name + SUFFIX[args.order], "scan_out", args.order),
+        "traffic": w.traffic,
         "hbm_achieved_gbs": round(hbm_gbs, 1),
         "hbm_frac": round(hbm_gbs / HBM_PEAK_GBS, 4),
         "avg_launch_ms": round(so_avg_ms, 5),
@@ -308,11 +380,13 @@ def main():
     }
     kernels = {k: {"ms_per_step": round(v[0] / args.steps, 4), "launches_per_step": v[1] / args.steps}
                for k, v in kern.items()}
+    plan, payload, metric, dtype, config, alg_bytes = w.plan, w.payload, w.metric, w.dtype, w.config, w.alg_bytes
+    cpu_fn = None if args.no_cpu else w.cpu
 
     if args.calib_copy:
         # A plain copy of known size: what the HBM counters read for it
         # calibrates FETCH_SIZE / WRITE_SIZE against true bytes.
-        del y, ws
+        del w
         torch.cuda.empty_cache()
         src = torch.ones(1 << 28, device=dev, dtype=torch.float32)
         dst = torch.empty_like(src)
@@ -320,13 +394,11 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-
-    cpu = None
-    if not args.no_cpu and args.order == 1 and not variant:
-        cpu = cpu_baseline(cfg, args.cpu_steps)
+        cpu_fn = None
+    cpu = cpu_fn() if cpu_fn is not None else None
 
     out = {
-        "metric": METRIC[args.order],
+        "metric": metric,
         "value": round(value, 3),
         "unit": "Gtok·ch/s",
         "n_gpus": 1,
@@ -336,12 +408,9 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32" if cfg.in_dtype == "f32" else "bf16-in/f32",
+        "dtype": dtype,
         "data": "synthetic (seeded workload recipe)",
-        "config": {"workload": cfg.name + SUFFIX[args.order] + variant_suffix(args), "batch": B, "seq_len": L,
-                   "d_inner": D,
-                   "d_state": N, "n_dirs": 0 if args.order == 3 else K, "in_dtype": cfg.in_dtype,
-                   "parallelism": "single GPU"},
+        "config": config,
         "hbm_gbs_path": round(alg_bytes / (ms_step * 1e-3) / 1e9, 1),
         "hbm_frac_path": round(alg_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "vram": {"peak_bytes": int(peak), "payload_bytes": int(payload), "workspace_bytes": plan["workspace_bytes"],
@@ -386,6 +455,33 @@ def cpu_baseline(cfg, cpu_steps):
     tokch = sub.batch * Ls * sub.d_inner
     return {"value": round(tokch / dt / 1e9, 6), "unit": "Gtok·ch/s", "cores": threads, "kind": "oracle",
             "sample": f"{cfg.name} first {Ls} steps, all {sub.d_inner} channels, batch {sub.batch}, "
+                      f"{sub.n_dirs} direction(s); fp64; {dt:.2f}s"}
+
+
+def la_cpu_baseline(cfg, cpu_steps):
+    """The fp64 linear-attention oracle on the host cores over a prefix of
+    the same workload (all heads, the first Ls steps)."""
+    from oracle import oracle
+    from paper_2512_23068_amd import inputs
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    names = ("q", "k", "v", "g", "dq", "dk", "dv", "dg")
+
+    def run(Ls):
+        sub = cfg.with_(seqlen=Ls)
+        inp = inputs.make_la_inputs(sub)
+        t0 = time.perf_counter()
+        oracle.la_scan_jvp(*[inp[n] for n in names], nthreads=threads)
+        return sub, time.perf_counter() - t0
+
+    if cpu_steps:
+        Ls = cpu_steps
+    else:   # calibrate on a short prefix, then size the sample to ~15 s
+        _, t_cal = run(64)
+        Ls = int(max(64, min(cfg.seqlen, 64 * 15.0 / max(t_cal, 1e-3))))
+    sub, dt = run(Ls)
+    return {"value": round(sub.tok_ch / dt / 1e9, 6), "unit": "Gtok·ch/s", "cores": threads, "kind": "oracle",
+            "sample": f"{cfg.name} first {Ls} steps, all {sub.heads} heads, batch {sub.batch}, "
                       f"{sub.n_dirs} direction(s); fp64; {dt:.2f}s"}
 
 

@@ -207,6 +207,55 @@ int pgf_scan_jvp2(const void *x, const void *dx, const pgf_params *p,
 int pgf_param_grads(const void *x, const float *gy, const pgf_params *p,
                     float *y, float *grad_A, float *grad_B, float *grad_C, void *stream);
 
+/* ------------------------------------------------------------------------
+ * Decaying linear attention with its tangent flow (App. F: linear
+ * transformers, RetNet, RWKV-6 as general linear recurrences).  Per batch b
+ * and head h the state is a d_key x d_value matrix S with a per-key-dimension
+ * decay alpha_t = exp(g_t), g_t the log-decay (an input; g <= 0 decays):
+ *   S_t[i,j] = alpha_t[i]*S_{t-1}[i,j] + k_t[i]*v_t[j],  o_t[j] = sum_i q_t[i]*S_t[i,j]
+ * and, for each of K tangent directions (dq, dk, dv, dg) of the four input
+ * sequences, the total differential (d alpha = alpha*dg):
+ *   dS_t = alpha*dS_{t-1} + (alpha*dg)*S_{t-1} + dk*v^T + k*dv^T
+ *   do_t = S_t^T dq + dS_t^T q
+ * RetNet is a constant scalar decay, a linear transformer without
+ * normaliser g = 0.  As for the SSM, only the O(B*H*dk*dv*(1+K)) state
+ * crosses from one block of steps to the next and the workspace does not
+ * depend on L.
+ * ------------------------------------------------------------------------ */
+typedef struct pgf_la_params {
+    /* Sizes.  Supported: d_key in {16, 32, 64}; d_value a multiple of 64
+     * (at most 4096); n_dirs in {1, 2}; batch, heads >= 1; seqlen >= 0. */
+    int64_t batch, heads, seqlen, d_key, d_value, n_dirs;
+    /* Tiling overrides as in pgf_params (0 = default, seg_len -1 =
+     * sequential in L); results are bit-identical for every chunk_segs at
+     * a fixed seg_len. */
+    int32_t seg_len, chunk_segs;
+    /* Optional state hand-off (device, f32; NULL = zero in / not written):
+     * S [B,H,dk,dv], dS [K,B,H,dk,dv]. */
+    const float *S_in, *dS_in;
+    float *S_out, *dS_out;
+    /* Scratch (device), at least pgf_la_workspace_bytes(p), 256-byte aligned. */
+    void *workspace;
+    size_t workspace_bytes;
+} pgf_la_params;
+
+/* Workspace bytes for these sizes (0 if invalid or unsupported).  Host only. */
+size_t pgf_la_workspace_bytes(const pgf_la_params *p);
+
+/* Tiling of a call (n_per_thread = d_key, n_split = 1).  Host only. */
+int pgf_la_plan(const pgf_la_params *p, pgf_plan_info *info);
+
+/* The primal and tangent scan.  All arrays device, f32, dense row-major:
+ *   q, k, g      [B,H,L,dk]        v   [B,H,L,dv]                 (read)
+ *   dq, dk, dg   [K,B,H,L,dk]      dv  [K,B,H,L,dv]               (read)
+ *   o            [B,H,L,dv]        do_ [K,B,H,L,dv]   (fully overwritten)
+ * o and do_ must not overlap any input or each other.  Conventions as
+ * pgf_scan_jvp (asynchronous on stream, checks before any launch, current
+ * device). */
+int pgf_la_scan_jvp(const float *q, const float *k, const float *v, const float *g,
+                    const float *dq, const float *dk, const float *dv, const float *dg,
+                    const pgf_la_params *p, float *o, float *do_, void *stream);
+
 /* Static string for a status code. */
 const char *pgf_status_string(int status);
 

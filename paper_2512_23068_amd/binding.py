@@ -41,6 +41,16 @@ class PgfParams(ctypes.Structure):
     ]
 
 
+class PgfLaParams(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int64), ("heads", ctypes.c_int64), ("seqlen", ctypes.c_int64),
+        ("d_key", ctypes.c_int64), ("d_value", ctypes.c_int64), ("n_dirs", ctypes.c_int64),
+        ("seg_len", ctypes.c_int32), ("chunk_segs", ctypes.c_int32),
+        ("S_in", _c_f), ("dS_in", _c_f), ("S_out", _c_f), ("dS_out", _c_f),
+        ("workspace", _c_f), ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
 class PgfPlanInfo(ctypes.Structure):
     _fields_ = [
         ("n_per_thread", ctypes.c_int32), ("n_split", ctypes.c_int32), ("seg_len", ctypes.c_int32),
@@ -50,7 +60,8 @@ class PgfPlanInfo(ctypes.Structure):
 
 
 EXPORTED = ("pgf_workspace_bytes", "pgf_plan", "pgf_scan_jvp", "pgf_scan_jvp2", "pgf_param_grads",
-            "pgf_status_string", "pgf_timing_enable", "pgf_timing_read")
+            "pgf_la_workspace_bytes", "pgf_la_plan", "pgf_la_scan_jvp", "pgf_status_string", "pgf_timing_enable",
+            "pgf_timing_read")
 
 _lib = None
 
@@ -77,6 +88,13 @@ def lib():
     L.pgf_param_grads.restype = ctypes.c_int
     L.pgf_param_grads.argtypes = [ctypes.c_void_p, ctypes.c_void_p, P, ctypes.c_void_p, ctypes.c_void_p,
                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    LP = ctypes.POINTER(PgfLaParams)
+    L.pgf_la_workspace_bytes.restype = ctypes.c_size_t
+    L.pgf_la_workspace_bytes.argtypes = [LP]
+    L.pgf_la_plan.restype = ctypes.c_int
+    L.pgf_la_plan.argtypes = [LP, ctypes.POINTER(PgfPlanInfo)]
+    L.pgf_la_scan_jvp.restype = ctypes.c_int
+    L.pgf_la_scan_jvp.argtypes = [ctypes.c_void_p] * 8 + [LP, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     L.pgf_status_string.restype = ctypes.c_char_p
     L.pgf_status_string.argtypes = [ctypes.c_int]
     L.pgf_timing_enable.restype = ctypes.c_int
@@ -299,6 +317,73 @@ def param_grads(x: torch.Tensor, gy: torch.Tensor, params: dict, *, h_in=None, g
                                 _ptr(grads[2]), ctypes.c_void_p(st))
     _check(rc)
     return (y,) + grads + states
+
+
+def make_la_params(B, H, L, DK, DV, K, seg_len=0, chunk_segs=0) -> PgfLaParams:
+    p = PgfLaParams()
+    p.batch, p.heads, p.seqlen, p.d_key, p.d_value, p.n_dirs = int(B), int(H), int(L), int(DK), int(DV), int(K)
+    p.seg_len, p.chunk_segs = int(seg_len), int(chunk_segs)
+    return p
+
+
+def la_plan(B, H, L, DK, DV, K, seg_len=0, chunk_segs=0) -> dict:
+    info = PgfPlanInfo()
+    _check(lib().pgf_la_plan(ctypes.byref(make_la_params(B, H, L, DK, DV, K, seg_len, chunk_segs)),
+                             ctypes.byref(info)))
+    return {f: getattr(info, f) for f, _ in PgfPlanInfo._fields_}
+
+
+def la_scan_jvp(q, k, v, g, dq, dk, dv, dg, *, S_in=None, dS_in=None, return_state=False, seg_len=0,
+                chunk_segs=0, workspace=None, out=None, stream=None):
+    """Decaying linear attention and its tangent flow on the GPU.
+
+    q, k, g [B,H,L,dk]; v [B,H,L,dv]; dq, dk, dg [K,B,H,L,dk]; dv [K,B,H,L,dv]:
+    float32 CUDA tensors (g is the log-decay).  Returns (o [B,H,L,dv],
+    do [K,B,H,L,dv]), plus (S_out [B,H,dk,dv], dS_out [K,B,H,dk,dv]) when
+    return_state.  Asynchronous on the current stream.
+    """
+    L_ = lib()
+    ts = [q, k, v, g, dq, dk, dv, dg]
+    if not all(isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == torch.float32 for t in ts):
+        raise ValueError("q, k, v, g, dq, dk, dv, dg must be float32 device tensors")
+    if q.dim() != 4 or dq.dim() != 5:
+        raise ValueError("shapes: q, k, g [B,H,L,dk], v [B,H,L,dv], tangents with a leading K")
+    B, H, L, DK = q.shape
+    DV = v.shape[-1]
+    K = dq.shape[0]
+    for t, shape in ((k, (B, H, L, DK)), (g, (B, H, L, DK)), (v, (B, H, L, DV)), (dq, (K, B, H, L, DK)),
+                     (dk, (K, B, H, L, DK)), (dg, (K, B, H, L, DK)), (dv, (K, B, H, L, DV))):
+        if tuple(t.shape) != shape:
+            raise ValueError(f"expected shape {shape}, got {tuple(t.shape)}")
+    ts = [t.contiguous() for t in ts]
+    dev = q.device
+    pr = make_la_params(B, H, L, DK, DV, K, seg_len, chunk_segs)
+    S_in = _dev_param(S_in, (B, H, DK, DV), dev, "S_in")
+    dS_in = _dev_param(dS_in, (K, B, H, DK, DV), dev, "dS_in")
+    pr.S_in = None if S_in is None else S_in.data_ptr()
+    pr.dS_in = None if dS_in is None else dS_in.data_ptr()
+    states = ()
+    if return_state:
+        S_out = torch.empty((B, H, DK, DV), device=dev, dtype=torch.float32)
+        dS_out = torch.empty((K, B, H, DK, DV), device=dev, dtype=torch.float32)
+        pr.S_out, pr.dS_out = S_out.data_ptr(), dS_out.data_ptr()
+        states = (S_out, dS_out)
+    nbytes = int(L_.pgf_la_workspace_bytes(ctypes.byref(pr)))
+    if nbytes == 0:
+        _check(L_.pgf_la_plan(ctypes.byref(pr), ctypes.byref(PgfPlanInfo())))
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), device=dev, dtype=torch.uint8)
+    pr.workspace, pr.workspace_bytes = workspace.data_ptr(), workspace.numel()
+    if out is not None:
+        o, do = out
+    else:
+        o = torch.empty((B, H, L, DV), device=dev, dtype=torch.float32)
+        do = torch.empty((K, B, H, L, DV), device=dev, dtype=torch.float32)
+    st = torch.cuda.current_stream(dev).cuda_stream if stream is None else stream
+    with torch.cuda.device(dev):
+        rc = L_.pgf_la_scan_jvp(*[_ptr(t) for t in ts], ctypes.byref(pr), _ptr(o), _ptr(do), ctypes.c_void_p(st))
+    _check(rc)
+    return (o, do) + states
 
 
 def timing_enable(on: bool = True):

@@ -1,0 +1,459 @@
+// libpgf: decaying linear attention with its tangent flow (App. F: linear
+// transformers, RetNet and RWKV-6 as general linear recurrences) for gfx950.
+//
+// The state of one (batch, head) is a dk x dv matrix S.  A block owns 64
+// value columns j of one head (one lane each) and splits the key dimension
+// over its waves: wave w holds S[16w .. 16w+15, j] (and the tangents) in
+// registers.  Every lane of a wave needs the same 16 key-side values per
+// step (q, k, alpha = exp(g), their tangents): they are read with scalar
+// loads, 16 floats per field and step.  The per-lane inputs are v[j] and
+// dv_k[j]; each wave's partial outputs of a tile of steps are summed over
+// the waves through LDS in a fixed order.
+//
+// Kernels, per host block of steps [t0, t0+len):
+//   k_la_prep      alpha = exp(g) and alpha*dg_k per step into records, and
+//                  the segment sums of g and dg_k
+//   k_la_scan<false>  zero-start segment aggregates (end states)
+//   k_la_carry     sequential over the block's segments, per lane: a segment
+//                  maps (S, dS_k) to (P S + S0, P dS_k + Q_k S + dS0_k) with
+//                  P = exp(sum g), Q_k = P sum dg_k (multiplications only)
+//   k_la_scan<true>   rescan from the true entry states, writes o and do_k
+// The sequential evaluation (enough columns to fill the GPU) runs k_la_prep
+// and k_la_scan<true> only.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "pgf_plan.h"
+#include "pgf_timing.h"
+
+namespace pgf {
+namespace la {
+
+constexpr int kThreads = 256;       // threads per block of the elementwise kernels
+constexpr int kSlice = 16;          // key dimensions per wave in the scan
+constexpr float kLog2eHi = 1.44269502162933349609375f;  // log2(e) rounded to f32
+constexpr float kLog2eLo = 1.925963033500011079e-08f;   // log2(e) - kLog2eHi
+constexpr float kLn2 = 0.693147180559945309f;
+
+// e^v within a few ulp for moderate |v|: v*log2(e) split into p + lo (an fma
+// recovers the rounding of p), 2^p from the hardware exponential and
+// 2^lo ~ 1 + lo*ln2 as a correction.
+__device__ __forceinline__ float exp_acc(float v) {
+    const float p = v * kLog2eHi;
+    const float lo = fmaf(v, kLog2eHi, -p) + v * kLog2eLo;
+    const float e = __builtin_amdgcn_exp2f(p);
+    return fmaf(e, lo * kLn2, e);
+}
+
+// ---------------------------------------------------------------- records
+// Thread (segment g, key index i) of head bh, over the segment's steps:
+//   rec[bh][t] = [alpha | alpha*dg_0 | ..]  (DK each), alpha = exp(g),
+// and, when sums is set, the segment sums sums[bh][g][0][i] = sum_t g_t[i],
+// sums[bh][g][1+k][i] = sum_t dg_k,t[i].  Reads and writes along i are
+// coalesced.
+template <int DK, int K>
+__global__ __launch_bounds__(kThreads) void k_la_prep(
+    const float *__restrict__ g, const float *__restrict__ dg, float *__restrict__ rec, float *__restrict__ sums,
+    int64_t BH, int64_t L, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    constexpr int SPB = kThreads / DK;   // segments per block
+    constexpr int R = (1 + K) * DK;
+    const int tid = threadIdx.x;
+    const int i = tid % DK;
+    const int gs = blockIdx.x * SPB + tid / DK;
+    const int64_t bh = blockIdx.y;
+    if (gs >= G) return;
+    const int64_t ts = (int64_t)gs * S;
+    const int64_t te = ts + S < len ? ts + S : len;
+    const int64_t row0 = bh * L + t0;        // row of (bh, t0) in g
+    const int64_t kst = BH * L;              // rows between tangent directions
+    float *rb = rec + bh * Tc * R + i;
+    float sg = 0.0f, sdg[K];
+#pragma unroll
+    for (int kk = 0; kk < K; ++kk) sdg[kk] = 0.0f;
+    for (int64_t t = ts; t < te; ++t) {
+        const float gv = g[(row0 + t) * DK + i];
+        const float a = exp_acc(gv);
+        sg += gv;
+        float *r = rb + t * R;
+        r[0] = a;
+#pragma unroll
+        for (int kk = 0; kk < K; ++kk) {
+            const float dgv = dg[(kk * kst + row0 + t) * DK + i];
+            sdg[kk] += dgv;
+            r[(1 + kk) * DK] = a * dgv;
+        }
+    }
+    if (sums) {
+        float *sb = sums + (bh * G + gs) * (1 + K) * DK + i;
+        sb[0] = sg;
+#pragma unroll
+        for (int kk = 0; kk < K; ++kk) sb[(1 + kk) * DK] = sdg[kk];
+    }
+}
+
+// ---------------------------------------------------------------- scan
+// Grid (BH*DV/64, G); block of 64*NW threads (NW = DK/16 waves): block x ->
+// (head bh, 64-column group), wave w -> key slice [16w, 16w+16), lane ->
+// column j.  OUT=false: segment aggregate from a zero state into agg_h.
+// OUT=true: scan from the entry state at init[bh*ibs + g*igs + c*ics +
+// i*DV + j] and write o, do_k; end_state (sequential evaluation) receives
+// the exit state with the same indexing.  Outputs of a tile of TT steps are
+// reduced over the NW waves through LDS (double-buffered, one barrier per
+// tile), slice 0 first.
+template <int DK, int K, bool OUT>
+__global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per_eu(K == 1 ? 4 : 3))) void k_la_scan(
+    const float *__restrict__ q, const float *__restrict__ k, const float *__restrict__ v,
+    const float *__restrict__ dq, const float *__restrict__ dk, const float *__restrict__ dv,
+    const float *__restrict__ rec, const float *init, int64_t ibs, int64_t igs, int64_t ics,
+    float *__restrict__ o, float *__restrict__ do_, float *end_state, float *__restrict__ agg_h,
+    int64_t BH, int64_t L, int64_t DV, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    constexpr int NW = DK / kSlice;
+    constexpr int R = (1 + K) * DK;   // floats per step record
+    constexpr int TT = 4;             // steps per tile
+    __shared__ float red[OUT ? 2 : 1][TT][1 + K][NW][64];
+
+    const int lane = threadIdx.x % 64;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+    const int64_t groups = DV / 64;
+    const int64_t bh = blockIdx.x / groups;
+    const int64_t j = (blockIdx.x % groups) * 64 + lane;
+    const int g = blockIdx.y;
+    const int64_t ts = (int64_t)g * S;
+    const int64_t te = ts + S < len ? ts + S : len;
+    if (ts >= te) return;   // uniform over the block
+    const int i0 = w * kSlice;
+
+    float Sm[kSlice], dS[K][kSlice];
+    if constexpr (OUT) {
+        const float *ib = init + bh * ibs + g * igs + (int64_t)i0 * DV + j;
+#pragma unroll
+        for (int i = 0; i < kSlice; ++i) {
+            Sm[i] = ib[i * DV];
+#pragma unroll
+            for (int kk = 0; kk < K; ++kk) dS[kk][i] = ib[(1 + kk) * ics + i * DV];
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < kSlice; ++i) {
+            Sm[i] = 0.0f;
+#pragma unroll
+            for (int kk = 0; kk < K; ++kk) dS[kk][i] = 0.0f;
+        }
+    }
+
+    const int64_t kst = BH * L;                       // rows between tangent directions
+    const int64_t row0 = bh * L + t0;
+    // Wave-uniform bases of this block of steps for the wave's key slice;
+    // per-step offsets t*DK stay below 2^30 elements (checked by the planner).
+    const float *kb = k + row0 * DK + i0;
+    const float *qb = q + row0 * DK + i0;
+    const float *rb = rec + bh * Tc * R + i0;
+    const float *dkb[K], *dqb[K];
+#pragma unroll
+    for (int kk = 0; kk < K; ++kk) {
+        dkb[kk] = dk + (kk * kst + row0) * DK + i0;
+        dqb[kk] = dq + (kk * kst + row0) * DK + i0;
+    }
+    const float *vb = v + row0 * DV + j;
+
+    // One step t of the recurrence for this wave's key slice: the state
+    // update (alpha, k and the tangents' alpha*dg, dk), then the partial
+    // outputs (q, dq) summed over the slice.  The two phases read disjoint
+    // key-side fields, which bounds the scalar registers a step holds.
+    auto step = [&](int64_t t, float vv, const float *dvv, float *part) {
+        const uint32_t tr = (uint32_t)t * (uint32_t)R, tk = (uint32_t)t * (uint32_t)DK;
+#pragma unroll
+        for (int i = 0; i < kSlice; ++i) {
+            const float a = rb[tr + i], ki = kb[tk + i];
+            const float sn = fmaf(ki, vv, a * Sm[i]);
+#pragma unroll
+            for (int kk = 0; kk < K; ++kk) {
+                const float adg = rb[tr + (1 + kk) * DK + i];
+                const float dki = dkb[kk][tk + i];
+                dS[kk][i] = fmaf(a, dS[kk][i], fmaf(adg, Sm[i], fmaf(dki, vv, ki * dvv[kk])));
+            }
+            Sm[i] = sn;
+        }
+        if constexpr (OUT) {
+            float ov = 0.0f, dov[K];
+#pragma unroll
+            for (int kk = 0; kk < K; ++kk) dov[kk] = 0.0f;
+#pragma unroll
+            for (int i = 0; i < kSlice; ++i) {
+                const float qi = qb[tk + i];
+                ov = fmaf(qi, Sm[i], ov);
+#pragma unroll
+                for (int kk = 0; kk < K; ++kk) dov[kk] = fmaf(dqb[kk][tk + i], Sm[i], fmaf(qi, dS[kk][i], dov[kk]));
+            }
+            part[0] = ov;
+#pragma unroll
+            for (int kk = 0; kk < K; ++kk) part[1 + kk] = dov[kk];
+        }
+    };
+    auto load_vdv = [&](int64_t t, float &vv, float *dvv) {
+        vv = vb[t * DV];
+#pragma unroll
+        for (int kk = 0; kk < K; ++kk) dvv[kk] = dv[(kk * kst + row0 + t) * DV + j];
+    };
+
+    // Tiles of TT steps (the last one partial), v and dv of the next tile in
+    // flight.  Every trip of the tile loop is taken by the whole block.
+    float vc[TT], dvc[TT][K];
+#pragma unroll
+    for (int jj = 0; jj < TT; ++jj) load_vdv(ts + jj < te ? ts + jj : te - 1, vc[jj], dvc[jj]);
+    int buf = 0;
+    for (int64_t tb = ts; tb < te; tb += TT) {
+        float vn[TT], dvn[TT][K];
+#pragma unroll
+        for (int jj = 0; jj < TT; ++jj) {
+            const int64_t t = tb + TT + jj < te ? tb + TT + jj : te - 1;
+            load_vdv(t, vn[jj], dvn[jj]);
+        }
+        float part[TT][1 + K];
+        if (tb + TT <= te) {
+#pragma unroll
+            for (int jj = 0; jj < TT; ++jj) step(tb + jj, vc[jj], dvc[jj], part[jj]);
+        } else {
+            for (int jj = 0; jj < TT; ++jj)
+                if (tb + jj < te) step(tb + jj, vc[jj], dvc[jj], part[jj]);
+        }
+        if constexpr (OUT) {
+#pragma unroll
+            for (int jj = 0; jj < TT; ++jj)
+#pragma unroll
+                for (int c = 0; c <= K; ++c) red[buf][jj][c][w][lane] = part[jj][c];
+            __syncthreads();
+            // wave w completes steps jj = w, w + NW, ... of the tile
+            for (int jj = w; jj < TT; jj += NW) {
+                const int64_t t = tb + jj;
+                if (t >= te) break;
+#pragma unroll
+                for (int c = 0; c <= K; ++c) {
+                    float acc = red[buf][jj][c][0][lane];
+#pragma unroll
+                    for (int s = 1; s < NW; ++s) acc += red[buf][jj][c][s][lane];
+                    if (c == 0) o[(row0 + t) * DV + j] = acc;
+                    else do_[((c - 1) * kst + row0 + t) * DV + j] = acc;
+                }
+            }
+            buf ^= 1;
+        }
+#pragma unroll
+        for (int jj = 0; jj < TT; ++jj) {
+            vc[jj] = vn[jj];
+#pragma unroll
+            for (int kk = 0; kk < K; ++kk) dvc[jj][kk] = dvn[jj][kk];
+        }
+    }
+
+    if constexpr (OUT) {
+        if (end_state) {
+            float *eb = end_state + bh * ibs + (int64_t)i0 * DV + j;
+#pragma unroll
+            for (int i = 0; i < kSlice; ++i) {
+                eb[i * DV] = Sm[i];
+#pragma unroll
+                for (int kk = 0; kk < K; ++kk) eb[(1 + kk) * ics + i * DV] = dS[kk][i];
+            }
+        }
+    } else {
+        float *ab = agg_h + (bh * G + g) * (1 + K) * DK * DV + (int64_t)i0 * DV + j;
+#pragma unroll
+        for (int i = 0; i < kSlice; ++i) {
+            ab[i * DV] = Sm[i];
+#pragma unroll
+            for (int kk = 0; kk < K; ++kk) ab[((1 + kk) * DK + i) * DV] = dS[kk][i];
+        }
+    }
+}
+
+// ---------------------------------------------------------------- carry
+// One thread per lane (bh, i, j), sequential over the block's segments.
+// state [(1+K)][BH][DK][DV] enters and leaves; seg [BH][G][(1+K)][DK][DV]
+// holds each segment's zero-start end state on entry and is overwritten with
+// the true state entering the segment.  sums [BH][G][(1+K)][DK] as written
+// by k_la_prep.
+template <int K>
+__global__ __launch_bounds__(kThreads) void k_la_carry(
+    float *__restrict__ seg, const float *__restrict__ sums, float *__restrict__ state, int64_t BH, int64_t DK,
+    int64_t DV, int G) {
+    constexpr int GB = K == 1 ? 16 : 8;
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t per = DK * DV;
+    if (idx >= BH * per) return;
+    const int64_t bh = idx / per, r = idx % per, i = r / DV;
+    const int64_t cs = BH * per;
+    float s = state[idx], ds[K];
+#pragma unroll
+    for (int kk = 0; kk < K; ++kk) ds[kk] = state[(1 + kk) * cs + idx];
+    for (int g0 = 0; g0 < G; g0 += GB) {
+        float e0[GB], e1[K][GB], sg[GB], sdg[K][GB];
+#pragma unroll
+        for (int jj = 0; jj < GB; ++jj) {
+            const int g = g0 + jj < G ? g0 + jj : G - 1;
+            const int64_t base = (bh * G + g) * (1 + K);
+            e0[jj] = seg[base * per + r];
+            sg[jj] = sums[base * DK + i];
+#pragma unroll
+            for (int kk = 0; kk < K; ++kk) {
+                e1[kk][jj] = seg[(base + 1 + kk) * per + r];
+                sdg[kk][jj] = sums[(base + 1 + kk) * DK + i];
+            }
+        }
+#pragma unroll
+        for (int jj = 0; jj < GB; ++jj) {
+            if (g0 + jj >= G) break;
+            const int64_t base = (bh * G + g0 + jj) * (1 + K);
+            seg[base * per + r] = s;
+#pragma unroll
+            for (int kk = 0; kk < K; ++kk) seg[(base + 1 + kk) * per + r] = ds[kk];
+            const float P = exp_acc(sg[jj]);
+#pragma unroll
+            for (int kk = 0; kk < K; ++kk) ds[kk] = fmaf(P, ds[kk], fmaf(P * sdg[kk][jj], s, e1[kk][jj]));
+            s = fmaf(P, s, e0[jj]);
+        }
+    }
+    state[idx] = s;
+#pragma unroll
+    for (int kk = 0; kk < K; ++kk) state[(1 + kk) * cs + idx] = ds[kk];
+}
+
+// ---------------------------------------------------------------- state in/out
+// dst[i] = src ? src[i] : 0 over n floats (the state layout is the ABI's).
+__global__ __launch_bounds__(kThreads) void k_la_copy(const float *__restrict__ src, float *__restrict__ dst,
+                                                      int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < n) dst[i] = src ? src[i] : 0.0f;
+}
+
+// ---------------------------------------------------------------- dispatch
+struct LaLauncher {
+    const LaPlan &q;
+    const pgf_la_params &p;
+    const float *qv, *kv, *vv, *gv, *dqv, *dkv, *dvv, *dgv;
+    float *o, *dov;
+    hipStream_t st;
+    char *ws;
+
+    float *state() const { return (float *)(ws + q.state); }
+    float *rec() const { return (float *)(ws + q.rec); }
+    float *agg_h() const { return (float *)(ws + q.agg_h); }
+    float *agg_s() const { return (float *)(ws + q.agg_s); }
+
+    template <int DK, int K>
+    void block(int64_t t0, int64_t len) {
+        const int64_t ND = DK * q.DV;
+        const unsigned gx = (unsigned)(q.BH * q.DV / 64);
+        const dim3 blk(64 * (DK / kSlice));
+        const int64_t S = q.seg ? q.seg : len;
+        const int G = (int)((len + S - 1) / S);
+        {
+            constexpr int SPB = kThreads / DK;
+            Timed tm(0, st);
+            hipLaunchKernelGGL((k_la_prep<DK, K>), dim3((unsigned)((G + SPB - 1) / SPB), (unsigned)q.BH),
+                               dim3(kThreads), 0, st, gv, dgv, rec(), q.seg ? agg_s() : (float *)nullptr, q.BH, q.L,
+                               t0, len, q.chunk_len, S, G);
+        }
+        if (q.seg == 0) {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_la_scan<DK, K, true>), dim3(gx, 1), blk, 0, st, qv, kv, vv, dqv, dkv, dvv,
+                               (const float *)rec(), (const float *)state(), ND, (int64_t)0, q.BH * ND, o, dov,
+                               state(), (float *)nullptr, q.BH, q.L, q.DV, t0, len, q.chunk_len, len, 1);
+            return;
+        }
+        {
+            Timed tm(1, st);
+            hipLaunchKernelGGL((k_la_scan<DK, K, false>), dim3(gx, (unsigned)G), blk, 0, st, qv, kv, vv, dqv, dkv,
+                               dvv, (const float *)rec(), (const float *)nullptr, (int64_t)0, (int64_t)0, (int64_t)0,
+                               o, dov, (float *)nullptr, agg_h(), q.BH, q.L, q.DV, t0, len, q.chunk_len, S, G);
+        }
+        {
+            const int64_t lanes = q.BH * ND;
+            Timed tm(2, st);
+            hipLaunchKernelGGL((k_la_carry<K>), dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads),
+                               0, st, agg_h(), (const float *)agg_s(), state(), q.BH, (int64_t)DK, q.DV, G);
+        }
+        {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_la_scan<DK, K, true>), dim3(gx, (unsigned)G), blk, 0, st, qv, kv, vv, dqv, dkv,
+                               dvv, (const float *)rec(), (const float *)agg_h(), (int64_t)G * (1 + K) * ND,
+                               (int64_t)(1 + K) * ND, ND, o, dov, (float *)nullptr, (float *)nullptr, q.BH, q.L, q.DV,
+                               t0, len, q.chunk_len, S, G);
+        }
+    }
+
+    template <int DK, int K>
+    int run_t() {
+        const int64_t nst = q.BH * DK * q.DV;   // floats per state component
+        const unsigned gs = (unsigned)((nst + kThreads - 1) / kThreads);
+        {
+            Timed tm(4, st);
+            hipLaunchKernelGGL(k_la_copy, dim3(gs), dim3(kThreads), 0, st, p.S_in, state(), nst);
+            for (int kk = 0; kk < K; ++kk)
+                hipLaunchKernelGGL(k_la_copy, dim3(gs), dim3(kThreads), 0, st,
+                                   p.dS_in ? p.dS_in + kk * nst : (const float *)nullptr, state() + (1 + kk) * nst,
+                                   nst);
+        }
+        for (int64_t t0 = 0; t0 < q.L; t0 += q.chunk_len) {
+            const int64_t len = q.L - t0 < q.chunk_len ? q.L - t0 : q.chunk_len;
+            block<DK, K>(t0, len);
+        }
+        if (p.S_out || p.dS_out) {
+            Timed tm(4, st);
+            if (p.S_out)
+                hipLaunchKernelGGL(k_la_copy, dim3(gs), dim3(kThreads), 0, st, (const float *)state(), p.S_out, nst);
+            if (p.dS_out)
+                hipLaunchKernelGGL(k_la_copy, dim3((unsigned)((K * nst + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                                   st, (const float *)(state() + nst), p.dS_out, K * nst);
+        }
+        return hipGetLastError() == hipSuccess ? PGF_OK : PGF_ERR_HIP;
+    }
+
+    int run() {
+        switch (q.DK * 10 + q.K) {
+            case 161: return run_t<16, 1>();
+            case 162: return run_t<16, 2>();
+            case 321: return run_t<32, 1>();
+            case 322: return run_t<32, 2>();
+            case 641: return run_t<64, 1>();
+            case 642: return run_t<64, 2>();
+            default: return PGF_ERR_UNSUPPORTED;
+        }
+    }
+};
+
+bool overlap(const void *a, size_t na, const void *b, size_t nb) {
+    const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
+    return na && nb && pa < pb + nb && pb < pa + na;
+}
+
+}  // namespace la
+}  // namespace pgf
+
+extern "C" int pgf_la_scan_jvp(const float *q, const float *k, const float *v, const float *g, const float *dq,
+                               const float *dk, const float *dv, const float *dg, const pgf_la_params *p, float *o,
+                               float *do_, void *stream) {
+    using namespace pgf;
+    LaPlan pl;
+    const int rc = make_la_plan(p, &pl);
+    if (rc != PGF_OK) return rc;
+    if (!p->workspace || p->workspace_bytes < pl.total || ((uintptr_t)p->workspace & 255))
+        return PGF_ERR_WORKSPACE;
+    if (pl.L > 0) {
+        if (!q || !k || !v || !g || !dq || !dk || !dv || !dg || !o || !do_) return PGF_ERR_INVALID_ARG;
+        const size_t f = sizeof(float);
+        const size_t nk = (size_t)pl.BH * pl.L * pl.DK * f, nv = (size_t)pl.BH * pl.L * pl.DV * f;
+        const void *ins[8] = {q, k, v, g, dq, dk, dv, dg};
+        const size_t sz[8] = {nk, nk, nv, nk, nk * pl.K, nk * pl.K, nv * pl.K, nk * pl.K};
+        for (int i = 0; i < 8; ++i)
+            if (la::overlap(o, nv, ins[i], sz[i]) || la::overlap(do_, nv * pl.K, ins[i], sz[i]))
+                return PGF_ERR_INVALID_ARG;
+        if (la::overlap(o, nv, do_, nv * pl.K) || la::overlap(o, nv, p->workspace, pl.total) ||
+            la::overlap(do_, nv * pl.K, p->workspace, pl.total))
+            return PGF_ERR_INVALID_ARG;
+    }
+    (void)hipGetLastError();
+    la::LaLauncher l{pl, *p, q, k, v, g, dq, dk, dv, dg, o, do_, (hipStream_t)stream, (char *)p->workspace};
+    return l.run();
+}

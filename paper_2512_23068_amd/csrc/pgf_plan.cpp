@@ -153,7 +153,94 @@ int make_plan(const pgf_params *p, Plan *plan) {
     return PGF_OK;
 }
 
+int make_la_plan(const pgf_la_params *p, LaPlan *plan) {
+    if (!p || !plan) return PGF_ERR_INVALID_ARG;
+    const int64_t B = p->batch, H = p->heads, L = p->seqlen, DK = p->d_key, DV = p->d_value, K = p->n_dirs;
+    if (B < 1 || H < 1 || L < 0 || DK < 1 || DV < 1 || K < 1) return PGF_ERR_INVALID_ARG;
+    if (!(DK == 16 || DK == 32 || DK == 64)) return PGF_ERR_UNSUPPORTED;
+    if (DV % 64 != 0 || DV > 4096) return PGF_ERR_UNSUPPORTED;
+    if (K > 2) return PGF_ERR_UNSUPPORTED;
+    if (B * H > (int64_t(1) << 20) || L > (int64_t(1) << 40)) return PGF_ERR_UNSUPPORTED;
+    if ((double)K * B * H * (double)L * DV > 9.0e18 / 16) return PGF_ERR_UNSUPPORTED;
+    LaPlan q{};
+    q.B = B; q.H = H; q.L = L; q.DK = DK; q.DV = DV; q.K = K; q.BH = B * H;
+    // Scan blocks of one segment column, counted in 256-thread units (a
+    // block holds 64 value columns and DK/16 waves).
+    const int64_t nblk = (q.BH * DV / 64 * (DK / 16) + 3) / 4;
+    int64_t seg;
+    if (p->seg_len == -1) {
+        seg = 0;
+    } else if (p->seg_len != 0) {
+        if (p->seg_len < 16 || p->seg_len > kMaxSeg || !is_pow2(p->seg_len)) return PGF_ERR_INVALID_ARG;
+        seg = p->seg_len;
+    } else {
+        seg = (nblk * 4 >= kSimds) ? 0 : 128;
+    }
+    if (p->chunk_segs < 0 || p->chunk_segs > kMaxChunkSegs) return PGF_ERR_INVALID_ARG;
+    // Per-step offsets of one host block stay below 2^30 elements.
+    constexpr int64_t kMaxBlockElems = int64_t(1) << 30;
+    const int64_t unit = seg ? seg : kSeqChunk;
+    if (unit * std::max(DK, DV) > kMaxBlockElems) return PGF_ERR_UNSUPPORTED;
+    const size_t f = sizeof(float);
+    int64_t cs;
+    if (seg == 0) {
+        cs = p->chunk_segs ? p->chunk_segs : 1;
+        q.chunk_len = cs * kSeqChunk;
+        q.chunk_segs = 1;
+    } else if (p->chunk_segs) {
+        cs = p->chunk_segs;
+        q.chunk_len = cs * seg;
+        q.chunk_segs = (int)cs;
+    } else {
+        // At least three rounds of resident blocks per launch, bounded by
+        // a workspace cap of 1 GiB.
+        const size_t per_seg = (size_t)q.BH * (1 + K) * ((size_t)DK * DV + DK) * f +
+                               (size_t)q.BH * seg * (1 + K) * DK * f;
+        const int64_t cap = std::max<int64_t>(1, (int64_t)(4 * kWorkspaceCap / per_seg));
+        cs = (3 * kResidentBlocks + nblk - 1) / nblk;
+        cs = std::min<int64_t>(std::min<int64_t>(cs, cap), kMaxChunkSegs);
+        cs = std::min<int64_t>(cs, kMaxChunkLen / seg);
+        cs = std::max<int64_t>(cs, 1);
+        q.chunk_len = cs * seg;
+        q.chunk_segs = (int)cs;
+    }
+    if (q.chunk_len * std::max(DK, DV) > kMaxBlockElems) return PGF_ERR_INVALID_ARG;
+    q.seg = (int)seg;
+    q.n_chunks = (L + q.chunk_len - 1) / q.chunk_len;
+    const size_t comp = (size_t)(1 + K);
+    size_t off = 0;
+    q.state = off; off = align256(off + comp * q.BH * DK * DV * f);
+    q.rec = off;   off = align256(off + (size_t)q.BH * q.chunk_len * (1 + K) * DK * f);
+    const size_t G = seg ? (size_t)q.chunk_segs : 1;
+    q.agg_h = off; off = align256(off + (size_t)q.BH * G * comp * DK * DV * f);
+    q.agg_s = off; off = align256(off + (size_t)q.BH * G * comp * DK * f);
+    q.total = off;
+    *plan = q;
+    return PGF_OK;
+}
+
 }  // namespace pgf
+
+extern "C" size_t pgf_la_workspace_bytes(const pgf_la_params *p) {
+    pgf::LaPlan q;
+    if (pgf::make_la_plan(p, &q) != PGF_OK) return 0;
+    return q.total;
+}
+
+extern "C" int pgf_la_plan(const pgf_la_params *p, pgf_plan_info *info) {
+    if (!info) return PGF_ERR_INVALID_ARG;
+    pgf::LaPlan q;
+    const int rc = pgf::make_la_plan(p, &q);
+    if (rc != PGF_OK) return rc;
+    info->n_per_thread = (int32_t)q.DK;
+    info->n_split = 1;
+    info->seg_len = q.seg;
+    info->chunk_segs = q.chunk_segs;
+    info->chunk_len = q.chunk_len;
+    info->n_chunks = q.n_chunks;
+    info->workspace_bytes = q.total;
+    return PGF_OK;
+}
 
 extern "C" size_t pgf_workspace_bytes(const pgf_params *p) {
     pgf::Plan q;

@@ -45,4 +45,21 @@ struct Plan {
 // Validates the size fields and fills *plan.  Returns PGF_OK or an error.
 int make_plan(const pgf_params *p, Plan *plan);
 
+// Decaying linear attention.  Workspace sections (256-byte aligned):
+//   state [(1+K)][BH][DK][DV]      state carried between host blocks (the
+//                                  layout of S and dS in the ABI)
+//   rec   [BH][Tc][(1+K)][DK]      per-step alpha = exp(g) and alpha*dg_k
+//   agg_h [BH][G][(1+K)][DK][DV]   segment end states from a zero start,
+//                                  then (in place) the true entry states
+//   agg_s [BH][G][(1+K)][DK]       segment sums of g and dg_k
+struct LaPlan {
+    int64_t B, H, L, DK, DV, K, BH;
+    int seg;             // segment length; 0 = sequential evaluation
+    int chunk_segs;
+    int64_t chunk_len, n_chunks;
+    size_t state, rec, agg_h, agg_s, total;
+};
+
+int make_la_plan(const pgf_la_params *p, LaPlan *plan);
+
 }  // namespace pgf

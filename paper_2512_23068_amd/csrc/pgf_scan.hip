@@ -27,6 +27,7 @@
 #include <vector>
 
 #include "pgf_plan.h"
+#include "pgf_timing.h"
 
 namespace pgf {
 
@@ -1386,48 +1387,6 @@ __global__ __launch_bounds__(kThreads) void k_state_export(
     }
 }
 
-// ---------------------------------------------------------------- timing
-namespace {
-struct Timing {
-    std::mutex mu;
-    bool on = false;
-    struct Rec { int kind; hipEvent_t a, b; };
-    std::vector<Rec> recs;
-    std::vector<hipEvent_t> pool;
-} g_timing;
-
-hipEvent_t take_event() {
-    if (!g_timing.pool.empty()) {
-        hipEvent_t e = g_timing.pool.back();
-        g_timing.pool.pop_back();
-        return e;
-    }
-    hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
-    return e;
-}
-
-// Brackets one launch with events when timing is on.
-struct Timed {
-    int kind;
-    hipStream_t st;
-    hipEvent_t a = nullptr, b = nullptr;
-    Timed(int k, hipStream_t s) : kind(k), st(s) {
-        if (!g_timing.on) return;
-        std::lock_guard<std::mutex> lk(g_timing.mu);
-        a = take_event();
-        b = take_event();
-        if (a) (void)hipEventRecord(a, st);
-    }
-    ~Timed() {
-        if (!a || !b) return;
-        (void)hipEventRecord(b, st);
-        std::lock_guard<std::mutex> lk(g_timing.mu);
-        g_timing.recs.push_back({kind, a, b});
-    }
-};
-}  // namespace
-
 // ---------------------------------------------------------------- dispatch
 template <typename InT>
 struct Launcher {
@@ -1800,32 +1759,4 @@ extern "C" int pgf_scan_jvp(const void *x, const void *dx, const pgf_params *p, 
 extern "C" int pgf_scan_jvp2(const void *x, const void *dx, const pgf_params *p, float *y, float *dy, float *d2y,
                              void *stream) {
     return pgf::scan_common(x, dx, p, y, dy, d2y, stream, 2);
-}
-
-extern "C" int pgf_timing_enable(int on) {
-    std::lock_guard<std::mutex> lk(pgf::g_timing.mu);
-    pgf::g_timing.on = on != 0;
-    return PGF_OK;
-}
-
-extern "C" int pgf_timing_read(double *ms, int64_t *launches) {
-    using namespace pgf;
-    std::lock_guard<std::mutex> lk(g_timing.mu);
-    for (int i = 0; i < PGF_TIMING_KINDS; ++i) {
-        if (ms) ms[i] = 0.0;
-        if (launches) launches[i] = 0;
-    }
-    int rc = PGF_OK;
-    for (auto &r : g_timing.recs) {
-        float t = 0.0f;
-        if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&t, r.a, r.b) != hipSuccess) rc = PGF_ERR_HIP;
-        if (r.kind >= 0 && r.kind < PGF_TIMING_KINDS) {
-            if (ms) ms[r.kind] += t;
-            if (launches) launches[r.kind] += 1;
-        }
-        g_timing.pool.push_back(r.a);
-        g_timing.pool.push_back(r.b);
-    }
-    g_timing.recs.clear();
-    return rc;
 }

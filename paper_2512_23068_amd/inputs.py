@@ -116,15 +116,16 @@ def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
     return (bits.astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
-def _normal_rows(out: np.ndarray, cfg: ScanConfig, stream: int, b: int, threads: int) -> None:
-    """Fill out[L, D] (float32) with N(0,1) draws, block-seeded."""
+def _normal_rows(out: np.ndarray, index: int, stream: int, b: int, threads: int) -> None:
+    """Fill out[L, D] (float32) with N(0,1) draws, block-seeded by the
+    workload index, the stream, the row group b and the block."""
     L = out.shape[0]
     nblk = (L + ROWS_PER_BLOCK - 1) // ROWS_PER_BLOCK
 
     def work(blk):
         r0 = blk * ROWS_PER_BLOCK
         r1 = min(L, r0 + ROWS_PER_BLOCK)
-        g = np.random.default_rng([SEED_ROOT, cfg.index, stream, b, blk])
+        g = np.random.default_rng([SEED_ROOT, index, stream, b, blk])
         g.standard_normal(out=out[r0:r1], dtype=np.float32)
 
     if threads <= 1 or nblk == 1:
@@ -144,7 +145,7 @@ def make_x(cfg: ScanConfig, threads: int | None = None) -> np.ndarray:
     threads = threads or _threads()
     x = np.empty((cfg.batch, cfg.seqlen, cfg.d_inner), dtype=np.float32)
     for b in range(cfg.batch):
-        _normal_rows(x[b], cfg, 0, b, threads)
+        _normal_rows(x[b], cfg.index, 0, b, threads)
     if cfg.in_dtype == "bf16":
         x = bf16_bits_to_f32(round_to_bf16_bits(x)).reshape(x.shape)
     return x
@@ -158,7 +159,7 @@ def make_dx(cfg: ScanConfig, threads: int | None = None) -> np.ndarray:
     if cfg.dx_kind == "normal":
         for k in range(K):
             for b in range(B):
-                _normal_rows(dx[k, b], cfg, 1 + k, b, threads)
+                _normal_rows(dx[k, b], cfg.index, 1 + k, b, threads)
         if cfg.in_dtype == "bf16":
             dx = bf16_bits_to_f32(round_to_bf16_bits(dx)).reshape(dx.shape)
     elif cfg.dx_kind == "impulse_t0_d0":
@@ -183,7 +184,7 @@ def make_adjoint(cfg: ScanConfig, threads: int | None = None) -> np.ndarray:
     threads = threads or _threads()
     gy = np.empty((cfg.batch, cfg.seqlen, cfg.d_inner), dtype=np.float32)
     for b in range(cfg.batch):
-        _normal_rows(gy[b], cfg, ADJOINT_STREAM, b, threads)
+        _normal_rows(gy[b], cfg.index, ADJOINT_STREAM, b, threads)
     return gy
 
 
@@ -194,4 +195,79 @@ def make_inputs(key, threads: int | None = None) -> dict:
     out["x"] = make_x(cfg, threads)
     out["dx"] = make_dx(cfg, threads)
     out["cfg"] = cfg
+    return out
+
+
+# ------------------------------------------------------------------ linear attention
+# Decaying linear attention (RWKV-6 / RetNet / GLA style), head-major layout.
+# Recipe per workload index i: q, k ~ N(0,1)/sqrt(dk), v ~ N(0,1); the
+# log-decay g_t[h,j] = -exp(c[h,j] + 0.5*xi_t[h,j]) with c ~ U(ln 1e-3, ln 1e-1)
+# per (head, key dim) and xi ~ N(0,1) per step (a data-dependent decay whose
+# per-step rates lie mostly between 0.9 and 0.999); tangent directions
+# dq, dk ~ N(0,1)/sqrt(dk), dv ~ N(0,1), dg = g * N(0,1) (a relative change
+# of the decay rate).  Sequence draws are block-seeded like the SSM inputs,
+# with streams 200 + field.
+
+@dataclasses.dataclass(frozen=True)
+class LaConfig:
+    name: str
+    index: int
+    batch: int
+    heads: int
+    seqlen: int
+    d_key: int
+    d_value: int
+    n_dirs: int
+
+    def with_(self, **kw) -> "LaConfig":
+        return dataclasses.replace(self, **kw)
+
+    @property
+    def tok_ch(self) -> int:
+        return self.batch * self.seqlen * self.heads * self.d_value
+
+
+LA_CONFIGS = [
+    LaConfig("la_tiny", 10, 1, 2, 512, 16, 64, 1),
+    LaConfig("rwkv128k", 11, 1, 32, 131072, 64, 64, 1),
+]
+LA_BY_NAME = {c.name: c for c in LA_CONFIGS}
+
+LA_FIELDS = ("q", "k", "v", "xi", "dq", "dk", "dv", "dg")
+
+
+def _la_rows(cfg: LaConfig, field: int, shape_tail, threads: int) -> np.ndarray:
+    """N(0,1) draws [B,H,L,*tail] for one field, block-seeded per (b, h)."""
+    B, H, L = cfg.batch, cfg.heads, cfg.seqlen
+    out = np.empty((B, H, L) + tuple(shape_tail), dtype=np.float32)
+    for b in range(B):
+        for h in range(H):
+            _normal_rows(out[b, h].reshape(L, -1), cfg.index, 200 + field, b * H + h, threads)
+    return out
+
+
+def make_la_inputs(key, threads: int | None = None) -> dict:
+    """q, k, v, g and the tangents dq, dk, dv, dg (float32) of a workload."""
+    cfg = key if isinstance(key, LaConfig) else LA_BY_NAME[key]
+    threads = threads or _threads()
+    B, H, L, DK, DV, K = cfg.batch, cfg.heads, cfg.seqlen, cfg.d_key, cfg.d_value, cfg.n_dirs
+    rng = np.random.default_rng([SEED_ROOT, cfg.index])
+    c = rng.uniform(np.log(1e-3), np.log(1e-1), size=(H, DK)).astype(np.float32)
+    s = np.float32(1.0 / np.sqrt(DK))
+    out = {"cfg": cfg}
+    out["q"] = _la_rows(cfg, 0, (DK,), threads) * s
+    out["k"] = _la_rows(cfg, 1, (DK,), threads) * s
+    out["v"] = _la_rows(cfg, 2, (DV,), threads)
+    xi = _la_rows(cfg, 3, (DK,), threads)
+    out["g"] = -np.exp(c[None, :, None, :] + np.float32(0.5) * xi).astype(np.float32)
+    del xi
+    tan = {n: np.empty((K, B, H, L, d), dtype=np.float32) for n, d in (("dq", DK), ("dk", DK), ("dv", DV),
+                                                                        ("dg", DK))}
+    for kk in range(K):
+        sub = cfg.with_(index=cfg.index * 16 + kk)
+        tan["dq"][kk] = _la_rows(sub, 4, (DK,), threads) * s
+        tan["dk"][kk] = _la_rows(sub, 5, (DK,), threads) * s
+        tan["dv"][kk] = _la_rows(sub, 6, (DV,), threads)
+        tan["dg"][kk] = out["g"] * _la_rows(sub, 7, (DK,), threads)
+    out.update(tan)
     return out

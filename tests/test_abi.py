@@ -15,7 +15,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def _declared_functions():
     with open(os.path.join(ROOT, "include", "pgf.h")) as f:
         txt = f.read()
-    return sorted(set(re.findall(r"\b(pgf_[a-z0-9_]+)\s*\(", txt)))
+    # function declarations: a return type at the start of a line, then the name
+    return sorted(set(re.findall(r"^(?:int|size_t|const char \*)\s*(pgf_[a-z0-9_]+)\s*\(", txt, re.M)))
 
 
 def test_library_exports_every_declared_symbol():
@@ -168,3 +169,17 @@ def test_variant_plans_and_bad_variant_fields():
     assert binding.lib().pgf_workspace_bytes(ctypes.byref(pr)) == 0
     pr.drive, pr.activation = 0, 5
     assert binding.lib().pgf_workspace_bytes(ctypes.byref(pr)) == 0
+
+
+def test_linear_attention_plans():
+    p0 = binding.la_plan(1, 32, 8192, 64, 64, 1)
+    p1 = binding.la_plan(1, 32, 131072, 64, 64, 1)
+    for k in ("seg_len", "chunk_segs", "chunk_len", "workspace_bytes"):
+        assert p0[k] == p1[k], k
+    assert p1["chunk_len"] == p1["seg_len"] * p1["chunk_segs"] and p1["workspace_bytes"] <= 1 << 30
+    assert binding.la_plan(1, 32, 5000, 64, 64, 1, seg_len=-1)["seg_len"] == 0
+    for bad in ((1, 2, 100, 48, 64, 1), (1, 2, 100, 16, 96, 1), (1, 2, 100, 16, 64, 4)):
+        with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+            binding.la_plan(*bad)
+    with pytest.raises(RuntimeError, match="INVALID_ARG"):
+        binding.la_plan(1, 2, 100, 16, 64, 1, seg_len=100)
