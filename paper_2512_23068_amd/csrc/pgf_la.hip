@@ -5,10 +5,10 @@
 // value columns j of one head (one lane each) and splits the key dimension
 // over its waves: wave w holds S[16w .. 16w+15, j] (and the tangents) in
 // registers.  Every lane of a wave needs the same 16 key-side values per
-// step (q, k, alpha = exp(g), their tangents): they are read with scalar
-// loads, 16 floats per field and step.  The per-lane inputs are v[j] and
-// dv_k[j]; each wave's partial outputs of a tile of steps are summed over
-// the waves through LDS in a fixed order.
+// step (q, k, alpha = exp(g), their tangents): the block stages them in LDS
+// a tile of steps ahead and the lanes read them as broadcasts.  The
+// per-lane inputs are v[j] and dv_k[j]; each wave's partial outputs of a
+// tile of steps are summed over the waves through LDS in a fixed order.
 //
 // Kernels, per host block of steps [t0, t0+len):
 //   k_la_prep      alpha = exp(g) and alpha*dg_k per step into records, and
@@ -71,6 +71,7 @@ __global__ __launch_bounds__(kThreads) void k_la_prep(
     float sg = 0.0f, sdg[K];
 #pragma unroll
     for (int kk = 0; kk < K; ++kk) sdg[kk] = 0.0f;
+#pragma unroll 4
     for (int64_t t = ts; t < te; ++t) {
         const float gv = g[(row0 + t) * DK + i];
         const float a = exp_acc(gv);
@@ -98,23 +99,37 @@ __global__ __launch_bounds__(kThreads) void k_la_prep(
 // column j.  OUT=false: segment aggregate from a zero state into agg_h.
 // OUT=true: scan from the entry state at init[bh*ibs + g*igs + c*ics +
 // i*DV + j] and write o, do_k; end_state (sequential evaluation) receives
-// the exit state with the same indexing.  Outputs of a tile of TT steps are
-// reduced over the NW waves through LDS (double-buffered, one barrier per
-// tile), slice 0 first.
+// the exit state with the same indexing.
+//
+// The key-side vectors of a tile of TT steps (fields alpha, k, alpha*dg_k,
+// dk_k and, for outputs, q, dq_k; DK floats each) are loaded by the whole
+// block with coalesced loads one tile ahead and staged in LDS (double
+// buffered); every lane then reads them as broadcasts.  Outputs of a tile
+// are reduced over the NW waves through LDS, slice 0 first.  One barrier
+// per tile.
 template <int DK, int K, bool OUT>
-__global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per_eu(K == 1 ? 4 : 3))) void k_la_scan(
+constexpr int la_fields() { return 2 + 2 * K + (OUT ? 1 + K : 0); }
+
+template <int DK, int K, bool OUT>
+__global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per_eu(K == 1 && !OUT ? 4 : 3))) void k_la_scan(
     const float *__restrict__ q, const float *__restrict__ k, const float *__restrict__ v,
     const float *__restrict__ dq, const float *__restrict__ dk, const float *__restrict__ dv,
     const float *__restrict__ rec, const float *init, int64_t ibs, int64_t igs, int64_t ics,
     float *__restrict__ o, float *__restrict__ do_, float *end_state, float *__restrict__ agg_h,
     int64_t BH, int64_t L, int64_t DV, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
     constexpr int NW = DK / kSlice;
+    constexpr int NTH = 64 * NW;
     constexpr int R = (1 + K) * DK;   // floats per step record
     constexpr int TT = 4;             // steps per tile
+    constexpr int F = la_fields<DK, K, OUT>();
+    constexpr int FA = 2 + 2 * K;     // fields of the state update
+    constexpr int NPF = (TT * F * DK + NTH - 1) / NTH;   // key-side floats per thread and tile
+    __shared__ float kvs[2][TT][F][DK];
     __shared__ float red[OUT ? 2 : 1][TT][1 + K][NW][64];
 
-    const int lane = threadIdx.x % 64;
-    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+    const int tid = threadIdx.x;
+    const int lane = tid % 64;
+    const int w = __builtin_amdgcn_readfirstlane(tid / 64);
     const int64_t groups = DV / 64;
     const int64_t bh = blockIdx.x / groups;
     const int64_t j = (blockIdx.x % groups) * 64 + lane;
@@ -144,33 +159,54 @@ __global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per
 
     const int64_t kst = BH * L;                       // rows between tangent directions
     const int64_t row0 = bh * L + t0;
-    // Wave-uniform bases of this block of steps for the wave's key slice;
-    // per-step offsets t*DK stay below 2^30 elements (checked by the planner).
-    const float *kb = k + row0 * DK + i0;
-    const float *qb = q + row0 * DK + i0;
-    const float *rb = rec + bh * Tc * R + i0;
-    const float *dkb[K], *dqb[K];
-#pragma unroll
-    for (int kk = 0; kk < K; ++kk) {
-        dkb[kk] = dk + (kk * kst + row0) * DK + i0;
-        dqb[kk] = dq + (kk * kst + row0) * DK + i0;
-    }
+    const float *rb = rec + bh * Tc * R;
     const float *vb = v + row0 * DV + j;
 
-    // One step t of the recurrence for this wave's key slice: the state
-    // update (alpha, k and the tangents' alpha*dg, dk), then the partial
-    // outputs (q, dq) summed over the slice.  The two phases read disjoint
-    // key-side fields, which bounds the scalar registers a step holds.
-    auto step = [&](int64_t t, float vv, const float *dvv, float *part) {
-        const uint32_t tr = (uint32_t)t * (uint32_t)R, tk = (uint32_t)t * (uint32_t)DK;
+    // The key-side data of a tile is TT*F rows of DK floats (row r = step
+    // jj*F + field f); thread tid loads element tid % DK of the rows
+    // r = tid / DK (mod RPI), so every row is one coalesced load and the
+    // field of each load is known at compile time.  Steps past the segment
+    // repeat its last step.
+    constexpr int RPI = NTH / DK;          // rows covered by one pass of the block
+    const int myrow = tid / DK, ki_ = tid % DK;
+    auto key_row = [&](int f, int64_t t) -> const float * {
+        if (f == 0) return rb + t * R;
+        if (f == 1) return k + (row0 + t) * DK;
+        if (f < FA) {
+            const int kk = (f - 2) / 2;
+            return (f % 2 == 0) ? rb + t * R + (1 + kk) * DK : dk + (kk * kst + row0 + t) * DK;
+        }
+        if (f == FA) return q + (row0 + t) * DK;
+        return dq + ((f - FA - 1) * kst + row0 + t) * DK;
+    };
+    auto fetch = [&](int64_t tb, float *pre) {
+#pragma unroll
+        for (int r = 0; r < TT * F; ++r) {
+            if (r % RPI == myrow) {
+                const int jj = r / F, f = r % F;
+                const int64_t t = tb + jj < te ? tb + jj : te - 1;
+                pre[r / RPI] = key_row(f, t)[ki_];
+            }
+        }
+    };
+    auto stash = [&](int b, const float *pre) {
+#pragma unroll
+        for (int r = 0; r < TT * F; ++r)
+            if (r % RPI == myrow) kvs[b][r / F][r % F][ki_] = pre[r / RPI];
+    };
+
+    // One step (tile slot jj) for this wave's key slice: the state update,
+    // then the partial outputs summed over the slice.
+    auto step = [&](int b, int jj, float vv, const float *dvv, float *part) {
+        const float *rr = &kvs[b][jj][0][i0];
 #pragma unroll
         for (int i = 0; i < kSlice; ++i) {
-            const float a = rb[tr + i], ki = kb[tk + i];
+            const float a = rr[i], ki = rr[DK + i];
             const float sn = fmaf(ki, vv, a * Sm[i]);
 #pragma unroll
             for (int kk = 0; kk < K; ++kk) {
-                const float adg = rb[tr + (1 + kk) * DK + i];
-                const float dki = dkb[kk][tk + i];
+                const float adg = rr[(2 + 2 * kk) * DK + i];
+                const float dki = rr[(3 + 2 * kk) * DK + i];
                 dS[kk][i] = fmaf(a, dS[kk][i], fmaf(adg, Sm[i], fmaf(dki, vv, ki * dvv[kk])));
             }
             Sm[i] = sn;
@@ -181,10 +217,11 @@ __global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per
             for (int kk = 0; kk < K; ++kk) dov[kk] = 0.0f;
 #pragma unroll
             for (int i = 0; i < kSlice; ++i) {
-                const float qi = qb[tk + i];
+                const float qi = rr[FA * DK + i];
                 ov = fmaf(qi, Sm[i], ov);
 #pragma unroll
-                for (int kk = 0; kk < K; ++kk) dov[kk] = fmaf(dqb[kk][tk + i], Sm[i], fmaf(qi, dS[kk][i], dov[kk]));
+                for (int kk = 0; kk < K; ++kk)
+                    dov[kk] = fmaf(rr[(FA + 1 + kk) * DK + i], Sm[i], fmaf(qi, dS[kk][i], dov[kk]));
             }
             part[0] = ov;
 #pragma unroll
@@ -197,13 +234,20 @@ __global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per
         for (int kk = 0; kk < K; ++kk) dvv[kk] = dv[(kk * kst + row0 + t) * DV + j];
     };
 
-    // Tiles of TT steps (the last one partial), v and dv of the next tile in
-    // flight.  Every trip of the tile loop is taken by the whole block.
+    // Tiles of TT steps (the last one partial); the next tile's key-side data
+    // and v, dv are in flight while a tile computes.  Every trip of the tile
+    // loop is taken by the whole block.
+    float pre[NPF];
+    fetch(ts, pre);
+    stash(0, pre);
     float vc[TT], dvc[TT][K];
 #pragma unroll
     for (int jj = 0; jj < TT; ++jj) load_vdv(ts + jj < te ? ts + jj : te - 1, vc[jj], dvc[jj]);
+    __syncthreads();
     int buf = 0;
     for (int64_t tb = ts; tb < te; tb += TT) {
+        const bool more = tb + TT < te;
+        if (more) fetch(tb + TT, pre);
         float vn[TT], dvn[TT][K];
 #pragma unroll
         for (int jj = 0; jj < TT; ++jj) {
@@ -211,19 +255,18 @@ __global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per
             load_vdv(t, vn[jj], dvn[jj]);
         }
         float part[TT][1 + K];
-        if (tb + TT <= te) {
 #pragma unroll
-            for (int jj = 0; jj < TT; ++jj) step(tb + jj, vc[jj], dvc[jj], part[jj]);
-        } else {
-            for (int jj = 0; jj < TT; ++jj)
-                if (tb + jj < te) step(tb + jj, vc[jj], dvc[jj], part[jj]);
-        }
+        for (int jj = 0; jj < TT; ++jj)
+            if (tb + jj < te) step(buf, jj, vc[jj], dvc[jj], part[jj]);
         if constexpr (OUT) {
 #pragma unroll
             for (int jj = 0; jj < TT; ++jj)
 #pragma unroll
                 for (int c = 0; c <= K; ++c) red[buf][jj][c][w][lane] = part[jj][c];
-            __syncthreads();
+        }
+        if (more) stash(buf ^ 1, pre);
+        __syncthreads();
+        if constexpr (OUT) {
             // wave w completes steps jj = w, w + NW, ... of the tile
             for (int jj = w; jj < TT; jj += NW) {
                 const int64_t t = tb + jj;
@@ -232,13 +275,13 @@ __global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per
                 for (int c = 0; c <= K; ++c) {
                     float acc = red[buf][jj][c][0][lane];
 #pragma unroll
-                    for (int s = 1; s < NW; ++s) acc += red[buf][jj][c][s][lane];
+                    for (int s2 = 1; s2 < NW; ++s2) acc += red[buf][jj][c][s2][lane];
                     if (c == 0) o[(row0 + t) * DV + j] = acc;
                     else do_[((c - 1) * kst + row0 + t) * DV + j] = acc;
                 }
             }
-            buf ^= 1;
         }
+        buf ^= 1;
 #pragma unroll
         for (int jj = 0; jj < TT; ++jj) {
             vc[jj] = vn[jj];
