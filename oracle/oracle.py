@@ -68,6 +68,8 @@ def declare(lib):
     lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 13 + [ctypes.c_int]
     lib.pgf_oracle_la.restype = ctypes.c_int
     lib.pgf_oracle_la.argtypes = [i64] * 6 + [dp] * 12 + [ctypes.c_int]
+    lib.pgf_oracle_core_cplx.restype = ctypes.c_int
+    lib.pgf_oracle_core_cplx.argtypes = [i64] * 5 + [dp] * 16 + [ctypes.c_int]
     return lib
 
 
@@ -150,6 +152,30 @@ def project(x, dx, W_B, W_C, b_B=None, b_C=None):
     return Bm, Cm, dx @ WB, dx @ WC
 
 
+def core_cplx(A, Aim, x, dx, delta, ddelta, Bm, Cm, dBm, dCm, h=None, dh=None, nthreads=None):
+    """The recurrence with a complex diagonal transition A + i*Aim (see
+    pgf_oracle_core_cplx).  h [B,D,N] and dh [K,B,D,N] are complex (zero
+    when None).  Returns (y, dy, h_out, dh_out); y and dy are the real
+    read-out sum_n C Re(h)."""
+    lib = _load()
+    A, Aim = _f64(A), _f64(Aim)
+    x, dx, delta, ddelta = _f64(x), _f64(dx), _f64(delta), _f64(ddelta)
+    Bm, Cm, dBm, dCm = _f64(Bm), _f64(Cm), _f64(dBm), _f64(dCm)
+    K, B, L, D = dx.shape
+    N = A.shape[1]
+    h = np.zeros((B, D, N), complex) if h is None else np.asarray(h, complex)
+    dh = np.zeros((K, B, D, N), complex) if dh is None else np.asarray(dh, complex)
+    parts = [np.ascontiguousarray(a, dtype=np.float64) for a in (h.real, h.imag, dh.real, dh.imag)]
+    y = np.empty((B, L, D))
+    dy = np.empty((K, B, L, D))
+    rc = lib.pgf_oracle_core_cplx(B, L, D, N, K, _dp(A), _dp(Aim), _dp(x), _dp(dx), _dp(delta), _dp(ddelta),
+                                  _dp(Bm), _dp(Cm), _dp(dBm), _dp(dCm), *[_dp(p) for p in parts], _dp(y), _dp(dy),
+                                  _threads() if nthreads is None else nthreads)
+    if rc != 0:
+        raise RuntimeError("pgf_oracle_core_cplx failed")
+    return y, dy, parts[0] + 1j * parts[1], parts[2] + 1j * parts[3]
+
+
 ACTIVATIONS = ("identity", "silu")
 
 
@@ -178,7 +204,9 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
 
     x [B,L,D], dx [K,B,L,D] (any float dtype; converted exactly to fp64).
     params: dict with A, w_delta, b_delta, W_B, W_C and optional b_B, b_C,
-    D_res [D] (residual weight of the output map).
+    D_res [D] (residual weight of the output map) and A_im [D,N] (the
+    imaginary part of a complex diagonal transition: the state is complex,
+    h_out/dh_out are returned complex, and y reads Re(C h)).
     drive: "euler" or "zoh" (the input drive, see core); act: "identity" or
     "silu" (the output activation, see output_map).
     channels: optional 1-D index array of channels d to compute (the
@@ -191,8 +219,10 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
     N = A.shape[1]
     sel = np.arange(D) if channels is None else np.asarray(channels, dtype=np.int64)
     Ds = len(sel)
-    h = np.zeros((B, Ds, N)) if h_in is None else _f64(h_in)
-    dh = np.zeros((K, B, Ds, N)) if dh_in is None else _f64(dh_in)
+    cplx = params.get("A_im") is not None
+    cast = (lambda a: np.asarray(a, dtype=complex)) if cplx else _f64
+    h = np.zeros((B, Ds, N)) if h_in is None else cast(h_in)
+    dh = np.zeros((K, B, Ds, N)) if dh_in is None else cast(dh_in)
     if h.shape[1] == D and Ds != D:
         h = h[:, sel]
     if dh.shape[2] == D and Ds != D:
@@ -205,6 +235,12 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
     bd = _f64(params["b_delta"])[sel]
     Dr = None if params.get("D_res") is None else _f64(params["D_res"])[sel]
     As = A[sel]
+    if cplx:
+        if drive != "euler":
+            raise ValueError("the complex transition takes the Euler drive")
+        Ais = _f64(params["A_im"])[sel]
+        h = np.asarray(h, complex)
+        dh = np.asarray(dh, complex)
     for t0 in range(0, L, step):
         t1 = min(L, t0 + step)
         xc = _f64(x[:, t0:t1])
@@ -214,7 +250,10 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
         xs = np.ascontiguousarray(xc[..., sel])
         dxs = np.ascontiguousarray(dxc[..., sel])
         delta, ddelta = discretize(xs, dxs, w, bd)
-        yc, dyc, h, dh = core(As, xs, dxs, delta, ddelta, Bm, Cm, dBm, dCm, h, dh, nthreads, drive)
+        if cplx:
+            yc, dyc, h, dh = core_cplx(As, Ais, xs, dxs, delta, ddelta, Bm, Cm, dBm, dCm, h, dh, nthreads)
+        else:
+            yc, dyc, h, dh = core(As, xs, dxs, delta, ddelta, Bm, Cm, dBm, dCm, h, dh, nthreads, drive)
         y[:, t0:t1], dy[:, :, t0:t1] = output_map(yc, dyc, xs, dxs, Dr, act)
     return y, dy, h, dh
 

@@ -356,3 +356,75 @@ int pgf_oracle_la(int64_t B, int64_t H, int64_t L, int64_t DK, int64_t DV, int64
     }
     return 0;
 }
+
+/*
+ * Complex diagonal transition (Sec. 3: the state lives in C^{D x N}; the
+ * read-out takes the real part, y = Re(C h)).  A = A_re + i A_im per lane;
+ * B, C and Delta are real as in pgf_oracle_core (Euler drive).  The tangent
+ * is the derivative along the real input direction, so it obeys the same
+ * complex recurrence as the state:
+ *
+ *   Abar  = exp(Delta*A)                           (complex)
+ *   h'    = Abar*h + Delta*B*x
+ *   dh'_k = Abar*dh_k + Abar*A*dDelta_k*h + dDelta_k*B*x + Delta*dB_k*x + Delta*B*dx_k
+ *   y     = sum_n C*Re(h'),   dy_k = sum_n dC_k*Re(h') + C*Re(dh'_k)
+ *
+ * Shapes as pgf_oracle_core plus Aim [D,N]; the state is split into real
+ * and imaginary parts: h_re, h_im [B,D,N], dh_re, dh_im [K,B,D,N] (entry
+ * state in, exit state out).  Returns 0, or -1 on a bad argument.
+ */
+#include <complex.h>
+
+int pgf_oracle_core_cplx(int64_t B, int64_t L, int64_t D, int64_t N, int64_t K,
+                         const double *A, const double *Aim, const double *x, const double *dx,
+                         const double *delta, const double *ddelta,
+                         const double *Bm, const double *Cm, const double *dBm, const double *dCm,
+                         double *h_re, double *h_im, double *dh_re, double *dh_im,
+                         double *y, double *dy, int nthreads)
+{
+    if (B < 0 || L < 0 || D < 0 || N <= 0 || K <= 0) return -1;
+    if (!A || !Aim || !h_re || !h_im || !dh_re || !dh_im) return -1;
+    if (L > 0 && (!x || !dx || !delta || !ddelta || !Bm || !Cm || !dBm || !dCm || !y || !dy)) return -1;
+    const int64_t lanes = B * D;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t lane = 0; lane < lanes; ++lane) {
+        const int64_t b = lane / D, d = lane % D;
+        for (int64_t t = 0; t < L; ++t) {
+            const int64_t btd = (b * L + t) * D + d;
+            const double xt = x[btd], dl = delta[btd];
+            const int64_t btn = (b * L + t) * N;
+            double yt = 0.0;
+            for (int64_t kk = 0; kk < K; ++kk) dy[((kk * B + b) * L + t) * D + d] = 0.0;
+            for (int64_t n = 0; n < N; ++n) {
+                const int64_t i = (b * D + d) * N + n;
+                const double complex a = A[d * N + n] + I * Aim[d * N + n];
+                const double complex abar = cexp(dl * a);
+                const double complex hprev = h_re[i] + I * h_im[i];
+                const double complex hnew = abar * hprev + dl * Bm[btn + n] * xt;
+                for (int64_t kk = 0; kk < K; ++kk) {
+                    const int64_t kbtd = ((kk * B + b) * L + t) * D + d;
+                    const int64_t kbtn = ((kk * B + b) * L + t) * N + n;
+                    const int64_t ki = ((kk * B + b) * D + d) * N + n;
+                    const double ddl = ddelta[kbtd], dxt = dx[kbtd];
+                    const double complex dhprev = dh_re[ki] + I * dh_im[ki];
+                    const double complex dhnew = abar * dhprev + abar * a * ddl * hprev + ddl * Bm[btn + n] * xt +
+                                                 dl * dBm[kbtn] * xt + dl * Bm[btn + n] * dxt;
+                    dh_re[ki] = creal(dhnew);
+                    dh_im[ki] = cimag(dhnew);
+                    dy[kbtd] += dCm[kbtn] * creal(hnew) + Cm[btn + n] * creal(dhnew);
+                }
+                h_re[i] = creal(hnew);
+                h_im[i] = cimag(hnew);
+                yt += Cm[btn + n] * creal(hnew);
+            }
+            y[btd] = yt;
+        }
+    }
+    return 0;
+}
