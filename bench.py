@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--drive", default="euler", choices=("euler", "zoh"), help="input drive (first order)")
     ap.add_argument("--act", default="identity", choices=("identity", "silu"), help="output activation (first order)")
     ap.add_argument("--dres", action="store_true", help="add a residual weight D_res ~ N(0,1) to the output map")
+    ap.add_argument("--complex", action="store_true",
+                    help="complex diagonal transition with the S4D-Lin spectrum A = -1/2 + i*pi*n (first order)")
     ap.add_argument("--seg-len", type=int, default=0, help="tiling override (0 = library default)")
     ap.add_argument("--chunk-segs", type=int, default=0, help="tiling override (0 = library default)")
     return ap.parse_args()
@@ -60,6 +62,14 @@ def scan_flops_per_lane_step(K, order=1):
     if order == 3:
         return 7 + 12
     return 7 + 11 * K + (25 if order == 2 else 0)
+
+
+def cplx_flops_per_lane_step(K):
+    """The complex transition: |Abar|, cos and sin and their product (5),
+    Abar*h and A*(Abar*h) (6 + 6), the drive (2), C*Re(h') (2); per
+    direction Abar*dh (6), g*dDelta (4), B*p + dB*u (3) and dC*Re(h') +
+    C*Re(dh') (4)."""
+    return 21 + 17 * K
 
 
 SUFFIX = {1: "", 2: "-order2", 3: "-param"}
@@ -193,9 +203,9 @@ class Workload:
 
 def setup_ssm(args, np, torch, binding, inputs):
     cfg = inputs.get_config(args.workload)
-    variant = args.drive != "euler" or args.act != "identity" or args.dres
+    variant = args.drive != "euler" or args.act != "identity" or args.dres or args.complex
     if variant and args.order != 1:
-        print("bench.py: --drive/--act/--dres apply to the first order only", file=sys.stderr)
+        print("bench.py: --drive/--act/--dres/--complex apply to the first order only", file=sys.stderr)
         sys.exit(2)
     if args.order == 2:
         # two independent N(0,1) directions on the same workload shape
@@ -215,6 +225,9 @@ def setup_ssm(args, np, torch, binding, inputs):
     if args.dres:
         params["D_res"] = torch.from_numpy(
             np.random.default_rng([23068, 7]).standard_normal(D).astype(np.float32)).to(dev)
+    if args.complex:
+        params["A"] = torch.full((D, N), -0.5, device=dev)
+        params["A_im"] = (np.pi * torch.arange(N, device=dev, dtype=torch.float32)).expand(D, N).contiguous()
     s_in = x.element_size()
     y = torch.empty((B, L, D), device=dev)
     if args.order == 3:
@@ -230,7 +243,8 @@ def setup_ssm(args, np, torch, binding, inputs):
             outs = outs + (torch.empty((B, L, D), device=dev),)
             payload += x.numel() * 4
     del inp
-    plan = binding.plan(B, L, D, N, K, cfg.in_dtype, args.seg_len, args.chunk_segs, args.order, args.drive, args.act)
+    plan = binding.plan(B, L, D, N, K, cfg.in_dtype, args.seg_len, args.chunk_segs, args.order, args.drive, args.act,
+                        complex_a=args.complex)
     ws = torch.empty(plan["workspace_bytes"], device=dev, dtype=torch.uint8)
 
     if args.order == 3:
@@ -251,7 +265,8 @@ def setup_ssm(args, np, torch, binding, inputs):
         alg_bytes = tokch * ((1 + K) * (s_in + 4) + (4 if args.order == 2 else 0))
     name = cfg.name + SUFFIX[args.order]
     return Workload(
-        step=step, tokch=tokch, alg_bytes=alg_bytes, flops=tokch * N * scan_flops_per_lane_step(K, args.order),
+        step=step, tokch=tokch, alg_bytes=alg_bytes,
+        flops=tokch * N * (cplx_flops_per_lane_step(K) if args.complex else scan_flops_per_lane_step(K, args.order)),
         payload=payload, plan=plan, metric=METRIC[args.order], kernel="k_scan (scan with outputs)",
         traffic=None if variant else committed_traffic(name, "scan_out", args.order),
         dtype="f32" if cfg.in_dtype == "f32" else "bf16-in/f32",
@@ -426,7 +441,7 @@ def main():
 
 def variant_suffix(args):
     parts = ([args.drive] if args.drive != "euler" else []) + ([args.act] if args.act != "identity" else []) + \
-        (["dres"] if args.dres else [])
+        (["dres"] if args.dres else []) + (["s4dlin"] if args.complex else [])
     return "".join("-" + p for p in parts)
 
 

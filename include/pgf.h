@@ -127,6 +127,13 @@ typedef struct pgf_params {
     int32_t drive;
     int32_t activation;
     const float *D_res;
+    /* Complex diagonal transition (Sec. 3, state in C^{D x N}): the
+     * imaginary part of A, device [D,N] f32, or NULL for a real A.  With it
+     * the output is y = sum_n C Re(h) and dy_k = sum_n dC_k Re(h) + C Re(dh_k);
+     * h_in/h_out are [B,D,N] and dh_in/dh_out [K,B,D,N] complex (interleaved
+     * real, imaginary f32).  First order only, Euler drive, no output map,
+     * N <= 16, K <= 2. */
+    const float *A_im;
 } pgf_params;
 
 /* How a call is tiled (host-side planning; no device access). */
@@ -140,9 +147,10 @@ typedef struct pgf_plan_info {
     size_t  workspace_bytes;
 } pgf_plan_info;
 
-/* Bytes of workspace a call with these sizes needs (only the size fields,
- * in_dtype, seg_len and chunk_segs are read).  Returns 0 if the sizes are
- * invalid or unsupported.  Host only. */
+/* Bytes of workspace a call with these sizes needs.  Reads the size
+ * fields, in_dtype, seg_len, chunk_segs, order, drive and activation, and
+ * tests D_res and A_im for NULL (never dereferenced).  Returns 0 if the
+ * sizes are invalid or unsupported.  Host only. */
 size_t pgf_workspace_bytes(const pgf_params *p);
 
 /* Fill *info with the tiling a call would use.  Host only.  Returns a status. */

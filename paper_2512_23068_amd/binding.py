@@ -37,7 +37,7 @@ class PgfParams(ctypes.Structure):
         ("h_in", _c_f), ("dh_in", _c_f), ("h_out", _c_f), ("dh_out", _c_f),
         ("workspace", _c_f), ("workspace_bytes", ctypes.c_size_t),
         ("d2h_in", _c_f), ("d2h_out", _c_f),
-        ("drive", ctypes.c_int32), ("activation", ctypes.c_int32), ("D_res", _c_f),
+        ("drive", ctypes.c_int32), ("activation", ctypes.c_int32), ("D_res", _c_f), ("A_im", _c_f),
     ]
 
 
@@ -130,10 +130,15 @@ def workspace_bytes(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, orde
                                                                   order, drive, act))))
 
 
-def plan(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1, drive="euler", act="identity") -> dict:
+def plan(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1, drive="euler", act="identity",
+         complex_a=False) -> dict:
+    """The tiling a call would use (complex_a: with a complex transition;
+    the planner only tests A_im for NULL, the pointer is never read)."""
     info = PgfPlanInfo()
-    _check(lib().pgf_plan(ctypes.byref(make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs, order, drive,
-                                                   act)), ctypes.byref(info)))
+    pr = make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs, order, drive, act)
+    if complex_a:
+        pr.A_im = 1
+    _check(lib().pgf_plan(ctypes.byref(pr), ctypes.byref(info)))
     return {f: getattr(info, f) for f, _ in PgfPlanInfo._fields_}
 
 
@@ -164,6 +169,17 @@ def _model_params(pr, params, D, dev, keep):
         keep.append(v)
         setattr(pr, name, None if v is None else v.data_ptr())
     return N
+
+
+def _dev_state_c(v, shape, device, name):
+    """A complex state (complex64 on the device, interleaved real/imag)."""
+    if v is None:
+        return None
+    if not isinstance(v, torch.Tensor):
+        v = torch.as_tensor(v)
+    if tuple(v.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(v.shape)}")
+    return v.to(device=device, dtype=torch.complex64).contiguous()
 
 
 def _workspace(L_, pr, workspace, dev):
@@ -199,16 +215,25 @@ def _scan(x, dx, params, order, h_in, dh_in, d2h_in, return_state, seg_len, chun
     D_res = _dev_param(params.get("D_res"), (D,), dev, "D_res")
     keep.append(D_res)
     pr.D_res = None if D_res is None else D_res.data_ptr()
-    h_in = _dev_param(h_in, (B, D, N), dev, "h_in")
-    dh_in = _dev_param(dh_in, (K, B, D, N), dev, "dh_in")
+    A_im = _dev_param(params.get("A_im"), (D, N), dev, "A_im")
+    keep.append(A_im)
+    pr.A_im = None if A_im is None else A_im.data_ptr()
+    cplx = A_im is not None
+    if cplx:
+        h_in = _dev_state_c(h_in, (B, D, N), dev, "h_in")
+        dh_in = _dev_state_c(dh_in, (K, B, D, N), dev, "dh_in")
+    else:
+        h_in = _dev_param(h_in, (B, D, N), dev, "h_in")
+        dh_in = _dev_param(dh_in, (K, B, D, N), dev, "dh_in")
     d2h_in = _dev_param(d2h_in, (B, D, N), dev, "d2h_in")
     pr.h_in = None if h_in is None else h_in.data_ptr()
     pr.dh_in = None if dh_in is None else dh_in.data_ptr()
     pr.d2h_in = None if d2h_in is None else d2h_in.data_ptr()
     states = ()
     if return_state:
-        h_out = torch.empty((B, D, N), device=dev, dtype=torch.float32)
-        dh_out = torch.empty((K, B, D, N), device=dev, dtype=torch.float32)
+        sdt = torch.complex64 if cplx else torch.float32
+        h_out = torch.empty((B, D, N), device=dev, dtype=sdt)
+        dh_out = torch.empty((K, B, D, N), device=dev, dtype=sdt)
         pr.h_out, pr.dh_out = h_out.data_ptr(), dh_out.data_ptr()
         states = (h_out, dh_out)
         if order == 2:
@@ -240,8 +265,9 @@ def scan_jvp(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_i
     """Fused primal + tangent scan on the GPU.
 
     x [B,L,D] and dx [K,B,L,D]: float32 or bfloat16 CUDA tensors (same dtype).
-    params: A, W_B, W_C [D,N]; w_delta, b_delta [D]; optional b_B, b_C [N]
-    and D_res [D] (residual weight of the output map).
+    params: A, W_B, W_C [D,N]; w_delta, b_delta [D]; optional b_B, b_C [N],
+    D_res [D] (residual weight of the output map) and A_im [D,N] (imaginary
+    part of a complex transition; the states are then complex64).
     drive: "euler" or "zoh"; act: "identity" or "silu" (the variants need
     N <= 16 and K <= 2).
     Returns (y [B,L,D], dy [K,B,L,D]) in float32, plus (h_out [B,D,N],

@@ -70,13 +70,16 @@ int make_plan(const pgf_params *p, Plan *plan) {
                     ((p->activation != PGF_ACT_IDENTITY || p->D_res) ? 2 : 0);
     if (var && order != 1) return PGF_ERR_UNSUPPORTED;
     if (var && (K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
+    const int cplx = p->A_im ? 1 : 0;
+    if (cplx && (order != 1 || var || K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
 
     Plan q{};
     q.B = B; q.L = L; q.D = D; q.N = N; q.K = K;
     q.order = order;
     q.var = var;
     q.KP = order == 3 ? 0 : K;
-    q.comp = (int)(1 + K + (order == 2 ? 1 : 0));
+    q.cplx = cplx;
+    q.comp = (int)((1 + K + (order == 2 ? 1 : 0)) * (cplx ? 2 : 1));
     q.in_bf16 = p->in_dtype == PGF_BF16;
     // Registers per thread grow as nt*(3+K); keep them near 128.
     q.nt = (int)std::min<int64_t>(N, K >= 8 ? 4 : (K >= 4 ? 8 : 16));

@@ -31,7 +31,8 @@ struct Plan {
     int order;           // 1, 2, or 3 (parameter flows)
     int64_t KP;          // directions projected by k_proj (K, or 0 for order 3)
     int var;             // model variant bits of the first-order scan (kZoh 1, kOutMap 2)
-    int comp;            // states per lane: 1 + K (+ 1 for the mixed flow)
+    int cplx;            // complex diagonal transition (state in real/imaginary planes)
+    int comp;            // state planes per lane: 1 + K (+ 1 for the mixed flow), twice that if complex
     int in_bf16;
     int nt, ns;          // states per thread, threads per channel (nt*ns == N)
     int seg;             // segment length; 0 = sequential evaluation

@@ -1347,44 +1347,313 @@ __global__ __launch_bounds__(kThreads) void k_gout(
     out[d * N + n] += s;
 }
 
+// ---------------------------------------------------------------- complex
+// Complex diagonal transition A = A_re + i A_im (Sec. 3: state in C^{DxN},
+// read-out y = sum_n C Re(h)), Euler drive, one thread per channel with all
+// NT = N lanes.  Per lane and step, with Abar = exp(Delta A_re) (cos th +
+// i sin th), th = Delta A_im:
+//   s = Abar h,  h' = s + B u,  g = A s,
+//   dh'_k = Abar dh_k + g dDelta_k + (B p_k + dB_k u)     (drive real)
+//   y = sum_n C Re(h'),  dy_k = sum_n dC_k Re(h') + C Re(dh'_k)
+// The angle is reduced in revolutions (th/2pi minus its nearest integer)
+// before the hardware sine and cosine.  Layouts as k_scan with the state
+// split into planes: component c = 2m + part (m = 0 h, 1..K dh_k).
+constexpr float kInv2Pi = 0.159154943091895336f;
+
+__device__ __forceinline__ void rot(float rev, float &c, float &s) {
+    const float r = rev - __builtin_rintf(rev);
+    s = __builtin_amdgcn_sinf(r);
+    c = __builtin_amdgcn_cosf(r);
+}
+
+template <int NT, int K, bool OUT, typename InT>
+__global__ __launch_bounds__(kThreads) void k_cscan(
+    const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A, const float *__restrict__ Aim,
+    const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
+    const float *init, int64_t ibs, int64_t igs, int64_t ics, float *__restrict__ y, float *__restrict__ dy,
+    float *end_state, float *__restrict__ agg_h, float *__restrict__ agg_s, int64_t Bsz, int64_t L, int64_t D,
+    int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    constexpr int N = NT;
+    constexpr int R = 2 * N * (1 + K);
+    constexpr int TT = 8;
+    constexpr int CP = 2 * (1 + K);   // state planes
+
+    const int tid = threadIdx.x;
+    const int64_t d_raw = (int64_t)blockIdx.x * kThreads + tid;
+    const bool active = d_raw < D;
+    const int64_t d = active ? d_raw : D - 1;
+    const int g = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int64_t ts = (int64_t)g * S;
+    const int64_t te = ts + S < len ? ts + S : len;
+    if (ts >= te) return;
+
+    float Ar[NT], Ai[NT], At[NT], Ar2[NT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+        Ar[i] = A[d * N + i];
+        Ai[i] = Aim[d * N + i];
+        At[i] = Ar[i] * kLog2e;
+        Ar2[i] = Ai[i] * kInv2Pi;
+    }
+    const float w = w_delta[d], bd = b_delta[d];
+
+    float hr[NT], hi[NT], dr[K][NT], di[K][NT];
+    if constexpr (OUT) {
+        const float *ib = init + b * ibs + g * igs + d;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            hr[i] = ib[i * D];
+            hi[i] = ib[ics + i * D];
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                dr[k][i] = ib[(2 + 2 * k) * ics + i * D];
+                di[k][i] = ib[(3 + 2 * k) * ics + i * D];
+            }
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            hr[i] = hi[i] = 0.0f;
+#pragma unroll
+            for (int k = 0; k < K; ++k) dr[k][i] = di[k][i] = 0.0f;
+        }
+    }
+    float sD = 0.0f, sdD[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) sdD[k] = 0.0f;
+
+    const int64_t dxs = Bsz * L * D;
+    const InT *Xb = x + (b * L + t0) * D;
+    const InT *DXb = dx + (b * L + t0) * D;
+    float *Yb = y + (b * L + t0) * D;
+    float *DYb = dy + (b * L + t0) * D;
+    const uint32_t Du = (uint32_t)D, du = (uint32_t)d;
+    const float *rec0 = bc + b * Tc * R;
+
+    float xc[TT], dxc[K][TT];
+#pragma unroll
+    for (int j = 0; j < TT; ++j) {
+        const int64_t t = ts + j < te ? ts + j : te - 1;
+        xc[j] = load_in(Xb, (uint32_t)t * Du + du);
+#pragma unroll
+        for (int k = 0; k < K; ++k) dxc[k][j] = load_in(DXb + k * dxs, (uint32_t)t * Du + du);
+    }
+    for (int64_t tb = ts; tb < te; tb += TT) {
+        float xn[TT], dxn[K][TT];
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
+            xn[j] = load_in(Xb, (uint32_t)t * Du + du);
+#pragma unroll
+            for (int k = 0; k < K; ++k) dxn[k][j] = load_in(DXb + k * dxs, (uint32_t)t * Du + du);
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + j;
+            if (t < te) {
+                const float xv = xc[j];
+                float delta, sw;
+                discretize(xv, w, bd, delta, sw);
+                const float u = delta * xv;
+                float dD[K], pk[K];
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    dD[k] = sw * dxc[k][j];
+                    pk[k] = fmaf(dD[k], xv, delta * dxc[k][j]);
+                }
+                if constexpr (!OUT) {
+                    sD += delta;
+#pragma unroll
+                    for (int k = 0; k < K; ++k) sdD[k] += dD[k];
+                }
+                const float *rec = rec0 + t * R;
+                float yv = 0.0f, dyv[K];
+#pragma unroll
+                for (int k = 0; k < K; ++k) dyv[k] = 0.0f;
+#pragma unroll
+                for (int i = 0; i < NT; ++i) {
+                    const float Bn = rec[i];
+                    const float e = __builtin_amdgcn_exp2f(delta * At[i]);
+                    float cs, sn;
+                    rot(delta * Ar2[i], cs, sn);
+                    const float ar = e * cs, ai = e * sn;
+                    const float sr = fmaf(ar, hr[i], -ai * hi[i]);
+                    const float si = fmaf(ar, hi[i], ai * hr[i]);
+                    const float gr = fmaf(Ar[i], sr, -Ai[i] * si);
+                    const float gi = fmaf(Ar[i], si, Ai[i] * sr);
+                    const float hrn = fmaf(Bn, u, sr);
+#pragma unroll
+                    for (int k = 0; k < K; ++k) {
+                        const float dBn = rec[(1 + k) * N + i];
+                        const float tr = fmaf(ar, dr[k][i], -ai * di[k][i]);
+                        const float ti = fmaf(ar, di[k][i], ai * dr[k][i]);
+                        dr[k][i] = fmaf(gr, dD[k], tr) + fmaf(Bn, pk[k], dBn * u);
+                        di[k][i] = fmaf(gi, dD[k], ti);
+                    }
+                    hr[i] = hrn;
+                    hi[i] = si;
+                    if constexpr (OUT) {
+                        const float Cn = rec[(1 + K) * N + i];
+                        yv = fmaf(Cn, hrn, yv);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) {
+                            const float dCn = rec[(2 + K + k) * N + i];
+                            dyv[k] = fmaf(dCn, hrn, fmaf(Cn, dr[k][i], dyv[k]));
+                        }
+                    }
+                }
+                if constexpr (OUT) {
+                    if (active) {
+                        store_out(Yb, (uint32_t)t * Du + du, yv);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) store_out(DYb + k * dxs, (uint32_t)t * Du + du, dyv[k]);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            xc[j] = xn[j];
+#pragma unroll
+            for (int k = 0; k < K; ++k) dxc[k][j] = dxn[k][j];
+        }
+    }
+
+    if (!active) return;
+    if constexpr (OUT) {
+        if (end_state) {
+            float *eb = end_state + b * ibs + d;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                eb[i * D] = hr[i];
+                eb[ics + i * D] = hi[i];
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    eb[(2 + 2 * k) * ics + i * D] = dr[k][i];
+                    eb[(3 + 2 * k) * ics + i * D] = di[k][i];
+                }
+            }
+        }
+    } else {
+        const int64_t base = (b * G + g) * CP;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            agg_h[(base * N + i) * D + d] = hr[i];
+            agg_h[((base + 1) * N + i) * D + d] = hi[i];
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                agg_h[((base + 2 + 2 * k) * N + i) * D + d] = dr[k][i];
+                agg_h[((base + 3 + 2 * k) * N + i) * D + d] = di[k][i];
+            }
+        }
+        const int64_t sbase = (b * G + g) * (1 + K);
+        agg_s[sbase * D + d] = sD;
+#pragma unroll
+        for (int k = 0; k < K; ++k) agg_s[(sbase + 1 + k) * D + d] = sdD[k];
+    }
+}
+
+// Carry of the complex scan: a segment maps (h, dh_k) to (P h + h0,
+// P dh_k + Q_k h + dh0_k) with P = exp(A S) (complex), Q_k = P A S_k, S and
+// S_k the segment sums of Delta and dDelta_k.  Layout as k_carry with the
+// state split into planes (seg [B][G][2(1+K)][N][D], agg_s [B][G][1+K][D]).
+template <int K>
+__global__ __launch_bounds__(kThreads) void k_ccarry(
+    const float *__restrict__ A, const float *__restrict__ Aim, float *__restrict__ seg,
+    const float *__restrict__ agg_s, float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int G) {
+    constexpr int GB = 8;
+    constexpr int CP = 2 * (1 + K);
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t ND = N * D;
+    if (idx >= Bsz * ND) return;
+    const int64_t d = idx % D, n = (idx / D) % N, b = idx / ND;
+    const float ar = A[d * N + n], aim = Aim[d * N + n];
+    const float at = ar * kLog2e, arev = aim * kInv2Pi;
+    const int64_t cs = Bsz * ND;
+    const int64_t lane = b * ND + n * D + d;
+    const int64_t sl = n * D + d;
+    float st[CP];
+#pragma unroll
+    for (int c = 0; c < CP; ++c) st[c] = state[c * cs + lane];
+    for (int g0 = 0; g0 < G; g0 += GB) {
+        float e[GB][CP], sm[GB][1 + K];
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            const int g = g0 + j < G ? g0 + j : G - 1;
+#pragma unroll
+            for (int c = 0; c < CP; ++c) e[j][c] = seg[(((b * G + g) * CP) + c) * ND + sl];
+#pragma unroll
+            for (int c = 0; c <= K; ++c) sm[j][c] = agg_s[((b * G + g) * (1 + K) + c) * D + d];
+        }
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            if (g0 + j >= G) break;
+#pragma unroll
+            for (int c = 0; c < CP; ++c) seg[(((b * G + g0 + j) * CP) + c) * ND + sl] = st[c];
+            const float mag = __builtin_amdgcn_exp2f(at * sm[j][0]);
+            float cs_, sn_;
+            rot(arev * sm[j][0], cs_, sn_);
+            const float pr = mag * cs_, pi = mag * sn_;
+            const float hr = st[0], hi = st[1];
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                // Q_k = P A S_k
+                const float qr = (pr * ar - pi * aim) * sm[j][1 + k], qi = (pr * aim + pi * ar) * sm[j][1 + k];
+                const float dr = st[2 + 2 * k], di = st[3 + 2 * k];
+                st[2 + 2 * k] = fmaf(pr, dr, -pi * di) + fmaf(qr, hr, -qi * hi) + e[j][2 + 2 * k];
+                st[3 + 2 * k] = fmaf(pr, di, pi * dr) + fmaf(qr, hi, qi * hr) + e[j][3 + 2 * k];
+            }
+            st[0] = fmaf(pr, hr, -pi * hi) + e[j][0];
+            st[1] = fmaf(pr, hi, pi * hr) + e[j][1];
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < CP; ++c) state[c * cs + lane] = st[c];
+}
+
 // ---------------------------------------------------------------- state in/out
-// state [(1+K)][B][N][D] <-> h [B][D][N], dh [K][B][D][N].
-// Component c of the state: 0 -> h, 1..K -> dh_{c-1}, 1+K -> d2h (second
-// order only; comp = number of components).
+// state [comp][B][N][D] <-> h [B][D][N], dh [K][B][D][N].
+// Real state: component c = 0 -> h, 1..K -> dh_{c-1}, 1+K -> d2h (second
+// order only).  Complex state (cplx = 1): component c = 2m + part with
+// m = 0 -> h, 1..K -> dh_{m-1} and part 0/1 the real/imaginary plane; the
+// caller's arrays are complex (interleaved real, imaginary floats).
+__device__ __forceinline__ int64_t state_src(int64_t c, int64_t b, int64_t d, int64_t n, int64_t Bsz, int64_t D,
+                                             int64_t N, int K, int cplx, int &which) {
+    const int64_t m = cplx ? c / 2 : c, part = cplx ? c % 2 : 0;
+    const int64_t s = cplx ? 2 : 1;
+    if (m == 0) { which = 0; return ((b * D + d) * N + n) * s + part; }
+    if (m <= K) { which = 1; return ((((m - 1) * Bsz + b) * D + d) * N + n) * s + part; }
+    which = 2;
+    return (b * D + d) * N + n;
+}
+
 __global__ __launch_bounds__(kThreads) void k_state_import(
     const float *__restrict__ h_in, const float *__restrict__ dh_in, const float *__restrict__ d2h_in,
-    float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int K, int comp) {
+    float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int K, int comp, int cplx) {
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int64_t per = Bsz * N * D;
     if (idx >= per * comp) return;
     const int64_t c = idx / per, r = idx % per;
     const int64_t d = r % D, n = (r / D) % N, b = r / (N * D);
-    float v = 0.0f;
-    if (c == 0) {
-        if (h_in) v = h_in[(b * D + d) * N + n];
-    } else if (c <= K) {
-        if (dh_in) v = dh_in[(((c - 1) * Bsz + b) * D + d) * N + n];
-    } else if (d2h_in) {
-        v = d2h_in[(b * D + d) * N + n];
-    }
-    state[idx] = v;
+    int which;
+    const int64_t e = state_src(c, b, d, n, Bsz, D, N, K, cplx, which);
+    const float *src = which == 0 ? h_in : (which == 1 ? dh_in : d2h_in);
+    state[idx] = src ? src[e] : 0.0f;
 }
 
 __global__ __launch_bounds__(kThreads) void k_state_export(
     const float *__restrict__ state, float *__restrict__ h_out, float *__restrict__ dh_out,
-    float *__restrict__ d2h_out, int64_t Bsz, int64_t D, int64_t N, int K, int comp) {
+    float *__restrict__ d2h_out, int64_t Bsz, int64_t D, int64_t N, int K, int comp, int cplx) {
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int64_t per = Bsz * N * D;
     if (idx >= per * comp) return;
     const int64_t c = idx / per, r = idx % per;
     const int64_t d = r % D, n = (r / D) % N, b = r / (N * D);
-    if (c == 0) {
-        if (h_out) h_out[(b * D + d) * N + n] = state[idx];
-    } else if (c <= K) {
-        if (dh_out) dh_out[(((c - 1) * Bsz + b) * D + d) * N + n] = state[idx];
-    } else if (d2h_out) {
-        d2h_out[(b * D + d) * N + n] = state[idx];
-    }
+    int which;
+    const int64_t e = state_src(c, b, d, n, Bsz, D, N, K, cplx, which);
+    float *dst = which == 0 ? h_out : (which == 1 ? dh_out : d2h_out);
+    if (dst) dst[e] = state[idx];
 }
 
 // ---------------------------------------------------------------- dispatch
@@ -1558,6 +1827,53 @@ struct Launcher {
         }
     }
 
+    // Complex transition: one thread per channel with all N <= 16 lanes.
+    template <int NT, int K>
+    void cscans(int64_t t0, int64_t len) {
+        const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
+        const int64_t ND = q.N * q.D;
+        constexpr int CP = 2 * (1 + K);
+        if (q.seg == 0) {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_cscan<NT, K, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, dx,
+                               p.A, p.A_im, p.w_delta, p.b_delta, bcw(), (const float *)state(), ND, (int64_t)0,
+                               q.B * ND, y, dy, state(), (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len,
+                               q.chunk_len, len, 1);
+            return;
+        }
+        const int G = (int)((len + q.seg - 1) / q.seg);
+        {
+            Timed tm(1, st);
+            hipLaunchKernelGGL((k_cscan<NT, K, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0,
+                               st, x, dx, p.A, p.A_im, p.w_delta, p.b_delta, bcw(), (const float *)nullptr,
+                               (int64_t)0, (int64_t)0, (int64_t)0, y, dy, (float *)nullptr, agg_h(), agg_s(), q.B,
+                               q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+        }
+        {
+            const int64_t lanes = q.B * ND;
+            Timed tm(2, st);
+            hipLaunchKernelGGL((k_ccarry<K>), dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                               st, p.A, p.A_im, agg_h(), (const float *)agg_s(), state(), q.B, q.D, q.N, G);
+        }
+        {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_cscan<NT, K, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0,
+                               st, x, dx, p.A, p.A_im, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(),
+                               (int64_t)G * CP * ND, (int64_t)CP * ND, ND, y, dy, (float *)nullptr, (float *)nullptr,
+                               (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+        }
+    }
+
+    template <int K>
+    bool cscan_block(int64_t t0, int64_t len) {
+        switch (q.nt) {
+            case 4: cscans<4, K>(t0, len); return true;
+            case 8: cscans<8, K>(t0, len); return true;
+            case 16: cscans<16, K>(t0, len); return true;
+            default: return false;
+        }
+    }
+
     // Parameter flows: one thread per channel with all N <= 16 states.
     template <int NT>
     void pscans(int64_t t0, int64_t len) {
@@ -1600,6 +1916,10 @@ struct Launcher {
     }
 
     bool scan_block(int64_t t0, int64_t len) {
+        if (q.cplx) {
+            if (q.ns != 1) return false;
+            return q.K == 1 ? cscan_block<1>(t0, len) : (q.K == 2 ? cscan_block<2>(t0, len) : false);
+        }
         if (q.order == 3) {
             if (q.ns != 1) return false;
             switch (q.nt) {
@@ -1636,7 +1956,7 @@ struct Launcher {
         {
             Timed tm(4, st);
             hipLaunchKernelGGL(k_state_import, dim3(gs), dim3(kThreads), 0, st, p.h_in, p.dh_in, d2h_in, state(), q.B,
-                               q.D, q.N, (int)q.K, q.comp);
+                               q.D, q.N, (int)q.K, q.comp, q.cplx);
             if (q.order == 3)
                 hipLaunchKernelGGL(k_fill0, dim3((unsigned)((nacc + kThreads - 1) / kThreads)), dim3(kThreads), 0,
                                    st, gacc(), nacc);
@@ -1655,7 +1975,7 @@ struct Launcher {
         if (p.h_out || p.dh_out || d2h_out) {
             Timed tm(4, st);
             hipLaunchKernelGGL(k_state_export, dim3(gs), dim3(kThreads), 0, st, state(), p.h_out, p.dh_out, d2h_out,
-                               q.B, q.D, q.N, (int)q.K, q.comp);
+                               q.B, q.D, q.N, (int)q.K, q.comp, q.cplx);
         }
         return hipGetLastError() == hipSuccess ? PGF_OK : PGF_ERR_HIP;
     }

@@ -183,3 +183,17 @@ def test_linear_attention_plans():
             binding.la_plan(*bad)
     with pytest.raises(RuntimeError, match="INVALID_ARG"):
         binding.la_plan(1, 2, 100, 16, 64, 1, seg_len=100)
+
+
+def test_complex_transition_plans():
+    p = binding.make_params(1, 1000, 64, 16, 1)
+    base = binding.lib().pgf_workspace_bytes(ctypes.byref(p))
+    p.A_im = 1 << 30                      # any non-NULL pointer selects the complex state
+    cplx = binding.lib().pgf_workspace_bytes(ctypes.byref(p))
+    assert cplx > base
+    for kw in (dict(n_dirs=4), dict(order=2, n_dirs=2), dict(drive=1), dict(d_state=32)):
+        q = binding.make_params(1, 1000, 64, 16, 1)
+        q.A_im = 1 << 30
+        for k, v in kw.items():
+            setattr(q, k, v)
+        assert binding.lib().pgf_workspace_bytes(ctypes.byref(q)) == 0, kw

@@ -1,0 +1,91 @@
+"""Complex diagonal transition (Sec. 3: state in C^{D x N}, y = Re(C h)) on
+the GPU against the fp64 oracle: several state sizes, one and two
+directions, the segmented and sequential evaluations, an S4D-Lin style
+spectrum and a stiff bf16 case; the real limit; bit-identical results for
+every host block size and split calls chained through the complex state."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2512_23068_amd import binding
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+
+def _with_im(inp, kind="random", seed=9):
+    D, N = inp["A"].shape
+    if kind == "s4dlin":
+        inp["A"] = np.full((D, N), -0.5, np.float32)
+        inp["A_im"] = np.broadcast_to(np.pi * np.arange(N, dtype=np.float32), (D, N)).copy()
+    else:
+        r = np.random.default_rng(seed)
+        inp["A_im"] = (np.pi * r.uniform(0.1, 4.0, (D, N)) * r.choice([-1, 1], (D, N))).astype(np.float32)
+    return inp
+
+
+def _check(inp, what, **kw):
+    print(f"case {what}", flush=True)
+    y, dy = gu.run(inp, **kw)
+    yo, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp)
+    gu.assert_close(y.cpu().numpy(), dy.cpu().numpy(), yo, dyo, what=what)
+
+
+@pytest.mark.parametrize("N,K,seg", [(16, 1, 0), (16, 2, 0), (8, 1, -1), (4, 2, 64), (16, 1, -1)])
+def test_cplx_parity(N, K, seg):
+    inp = _with_im(gu.custom("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N, n_dirs=K))
+    _check(inp, f"complex N={N} K={K} seg={seg}", seg_len=seg)
+
+
+def test_cplx_s4dlin_and_stiff():
+    _check(_with_im(gu.custom("mamba130m", seqlen=3000, d_inner=64), "s4dlin"), "complex s4d-lin")
+    _check(_with_im(gu.custom("stiff128k", seqlen=1500, d_inner=64)), "complex stiff bf16")
+
+
+def test_cplx_real_limit():
+    inp = gu.custom("mamba130m", batch=1, seqlen=800, d_inner=64, n_dirs=2)
+    y0, dy0 = gu.run(inp)
+    inp["A_im"] = np.zeros_like(inp["A"])
+    y1, dy1 = gu.run(inp)
+    assert gu.rel_l2(y1.cpu().numpy(), y0.cpu().numpy()) < 1e-6
+    assert gu.rel_l2(dy1.cpu().numpy(), dy0.cpu().numpy()) < 1e-6
+
+
+def test_cplx_block_invariance_and_handoff():
+    inp = _with_im(gu.custom("mamba130m", batch=2, seqlen=1000, d_inner=48, n_dirs=2))
+    ref = gu.run(inp, seg_len=64, chunk_segs=1, return_state=True)
+    assert ref[2].dtype == torch.complex64
+    for cs in (3, 0):
+        got = gu.run(inp, seg_len=64, chunk_segs=cs, return_state=True)
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), cs
+    x, dx = gu.inputs_to_dev(inp)
+    prm = gu.params_to_dev(inp)
+    s = 384
+    a = binding.scan_jvp(x[:, :s], dx[:, :, :s], prm, seg_len=64, return_state=True)
+    b = binding.scan_jvp(x[:, s:], dx[:, :, s:], prm, seg_len=64, h_in=a[2], dh_in=a[3], return_state=True)
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat([a[0], b[0]], 1), ref[0])
+    assert torch.equal(torch.cat([a[1], b[1]], 2), ref[1])
+    assert torch.equal(b[2], ref[2]) and torch.equal(b[3], ref[3])
+
+
+def test_cplx_entry_state_matches_oracle():
+    inp = _with_im(gu.custom("mamba130m", batch=1, seqlen=600, d_inner=40))
+    r = np.random.default_rng(4)
+    h0 = (r.standard_normal((1, 40, 16)) + 1j * r.standard_normal((1, 40, 16))).astype(np.complex64)
+    dh0 = (r.standard_normal((1, 1, 40, 16)) + 1j * r.standard_normal((1, 1, 40, 16))).astype(np.complex64)
+    y, dy, h, dh = gu.run(inp, h_in=torch.from_numpy(h0), dh_in=torch.from_numpy(dh0), return_state=True)
+    yo, dyo, ho, dho = oracle.scan_jvp(inp["x"], inp["dx"], inp, h_in=h0, dh_in=dh0)
+    for got, ref in ((y, yo), (dy, dyo), (h, ho), (dh, dho)):
+        assert gu.rel_l2(got.cpu().numpy(), ref) < gu.TOL
+
+
+def test_cplx_limits():
+    inp = _with_im(gu.custom("tiny", seqlen=64, n_dirs=4))
+    with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+        gu.run(inp)
+    inp = _with_im(gu.custom("tiny", seqlen=64))
+    with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+        gu.run(inp, drive="zoh")
