@@ -176,6 +176,11 @@ def core_cplx(A, Aim, x, dx, delta, ddelta, Bm, Cm, dBm, dCm, h=None, dh=None, n
     return y, dy, parts[0] + 1j * parts[1], parts[2] + 1j * parts[3]
 
 
+def channel_groups(channels, D, G):
+    """Group of each channel: contiguous blocks of D/G channels."""
+    return np.asarray(channels) // (D // G)
+
+
 ACTIVATIONS = ("identity", "silu")
 
 
@@ -206,7 +211,9 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
     params: dict with A, w_delta, b_delta, W_B, W_C and optional b_B, b_C,
     D_res [D] (residual weight of the output map) and A_im [D,N] (the
     imaginary part of a complex diagonal transition: the state is complex,
-    h_out/dh_out are returned complex, and y reads Re(C h)).
+    h_out/dh_out are returned complex, and y reads Re(C h)), and n_groups G
+    (channel groups with their own B and C: W_B, W_C [D, G*N], b_B, b_C
+    [G*N]; channel d uses group d // (D/G)).
     drive: "euler" or "zoh" (the input drive, see core); act: "identity" or
     "silu" (the output activation, see output_map).
     channels: optional 1-D index array of channels d to compute (the
@@ -235,6 +242,12 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
     bd = _f64(params["b_delta"])[sel]
     Dr = None if params.get("D_res") is None else _f64(params["D_res"])[sel]
     As = A[sel]
+    G = int(params.get("n_groups") or 1)
+    if D % G:
+        raise ValueError("n_groups must divide the channel count")
+    grp = channel_groups(sel, D, G)
+    h = np.array(h, copy=True)
+    dh = np.array(dh, copy=True)
     if cplx:
         if drive != "euler":
             raise ValueError("the complex transition takes the Euler drive")
@@ -250,10 +263,24 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
         xs = np.ascontiguousarray(xc[..., sel])
         dxs = np.ascontiguousarray(dxc[..., sel])
         delta, ddelta = discretize(xs, dxs, w, bd)
-        if cplx:
-            yc, dyc, h, dh = core_cplx(As, Ais, xs, dxs, delta, ddelta, Bm, Cm, dBm, dCm, h, dh, nthreads)
-        else:
-            yc, dyc, h, dh = core(As, xs, dxs, delta, ddelta, Bm, Cm, dBm, dCm, h, dh, nthreads, drive)
+        # Channel groups: channel d reads the B, C of group d // (D / G)
+        # (columns [g N, (g+1) N) of the projections); groups are independent
+        # given their B and C, so each runs as its own recurrence.
+        yc = np.empty((B, t1 - t0, Ds))
+        dyc = np.empty((K, B, t1 - t0, Ds))
+        for g in range(G):
+            m = grp == g
+            if not m.any():
+                continue
+            cols = slice(g * N, (g + 1) * N)
+            args = (As[m], xs[..., m], dxs[..., m], delta[..., m], ddelta[..., m], Bm[..., cols], Cm[..., cols],
+                    dBm[..., cols], dCm[..., cols], h[:, m], dh[:, :, m], nthreads)
+            if cplx:
+                yg, dyg, hg, dhg = core_cplx(args[0], Ais[m], *args[1:])
+            else:
+                yg, dyg, hg, dhg = core(*args, drive)
+            yc[..., m], dyc[..., m] = yg, dyg
+            h[:, m], dh[:, :, m] = hg, dhg
         y[:, t0:t1], dy[:, :, t0:t1] = output_map(yc, dyc, xs, dxs, Dr, act)
     return y, dy, h, dh
 
