@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--drive", default="euler", choices=("euler", "zoh"), help="input drive (first order)")
     ap.add_argument("--act", default="identity", choices=("identity", "silu"), help="output activation (first order)")
     ap.add_argument("--dres", action="store_true", help="add a residual weight D_res ~ N(0,1) to the output map")
+    ap.add_argument("--groups", type=int, default=1,
+                    help="channel groups with their own B and C (first order; D/groups a multiple of 64)")
     ap.add_argument("--complex", action="store_true",
                     help="complex diagonal transition with the S4D-Lin spectrum A = -1/2 + i*pi*n (first order)")
     ap.add_argument("--seg-len", type=int, default=0, help="tiling override (0 = library default)")
@@ -203,7 +205,7 @@ class Workload:
 
 def setup_ssm(args, np, torch, binding, inputs):
     cfg = inputs.get_config(args.workload)
-    variant = args.drive != "euler" or args.act != "identity" or args.dres or args.complex
+    variant = args.drive != "euler" or args.act != "identity" or args.dres or args.complex or args.groups > 1
     if variant and args.order != 1:
         print("bench.py: --drive/--act/--dres/--complex apply to the first order only", file=sys.stderr)
         sys.exit(2)
@@ -225,6 +227,12 @@ def setup_ssm(args, np, torch, binding, inputs):
     if args.dres:
         params["D_res"] = torch.from_numpy(
             np.random.default_rng([23068, 7]).standard_normal(D).astype(np.float32)).to(dev)
+    if args.groups > 1:
+        G = args.groups
+        r = np.random.default_rng([23068, 8])
+        params["n_groups"] = G
+        params["W_B"] = torch.from_numpy((r.standard_normal((D, G * N)) / np.sqrt(D)).astype(np.float32)).to(dev)
+        params["W_C"] = torch.from_numpy((r.standard_normal((D, G * N)) / np.sqrt(D)).astype(np.float32)).to(dev)
     if args.complex:
         params["A"] = torch.full((D, N), -0.5, device=dev)
         params["A_im"] = (np.pi * torch.arange(N, device=dev, dtype=torch.float32)).expand(D, N).contiguous()
@@ -244,7 +252,7 @@ def setup_ssm(args, np, torch, binding, inputs):
             payload += x.numel() * 4
     del inp
     plan = binding.plan(B, L, D, N, K, cfg.in_dtype, args.seg_len, args.chunk_segs, args.order, args.drive, args.act,
-                        complex_a=args.complex)
+                        complex_a=args.complex, groups=args.groups)
     ws = torch.empty(plan["workspace_bytes"], device=dev, dtype=torch.uint8)
 
     if args.order == 3:
@@ -441,7 +449,8 @@ def main():
 
 def variant_suffix(args):
     parts = ([args.drive] if args.drive != "euler" else []) + ([args.act] if args.act != "identity" else []) + \
-        (["dres"] if args.dres else []) + (["s4dlin"] if args.complex else [])
+        (["dres"] if args.dres else []) + (["s4dlin"] if args.complex else []) + \
+        ([f"g{args.groups}"] if args.groups > 1 else [])
     return "".join("-" + p for p in parts)
 
 

@@ -134,6 +134,13 @@ typedef struct pgf_params {
      * real, imaginary f32).  First order only, Euler drive, no output map,
      * N <= 16, K <= 2. */
     const float *A_im;
+    /* Channel groups with their own B and C (Mamba-style grouped
+     * projections), 0 or 1 = one group.  With G > 1 groups, W_B and W_C are
+     * [D, G*N], b_B and b_C [G*N], and channel d uses the columns
+     * [gN, (g+1)N) of group g = d / (D/G).  D/G must be a multiple of 64
+     * and G*N a power of two, at most 64.  First order only, Euler drive (the output map is
+     * allowed), N <= 16, K <= 2. */
+    int32_t n_groups;
 } pgf_params;
 
 /* How a call is tiled (host-side planning; no device access). */
@@ -148,8 +155,8 @@ typedef struct pgf_plan_info {
 } pgf_plan_info;
 
 /* Bytes of workspace a call with these sizes needs.  Reads the size
- * fields, in_dtype, seg_len, chunk_segs, order, drive and activation, and
- * tests D_res and A_im for NULL (never dereferenced).  Returns 0 if the
+ * fields, in_dtype, seg_len, chunk_segs, order, drive, activation and
+ * n_groups, and tests D_res and A_im for NULL (never dereferenced).  Returns 0 if the
  * sizes are invalid or unsupported.  Host only. */
 size_t pgf_workspace_bytes(const pgf_params *p);
 

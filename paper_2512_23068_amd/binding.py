@@ -38,6 +38,7 @@ class PgfParams(ctypes.Structure):
         ("workspace", _c_f), ("workspace_bytes", ctypes.c_size_t),
         ("d2h_in", _c_f), ("d2h_out", _c_f),
         ("drive", ctypes.c_int32), ("activation", ctypes.c_int32), ("D_res", _c_f), ("A_im", _c_f),
+        ("n_groups", ctypes.c_int32),
     ]
 
 
@@ -131,11 +132,12 @@ def workspace_bytes(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, orde
 
 
 def plan(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1, drive="euler", act="identity",
-         complex_a=False) -> dict:
+         complex_a=False, groups=1) -> dict:
     """The tiling a call would use (complex_a: with a complex transition;
     the planner only tests A_im for NULL, the pointer is never read)."""
     info = PgfPlanInfo()
     pr = make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs, order, drive, act)
+    pr.n_groups = int(groups)
     if complex_a:
         pr.A_im = 1
     _check(lib().pgf_plan(ctypes.byref(pr), ctypes.byref(info)))
@@ -161,9 +163,11 @@ def _model_params(pr, params, D, dev, keep):
     pointers in pr; returns N."""
     A = _dev_param(params["A"], (D, params["A"].shape[1]), dev, "A")
     N = A.shape[1]
+    G = int(params.get("n_groups") or 1)
+    pr.n_groups = G
     vals = {"A": A}
-    for name, shape in (("w_delta", (D,)), ("b_delta", (D,)), ("W_B", (D, N)), ("W_C", (D, N)),
-                        ("b_B", (N,)), ("b_C", (N,))):
+    for name, shape in (("w_delta", (D,)), ("b_delta", (D,)), ("W_B", (D, G * N)), ("W_C", (D, G * N)),
+                        ("b_B", (G * N,)), ("b_C", (G * N,))):
         vals[name] = _dev_param(params.get(name), shape, dev, name)
     for name, v in vals.items():
         keep.append(v)

@@ -72,11 +72,20 @@ int make_plan(const pgf_params *p, Plan *plan) {
     if (var && (K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
     const int cplx = p->A_im ? 1 : 0;
     if (cplx && (order != 1 || var || K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
+    if (p->n_groups < 0) return PGF_ERR_INVALID_ARG;
+    const int64_t groups = p->n_groups > 1 ? p->n_groups : 1;
+    if (groups > 1) {
+        if (D % groups != 0 || (D / groups) % 64 != 0) return PGF_ERR_INVALID_ARG;
+        if (order != 1 || cplx || (var & 1) || K > 2 || N > 16) return PGF_ERR_UNSUPPORTED;
+        // one projection pass of 2*groups*N <= 128 columns, a power of two
+        if (groups * N > 64 || !is_pow2(groups * N)) return PGF_ERR_UNSUPPORTED;
+    }
 
     Plan q{};
     q.B = B; q.L = L; q.D = D; q.N = N; q.K = K;
     q.order = order;
-    q.var = var;
+    q.var = var | (groups > 1 ? 4 : 0);
+    q.groups = (int)groups;
     q.KP = order == 3 ? 0 : K;
     q.cplx = cplx;
     q.comp = (int)((1 + K + (order == 2 ? 1 : 0)) * (cplx ? 2 : 1));
@@ -84,7 +93,7 @@ int make_plan(const pgf_params *p, Plan *plan) {
     // Registers per thread grow as nt*(3+K); keep them near 128.
     q.nt = (int)std::min<int64_t>(N, K >= 8 ? 4 : (K >= 4 ? 8 : 16));
     q.ns = (int)(N / q.nt);
-    q.R = (int)(2 * N * (1 + q.KP));
+    q.R = (int)(groups * 2 * N * (1 + q.KP));
 
     // Blocks of one segment column (every channel, one segment).
     const int64_t nblk = B * ((D * q.ns + 255) / 256);

@@ -13,7 +13,7 @@ namespace pgf {
 // Offsets (bytes) of the workspace sections; each is 256-byte aligned.
 //   state   [(1+K)][B][N][D]         state carried between host blocks
 //   bc      [B][Tc][R]               per-step projections of one host block,
-//                                    R = 2N(1+KP): B, dB_0..dB_{KP-1}, C, dC_0..
+//                                    per group 2N(1+KP): B, dB_0..dB_{KP-1}, C, dC_0..
 //   agg_h   [B][G][(1+K)][N][D]      segment end states from a zero start,
 //                                    then (in place) the true state
 //                                    entering each segment
@@ -30,7 +30,8 @@ struct Plan {
     int64_t B, L, D, N, K;
     int order;           // 1, 2, or 3 (parameter flows)
     int64_t KP;          // directions projected by k_proj (K, or 0 for order 3)
-    int var;             // model variant bits of the first-order scan (kZoh 1, kOutMap 2)
+    int var;             // model variant bits of the first-order scan (kZoh 1, kOutMap 2, kGroups 4)
+    int groups;          // channel groups with their own B and C (1 = one group)
     int cplx;            // complex diagonal transition (state in real/imaginary planes)
     int comp;            // state planes per lane: 1 + K (+ 1 for the mixed flow), twice that if complex
     int in_bf16;
@@ -39,7 +40,7 @@ struct Plan {
     int chunk_segs;      // segments per host block (1 when sequential)
     int64_t chunk_len;   // steps per host block
     int64_t n_chunks;
-    int R;               // floats per step record in bc: 2N(1+KP)
+    int R;               // floats per step in bc: groups * 2N(1+KP)
     Layout ws;
 };
 

@@ -125,12 +125,18 @@ __device__ __forceinline__ void discretize2(float xv, float w, float bd, float &
 // Model variants of the first-order scan, selected by the VAR template
 // argument of k_scan: bit 0 (kZoh) replaces the Euler drive Delta*B*x with
 // the zero-order-hold drive (Abar - 1)/A * B*x; bit 1 (kOutMap) applies the
-// output map y = act(sum_n C h + D_res x) with its derivative.
+// output map y = act(sum_n C h + D_res x) with its derivative; bit 2
+// (kGroups) reads the B and C of the channel's group (Mamba-style grouped
+// projections): a step's records hold G blocks of 2N(1+K) floats and a
+// wave (64 consecutive channels) lies in one group.
 constexpr int kZoh = 1;
 constexpr int kOutMap = 2;
+constexpr int kGroups = 4;   // channel groups with their own B and C
 struct Variant {
     const float *D_res;   // [D] residual weight, or NULL (= 0)
     int act;              // PGF_ACT_IDENTITY or PGF_ACT_SILU
+    int groups;           // channel groups G (records hold G blocks per step)
+    int64_t group_ch;     // channels per group, a multiple of 64
 };
 
 // The ZOH drive coefficient e = (Abar - 1)/A of one lane, z = Delta*A,
@@ -163,6 +169,8 @@ __device__ __forceinline__ void silu_and_slope(float v, float &f, float &df) {
 
 // ---------------------------------------------------------------- k_proj
 // rec[b][t-t0] = [B(N) | dB_0..dB_{K-1} (N each) | C(N) | dC_0..dC_{K-1}]
+// (GROUPED: one such record of gn-wide blocks per channel group, NC =
+// 2 * groups * gn columns of [W_B | W_C]).
 // Row source s = blockIdx.y: 0 -> x (bias added), 1+k -> dx_k.
 // out[row][j] = sum_d X[row][d] * W[d][j], W = [W_B | W_C], on the matrix
 // cores: v_mfma_f32_16x16x4f32 computes D(16x16) += A(16x4) B(4x16) with,
@@ -199,11 +207,12 @@ __device__ __forceinline__ floatx4 load4<uint16_t>(const uint16_t *__restrict__ 
     return v;
 }
 
-template <int NC, typename InT>
+template <int NC, typename InT, bool GROUPED>
 __global__ __launch_bounds__(kThreads) void k_proj(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ WB,
     const float *__restrict__ WC, const float *__restrict__ bB, const float *__restrict__ bC,
-    float *__restrict__ bc, int64_t Bsz, int64_t L, int64_t D, int K, int64_t t0, int64_t len, int64_t Tc) {
+    float *__restrict__ bc, int64_t Bsz, int64_t L, int64_t D, int K, int64_t t0, int64_t len, int64_t Tc,
+    int gn) {
     constexpr int N = NC / 2;
     constexpr int CT = (NC + 15) / 16;  // 16-column tiles (zero-padded)
     constexpr int NCP = CT * 16;
@@ -286,7 +295,7 @@ __global__ __launch_bounds__(kThreads) void k_proj(
         if (st + 1 < nst) stash(buf ^ 1);
         __syncthreads();
     }
-    const int R = 2 * N * (1 + K);
+    const int R = 2 * N * (1 + K);     // a step's records (all groups)
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
@@ -298,12 +307,16 @@ __global__ __launch_bounds__(kThreads) void k_proj(
                 if (row >= len || col >= NC) continue;
                 float *out = bc + (b * Tc + row) * R;
                 float v = acc[rt][c][r];
-                if (col < N) {
-                    if (s == 0 && bB) v += bB[col];
-                    out[s * N + col] = v;
+                const bool isB = col < N;
+                const int cc = isB ? col : col - N;
+                if (s == 0 && (isB ? bB : bC)) v += (isB ? bB : bC)[cc];
+                if constexpr (GROUPED) {
+                    // column cc of [W_B | W_C] belongs to group cc / gn; a
+                    // group's record is [B | dB_k | C | dC_k], gn each
+                    const int g = cc / gn, n = cc % gn;
+                    out[g * 2 * gn * (1 + K) + (isB ? 0 : (1 + K) * gn) + s * gn + n] = v;
                 } else {
-                    if (s == 0 && bC) v += bC[col - N];
-                    out[(1 + K) * N + s * N + (col - N)] = v;
+                    out[(isB ? 0 : (1 + K) * N) + s * N + cc] = v;
                 }
             }
         }
@@ -382,7 +395,14 @@ __global__ __launch_bounds__(kThreads) void k_scan(
     float *Yb = y + (b * L + t0) * D;
     float *DYb = dy + (b * L + t0) * D;
     const uint32_t Du = (uint32_t)D, du = (uint32_t)d;
+    // Records of this channel's group; with groups a step holds G records.
+    int64_t Rt = R;
     const float *rec0 = bc + b * Tc * R;
+    if constexpr ((VAR & kGroups) != 0) {
+        Rt = (int64_t)vr.groups * R;
+        const int grp = __builtin_amdgcn_readfirstlane((int)(d / vr.group_ch));
+        rec0 = bc + b * Tc * Rt + (int64_t)grp * R;
+    }
 
     float xc[TT], dxc[K][TT];
 #pragma unroll
@@ -421,7 +441,7 @@ __global__ __launch_bounds__(kThreads) void k_scan(
 #pragma unroll
                     for (int k = 0; k < K; ++k) sdD[k] += dD[k];
                 }
-                const float *rec = rec0 + t * R;
+                const float *rec = rec0 + t * Rt;
                 float yv = 0.0f, dyv[K];
 #pragma unroll
                 for (int k = 0; k < K; ++k) dyv[k] = 0.0f;
@@ -789,7 +809,7 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
 // drive bit of a variant.
 template <int NT, int NS, int K, bool OUT, typename InT, int VAR>
 constexpr auto scan_kernel() {
-    if constexpr (NS == 1) return &k_scan<NT, NS, K, OUT, InT, OUT ? VAR : (VAR & kZoh)>;
+    if constexpr (NS == 1) return &k_scan<NT, NS, K, OUT, InT, OUT ? VAR : (VAR & (kZoh | kGroups))>;
     else return &k_scan_sh<NT, NS, K, OUT, InT>;
 }
 
@@ -1682,17 +1702,25 @@ struct Launcher {
         constexpr int TM = 128;
         dim3 grid((unsigned)((len + TM - 1) / TM), (unsigned)(1 + q.KP), (unsigned)q.B);
         Timed tm(0, st);
-        hipLaunchKernelGGL((k_proj<NC, InT>), grid, dim3(kThreads), 0, st, x, dx, p.W_B, p.W_C, p.b_B, p.b_C,
-                           bcw(), q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len);
+        if (q.groups > 1)
+            hipLaunchKernelGGL((k_proj<NC, InT, true>), grid, dim3(kThreads), 0, st, x, dx, p.W_B, p.W_C, p.b_B,
+                               p.b_C, bcw(), q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len, (int)q.N);
+        else
+            hipLaunchKernelGGL((k_proj<NC, InT, false>), grid, dim3(kThreads), 0, st, x, dx, p.W_B, p.W_C, p.b_B,
+                               p.b_C, bcw(), q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len, (int)q.N);
     }
 
-    void proj(int64_t t0, int64_t len) {
-        switch (q.N) {
-            case 4: proj_nc<8>(t0, len); break;
-            case 8: proj_nc<16>(t0, len); break;
-            case 16: proj_nc<32>(t0, len); break;
-            case 32: proj_nc<64>(t0, len); break;
-            default: proj_nc<128>(t0, len); break;
+    // One pass over x (and each dx_k) computes the B and C columns of every
+    // channel group: 2 * groups * N columns (a power of two, checked by the
+    // planner).
+    bool proj(int64_t t0, int64_t len) {
+        switch (2 * q.groups * q.N) {
+            case 8: proj_nc<8>(t0, len); return true;
+            case 16: proj_nc<16>(t0, len); return true;
+            case 32: proj_nc<32>(t0, len); return true;
+            case 64: proj_nc<64>(t0, len); return true;
+            case 128: proj_nc<128>(t0, len); return true;
+            default: return false;
         }
     }
 
@@ -1700,7 +1728,7 @@ struct Launcher {
     void scans(int64_t t0, int64_t len) {
         const unsigned gx = (unsigned)((q.D * NS + kThreads - 1) / kThreads);
         const int64_t ND = q.N * q.D;
-        const Variant vr{p.D_res, p.activation};
+        const Variant vr{p.D_res, p.activation, q.groups, q.D / q.groups};
         if (q.seg == 0) {
             // Sequential evaluation: one segment per block, state in place.
             Timed tm(3, st);
@@ -1756,6 +1784,8 @@ struct Launcher {
                 case kZoh: return variant_block<K, kZoh>(t0, len);
                 case kOutMap: return variant_block<K, kOutMap>(t0, len);
                 case kZoh | kOutMap: return variant_block<K, kZoh | kOutMap>(t0, len);
+                case kGroups: return variant_block<K, kGroups>(t0, len);
+                case kGroups | kOutMap: return variant_block<K, kGroups | kOutMap>(t0, len);
                 default: return false;
             }
         } else if (q.var != 0) {
@@ -1963,8 +1993,7 @@ struct Launcher {
         }
         for (int64_t t0 = 0; t0 < q.L; t0 += q.chunk_len) {
             const int64_t len = q.L - t0 < q.chunk_len ? q.L - t0 : q.chunk_len;
-            proj(t0, len);
-            if (!scan_block(t0, len)) return PGF_ERR_UNSUPPORTED;
+            if (!proj(t0, len) || !scan_block(t0, len)) return PGF_ERR_UNSUPPORTED;
         }
         if (q.order == 3) {
             Timed tm(4, st);

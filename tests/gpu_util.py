@@ -7,6 +7,7 @@ from oracle import oracle
 from paper_2512_23068_amd import binding, inputs
 
 PARAM_KEYS = ("A", "w_delta", "b_delta", "W_B", "W_C", "b_B", "b_C", "D_res", "A_im")
+INT_KEYS = ("n_groups",)
 TOL = 1e-5   # relative L2, f32 state against the fp64 oracle
 
 
@@ -15,7 +16,9 @@ def dev():
 
 
 def params_to_dev(inp):
-    return {k: torch.from_numpy(np.ascontiguousarray(inp[k])).to(dev()) for k in PARAM_KEYS if k in inp}
+    out = {k: torch.from_numpy(np.ascontiguousarray(inp[k])).to(dev()) for k in PARAM_KEYS if k in inp}
+    out.update({k: inp[k] for k in INT_KEYS if k in inp})
+    return out
 
 
 def inputs_to_dev(inp, bf16=None):

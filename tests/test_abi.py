@@ -197,3 +197,18 @@ def test_complex_transition_plans():
         for k, v in kw.items():
             setattr(q, k, v)
         assert binding.lib().pgf_workspace_bytes(ctypes.byref(q)) == 0, kw
+
+
+def test_group_plans():
+    base = binding.make_params(1, 1000, 256, 16, 1)
+    g = binding.make_params(1, 1000, 256, 16, 1)
+    g.n_groups = 4
+    lib = binding.lib()
+    assert lib.pgf_workspace_bytes(ctypes.byref(g)) > lib.pgf_workspace_bytes(ctypes.byref(base))
+    for D, G in ((256, 3), (192, 2), (192, 3)):   # D/G a multiple of 64, G*N a power of two
+        q = binding.make_params(1, 1000, D, 16, 1)
+        q.n_groups = G
+        assert lib.pgf_workspace_bytes(ctypes.byref(q)) == 0
+    q = binding.make_params(1, 1000, 256, 16, 2, order=2)
+    q.n_groups = 2
+    assert lib.pgf_workspace_bytes(ctypes.byref(q)) == 0
