@@ -138,6 +138,18 @@ def discretize(x, dx, w_delta, b_delta):
     return delta, ddelta
 
 
+def discretize_lowrank(x, dx, W_dx, W_dt, b_dt):
+    """Mamba's low-rank step size: z = (x W_dx) W_dt + b_dt with W_dx [D,R],
+    W_dt [R,D] (the rank-R bottleneck over all channels), Delta =
+    softplus(z), dDelta_k = sigmoid(z) * ((dx_k W_dx) W_dt).
+    x [B,L,D], dx [K,B,L,D] -> Delta [B,L,D], dDelta [K,B,L,D]."""
+    x, dx = _f64(x), _f64(dx)
+    Wx, Wt = _f64(W_dx), _f64(W_dt)
+    z = (x @ Wx) @ Wt + _f64(b_dt)
+    dz = (dx @ Wx) @ Wt
+    return np.logaddexp(0.0, z), expit(z)[None] * dz
+
+
 def project(x, dx, W_B, W_C, b_B=None, b_C=None):
     """B = x W_B (+b_B), C = x W_C (+b_C), dB_k = dx_k W_B, dC_k = dx_k W_C.
     x [B,L,D] -> [B,L,N]; dx [K,B,L,D] -> [K,B,L,N]."""
@@ -213,7 +225,9 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
     imaginary part of a complex diagonal transition: the state is complex,
     h_out/dh_out are returned complex, and y reads Re(C h)), and n_groups G
     (channel groups with their own B and C: W_B, W_C [D, G*N], b_B, b_C
-    [G*N]; channel d uses group d // (D/G)).
+    [G*N]; channel d uses group d // (D/G)), and W_dx [D,R], W_dt [R,D]
+    (Mamba's low-rank step size, see discretize_lowrank; b_delta is its
+    bias and w_delta is not used).
     drive: "euler" or "zoh" (the input drive, see core); act: "identity" or
     "silu" (the output activation, see output_map).
     channels: optional 1-D index array of channels d to compute (the
@@ -238,7 +252,8 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
     dy = np.empty((K, B, L, Ds))
     step = L if not chunk else int(chunk)
     step = max(step, 1)
-    w = _f64(params["w_delta"])[sel]
+    lowrank = params.get("W_dt") is not None
+    w = None if lowrank else _f64(params["w_delta"])[sel]
     bd = _f64(params["b_delta"])[sel]
     Dr = None if params.get("D_res") is None else _f64(params["D_res"])[sel]
     As = A[sel]
@@ -262,7 +277,11 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
                                    params.get("b_B"), params.get("b_C"))
         xs = np.ascontiguousarray(xc[..., sel])
         dxs = np.ascontiguousarray(dxc[..., sel])
-        delta, ddelta = discretize(xs, dxs, w, bd)
+        if lowrank:
+            delta, ddelta = discretize_lowrank(xc, dxc, params["W_dx"], params["W_dt"], params["b_delta"])
+            delta, ddelta = np.ascontiguousarray(delta[..., sel]), np.ascontiguousarray(ddelta[..., sel])
+        else:
+            delta, ddelta = discretize(xs, dxs, w, bd)
         # Channel groups: channel d reads the B, C of group d // (D / G)
         # (columns [g N, (g+1) N) of the projections); groups are independent
         # given their B and C, so each runs as its own recurrence.
