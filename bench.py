@@ -46,6 +46,8 @@ def parse():
                     help="channel groups with their own B and C (first order; D/groups a multiple of 64)")
     ap.add_argument("--complex", action="store_true",
                     help="complex diagonal transition with the S4D-Lin spectrum A = -1/2 + i*pi*n (first order)")
+    ap.add_argument("--lowrank", type=int, default=0,
+                    help="low-rank step size of rank R (Mamba's step-size projection; first order)")
     ap.add_argument("--seg-len", type=int, default=0, help="tiling override (0 = library default)")
     ap.add_argument("--chunk-segs", type=int, default=0, help="tiling override (0 = library default)")
     return ap.parse_args()
@@ -83,7 +85,7 @@ COPY_BYTES = 1 << 30
 KERNEL_KIND = {"k_proj": "proj", "k_la_prep": "proj", "k_carry": "carry", "k_pcarry": "carry", "k_la_carry": "carry",
                "k_gsum": "gsum", "k_state": "state_io", "k_gout": "state_io", "k_fill0": "state_io",
                "k_la_copy": "state_io"}
-SCAN_SRC = "paper_2512_23068_amd/csrc/pgf_scan.hip"
+SCAN_SRC = "paper_2512_23068_amd/csrc/pgf_scan_kernels.h"
 PLAN_SRC = "paper_2512_23068_amd/csrc/pgf_plan.cpp"
 LA_SRC = "paper_2512_23068_amd/csrc/pgf_la.hip"
 # Sections of the kernel source (delimited by "// ----...---- name" lines)
@@ -205,9 +207,11 @@ class Workload:
 
 def setup_ssm(args, np, torch, binding, inputs):
     cfg = inputs.get_config(args.workload)
-    variant = args.drive != "euler" or args.act != "identity" or args.dres or args.complex or args.groups > 1
+    variant = args.drive != "euler" or args.act != "identity" or args.dres or args.complex or args.groups > 1 or \
+        args.lowrank > 0
     if variant and args.order != 1:
-        print("bench.py: --drive/--act/--dres/--complex apply to the first order only", file=sys.stderr)
+        print("bench.py: --drive/--act/--dres/--complex/--groups/--lowrank apply to the first order only",
+              file=sys.stderr)
         sys.exit(2)
     if args.order == 2:
         # two independent N(0,1) directions on the same workload shape
@@ -233,6 +237,13 @@ def setup_ssm(args, np, torch, binding, inputs):
         params["n_groups"] = G
         params["W_B"] = torch.from_numpy((r.standard_normal((D, G * N)) / np.sqrt(D)).astype(np.float32)).to(dev)
         params["W_C"] = torch.from_numpy((r.standard_normal((D, G * N)) / np.sqrt(D)).astype(np.float32)).to(dev)
+    if args.lowrank > 0:
+        # x W_dx ~ N(0, |x|^2/D) per rank column; W_dt ~ U(-1, 1)/sqrt(R), the
+        # step-size projection's usual initialisation; b_delta stays the bias
+        R = args.lowrank
+        r = np.random.default_rng([23068, 9])
+        params["W_dx"] = torch.from_numpy((r.standard_normal((D, R)) / np.sqrt(D)).astype(np.float32)).to(dev)
+        params["W_dt"] = torch.from_numpy((r.uniform(-1.0, 1.0, (R, D)) / np.sqrt(R)).astype(np.float32)).to(dev)
     if args.complex:
         params["A"] = torch.full((D, N), -0.5, device=dev)
         params["A_im"] = (np.pi * torch.arange(N, device=dev, dtype=torch.float32)).expand(D, N).contiguous()
@@ -252,7 +263,7 @@ def setup_ssm(args, np, torch, binding, inputs):
             payload += x.numel() * 4
     del inp
     plan = binding.plan(B, L, D, N, K, cfg.in_dtype, args.seg_len, args.chunk_segs, args.order, args.drive, args.act,
-                        complex_a=args.complex, groups=args.groups)
+                        complex_a=args.complex, groups=args.groups, dt_rank=args.lowrank)
     ws = torch.empty(plan["workspace_bytes"], device=dev, dtype=torch.uint8)
 
     if args.order == 3:
@@ -450,7 +461,7 @@ def main():
 def variant_suffix(args):
     parts = ([args.drive] if args.drive != "euler" else []) + ([args.act] if args.act != "identity" else []) + \
         (["dres"] if args.dres else []) + (["s4dlin"] if args.complex else []) + \
-        ([f"g{args.groups}"] if args.groups > 1 else [])
+        ([f"g{args.groups}"] if args.groups > 1 else []) + ([f"lr{args.lowrank}"] if args.lowrank > 0 else [])
     return "".join("-" + p for p in parts)
 
 

@@ -141,6 +141,19 @@ typedef struct pgf_params {
      * and G*N a power of two, at most 64.  First order only, Euler drive (the output map is
      * allowed), N <= 16, K <= 2. */
     int32_t n_groups;
+    /* Low-rank step size (the Mamba step-size projection through a rank-R
+     * bottleneck over all channels, Sec. 3 with z_t = W_dt (W_dx^T x_t) + b):
+     * dt_rank = R in 1..128, or 0 for the per-channel step size above.  With
+     * R > 0 the step size is Delta = softplus(z), z = (x W_dx) W_dt +
+     * b_delta, and its tangent dDelta_k = sigmoid(z) (dx_k W_dx) W_dt;
+     *   W_dx : device, [D, R] f32, row-major
+     *   W_dt : device, [R, D] f32, row-major
+     * w_delta is not read (may be NULL).  First order only, Euler drive (the
+     * output map is allowed), one group, real A, N <= 16, K <= 2.  The
+     * workspace then also holds z and dz_k of one host block, [1+K][B][Tc][D]
+     * f32, and may reach 2 GiB. */
+    int32_t dt_rank;
+    const float *W_dx, *W_dt;
 } pgf_params;
 
 /* How a call is tiled (host-side planning; no device access). */
@@ -155,9 +168,10 @@ typedef struct pgf_plan_info {
 } pgf_plan_info;
 
 /* Bytes of workspace a call with these sizes needs.  Reads the size
- * fields, in_dtype, seg_len, chunk_segs, order, drive, activation and
- * n_groups, and tests D_res and A_im for NULL (never dereferenced).  Returns 0 if the
- * sizes are invalid or unsupported.  Host only. */
+ * fields, in_dtype, seg_len, chunk_segs, order, drive, activation,
+ * n_groups and dt_rank, and tests D_res and A_im for NULL (never
+ * dereferenced).  Returns 0 if the sizes are invalid or unsupported.  Host
+ * only. */
 size_t pgf_workspace_bytes(const pgf_params *p);
 
 /* Fill *info with the tiling a call would use.  Host only.  Returns a status. */

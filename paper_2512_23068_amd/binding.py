@@ -38,7 +38,7 @@ class PgfParams(ctypes.Structure):
         ("workspace", _c_f), ("workspace_bytes", ctypes.c_size_t),
         ("d2h_in", _c_f), ("d2h_out", _c_f),
         ("drive", ctypes.c_int32), ("activation", ctypes.c_int32), ("D_res", _c_f), ("A_im", _c_f),
-        ("n_groups", ctypes.c_int32),
+        ("n_groups", ctypes.c_int32), ("dt_rank", ctypes.c_int32), ("W_dx", _c_f), ("W_dt", _c_f),
     ]
 
 
@@ -132,12 +132,13 @@ def workspace_bytes(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, orde
 
 
 def plan(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1, drive="euler", act="identity",
-         complex_a=False, groups=1) -> dict:
+         complex_a=False, groups=1, dt_rank=0) -> dict:
     """The tiling a call would use (complex_a: with a complex transition;
     the planner only tests A_im for NULL, the pointer is never read)."""
     info = PgfPlanInfo()
     pr = make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs, order, drive, act)
     pr.n_groups = int(groups)
+    pr.dt_rank = int(dt_rank)
     if complex_a:
         pr.A_im = 1
     _check(lib().pgf_plan(ctypes.byref(pr), ctypes.byref(info)))
@@ -165,9 +166,14 @@ def _model_params(pr, params, D, dev, keep):
     N = A.shape[1]
     G = int(params.get("n_groups") or 1)
     pr.n_groups = G
+    # Low-rank step size: W_dx [D,R] and W_dt [R,D] replace w_delta.
+    R = 0 if params.get("W_dt") is None else int(params["W_dt"].shape[0])
+    pr.dt_rank = R
     vals = {"A": A}
     for name, shape in (("w_delta", (D,)), ("b_delta", (D,)), ("W_B", (D, G * N)), ("W_C", (D, G * N)),
-                        ("b_B", (G * N,)), ("b_C", (G * N,))):
+                        ("b_B", (G * N,)), ("b_C", (G * N,)), ("W_dx", (D, R)), ("W_dt", (R, D))):
+        if R and name == "w_delta":
+            continue
         vals[name] = _dev_param(params.get(name), shape, dev, name)
     for name, v in vals.items():
         keep.append(v)
@@ -270,8 +276,10 @@ def scan_jvp(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_i
 
     x [B,L,D] and dx [K,B,L,D]: float32 or bfloat16 CUDA tensors (same dtype).
     params: A, W_B, W_C [D,N]; w_delta, b_delta [D]; optional b_B, b_C [N],
-    D_res [D] (residual weight of the output map) and A_im [D,N] (imaginary
-    part of a complex transition; the states are then complex64).
+    D_res [D] (residual weight of the output map), A_im [D,N] (imaginary
+    part of a complex transition; the states are then complex64),
+    n_groups (W_B, W_C [D,G*N], b_B, b_C [G*N]) and W_dx [D,R], W_dt [R,D]
+    (low-rank step size; w_delta is then not used).
     drive: "euler" or "zoh"; act: "identity" or "silu" (the variants need
     N <= 16 and K <= 2).
     Returns (y [B,L,D], dy [K,B,L,D]) in float32, plus (h_out [B,D,N],

@@ -30,6 +30,10 @@ constexpr int64_t kDefaultSeg = 256;
 constexpr int64_t kSeqChunk = 4096;
 constexpr int64_t kMaxChunkLen = int64_t(1) << 18;
 constexpr size_t kWorkspaceCap = size_t(256) << 20;
+// A low-rank call also keeps Delta and dDelta_k of its host block: a larger cap keeps
+// its host blocks as long as the others' (2 GiB of 288 GB).
+constexpr size_t kLowRankWorkspaceCap = size_t(2) << 30;
+constexpr int kMaxRank = 128;
 
 int64_t gcd64(int64_t a, int64_t b) {
     while (b) {
@@ -80,11 +84,18 @@ int make_plan(const pgf_params *p, Plan *plan) {
         // one projection pass of 2*groups*N <= 128 columns, a power of two
         if (groups * N > 64 || !is_pow2(groups * N)) return PGF_ERR_UNSUPPORTED;
     }
+    if (p->dt_rank < 0 || p->dt_rank > kMaxRank) return PGF_ERR_INVALID_ARG;
+    const int rank = p->dt_rank;
+    if (rank && (order != 1 || cplx || groups > 1 || (var & 1) || K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
 
     Plan q{};
     q.B = B; q.L = L; q.D = D; q.N = N; q.K = K;
     q.order = order;
-    q.var = var | (groups > 1 ? 4 : 0);
+    q.var = var | (groups > 1 ? 4 : 0) | (rank ? 8 : 0);
+    q.rank = rank;
+    // the rank padded for the projection kernels: to a multiple of 16 up to
+    // 64, of 32 above
+    q.rc = rank <= 64 ? (rank + 15) / 16 * 16 : (rank + 31) / 32 * 32;
     q.groups = (int)groups;
     q.KP = order == 3 ? 0 : K;
     q.cplx = cplx;
@@ -129,8 +140,10 @@ int make_plan(const pgf_params *p, Plan *plan) {
         // At least three rounds of resident blocks per launch, rounded to a
         // whole number of rounds when the workspace allows it.
         const size_t per_seg = (size_t)B * q.comp * (size_t)(N * D + D) * sizeof(float) +
-                               (size_t)B * seg * q.R * sizeof(float);
-        const int64_t cap = std::max<int64_t>(1, (int64_t)(kWorkspaceCap / per_seg));
+                               (size_t)B * seg * q.R * sizeof(float) +
+                               (size_t)(1 + K) * B * seg * (size_t)(rank ? q.rc + D : 0) * sizeof(float);
+        const size_t wcap = rank ? kLowRankWorkspaceCap : kWorkspaceCap;
+        const int64_t cap = std::max<int64_t>(1, (int64_t)(wcap / per_seg));
         const int64_t period = kResidentBlocks / gcd64(nblk, kResidentBlocks);
         const int64_t want = (3 * kResidentBlocks + nblk - 1) / nblk;
         cs = (want + period - 1) / period * period;
@@ -159,6 +172,10 @@ int make_plan(const pgf_params *p, Plan *plan) {
     }
     w.gacc = off;
     if (order == 3) off = align256(off + 3 * (size_t)B * N * D * f);
+    w.lr = off;
+    if (rank) off = align256(off + (size_t)(1 + K) * B * q.chunk_len * q.rc * f);
+    w.dt = off;
+    if (rank) off = align256(off + (size_t)(1 + K) * B * q.chunk_len * D * f);
     w.total = off;
     q.ws = w;
     *plan = q;

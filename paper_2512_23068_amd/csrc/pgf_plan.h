@@ -20,17 +20,21 @@ namespace pgf {
 //   agg_s   [B][G][(1+K)][D]         segment sums of Delta and dDelta_k
 //   gacc    [3][B][N][D]             parameter flows only: running gradient
 //                                    sums (A, B offset, C offset) of the call
+//   lr      [(1+K)][B][Tc][RC]       low rank only: x W_dx and dx_k W_dx, the
+//                                    rank padded to RC (zero columns)
+//   dt      [(1+K)][B][Tc][D]        low rank only: Delta and dDelta_k
 // In the parameter flows K = 2 (the states dh/dA and dh/dB) and agg_h also
 // receives each segment's gradient partials after its rescan.
 struct Layout {
-    size_t state, bc, agg_h, agg_s, gacc, total;
+    size_t state, bc, agg_h, agg_s, gacc, lr, dt, total;
 };
 
 struct Plan {
     int64_t B, L, D, N, K;
     int order;           // 1, 2, or 3 (parameter flows)
     int64_t KP;          // directions projected by k_proj (K, or 0 for order 3)
-    int var;             // model variant bits of the first-order scan (kZoh 1, kOutMap 2, kGroups 4)
+    int var;             // model variant bits of the first-order scan (kZoh 1, kOutMap 2, kGroups 4, kLowRank 8)
+    int rank, rc;        // low-rank step size: rank R and its padded width (0 when off)
     int groups;          // channel groups with their own B and C (1 = one group)
     int cplx;            // complex diagonal transition (state in real/imaginary planes)
     int comp;            // state planes per lane: 1 + K (+ 1 for the mixed flow), twice that if complex

@@ -1,0 +1,2259 @@
+// libpgf kernels: fused primal + tangent (forward-mode JVP) scan of a
+// selective diagonal SSM for gfx950 (MI355X), and their launch sequence.
+// Included by one source file per input type (pgf_scan_f32.hip,
+// pgf_scan_bf16.hip), which instantiate pgf::launch; the entry points are in
+// pgf_scan.hip.
+//
+// Kernels, per host block of steps [t0, t0+len) (the block loop of Alg. 1):
+//   k_proj   per-step projections B, C (x W + b) and their tangents dB_k, dC_k
+//            (dx_k W) -- the contraction over channels, Sec. 3 selective maps.
+//   k_scan<false>  segment aggregate: each segment scanned from a zero state;
+//            writes its end state (h0, dh0_k) and the sums of Delta, dDelta_k.
+//   k_carry  sequential over the block's segments, per lane: composes the
+//            segment operators (Prop. 3.2, Eq. 5 summed over a segment:
+//            P = exp(A sum Delta), Q_k = P A sum dDelta_k) into the true
+//            state entering each segment.  Division-free: P underflowing to
+//            zero is exact and cannot produce Inf or NaN.
+//   k_scan<true>   rescans each segment from its true entry state and writes
+//            y and dy_k (Lemma 3.1 Eq. 3 with the full output derivative).
+// In the sequential evaluation (enough channels to fill the GPU) only k_proj
+// and k_scan<true> run, with the state handed from block to block.
+//
+// Arithmetic is f32 throughout; per lane and step the order of operations is
+// fixed, so results do not depend on the block size.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+#include <string.h>
+
+#include <mutex>
+#include <vector>
+
+#include "pgf_plan.h"
+#include "pgf_scan_launch.h"
+#include "pgf_timing.h"
+
+namespace pgf {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kThreads = 256;
+
+// ---------------------------------------------------------------- helpers
+
+// Loads of the input sequences at a 32-bit element offset from a base
+// pointer that is the same for the whole wave: the address is formed from a
+// scalar base and a 32-bit vector offset, with no 64-bit arithmetic per step.
+__device__ __forceinline__ float load_in(const float *__restrict__ base, uint32_t i) {
+    return *(const float *)((const char *)base + (size_t)(i * 4u));
+}
+__device__ __forceinline__ float load_in(const uint16_t *__restrict__ base, uint32_t i) {
+    const uint16_t v = *(const uint16_t *)((const char *)base + (size_t)(i * 2u));
+    return __uint_as_float(((uint32_t)v) << 16);
+}
+__device__ __forceinline__ void store_out(float *__restrict__ base, uint32_t i, float v) {
+    *(float *)((char *)base + (size_t)(i * 4u)) = v;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the NS consecutive lanes that share a channel (all of them get
+// the same bits: every step adds a lane pair symmetrically).
+template <int NS>
+__device__ __forceinline__ float group_sum(float v) {
+    if constexpr (NS >= 2) v += dpp_mov<0xB1>(v);   // quad_perm [1,0,3,2]
+    if constexpr (NS >= 4) v += dpp_mov<0x4E>(v);   // quad_perm [2,3,0,1]
+    if constexpr (NS >= 8) v += dpp_mov<0x141>(v);  // row_half_mirror
+    if constexpr (NS >= 16) v += dpp_mov<0x140>(v); // row_mirror
+    return v;
+}
+
+constexpr float kLog2eHi = 1.44269502162933349609375f;  // log2(e) rounded to f32
+constexpr float kLog2eLo = 1.925963033500011079e-08f;   // log2(e) - kLog2eHi
+constexpr float kLn2 = 0.693147180559945309f;
+
+// e^v for v <= 0 within ~2 ulp: v*log2(e) = p + lo exactly to f32 working
+// precision (an fma recovers the rounding error of p), 2^p from the
+// hardware exponential, and 2^lo ~ 1 + lo*ln2 applied as a correction.
+__device__ __forceinline__ float exp_nonpos(float v) {
+    const float p = v * kLog2eHi;
+    const float lo = fmaf(v, kLog2eHi, -p) + v * kLog2eLo;
+    const float e = __builtin_amdgcn_exp2f(p);
+    return fmaf(e, lo * kLn2, e);
+}
+
+// Step size and its sensitivity factor for one (t, d):
+//   Delta = softplus(z) = max(z, 0) + log1p(e),  e = exp(-|z|),  z = x*w + b
+//   dDelta = sigmoid(z) * w * dx = sw * dx.
+// log1p(e) for e in (0, 1] is 2 atanh(s) with s = e/(2+e) <= 1/3, summed as
+// 2s(1 + s^2/3 + ... + s^12/13): the first omitted term is below 2e-8
+// relative, and no 1+e is ever rounded, so small steps keep full precision.
+__device__ __forceinline__ void discretize(float xv, float w, float bd, float &delta, float &sw) {
+    const float z = fmaf(xv, w, bd);
+    const float e = exp_nonpos(-fabsf(z));
+    const float sv = e * __builtin_amdgcn_rcpf(2.0f + e);
+    const float q = sv * sv;
+    float poly = fmaf(q, 1.0f / 13.0f, 1.0f / 11.0f);
+    poly = fmaf(q, poly, 1.0f / 9.0f);
+    poly = fmaf(q, poly, 1.0f / 7.0f);
+    poly = fmaf(q, poly, 1.0f / 5.0f);
+    poly = fmaf(q, poly, 1.0f / 3.0f);
+    poly = fmaf(q, poly, 1.0f);
+    delta = fmaxf(z, 0.0f) + 2.0f * sv * poly;
+    const float r = __builtin_amdgcn_rcpf(1.0f + e);
+    sw = (z >= 0.0f ? r : e * r) * w;
+}
+
+// Also returns s2 = softplus''(z) * w^2 = sigmoid(z)(1 - sigmoid(z)) w^2,
+// which is e/(1+e)^2 * w^2 on both sides of z = 0.
+__device__ __forceinline__ void discretize2(float xv, float w, float bd, float &delta, float &sw, float &s2) {
+    const float z = fmaf(xv, w, bd);
+    const float e = exp_nonpos(-fabsf(z));
+    const float sv = e * __builtin_amdgcn_rcpf(2.0f + e);
+    const float q = sv * sv;
+    float poly = fmaf(q, 1.0f / 13.0f, 1.0f / 11.0f);
+    poly = fmaf(q, poly, 1.0f / 9.0f);
+    poly = fmaf(q, poly, 1.0f / 7.0f);
+    poly = fmaf(q, poly, 1.0f / 5.0f);
+    poly = fmaf(q, poly, 1.0f / 3.0f);
+    poly = fmaf(q, poly, 1.0f);
+    delta = fmaxf(z, 0.0f) + 2.0f * sv * poly;
+    const float r = __builtin_amdgcn_rcpf(1.0f + e);
+    sw = (z >= 0.0f ? r : e * r) * w;
+    s2 = (e * r) * r * (w * w);
+}
+
+// ---------------------------------------------------------------- variants
+// Model variants of the first-order scan, selected by the VAR template
+// argument of k_scan: bit 0 (kZoh) replaces the Euler drive Delta*B*x with
+// the zero-order-hold drive (Abar - 1)/A * B*x; bit 1 (kOutMap) applies the
+// output map y = act(sum_n C h + D_res x) with its derivative; bit 2
+// (kGroups) reads the B and C of the channel's group (Mamba-style grouped
+// projections): a step's records hold G blocks of 2N(1+K) floats and a
+// wave (64 consecutive channels) lies in one group; bit 3 (kLowRank) reads
+// Delta and dDelta_k precomputed by the low-rank projection (k_lowdt).
+constexpr int kZoh = 1;
+constexpr int kOutMap = 2;
+constexpr int kGroups = 4;   // channel groups with their own B and C
+constexpr int kLowRank = 8;  // low-rank step-size projection
+struct Variant {
+    const float *D_res;   // [D] residual weight, or NULL (= 0)
+    int act;              // PGF_ACT_IDENTITY or PGF_ACT_SILU
+    int groups;           // channel groups G (records hold G blocks per step)
+    int64_t group_ch;     // channels per group, a multiple of 64
+    const float *z;       // low rank: Delta, dDelta_k of the host block, [(1+K)][B][Tc][D]
+    int64_t zs;           // low rank: stride between its planes, B*Tc*D
+};
+
+// The ZOH drive coefficient e = (Abar - 1)/A of one lane, z = Delta*A,
+// Abar = exp(z) as computed by the caller.  For |z| < 1/4, e = Delta * phi(z) with
+// phi(z) = expm1(z)/z = sum_k z^k/(k+1)! summed to z^6 (the first omitted
+// term is below 2e-9 relative); otherwise (Abar - 1) * (1/A), where the
+// subtraction loses less than 3 bits.  A = 0 takes the first branch (e = Delta).
+__device__ __forceinline__ float zoh_coef(float delta, float a_n, float inv_a, float abar) {
+    const float z = delta * a_n;
+    float ph = fmaf(z, 1.0f / 5040.0f, 1.0f / 720.0f);
+    ph = fmaf(z, ph, 1.0f / 120.0f);
+    ph = fmaf(z, ph, 1.0f / 24.0f);
+    ph = fmaf(z, ph, 1.0f / 6.0f);
+    ph = fmaf(z, ph, 0.5f);
+    ph = fmaf(z, ph, 1.0f);
+    return fabsf(z) < 0.25f ? delta * ph : (abar - 1.0f) * inv_a;
+}
+
+// SiLU and its derivative at v: s = sigmoid(v) and 1 - s from one
+// e = exp(-|v|) (no cancellation on either side), silu = v s,
+// silu' = s + v s (1 - s).
+__device__ __forceinline__ void silu_and_slope(float v, float &f, float &df) {
+    const float e = exp_nonpos(-fabsf(v));
+    const float r = __builtin_amdgcn_rcpf(1.0f + e);
+    const float s = v >= 0.0f ? r : e * r;
+    const float sc = v >= 0.0f ? e * r : r;
+    f = v * s;
+    df = fmaf(v * s, sc, s);
+}
+
+// ---------------------------------------------------------------- k_proj
+// rec[b][t-t0] = [B(N) | dB_0..dB_{K-1} (N each) | C(N) | dC_0..dC_{K-1}]
+// (GROUPED: one such record of gn-wide blocks per channel group, NC =
+// 2 * groups * gn columns of [W_B | W_C]).
+// Row source s = blockIdx.y: 0 -> x (bias added), 1+k -> dx_k.
+// out[row][j] = sum_d X[row][d] * W[d][j], W = [W_B | W_C], on the matrix
+// cores: v_mfma_f32_16x16x4f32 computes D(16x16) += A(16x4) B(4x16) with,
+// for lane l, A[l%16][l/16], B[l/16][l%16] and D[4(l/16)+r][l%16] in
+// accumulator r.  Each wave owns 16 rows and every column; the channel
+// order of the sum is fixed (ascending blocks of 4), whatever the block of
+// rows, so outputs do not depend on how the sequence is tiled.
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// Loads 4 consecutive input values of one row (zero past D) as f32.
+template <typename InT>
+__device__ __forceinline__ floatx4 load4(const InT *__restrict__ row, int64_t d, int64_t D);
+template <>
+__device__ __forceinline__ floatx4 load4<float>(const float *__restrict__ row, int64_t d, int64_t D) {
+    if (d + 4 <= D && ((D & 3) == 0)) return *(const floatx4 *)(row + d);
+    floatx4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = d + i < D ? row[d + i] : 0.0f;
+    return v;
+}
+template <>
+__device__ __forceinline__ floatx4 load4<uint16_t>(const uint16_t *__restrict__ row, int64_t d, int64_t D) {
+    floatx4 v;
+    if (d + 4 <= D && ((D & 3) == 0)) {
+        const uint2 u = *(const uint2 *)(row + d);
+        v[0] = __uint_as_float(u.x << 16);
+        v[1] = __uint_as_float(u.x & 0xffff0000u);
+        v[2] = __uint_as_float(u.y << 16);
+        v[3] = __uint_as_float(u.y & 0xffff0000u);
+        return v;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = d + i < D ? __uint_as_float(((uint32_t)row[d + i]) << 16) : 0.0f;
+    return v;
+}
+
+// Rows x W on the matrix cores, for one block of TM = 128 rows of a row
+// source src ([len][D], row-major): acc[rt][c] receives the 16x16 tile
+// (rows wave*32 + rt*16 .., columns c*16 ..) of src[r0.., :] * W, where
+// wload(d, j) is W[d][j] for j < NC (zero is returned past the matrix).
+// X tiles are staged through LDS, double-buffered, with the next channel
+// stage in flight; the channel order of the sum is fixed.
+constexpr int kProjRT = 2;                      // 16-row tiles per wave
+constexpr int kProjTM = 4 * 16 * kProjRT;       // rows per block
+
+template <int NC, typename InT, class WLoad>
+__device__ __forceinline__ void xw_tiles(const InT *__restrict__ src, int64_t D, int64_t len, int64_t r0,
+                                         WLoad wload, floatx4 (&acc)[kProjRT][(NC + 15) / 16]) {
+    constexpr int CT = (NC + 15) / 16;  // 16-column tiles (zero-padded)
+    constexpr int NCP = CT * 16;
+    constexpr int RT = kProjRT;
+    constexpr int TM = kProjTM;
+    constexpr int DT = 32;              // channels per stage
+    constexpr int XP = DT + 4;          // padded LDS row pitch
+    constexpr int XV = TM * DT / 4 / kThreads;   // float4 of X per thread per stage
+    constexpr int WE = (DT * NCP + kThreads - 1) / kThreads;
+    __shared__ float Xs[2][TM][XP];
+    __shared__ float Ws[2][DT][NCP + 4];
+
+    const int tid = threadIdx.x;
+    const int wave = tid / 64, lane = tid % 64;
+    floatx4 xr[XV];
+    float wr[WE];
+    auto fetch = [&](int64_t d0) {
+#pragma unroll
+        for (int i = 0; i < XV; ++i) {
+            const int e = tid + i * kThreads;          // float4 index in the tile
+            const int r = e / (DT / 4), c4 = e % (DT / 4);
+            const int64_t row = r0 + r;
+            xr[i] = row < len ? load4<InT>(src + row * D, d0 + 4 * c4, D) : floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+        }
+#pragma unroll
+        for (int i = 0; i < WE; ++i) {
+            const int e = tid + i * kThreads;
+            const int dd = e / NCP, j = e % NCP;
+            const int64_t d = d0 + dd;
+            float v = 0.0f;
+            if (e < DT * NCP && d < D && j < NC) v = wload(d, j);
+            wr[i] = v;
+        }
+    };
+    auto stash = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < XV; ++i) {
+            const int e = tid + i * kThreads;
+            const int r = e / (DT / 4), c4 = e % (DT / 4);
+            *(floatx4 *)&Xs[buf][r][4 * c4] = xr[i];
+        }
+#pragma unroll
+        for (int i = 0; i < WE; ++i) {
+            const int e = tid + i * kThreads;
+            if (e < DT * NCP) Ws[buf][e / NCP][e % NCP] = wr[i];
+        }
+    };
+
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int c = 0; c < CT; ++c) acc[rt][c] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    const int64_t nst = (D + DT - 1) / DT;
+    fetch(0);
+    stash(0);
+    __syncthreads();
+    for (int64_t st = 0; st < nst; ++st) {
+        const int buf = (int)(st & 1);
+        if (st + 1 < nst) fetch((st + 1) * DT);
+#pragma unroll
+        for (int kk = 0; kk < DT / 4; ++kk) {
+            float bv[CT];
+#pragma unroll
+            for (int c = 0; c < CT; ++c) bv[c] = Ws[buf][kk * 4 + lane / 16][c * 16 + lane % 16];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                const float a = Xs[buf][wave * 16 * RT + rt * 16 + lane % 16][kk * 4 + lane / 16];
+#pragma unroll
+                for (int c = 0; c < CT; ++c)
+                    acc[rt][c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[c], acc[rt][c], 0, 0, 0);
+            }
+        }
+        if (st + 1 < nst) stash(buf ^ 1);
+        __syncthreads();
+    }
+}
+
+// Row source s = blockIdx.y: 0 -> x, 1+k -> dx_k, of batch b = blockIdx.z.
+template <typename InT>
+__device__ __forceinline__ const InT *row_source(const InT *x, const InT *dx, int s, int64_t b, int64_t Bsz,
+                                                 int64_t L, int64_t t0, int64_t D) {
+    return s == 0 ? x + (b * L + t0) * D : dx + (((int64_t)(s - 1) * Bsz + b) * L + t0) * D;
+}
+
+// Per-step projections of one host block.  Grid (ceil(len/128), 1+KP, B):
+// rows of x (s = 0) or dx_{s-1} times [W_B | W_C] (NC = 2 * groups * N
+// columns) give B, dB_k, C, dC_k (per group), with the biases on s = 0.
+template <int NC, typename InT, bool GROUPED>
+__global__ __launch_bounds__(kThreads) void k_proj(
+    const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ WB,
+    const float *__restrict__ WC, const float *__restrict__ bB, const float *__restrict__ bC,
+    float *__restrict__ bc, int64_t Bsz, int64_t L, int64_t D, int K, int64_t t0, int64_t len, int64_t Tc,
+    int gn) {
+    constexpr int N = NC / 2;
+    constexpr int CT = (NC + 15) / 16;
+    constexpr int RT = kProjRT;
+    const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
+    const int s = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int64_t r0 = (int64_t)blockIdx.x * kProjTM;  // chunk-relative first row
+    floatx4 acc[RT][CT];
+    xw_tiles<NC, InT>(row_source(x, dx, s, b, Bsz, L, t0, D), D, len, r0,
+                      [&](int64_t d, int j) { return j < N ? WB[d * N + j] : WC[d * N + (j - N)]; }, acc);
+    const int R = 2 * N * (1 + K);     // a step's records (all groups)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+        for (int c = 0; c < CT; ++c) {
+            const int col = c * 16 + lane % 16;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int64_t row = r0 + wave * 16 * RT + rt * 16 + 4 * (lane / 16) + r;
+                if (row >= len || col >= NC) continue;
+                float *out = bc + (b * Tc + row) * R;
+                float v = acc[rt][c][r];
+                const bool isB = col < N;
+                const int cc = isB ? col : col - N;
+                if (s == 0 && (isB ? bB : bC)) v += (isB ? bB : bC)[cc];
+                if constexpr (GROUPED) {
+                    // column cc of [W_B | W_C] belongs to group cc / gn; a
+                    // group's record is [B | dB_k | C | dC_k], gn each
+                    const int g = cc / gn, n = cc % gn;
+                    out[g * 2 * gn * (1 + K) + (isB ? 0 : (1 + K) * gn) + s * gn + n] = v;
+                } else {
+                    out[(isB ? 0 : (1 + K) * N) + s * N + cc] = v;
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- low-rank step size
+// Mamba's step size through a rank-R bottleneck over all channels:
+//   z = (x W_dx) W_dt + b_dt,   dz_k = (dx_k W_dx) W_dt,
+//   Delta = softplus(z),        dDelta_k = sigmoid(z) dz_k,
+// per host block in two products on the matrix cores:
+//   k_lowx  : lr_s = X_s W_dx with the rank padded to RC (a multiple of 16;
+//             the padding columns are zero), s = 0 for x and 1+k for dx_k;
+//   k_lowdt : z and dz_k from lr and W_dt, stored as Delta and dDelta_k,
+//             which the scan reads in place of its own discretisation.
+//
+// k_lowdt reduces over r in the order r = q*KS + kk (KS = RC/4) on MFMA step
+// kk, where lane l of a 16-step group supplies step l%16 and q = l/16.  lr is
+// stored in that operand order: per 16-step group, RC/16 chunks of 64 lanes
+// x 4 floats, chunk i holding for lane l = 16q + j the entries
+// r = q*KS + 4i .. q*KS + 4i + 3 of step j, so a wave reads one chunk with
+// one contiguous 1 KiB load.
+__device__ __forceinline__ int64_t lr_offset(int64_t row, int r, int RC) {
+    const int KS = RC / 4, q = r / KS, kk = r % KS;
+    return (row / 16) * 16 * RC + (kk / 4) * 256 + (q * 16 + row % 16) * 4 + kk % 4;
+}
+
+template <int RC, typename InT>
+__global__ __launch_bounds__(kThreads) void k_lowx(
+    const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ Wdx, float *__restrict__ lr,
+    int64_t Bsz, int64_t L, int64_t D, int R, int64_t t0, int64_t len, int64_t Tc) {
+    constexpr int CT = RC / 16;
+    constexpr int RT = kProjRT;
+    const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
+    const int s = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int64_t r0 = (int64_t)blockIdx.x * kProjTM;
+    floatx4 acc[RT][CT];
+    xw_tiles<RC, InT>(row_source(x, dx, s, b, Bsz, L, t0, D), D, len, r0,
+                      [&](int64_t d, int j) { return j < R ? Wdx[d * R + j] : 0.0f; }, acc);
+    float *out = lr + ((int64_t)s * Bsz + b) * Tc * RC;
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+        for (int c = 0; c < CT; ++c) {
+            const int col = c * 16 + lane % 16;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int64_t row = r0 + wave * 16 * RT + rt * 16 + 4 * (lane / 16) + r;
+                if (row < len) out[lr_offset(row, col, RC)] = acc[rt][c][r];
+            }
+        }
+    }
+}
+
+// Grid (ncol * ceil(len/kLowRows), B): a block owns kLowCols channels and up
+// to kLowRows steps of one batch row, and its waves take 16-step groups in
+// turn (the last group of a block may be partial: its extra rows are
+// computed from whatever the workspace holds and never stored).  Lane l
+// keeps its B operands (W_dt entries) in registers for the whole block; the
+// next group's lr chunks are loaded while the current one's Delta and
+// dDelta_k are formed.  These go through a per-wave LDS tile so that every
+// store instruction writes whole 256-byte rows.
+constexpr int kLowCols = 64;
+constexpr int kLowRows = 1024;
+
+template <int RC, int K>
+__global__ __launch_bounds__(kThreads) void k_lowdt(
+    const float *__restrict__ lr, const float *__restrict__ Wdt, const float *__restrict__ bdt,
+    float *__restrict__ dt, int64_t Bsz, int64_t D, int R, int64_t len, int64_t Tc) {
+    constexpr int KS = RC / 4, CT = kLowCols / 16, TP = kLowCols + 4;
+    __shared__ __align__(16) float tile[4][1 + K][16][TP];   // per wave: Delta, dDelta_k of one group
+    const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
+    const int q = lane / 16;
+    const int64_t b = blockIdx.y;
+    const int64_t ncol = (D + kLowCols - 1) / kLowCols;
+    const int64_t col0 = (int64_t)(blockIdx.x % ncol) * kLowCols;
+    const int64_t rb = (int64_t)(blockIdx.x / ncol) * kLowRows;
+    const int64_t re = rb + kLowRows < len ? rb + kLowRows : len;
+    float wb[KS][CT], bias[CT];
+#pragma unroll
+    for (int c = 0; c < CT; ++c) {
+        const int64_t col = col0 + c * 16 + lane % 16;
+        bias[c] = col < D ? bdt[col] : 0.0f;
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+            const int r = q * KS + kk;
+            wb[kk][c] = (r < R && col < D) ? Wdt[(int64_t)r * D + col] : 0.0f;
+        }
+    }
+    const int64_t plane = Bsz * Tc;            // rows between directions
+    floatx4 a[1 + K][KS / 4];
+    auto fetch = [&](int64_t g0) {
+#pragma unroll
+        for (int s = 0; s < 1 + K; ++s) {
+            const float *src = lr + ((int64_t)s * plane + b * Tc + g0) * RC + lane * 4;
+#pragma unroll
+            for (int i = 0; i < KS / 4; ++i) a[s][i] = *(const floatx4 *)(src + 256 * i);
+        }
+    };
+    const bool vec = (D & 3) == 0;
+    int64_t g0 = rb + wave * 16;
+    if (g0 < re) fetch(g0);
+    for (; g0 < re; g0 += 4 * 16) {
+        floatx4 acc[1 + K][CT];
+#pragma unroll
+        for (int s = 0; s < 1 + K; ++s) {
+#pragma unroll
+            for (int c = 0; c < CT; ++c) acc[s][c] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+                for (int c = 0; c < CT; ++c)
+                    acc[s][c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s][kk / 4][kk % 4], wb[kk][c], acc[s][c], 0,
+                                                                     0, 0);
+        }
+        if (g0 + 4 * 16 < re) fetch(g0 + 4 * 16);
+#pragma unroll
+        for (int c = 0; c < CT; ++c) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                float delta, sig;
+                discretize(acc[0][c][r] + bias[c], 1.0f, 0.0f, delta, sig);
+                tile[wave][0][4 * q + r][c * 16 + lane % 16] = delta;
+#pragma unroll
+                for (int k = 0; k < K; ++k) tile[wave][1 + k][4 * q + r][c * 16 + lane % 16] = sig * acc[1 + k][c][r];
+            }
+        }
+        // The tile is private to this wave, whose LDS accesses complete in
+        // program order; the barrier keeps the compiler from reordering them.
+        __builtin_amdgcn_wave_barrier();
+        const int64_t col = col0 + 4 * (lane % 16);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int row = 4 * i + q;
+            if (g0 + row >= re) continue;
+#pragma unroll
+            for (int s = 0; s < 1 + K; ++s) {
+                const floatx4 v = *(const floatx4 *)&tile[wave][s][row][4 * (lane % 16)];
+                float *o = dt + (int64_t)s * plane * D + (b * Tc + g0 + row) * D + col;
+                if (vec && col + 4 <= D) {
+                    *(floatx4 *)o = v;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (col + e < D) o[e] = v[e];
+                }
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
+// ---------------------------------------------------------------- k_scan
+// Grid (ceil(D*NS/256), G, B); thread -> (channel d, state group ns).
+// OUT=false: segment aggregate from a zero state.  OUT=true: scan from the
+// entry state at init[b*ibs + g*igs + c*ics + n*D + d] and write y, dy; if
+// end_state is set (sequential evaluation) the exit state is stored there
+// with the same indexing (g = 0).
+template <int NT, int NS, int K, bool OUT, typename InT, int VAR = 0>
+__global__ __launch_bounds__(kThreads) void k_scan(
+    const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A,
+    const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
+    const float *__restrict__ init, int64_t ibs, int64_t igs, int64_t ics,
+    float *__restrict__ y, float *__restrict__ dy, float *__restrict__ end_state,
+    float *__restrict__ agg_h, float *__restrict__ agg_s,
+    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G, Variant vr) {
+    static_assert(VAR == 0 || NS == 1, "model variants run one thread per channel");
+    constexpr int N = NT * NS;
+    constexpr int R = 2 * N * (1 + K);
+    constexpr int DPB = kThreads / NS;
+    constexpr bool LR = (VAR & kLowRank) != 0;
+    constexpr int TT = LR ? 4 : 8;  // steps per register-prefetched tile
+    constexpr int KZ = LR ? 1 + K : 0;
+
+    const int tid = threadIdx.x;
+    const int ns = tid % NS;
+    const int64_t d_raw = (int64_t)blockIdx.x * DPB + tid / NS;
+    const bool active = d_raw < D;
+    const int64_t d = active ? d_raw : D - 1;
+    const int g = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int64_t ts = (int64_t)g * S;
+    const int64_t te = ts + S < len ? ts + S : len;
+    if (ts >= te) return;
+
+    float Af[NT], At[NT], Ai[NT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+        Af[i] = A[d * N + ns * NT + i];
+        At[i] = Af[i] * kLog2e;
+        if constexpr ((VAR & kZoh) != 0) Ai[i] = 1.0f / Af[i];
+    }
+    // With the low-rank projection Delta and dDelta_k arrive precomputed.
+    const float w = LR ? 0.0f : w_delta[d], bd = LR ? 0.0f : b_delta[d];
+    float Dr = 0.0f;
+    if constexpr ((VAR & kOutMap) != 0 && OUT) Dr = vr.D_res ? vr.D_res[d] : 0.0f;
+
+    float h[NT], dh[K][NT];
+    if constexpr (OUT) {
+        const float *ib = init + b * ibs + g * igs + d;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            const int n = ns * NT + i;
+            h[i] = ib[n * D];
+#pragma unroll
+            for (int k = 0; k < K; ++k) dh[k][i] = ib[(1 + k) * ics + n * D];
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            h[i] = 0.0f;
+#pragma unroll
+            for (int k = 0; k < K; ++k) dh[k][i] = 0.0f;
+        }
+    }
+    float sD = 0.0f, sdD[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) sdD[k] = 0.0f;
+
+    // Wave-uniform bases of this block of steps; per-lane offsets t*D + d
+    // stay below 2^30 elements (checked by the planner).
+    const int64_t dxs = Bsz * L * D;  // stride between directions
+    const InT *Xb = x + (b * L + t0) * D;
+    const InT *DXb = dx + (b * L + t0) * D;
+    float *Yb = y + (b * L + t0) * D;
+    float *DYb = dy + (b * L + t0) * D;
+    const uint32_t Du = (uint32_t)D, du = (uint32_t)d;
+    // Records of this channel's group; with groups a step holds G records.
+    int64_t Rt = R;
+    const float *rec0 = bc + b * Tc * R;
+    if constexpr ((VAR & kGroups) != 0) {
+        Rt = (int64_t)vr.groups * R;
+        const int grp = __builtin_amdgcn_readfirstlane((int)(d / vr.group_ch));
+        rec0 = bc + b * Tc * Rt + (int64_t)grp * R;
+    }
+
+    // Delta and dDelta_k of the host block (chunk-relative steps), low rank only.
+    const float *Zb = nullptr;
+    if constexpr (LR) Zb = vr.z + b * Tc * D;
+    float xc[TT], dxc[K][TT], zc[1 + K][TT];
+#pragma unroll
+    for (int j = 0; j < TT; ++j) {
+        const int64_t t = ts + j < te ? ts + j : te - 1;
+        xc[j] = load_in(Xb, (uint32_t)t * Du + du);
+#pragma unroll
+        for (int k = 0; k < K; ++k) dxc[k][j] = load_in(DXb + k * dxs, (uint32_t)t * Du + du);
+#pragma unroll
+        for (int k = 0; k < KZ; ++k) zc[k][j] = Zb[k * vr.zs + (uint32_t)t * Du + du];
+    }
+
+    for (int64_t tb = ts; tb < te; tb += TT) {
+        float xn[TT], dxn[K][TT], zn[1 + K][TT];
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
+            xn[j] = load_in(Xb, (uint32_t)t * Du + du);
+#pragma unroll
+            for (int k = 0; k < K; ++k) dxn[k][j] = load_in(DXb + k * dxs, (uint32_t)t * Du + du);
+#pragma unroll
+            for (int k = 0; k < KZ; ++k) zn[k][j] = Zb[k * vr.zs + (uint32_t)t * Du + du];
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + j;
+            if (t < te) {
+                const float xv = xc[j];
+                float delta, sw = 0.0f;
+                if constexpr (LR) delta = zc[0][j];
+                else discretize(xv, w, bd, delta, sw);
+                const float u = delta * xv;
+                float dD[K], pk[K];
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    dD[k] = LR ? zc[1 + k][j] : sw * dxc[k][j];
+                    pk[k] = fmaf(dD[k], xv, delta * dxc[k][j]);
+                }
+                if constexpr (!OUT) {
+                    sD += delta;
+#pragma unroll
+                    for (int k = 0; k < K; ++k) sdD[k] += dD[k];
+                }
+                const float *rec = rec0 + t * Rt;
+                float yv = 0.0f, dyv[K];
+#pragma unroll
+                for (int k = 0; k < K; ++k) dyv[k] = 0.0f;
+#pragma unroll
+                for (int i = 0; i < NT; ++i) {
+                    const int n = ns * NT + i;
+                    const float Bn = rec[n];
+                    const float a = __builtin_amdgcn_exp2f(delta * At[i]);
+                    const float sv = a * h[i];
+                    const float gv = Af[i] * sv;
+                    float hn;
+                    if constexpr ((VAR & kZoh) != 0) {
+                        // b = e B x, db_k = Abar dDelta_k B x + e (dB_k x + B dx_k)
+                        const float e = zoh_coef(delta, Af[i], Ai[i], a);
+                        const float Bx = Bn * xv;
+                        hn = fmaf(e, Bx, sv);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) {
+                            const float dBn = rec[(1 + k) * N + n];
+                            const float jk = fmaf(a * dD[k], Bx, e * fmaf(dBn, xv, Bn * dxc[k][j]));
+                            dh[k][i] = fmaf(a, dh[k][i], fmaf(gv, dD[k], jk));
+                        }
+                    } else {
+                        hn = fmaf(Bn, u, sv);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) {
+                            const float dBn = rec[(1 + k) * N + n];
+                            dh[k][i] = fmaf(a, dh[k][i], fmaf(gv, dD[k], fmaf(Bn, pk[k], dBn * u)));
+                        }
+                    }
+                    h[i] = hn;
+                    if constexpr (OUT) {
+                        const float Cn = rec[(1 + K) * N + n];
+                        yv = fmaf(Cn, hn, yv);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) {
+                            const float dCn = rec[(2 + K + k) * N + n];
+                            dyv[k] = fmaf(dCn, hn, fmaf(Cn, dh[k][i], dyv[k]));
+                        }
+                    }
+                }
+                if constexpr (OUT) {
+                    yv = group_sum<NS>(yv);
+#pragma unroll
+                    for (int k = 0; k < K; ++k) dyv[k] = group_sum<NS>(dyv[k]);
+                    if constexpr ((VAR & kOutMap) != 0) {
+                        yv = fmaf(Dr, xv, yv);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) dyv[k] = fmaf(Dr, dxc[k][j], dyv[k]);
+                        if (vr.act == PGF_ACT_SILU) {
+                            float f, df;
+                            silu_and_slope(yv, f, df);
+                            yv = f;
+#pragma unroll
+                            for (int k = 0; k < K; ++k) dyv[k] *= df;
+                        }
+                    }
+                    if (active && ns == 0) {
+                        store_out(Yb, (uint32_t)t * Du + du, yv);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) store_out(DYb + k * dxs, (uint32_t)t * Du + du, dyv[k]);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            xc[j] = xn[j];
+#pragma unroll
+            for (int k = 0; k < K; ++k) dxc[k][j] = dxn[k][j];
+#pragma unroll
+            for (int k = 0; k < KZ; ++k) zc[k][j] = zn[k][j];
+        }
+    }
+
+    if (!active) return;
+    if constexpr (OUT) {
+        if (end_state) {
+            float *eb = end_state + b * ibs + d;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                const int n = ns * NT + i;
+                eb[n * D] = h[i];
+#pragma unroll
+                for (int k = 0; k < K; ++k) eb[(1 + k) * ics + n * D] = dh[k][i];
+            }
+        }
+    } else {
+        const int64_t base = (b * G + g) * (1 + K);
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            const int n = ns * NT + i;
+            agg_h[(base * N + n) * D + d] = h[i];
+#pragma unroll
+            for (int k = 0; k < K; ++k) agg_h[((base + 1 + k) * N + n) * D + d] = dh[k][i];
+        }
+        if (ns == 0) {
+            agg_s[base * D + d] = sD;
+#pragma unroll
+            for (int k = 0; k < K; ++k) agg_s[(base + 1 + k) * D + d] = sdD[k];
+        }
+    }
+}
+
+// ---------------------------------------------------------------- k_scan_sh
+// The same scan for NS >= 2 threads per channel.  Per tile of TT steps the
+// block stages in LDS (double-buffered through registers, so the global
+// loads of tile i+1 overlap the arithmetic of tile i):
+//   s_rec  the TT step records (B, dB_k, C, dC_k), read by every channel;
+//   s_sc   per (t, d): Delta, u = Delta*x, dDelta_k, p_k = dDelta_k*x +
+//          Delta*dx_k, each computed once per channel instead of once per
+//          thread sharing it.
+template <int NT, int NS, int K, bool OUT, typename InT>
+__global__ __launch_bounds__(kThreads) void k_scan_sh(
+    const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A,
+    const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
+    const float *__restrict__ init, int64_t ibs, int64_t igs, int64_t ics,
+    float *__restrict__ y, float *__restrict__ dy, float *__restrict__ end_state,
+    float *__restrict__ agg_h, float *__restrict__ agg_s,
+    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G, Variant) {
+    static_assert(NS >= 2, "one thread per channel uses k_scan");
+    constexpr int N = NT * NS;
+    constexpr int R = 2 * N * (1 + K);
+    constexpr int DPB = kThreads / NS;       // channels per block
+    constexpr int TT = 8;                    // steps per tile
+    constexpr int SCW = 2 + 2 * K;           // Delta, u, dDelta_k, p_k
+    constexpr int SCP = SCW | 1;             // odd pitch against bank conflicts
+    constexpr int RV4 = (TT * R / 4 + kThreads - 1) / kThreads;  // record float4s per thread
+    constexpr int TQ = (TT * DPB + kThreads - 1) / kThreads;     // (t, d) tasks per thread
+    __shared__ floatx4 s_rec4[TT * R / 4];
+    __shared__ float s_sc[TT][DPB][SCP];
+    const float *s_rec = (const float *)s_rec4;
+    constexpr int O = 1 + K;                 // outputs per channel
+    constexpr int OP = O | 1;                // odd pitch of one lane's partials
+    constexpr int CW = 64 / NS;              // channels per wave
+    __shared__ float s_out[OUT ? 4 * CW * NS * OP : 1];
+
+    const int tid = threadIdx.x;
+    const int ns = tid % NS;
+    const int dl = tid / NS;
+    const int64_t d0 = (int64_t)blockIdx.x * DPB;
+    const bool active = d0 + dl < D;
+    const int64_t d = active ? d0 + dl : D - 1;
+    const int g = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int64_t ts = (int64_t)g * S;
+    const int64_t te = ts + S < len ? ts + S : len;
+    if (ts >= te) return;
+
+    float Af[NT], At[NT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+        Af[i] = A[d * N + ns * NT + i];
+        At[i] = Af[i] * kLog2e;
+    }
+    float h[NT], dh[K][NT];
+    if constexpr (OUT) {
+        const float *ib = init + b * ibs + g * igs + d;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            const int n = ns * NT + i;
+            h[i] = ib[n * D];
+#pragma unroll
+            for (int k = 0; k < K; ++k) dh[k][i] = ib[(1 + k) * ics + n * D];
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            h[i] = 0.0f;
+#pragma unroll
+            for (int k = 0; k < K; ++k) dh[k][i] = 0.0f;
+        }
+    }
+    float sD = 0.0f, sdD[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) sdD[k] = 0.0f;
+
+    const int64_t dxs = Bsz * L * D;
+    const InT *Xb = x + (b * L + t0) * D;
+    const InT *DXb = dx + (b * L + t0) * D;
+    float *Yb = y + (b * L + t0) * D;
+    float *DYb = dy + (b * L + t0) * D;
+    const uint32_t Du = (uint32_t)D;
+    const float *rec0 = bc + b * Tc * R;
+
+    // Registers holding the next tile while the current one is computed.
+    // Thread tid always owns the same tasks (channel d0 + j of step slot tt).
+    // Indices past the tile or past D are clamped to valid ones (their
+    // values are never used), so the loads need no branches.
+    floatx4 rr[RV4];
+    float xq[TQ], dxq[TQ][K], wq[TQ], bq[TQ];
+    int qt[TQ];          // step slot of task i
+    uint32_t qd[TQ];     // channel of task i
+#pragma unroll
+    for (int i = 0; i < TQ; ++i) {
+        const int qi = tid + i * kThreads;
+        const int j = qi % DPB;
+        const int64_t dj = d0 + j < D ? d0 + j : D - 1;
+        wq[i] = w_delta[dj];
+        bq[i] = b_delta[dj];
+        qt[i] = qi / DPB;
+        qd[i] = (uint32_t)dj;
+    }
+    auto fetch = [&](int64_t tb) {
+        const int nrow = (int)(te - tb < TT ? te - tb : TT);
+        const int lim4 = nrow * (R / 4) - 1;
+        const floatx4 *src4 = (const floatx4 *)(rec0 + tb * R);
+#pragma unroll
+        for (int i = 0; i < RV4; ++i) {
+            const int e4 = tid + i * kThreads;
+            rr[i] = src4[e4 < lim4 ? e4 : lim4];
+        }
+#pragma unroll
+        for (int i = 0; i < TQ; ++i) {
+            const int tt = qt[i] < nrow ? qt[i] : nrow - 1;
+            const uint32_t o = (uint32_t)(tb + tt) * Du + qd[i];
+            xq[i] = load_in(Xb, o);
+#pragma unroll
+            for (int k = 0; k < K; ++k) dxq[i][k] = load_in(DXb + k * dxs, o);
+        }
+    };
+    auto stash = [&]() {
+#pragma unroll
+        for (int i = 0; i < RV4; ++i) {
+            const int e4 = tid + i * kThreads;
+            if (e4 < TT * R / 4) s_rec4[e4] = rr[i];
+        }
+#pragma unroll
+        for (int i = 0; i < TQ; ++i) {
+            const int qi = tid + i * kThreads;
+            if (qi >= TT * DPB) break;
+            const int tt = qi / DPB, j = qi % DPB;
+            float delta, sw;
+            discretize(xq[i], wq[i], bq[i], delta, sw);
+            float *o = &s_sc[tt][j][0];
+            o[0] = delta;
+            o[1] = delta * xq[i];
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const float ddl = sw * dxq[i][k];
+                o[2 + k] = ddl;
+                o[2 + K + k] = fmaf(ddl, xq[i], delta * dxq[i][k]);
+            }
+        }
+    };
+
+    fetch(ts);
+    stash();
+    __syncthreads();
+    for (int64_t tb = ts; tb < te; tb += TT) {
+        const bool more = tb + TT < te;
+        if (more) fetch(tb + TT);
+        // Not unrolled: keeps the scheduler from hoisting the LDS reads of
+        // later steps, which would multiply the live registers.
+#pragma unroll 1
+        for (int tt = 0; tt < TT; ++tt) {
+            const int64_t t = tb + tt;
+            if (t >= te) break;
+            const float *sc = &s_sc[tt][dl][0];
+            const float delta = sc[0], u = sc[1];
+            float dD[K], pk[K];
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                dD[k] = sc[2 + k];
+                pk[k] = sc[2 + K + k];
+            }
+            if constexpr (!OUT) {
+                sD += delta;
+#pragma unroll
+                for (int k = 0; k < K; ++k) sdD[k] += dD[k];
+            }
+            const float *rec = s_rec + tt * R;
+            float yv = 0.0f, dyv[K];
+#pragma unroll
+            for (int k = 0; k < K; ++k) dyv[k] = 0.0f;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                const int n = ns * NT + i;
+                const float Bn = rec[n];
+                const float a = __builtin_amdgcn_exp2f(delta * At[i]);
+                const float sv = a * h[i];
+                const float gv = Af[i] * sv;
+                const float hn = fmaf(Bn, u, sv);
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    const float dBn = rec[(1 + k) * N + n];
+                    dh[k][i] = fmaf(a, dh[k][i], fmaf(gv, dD[k], fmaf(Bn, pk[k], dBn * u)));
+                }
+                h[i] = hn;
+                if constexpr (OUT) {
+                    const float Cn = rec[(1 + K) * N + n];
+                    yv = fmaf(Cn, hn, yv);
+#pragma unroll
+                    for (int k = 0; k < K; ++k) {
+                        const float dCn = rec[(2 + K + k) * N + n];
+                        dyv[k] = fmaf(dCn, hn, fmaf(Cn, dh[k][i], dyv[k]));
+                    }
+                }
+            }
+            if constexpr (OUT) {
+                // Sum the NS partial outputs of each channel through this
+                // wave's LDS slice: every lane writes its K+1 partials, then
+                // lane j adds the NS partials of output j (channel j / O,
+                // output j % O) in ascending order and stores it.  A wave's
+                // LDS operations complete in order, so no barrier is needed.
+                float *wo = s_out + (tid / 64) * (CW * NS * OP);
+                const int lw = tid % 64;
+                float *mine = wo + ((lw / NS) * NS + ns) * OP;
+                mine[0] = yv;
+#pragma unroll
+                for (int k = 0; k < K; ++k) mine[1 + k] = dyv[k];
+                __builtin_amdgcn_wave_barrier();
+#pragma unroll
+                for (int j = lw; j < CW * O; j += 64) {
+                    const int c = j / O, oi = j % O;
+                    const float *src = wo + c * NS * OP + oi;
+                    float v = src[0];
+#pragma unroll
+                    for (int q = 1; q < NS; ++q) v += src[q * OP];
+                    const int64_t dc = d0 + (tid / 64) * CW + c;
+                    if (dc < D) {
+                        float *base = oi == 0 ? Yb : DYb + (int64_t)(oi - 1) * dxs;
+                        store_out(base, (uint32_t)t * Du + (uint32_t)dc, v);
+                    }
+                }
+                __builtin_amdgcn_wave_barrier();
+            }
+        }
+        __syncthreads();
+        if (more) {
+            stash();
+            __syncthreads();
+        }
+    }
+
+    if (!active) return;
+    if constexpr (OUT) {
+        if (end_state) {
+            float *eb = end_state + b * ibs + d;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                const int n = ns * NT + i;
+                eb[n * D] = h[i];
+#pragma unroll
+                for (int k = 0; k < K; ++k) eb[(1 + k) * ics + n * D] = dh[k][i];
+            }
+        }
+    } else {
+        const int64_t base = (b * G + g) * (1 + K);
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            const int n = ns * NT + i;
+            agg_h[(base * N + n) * D + d] = h[i];
+#pragma unroll
+            for (int k = 0; k < K; ++k) agg_h[((base + 1 + k) * N + n) * D + d] = dh[k][i];
+        }
+        if (ns == 0) {
+            agg_s[base * D + d] = sD;
+#pragma unroll
+            for (int k = 0; k < K; ++k) agg_s[(base + 1 + k) * D + d] = sdD[k];
+        }
+    }
+}
+
+// Kernel for a tiling: one thread per channel, or several sharing one.
+// The aggregate pass (OUT = false) writes no outputs, so it drops the
+// output map of a variant.
+template <int NT, int NS, int K, bool OUT, typename InT, int VAR>
+constexpr auto scan_kernel() {
+    if constexpr (NS == 1) return &k_scan<NT, NS, K, OUT, InT, OUT ? VAR : (VAR & (kZoh | kGroups | kLowRank))>;
+    else return &k_scan_sh<NT, NS, K, OUT, InT>;
+}
+
+// ---------------------------------------------------------------- k_scan2
+// Second-order flow, one thread per channel with all NT = N states: the
+// primal h, the first-order flows hv, hw along v = dx[0] and w = dx[1]
+// (same operation order as k_scan, so y, dy match the first-order kernel)
+// and the mixed flow (App. G):
+//   hvw' = Abar hvw + Abar_w hv + Abar_v hw + Abar_vw h + b_vw
+// with Abar_v = A Abar dv, Abar_vw = A Abar (A dv dw + dvw) and
+// b_vw = B q + dBv pw + dBw pv,  q = dvw x + dv xw + dw xv,
+// pv = dv x + Delta xv, pw = dw x + Delta xw.  Layouts and grid as k_scan
+// with 4 state components (h, hv, hw, hvw).
+template <int NT, bool OUT, typename InT>
+__global__ __launch_bounds__(kThreads) void k_scan2(
+    const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A,
+    const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
+    const float *__restrict__ init, int64_t ibs, int64_t igs, int64_t ics,
+    float *__restrict__ y, float *__restrict__ dy, float *__restrict__ d2y, float *__restrict__ end_state,
+    float *__restrict__ agg_h, float *__restrict__ agg_s,
+    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    constexpr int N = NT;
+    constexpr int R = 6 * N;          // B, dBv, dBw, C, dCv, dCw
+    constexpr int TT = NT >= 16 ? 4 : 8;   // prefetch depth, bounded by the VGPR budget
+
+    const int tid = threadIdx.x;
+    const int64_t d_raw = (int64_t)blockIdx.x * kThreads + tid;
+    const bool active = d_raw < D;
+    const int64_t d = active ? d_raw : D - 1;
+    const int g = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int64_t ts = (int64_t)g * S;
+    const int64_t te = ts + S < len ? ts + S : len;
+    if (ts >= te) return;
+
+    float Af[NT], At[NT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+        Af[i] = A[d * N + i];
+        At[i] = Af[i] * kLog2e;
+    }
+    const float w = w_delta[d], bd = b_delta[d];
+
+    float h[NT], hv[NT], hw[NT], hvw[NT];
+    if constexpr (OUT) {
+        const float *ib = init + b * ibs + g * igs + d;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            h[i] = ib[i * D];
+            hv[i] = ib[ics + i * D];
+            hw[i] = ib[2 * ics + i * D];
+            hvw[i] = ib[3 * ics + i * D];
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NT; ++i) h[i] = hv[i] = hw[i] = hvw[i] = 0.0f;
+    }
+    float sD = 0.0f, sDv = 0.0f, sDw = 0.0f, sDvw = 0.0f;
+
+    const int64_t dxs = Bsz * L * D;
+    const InT *Xb = x + (b * L + t0) * D;
+    const InT *Vb = dx + (b * L + t0) * D;
+    const InT *Wb = Vb + dxs;
+    float *Yb = y + (b * L + t0) * D;
+    float *DVb = dy + (b * L + t0) * D;
+    float *DWb = DVb + dxs;
+    float *D2b = d2y + (b * L + t0) * D;
+    const uint32_t Du = (uint32_t)D, du = (uint32_t)d;
+    const float *rec0 = bc + b * Tc * R;
+
+    float xc[TT], vc[TT], wc[TT];
+#pragma unroll
+    for (int j = 0; j < TT; ++j) {
+        const int64_t t = ts + j < te ? ts + j : te - 1;
+        const uint32_t o = (uint32_t)t * Du + du;
+        xc[j] = load_in(Xb, o);
+        vc[j] = load_in(Vb, o);
+        wc[j] = load_in(Wb, o);
+    }
+    for (int64_t tb = ts; tb < te; tb += TT) {
+        float xn[TT], vn[TT], wn[TT];
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
+            const uint32_t o = (uint32_t)t * Du + du;
+            xn[j] = load_in(Xb, o);
+            vn[j] = load_in(Vb, o);
+            wn[j] = load_in(Wb, o);
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + j;
+            if (t < te) {
+                const float xv = xc[j], vv = vc[j], wv = wc[j];
+                float delta, sw, s2;
+                discretize2(xv, w, bd, delta, sw, s2);
+                const float dv = sw * vv, dw = sw * wv;
+                const float dvw = s2 * vv * wv;
+                const float u = delta * xv;
+                const float pv = fmaf(dv, xv, delta * vv);
+                const float pw = fmaf(dw, xv, delta * wv);
+                const float q = fmaf(dvw, xv, fmaf(dv, wv, dw * vv));
+                const float c1 = dv * dw;
+                if constexpr (!OUT) {
+                    sD += delta;
+                    sDv += dv;
+                    sDw += dw;
+                    sDvw += dvw;
+                }
+                const float *rec = rec0 + t * R;
+                float yv = 0.0f, y1 = 0.0f, y2 = 0.0f, y3 = 0.0f;
+#pragma unroll
+                for (int i = 0; i < NT; ++i) {
+                    const float Bn = rec[i], dBv = rec[N + i], dBw = rec[2 * N + i];
+                    const float a = __builtin_amdgcn_exp2f(delta * At[i]);
+                    const float sv = a * h[i];
+                    const float gv = Af[i] * sv;
+                    const float hn = fmaf(Bn, u, sv);
+                    // Abar_w hv + Abar_v hw + Abar_vw h = (A Abar)(dw hv + dv hw + cvw h)
+                    const float cvw = fmaf(Af[i], c1, dvw);
+                    const float cross = fmaf(dw, hv[i], fmaf(dv, hw[i], cvw * h[i]));
+                    const float hvwn = fmaf(a, hvw[i], fmaf(Af[i] * a, cross, fmaf(Bn, q, fmaf(dBv, pw, dBw * pv))));
+                    const float hvn = fmaf(a, hv[i], fmaf(gv, dv, fmaf(Bn, pv, dBv * u)));
+                    const float hwn = fmaf(a, hw[i], fmaf(gv, dw, fmaf(Bn, pw, dBw * u)));
+                    h[i] = hn;
+                    hv[i] = hvn;
+                    hw[i] = hwn;
+                    hvw[i] = hvwn;
+                    if constexpr (OUT) {
+                        const float Cn = rec[3 * N + i], dCv = rec[4 * N + i], dCw = rec[5 * N + i];
+                        yv = fmaf(Cn, hn, yv);
+                        y1 = fmaf(dCv, hn, fmaf(Cn, hvn, y1));
+                        y2 = fmaf(dCw, hn, fmaf(Cn, hwn, y2));
+                        y3 = fmaf(Cn, hvwn, fmaf(dCw, hvn, fmaf(dCv, hwn, y3)));
+                    }
+                }
+                if constexpr (OUT) {
+                    if (active) {
+                        const uint32_t o = (uint32_t)t * Du + du;
+                        store_out(Yb, o, yv);
+                        store_out(DVb, o, y1);
+                        store_out(DWb, o, y2);
+                        store_out(D2b, o, y3);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            xc[j] = xn[j];
+            vc[j] = vn[j];
+            wc[j] = wn[j];
+        }
+    }
+
+    if (!active) return;
+    if constexpr (OUT) {
+        if (end_state) {
+            float *eb = end_state + b * ibs + d;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                eb[i * D] = h[i];
+                eb[ics + i * D] = hv[i];
+                eb[2 * ics + i * D] = hw[i];
+                eb[3 * ics + i * D] = hvw[i];
+            }
+        }
+    } else {
+        const int64_t base = (b * G + g) * 4;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            agg_h[(base * N + i) * D + d] = h[i];
+            agg_h[((base + 1) * N + i) * D + d] = hv[i];
+            agg_h[((base + 2) * N + i) * D + d] = hw[i];
+            agg_h[((base + 3) * N + i) * D + d] = hvw[i];
+        }
+        agg_s[base * D + d] = sD;
+        agg_s[(base + 1) * D + d] = sDv;
+        agg_s[(base + 2) * D + d] = sDw;
+        agg_s[(base + 3) * D + d] = sDvw;
+    }
+}
+
+// Carry of the second-order flow: each segment acts on (h, hv, hw, hvw) as
+//   h' = P h + h0, hv' = P hv + Pv h + hv0, hw' = P hw + Pw h + hw0,
+//   hvw' = P hvw + Pw hv + Pv hw + Pvw h + hvw0,
+// P = 2^(At S), Pv = P (A Sv), Pw = P (A Sw), Pvw = P ((A Sv)(A Sw) + A Svw):
+// the derivatives of the segment's map h_in -> P h_in + h0 along v, w.
+static __global__ __launch_bounds__(kThreads) void k_carry2(
+    const float *__restrict__ A, float *__restrict__ seg, const float *__restrict__ agg_s,
+    float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int G) {
+    constexpr int GB = 16;
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t ND = N * D;
+    if (idx >= Bsz * ND) return;
+    const int64_t d = idx % D, n = (idx / D) % N, b = idx / ND;
+    const float a = A[d * N + n];
+    const float at = a * kLog2e;
+    const int64_t cs = Bsz * ND;
+    const int64_t lane = n * D + d;
+    float h = state[b * ND + lane], hv = state[cs + b * ND + lane];
+    float hw = state[2 * cs + b * ND + lane], hvw = state[3 * cs + b * ND + lane];
+    for (int g0 = 0; g0 < G; g0 += GB) {
+        float e0[GB], e1[GB], e2[GB], e3[GB], s0[GB], s1[GB], s2[GB], s3[GB];
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            const int g = g0 + j < G ? g0 + j : G - 1;
+            const int64_t base = (b * G + g) * 4;
+            e0[j] = seg[base * ND + lane];
+            e1[j] = seg[(base + 1) * ND + lane];
+            e2[j] = seg[(base + 2) * ND + lane];
+            e3[j] = seg[(base + 3) * ND + lane];
+            s0[j] = agg_s[base * D + d];
+            s1[j] = agg_s[(base + 1) * D + d];
+            s2[j] = agg_s[(base + 2) * D + d];
+            s3[j] = agg_s[(base + 3) * D + d];
+        }
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            if (g0 + j >= G) break;
+            const int64_t base = (b * G + g0 + j) * 4;
+            seg[base * ND + lane] = h;
+            seg[(base + 1) * ND + lane] = hv;
+            seg[(base + 2) * ND + lane] = hw;
+            seg[(base + 3) * ND + lane] = hvw;
+            const float P = __builtin_amdgcn_exp2f(at * s0[j]);
+            const float asv = a * s1[j], asw = a * s2[j];
+            const float Pv = P * asv, Pw = P * asw;
+            const float Pvw = P * fmaf(asv, asw, a * s3[j]);
+            const float hvw1 = fmaf(P, hvw, fmaf(Pw, hv, fmaf(Pv, hw, fmaf(Pvw, h, e3[j]))));
+            const float hv1 = fmaf(P, hv, fmaf(Pv, h, e1[j]));
+            const float hw1 = fmaf(P, hw, fmaf(Pw, h, e2[j]));
+            h = fmaf(P, h, e0[j]);
+            hv = hv1;
+            hw = hw1;
+            hvw = hvw1;
+        }
+    }
+    state[b * ND + lane] = h;
+    state[cs + b * ND + lane] = hv;
+    state[2 * cs + b * ND + lane] = hw;
+    state[3 * cs + b * ND + lane] = hvw;
+}
+
+// ---------------------------------------------------------------- k_carry
+// One thread per lane (b, n, d), sequential over the block's segments.
+// state [(1+K)][B][N][D] enters the block and leaves it.  seg [B][G][(1+K)]
+// [N][D] holds each segment's end state from a zero start on entry and is
+// overwritten, segment by segment, with the true state entering it.  Loads
+// for GB segments are issued together so their latencies overlap.
+template <int K>
+__global__ __launch_bounds__(kThreads) void k_carry(
+    const float *__restrict__ A, float *__restrict__ seg, const float *__restrict__ agg_s,
+    float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int G) {
+    constexpr int GB = K == 1 ? 32 : (K == 2 ? 16 : (K == 4 ? 8 : 4));
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t ND = N * D;
+    if (idx >= Bsz * ND) return;
+    const int64_t d = idx % D, n = (idx / D) % N, b = idx / ND;
+    const float a = A[d * N + n];
+    const float at = a * kLog2e;
+    const int64_t cstride = Bsz * ND;  // state: component stride
+    const int64_t lane = n * D + d;
+    float h = state[b * ND + lane];
+    float dh[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) dh[k] = state[(1 + k) * cstride + b * ND + lane];
+    for (int g0 = 0; g0 < G; g0 += GB) {
+        float h0[GB], dh0[GB][K], sD[GB], sdD[GB][K];
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            const int g = g0 + j < G ? g0 + j : G - 1;
+            const int64_t base = (b * G + g) * (1 + K);
+            h0[j] = seg[base * ND + lane];
+            sD[j] = agg_s[base * D + d];
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                dh0[j][k] = seg[(base + 1 + k) * ND + lane];
+                sdD[j][k] = agg_s[(base + 1 + k) * D + d];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            if (g0 + j >= G) break;
+            const int64_t base = (b * G + g0 + j) * (1 + K);
+            seg[base * ND + lane] = h;
+#pragma unroll
+            for (int k = 0; k < K; ++k) seg[(base + 1 + k) * ND + lane] = dh[k];
+            const float P = __builtin_amdgcn_exp2f(at * sD[j]);
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const float q = P * (a * sdD[j][k]);
+                dh[k] = fmaf(P, dh[k], fmaf(q, h, dh0[j][k]));
+            }
+            h = fmaf(P, h, h0[j]);
+        }
+    }
+    state[b * ND + lane] = h;
+#pragma unroll
+    for (int k = 0; k < K; ++k) state[(1 + k) * cstride + b * ND + lane] = dh[k];
+}
+
+// ---------------------------------------------------------------- parameter flows
+// Sensitivity flows of the parameters with online gradient accumulation
+// against an adjoint signal gy = dl/dy (App. E, Alg. 2).  One thread per
+// channel with all NT = N states; per lane the state is (h, GA, GB):
+//   GA' = Abar GA + Delta Abar h     (dh/dA; the Euler drive has no A)
+//   GB' = Abar GB + Delta x          (dh/d offset of B)
+//   h'  = Abar h + Delta B x,        y = sum_n C h'
+// and the rescan (OUT) accumulates, per lane, over its segment
+//   gradA += gy C GA',  gradB += gy C GB',  gradC += gy h'.
+// Records are [B(N) | C(N)].  OUT=false: zero-start segment aggregates
+// (end state in agg_h [B][G][3][N][D], sum of Delta in agg_s [B][G][3][D],
+// component 0).  OUT=true: scan from the entry state in init (as k_scan) and
+// write y; the three gradient sums go to gout at the same place as the
+// entry state (the entry slot is read before it is overwritten, by the same
+// thread), or are added to gout when gadd is set (sequential evaluation:
+// gout is the running sum of the call, and end_state receives the state).
+template <int NT, bool OUT, typename InT>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_pscan(
+    const InT *__restrict__ x, const float *__restrict__ gy, const float *__restrict__ A,
+    const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
+    const float *init, int64_t ibs, int64_t igs, int64_t ics,
+    float *__restrict__ y, float *end_state, float *gout, int gadd,
+    float *__restrict__ agg_h, float *__restrict__ agg_s,
+    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    constexpr int N = NT;
+    constexpr int R = 2 * N;          // B, C
+    constexpr int TT = OUT && NT >= 16 ? 4 : 8;   // prefetch depth, bounded by the VGPR budget
+
+    const int tid = threadIdx.x;
+    const int64_t d_raw = (int64_t)blockIdx.x * kThreads + tid;
+    const bool active = d_raw < D;
+    const int64_t d = active ? d_raw : D - 1;
+    const int g = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int64_t ts = (int64_t)g * S;
+    const int64_t te = ts + S < len ? ts + S : len;
+    if (ts >= te) return;
+
+    float At[NT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i) At[i] = A[d * N + i] * kLog2e;
+    const float w = w_delta[d], bd = b_delta[d];
+
+    float h[NT], ga[NT], gb[NT];
+    float sA[NT], sB[NT], sC[NT];
+    if constexpr (OUT) {
+        const float *ib = init + b * ibs + g * igs + d;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            h[i] = ib[i * D];
+            ga[i] = ib[ics + i * D];
+            gb[i] = ib[2 * ics + i * D];
+            sA[i] = sB[i] = sC[i] = 0.0f;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NT; ++i) h[i] = ga[i] = gb[i] = 0.0f;
+    }
+    float sD = 0.0f;
+
+    const InT *Xb = x + (b * L + t0) * D;
+    const float *Gb = gy + (b * L + t0) * D;
+    float *Yb = y + (b * L + t0) * D;
+    const uint32_t Du = (uint32_t)D, du = (uint32_t)d;
+    const float *rec0 = bc + b * Tc * R;
+
+    float xc[TT], gc[TT];
+#pragma unroll
+    for (int j = 0; j < TT; ++j) {
+        const int64_t t = ts + j < te ? ts + j : te - 1;
+        const uint32_t o = (uint32_t)t * Du + du;
+        xc[j] = load_in(Xb, o);
+        if constexpr (OUT) gc[j] = load_in(Gb, o);
+    }
+    for (int64_t tb = ts; tb < te; tb += TT) {
+        float xn[TT], gn[TT];
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
+            const uint32_t o = (uint32_t)t * Du + du;
+            xn[j] = load_in(Xb, o);
+            if constexpr (OUT) gn[j] = load_in(Gb, o);
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + j;
+            if (t < te) {
+                const float xv = xc[j];
+                float delta, sw;
+                discretize(xv, w, bd, delta, sw);
+                const float u = delta * xv;
+                if constexpr (!OUT) sD += delta;
+                const float *rec = rec0 + t * R;
+                float yv = 0.0f;
+#pragma unroll
+                for (int i = 0; i < NT; ++i) {
+                    const float Bn = rec[i];
+                    const float a = __builtin_amdgcn_exp2f(delta * At[i]);
+                    const float sv = a * h[i];
+                    ga[i] = fmaf(a, ga[i], delta * sv);
+                    gb[i] = fmaf(a, gb[i], u);
+                    h[i] = fmaf(Bn, u, sv);
+                    if constexpr (OUT) {
+                        const float Cn = rec[N + i];
+                        const float gC = gc[j] * Cn;
+                        yv = fmaf(Cn, h[i], yv);
+                        sA[i] = fmaf(gC, ga[i], sA[i]);
+                        sB[i] = fmaf(gC, gb[i], sB[i]);
+                        sC[i] = fmaf(gc[j], h[i], sC[i]);
+                    }
+                }
+                if constexpr (OUT) {
+                    if (active) store_out(Yb, (uint32_t)t * Du + du, yv);
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            xc[j] = xn[j];
+            if constexpr (OUT) gc[j] = gn[j];
+        }
+    }
+
+    if (!active) return;
+    if constexpr (OUT) {
+        if (end_state) {
+            float *eb = end_state + b * ibs + d;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                eb[i * D] = h[i];
+                eb[ics + i * D] = ga[i];
+                eb[2 * ics + i * D] = gb[i];
+            }
+        }
+        float *ob = gout + b * ibs + g * igs + d;
+        if (gadd) {
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                ob[i * D] += sA[i];
+                ob[ics + i * D] += sB[i];
+                ob[2 * ics + i * D] += sC[i];
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                ob[i * D] = sA[i];
+                ob[ics + i * D] = sB[i];
+                ob[2 * ics + i * D] = sC[i];
+            }
+        }
+    } else {
+        const int64_t base = (b * G + g) * 3;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            agg_h[(base * N + i) * D + d] = h[i];
+            agg_h[((base + 1) * N + i) * D + d] = ga[i];
+            agg_h[((base + 2) * N + i) * D + d] = gb[i];
+        }
+        agg_s[base * D + d] = sD;
+    }
+}
+
+// Carry of the parameter flows: a segment maps its entry state to
+//   h' = P h + h0,  GA' = P GA + S P h + GA0,  GB' = P GB + GB0,
+// P = exp(A S), S = the segment's sum of Delta (dP/dA = S P).  Same layout
+// and in-place convention as k_carry.
+static __global__ __launch_bounds__(kThreads) void k_pcarry(
+    const float *__restrict__ A, float *__restrict__ seg, const float *__restrict__ agg_s,
+    float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int G) {
+    constexpr int GB = 16;
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t ND = N * D;
+    if (idx >= Bsz * ND) return;
+    const int64_t d = idx % D, n = (idx / D) % N, b = idx / ND;
+    const float a = A[d * N + n];
+    const float at = a * kLog2e;
+    const int64_t cs = Bsz * ND;
+    const int64_t lane = n * D + d;
+    float h = state[b * ND + lane], ga = state[cs + b * ND + lane], gb = state[2 * cs + b * ND + lane];
+    for (int g0 = 0; g0 < G; g0 += GB) {
+        float e0[GB], e1[GB], e2[GB], s0[GB];
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            const int g = g0 + j < G ? g0 + j : G - 1;
+            const int64_t base = (b * G + g) * 3;
+            e0[j] = seg[base * ND + lane];
+            e1[j] = seg[(base + 1) * ND + lane];
+            e2[j] = seg[(base + 2) * ND + lane];
+            s0[j] = agg_s[base * D + d];
+        }
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            if (g0 + j >= G) break;
+            const int64_t base = (b * G + g0 + j) * 3;
+            seg[base * ND + lane] = h;
+            seg[(base + 1) * ND + lane] = ga;
+            seg[(base + 2) * ND + lane] = gb;
+            const float P = __builtin_amdgcn_exp2f(at * s0[j]);
+            ga = fmaf(P, ga, fmaf(P * s0[j], h, e1[j]));
+            gb = fmaf(P, gb, e2[j]);
+            h = fmaf(P, h, e0[j]);
+        }
+    }
+    state[b * ND + lane] = h;
+    state[cs + b * ND + lane] = ga;
+    state[2 * cs + b * ND + lane] = gb;
+}
+
+// Adds the block's per-segment gradient partials part [B][G][3][N][D] to the
+// running sums acc [3][B][N][D] (the state layout), one segment after the
+// other in order, so the sums do not depend on how the call is split into
+// host blocks.
+static __global__ __launch_bounds__(kThreads) void k_gsum(
+    const float *__restrict__ part, float *__restrict__ acc, int64_t Bsz, int64_t ND, int G) {
+    constexpr int GB = 16;
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= 3 * Bsz * ND) return;
+    const int64_t c = idx / (Bsz * ND), b = (idx / ND) % Bsz, r = idx % ND;
+    float s = acc[idx];
+    for (int g0 = 0; g0 < G; g0 += GB) {
+        float v[GB];
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            const int g = g0 + j < G ? g0 + j : G - 1;
+            v[j] = part[((b * G + g) * 3 + c) * ND + r];
+        }
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            if (g0 + j >= G) break;
+            s += v[j];
+        }
+    }
+    acc[idx] = s;
+}
+
+static __global__ __launch_bounds__(kThreads) void k_fill0(float *__restrict__ p, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < n) p[i] = 0.0f;
+}
+
+// grad_c[d][n] += sum over b (in order) of acc[c][b][n][d], c = A, B, C.
+static __global__ __launch_bounds__(kThreads) void k_gout(
+    const float *__restrict__ acc, float *__restrict__ gA, float *__restrict__ gB, float *__restrict__ gC,
+    int64_t Bsz, int64_t D, int64_t N) {
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t ND = N * D;
+    if (idx >= 3 * ND) return;
+    const int64_t c = idx / ND, r = idx % ND;
+    const int64_t d = r % D, n = r / D;
+    float s = 0.0f;
+    for (int64_t b = 0; b < Bsz; ++b) s += acc[(c * Bsz + b) * ND + r];
+    float *out = c == 0 ? gA : (c == 1 ? gB : gC);
+    out[d * N + n] += s;
+}
+
+// ---------------------------------------------------------------- complex
+// Complex diagonal transition A = A_re + i A_im (Sec. 3: state in C^{DxN},
+// read-out y = sum_n C Re(h)), Euler drive, one thread per channel with all
+// NT = N lanes.  Per lane and step, with Abar = exp(Delta A_re) (cos th +
+// i sin th), th = Delta A_im:
+//   s = Abar h,  h' = s + B u,  g = A s,
+//   dh'_k = Abar dh_k + g dDelta_k + (B p_k + dB_k u)     (drive real)
+//   y = sum_n C Re(h'),  dy_k = sum_n dC_k Re(h') + C Re(dh'_k)
+// The angle is reduced in revolutions (th/2pi minus its nearest integer)
+// before the hardware sine and cosine.  Layouts as k_scan with the state
+// split into planes: component c = 2m + part (m = 0 h, 1..K dh_k).
+constexpr float kInv2Pi = 0.159154943091895336f;
+
+__device__ __forceinline__ void rot(float rev, float &c, float &s) {
+    const float r = rev - __builtin_rintf(rev);
+    s = __builtin_amdgcn_sinf(r);
+    c = __builtin_amdgcn_cosf(r);
+}
+
+template <int NT, int K, bool OUT, typename InT>
+__global__ __launch_bounds__(kThreads) void k_cscan(
+    const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A, const float *__restrict__ Aim,
+    const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
+    const float *init, int64_t ibs, int64_t igs, int64_t ics, float *__restrict__ y, float *__restrict__ dy,
+    float *end_state, float *__restrict__ agg_h, float *__restrict__ agg_s, int64_t Bsz, int64_t L, int64_t D,
+    int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    constexpr int N = NT;
+    constexpr int R = 2 * N * (1 + K);
+    constexpr int TT = 8;
+    constexpr int CP = 2 * (1 + K);   // state planes
+
+    const int tid = threadIdx.x;
+    const int64_t d_raw = (int64_t)blockIdx.x * kThreads + tid;
+    const bool active = d_raw < D;
+    const int64_t d = active ? d_raw : D - 1;
+    const int g = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int64_t ts = (int64_t)g * S;
+    const int64_t te = ts + S < len ? ts + S : len;
+    if (ts >= te) return;
+
+    float Ar[NT], Ai[NT], At[NT], Ar2[NT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+        Ar[i] = A[d * N + i];
+        Ai[i] = Aim[d * N + i];
+        At[i] = Ar[i] * kLog2e;
+        Ar2[i] = Ai[i] * kInv2Pi;
+    }
+    const float w = w_delta[d], bd = b_delta[d];
+
+    float hr[NT], hi[NT], dr[K][NT], di[K][NT];
+    if constexpr (OUT) {
+        const float *ib = init + b * ibs + g * igs + d;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            hr[i] = ib[i * D];
+            hi[i] = ib[ics + i * D];
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                dr[k][i] = ib[(2 + 2 * k) * ics + i * D];
+                di[k][i] = ib[(3 + 2 * k) * ics + i * D];
+            }
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            hr[i] = hi[i] = 0.0f;
+#pragma unroll
+            for (int k = 0; k < K; ++k) dr[k][i] = di[k][i] = 0.0f;
+        }
+    }
+    float sD = 0.0f, sdD[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) sdD[k] = 0.0f;
+
+    const int64_t dxs = Bsz * L * D;
+    const InT *Xb = x + (b * L + t0) * D;
+    const InT *DXb = dx + (b * L + t0) * D;
+    float *Yb = y + (b * L + t0) * D;
+    float *DYb = dy + (b * L + t0) * D;
+    const uint32_t Du = (uint32_t)D, du = (uint32_t)d;
+    const float *rec0 = bc + b * Tc * R;
+
+    float xc[TT], dxc[K][TT];
+#pragma unroll
+    for (int j = 0; j < TT; ++j) {
+        const int64_t t = ts + j < te ? ts + j : te - 1;
+        xc[j] = load_in(Xb, (uint32_t)t * Du + du);
+#pragma unroll
+        for (int k = 0; k < K; ++k) dxc[k][j] = load_in(DXb + k * dxs, (uint32_t)t * Du + du);
+    }
+    for (int64_t tb = ts; tb < te; tb += TT) {
+        float xn[TT], dxn[K][TT];
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
+            xn[j] = load_in(Xb, (uint32_t)t * Du + du);
+#pragma unroll
+            for (int k = 0; k < K; ++k) dxn[k][j] = load_in(DXb + k * dxs, (uint32_t)t * Du + du);
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            const int64_t t = tb + j;
+            if (t < te) {
+                const float xv = xc[j];
+                float delta, sw;
+                discretize(xv, w, bd, delta, sw);
+                const float u = delta * xv;
+                float dD[K], pk[K];
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    dD[k] = sw * dxc[k][j];
+                    pk[k] = fmaf(dD[k], xv, delta * dxc[k][j]);
+                }
+                if constexpr (!OUT) {
+                    sD += delta;
+#pragma unroll
+                    for (int k = 0; k < K; ++k) sdD[k] += dD[k];
+                }
+                const float *rec = rec0 + t * R;
+                float yv = 0.0f, dyv[K];
+#pragma unroll
+                for (int k = 0; k < K; ++k) dyv[k] = 0.0f;
+#pragma unroll
+                for (int i = 0; i < NT; ++i) {
+                    const float Bn = rec[i];
+                    const float e = __builtin_amdgcn_exp2f(delta * At[i]);
+                    float cs, sn;
+                    rot(delta * Ar2[i], cs, sn);
+                    const float ar = e * cs, ai = e * sn;
+                    const float sr = fmaf(ar, hr[i], -ai * hi[i]);
+                    const float si = fmaf(ar, hi[i], ai * hr[i]);
+                    const float gr = fmaf(Ar[i], sr, -Ai[i] * si);
+                    const float gi = fmaf(Ar[i], si, Ai[i] * sr);
+                    const float hrn = fmaf(Bn, u, sr);
+#pragma unroll
+                    for (int k = 0; k < K; ++k) {
+                        const float dBn = rec[(1 + k) * N + i];
+                        const float tr = fmaf(ar, dr[k][i], -ai * di[k][i]);
+                        const float ti = fmaf(ar, di[k][i], ai * dr[k][i]);
+                        dr[k][i] = fmaf(gr, dD[k], tr) + fmaf(Bn, pk[k], dBn * u);
+                        di[k][i] = fmaf(gi, dD[k], ti);
+                    }
+                    hr[i] = hrn;
+                    hi[i] = si;
+                    if constexpr (OUT) {
+                        const float Cn = rec[(1 + K) * N + i];
+                        yv = fmaf(Cn, hrn, yv);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) {
+                            const float dCn = rec[(2 + K + k) * N + i];
+                            dyv[k] = fmaf(dCn, hrn, fmaf(Cn, dr[k][i], dyv[k]));
+                        }
+                    }
+                }
+                if constexpr (OUT) {
+                    if (active) {
+                        store_out(Yb, (uint32_t)t * Du + du, yv);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) store_out(DYb + k * dxs, (uint32_t)t * Du + du, dyv[k]);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < TT; ++j) {
+            xc[j] = xn[j];
+#pragma unroll
+            for (int k = 0; k < K; ++k) dxc[k][j] = dxn[k][j];
+        }
+    }
+
+    if (!active) return;
+    if constexpr (OUT) {
+        if (end_state) {
+            float *eb = end_state + b * ibs + d;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                eb[i * D] = hr[i];
+                eb[ics + i * D] = hi[i];
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    eb[(2 + 2 * k) * ics + i * D] = dr[k][i];
+                    eb[(3 + 2 * k) * ics + i * D] = di[k][i];
+                }
+            }
+        }
+    } else {
+        const int64_t base = (b * G + g) * CP;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            agg_h[(base * N + i) * D + d] = hr[i];
+            agg_h[((base + 1) * N + i) * D + d] = hi[i];
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                agg_h[((base + 2 + 2 * k) * N + i) * D + d] = dr[k][i];
+                agg_h[((base + 3 + 2 * k) * N + i) * D + d] = di[k][i];
+            }
+        }
+        const int64_t sbase = (b * G + g) * (1 + K);
+        agg_s[sbase * D + d] = sD;
+#pragma unroll
+        for (int k = 0; k < K; ++k) agg_s[(sbase + 1 + k) * D + d] = sdD[k];
+    }
+}
+
+// Carry of the complex scan: a segment maps (h, dh_k) to (P h + h0,
+// P dh_k + Q_k h + dh0_k) with P = exp(A S) (complex), Q_k = P A S_k, S and
+// S_k the segment sums of Delta and dDelta_k.  Layout as k_carry with the
+// state split into planes (seg [B][G][2(1+K)][N][D], agg_s [B][G][1+K][D]).
+template <int K>
+__global__ __launch_bounds__(kThreads) void k_ccarry(
+    const float *__restrict__ A, const float *__restrict__ Aim, float *__restrict__ seg,
+    const float *__restrict__ agg_s, float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int G) {
+    constexpr int GB = 8;
+    constexpr int CP = 2 * (1 + K);
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t ND = N * D;
+    if (idx >= Bsz * ND) return;
+    const int64_t d = idx % D, n = (idx / D) % N, b = idx / ND;
+    const float ar = A[d * N + n], aim = Aim[d * N + n];
+    const float at = ar * kLog2e, arev = aim * kInv2Pi;
+    const int64_t cs = Bsz * ND;
+    const int64_t lane = b * ND + n * D + d;
+    const int64_t sl = n * D + d;
+    float st[CP];
+#pragma unroll
+    for (int c = 0; c < CP; ++c) st[c] = state[c * cs + lane];
+    for (int g0 = 0; g0 < G; g0 += GB) {
+        float e[GB][CP], sm[GB][1 + K];
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            const int g = g0 + j < G ? g0 + j : G - 1;
+#pragma unroll
+            for (int c = 0; c < CP; ++c) e[j][c] = seg[(((b * G + g) * CP) + c) * ND + sl];
+#pragma unroll
+            for (int c = 0; c <= K; ++c) sm[j][c] = agg_s[((b * G + g) * (1 + K) + c) * D + d];
+        }
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+            if (g0 + j >= G) break;
+#pragma unroll
+            for (int c = 0; c < CP; ++c) seg[(((b * G + g0 + j) * CP) + c) * ND + sl] = st[c];
+            const float mag = __builtin_amdgcn_exp2f(at * sm[j][0]);
+            float cs_, sn_;
+            rot(arev * sm[j][0], cs_, sn_);
+            const float pr = mag * cs_, pi = mag * sn_;
+            const float hr = st[0], hi = st[1];
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                // Q_k = P A S_k
+                const float qr = (pr * ar - pi * aim) * sm[j][1 + k], qi = (pr * aim + pi * ar) * sm[j][1 + k];
+                const float dr = st[2 + 2 * k], di = st[3 + 2 * k];
+                st[2 + 2 * k] = fmaf(pr, dr, -pi * di) + fmaf(qr, hr, -qi * hi) + e[j][2 + 2 * k];
+                st[3 + 2 * k] = fmaf(pr, di, pi * dr) + fmaf(qr, hi, qi * hr) + e[j][3 + 2 * k];
+            }
+            st[0] = fmaf(pr, hr, -pi * hi) + e[j][0];
+            st[1] = fmaf(pr, hi, pi * hr) + e[j][1];
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < CP; ++c) state[c * cs + lane] = st[c];
+}
+
+// ---------------------------------------------------------------- state in/out
+// state [comp][B][N][D] <-> h [B][D][N], dh [K][B][D][N].
+// Real state: component c = 0 -> h, 1..K -> dh_{c-1}, 1+K -> d2h (second
+// order only).  Complex state (cplx = 1): component c = 2m + part with
+// m = 0 -> h, 1..K -> dh_{m-1} and part 0/1 the real/imaginary plane; the
+// caller's arrays are complex (interleaved real, imaginary floats).
+__device__ __forceinline__ int64_t state_src(int64_t c, int64_t b, int64_t d, int64_t n, int64_t Bsz, int64_t D,
+                                             int64_t N, int K, int cplx, int &which) {
+    const int64_t m = cplx ? c / 2 : c, part = cplx ? c % 2 : 0;
+    const int64_t s = cplx ? 2 : 1;
+    if (m == 0) { which = 0; return ((b * D + d) * N + n) * s + part; }
+    if (m <= K) { which = 1; return ((((m - 1) * Bsz + b) * D + d) * N + n) * s + part; }
+    which = 2;
+    return (b * D + d) * N + n;
+}
+
+static __global__ __launch_bounds__(kThreads) void k_state_import(
+    const float *__restrict__ h_in, const float *__restrict__ dh_in, const float *__restrict__ d2h_in,
+    float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int K, int comp, int cplx) {
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t per = Bsz * N * D;
+    if (idx >= per * comp) return;
+    const int64_t c = idx / per, r = idx % per;
+    const int64_t d = r % D, n = (r / D) % N, b = r / (N * D);
+    int which;
+    const int64_t e = state_src(c, b, d, n, Bsz, D, N, K, cplx, which);
+    const float *src = which == 0 ? h_in : (which == 1 ? dh_in : d2h_in);
+    state[idx] = src ? src[e] : 0.0f;
+}
+
+static __global__ __launch_bounds__(kThreads) void k_state_export(
+    const float *__restrict__ state, float *__restrict__ h_out, float *__restrict__ dh_out,
+    float *__restrict__ d2h_out, int64_t Bsz, int64_t D, int64_t N, int K, int comp, int cplx) {
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t per = Bsz * N * D;
+    if (idx >= per * comp) return;
+    const int64_t c = idx / per, r = idx % per;
+    const int64_t d = r % D, n = (r / D) % N, b = r / (N * D);
+    int which;
+    const int64_t e = state_src(c, b, d, n, Bsz, D, N, K, cplx, which);
+    float *dst = which == 0 ? h_out : (which == 1 ? dh_out : d2h_out);
+    if (dst) dst[e] = state[idx];
+}
+
+// ---------------------------------------------------------------- dispatch
+template <typename InT>
+struct Launcher {
+    const Plan &q;
+    const pgf_params &p;
+    const InT *x;
+    const InT *dx;
+    float *y, *dy;
+    float *d2y;        // second order only
+    hipStream_t st;
+    char *ws;
+    const float *gy = nullptr;                          // parameter flows only
+    float *gA = nullptr, *gB = nullptr, *gC = nullptr;  // parameter flows only
+
+    float *state() const { return (float *)(ws + q.ws.state); }
+    float *bcw() const { return (float *)(ws + q.ws.bc); }
+    float *agg_h() const { return (float *)(ws + q.ws.agg_h); }
+    float *agg_s() const { return (float *)(ws + q.ws.agg_s); }
+    float *seg_in() const { return (float *)(ws + q.ws.agg_h); }  // overwritten in place by k_carry
+    float *gacc() const { return (float *)(ws + q.ws.gacc); }
+    float *lrw() const { return (float *)(ws + q.ws.lr); }
+    float *dtw() const { return (float *)(ws + q.ws.dt); }
+
+    template <int NC>
+    void proj_nc(int64_t t0, int64_t len) {
+        dim3 grid((unsigned)((len + kProjTM - 1) / kProjTM), (unsigned)(1 + q.KP), (unsigned)q.B);
+        Timed tm(0, st);
+        if (q.groups > 1)
+            hipLaunchKernelGGL((k_proj<NC, InT, true>), grid, dim3(kThreads), 0, st, x, dx, p.W_B, p.W_C, p.b_B,
+                               p.b_C, bcw(), q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len, (int)q.N);
+        else
+            hipLaunchKernelGGL((k_proj<NC, InT, false>), grid, dim3(kThreads), 0, st, x, dx, p.W_B, p.W_C, p.b_B,
+                               p.b_C, bcw(), q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len, (int)q.N);
+    }
+
+    // One pass over x (and each dx_k) computes the B and C columns of every
+    // channel group: 2 * groups * N columns (a power of two, checked by the
+    // planner).
+    bool proj(int64_t t0, int64_t len) {
+        switch (2 * q.groups * q.N) {
+            case 8: proj_nc<8>(t0, len); return true;
+            case 16: proj_nc<16>(t0, len); return true;
+            case 32: proj_nc<32>(t0, len); return true;
+            case 64: proj_nc<64>(t0, len); return true;
+            case 128: proj_nc<128>(t0, len); return true;
+            default: return false;
+        }
+    }
+
+    // Low-rank step size of one host block: lr = X_s W_dx for every
+    // direction, then Delta and dDelta_k.
+    template <int RC>
+    bool lowrank_rc(int64_t t0, int64_t len) {
+        {
+            Timed tm(0, st);
+            hipLaunchKernelGGL((k_lowx<RC, InT>),
+                               dim3((unsigned)((len + kProjTM - 1) / kProjTM), (unsigned)(1 + q.K), (unsigned)q.B),
+                               dim3(kThreads), 0, st, x, dx, p.W_dx, lrw(), q.B, q.L, q.D, q.rank, t0, len,
+                               q.chunk_len);
+        }
+        const int64_t ncol = (q.D + kLowCols - 1) / kLowCols;
+        const dim3 grid((unsigned)(ncol * ((len + kLowRows - 1) / kLowRows)), (unsigned)q.B);
+        Timed tm(0, st);
+        if (q.K == 1)
+            hipLaunchKernelGGL((k_lowdt<RC, 1>), grid, dim3(kThreads), 0, st, (const float *)lrw(), p.W_dt,
+                               p.b_delta, dtw(), q.B, q.D, q.rank, len, q.chunk_len);
+        else if (q.K == 2)
+            hipLaunchKernelGGL((k_lowdt<RC, 2>), grid, dim3(kThreads), 0, st, (const float *)lrw(), p.W_dt,
+                               p.b_delta, dtw(), q.B, q.D, q.rank, len, q.chunk_len);
+        else
+            return false;
+        return true;
+    }
+
+    bool lowrank(int64_t t0, int64_t len) {
+        switch (q.rc) {
+            case 16: return lowrank_rc<16>(t0, len);
+            case 32: return lowrank_rc<32>(t0, len);
+            case 48: return lowrank_rc<48>(t0, len);
+            case 64: return lowrank_rc<64>(t0, len);
+            case 96: return lowrank_rc<96>(t0, len);
+            case 128: return lowrank_rc<128>(t0, len);
+            default: return false;
+        }
+    }
+
+    template <int NT, int NS, int K, int VAR = 0>
+    void scans(int64_t t0, int64_t len) {
+        const unsigned gx = (unsigned)((q.D * NS + kThreads - 1) / kThreads);
+        const int64_t ND = q.N * q.D;
+        const Variant vr{p.D_res, p.activation, q.groups, q.D / q.groups, dtw(), q.B * q.chunk_len * q.D};
+        if (q.seg == 0) {
+            // Sequential evaluation: one segment per block, state in place.
+            Timed tm(3, st);
+            hipLaunchKernelGGL((scan_kernel<NT, NS, K, true, InT, VAR>()), dim3(gx, 1, (unsigned)q.B), dim3(kThreads),
+                               0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(), state(), ND, (int64_t)0, q.B * ND, y,
+                               dy, state(), (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len,
+                               len, 1, vr);
+            return;
+        }
+        const int G = (int)((len + q.seg - 1) / q.seg);
+        {
+            Timed tm(1, st);
+            hipLaunchKernelGGL((scan_kernel<NT, NS, K, false, InT, VAR>()), dim3(gx, (unsigned)G, (unsigned)q.B),
+                               dim3(kThreads), 0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(),
+                               (const float *)nullptr, (int64_t)0, (int64_t)0, (int64_t)0, y, dy, (float *)nullptr,
+                               agg_h(), agg_s(), q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G, vr);
+        }
+        {
+            const int64_t lanes = q.B * ND;
+            Timed tm(2, st);
+            hipLaunchKernelGGL((k_carry<K>), dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                               st, p.A, agg_h(), agg_s(), state(), q.B, q.D, q.N, G);
+        }
+        {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((scan_kernel<NT, NS, K, true, InT, VAR>()), dim3(gx, (unsigned)G, (unsigned)q.B),
+                               dim3(kThreads), 0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(), seg_in(),
+                               (int64_t)G * (1 + K) * ND, (int64_t)(1 + K) * ND, ND, y, dy, (float *)nullptr,
+                               (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg,
+                               G, vr);
+        }
+    }
+
+    // Tilings the planner can choose: nt = min(N, 16) for K <= 2,
+    // nt = min(N, 8) for K = 4 and nt = min(N, 4) for K = 8; ns = N / nt.
+    // Model variants: one thread per channel, N <= 16, K <= 2.
+    template <int K, int VAR>
+    bool variant_block(int64_t t0, int64_t len) {
+        if (q.ns != 1) return false;
+        switch (q.nt) {
+            case 4: scans<4, 1, K, VAR>(t0, len); return true;
+            case 8: scans<8, 1, K, VAR>(t0, len); return true;
+            case 16: scans<16, 1, K, VAR>(t0, len); return true;
+            default: return false;
+        }
+    }
+
+    template <int K>
+    bool scan_block_k(int64_t t0, int64_t len) {
+        if constexpr (K <= 2) {
+            switch (q.var) {
+                case 0: break;
+                case kZoh: return variant_block<K, kZoh>(t0, len);
+                case kOutMap: return variant_block<K, kOutMap>(t0, len);
+                case kZoh | kOutMap: return variant_block<K, kZoh | kOutMap>(t0, len);
+                case kGroups: return variant_block<K, kGroups>(t0, len);
+                case kGroups | kOutMap: return variant_block<K, kGroups | kOutMap>(t0, len);
+                case kLowRank: return variant_block<K, kLowRank>(t0, len);
+                case kLowRank | kOutMap: return variant_block<K, kLowRank | kOutMap>(t0, len);
+                default: return false;
+            }
+        } else if (q.var != 0) {
+            return false;
+        }
+        const int code = q.nt * 100 + q.ns;
+        if constexpr (K <= 2) {
+            switch (code) {
+                case 401: scans<4, 1, K>(t0, len); return true;
+                case 801: scans<8, 1, K>(t0, len); return true;
+                case 1601: scans<16, 1, K>(t0, len); return true;
+                case 1602: scans<16, 2, K>(t0, len); return true;
+                case 1604: scans<16, 4, K>(t0, len); return true;
+                default: return false;
+            }
+        } else if constexpr (K == 4) {
+            switch (code) {
+                case 401: scans<4, 1, K>(t0, len); return true;
+                case 801: scans<8, 1, K>(t0, len); return true;
+                case 802: scans<8, 2, K>(t0, len); return true;
+                case 804: scans<8, 4, K>(t0, len); return true;
+                case 808: scans<8, 8, K>(t0, len); return true;
+                default: return false;
+            }
+        } else {
+            switch (code) {
+                case 401: scans<4, 1, K>(t0, len); return true;
+                case 402: scans<4, 2, K>(t0, len); return true;
+                case 404: scans<4, 4, K>(t0, len); return true;
+                case 408: scans<4, 8, K>(t0, len); return true;
+                case 416: scans<4, 16, K>(t0, len); return true;
+                default: return false;
+            }
+        }
+    }
+
+    // Second order: one thread per channel with all N <= 16 states.
+    template <int NT>
+    void scans2(int64_t t0, int64_t len) {
+        const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
+        const int64_t ND = q.N * q.D;
+        if (q.seg == 0) {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_scan2<NT, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, dx, p.A,
+                               p.w_delta, p.b_delta, bcw(), state(), ND, (int64_t)0, q.B * ND, y, dy, d2y, state(),
+                               (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, len, 1);
+            return;
+        }
+        const int G = (int)((len + q.seg - 1) / q.seg);
+        {
+            Timed tm(1, st);
+            hipLaunchKernelGGL((k_scan2<NT, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
+                               x, dx, p.A, p.w_delta, p.b_delta, bcw(), (const float *)nullptr, (int64_t)0, (int64_t)0,
+                               (int64_t)0, y, dy, d2y, (float *)nullptr, agg_h(), agg_s(), q.B, q.L, q.D, t0, len,
+                               q.chunk_len, (int64_t)q.seg, G);
+        }
+        {
+            const int64_t lanes = q.B * ND;
+            Timed tm(2, st);
+            hipLaunchKernelGGL(k_carry2, dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
+                               p.A, agg_h(), agg_s(), state(), q.B, q.D, q.N, G);
+        }
+        {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_scan2<NT, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
+                               x, dx, p.A, p.w_delta, p.b_delta, bcw(), seg_in(), (int64_t)G * 4 * ND, (int64_t)4 * ND,
+                               ND, y, dy, d2y, (float *)nullptr, (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0,
+                               len, q.chunk_len, (int64_t)q.seg, G);
+        }
+    }
+
+    // Complex transition: one thread per channel with all N <= 16 lanes.
+    template <int NT, int K>
+    void cscans(int64_t t0, int64_t len) {
+        const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
+        const int64_t ND = q.N * q.D;
+        constexpr int CP = 2 * (1 + K);
+        if (q.seg == 0) {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_cscan<NT, K, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, dx,
+                               p.A, p.A_im, p.w_delta, p.b_delta, bcw(), (const float *)state(), ND, (int64_t)0,
+                               q.B * ND, y, dy, state(), (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len,
+                               q.chunk_len, len, 1);
+            return;
+        }
+        const int G = (int)((len + q.seg - 1) / q.seg);
+        {
+            Timed tm(1, st);
+            hipLaunchKernelGGL((k_cscan<NT, K, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0,
+                               st, x, dx, p.A, p.A_im, p.w_delta, p.b_delta, bcw(), (const float *)nullptr,
+                               (int64_t)0, (int64_t)0, (int64_t)0, y, dy, (float *)nullptr, agg_h(), agg_s(), q.B,
+                               q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+        }
+        {
+            const int64_t lanes = q.B * ND;
+            Timed tm(2, st);
+            hipLaunchKernelGGL((k_ccarry<K>), dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                               st, p.A, p.A_im, agg_h(), (const float *)agg_s(), state(), q.B, q.D, q.N, G);
+        }
+        {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_cscan<NT, K, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0,
+                               st, x, dx, p.A, p.A_im, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(),
+                               (int64_t)G * CP * ND, (int64_t)CP * ND, ND, y, dy, (float *)nullptr, (float *)nullptr,
+                               (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+        }
+    }
+
+    template <int K>
+    bool cscan_block(int64_t t0, int64_t len) {
+        switch (q.nt) {
+            case 4: cscans<4, K>(t0, len); return true;
+            case 8: cscans<8, K>(t0, len); return true;
+            case 16: cscans<16, K>(t0, len); return true;
+            default: return false;
+        }
+    }
+
+    // Parameter flows: one thread per channel with all N <= 16 states.
+    template <int NT>
+    void pscans(int64_t t0, int64_t len) {
+        const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
+        const int64_t ND = q.N * q.D;
+        if (q.seg == 0) {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_pscan<NT, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, gy, p.A,
+                               p.w_delta, p.b_delta, bcw(), (const float *)state(), ND, (int64_t)0, q.B * ND, y,
+                               state(), gacc(), 1, (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len,
+                               q.chunk_len, len, 1);
+            return;
+        }
+        const int G = (int)((len + q.seg - 1) / q.seg);
+        {
+            Timed tm(1, st);
+            hipLaunchKernelGGL((k_pscan<NT, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
+                               x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)nullptr, (int64_t)0,
+                               (int64_t)0, (int64_t)0, y, (float *)nullptr, (float *)nullptr, 0, agg_h(), agg_s(),
+                               q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+        }
+        const int64_t lanes = q.B * ND;
+        {
+            Timed tm(2, st);
+            hipLaunchKernelGGL(k_pcarry, dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
+                               p.A, agg_h(), agg_s(), state(), q.B, q.D, q.N, G);
+        }
+        {
+            Timed tm(3, st);
+            hipLaunchKernelGGL((k_pscan<NT, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
+                               x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(), (int64_t)G * 3 * ND,
+                               (int64_t)3 * ND, ND, y, (float *)nullptr, seg_in(), 0, (float *)nullptr,
+                               (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+        }
+        {
+            Timed tm(2, st);
+            hipLaunchKernelGGL(k_gsum, dim3((unsigned)((3 * lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
+                               (const float *)seg_in(), gacc(), q.B, ND, G);
+        }
+    }
+
+    bool scan_block(int64_t t0, int64_t len) {
+        if (q.cplx) {
+            if (q.ns != 1) return false;
+            return q.K == 1 ? cscan_block<1>(t0, len) : (q.K == 2 ? cscan_block<2>(t0, len) : false);
+        }
+        if (q.order == 3) {
+            if (q.ns != 1) return false;
+            switch (q.nt) {
+                case 4: pscans<4>(t0, len); return true;
+                case 8: pscans<8>(t0, len); return true;
+                case 16: pscans<16>(t0, len); return true;
+                default: return false;
+            }
+        }
+        if (q.order == 2) {
+            if (q.ns != 1) return false;
+            switch (q.nt) {
+                case 4: scans2<4>(t0, len); return true;
+                case 8: scans2<8>(t0, len); return true;
+                case 16: scans2<16>(t0, len); return true;
+                default: return false;
+            }
+        }
+        switch (q.K) {
+            case 1: return scan_block_k<1>(t0, len);
+            case 2: return scan_block_k<2>(t0, len);
+            case 4: return scan_block_k<4>(t0, len);
+            case 8: return scan_block_k<8>(t0, len);
+            default: return false;
+        }
+    }
+
+    int run() {
+        const int64_t lanes_all = (int64_t)q.comp * q.B * q.N * q.D;
+        const unsigned gs = (unsigned)((lanes_all + kThreads - 1) / kThreads);
+        const float *d2h_in = q.order == 2 ? p.d2h_in : nullptr;
+        float *d2h_out = q.order == 2 ? p.d2h_out : nullptr;
+        const int64_t nacc = 3 * q.B * q.N * q.D;
+        {
+            Timed tm(4, st);
+            hipLaunchKernelGGL(k_state_import, dim3(gs), dim3(kThreads), 0, st, p.h_in, p.dh_in, d2h_in, state(), q.B,
+                               q.D, q.N, (int)q.K, q.comp, q.cplx);
+            if (q.order == 3)
+                hipLaunchKernelGGL(k_fill0, dim3((unsigned)((nacc + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                                   st, gacc(), nacc);
+        }
+        for (int64_t t0 = 0; t0 < q.L; t0 += q.chunk_len) {
+            const int64_t len = q.L - t0 < q.chunk_len ? q.L - t0 : q.chunk_len;
+            if (!proj(t0, len) || (q.rank && !lowrank(t0, len)) || !scan_block(t0, len))
+                return PGF_ERR_UNSUPPORTED;
+        }
+        if (q.order == 3) {
+            Timed tm(4, st);
+            const int64_t nd3 = 3 * q.N * q.D;
+            hipLaunchKernelGGL(k_gout, dim3((unsigned)((nd3 + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
+                               (const float *)gacc(), gA, gB, gC, q.B, q.D, q.N);
+        }
+        if (p.h_out || p.dh_out || d2h_out) {
+            Timed tm(4, st);
+            hipLaunchKernelGGL(k_state_export, dim3(gs), dim3(kThreads), 0, st, state(), p.h_out, p.dh_out, d2h_out,
+                               q.B, q.D, q.N, (int)q.K, q.comp, q.cplx);
+        }
+        return hipGetLastError() == hipSuccess ? PGF_OK : PGF_ERR_HIP;
+    }
+};
+
+// Runs one planned call, every host block, for inputs of type InT.
+template <typename InT>
+int launch(const Plan &q, const pgf_params &p, const InT *x, const InT *dx, float *y, float *dy, float *d2y,
+           hipStream_t st, const float *gy, float *gA, float *gB, float *gC) {
+    Launcher<InT> l{q, p, x, dx, y, dy, d2y, st, (char *)p.workspace, gy, gA, gB, gC};
+    return l.run();
+}
+
+}  // namespace pgf

@@ -6,7 +6,7 @@ import torch
 from oracle import oracle
 from paper_2512_23068_amd import binding, inputs
 
-PARAM_KEYS = ("A", "w_delta", "b_delta", "W_B", "W_C", "b_B", "b_C", "D_res", "A_im")
+PARAM_KEYS = ("A", "w_delta", "b_delta", "W_B", "W_C", "b_B", "b_C", "D_res", "A_im", "W_dx", "W_dt")
 INT_KEYS = ("n_groups",)
 TOL = 1e-5   # relative L2, f32 state against the fp64 oracle
 

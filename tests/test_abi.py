@@ -98,6 +98,12 @@ def _valid_params(L=100, D=16, N=16, K=1):
     return p
 
 
+def _copy_params(p):
+    q = binding.PgfParams()
+    ctypes.memmove(ctypes.byref(q), ctypes.byref(p), ctypes.sizeof(p))
+    return q
+
+
 def test_scan_rejects_bad_arguments_before_launch():
     ok = _valid_params()
     # the fake pointers above are all disjoint: only the listed defects fail
@@ -212,3 +218,42 @@ def test_group_plans():
     q = binding.make_params(1, 1000, 256, 16, 2, order=2)
     q.n_groups = 2
     assert lib.pgf_workspace_bytes(ctypes.byref(q)) == 0
+
+
+def test_low_rank_plans_and_bad_fields():
+    lib = binding.lib()
+    base = binding.make_params(1, 1000, 256, 16, 1)
+    for R in (1, 16, 48, 128):
+        q = binding.make_params(1, 1000, 256, 16, 1)
+        q.dt_rank = R
+        # the workspace grows by z and dz_k of one host block
+        assert lib.pgf_workspace_bytes(ctypes.byref(q)) > lib.pgf_workspace_bytes(ctypes.byref(base)), R
+    info = binding.plan(1, 131072, 1536, 16, 1, dt_rank=48)
+    assert info["workspace_bytes"] <= 2 << 30 and info["n_per_thread"] == 16 and info["n_split"] == 1
+    assert info["workspace_bytes"] == binding.plan(1, 1 << 22, 1536, 16, 1, dt_rank=48)["workspace_bytes"]
+    for kw in (dict(dt_rank=-1), dict(dt_rank=129)):
+        q = binding.make_params(1, 1000, 256, 16, 1)
+        for k, v in kw.items():
+            setattr(q, k, v)
+        assert lib.pgf_workspace_bytes(ctypes.byref(q)) == 0, kw
+    # first order, Euler drive, one group, real A, N <= 16, K <= 2
+    for args, extra in (((1, 1000, 256, 16, 2), dict(order=2)), ((1, 1000, 256, 16, 1), dict(drive="zoh")),
+                        ((1, 1000, 256, 32, 1), {}), ((1, 1000, 256, 16, 4), {})):
+        q = binding.make_params(*args, **extra)
+        q.dt_rank = 16
+        assert lib.pgf_workspace_bytes(ctypes.byref(q)) == 0, (args, extra)
+    for field, val in (("n_groups", 2), ("A_im", 1 << 30)):
+        q = binding.make_params(1, 1000, 256, 16, 1)
+        q.dt_rank = 16
+        setattr(q, field, val)
+        assert lib.pgf_workspace_bytes(ctypes.byref(q)) == 0, field
+    # w_delta may be NULL with the low rank; W_dx and W_dt may not
+    p = _valid_params()
+    p.dt_rank = 8
+    p.W_dx, p.W_dt = (1 << 30) + 8 * 4096, (1 << 30) + 9 * 4096
+    p.w_delta = None
+    p.workspace_bytes = lib.pgf_workspace_bytes(ctypes.byref(p))
+    for field in ("W_dx", "W_dt", "b_delta"):
+        q = _copy_params(p)
+        setattr(q, field, None)
+        assert _call(q) == -1, field
