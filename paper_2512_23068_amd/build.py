@@ -9,7 +9,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(_HERE)
 CSRC = os.path.join(_HERE, "csrc")
 OUT = os.path.join(_HERE, "libpgf.so")
-SOURCES = ["pgf_scan.hip", "pgf_scan_f32.hip", "pgf_scan_bf16.hip", "pgf_la.hip", "pgf_plan.cpp", "pgf_timing.cpp"]
+SOURCES = ["pgf_scan.hip", "pgf_scan_f32.hip", "pgf_scan_bf16.hip", "pgf_la.hip", "pgf_plan.cpp", "pgf_timing.cpp",
+           "pgf_stream.cpp"]
 # Packed FP32 instructions stay disabled in every HIP object of this library.
 HIPCC_FLAGS = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC",
                "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

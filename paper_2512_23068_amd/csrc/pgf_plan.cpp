@@ -140,7 +140,7 @@ int make_plan(const pgf_params *p, Plan *plan) {
         // At least three rounds of resident blocks per launch, rounded to a
         // whole number of rounds when the workspace allows it.
         const size_t per_seg = (size_t)B * q.comp * (size_t)(N * D + D) * sizeof(float) +
-                               (size_t)B * seg * q.R * sizeof(float) +
+                               2 * (size_t)B * seg * q.R * sizeof(float) +
                                (size_t)(1 + K) * B * seg * (size_t)(rank ? q.rc + D : 0) * sizeof(float);
         const size_t wcap = rank ? kLowRankWorkspaceCap : kWorkspaceCap;
         const int64_t cap = std::max<int64_t>(1, (int64_t)(wcap / per_seg));
@@ -162,7 +162,9 @@ int make_plan(const pgf_params *p, Plan *plan) {
     Layout w{};
     size_t off = 0;
     w.state = off; off = align256(off + comp * B * N * D * f);
-    w.bc = off;    off = align256(off + (size_t)B * q.chunk_len * q.R * f);
+    w.bc = off;
+    w.bc_half = align256((size_t)B * q.chunk_len * q.R * f);
+    off += 2 * w.bc_half;
     if (seg) {
         const size_t G = (size_t)cs;
         w.agg_h = off;  off = align256(off + (size_t)B * G * comp * N * D * f);

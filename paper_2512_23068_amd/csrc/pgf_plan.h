@@ -12,7 +12,8 @@ namespace pgf {
 
 // Offsets (bytes) of the workspace sections; each is 256-byte aligned.
 //   state   [(1+K)][B][N][D]         state carried between host blocks
-//   bc      [B][Tc][R]               per-step projections of one host block,
+//   bc      [2][B][Tc][R]            per-step projections of two host blocks
+//                                    (the one being scanned and the next),
 //                                    per group 2N(1+KP): B, dB_0..dB_{KP-1}, C, dC_0..
 //   agg_h   [B][G][(1+K)][N][D]      segment end states from a zero start,
 //                                    then (in place) the true state
@@ -26,7 +27,7 @@ namespace pgf {
 // In the parameter flows K = 2 (the states dh/dA and dh/dB) and agg_h also
 // receives each segment's gradient partials after its rescan.
 struct Layout {
-    size_t state, bc, agg_h, agg_s, gacc, lr, dt, total;
+    size_t state, bc, bc_half, agg_h, agg_s, gacc, lr, dt, total;   // bc_half: bytes of one bc buffer
 };
 
 struct Plan {

@@ -33,6 +33,7 @@
 
 #include "pgf_plan.h"
 #include "pgf_scan_launch.h"
+#include "pgf_stream.h"
 #include "pgf_timing.h"
 
 namespace pgf {
@@ -1888,7 +1889,9 @@ struct Launcher {
     float *gA = nullptr, *gB = nullptr, *gC = nullptr;  // parameter flows only
 
     float *state() const { return (float *)(ws + q.ws.state); }
-    float *bcw() const { return (float *)(ws + q.ws.bc); }
+    int cur = 0;   // projection buffer of the host block being scanned
+    float *bc_buf(int i) const { return (float *)(ws + q.ws.bc + (size_t)i * q.ws.bc_half); }
+    float *bcw() const { return bc_buf(cur); }
     float *agg_h() const { return (float *)(ws + q.ws.agg_h); }
     float *agg_s() const { return (float *)(ws + q.ws.agg_s); }
     float *seg_in() const { return (float *)(ws + q.ws.agg_h); }  // overwritten in place by k_carry
@@ -1897,27 +1900,28 @@ struct Launcher {
     float *dtw() const { return (float *)(ws + q.ws.dt); }
 
     template <int NC>
-    void proj_nc(int64_t t0, int64_t len) {
+    void proj_nc(int64_t t0, int64_t len, float *dst, hipStream_t ps) {
         dim3 grid((unsigned)((len + kProjTM - 1) / kProjTM), (unsigned)(1 + q.KP), (unsigned)q.B);
-        Timed tm(0, st);
+        Timed tm(0, ps);
         if (q.groups > 1)
-            hipLaunchKernelGGL((k_proj<NC, InT, true>), grid, dim3(kThreads), 0, st, x, dx, p.W_B, p.W_C, p.b_B,
-                               p.b_C, bcw(), q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len, (int)q.N);
+            hipLaunchKernelGGL((k_proj<NC, InT, true>), grid, dim3(kThreads), 0, ps, x, dx, p.W_B, p.W_C, p.b_B,
+                               p.b_C, dst, q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len, (int)q.N);
         else
-            hipLaunchKernelGGL((k_proj<NC, InT, false>), grid, dim3(kThreads), 0, st, x, dx, p.W_B, p.W_C, p.b_B,
-                               p.b_C, bcw(), q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len, (int)q.N);
+            hipLaunchKernelGGL((k_proj<NC, InT, false>), grid, dim3(kThreads), 0, ps, x, dx, p.W_B, p.W_C, p.b_B,
+                               p.b_C, dst, q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len, (int)q.N);
     }
 
     // One pass over x (and each dx_k) computes the B and C columns of every
     // channel group: 2 * groups * N columns (a power of two, checked by the
-    // planner).
-    bool proj(int64_t t0, int64_t len) {
+    // planner), into projection buffer buf, on stream ps.
+    bool proj(int64_t t0, int64_t len, int buf, hipStream_t ps) {
+        float *dst = bc_buf(buf);
         switch (2 * q.groups * q.N) {
-            case 8: proj_nc<8>(t0, len); return true;
-            case 16: proj_nc<16>(t0, len); return true;
-            case 32: proj_nc<32>(t0, len); return true;
-            case 64: proj_nc<64>(t0, len); return true;
-            case 128: proj_nc<128>(t0, len); return true;
+            case 8: proj_nc<8>(t0, len, dst, ps); return true;
+            case 16: proj_nc<16>(t0, len, dst, ps); return true;
+            case 32: proj_nc<32>(t0, len, dst, ps); return true;
+            case 64: proj_nc<64>(t0, len, dst, ps); return true;
+            case 128: proj_nc<128>(t0, len, dst, ps); return true;
             default: return false;
         }
     }
@@ -2228,10 +2232,33 @@ struct Launcher {
                 hipLaunchKernelGGL(k_fill0, dim3((unsigned)((nacc + kThreads - 1) / kThreads)), dim3(kThreads), 0,
                                    st, gacc(), nacc);
         }
-        for (int64_t t0 = 0; t0 < q.L; t0 += q.chunk_len) {
-            const int64_t len = q.L - t0 < q.chunk_len ? q.L - t0 : q.chunk_len;
-            if (!proj(t0, len) || (q.rank && !lowrank(t0, len)) || !scan_block(t0, len))
-                return PGF_ERR_UNSUPPORTED;
+        // Host blocks.  The projection of block c+1 goes to the other buffer
+        // on the helper stream while block c is scanned on the caller's
+        // stream: it starts once everything enqueued before block c's scans
+        // (block c-1's scans, the last readers of that buffer) is done, and
+        // block c+1's scans wait for it.  Without a helper it runs in order.
+        Helper *hp = q.n_chunks > 1 ? helper() : nullptr;
+        std::unique_lock<std::mutex> lk;
+        if (hp) lk = std::unique_lock<std::mutex>(hp->mu);
+        const hipStream_t ps = hp ? hp->side : st;
+        auto block_len = [&](int64_t c) {
+            const int64_t t0 = c * q.chunk_len;
+            return q.L - t0 < q.chunk_len ? q.L - t0 : q.chunk_len;
+        };
+        if (q.n_chunks > 0 && !proj(0, block_len(0), 0, st)) return PGF_ERR_UNSUPPORTED;
+        for (int64_t c = 0; c < q.n_chunks; ++c) {
+            const int64_t t0 = c * q.chunk_len, len = block_len(c);
+            cur = (int)(c & 1);
+            if (c + 1 < q.n_chunks) {
+                if (hp) {
+                    (void)hipEventRecord(hp->fork, st);
+                    (void)hipStreamWaitEvent(ps, hp->fork, 0);
+                }
+                if (!proj(t0 + q.chunk_len, block_len(c + 1), cur ^ 1, ps)) return PGF_ERR_UNSUPPORTED;
+                if (hp) (void)hipEventRecord(hp->join, ps);
+            }
+            if ((q.rank && !lowrank(t0, len)) || !scan_block(t0, len)) return PGF_ERR_UNSUPPORTED;
+            if (hp && c + 1 < q.n_chunks) (void)hipStreamWaitEvent(st, hp->join, 0);
         }
         if (q.order == 3) {
             Timed tm(4, st);
