@@ -2,13 +2,16 @@
 // transformers, RetNet and RWKV-6 as general linear recurrences) for gfx950.
 //
 // The state of one (batch, head) is a dk x dv matrix S.  A block owns 64
-// value columns j of one head (one lane each) and splits the key dimension
-// over its waves: wave w holds S[16w .. 16w+15, j] (and the tangents) in
-// registers.  Every lane of a wave needs the same 16 key-side values per
-// step (q, k, alpha = exp(g), their tangents): the block stages them in LDS
-// a tile of steps ahead and the lanes read them as broadcasts.  The
-// per-lane inputs are v[j] and dv_k[j]; each wave's partial outputs of a
-// tile of steps are summed over the waves through LDS in a fixed order.
+// value columns of one head and splits the key dimension into slices of
+// kKeys: a thread holds S[s*kKeys .. (s+1)*kKeys - 1, j .. j+kCols-1] (and
+// the tangents) in registers, kKeys * kCols = 16 entries, so each key-side
+// value it reads serves kCols columns (la_cols: 2 in the pass with outputs,
+// 4 in the aggregate pass).  The lanes that share a slice need the same
+// key-side values per step (q, k, alpha = exp(g), their tangents): the
+// block stages them in LDS a tile of steps ahead and the lanes read them as
+// broadcasts.  The per-lane inputs are v and dv_k of its columns; the
+// partial outputs of a tile of steps are summed over the slices through LDS
+// in a fixed order.
 //
 // Kernels, per host block of steps [t0, t0+len):
 //   k_la_prep      alpha = exp(g) and alpha*dg_k per step into records, and
@@ -31,7 +34,12 @@ namespace pgf {
 namespace la {
 
 constexpr int kThreads = 256;       // threads per block of the elementwise kernels
-constexpr int kSlice = 16;          // key dimensions per wave in the scan
+// Value columns per thread in the scan (the key dimensions per thread are
+// 16 / columns, so a thread holds 16 entries of S): two in the pass with
+// outputs, four in the aggregate pass, whose fewer fields per step leave
+// room for the wider column block.
+template <bool OUT>
+constexpr int la_cols() { return OUT ? 2 : 4; }
 constexpr float kLog2eHi = 1.44269502162933349609375f;  // log2(e) rounded to f32
 constexpr float kLog2eLo = 1.925963033500011079e-08f;   // log2(e) - kLog2eHi
 constexpr float kLn2 = 0.693147180559945309f;
@@ -94,66 +102,65 @@ __global__ __launch_bounds__(kThreads) void k_la_prep(
 }
 
 // ---------------------------------------------------------------- scan
-// Grid (BH*DV/64, G); block of 64*NW threads (NW = DK/16 waves): block x ->
-// (head bh, 64-column group), wave w -> key slice [16w, 16w+16), lane ->
-// column j.  OUT=false: segment aggregate from a zero state into agg_h.
-// OUT=true: scan from the entry state at init[bh*ibs + g*igs + c*ics +
-// i*DV + j] and write o, do_k; end_state (sequential evaluation) receives
-// the exit state with the same indexing.
-//
-// The key-side vectors of a tile of TT steps (fields alpha, k, alpha*dg_k,
-// dk_k and, for outputs, q, dq_k; DK floats each) are loaded by the whole
-// block with coalesced loads one tile ahead and staged in LDS (double
-// buffered); every lane then reads them as broadcasts.  Outputs of a tile
-// are reduced over the NW waves through LDS, slice 0 first.  One barrier
-// per tile.
 template <int DK, int K, bool OUT>
 constexpr int la_fields() { return 2 + 2 * K + (OUT ? 1 + K : 0); }
 
 template <int DK, int K, bool OUT>
-__global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per_eu(K == 1 && !OUT ? 4 : 3))) void k_la_scan(
+__global__ __launch_bounds__(64 * (DK / 16)) __attribute__((amdgpu_waves_per_eu(K == 1 ? 4 : 2))) void k_la_scan(
     const float *__restrict__ q, const float *__restrict__ k, const float *__restrict__ v,
     const float *__restrict__ dq, const float *__restrict__ dk, const float *__restrict__ dv,
     const float *__restrict__ rec, const float *init, int64_t ibs, int64_t igs, int64_t ics,
     float *__restrict__ o, float *__restrict__ do_, float *end_state, float *__restrict__ agg_h,
     int64_t BH, int64_t L, int64_t DV, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
-    constexpr int NW = DK / kSlice;
+    constexpr int NW = DK / 16;
+    constexpr int kCols = la_cols<OUT>();
+    constexpr int kKeys = 16 / kCols;
+    constexpr int NS = DK / kKeys;    // key slices (kCols per wave)
     constexpr int NTH = 64 * NW;
     constexpr int R = (1 + K) * DK;   // floats per step record
-    constexpr int TT = 4;             // steps per tile
+    constexpr int TT = 2;             // steps per tile
     constexpr int F = la_fields<DK, K, OUT>();
     constexpr int FA = 2 + 2 * K;     // fields of the state update
     constexpr int NPF = (TT * F * DK + NTH - 1) / NTH;   // key-side floats per thread and tile
     __shared__ float kvs[2][TT][F][DK];
-    __shared__ float red[OUT ? 2 : 1][TT][1 + K][NW][64];
+    __shared__ float red[OUT ? 2 : 1][TT][1 + K][NS][64];
 
     const int tid = threadIdx.x;
     const int lane = tid % 64;
     const int w = __builtin_amdgcn_readfirstlane(tid / 64);
     const int64_t groups = DV / 64;
     const int64_t bh = blockIdx.x / groups;
-    const int64_t j = (blockIdx.x % groups) * 64 + lane;
+    const int64_t jg = (blockIdx.x % groups) * 64;   // first column of the block
+    constexpr int LPS = 64 / kCols;                   // lanes per key slice
+    const int64_t j = jg + kCols * (lane % LPS);      // this thread's columns j .. j+kCols-1
     const int g = blockIdx.y;
     const int64_t ts = (int64_t)g * S;
     const int64_t te = ts + S < len ? ts + S : len;
     if (ts >= te) return;   // uniform over the block
-    const int i0 = w * kSlice;
+    const int sl = kCols * w + lane / LPS;            // key slice
+    const int i0 = sl * kKeys;
 
-    float Sm[kSlice], dS[K][kSlice];
+    float Sm[kKeys][kCols], dS[K][kKeys][kCols];
     if constexpr (OUT) {
         const float *ib = init + bh * ibs + g * igs + (int64_t)i0 * DV + j;
 #pragma unroll
-        for (int i = 0; i < kSlice; ++i) {
-            Sm[i] = ib[i * DV];
+        for (int i = 0; i < kKeys; ++i) {
 #pragma unroll
-            for (int kk = 0; kk < K; ++kk) dS[kk][i] = ib[(1 + kk) * ics + i * DV];
+            for (int c = 0; c < kCols; ++c) {
+                Sm[i][c] = ib[i * DV + c];
+#pragma unroll
+                for (int kk = 0; kk < K; ++kk) dS[kk][i][c] = ib[(1 + kk) * ics + i * DV + c];
+            }
         }
     } else {
 #pragma unroll
-        for (int i = 0; i < kSlice; ++i) {
-            Sm[i] = 0.0f;
+        for (int i = 0; i < kKeys; ++i) {
 #pragma unroll
-            for (int kk = 0; kk < K; ++kk) dS[kk][i] = 0.0f;
+            for (int c = 0; c < kCols; ++c) {
+                Sm[i][c] = 0.0f;
+#pragma unroll
+                for (int kk = 0; kk < K; ++kk) dS[kk][i][c] = 0.0f;
+            }
         }
     }
 
@@ -165,8 +172,12 @@ __global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per
     // The key-side data of a tile is TT*F rows of DK floats (row r = step
     // jj*F + field f); thread tid loads element tid % DK of the rows
     // r = tid / DK (mod RPI), so every row is one coalesced load and the
-    // field of each load is known at compile time.  Steps past the segment
-    // repeat its last step.
+    // field of each load is known at compile time.  Loads past the segment
+    // repeat its last step.  In the pass with outputs, those steps are
+    // staged as neutral data (alpha = 1, every other field 0): such a step
+    // leaves S and dS exactly as they are, so whole tiles run without a
+    // per-step guard (their outputs are never written); the aggregate pass
+    // skips them.
     constexpr int RPI = NTH / DK;          // rows covered by one pass of the block
     const int myrow = tid / DK, ki_ = tid % DK;
     auto key_row = [&](int f, int64_t t) -> const float * {
@@ -189,49 +200,80 @@ __global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per
             }
         }
     };
-    auto stash = [&](int b, const float *pre) {
+    auto stash = [&](int b, int64_t tb, const float *pre) {
 #pragma unroll
-        for (int r = 0; r < TT * F; ++r)
-            if (r % RPI == myrow) kvs[b][r / F][r % F][ki_] = pre[r / RPI];
+        for (int r = 0; r < TT * F; ++r) {
+            if (r % RPI == myrow) {
+                const int f = r % F;
+                float val = pre[r / RPI];
+                if constexpr (OUT) val = tb + r / F < te ? val : (f == 0 ? 1.0f : 0.0f);
+                kvs[b][r / F][f][ki_] = val;
+            }
+        }
     };
 
-    // One step (tile slot jj) for this wave's key slice: the state update,
-    // then the partial outputs summed over the slice.
-    auto step = [&](int b, int jj, float vv, const float *dvv, float *part) {
+    // One step (tile slot jj) for this thread's key slice and kCols columns:
+    // the state update, then the partial outputs summed over the slice.
+    // part[c][0] = o, part[c][1+k] = do_k of column j + c.
+    auto step = [&](int b, int jj, const float *vv, const float (*dvv)[kCols], float (*part)[1 + K]) {
         const float *rr = &kvs[b][jj][0][i0];
 #pragma unroll
-        for (int i = 0; i < kSlice; ++i) {
+        for (int i = 0; i < kKeys; ++i) {
             const float a = rr[i], ki = rr[DK + i];
-            const float sn = fmaf(ki, vv, a * Sm[i]);
 #pragma unroll
-            for (int kk = 0; kk < K; ++kk) {
-                const float adg = rr[(2 + 2 * kk) * DK + i];
-                const float dki = rr[(3 + 2 * kk) * DK + i];
-                dS[kk][i] = fmaf(a, dS[kk][i], fmaf(adg, Sm[i], fmaf(dki, vv, ki * dvv[kk])));
+            for (int c = 0; c < kCols; ++c) {
+                // the tangents read the old S; the two passes order the
+                // updates differently (same values), whichever schedules
+                // better
+                if constexpr (OUT) {
+#pragma unroll
+                    for (int kk = 0; kk < K; ++kk) {
+                        const float adg = rr[(2 + 2 * kk) * DK + i];
+                        const float dki = rr[(3 + 2 * kk) * DK + i];
+                        dS[kk][i][c] =
+                            fmaf(a, dS[kk][i][c], fmaf(adg, Sm[i][c], fmaf(dki, vv[c], ki * dvv[kk][c])));
+                    }
+                    Sm[i][c] = fmaf(ki, vv[c], a * Sm[i][c]);
+                } else {
+                    const float sn = fmaf(ki, vv[c], a * Sm[i][c]);
+#pragma unroll
+                    for (int kk = 0; kk < K; ++kk) {
+                        const float adg = rr[(2 + 2 * kk) * DK + i];
+                        const float dki = rr[(3 + 2 * kk) * DK + i];
+                        dS[kk][i][c] =
+                            fmaf(a, dS[kk][i][c], fmaf(adg, Sm[i][c], fmaf(dki, vv[c], ki * dvv[kk][c])));
+                    }
+                    Sm[i][c] = sn;
+                }
             }
-            Sm[i] = sn;
         }
         if constexpr (OUT) {
-            float ov = 0.0f, dov[K];
 #pragma unroll
-            for (int kk = 0; kk < K; ++kk) dov[kk] = 0.0f;
+            for (int c = 0; c < kCols; ++c) {
+                float ov = 0.0f, dov[K];
 #pragma unroll
-            for (int i = 0; i < kSlice; ++i) {
-                const float qi = rr[FA * DK + i];
-                ov = fmaf(qi, Sm[i], ov);
+                for (int kk = 0; kk < K; ++kk) dov[kk] = 0.0f;
 #pragma unroll
-                for (int kk = 0; kk < K; ++kk)
-                    dov[kk] = fmaf(rr[(FA + 1 + kk) * DK + i], Sm[i], fmaf(qi, dS[kk][i], dov[kk]));
+                for (int i = 0; i < kKeys; ++i) {
+                    const float qi = rr[FA * DK + i];
+                    ov = fmaf(qi, Sm[i][c], ov);
+#pragma unroll
+                    for (int kk = 0; kk < K; ++kk)
+                        dov[kk] = fmaf(rr[(FA + 1 + kk) * DK + i], Sm[i][c], fmaf(qi, dS[kk][i][c], dov[kk]));
+                }
+                part[c][0] = ov;
+#pragma unroll
+                for (int kk = 0; kk < K; ++kk) part[c][1 + kk] = dov[kk];
             }
-            part[0] = ov;
-#pragma unroll
-            for (int kk = 0; kk < K; ++kk) part[1 + kk] = dov[kk];
         }
     };
-    auto load_vdv = [&](int64_t t, float &vv, float *dvv) {
-        vv = vb[t * DV];
+    auto load_vdv = [&](int64_t t, float *vv, float (*dvv)[kCols]) {
 #pragma unroll
-        for (int kk = 0; kk < K; ++kk) dvv[kk] = dv[(kk * kst + row0 + t) * DV + j];
+        for (int c = 0; c < kCols; ++c) {
+            vv[c] = vb[t * DV + c];
+#pragma unroll
+            for (int kk = 0; kk < K; ++kk) dvv[kk][c] = dv[(kk * kst + row0 + t) * DV + j + c];
+        }
     };
 
     // Tiles of TT steps (the last one partial); the next tile's key-side data
@@ -239,8 +281,8 @@ __global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per
     // loop is taken by the whole block.
     float pre[NPF];
     fetch(ts, pre);
-    stash(0, pre);
-    float vc[TT], dvc[TT][K];
+    stash(0, ts, pre);
+    float vc[TT][kCols], dvc[TT][K][kCols];
 #pragma unroll
     for (int jj = 0; jj < TT; ++jj) load_vdv(ts + jj < te ? ts + jj : te - 1, vc[jj], dvc[jj]);
     __syncthreads();
@@ -248,26 +290,35 @@ __global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per
     for (int64_t tb = ts; tb < te; tb += TT) {
         const bool more = tb + TT < te;
         if (more) fetch(tb + TT, pre);
-        float vn[TT], dvn[TT][K];
+        float vn[TT][kCols], dvn[TT][K][kCols];
 #pragma unroll
         for (int jj = 0; jj < TT; ++jj) {
             const int64_t t = tb + TT + jj < te ? tb + TT + jj : te - 1;
             load_vdv(t, vn[jj], dvn[jj]);
         }
-        float part[TT][1 + K];
+        float part[TT][kCols][1 + K];
+        if constexpr (OUT) {
 #pragma unroll
-        for (int jj = 0; jj < TT; ++jj)
-            if (tb + jj < te) step(buf, jj, vc[jj], dvc[jj], part[jj]);
+            for (int jj = 0; jj < TT; ++jj) step(buf, jj, vc[jj], dvc[jj], part[jj]);
+        } else {
+            // (measured: the aggregate pass runs faster with the guard)
+#pragma unroll
+            for (int jj = 0; jj < TT; ++jj)
+                if (tb + jj < te) step(buf, jj, vc[jj], dvc[jj], part[jj]);
+        }
         if constexpr (OUT) {
 #pragma unroll
             for (int jj = 0; jj < TT; ++jj)
 #pragma unroll
-                for (int c = 0; c <= K; ++c) red[buf][jj][c][w][lane] = part[jj][c];
+                for (int c = 0; c <= K; ++c)
+#pragma unroll
+                    for (int e = 0; e < kCols; ++e) red[buf][jj][c][sl][kCols * (lane % LPS) + e] = part[jj][e][c];
         }
-        if (more) stash(buf ^ 1, pre);
+        if (more) stash(buf ^ 1, tb + TT, pre);
         __syncthreads();
         if constexpr (OUT) {
-            // wave w completes steps jj = w, w + NW, ... of the tile
+            // wave w completes steps jj = w, w + NW, ... of the tile, lane =
+            // column jg + lane
             for (int jj = w; jj < TT; jj += NW) {
                 const int64_t t = tb + jj;
                 if (t >= te) break;
@@ -275,39 +326,45 @@ __global__ __launch_bounds__(64 * (DK / kSlice)) __attribute__((amdgpu_waves_per
                 for (int c = 0; c <= K; ++c) {
                     float acc = red[buf][jj][c][0][lane];
 #pragma unroll
-                    for (int s2 = 1; s2 < NW; ++s2) acc += red[buf][jj][c][s2][lane];
-                    if (c == 0) o[(row0 + t) * DV + j] = acc;
-                    else do_[((c - 1) * kst + row0 + t) * DV + j] = acc;
+                    for (int s2 = 1; s2 < NS; ++s2) acc += red[buf][jj][c][s2][lane];
+                    if (c == 0) o[(row0 + t) * DV + jg + lane] = acc;
+                    else do_[((c - 1) * kst + row0 + t) * DV + jg + lane] = acc;
                 }
             }
         }
         buf ^= 1;
 #pragma unroll
-        for (int jj = 0; jj < TT; ++jj) {
-            vc[jj] = vn[jj];
+        for (int jj = 0; jj < TT; ++jj)
 #pragma unroll
-            for (int kk = 0; kk < K; ++kk) dvc[jj][kk] = dvn[jj][kk];
-        }
+            for (int c = 0; c < kCols; ++c) {
+                vc[jj][c] = vn[jj][c];
+#pragma unroll
+                for (int kk = 0; kk < K; ++kk) dvc[jj][kk][c] = dvn[jj][kk][c];
+            }
     }
 
     if constexpr (OUT) {
         if (end_state) {
             float *eb = end_state + bh * ibs + (int64_t)i0 * DV + j;
 #pragma unroll
-            for (int i = 0; i < kSlice; ++i) {
-                eb[i * DV] = Sm[i];
+            for (int i = 0; i < kKeys; ++i)
 #pragma unroll
-                for (int kk = 0; kk < K; ++kk) eb[(1 + kk) * ics + i * DV] = dS[kk][i];
-            }
+                for (int c = 0; c < kCols; ++c) {
+                    eb[i * DV + c] = Sm[i][c];
+#pragma unroll
+                    for (int kk = 0; kk < K; ++kk) eb[(1 + kk) * ics + i * DV + c] = dS[kk][i][c];
+                }
         }
     } else {
         float *ab = agg_h + (bh * G + g) * (1 + K) * DK * DV + (int64_t)i0 * DV + j;
 #pragma unroll
-        for (int i = 0; i < kSlice; ++i) {
-            ab[i * DV] = Sm[i];
+        for (int i = 0; i < kKeys; ++i)
 #pragma unroll
-            for (int kk = 0; kk < K; ++kk) ab[((1 + kk) * DK + i) * DV] = dS[kk][i];
-        }
+            for (int c = 0; c < kCols; ++c) {
+                ab[i * DV + c] = Sm[i][c];
+#pragma unroll
+                for (int kk = 0; kk < K; ++kk) ab[((1 + kk) * DK + i) * DV + c] = dS[kk][i][c];
+            }
     }
 }
 
@@ -388,7 +445,7 @@ struct LaLauncher {
     void block(int64_t t0, int64_t len) {
         const int64_t ND = DK * q.DV;
         const unsigned gx = (unsigned)(q.BH * q.DV / 64);
-        const dim3 blk(64 * (DK / kSlice));
+        const dim3 blk(64 * (DK / 16));
         const int64_t S = q.seg ? q.seg : len;
         const int G = (int)((len + S - 1) / S);
         {
