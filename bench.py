@@ -227,26 +227,9 @@ def setup_ssm(args, np, torch, binding, inputs):
           f"{time.time() - t_gen:.1f}s", file=sys.stderr, flush=True)
     tdt = torch.bfloat16 if cfg.in_dtype == "bf16" else torch.float32
     x = torch.from_numpy(inp["x"]).to(dev).to(tdt)
-    params = {k: torch.from_numpy(inp[k]).to(dev) for k in ("A", "w_delta", "b_delta", "W_B", "W_C")}
-    if args.dres:
-        params["D_res"] = torch.from_numpy(
-            np.random.default_rng([23068, 7]).standard_normal(D).astype(np.float32)).to(dev)
-    if args.groups > 1:
-        G = args.groups
-        r = np.random.default_rng([23068, 8])
-        params["n_groups"] = G
-        params["W_B"] = torch.from_numpy((r.standard_normal((D, G * N)) / np.sqrt(D)).astype(np.float32)).to(dev)
-        params["W_C"] = torch.from_numpy((r.standard_normal((D, G * N)) / np.sqrt(D)).astype(np.float32)).to(dev)
-    if args.lowrank > 0:
-        # x W_dx ~ N(0, |x|^2/D) per rank column; W_dt ~ U(-1, 1)/sqrt(R), the
-        # step-size projection's usual initialisation; b_delta stays the bias
-        R = args.lowrank
-        r = np.random.default_rng([23068, 9])
-        params["W_dx"] = torch.from_numpy((r.standard_normal((D, R)) / np.sqrt(D)).astype(np.float32)).to(dev)
-        params["W_dt"] = torch.from_numpy((r.uniform(-1.0, 1.0, (R, D)) / np.sqrt(R)).astype(np.float32)).to(dev)
-    if args.complex:
-        params["A"] = torch.full((D, N), -0.5, device=dev)
-        params["A_im"] = (np.pi * torch.arange(N, device=dev, dtype=torch.float32)).expand(D, N).contiguous()
+    vp = inputs.variant_params({k: inp[k] for k in ("A", "w_delta", "b_delta", "W_B", "W_C")}, cfg,
+                               dres=args.dres, groups=args.groups, lowrank=args.lowrank, complex_a=args.complex)
+    params = {k: (torch.from_numpy(v).to(dev) if isinstance(v, np.ndarray) else v) for k, v in vp.items()}
     s_in = x.element_size()
     y = torch.empty((B, L, D), device=dev)
     if args.order == 3:

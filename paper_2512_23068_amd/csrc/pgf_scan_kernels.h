@@ -1573,15 +1573,46 @@ static __global__ __launch_bounds__(kThreads) void k_gout(
 //   s = Abar h,  h' = s + B u,  g = A s,
 //   dh'_k = Abar dh_k + g dDelta_k + (B p_k + dB_k u)     (drive real)
 //   y = sum_n C Re(h'),  dy_k = sum_n dC_k Re(h') + C Re(dh'_k)
-// The angle is reduced in revolutions (th/2pi minus its nearest integer)
-// before the hardware sine and cosine.  Layouts as k_scan with the state
-// split into planes: component c = 2m + part (m = 0 h, 1..K dh_k).
+// The angle is reduced in revolutions and its sine and cosine evaluated to
+// about one ulp (rot); the hardware sine and cosine were not accurate enough
+// for long sequences.  Layouts as k_scan with the state split into planes:
+// component c = 2m + part (m = 0 h, 1..K dh_k).
 constexpr float kInv2Pi = 0.159154943091895336f;
+constexpr float kTwoPiHi = 6.28318548202514648f;   // 2 pi rounded to f32
+constexpr float kTwoPiLo = -1.74845553e-07f;        // 2 pi - kTwoPiHi
 
+// c = cos(2 pi rev), s = sin(2 pi rev).  The angle in revolutions is reduced
+// to r = rev - rint(rev) in [-1/2, 1/2] and then by half turns to
+// f = r - k/2 in [-1/4, 1/4] (k = rint(2r); both subtractions are exact);
+// phi = 2 pi f in [-pi/2, pi/2] is formed with 2 pi split into two floats.
+// sin and cos of phi are their Taylor series to phi^13 and phi^14 (the
+// first omitted terms are below 1e-9 on that interval), and an odd k turns
+// both signs.  Measured on gfx950 the hardware sine and cosine err by up to
+// 1.2e-7 absolute (9e-7 relative for small angles), which accumulates over
+// the long memory of a weakly damped lane; this evaluation stays near one
+// ulp.
 __device__ __forceinline__ void rot(float rev, float &c, float &s) {
     const float r = rev - __builtin_rintf(rev);
-    s = __builtin_amdgcn_sinf(r);
-    c = __builtin_amdgcn_cosf(r);
+    const float k = __builtin_rintf(2.0f * r);
+    const float f = fmaf(k, -0.5f, r);
+    const float p = fmaf(f, kTwoPiHi, f * kTwoPiLo);
+    const float q = p * p;
+    float sp = fmaf(q, 1.0f / 6227020800.0f, -1.0f / 39916800.0f);
+    sp = fmaf(q, sp, 1.0f / 362880.0f);
+    sp = fmaf(q, sp, -1.0f / 5040.0f);
+    sp = fmaf(q, sp, 1.0f / 120.0f);
+    sp = fmaf(q, sp, -1.0f / 6.0f);
+    sp = fmaf(q * p, sp, p);
+    float cp = fmaf(q, -1.0f / 87178291200.0f, 1.0f / 479001600.0f);
+    cp = fmaf(q, cp, -1.0f / 3628800.0f);
+    cp = fmaf(q, cp, 1.0f / 40320.0f);
+    cp = fmaf(q, cp, -1.0f / 720.0f);
+    cp = fmaf(q, cp, 1.0f / 24.0f);
+    cp = fmaf(q, cp, -0.5f);
+    cp = fmaf(q, cp, 1.0f);
+    const float sg = k != 0.0f ? -1.0f : 1.0f;   // k in {-1, 0, 1}
+    s = sg * sp;
+    c = sg * cp;
 }
 
 template <int NT, int K, bool OUT, typename InT>

@@ -198,6 +198,37 @@ def make_inputs(key, threads: int | None = None) -> dict:
     return out
 
 
+def variant_params(params: dict, cfg: ScanConfig, dres: bool = False, groups: int = 1, lowrank: int = 0,
+                   complex_a: bool = False) -> dict:
+    """The parameters of the model variants on a workload's shape, added to
+    (a copy of) params, float32 numpy:
+      dres      D_res [D] ~ N(0, 1)                           (seed [23068, 7])
+      groups    G groups: W_B, W_C [D, G*N] ~ N(0, 1/D)      (seed [23068, 8])
+      lowrank   rank R: W_dx [D, R] ~ N(0, 1/D), W_dt [R, D] ~ U(-1, 1)/sqrt(R),
+                the usual initialisation of the step-size projection; b_delta
+                stays the bias, w_delta is dropped          (seed [23068, 9])
+      complex_a the S4D-Lin spectrum A = -1/2 + i*pi*n (A [D, N], A_im [D, N])."""
+    out = dict(params)
+    D, N = cfg.d_inner, cfg.d_state
+    f = lambda a: np.ascontiguousarray(a, dtype=np.float32)
+    if dres:
+        out["D_res"] = f(np.random.default_rng([23068, 7]).standard_normal(D))
+    if groups > 1:
+        r = np.random.default_rng([23068, 8])
+        out["n_groups"] = int(groups)
+        out["W_B"] = f(r.standard_normal((D, groups * N)) / np.sqrt(D))
+        out["W_C"] = f(r.standard_normal((D, groups * N)) / np.sqrt(D))
+    if lowrank > 0:
+        r = np.random.default_rng([23068, 9])
+        out["W_dx"] = f(r.standard_normal((D, lowrank)) / np.sqrt(D))
+        out["W_dt"] = f(r.uniform(-1.0, 1.0, (lowrank, D)) / np.sqrt(lowrank))
+        out.pop("w_delta", None)
+    if complex_a:
+        out["A"] = f(np.full((D, N), -0.5))
+        out["A_im"] = f(np.broadcast_to(np.pi * np.arange(N), (D, N)))
+    return out
+
+
 # ------------------------------------------------------------------ linear attention
 # Decaying linear attention (RWKV-6 / RetNet / GLA style), head-major layout.
 # Recipe per workload index i: q, k ~ N(0,1)/sqrt(dk), v ~ N(0,1); the
