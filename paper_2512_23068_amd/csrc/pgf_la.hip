@@ -118,7 +118,7 @@ __global__ __launch_bounds__(64 * (DK / 16)) __attribute__((amdgpu_waves_per_eu(
     constexpr int NS = DK / kKeys;    // key slices (kCols per wave)
     constexpr int NTH = 64 * NW;
     constexpr int R = (1 + K) * DK;   // floats per step record
-    constexpr int TT = 2;             // steps per tile
+    constexpr int TT = OUT ? 4 : 2;   // steps per tile
     constexpr int F = la_fields<DK, K, OUT>();
     constexpr int FA = 2 + 2 * K;     // fields of the state update
     constexpr int NPF = (TT * F * DK + NTH - 1) / NTH;   // key-side floats per thread and tile
