@@ -105,6 +105,10 @@ int make_plan(const pgf_params *p, Plan *plan) {
     q.nt = (int)std::min<int64_t>(N, K >= 8 ? 4 : (K >= 4 ? 8 : 16));
     q.ns = (int)(N / q.nt);
     q.R = (int)(groups * 2 * N * (1 + q.KP));
+    // Wide channel sums are cut into splits of at most about 2048 channels,
+    // so that a projection launch has enough blocks of moderate length.
+    q.ksplit = (int)std::min<int64_t>(4, (D + 2047) / 2048);
+    q.dchunk = ((D + q.ksplit - 1) / q.ksplit + 31) / 32 * 32;
 
     // Blocks of one segment column (every channel, one segment).
     const int64_t nblk = B * ((D * q.ns + 255) / 256);
@@ -140,7 +144,7 @@ int make_plan(const pgf_params *p, Plan *plan) {
         // At least three rounds of resident blocks per launch, rounded to a
         // whole number of rounds when the workspace allows it.
         const size_t per_seg = (size_t)B * q.comp * (size_t)(N * D + D) * sizeof(float) +
-                               2 * (size_t)B * seg * q.R * sizeof(float) +
+                               (size_t)(1 + q.ksplit) * B * seg * q.R * sizeof(float) +
                                (size_t)(1 + K) * B * seg * (size_t)(rank ? q.rc + D : 0) * sizeof(float);
         const size_t wcap = rank ? kLowRankWorkspaceCap : kWorkspaceCap;
         const int64_t cap = std::max<int64_t>(1, (int64_t)(wcap / per_seg));
@@ -165,6 +169,8 @@ int make_plan(const pgf_params *p, Plan *plan) {
     w.bc = off;
     w.bc_half = align256((size_t)B * q.chunk_len * q.R * f);
     off += 2 * w.bc_half;
+    w.part = off;
+    off += (size_t)(q.ksplit - 1) * w.bc_half;
     if (seg) {
         const size_t G = (size_t)cs;
         w.agg_h = off;  off = align256(off + (size_t)B * G * comp * N * D * f);

@@ -15,6 +15,7 @@ namespace pgf {
 //   bc      [2][B][Tc][R]            per-step projections of two host blocks
 //                                    (the one being scanned and the next),
 //                                    per group 2N(1+KP): B, dB_0..dB_{KP-1}, C, dC_0..
+//   part    [S-1][B][Tc][R]          partial projections of channel splits 1..S-1
 //   agg_h   [B][G][(1+K)][N][D]      segment end states from a zero start,
 //                                    then (in place) the true state
 //                                    entering each segment
@@ -27,7 +28,7 @@ namespace pgf {
 // In the parameter flows K = 2 (the states dh/dA and dh/dB) and agg_h also
 // receives each segment's gradient partials after its rescan.
 struct Layout {
-    size_t state, bc, bc_half, agg_h, agg_s, gacc, lr, dt, total;   // bc_half: bytes of one bc buffer
+    size_t state, bc, bc_half, part, agg_h, agg_s, gacc, lr, dt, total;   // bc_half: bytes of one bc buffer
 };
 
 struct Plan {
@@ -46,6 +47,8 @@ struct Plan {
     int64_t chunk_len;   // steps per host block
     int64_t n_chunks;
     int R;               // floats per step in bc: groups * 2N(1+KP)
+    int ksplit;          // channel splits S of the projections (1 up to 2048 channels)
+    int64_t dchunk;      // channels per split, a multiple of 32
     Layout ws;
 };
 

@@ -192,21 +192,23 @@ __device__ __forceinline__ void silu_and_slope(float v, float &f, float &df) {
 // rows, so outputs do not depend on how the sequence is tiled.
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-// Loads 4 consecutive input values of one row (zero past D) as f32.
+// Loads 4 consecutive input values of one row (zero from n on) as f32;
+// vec: rows and the row start are 4-element aligned.
 template <typename InT>
-__device__ __forceinline__ floatx4 load4(const InT *__restrict__ row, int64_t d, int64_t D);
+__device__ __forceinline__ floatx4 load4(const InT *__restrict__ row, int64_t d, int64_t n, bool vec);
 template <>
-__device__ __forceinline__ floatx4 load4<float>(const float *__restrict__ row, int64_t d, int64_t D) {
-    if (d + 4 <= D && ((D & 3) == 0)) return *(const floatx4 *)(row + d);
+__device__ __forceinline__ floatx4 load4<float>(const float *__restrict__ row, int64_t d, int64_t n, bool vec) {
+    if (d + 4 <= n && vec) return *(const floatx4 *)(row + d);
     floatx4 v;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = d + i < D ? row[d + i] : 0.0f;
+    for (int i = 0; i < 4; ++i) v[i] = d + i < n ? row[d + i] : 0.0f;
     return v;
 }
 template <>
-__device__ __forceinline__ floatx4 load4<uint16_t>(const uint16_t *__restrict__ row, int64_t d, int64_t D) {
+__device__ __forceinline__ floatx4 load4<uint16_t>(const uint16_t *__restrict__ row, int64_t d, int64_t n,
+                                                   bool vec) {
     floatx4 v;
-    if (d + 4 <= D && ((D & 3) == 0)) {
+    if (d + 4 <= n && vec) {
         const uint2 u = *(const uint2 *)(row + d);
         v[0] = __uint_as_float(u.x << 16);
         v[1] = __uint_as_float(u.x & 0xffff0000u);
@@ -215,22 +217,23 @@ __device__ __forceinline__ floatx4 load4<uint16_t>(const uint16_t *__restrict__ 
         return v;
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = d + i < D ? __uint_as_float(((uint32_t)row[d + i]) << 16) : 0.0f;
+    for (int i = 0; i < 4; ++i) v[i] = d + i < n ? __uint_as_float(((uint32_t)row[d + i]) << 16) : 0.0f;
     return v;
 }
 
 // Rows x W on the matrix cores, for one block of TM = 128 rows of a row
-// source src ([len][D], row-major): acc[rt][c] receives the 16x16 tile
-// (rows wave*32 + rt*16 .., columns c*16 ..) of src[r0.., :] * W, where
-// wload(d, j) is W[d][j] for j < NC (zero is returned past the matrix).
+// source src (rows of stride ld, row-major; the dn channels from src on):
+// acc[rt][c] receives the 16x16 tile (rows wave*32 + rt*16 .., columns
+// c*16 ..) of src[r0.., 0..dn) * W, where wload(d, j) is W[d][j] (d counted
+// from src) for j < NC (zero is returned past the matrix).
 // X tiles are staged through LDS, double-buffered, with the next channel
 // stage in flight; the channel order of the sum is fixed.
 constexpr int kProjRT = 2;                      // 16-row tiles per wave
 constexpr int kProjTM = 4 * 16 * kProjRT;       // rows per block
 
 template <int NC, typename InT, class WLoad>
-__device__ __forceinline__ void xw_tiles(const InT *__restrict__ src, int64_t D, int64_t len, int64_t r0,
-                                         WLoad wload, floatx4 (&acc)[kProjRT][(NC + 15) / 16]) {
+__device__ __forceinline__ void xw_tiles(const InT *__restrict__ src, int64_t ld, int64_t dn, int64_t len,
+                                         int64_t r0, WLoad wload, floatx4 (&acc)[kProjRT][(NC + 15) / 16]) {
     constexpr int CT = (NC + 15) / 16;  // 16-column tiles (zero-padded)
     constexpr int NCP = CT * 16;
     constexpr int RT = kProjRT;
@@ -244,6 +247,7 @@ __device__ __forceinline__ void xw_tiles(const InT *__restrict__ src, int64_t D,
 
     const int tid = threadIdx.x;
     const int wave = tid / 64, lane = tid % 64;
+    const bool vec = (ld & 3) == 0 && (((uintptr_t)src / sizeof(InT)) & 3) == 0;
     floatx4 xr[XV];
     float wr[WE];
     auto fetch = [&](int64_t d0) {
@@ -252,7 +256,7 @@ __device__ __forceinline__ void xw_tiles(const InT *__restrict__ src, int64_t D,
             const int e = tid + i * kThreads;          // float4 index in the tile
             const int r = e / (DT / 4), c4 = e % (DT / 4);
             const int64_t row = r0 + r;
-            xr[i] = row < len ? load4<InT>(src + row * D, d0 + 4 * c4, D) : floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+            xr[i] = row < len ? load4<InT>(src + row * ld, d0 + 4 * c4, dn, vec) : floatx4{0.0f, 0.0f, 0.0f, 0.0f};
         }
 #pragma unroll
         for (int i = 0; i < WE; ++i) {
@@ -260,7 +264,7 @@ __device__ __forceinline__ void xw_tiles(const InT *__restrict__ src, int64_t D,
             const int dd = e / NCP, j = e % NCP;
             const int64_t d = d0 + dd;
             float v = 0.0f;
-            if (e < DT * NCP && d < D && j < NC) v = wload(d, j);
+            if (e < DT * NCP && d < dn && j < NC) v = wload(d, j);
             wr[i] = v;
         }
     };
@@ -283,7 +287,7 @@ __device__ __forceinline__ void xw_tiles(const InT *__restrict__ src, int64_t D,
 #pragma unroll
         for (int c = 0; c < CT; ++c) acc[rt][c] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
 
-    const int64_t nst = (D + DT - 1) / DT;
+    const int64_t nst = (dn + DT - 1) / DT;
     fetch(0);
     stash(0);
     __syncthreads();
@@ -315,25 +319,40 @@ __device__ __forceinline__ const InT *row_source(const InT *x, const InT *dx, in
     return s == 0 ? x + (b * L + t0) * D : dx + (((int64_t)(s - 1) * Bsz + b) * L + t0) * D;
 }
 
-// Per-step projections of one host block.  Grid (ceil(len/128), 1+KP, B):
-// rows of x (s = 0) or dx_{s-1} times [W_B | W_C] (NC = 2 * groups * N
+// Per-step projections of one host block.  Grid (ceil(len/128) * S, 1+KP,
+// B): rows of x (s = 0) or dx_{s-1} times [W_B | W_C] (NC = 2 * groups * N
 // columns) give B, dB_k, C, dC_k (per group), with the biases on s = 0.
+// With S > 1 splits the channel sum is cut into S ranges of dchunk
+// channels: split 0 writes bc (with the biases), split q > 0 writes the
+// same records to part + (q-1) * part_stride, and k_psum adds them in order.
 template <int NC, typename InT, bool GROUPED>
 __global__ __launch_bounds__(kThreads) void k_proj(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ WB,
     const float *__restrict__ WC, const float *__restrict__ bB, const float *__restrict__ bC,
     float *__restrict__ bc, int64_t Bsz, int64_t L, int64_t D, int K, int64_t t0, int64_t len, int64_t Tc,
-    int gn) {
+    int gn, int S, int64_t dchunk, float *__restrict__ part, int64_t part_stride) {
     constexpr int N = NC / 2;
     constexpr int CT = (NC + 15) / 16;
     constexpr int RT = kProjRT;
     const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
     const int s = blockIdx.y;
     const int64_t b = blockIdx.z;
-    const int64_t r0 = (int64_t)blockIdx.x * kProjTM;  // chunk-relative first row
+    const int q = (int)(blockIdx.x % S);                       // channel split
+    const int64_t r0 = (int64_t)(blockIdx.x / S) * kProjTM;    // chunk-relative first row
+    const int64_t dlo = q * dchunk;
+    const int64_t dn = D - dlo < dchunk ? D - dlo : dchunk;
+    if (q > 0) {
+        bc = part + (int64_t)(q - 1) * part_stride;
+        bB = nullptr;
+        bC = nullptr;
+    }
     floatx4 acc[RT][CT];
-    xw_tiles<NC, InT>(row_source(x, dx, s, b, Bsz, L, t0, D), D, len, r0,
-                      [&](int64_t d, int j) { return j < N ? WB[d * N + j] : WC[d * N + (j - N)]; }, acc);
+    xw_tiles<NC, InT>(row_source(x, dx, s, b, Bsz, L, t0, D) + dlo, D, dn, len, r0,
+                      [&](int64_t d, int j) {
+                          const int64_t dd = dlo + d;
+                          return j < N ? WB[dd * N + j] : WC[dd * N + (j - N)];
+                      },
+                      acc);
     const int R = 2 * N * (1 + K);     // a step's records (all groups)
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
@@ -360,6 +379,17 @@ __global__ __launch_bounds__(kThreads) void k_proj(
             }
         }
     }
+}
+
+// bc[i] += part[0][i] + ... in split order, for the n floats of a host
+// block's records (S > 1 channel splits).
+static __global__ __launch_bounds__(kThreads) void k_psum(float *__restrict__ bc, const float *__restrict__ part,
+                                                         int64_t part_stride, int S, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= n) return;
+    float v = bc[i];
+    for (int q = 1; q < S; ++q) v += part[(int64_t)(q - 1) * part_stride + i];
+    bc[i] = v;
 }
 
 // ---------------------------------------------------------------- low-rank step size
@@ -394,7 +424,7 @@ __global__ __launch_bounds__(kThreads) void k_lowx(
     const int64_t b = blockIdx.z;
     const int64_t r0 = (int64_t)blockIdx.x * kProjTM;
     floatx4 acc[RT][CT];
-    xw_tiles<RC, InT>(row_source(x, dx, s, b, Bsz, L, t0, D), D, len, r0,
+    xw_tiles<RC, InT>(row_source(x, dx, s, b, Bsz, L, t0, D), D, D, len, r0,
                       [&](int64_t d, int j) { return j < R ? Wdx[d * R + j] : 0.0f; }, acc);
     float *out = lr + ((int64_t)s * Bsz + b) * Tc * RC;
 #pragma unroll
@@ -1953,14 +1983,27 @@ struct Launcher {
 
     template <int NC>
     void proj_nc(int64_t t0, int64_t len, float *dst, hipStream_t ps) {
-        dim3 grid((unsigned)((len + kProjTM - 1) / kProjTM), (unsigned)(1 + q.KP), (unsigned)q.B);
-        Timed tm(0, ps);
-        if (q.groups > 1)
-            hipLaunchKernelGGL((k_proj<NC, InT, true>), grid, dim3(kThreads), 0, ps, x, dx, p.W_B, p.W_C, p.b_B,
-                               p.b_C, dst, q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len, (int)q.N);
-        else
-            hipLaunchKernelGGL((k_proj<NC, InT, false>), grid, dim3(kThreads), 0, ps, x, dx, p.W_B, p.W_C, p.b_B,
-                               p.b_C, dst, q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len, (int)q.N);
+        const int S = q.ksplit;
+        dim3 grid((unsigned)((len + kProjTM - 1) / kProjTM * S), (unsigned)(1 + q.KP), (unsigned)q.B);
+        float *part = (float *)(ws + q.ws.part);
+        const int64_t pstride = (int64_t)(q.ws.bc_half / sizeof(float));
+        {
+            Timed tm(0, ps);
+            if (q.groups > 1)
+                hipLaunchKernelGGL((k_proj<NC, InT, true>), grid, dim3(kThreads), 0, ps, x, dx, p.W_B, p.W_C, p.b_B,
+                                   p.b_C, dst, q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len, (int)q.N, S,
+                                   q.dchunk, part, pstride);
+            else
+                hipLaunchKernelGGL((k_proj<NC, InT, false>), grid, dim3(kThreads), 0, ps, x, dx, p.W_B, p.W_C,
+                                   p.b_B, p.b_C, dst, q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len, (int)q.N, S,
+                                   q.dchunk, part, pstride);
+        }
+        if (S > 1) {
+            const int64_t n = q.B * q.chunk_len * q.R;
+            Timed tm(0, ps);
+            hipLaunchKernelGGL(k_psum, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, ps, dst,
+                               (const float *)part, pstride, S, n);
+        }
     }
 
     // One pass over x (and each dx_k) computes the B and C columns of every

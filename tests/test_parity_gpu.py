@@ -139,3 +139,19 @@ def test_timing_api_counts_launches():
     assert t["scan_out"][1] == 3 and t["state_io"][1] == 1
     assert all(ms >= 0 for ms, _ in t.values()) and t["scan_out"][0] > 0
     assert binding.timing_read()["scan_out"] == (0.0, 0)      # read clears
+
+
+@pytest.mark.parametrize("in_dtype", ["f32", "bf16"])
+def test_wide_channel_sum_splits(in_dtype):
+    """D = 2112 > 2048: the projections cut the channel sum into two
+    splits (2 x 1056 channels) and add them in order; parity with the
+    oracle, and bit-identical results for every host block size."""
+    name = "stiff128k" if in_dtype == "bf16" else "mamba130m"
+    inp = gu.custom(name, batch=1, seqlen=700, d_inner=2112, n_dirs=1)
+    print(f"case wide D=2112 {in_dtype}", flush=True)
+    y, dy = gu.run(inp, seg_len=64, chunk_segs=0)
+    yo, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp)
+    gu.assert_close(y.cpu().numpy(), dy.cpu().numpy(), yo, dyo, what=f"wide D {in_dtype}")
+    for cs in (1, 3):
+        y2, dy2 = gu.run(inp, seg_len=64, chunk_segs=cs)
+        assert torch.equal(y2, y) and torch.equal(dy2, dy), cs
