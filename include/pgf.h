@@ -43,11 +43,18 @@
  *     Argument checks are synchronous and happen before any launch; on a
  *     failed check nothing is launched and the outputs are untouched.
  *     Faults inside kernels surface at the caller's next synchronisation.
+ *   - A call whose sequence spans several host blocks runs the projections
+ *     of the next block on a helper stream of the device (default priority,
+ *     created on first use and kept until the process ends), forked from
+ *     and joined back to `stream` with events: the call stays ordered with
+ *     the work on `stream` before and after it, also under stream capture.
  *   - Launches go to the device that is current on the calling thread; the
  *     stream must belong to it.
- *   - The library keeps no state between calls (except the optional
- *     launch-timing record, see pgf_timing_*), and is reentrant on distinct
- *     workspaces.  Two calls in flight on the same workspace race.
+ *   - Apart from the helper streams and the optional launch-timing record
+ *     (see pgf_timing_*) the library keeps no state between calls.  It is
+ *     reentrant on distinct workspaces (calls from several host threads
+ *     that use one device's helper enqueue one at a time).  Two calls in
+ *     flight on the same workspace race.
  *   - No C++ exception crosses this boundary.
  */
 #ifndef PGF_H_
