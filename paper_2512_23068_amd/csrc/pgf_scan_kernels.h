@@ -801,6 +801,11 @@ void k_scan(
 //   s_sc   per (t, d): Delta, u = Delta*x, dDelta_k, p_k = dDelta_k*x +
 //          Delta*dx_k, each computed once per channel instead of once per
 //          thread sharing it.
+// Every tile runs all TT steps: the slots of a short last tile hold
+// Delta = u = dDelta_k = p_k = 0, so Abar = 1 and the drive is zero, which
+// leaves h and dh_k exactly unchanged; only their output stores are
+// skipped.  With no early exit the loop keeps the state in place (an exit
+// inside the loop made the compiler copy the state on every step).
 template <int NT, int NS, int K, bool OUT, typename InT>
 __global__ __launch_bounds__(kThreads) void k_scan_sh(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A,
@@ -892,8 +897,9 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
         qt[i] = qi / DPB;
         qd[i] = (uint32_t)dj;
     }
+    int nrow = 0;        // steps of the tile held in the registers
     auto fetch = [&](int64_t tb) {
-        const int nrow = (int)(te - tb < TT ? te - tb : TT);
+        nrow = (int)(te - tb < TT ? te - tb : TT);
         const int lim4 = nrow * (R / 4) - 1;
         const floatx4 *src4 = (const floatx4 *)(rec0 + tb * R);
 #pragma unroll
@@ -923,6 +929,9 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
             const int tt = qi / DPB, j = qi % DPB;
             float delta, sw;
             discretize(xq[i], wq[i], bq[i], delta, sw);
+            const bool live = tt < nrow;
+            delta = live ? delta : 0.0f;
+            sw = live ? sw : 0.0f;
             float *o = &s_sc[tt][j][0];
             o[0] = delta;
             o[1] = delta * xq[i];
@@ -946,7 +955,6 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
 #pragma unroll 1
         for (int tt = 0; tt < TT; ++tt) {
             const int64_t t = tb + tt;
-            if (t >= te) break;
             const float *sc = &s_sc[tt][dl][0];
             const float delta = sc[0], u = sc[1];
             float dD[K], pk[K];
@@ -972,10 +980,18 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
                 const float sv = a * h[i];
                 const float gv = Af[i] * sv;
                 const float hn = fmaf(Bn, u, sv);
+                // The tangent is accumulated in place, scaled first:
+                // dh = ((a dh + g dDelta) + B p) + dB u.  Ending the chain on
+                // dh itself keeps each dh_k in one register across steps (the
+                // form a dh + (...) ends in a temporary, which this loop then
+                // copied back on every step).
 #pragma unroll
                 for (int k = 0; k < K; ++k) {
                     const float dBn = rec[(1 + k) * N + n];
-                    dh[k][i] = fmaf(a, dh[k][i], fmaf(gv, dD[k], fmaf(Bn, pk[k], dBn * u)));
+                    float v = a * dh[k][i];
+                    v = fmaf(gv, dD[k], v);
+                    v = fmaf(Bn, pk[k], v);
+                    dh[k][i] = fmaf(dBn, u, v);
                 }
                 h[i] = hn;
                 if constexpr (OUT) {
@@ -1009,7 +1025,7 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
 #pragma unroll
                     for (int q = 1; q < NS; ++q) v += src[q * OP];
                     const int64_t dc = d0 + (tid / 64) * CW + c;
-                    if (dc < D) {
+                    if (dc < D && t < te) {
                         float *base = oi == 0 ? Yb : DYb + (int64_t)(oi - 1) * dxs;
                         store_out(base, (uint32_t)t * Du + (uint32_t)dc, v);
                     }
