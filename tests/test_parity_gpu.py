@@ -33,12 +33,13 @@ def test_multi_tile_ragged(seg):
     _check(inp, f"ragged seg={seg}", seg_len=seg)
 
 
-# Every (n_per_thread, n_split) the planner can choose, for K <= 2 and K >= 4.
+# Every (n_per_thread, n_split) the planner can choose, for K <= 2 and K >= 4;
+# 605 steps end every evaluation on a partial tile of steps.
 @pytest.mark.parametrize("N,K", [(4, 1), (8, 2), (16, 1), (32, 2), (64, 1),
                                  (4, 4), (8, 8), (16, 4), (32, 8), (64, 8)])
 def test_tilings(N, K):
-    inp = gu.custom("multidir", batch=1, seqlen=600, d_inner=72, d_state=N, n_dirs=K)
-    p = binding.plan(1, 600, 72, N, K)
+    inp = gu.custom("multidir", batch=1, seqlen=605, d_inner=72, d_state=N, n_dirs=K)
+    p = binding.plan(1, 605, 72, N, K)
     _check(inp, f"N={N} K={K} nt={p['n_per_thread']} ns={p['n_split']}")
 
 
