@@ -190,8 +190,8 @@ int pgf_plan(const pgf_params *p, pgf_plan_info *info);
  *   y  : device, [B,L,D] f32                    (fully overwritten)
  *   dy : device, [K,B,L,D] f32                  (fully overwritten)
  *   stream : a hipStream_t (NULL = the default stream)
- * y and dy must not overlap x, dx or each other.  Returns PGF_OK or an
- * error code; see the conventions above. */
+ * y and dy must not overlap x, dx or each other, and the workspace none of
+ * them.  Returns PGF_OK or an error code; see the conventions above. */
 int pgf_scan_jvp(const void *x, const void *dx, const pgf_params *p,
                  float *y, float *dy, void *stream);
 
@@ -238,8 +238,9 @@ int pgf_scan_jvp2(const void *x, const void *dx, const pgf_params *p,
  * dh_in/dh_out hold [GammaA; GammaB] as [2,B,D,N].  Chaining calls through
  * the state and adding into the same gradients gives the gradients of the
  * whole sequence (up to the rounding of the additions).  y must not overlap
- * x or gy; the gradients must not overlap any other array or each other.
- * Other conventions as pgf_scan_jvp. */
+ * x or gy; the gradients must not overlap any other array or each other;
+ * the workspace must not overlap x, gy, y or the gradients.  Other
+ * conventions as pgf_scan_jvp. */
 int pgf_param_grads(const void *x, const float *gy, const pgf_params *p,
                     float *y, float *grad_A, float *grad_B, float *grad_C, void *stream);
 
@@ -285,9 +286,9 @@ int pgf_la_plan(const pgf_la_params *p, pgf_plan_info *info);
  *   q, k, g      [B,H,L,dk]        v   [B,H,L,dv]                 (read)
  *   dq, dk, dg   [K,B,H,L,dk]      dv  [K,B,H,L,dv]               (read)
  *   o            [B,H,L,dv]        do_ [K,B,H,L,dv]   (fully overwritten)
- * o and do_ must not overlap any input or each other.  Conventions as
- * pgf_scan_jvp (asynchronous on stream, checks before any launch, current
- * device). */
+ * o and do_ must not overlap any input or each other, and the workspace
+ * none of them.  Conventions as pgf_scan_jvp (asynchronous on stream,
+ * checks before any launch, current device). */
 int pgf_la_scan_jvp(const float *q, const float *k, const float *v, const float *g,
                     const float *dq, const float *dk, const float *dv, const float *dg,
                     const pgf_la_params *p, float *o, float *do_, void *stream);

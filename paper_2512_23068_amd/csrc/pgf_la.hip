@@ -547,7 +547,8 @@ extern "C" int pgf_la_scan_jvp(const float *q, const float *k, const float *v, c
         const void *ins[8] = {q, k, v, g, dq, dk, dv, dg};
         const size_t sz[8] = {nk, nk, nv, nk, nk * pl.K, nk * pl.K, nv * pl.K, nk * pl.K};
         for (int i = 0; i < 8; ++i)
-            if (la::overlap(o, nv, ins[i], sz[i]) || la::overlap(do_, nv * pl.K, ins[i], sz[i]))
+            if (la::overlap(o, nv, ins[i], sz[i]) || la::overlap(do_, nv * pl.K, ins[i], sz[i]) ||
+                la::overlap(p->workspace, pl.total, ins[i], sz[i]))
                 return PGF_ERR_INVALID_ARG;
         if (la::overlap(o, nv, do_, nv * pl.K) || la::overlap(o, nv, p->workspace, pl.total) ||
             la::overlap(do_, nv * pl.K, p->workspace, pl.total))

@@ -33,7 +33,8 @@ int scan_common(const void *x, const void *dx, const pgf_params *p, float *y, fl
         if (overlap(y, by, x, bx) || overlap(y, by, dx, bdx) || overlap(dy, bdy, x, bx) ||
             overlap(dy, bdy, dx, bdx) || overlap(y, by, dy, bdy))
             return PGF_ERR_INVALID_ARG;
-        if (overlap(p->workspace, q.ws.total, y, by) || overlap(p->workspace, q.ws.total, dy, bdy))
+        if (overlap(p->workspace, q.ws.total, y, by) || overlap(p->workspace, q.ws.total, dy, bdy) ||
+            overlap(p->workspace, q.ws.total, x, bx) || overlap(p->workspace, q.ws.total, dx, bdx))
             return PGF_ERR_INVALID_ARG;
         if (order == 2 && (overlap(d2y, by, x, bx) || overlap(d2y, by, dx, bdx) || overlap(d2y, by, y, by) ||
                            overlap(d2y, by, dy, bdy) || overlap(d2y, by, p->workspace, q.ws.total)))
@@ -71,7 +72,8 @@ int param_common(const void *x, const float *gy, const pgf_params *p, float *y, 
     }
     if (q.L > 0) {
         if (!x || !gy || !y) return PGF_ERR_INVALID_ARG;
-        if (overlap(y, by, x, bx) || overlap(y, by, gy, bg) || overlap(y, by, p->workspace, bw))
+        if (overlap(y, by, x, bx) || overlap(y, by, gy, bg) || overlap(y, by, p->workspace, bw) ||
+            overlap(p->workspace, bw, x, bx) || overlap(p->workspace, bw, gy, bg))
             return PGF_ERR_INVALID_ARG;
         for (int i = 0; i < 3; ++i)
             if (overlap(grads[i], bp, x, bx) || overlap(grads[i], bp, gy, bg) || overlap(grads[i], bp, y, by))

@@ -126,6 +126,9 @@ def test_scan_rejects_bad_arguments_before_launch():
     assert _call(ok, x=1 << 20, y=(1 << 20) + 64) == -1
     # dy overlapping y
     assert _call(ok, y=3 << 20, dy=(3 << 20) + 128) == -1
+    # the workspace overlapping an input
+    assert _call(ok, x=(1 << 36) + 256) == -1
+    assert _call(ok, dx=(1 << 36) - 1024) == -1
     p = _valid_params()
     p.in_dtype = 5
     assert _call(p) == -1
@@ -189,6 +192,32 @@ def test_linear_attention_plans():
             binding.la_plan(*bad)
     with pytest.raises(RuntimeError, match="INVALID_ARG"):
         binding.la_plan(1, 2, 100, 16, 64, 1, seg_len=100)
+
+
+def test_linear_attention_rejects_bad_arguments_before_launch():
+    """pgf_la_scan_jvp with fake (never dereferenced) addresses: overlapping
+    arrays fail the host-side checks, which run before any HIP call."""
+    lib = binding.lib()
+    p = binding.make_la_params(1, 2, 100, 16, 64, 1)
+    p.workspace_bytes = lib.pgf_la_workspace_bytes(ctypes.byref(p))
+    p.workspace = 1 << 36
+    v = lambda a: ctypes.c_void_p(a) if a else None
+
+    def call(**kw):
+        a = dict(q=1 << 20, k=2 << 20, v=3 << 20, g=4 << 20, dq=5 << 20, dk=6 << 20, dv=7 << 20, dg=8 << 20,
+                 o=9 << 20, do=10 << 20)
+        a.update(kw)
+        return lib.pgf_la_scan_jvp(*(v(a[n]) for n in ("q", "k", "v", "g", "dq", "dk", "dv", "dg")),
+                                   ctypes.byref(p), v(a["o"]), v(a["do"]), None)
+
+    assert call(q=0) == -1
+    assert call(o=(2 << 20) + 64) == -1            # o overlapping k
+    assert call(do=(9 << 20) + 4) == -1            # do overlapping o
+    assert call(g=(1 << 36) + 512) == -1           # the workspace overlapping g
+    ws = p.workspace
+    p.workspace = ws + 4                           # misaligned
+    assert call() == -3
+    p.workspace = ws
 
 
 def test_complex_transition_plans():
