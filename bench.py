@@ -108,22 +108,35 @@ def _sections(text):
     return out
 
 
+def _code(text):
+    """The code of a C++ source: line comments, trailing blanks and empty
+    lines dropped, so that editing a comment keeps a digest."""
+    out = []
+    for line in text.splitlines():
+        i = line.find("//")
+        line = (line if i < 0 else line[:i]).rstrip()
+        if line:
+            out.append(line)
+    return "\n".join(out)
+
+
 def source_digest(order=1):
-    """Digest of the kernel sections and the planner the counters of an
-    order (1, 2, 3, or "la" for linear attention) were taken on."""
+    """Digest of the code (comments aside) of the kernel sections and the
+    planner the counters of an order (1, 2, 3, or "la" for linear
+    attention) were taken on."""
     import hashlib
     h = hashlib.sha256()
     if order == "la":
-        with open(os.path.join(ROOT, LA_SRC), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, LA_SRC)) as f:
+            h.update(_code(f.read()).encode())
     else:
         with open(os.path.join(ROOT, SCAN_SRC)) as f:
             sec = _sections(f.read())
         for name in TRAFFIC_SECTIONS[order]:
             h.update(name.encode())
-            h.update(sec[name].encode())
-    with open(os.path.join(ROOT, PLAN_SRC), "rb") as f:
-        h.update(f.read())
+            h.update(_code(sec[name]).encode())
+    with open(os.path.join(ROOT, PLAN_SRC)) as f:
+        h.update(_code(f.read()).encode())
     return h.hexdigest()
 
 

@@ -187,9 +187,9 @@ __device__ __forceinline__ void silu_and_slope(float v, float &f, float &df) {
 // out[row][j] = sum_d X[row][d] * W[d][j], W = [W_B | W_C], on the matrix
 // cores: v_mfma_f32_16x16x4f32 computes D(16x16) += A(16x4) B(4x16) with,
 // for lane l, A[l%16][l/16], B[l/16][l%16] and D[4(l/16)+r][l%16] in
-// accumulator r.  Each wave owns 16 rows and every column; the channel
-// order of the sum is fixed (ascending blocks of 4), whatever the block of
-// rows, so outputs do not depend on how the sequence is tiled.
+// accumulator r.  Each wave owns 16 * kProjRT rows and every column; the
+// channel order of the sum is fixed (ascending blocks of 4), whatever the
+// block of rows, so outputs do not depend on how the sequence is tiled.
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 // Loads 4 consecutive input values of one row (zero from n on) as f32;
