@@ -192,32 +192,13 @@ __device__ __forceinline__ void silu_and_slope(float v, float &f, float &df) {
 // block of rows, so outputs do not depend on how the sequence is tiled.
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-// Loads 4 consecutive input values of one row (zero from n on) as f32;
-// vec: rows and the row start are 4-element aligned.
-template <typename InT>
-__device__ __forceinline__ floatx4 load4(const InT *__restrict__ row, int64_t d, int64_t n, bool vec);
-template <>
-__device__ __forceinline__ floatx4 load4<float>(const float *__restrict__ row, int64_t d, int64_t n, bool vec) {
+// Loads 4 consecutive values of one f32 row (zero from n on); vec: rows
+// and the row start are 4-element aligned.
+__device__ __forceinline__ floatx4 load4(const float *__restrict__ row, int64_t d, int64_t n, bool vec) {
     if (d + 4 <= n && vec) return *(const floatx4 *)(row + d);
     floatx4 v;
 #pragma unroll
     for (int i = 0; i < 4; ++i) v[i] = d + i < n ? row[d + i] : 0.0f;
-    return v;
-}
-template <>
-__device__ __forceinline__ floatx4 load4<uint16_t>(const uint16_t *__restrict__ row, int64_t d, int64_t n,
-                                                   bool vec) {
-    floatx4 v;
-    if (d + 4 <= n && vec) {
-        const uint2 u = *(const uint2 *)(row + d);
-        v[0] = __uint_as_float(u.x << 16);
-        v[1] = __uint_as_float(u.x & 0xffff0000u);
-        v[2] = __uint_as_float(u.y << 16);
-        v[3] = __uint_as_float(u.y & 0xffff0000u);
-        return v;
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = d + i < n ? __uint_as_float(((uint32_t)row[d + i]) << 16) : 0.0f;
     return v;
 }
 
@@ -227,13 +208,131 @@ __device__ __forceinline__ floatx4 load4<uint16_t>(const uint16_t *__restrict__ 
 // c*16 ..) of src[r0.., 0..dn) * W, where wload(d, j) is W[d][j] (d counted
 // from src) for j < NC (zero is returned past the matrix).
 // X tiles are staged through LDS, double-buffered, with the next channel
-// stage in flight; the channel order of the sum is fixed.
+// stage in flight; the channel order of the sum is fixed.  f32 rows run on
+// v_mfma_f32_16x16x4f32; bf16 rows on v_mfma_f32_16x16x32_bf16 (below).
 constexpr int kProjRT = 2;                      // 16-row tiles per wave
 constexpr int kProjTM = 4 * 16 * kProjRT;       // rows per block
 
-template <int NC, typename InT, class WLoad>
-__device__ __forceinline__ void xw_tiles(const InT *__restrict__ src, int64_t ld, int64_t dn, int64_t len,
-                                         int64_t r0, WLoad wload, floatx4 (&acc)[kProjRT][(NC + 15) / 16]) {
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// bf16 rows: the products x*W run exactly on the bf16 matrix cores.  W (f32)
+// is cut into three bf16 planes, hi = W with its significand truncated to 8
+// bits, mid = the same of W - hi, lo = W - hi - mid, which has at most 8
+// significant bits left, so hi + mid + lo = W exactly (for |W| above
+// 2^-100); x is bf16 already, each product of two bf16 values is exact in
+// f32, and the matrix core adds them in f32.  Per stage of 32 channels one
+// v_mfma_f32_16x16x32_bf16 per plane: lane l supplies A[l%16][8(l/16)+j]
+// and B[8(l/16)+j][l%16], j < 8, and receives D[4(l/16)+r][l%16] as the f32
+// instruction does.  X is staged raw (bf16) and W transposed per plane, so
+// every fragment is one 16-byte LDS read.
+template <int NC, class WLoad>
+__device__ __forceinline__ void xw_tiles_bf16(const uint16_t *__restrict__ src, int64_t ld, int64_t dn, int64_t len,
+                                              int64_t r0, WLoad wload, floatx4 (&acc)[kProjRT][(NC + 15) / 16]) {
+    constexpr int CT = (NC + 15) / 16;
+    constexpr int NCP = CT * 16;
+    constexpr int RT = kProjRT;
+    constexpr int TM = kProjTM;
+    constexpr int DT = 32;                       // channels per stage (one k-step)
+    constexpr int XP = DT + 8;                   // LDS row pitch in bf16 (80 bytes)
+    constexpr int XV = TM * DT / 4 / kThreads;   // 4-channel groups of X per thread per stage
+    constexpr int WE = (DT * NCP + kThreads - 1) / kThreads;
+    __shared__ __align__(16) uint16_t Xs[2][TM][XP];
+    __shared__ __align__(16) uint16_t Ws[2][3][NCP][XP];
+
+    const int tid = threadIdx.x;
+    const int wave = tid / 64, lane = tid % 64;
+    const bool vec = (ld & 3) == 0 && (((uintptr_t)src / sizeof(uint16_t)) & 3) == 0;
+    uint2 xr[XV];
+    float wr[WE];
+    auto fetch = [&](int64_t d0) {
+#pragma unroll
+        for (int i = 0; i < XV; ++i) {
+            const int e = tid + i * kThreads;
+            const int r = e / (DT / 4), c4 = e % (DT / 4);
+            const int64_t row = r0 + r, d = d0 + 4 * c4;
+            uint2 u = {0u, 0u};
+            if (row < len) {
+                const uint16_t *p = src + row * ld;
+                if (d + 4 <= dn && vec) {
+                    u = *(const uint2 *)(p + d);
+                } else {
+                    const uint32_t v0 = d < dn ? p[d] : 0u, v1 = d + 1 < dn ? p[d + 1] : 0u;
+                    const uint32_t v2 = d + 2 < dn ? p[d + 2] : 0u, v3 = d + 3 < dn ? p[d + 3] : 0u;
+                    u.x = v0 | (v1 << 16);
+                    u.y = v2 | (v3 << 16);
+                }
+            }
+            xr[i] = u;
+        }
+#pragma unroll
+        for (int i = 0; i < WE; ++i) {
+            const int e = tid + i * kThreads;
+            const int dd = e / NCP, j = e % NCP;
+            const int64_t d = d0 + dd;
+            float v = 0.0f;
+            if (e < DT * NCP && d < dn && j < NC) v = wload(d, j);
+            wr[i] = v;
+        }
+    };
+    auto stash = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < XV; ++i) {
+            const int e = tid + i * kThreads;
+            const int r = e / (DT / 4), c4 = e % (DT / 4);
+            *(uint2 *)&Xs[buf][r][4 * c4] = xr[i];
+        }
+#pragma unroll
+        for (int i = 0; i < WE; ++i) {
+            const int e = tid + i * kThreads;
+            if (e < DT * NCP) {
+                const int dd = e / NCP, j = e % NCP;
+                const float w = wr[i];
+                const float hi = __uint_as_float(__float_as_uint(w) & 0xffff0000u);
+                const float r1 = w - hi;
+                const float mid = __uint_as_float(__float_as_uint(r1) & 0xffff0000u);
+                const float lo = r1 - mid;
+                Ws[buf][0][j][dd] = (uint16_t)(__float_as_uint(hi) >> 16);
+                Ws[buf][1][j][dd] = (uint16_t)(__float_as_uint(mid) >> 16);
+                Ws[buf][2][j][dd] = (uint16_t)(__float_as_uint(lo) >> 16);
+            }
+        }
+    };
+
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int c = 0; c < CT; ++c) acc[rt][c] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    const int64_t nst = (dn + DT - 1) / DT;
+    fetch(0);
+    stash(0);
+    __syncthreads();
+    for (int64_t st = 0; st < nst; ++st) {
+        const int buf = (int)(st & 1);
+        if (st + 1 < nst) fetch((st + 1) * DT);
+        bf16x8 a[RT];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+            a[rt] = *(const bf16x8 *)&Xs[buf][wave * 16 * RT + rt * 16 + lane % 16][8 * (lane / 16)];
+#pragma unroll
+        for (int c = 0; c < CT; ++c) {
+            bf16x8 bv[3];
+#pragma unroll
+            for (int q = 0; q < 3; ++q) bv[q] = *(const bf16x8 *)&Ws[buf][q][c * 16 + lane % 16][8 * (lane / 16)];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                for (int q = 0; q < 3; ++q)
+                    acc[rt][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt], bv[q], acc[rt][c], 0, 0, 0);
+        }
+        if (st + 1 < nst) stash(buf ^ 1);
+        __syncthreads();
+    }
+}
+
+template <int NC, class WLoad>
+__device__ __forceinline__ void xw_tiles_f32(const float *__restrict__ src, int64_t ld, int64_t dn, int64_t len,
+                                             int64_t r0, WLoad wload, floatx4 (&acc)[kProjRT][(NC + 15) / 16]) {
     constexpr int CT = (NC + 15) / 16;  // 16-column tiles (zero-padded)
     constexpr int NCP = CT * 16;
     constexpr int RT = kProjRT;
@@ -247,7 +346,7 @@ __device__ __forceinline__ void xw_tiles(const InT *__restrict__ src, int64_t ld
 
     const int tid = threadIdx.x;
     const int wave = tid / 64, lane = tid % 64;
-    const bool vec = (ld & 3) == 0 && (((uintptr_t)src / sizeof(InT)) & 3) == 0;
+    const bool vec = (ld & 3) == 0 && (((uintptr_t)src / sizeof(float)) & 3) == 0;
     floatx4 xr[XV];
     float wr[WE];
     auto fetch = [&](int64_t d0) {
@@ -256,7 +355,7 @@ __device__ __forceinline__ void xw_tiles(const InT *__restrict__ src, int64_t ld
             const int e = tid + i * kThreads;          // float4 index in the tile
             const int r = e / (DT / 4), c4 = e % (DT / 4);
             const int64_t row = r0 + r;
-            xr[i] = row < len ? load4<InT>(src + row * ld, d0 + 4 * c4, dn, vec) : floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+            xr[i] = row < len ? load4(src + row * ld, d0 + 4 * c4, dn, vec) : floatx4{0.0f, 0.0f, 0.0f, 0.0f};
         }
 #pragma unroll
         for (int i = 0; i < WE; ++i) {
@@ -310,6 +409,13 @@ __device__ __forceinline__ void xw_tiles(const InT *__restrict__ src, int64_t ld
         if (st + 1 < nst) stash(buf ^ 1);
         __syncthreads();
     }
+}
+
+template <int NC, typename InT, class WLoad>
+__device__ __forceinline__ void xw_tiles(const InT *__restrict__ src, int64_t ld, int64_t dn, int64_t len,
+                                         int64_t r0, WLoad wload, floatx4 (&acc)[kProjRT][(NC + 15) / 16]) {
+    if constexpr (std::is_same<InT, uint16_t>::value) xw_tiles_bf16<NC>(src, ld, dn, len, r0, wload, acc);
+    else xw_tiles_f32<NC>(src, ld, dn, len, r0, wload, acc);
 }
 
 // Row source s = blockIdx.y: 0 -> x, 1+k -> dx_k, of batch b = blockIdx.z.
