@@ -109,9 +109,11 @@ int make_plan(const pgf_params *p, Plan *plan) {
     q.nt = (int)std::min<int64_t>(N, K >= 8 ? 4 : (K >= 4 ? 8 : 16));
     q.ns = (int)(N / q.nt);
     q.R = (int)(groups * 2 * N * (1 + q.KP));
-    // Wide channel sums are cut into splits of at most about 2048 channels,
-    // so that a projection launch has enough blocks of moderate length.
-    q.ksplit = (int)std::min<int64_t>(4, (D + 2047) / 2048);
+    // Wide f32 channel sums are cut into splits of at most about 2048
+    // channels, so that a projection launch has enough blocks of moderate
+    // length; bf16 rows (half the bytes, on the bf16 matrix cores) were
+    // faster unsplit.
+    q.ksplit = q.in_bf16 ? 1 : (int)std::min<int64_t>(4, (D + 2047) / 2048);
     q.dchunk = ((D + q.ksplit - 1) / q.ksplit + 31) / 32 * 32;
 
     // Blocks of one segment column (every channel, one segment).

@@ -144,9 +144,10 @@ def test_timing_api_counts_launches():
 
 @pytest.mark.parametrize("in_dtype", ["f32", "bf16"])
 def test_wide_channel_sum_splits(in_dtype):
-    """D = 2112 > 2048: the projections cut the channel sum into two
-    splits (2 x 1056 channels) and add them in order; parity with the
-    oracle, and bit-identical results for every host block size."""
+    """D = 2112 > 2048: f32 projections cut the channel sum into two splits
+    (2 x 1056 channels) and add them in order, bf16 ones take it whole;
+    parity with the oracle, and bit-identical results for every host block
+    size."""
     name = "stiff128k" if in_dtype == "bf16" else "mamba130m"
     inp = gu.custom(name, batch=1, seqlen=700, d_inner=2112, n_dirs=1)
     print(f"case wide D=2112 {in_dtype}", flush=True)
