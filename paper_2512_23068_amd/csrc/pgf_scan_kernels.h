@@ -926,11 +926,11 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
     constexpr int DPB = kThreads / NS;       // channels per block
     constexpr int TT = 8;                    // steps per tile
     constexpr int SCW = 2 + 2 * K;           // Delta, u, dDelta_k, p_k
-    constexpr int SCP = SCW | 1;             // odd pitch against bank conflicts
+    constexpr int SCP = (SCW + 3) / 4 * 4;   // 16-byte rows: 128-bit reads
     constexpr int RV4 = (TT * R / 4 + kThreads - 1) / kThreads;  // record float4s per thread
     constexpr int TQ = (TT * DPB + kThreads - 1) / kThreads;     // (t, d) tasks per thread
     __shared__ floatx4 s_rec4[TT * R / 4];
-    __shared__ float s_sc[TT][DPB][SCP];
+    __shared__ __align__(16) float s_sc[TT][DPB][SCP];
     const float *s_rec = (const float *)s_rec4;
     constexpr int O = 1 + K;                 // outputs per channel
     constexpr int OP = O | 1;                // odd pitch of one lane's partials
