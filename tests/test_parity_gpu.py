@@ -117,6 +117,22 @@ def test_workspace_too_small_is_rejected():
     assert torch.all(y == 7.0) and torch.all(dy == 7.0)   # outputs untouched
 
 
+def test_bf16_rows_match_f32_rows():
+    """bf16 rows take their projections on the bf16 matrix cores with W cut
+    into three bf16 planes (hi + mid + lo = W); the same values given as f32
+    rows take the f32 matrix cores.  Both form exact products summed in f32,
+    so the outputs agree to the rounding of the sums, far inside the oracle
+    bar (a dropped plane, 2^-16 relative in B and C, would not)."""
+    for N, D in ((16, 96), (64, 70)):
+        inp = gu.custom("stiff128k", seqlen=1000, d_inner=D, d_state=N)
+        y16, dy16 = gu.run(inp)
+        y32, dy32 = gu.run(inp, bf16=False)
+        ey = gu.rel_l2(y16.cpu().numpy(), y32.cpu().numpy())
+        edy = gu.rel_l2(dy16.cpu().numpy(), dy32.cpu().numpy())
+        print(f"bf16 rows vs f32 rows N={N} D={D}: y {ey:.2e} dy {edy:.2e}", flush=True)
+        assert ey < 1e-6 and edy < 1e-6, (N, D, ey, edy)
+
+
 @pytest.mark.parametrize("N,K,D", [(64, 8, 40), (32, 2, 98), (16, 4, 70)])
 def test_bf16_multi_thread_channels(N, K, D):
     """bf16 inputs through the tilings where several threads share a channel,
