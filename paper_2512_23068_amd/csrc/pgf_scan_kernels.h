@@ -411,10 +411,148 @@ __device__ __forceinline__ void xw_tiles_f32(const float *__restrict__ src, int6
     }
 }
 
+// f32 rows against 64 or more columns, where the f32 matrix cores bound the
+// projection: both operands are cut into three bf16 planes as above (x =
+// x0 + x1 + x2, W = w0 + w1 + w2, exactly) and the six products x_i w_j
+// with i + j <= 2 run on v_mfma_f32_16x16x32_bf16, in that fixed order.
+// The three dropped products are below 2^-22 of x*W, the size of the
+// rounding of an f32 product.  X is staged as f32 and cut per fragment; X
+// and the W planes have one LDS buffer each (two barriers per stage), which
+// leaves room for three blocks per CU.
+template <int NC, class WLoad>
+__device__ __forceinline__ void xw_tiles_split(const float *__restrict__ src, int64_t ld, int64_t dn, int64_t len,
+                                               int64_t r0, WLoad wload, floatx4 (&acc)[kProjRT][(NC + 15) / 16]) {
+    constexpr int CT = (NC + 15) / 16;
+    constexpr int NCP = CT * 16;
+    constexpr int RT = kProjRT;
+    constexpr int TM = kProjTM;
+    constexpr int DT = 32;                       // channels per stage (one k-step)
+    constexpr int XP = DT + 4;                   // f32 pitch of X rows (144 bytes)
+    constexpr int WP = DT + 8;                   // bf16 pitch of W rows (80 bytes)
+    constexpr int XV = TM * DT / 4 / kThreads;
+    constexpr int WE = (DT * NCP + kThreads - 1) / kThreads;
+    __shared__ __align__(16) float Xs[TM][XP];
+    __shared__ __align__(16) uint16_t Ws[3][NCP][WP];
+    typedef unsigned int uintx4 __attribute__((ext_vector_type(4)));
+
+    const int tid = threadIdx.x;
+    const int wave = tid / 64, lane = tid % 64;
+    const bool vec = (ld & 3) == 0 && (((uintptr_t)src / sizeof(float)) & 3) == 0;
+    floatx4 xr[XV];
+    float wr[WE];
+    auto fetch = [&](int64_t d0) {
+#pragma unroll
+        for (int i = 0; i < XV; ++i) {
+            const int e = tid + i * kThreads;
+            const int r = e / (DT / 4), c4 = e % (DT / 4);
+            const int64_t row = r0 + r;
+            xr[i] = row < len ? load4(src + row * ld, d0 + 4 * c4, dn, vec) : floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+        }
+#pragma unroll
+        for (int i = 0; i < WE; ++i) {
+            const int e = tid + i * kThreads;
+            const int dd = e / NCP, j = e % NCP;
+            const int64_t d = d0 + dd;
+            float v = 0.0f;
+            if (e < DT * NCP && d < dn && j < NC) v = wload(d, j);
+            wr[i] = v;
+        }
+    };
+    auto stash = [&]() {
+#pragma unroll
+        for (int i = 0; i < XV; ++i) {
+            const int e = tid + i * kThreads;
+            const int r = e / (DT / 4), c4 = e % (DT / 4);
+            *(floatx4 *)&Xs[r][4 * c4] = xr[i];
+        }
+#pragma unroll
+        for (int i = 0; i < WE; ++i) {
+            const int e = tid + i * kThreads;
+            if (e < DT * NCP) {
+                const int dd = e / NCP, j = e % NCP;
+                const float w = wr[i];
+                const float hi = __uint_as_float(__float_as_uint(w) & 0xffff0000u);
+                const float r1 = w - hi;
+                const float mid = __uint_as_float(__float_as_uint(r1) & 0xffff0000u);
+                const float lo = r1 - mid;
+                Ws[0][j][dd] = (uint16_t)(__float_as_uint(hi) >> 16);
+                Ws[1][j][dd] = (uint16_t)(__float_as_uint(mid) >> 16);
+                Ws[2][j][dd] = (uint16_t)(__float_as_uint(lo) >> 16);
+            }
+        }
+    };
+    // The three planes of 8 consecutive f32 values as bf16x8 fragments.
+    auto planes = [&](const float *v, bf16x8 (&pl)[3]) {
+        uintx4 u[3];
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+            uint32_t b[3][2];
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                const float x = v[2 * h + e];
+                const float hi = __uint_as_float(__float_as_uint(x) & 0xffff0000u);
+                const float r1 = x - hi;
+                const float mid = __uint_as_float(__float_as_uint(r1) & 0xffff0000u);
+                const float lo = r1 - mid;
+                b[0][e] = __float_as_uint(hi);
+                b[1][e] = __float_as_uint(mid);
+                b[2][e] = __float_as_uint(lo);
+            }
+#pragma unroll
+            for (int q = 0; q < 3; ++q) u[q][h] = (b[q][0] >> 16) | (b[q][1] & 0xffff0000u);
+        }
+#pragma unroll
+        for (int q = 0; q < 3; ++q) pl[q] = __builtin_bit_cast(bf16x8, u[q]);
+    };
+
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int c = 0; c < CT; ++c) acc[rt][c] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    const int64_t nst = (dn + DT - 1) / DT;
+    fetch(0);
+    stash();
+    __syncthreads();
+    for (int64_t st = 0; st < nst; ++st) {
+        if (st + 1 < nst) fetch((st + 1) * DT);
+        bf16x8 a[RT][3];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            const float *xrow = &Xs[wave * 16 * RT + rt * 16 + lane % 16][8 * (lane / 16)];
+            float v[8];
+            *(floatx4 *)&v[0] = *(const floatx4 *)xrow;
+            *(floatx4 *)&v[4] = *(const floatx4 *)(xrow + 4);
+            planes(v, a[rt]);
+        }
+#pragma unroll
+        for (int c = 0; c < CT; ++c) {
+            bf16x8 bv[3];
+#pragma unroll
+            for (int q = 0; q < 3; ++q) bv[q] = *(const bf16x8 *)&Ws[q][c * 16 + lane % 16][8 * (lane / 16)];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                acc[rt][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][0], bv[0], acc[rt][c], 0, 0, 0);
+                acc[rt][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][0], bv[1], acc[rt][c], 0, 0, 0);
+                acc[rt][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][1], bv[0], acc[rt][c], 0, 0, 0);
+                acc[rt][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][0], bv[2], acc[rt][c], 0, 0, 0);
+                acc[rt][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][1], bv[1], acc[rt][c], 0, 0, 0);
+                acc[rt][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[rt][2], bv[0], acc[rt][c], 0, 0, 0);
+            }
+        }
+        __syncthreads();
+        if (st + 1 < nst) {
+            stash();
+            __syncthreads();
+        }
+    }
+}
+
 template <int NC, typename InT, class WLoad>
 __device__ __forceinline__ void xw_tiles(const InT *__restrict__ src, int64_t ld, int64_t dn, int64_t len,
                                          int64_t r0, WLoad wload, floatx4 (&acc)[kProjRT][(NC + 15) / 16]) {
     if constexpr (std::is_same<InT, uint16_t>::value) xw_tiles_bf16<NC>(src, ld, dn, len, r0, wload, acc);
+    else if constexpr (NC >= 64) xw_tiles_split<NC>(src, ld, dn, len, r0, wload, acc);
     else xw_tiles_f32<NC>(src, ld, dn, len, r0, wload, acc);
 }
 
@@ -431,8 +569,12 @@ __device__ __forceinline__ const InT *row_source(const InT *x, const InT *dx, in
 // With S > 1 splits the channel sum is cut into S ranges of dchunk
 // channels: split 0 writes bc (with the biases), split q > 0 writes the
 // same records to part + (q-1) * part_stride, and k_psum adds them in order.
+// The 128-column forms are held to 256 VGPRs (two waves per SIMD): they
+// took 260 and ran one block per CU, which left each stage's global loads
+// exposed.  (The hint also reschedules the narrower forms, so it is not
+// given to them.)
 template <int NC, typename InT, bool GROUPED>
-__global__ __launch_bounds__(kThreads) void k_proj(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NC >= 128 ? 2 : 1))) void k_proj(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ WB,
     const float *__restrict__ WC, const float *__restrict__ bB, const float *__restrict__ bC,
     float *__restrict__ bc, int64_t Bsz, int64_t L, int64_t D, int K, int64_t t0, int64_t len, int64_t Tc,
