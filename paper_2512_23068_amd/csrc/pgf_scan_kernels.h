@@ -207,9 +207,12 @@ __device__ __forceinline__ floatx4 load4(const float *__restrict__ row, int64_t 
 // acc[rt][c] receives the 16x16 tile (rows wave*32 + rt*16 .., columns
 // c*16 ..) of src[r0.., 0..dn) * W, where wload(d, j) is W[d][j] (d counted
 // from src) for j < NC (zero is returned past the matrix).
-// X tiles are staged through LDS, double-buffered, with the next channel
-// stage in flight; the channel order of the sum is fixed.  f32 rows run on
-// v_mfma_f32_16x16x4f32; bf16 rows on v_mfma_f32_16x16x32_bf16 (below).
+// X tiles are staged through LDS with the next channel stage in flight; the
+// channel order of the sum is fixed.  Three forms (xw_tiles picks one):
+// f32 rows on v_mfma_f32_16x16x4f32 (xw_tiles_f32); bf16 rows on
+// v_mfma_f32_16x16x32_bf16 with W cut into exact bf16 planes
+// (xw_tiles_bf16); f32 rows against 64 or more columns with both operands
+// cut into planes (xw_tiles_split).
 constexpr int kProjRT = 2;                      // 16-row tiles per wave
 constexpr int kProjTM = 4 * 16 * kProjRT;       // rows per block
 
