@@ -337,7 +337,7 @@ def main():
         summarize_counters(args.workload, args.order, *args.summarize_counters, out_path=args.traffic_out)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on one GPU only; --gpus must be 1", file=sys.stderr)
+        print("bench.py: the scan runs on one GPU (no multi-GPU mode); --gpus must be 1", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
