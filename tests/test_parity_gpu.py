@@ -133,10 +133,11 @@ def test_bf16_rows_match_f32_rows():
         assert ey < 1e-6 and edy < 1e-6, (N, D, ey, edy)
 
 
-@pytest.mark.parametrize("N,K,D", [(64, 8, 40), (32, 2, 98), (16, 4, 70)])
+@pytest.mark.parametrize("N,K,D", [(64, 8, 40), (32, 2, 98), (16, 4, 70), (8, 2, 64), (4, 1, 37)])
 def test_bf16_multi_thread_channels(N, K, D):
     """bf16 inputs through the tilings where several threads share a channel,
-    with channel counts that are not multiples of 4 (scalar load paths)."""
+    and through the narrow projections (2N = 8 and 16 columns), with channel
+    counts that are not multiples of 4 (scalar load paths)."""
     inp = gu.custom("stiff128k", seqlen=900, d_inner=D, d_state=N, n_dirs=K)
     _check(inp, f"bf16 N={N} K={K} D={D}")
 
