@@ -117,6 +117,15 @@ def test_workspace_too_small_is_rejected():
     assert torch.all(y == 7.0) and torch.all(dy == 7.0)   # outputs untouched
 
 
+@pytest.mark.parametrize("N,K,D", [(64, 2, 70), (32, 1, 37)])
+def test_wide_f32_projection_ragged_channels(N, K, D):
+    """f32 rows against 2N >= 64 columns take the split-plane projection;
+    channel counts that are not multiples of 4 (scalar loads) and end in a
+    partial 32-channel stage."""
+    inp = gu.custom("multidir", batch=2, seqlen=500, d_inner=D, d_state=N, n_dirs=K)
+    _check(inp, f"wide f32 N={N} K={K} D={D}")
+
+
 def test_bf16_rows_match_f32_rows():
     """bf16 rows take their projections on the bf16 matrix cores with W cut
     into three bf16 planes (hi + mid + lo = W); the same values given as f32
