@@ -129,6 +129,26 @@ __device__ __forceinline__ void discretize2(float xv, float w, float bd, float &
     s2 = (e * r) * r * (w * w);
 }
 
+// The scan kernels read each step's record with scalar loads that are waited
+// for right after issue (a second step's record does not fit the SGPRs, and
+// scalar loads can only be waited for all together).  touch_records reads,
+// with one vector load, one float of each 128-byte line of the records of
+// steps [ps, pe) of a segment ending at te (lane l the l-th line; a tile's
+// records span at most 64 lines), so that the scalar loads of those steps
+// find them in L2.  The caller keeps the value alive (empty asm) until the
+// next tile and never uses it.  rec0 points at this channel's record of
+// step 0, Rt floats apart, R of them its own.  Used by k_scan and k_cscan;
+// the second-order and parameter-flow scans measured slower with it (their
+// output passes are tighter on registers).
+__device__ __forceinline__ float touch_records(const float *rec0, int64_t ps, int64_t pe, int64_t te, int64_t Rt,
+                                               int R) {
+    ps = ps < te ? ps : te - 1;
+    pe = pe < te ? pe : te;
+    const int64_t last = (pe - 1) * Rt + R - 1;
+    const int64_t i = ps * Rt + 32 * (int64_t)(threadIdx.x % 64);
+    return rec0[i < last ? i : last];
+}
+
 // ---------------------------------------------------------------- variants
 // Model variants of the first-order scan, selected by the VAR template
 // argument of k_scan: bit 0 (kZoh) replaces the Euler drive Delta*B*x with
@@ -893,8 +913,11 @@ void k_scan(
         for (int k = 0; k < KZ; ++k) zc[k][j] = Zb[k * vr.zs + (uint32_t)t * Du + du];
     }
 
+    float pf = 0.0f;     // records of the tile after next, touched (touch_records)
     for (int64_t tb = ts; tb < te; tb += TT) {
         float xn[TT], dxn[K][TT], zn[1 + K][TT];
+        asm volatile("" ::"v"(pf));
+        pf = touch_records(rec0, tb + 2 * TT, tb + 3 * TT, te, Rt, R);
 #pragma unroll
         for (int j = 0; j < TT; ++j) {
             const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
@@ -2008,8 +2031,11 @@ __global__ __launch_bounds__(kThreads) void k_cscan(
 #pragma unroll
         for (int k = 0; k < K; ++k) dxc[k][j] = load_in(DXb + k * dxs, (uint32_t)t * Du + du);
     }
+    float pf = 0.0f;     // records of the tile after next, touched (touch_records)
     for (int64_t tb = ts; tb < te; tb += TT) {
         float xn[TT], dxn[K][TT];
+        asm volatile("" ::"v"(pf));
+        pf = touch_records(rec0, tb + 2 * TT, tb + 3 * TT, te, R, R);
 #pragma unroll
         for (int j = 0; j < TT; ++j) {
             const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
