@@ -135,11 +135,12 @@ __device__ __forceinline__ void discretize2(float xv, float w, float bd, float &
 // with one vector load, one float of each 128-byte line of the records of
 // steps [ps, pe) of a segment ending at te (lane l the l-th line; a tile's
 // records span at most 64 lines), so that the scalar loads of those steps
-// find them in L2.  The caller keeps the value alive (empty asm) until the
-// next tile and never uses it.  rec0 points at this channel's record of
-// step 0, Rt floats apart, R of them its own.  Used by k_scan and k_cscan;
-// the second-order and parameter-flow scans measured slower with it (their
-// output passes are tighter on registers).
+// find them in L2 (k_scan touches the next tile's records, k_cscan those
+// of the tile after next).  The caller keeps the value alive (empty asm)
+// until its next tile and never uses it.  rec0 points at this channel's
+// record of step 0, Rt floats apart, R of them its own.  The second-order
+// and parameter-flow scans measured slower with it (their output passes
+// are tighter on registers) and do not use it.
 __device__ __forceinline__ float touch_records(const float *rec0, int64_t ps, int64_t pe, int64_t te, int64_t Rt,
                                                int R) {
     ps = ps < te ? ps : te - 1;
@@ -917,7 +918,7 @@ void k_scan(
     for (int64_t tb = ts; tb < te; tb += TT) {
         float xn[TT], dxn[K][TT], zn[1 + K][TT];
         asm volatile("" ::"v"(pf));
-        pf = touch_records(rec0, tb + 2 * TT, tb + 3 * TT, te, Rt, R);
+        pf = touch_records(rec0, tb + TT, tb + 2 * TT, te, Rt, R);
 #pragma unroll
         for (int j = 0; j < TT; ++j) {
             const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
