@@ -138,9 +138,9 @@ __device__ __forceinline__ void discretize2(float xv, float w, float bd, float &
 // find them in L2 (k_scan touches the next tile's records, k_cscan those
 // of the tile after next).  The caller keeps the value alive (empty asm)
 // until its next tile and never uses it.  rec0 points at this channel's
-// record of step 0, Rt floats apart, R of them its own.  The second-order
-// and parameter-flow scans measured slower with it (their output passes
-// are tighter on registers) and do not use it.
+// record of step 0, Rt floats apart, R of them its own.  Where it measured
+// slower (the second-order scan with bf16 rows, the parameter flows' output
+// pass, both tight on registers) it is left out.
 __device__ __forceinline__ float touch_records(const float *rec0, int64_t ps, int64_t pe, int64_t te, int64_t Rt,
                                                int R) {
     ps = ps < te ? ps : te - 1;
@@ -1431,8 +1431,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(OUT ? 
         vc[j] = load_in(Vb, o);
         wc[j] = load_in(Wb, o);
     }
+    float pf = 0.0f;     // records of the next tile, touched (touch_records)
     for (int64_t tb = ts; tb < te; tb += TT) {
         float xn[TT], vn[TT], wn[TT];
+        if constexpr (std::is_same<InT, float>::value) {   // (slower with bf16 rows)
+            asm volatile("" ::"v"(pf));
+            pf = touch_records(rec0, tb + TT, tb + 2 * TT, te, R, R);
+        }
 #pragma unroll
         for (int j = 0; j < TT; ++j) {
             const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
@@ -1728,8 +1733,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
         xc[j] = load_in(Xb, o);
         if constexpr (OUT) gc[j] = load_in(Gb, o);
     }
+    float pf = 0.0f;     // records of the next tile, touched (touch_records)
     for (int64_t tb = ts; tb < te; tb += TT) {
         float xn[TT], gn[TT];
+        if constexpr (!OUT) {   // (the output pass is slower with it)
+            asm volatile("" ::"v"(pf));
+            pf = touch_records(rec0, tb + TT, tb + 2 * TT, te, R, R);
+        }
 #pragma unroll
         for (int j = 0; j < TT; ++j) {
             const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
