@@ -135,8 +135,8 @@ __device__ __forceinline__ void discretize2(float xv, float w, float bd, float &
 // with one vector load, one float of each 128-byte line of the records of
 // steps [ps, pe) of a segment ending at te (lane l the l-th line; a tile's
 // records span at most 64 lines), so that the scalar loads of those steps
-// find them in L2 (k_scan touches the next tile's records, k_cscan those
-// of the tile after next).  The caller keeps the value alive (empty asm)
+// find them in L2 (each caller touches the next tile's records; two tiles
+// ahead measured slower).  The caller keeps the value alive (empty asm)
 // until its next tile and never uses it.  rec0 points at this channel's
 // record of step 0, Rt floats apart, R of them its own.  Where it measured
 // slower (the second-order scan with bf16 rows, the parameter flows' output
@@ -914,7 +914,7 @@ void k_scan(
         for (int k = 0; k < KZ; ++k) zc[k][j] = Zb[k * vr.zs + (uint32_t)t * Du + du];
     }
 
-    float pf = 0.0f;     // records of the tile after next, touched (touch_records)
+    float pf = 0.0f;     // records of the next tile, touched (touch_records)
     for (int64_t tb = ts; tb < te; tb += TT) {
         float xn[TT], dxn[K][TT], zn[1 + K][TT];
         asm volatile("" ::"v"(pf));
@@ -2042,11 +2042,11 @@ __global__ __launch_bounds__(kThreads) void k_cscan(
 #pragma unroll
         for (int k = 0; k < K; ++k) dxc[k][j] = load_in(DXb + k * dxs, (uint32_t)t * Du + du);
     }
-    float pf = 0.0f;     // records of the tile after next, touched (touch_records)
+    float pf = 0.0f;     // records of the next tile, touched (touch_records)
     for (int64_t tb = ts; tb < te; tb += TT) {
         float xn[TT], dxn[K][TT];
         asm volatile("" ::"v"(pf));
-        pf = touch_records(rec0, tb + 2 * TT, tb + 3 * TT, te, R, R);
+        pf = touch_records(rec0, tb + TT, tb + 2 * TT, te, R, R);
 #pragma unroll
         for (int j = 0; j < TT; ++j) {
             const int64_t t = tb + TT + j < te ? tb + TT + j : te - 1;
