@@ -593,12 +593,12 @@ __device__ __forceinline__ const InT *row_source(const InT *x, const InT *dx, in
 // With S > 1 splits the channel sum is cut into S ranges of dchunk
 // channels: split 0 writes bc (with the biases), split q > 0 writes the
 // same records to part + (q-1) * part_stride, and k_psum adds them in order.
-// The 128-column forms are held to 256 VGPRs (two waves per SIMD): they
+// The grouped 128-column form is held to 256 VGPRs (two waves per SIMD): it
 // took 260 and ran one block per CU, which left each stage's global loads
-// exposed.  (The hint also reschedules the narrower forms, so it is not
-// given to them.)
+// exposed.  (The hint reschedules the other forms, which measured faster
+// without it.)
 template <int NC, typename InT, bool GROUPED>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NC >= 128 ? 2 : 1))) void k_proj(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NC >= 128 && GROUPED ? 2 : 1))) void k_proj(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ WB,
     const float *__restrict__ WC, const float *__restrict__ bB, const float *__restrict__ bC,
     float *__restrict__ bc, int64_t Bsz, int64_t L, int64_t D, int K, int64_t t0, int64_t len, int64_t Tc,
