@@ -8,6 +8,7 @@ compute path: if the library is missing, every call raises.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 
@@ -192,21 +193,78 @@ def _dev_state_c(v, shape, device, name):
     return v.to(device=device, dtype=torch.complex64).contiguous()
 
 
+def _checked_workspace(workspace, nbytes, dev):
+    """The caller's workspace (a contiguous uint8 tensor on dev of at least
+    nbytes) or, when None, a new one."""
+    if workspace is None:
+        return torch.empty(max(nbytes, 1), device=dev, dtype=torch.uint8)
+    if not (isinstance(workspace, torch.Tensor) and workspace.dtype == torch.uint8 and workspace.device == dev
+            and workspace.is_contiguous()):
+        raise ValueError(f"workspace: expected a contiguous uint8 tensor on {dev}")
+    if workspace.numel() < nbytes:
+        raise ValueError(f"workspace: {workspace.numel()} bytes, the call needs {nbytes}")
+    return workspace
+
+
 def _workspace(L_, pr, workspace, dev):
     nbytes = int(L_.pgf_workspace_bytes(ctypes.byref(pr)))
     if nbytes == 0:
         _check(L_.pgf_plan(ctypes.byref(pr), ctypes.byref(PgfPlanInfo())))
-    if workspace is None or workspace.numel() < nbytes:
-        workspace = torch.empty(max(nbytes, 1), device=dev, dtype=torch.uint8)
+    workspace = _checked_workspace(workspace, nbytes, dev)
     pr.workspace, pr.workspace_bytes = workspace.data_ptr(), workspace.numel()
     return workspace
 
 
+def _check_out(t, shape, dev, name):
+    """A caller-provided output must be exactly what the kernels write: the
+    library only sees its address."""
+    if not (isinstance(t, torch.Tensor) and t.dtype == torch.float32 and t.device == dev
+            and tuple(t.shape) == tuple(shape) and t.is_contiguous()):
+        got = (tuple(t.shape), t.dtype, str(t.device), t.is_contiguous()) if isinstance(t, torch.Tensor) else type(t)
+        raise ValueError(f"{name}: expected a contiguous float32 tensor of shape {tuple(shape)} on {dev}, got {got}")
+    return t
+
+
+def _outputs(out, shapes, names, dev):
+    """Checked caller outputs, or new ones."""
+    if out is None:
+        return tuple(torch.empty(s, device=dev, dtype=torch.float32) for s in shapes)
+    if isinstance(out, torch.Tensor):
+        out = (out,)
+    out = tuple(out)
+    if len(out) != len(shapes):
+        raise ValueError(f"out: expected {len(shapes)} tensors ({', '.join(names)}), got {len(out)}")
+    return tuple(_check_out(t, s, dev, n) for t, s, n in zip(out, shapes, names))
+
+
+def _on_stream(stream, dev):
+    """Context in which the call allocates its temporaries and launches:
+    the caller's torch.cuda.Stream when given (so that the caching allocator
+    ties every temporary to the stream the kernels run on), else the current
+    stream of dev."""
+    if stream is None:
+        return contextlib.nullcontext()
+    if not isinstance(stream, torch.cuda.Stream):
+        raise ValueError("stream: expected a torch.cuda.Stream (or None for the current stream)")
+    if stream.device != dev:
+        raise ValueError(f"stream: on {stream.device}, the tensors are on {dev}")
+    return torch.cuda.stream(stream)
+
+
 def _scan(x, dx, params, order, h_in, dh_in, d2h_in, return_state, seg_len, chunk_segs, workspace, out, stream,
           drive="euler", act="identity"):
-    L_ = lib()
-    if not (x.is_cuda and dx.is_cuda):
+    if not (isinstance(x, torch.Tensor) and isinstance(dx, torch.Tensor) and x.is_cuda and dx.is_cuda):
         raise ValueError("x and dx must be device tensors")
+    if dx.device != x.device:
+        raise ValueError("x and dx must be on the same device")
+    with torch.cuda.device(x.device), _on_stream(stream, x.device):
+        return _scan_on(x, dx, params, order, h_in, dh_in, d2h_in, return_state, seg_len, chunk_segs, workspace,
+                        out, drive, act)
+
+
+def _scan_on(x, dx, params, order, h_in, dh_in, d2h_in, return_state, seg_len, chunk_segs, workspace, out, drive,
+             act):
+    L_ = lib()
     if x.dtype not in (torch.float32, torch.bfloat16) or dx.dtype != x.dtype:
         raise ValueError("x and dx must both be float32 or both bfloat16")
     if x.dim() != 3 or dx.dim() != 4 or tuple(dx.shape[1:]) != tuple(x.shape):
@@ -250,22 +308,18 @@ def _scan(x, dx, params, order, h_in, dh_in, d2h_in, return_state, seg_len, chun
             d2h_out = torch.empty((B, D, N), device=dev, dtype=torch.float32)
             pr.d2h_out = d2h_out.data_ptr()
             states = states + (d2h_out,)
-    workspace = _workspace(L_, pr, workspace, dev)
-    if out is not None:
-        outs = tuple(out)
+    if order == 2:
+        outs = _outputs(out, ((B, L, D), (K, B, L, D), (B, L, D)), ("y", "dy", "d2y"), dev)
     else:
-        outs = (torch.empty((B, L, D), device=dev, dtype=torch.float32),
-                torch.empty((K, B, L, D), device=dev, dtype=torch.float32))
-        if order == 2:
-            outs = outs + (torch.empty((B, L, D), device=dev, dtype=torch.float32),)
-    st = torch.cuda.current_stream(dev).cuda_stream if stream is None else stream
-    with torch.cuda.device(dev):   # the library launches on the current device
-        if order == 2:
-            rc = L_.pgf_scan_jvp2(_ptr(x), _ptr(dx), ctypes.byref(pr), _ptr(outs[0]), _ptr(outs[1]),
-                                  _ptr(outs[2]), ctypes.c_void_p(st))
-        else:
-            rc = L_.pgf_scan_jvp(_ptr(x), _ptr(dx), ctypes.byref(pr), _ptr(outs[0]), _ptr(outs[1]),
-                                 ctypes.c_void_p(st))
+        outs = _outputs(out, ((B, L, D), (K, B, L, D)), ("y", "dy"), dev)
+    workspace = _workspace(L_, pr, workspace, dev)
+    st = torch.cuda.current_stream(dev).cuda_stream
+    if order == 2:
+        rc = L_.pgf_scan_jvp2(_ptr(x), _ptr(dx), ctypes.byref(pr), _ptr(outs[0]), _ptr(outs[1]), _ptr(outs[2]),
+                              ctypes.c_void_p(st))
+    else:
+        rc = L_.pgf_scan_jvp(_ptr(x), _ptr(dx), ctypes.byref(pr), _ptr(outs[0]), _ptr(outs[1]),
+                             ctypes.c_void_p(st))
     _check(rc)
     return outs + states
 
@@ -315,9 +369,17 @@ def param_grads(x: torch.Tensor, gy: torch.Tensor, params: dict, *, h_in=None, g
     gradients of per-lane offsets of B and C; their sums over d are
     dl/db_B and dl/db_C.  Asynchronous on the current stream.
     """
-    L_ = lib()
-    if not (x.is_cuda and gy.is_cuda):
+    if not (isinstance(x, torch.Tensor) and isinstance(gy, torch.Tensor) and x.is_cuda and gy.is_cuda):
         raise ValueError("x and gy must be device tensors")
+    if gy.device != x.device:
+        raise ValueError("x and gy must be on the same device")
+    with torch.cuda.device(x.device), _on_stream(stream, x.device):
+        return _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len, chunk_segs, workspace,
+                               out)
+
+
+def _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len, chunk_segs, workspace, out):
+    L_ = lib()
     if x.dtype not in (torch.float32, torch.bfloat16) or gy.dtype != torch.float32:
         raise ValueError("x must be float32 or bfloat16 and gy float32")
     if x.dim() != 3 or tuple(gy.shape) != tuple(x.shape):
@@ -344,15 +406,14 @@ def param_grads(x: torch.Tensor, gy: torch.Tensor, params: dict, *, h_in=None, g
         grads = tuple(torch.zeros((D, N), device=dev, dtype=torch.float32) for _ in range(3))
     else:
         grads = tuple(grads)
-        for g in grads:
-            if not (g.is_cuda and g.dtype == torch.float32 and tuple(g.shape) == (D, N) and g.is_contiguous()):
-                raise ValueError("grads: three contiguous float32 device tensors of shape [D,N]")
+        if len(grads) != 3 or not all(isinstance(g, torch.Tensor) and g.dtype == torch.float32 and g.device == dev
+                                      and tuple(g.shape) == (D, N) and g.is_contiguous() for g in grads):
+            raise ValueError(f"grads: three contiguous float32 tensors of shape [D,N] = [{D},{N}] on {dev}")
+    y, = _outputs(out, ((B, L, D),), ("y",), dev)
     workspace = _workspace(L_, pr, workspace, dev)
-    y = out if out is not None else torch.empty((B, L, D), device=dev, dtype=torch.float32)
-    st = torch.cuda.current_stream(dev).cuda_stream if stream is None else stream
-    with torch.cuda.device(dev):
-        rc = L_.pgf_param_grads(_ptr(x), _ptr(gy), ctypes.byref(pr), _ptr(y), _ptr(grads[0]), _ptr(grads[1]),
-                                _ptr(grads[2]), ctypes.c_void_p(st))
+    st = torch.cuda.current_stream(dev).cuda_stream
+    rc = L_.pgf_param_grads(_ptr(x), _ptr(gy), ctypes.byref(pr), _ptr(y), _ptr(grads[0]), _ptr(grads[1]),
+                            _ptr(grads[2]), ctypes.c_void_p(st))
     _check(rc)
     return (y,) + grads + states
 
@@ -380,10 +441,18 @@ def la_scan_jvp(q, k, v, g, dq, dk, dv, dg, *, S_in=None, dS_in=None, return_sta
     do [K,B,H,L,dv]), plus (S_out [B,H,dk,dv], dS_out [K,B,H,dk,dv]) when
     return_state.  Asynchronous on the current stream.
     """
-    L_ = lib()
     ts = [q, k, v, g, dq, dk, dv, dg]
     if not all(isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == torch.float32 for t in ts):
         raise ValueError("q, k, v, g, dq, dk, dv, dg must be float32 device tensors")
+    if any(t.device != q.device for t in ts):
+        raise ValueError("q, k, v, g, dq, dk, dv, dg must be on one device")
+    with torch.cuda.device(q.device), _on_stream(stream, q.device):
+        return _la_scan_jvp_on(ts, S_in, dS_in, return_state, seg_len, chunk_segs, workspace, out)
+
+
+def _la_scan_jvp_on(ts, S_in, dS_in, return_state, seg_len, chunk_segs, workspace, out):
+    L_ = lib()
+    q, k, v, g, dq, dk, dv, dg = ts
     if q.dim() != 4 or dq.dim() != 5:
         raise ValueError("shapes: q, k, g [B,H,L,dk], v [B,H,L,dv], tangents with a leading K")
     B, H, L, DK = q.shape
@@ -409,17 +478,11 @@ def la_scan_jvp(q, k, v, g, dq, dk, dv, dg, *, S_in=None, dS_in=None, return_sta
     nbytes = int(L_.pgf_la_workspace_bytes(ctypes.byref(pr)))
     if nbytes == 0:
         _check(L_.pgf_la_plan(ctypes.byref(pr), ctypes.byref(PgfPlanInfo())))
-    if workspace is None or workspace.numel() < nbytes:
-        workspace = torch.empty(max(nbytes, 1), device=dev, dtype=torch.uint8)
+    o, do = _outputs(out, ((B, H, L, DV), (K, B, H, L, DV)), ("o", "do"), dev)
+    workspace = _checked_workspace(workspace, nbytes, dev)
     pr.workspace, pr.workspace_bytes = workspace.data_ptr(), workspace.numel()
-    if out is not None:
-        o, do = out
-    else:
-        o = torch.empty((B, H, L, DV), device=dev, dtype=torch.float32)
-        do = torch.empty((K, B, H, L, DV), device=dev, dtype=torch.float32)
-    st = torch.cuda.current_stream(dev).cuda_stream if stream is None else stream
-    with torch.cuda.device(dev):
-        rc = L_.pgf_la_scan_jvp(*[_ptr(t) for t in ts], ctypes.byref(pr), _ptr(o), _ptr(do), ctypes.c_void_p(st))
+    st = torch.cuda.current_stream(dev).cuda_stream
+    rc = L_.pgf_la_scan_jvp(*[_ptr(t) for t in ts], ctypes.byref(pr), _ptr(o), _ptr(do), ctypes.c_void_p(st))
     _check(rc)
     return (o, do) + states
 

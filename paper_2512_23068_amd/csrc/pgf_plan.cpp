@@ -15,6 +15,8 @@
 
 #include <algorithm>
 
+#include "pgf_scan_launch.h"
+
 namespace pgf {
 
 namespace {
@@ -27,7 +29,6 @@ constexpr int kMaxChunkSegs = 4096;
 constexpr int64_t kResidentBlocks = 1024;
 constexpr int64_t kSimds = 1024;
 constexpr int64_t kDefaultSeg = 256;
-constexpr int64_t kSeqChunk = 4096;
 constexpr int64_t kMaxChunkLen = int64_t(1) << 18;
 // Workspace caps (of 288 GB of HBM): large enough that the benchmarked
 // configurations of every order and variant run long sequences in one host
@@ -285,16 +286,28 @@ extern "C" int pgf_la_plan(const pgf_la_params *p, pgf_plan_info *info) {
     return PGF_OK;
 }
 
+namespace {
+
+// The plan, and whether the kernel tables cover it (host only).
+int plan_checked(const pgf_params *p, pgf::Plan *q) {
+    const int rc = pgf::make_plan(p, q);
+    if (rc != PGF_OK) return rc;
+    const bool ok = q->in_bf16 ? pgf::launch_supported<uint16_t>(*q, *p) : pgf::launch_supported<float>(*q, *p);
+    return ok ? PGF_OK : PGF_ERR_UNSUPPORTED;
+}
+
+}  // namespace
+
 extern "C" size_t pgf_workspace_bytes(const pgf_params *p) {
     pgf::Plan q;
-    if (pgf::make_plan(p, &q) != PGF_OK) return 0;
+    if (plan_checked(p, &q) != PGF_OK) return 0;
     return q.ws.total;
 }
 
 extern "C" int pgf_plan(const pgf_params *p, pgf_plan_info *info) {
     if (!info) return PGF_ERR_INVALID_ARG;
     pgf::Plan q;
-    const int rc = pgf::make_plan(p, &q);
+    const int rc = plan_checked(p, &q);
     if (rc != PGF_OK) return rc;
     info->n_per_thread = q.nt;
     info->n_split = q.ns;

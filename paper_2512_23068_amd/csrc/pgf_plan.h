@@ -10,6 +10,11 @@
 
 namespace pgf {
 
+// Steps per unit of a sequential host block (a block is chunk_segs units).
+// The parameter flows add their gradient partials to the running sums once
+// per unit, so the order of those additions does not depend on the blocks.
+constexpr int64_t kSeqChunk = 4096;
+
 // Offsets (bytes) of the workspace sections; each is 256-byte aligned.
 //   state   [(1+K)][B][N][D]         state carried between host blocks
 //   bc      [2][B][Tc][R]            per-step projections of two host blocks

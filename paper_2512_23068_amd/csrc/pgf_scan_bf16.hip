@@ -6,4 +6,6 @@ namespace pgf {
 template int launch<uint16_t>(const Plan &, const pgf_params &, const uint16_t *, const uint16_t *, float *, float *, float *,
                         hipStream_t, const float *, float *, float *, float *);
 
+template bool launch_supported<uint16_t>(const Plan &, const pgf_params &);
+
 }  // namespace pgf

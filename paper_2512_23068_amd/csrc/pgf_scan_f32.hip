@@ -6,4 +6,6 @@ namespace pgf {
 template int launch<float>(const Plan &, const pgf_params &, const float *, const float *, float *, float *, float *,
                         hipStream_t, const float *, float *, float *, float *);
 
+template bool launch_supported<float>(const Plan &, const pgf_params &);
+
 }  // namespace pgf

@@ -1673,14 +1673,17 @@ __global__ __launch_bounds__(kThreads) void k_carry(
 // component 0).  OUT=true: scan from the entry state in init (as k_scan) and
 // write y; the three gradient sums go to gout at the same place as the
 // entry state (the entry slot is read before it is overwritten, by the same
-// thread), or are added to gout when gadd is set (sequential evaluation:
-// gout is the running sum of the call, and end_state receives the state).
+// thread), or, when gflush > 0 (sequential evaluation: gout is the running
+// sum of the call, and end_state receives the state), are added to gout
+// every gflush steps of the sequence and at the end of the block, so that
+// the additions happen in the same order for every host block size (blocks
+// start at multiples of gflush).
 template <int NT, bool OUT, typename InT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_pscan(
     const InT *__restrict__ x, const float *__restrict__ gy, const float *__restrict__ A,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *init, int64_t ibs, int64_t igs, int64_t ics,
-    float *__restrict__ y, float *end_state, float *gout, int gadd,
+    float *__restrict__ y, float *end_state, float *gout, int64_t gflush,
     float *__restrict__ agg_h, float *__restrict__ agg_s,
     int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
     constexpr int N = NT;
@@ -1739,6 +1742,22 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
         if constexpr (!OUT) {   // (the output pass is slower with it)
             asm volatile("" ::"v"(pf));
             pf = touch_records(rec0, tb + TT, tb + 2 * TT, te, R, R);
+        } else {
+            // wave-uniform: tb is the same for every lane (gflush is a
+            // multiple of TT)
+            if (gflush && tb != ts && tb % gflush == 0) {
+                if (active) {
+                    float *ob = gout + b * ibs + d;
+#pragma unroll
+                    for (int i = 0; i < NT; ++i) {
+                        ob[i * D] += sA[i];
+                        ob[ics + i * D] += sB[i];
+                        ob[2 * ics + i * D] += sC[i];
+                    }
+                }
+#pragma unroll
+                for (int i = 0; i < NT; ++i) sA[i] = sB[i] = sC[i] = 0.0f;
+            }
         }
 #pragma unroll
         for (int j = 0; j < TT; ++j) {
@@ -1799,7 +1818,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
             }
         }
         float *ob = gout + b * ibs + g * igs + d;
-        if (gadd) {
+        if (gflush) {
 #pragma unroll
             for (int i = 0; i < NT; ++i) {
                 ob[i * D] += sA[i];
@@ -2287,8 +2306,14 @@ struct Launcher {
     float *lrw() const { return (float *)(ws + q.ws.lr); }
     float *dtw() const { return (float *)(ws + q.ws.dt); }
 
+    // Dry run: every launch function returns before enqueuing anything, so
+    // the dispatch below only reports whether a kernel exists for the plan.
+    bool dry = false;
+
     template <int NC>
-    void proj_nc(int64_t t0, int64_t len, float *dst, hipStream_t ps) {
+    void proj_nc(int64_t t0, int64_t len, int buf, hipStream_t ps) {
+        if (dry) return;
+        float *dst = bc_buf(buf);
         const int S = q.ksplit;
         dim3 grid((unsigned)((len + kProjTM - 1) / kProjTM * S), (unsigned)(1 + q.KP), (unsigned)q.B);
         float *part = (float *)(ws + q.ws.part);
@@ -2316,13 +2341,12 @@ struct Launcher {
     // channel group: 2 * groups * N columns (a power of two, checked by the
     // planner), into projection buffer buf, on stream ps.
     bool proj(int64_t t0, int64_t len, int buf, hipStream_t ps) {
-        float *dst = bc_buf(buf);
         switch (2 * q.groups * q.N) {
-            case 8: proj_nc<8>(t0, len, dst, ps); return true;
-            case 16: proj_nc<16>(t0, len, dst, ps); return true;
-            case 32: proj_nc<32>(t0, len, dst, ps); return true;
-            case 64: proj_nc<64>(t0, len, dst, ps); return true;
-            case 128: proj_nc<128>(t0, len, dst, ps); return true;
+            case 8: proj_nc<8>(t0, len, buf, ps); return true;
+            case 16: proj_nc<16>(t0, len, buf, ps); return true;
+            case 32: proj_nc<32>(t0, len, buf, ps); return true;
+            case 64: proj_nc<64>(t0, len, buf, ps); return true;
+            case 128: proj_nc<128>(t0, len, buf, ps); return true;
             default: return false;
         }
     }
@@ -2331,6 +2355,7 @@ struct Launcher {
     // direction, then Delta and dDelta_k.
     template <int RC>
     bool lowrank_rc(int64_t t0, int64_t len) {
+        if (dry) return q.K == 1 || q.K == 2;
         {
             Timed tm(0, st);
             hipLaunchKernelGGL((k_lowx<RC, InT>),
@@ -2366,6 +2391,7 @@ struct Launcher {
 
     template <int NT, int NS, int K, int VAR = 0>
     void scans(int64_t t0, int64_t len) {
+        if (dry) return;
         const unsigned gx = (unsigned)((q.D * NS + kThreads - 1) / kThreads);
         const int64_t ND = q.N * q.D;
         const Variant vr{p.D_res, p.activation, q.groups, q.D / q.groups, dtw(), q.B * q.chunk_len * q.D};
@@ -2467,6 +2493,7 @@ struct Launcher {
     // Second order: one thread per channel with all N <= 16 states.
     template <int NT>
     void scans2(int64_t t0, int64_t len) {
+        if (dry) return;
         const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
         const int64_t ND = q.N * q.D;
         if (q.seg == 0) {
@@ -2502,6 +2529,7 @@ struct Launcher {
     // Complex transition: one thread per channel with all N <= 16 lanes.
     template <int NT, int K>
     void cscans(int64_t t0, int64_t len) {
+        if (dry) return;
         const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
         const int64_t ND = q.N * q.D;
         constexpr int CP = 2 * (1 + K);
@@ -2549,13 +2577,14 @@ struct Launcher {
     // Parameter flows: one thread per channel with all N <= 16 states.
     template <int NT>
     void pscans(int64_t t0, int64_t len) {
+        if (dry) return;
         const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
         const int64_t ND = q.N * q.D;
         if (q.seg == 0) {
             Timed tm(3, st);
             hipLaunchKernelGGL((k_pscan<NT, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, gy, p.A,
                                p.w_delta, p.b_delta, bcw(), (const float *)state(), ND, (int64_t)0, q.B * ND, y,
-                               state(), gacc(), 1, (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len,
+                               state(), gacc(), kSeqChunk, (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len,
                                q.chunk_len, len, 1);
             return;
         }
@@ -2564,7 +2593,8 @@ struct Launcher {
             Timed tm(1, st);
             hipLaunchKernelGGL((k_pscan<NT, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
                                x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)nullptr, (int64_t)0,
-                               (int64_t)0, (int64_t)0, y, (float *)nullptr, (float *)nullptr, 0, agg_h(), agg_s(),
+                               (int64_t)0, (int64_t)0, y, (float *)nullptr, (float *)nullptr, (int64_t)0, agg_h(),
+                               agg_s(),
                                q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
         }
         const int64_t lanes = q.B * ND;
@@ -2577,7 +2607,7 @@ struct Launcher {
             Timed tm(3, st);
             hipLaunchKernelGGL((k_pscan<NT, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
                                x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(), (int64_t)G * 3 * ND,
-                               (int64_t)3 * ND, ND, y, (float *)nullptr, seg_in(), 0, (float *)nullptr,
+                               (int64_t)3 * ND, ND, y, (float *)nullptr, seg_in(), (int64_t)0, (float *)nullptr,
                                (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
         }
         {
@@ -2619,7 +2649,18 @@ struct Launcher {
         }
     }
 
+    // Whether every kernel the plan needs exists (no device work).
+    bool supported() {
+        dry = true;
+        const bool ok = proj(0, 0, 0, st) && (!q.rank || lowrank(0, 0)) && scan_block(0, 0);
+        dry = false;
+        return ok;
+    }
+
     int run() {
+        // Checked before anything is enqueued: the launch functions below
+        // cannot fail on a missing kernel once this has passed.
+        if (!supported()) return PGF_ERR_UNSUPPORTED;
         const int64_t lanes_all = (int64_t)q.comp * q.B * q.N * q.D;
         const unsigned gs = (unsigned)((lanes_all + kThreads - 1) / kThreads);
         const float *d2h_in = q.order == 2 ? p.d2h_in : nullptr;
@@ -2682,6 +2723,13 @@ int launch(const Plan &q, const pgf_params &p, const InT *x, const InT *dx, floa
            hipStream_t st, const float *gy, float *gA, float *gB, float *gC) {
     Launcher<InT> l{q, p, x, dx, y, dy, d2y, st, (char *)p.workspace, gy, gA, gB, gC};
     return l.run();
+}
+
+// Whether a kernel exists for every launch of the plan (host only).
+template <typename InT>
+bool launch_supported(const Plan &q, const pgf_params &p) {
+    Launcher<InT> l{q, p, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+    return l.supported();
 }
 
 }  // namespace pgf

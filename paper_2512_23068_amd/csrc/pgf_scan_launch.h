@@ -20,6 +20,13 @@ template <typename InT>
 int launch(const Plan &q, const pgf_params &p, const InT *x, const InT *dx, float *y, float *dy, float *d2y,
            hipStream_t st, const float *gy, float *gA, float *gB, float *gC);
 
+// Whether launch() has a kernel for every step of the plan (no device
+// work; the planner and the kernel tables must agree, and pgf_plan checks).
+template <typename InT>
+bool launch_supported(const Plan &q, const pgf_params &p);
+
+extern template bool launch_supported<float>(const Plan &, const pgf_params &);
+extern template bool launch_supported<uint16_t>(const Plan &, const pgf_params &);
 extern template int launch<float>(const Plan &, const pgf_params &, const float *, const float *, float *, float *,
                                   float *, hipStream_t, const float *, float *, float *, float *);
 extern template int launch<uint16_t>(const Plan &, const pgf_params &, const uint16_t *, const uint16_t *, float *,

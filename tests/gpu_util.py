@@ -1,5 +1,8 @@
 """Helpers of the GPU tests: run the HIP path on seeded inputs and compare
 with the fp64 oracle."""
+import json
+import os
+
 import numpy as np
 import torch
 
@@ -9,6 +12,10 @@ from paper_2512_23068_amd import binding, inputs
 PARAM_KEYS = ("A", "w_delta", "b_delta", "W_B", "W_C", "b_B", "b_C", "D_res", "A_im", "W_dx", "W_dt")
 INT_KEYS = ("n_groups",)
 TOL = 1e-5   # relative L2, f32 state against the fp64 oracle
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+# Where the full-size parity tests record their errors (one JSON object,
+# merged key by key; the summary under profiles/ is copied from it).
+PARITY_JSON = os.environ.get("PGF_PARITY_JSON", os.path.join(ROOT, "gpurun_out", "parity_full.json"))
 
 
 def dev():
@@ -39,8 +46,12 @@ def run(inp, bf16=None, **kw):
 
 
 def rel_l2(got, ref):
-    got = np.asarray(got, dtype=np.float64)
-    ref = np.asarray(ref, dtype=np.float64)
+    """||got - ref|| / ||ref|| in fp64; complex inputs compare both the real
+    and the imaginary parts."""
+    cplx = np.iscomplexobj(got) or np.iscomplexobj(ref)
+    dt = np.complex128 if cplx else np.float64
+    got = np.asarray(got, dtype=dt)
+    ref = np.asarray(ref, dtype=dt)
     den = np.linalg.norm(ref.ravel())
     return float(np.linalg.norm((got - ref).ravel()) / (den if den > 0 else 1.0))
 
@@ -58,3 +69,16 @@ def assert_close(y, dy, yo, dyo, tol=TOL, what=""):
 def custom(name, **kw):
     """A workload with the recipe of `name` and some sizes changed."""
     return inputs.make_inputs(inputs.get_config(name).with_(**kw))
+
+
+def record(key, values):
+    """Merges {key: values} into the parity record (PARITY_JSON)."""
+    os.makedirs(os.path.dirname(PARITY_JSON), exist_ok=True)
+    data = {}
+    if os.path.exists(PARITY_JSON):
+        with open(PARITY_JSON) as f:
+            data = json.load(f)
+    data[key] = values
+    with open(PARITY_JSON + ".tmp", "w") as f:
+        json.dump(data, f, indent=1, sort_keys=True)
+    os.replace(PARITY_JSON + ".tmp", PARITY_JSON)

@@ -286,3 +286,27 @@ def test_low_rank_plans_and_bad_fields():
         q = _copy_params(p)
         setattr(q, field, None)
         assert _call(q) == -1, field
+
+
+def test_support_matrix_has_kernels():
+    """pgf_plan succeeds only when the launch sequence has a kernel for every
+    step (a host-side dry run of the dispatch, the same check the entry
+    points make before enqueuing anything); every combination the header
+    documents as supported passes it, the others are rejected."""
+    for dt in ("f32", "bf16"):
+        for seg in (0, -1, 64):
+            for N in (4, 8, 16, 32, 64):
+                for K in (1, 2, 4, 8):
+                    p = binding.plan(2, 3000, 256, N, K, in_dtype=dt, seg_len=seg)
+                    assert p["n_per_thread"] * p["n_split"] == N
+                    # follow-on paths: one thread per channel, N <= 16, K <= 2
+                    for kw in (dict(order=2), dict(order=3), dict(drive="zoh"), dict(act="silu"),
+                               dict(complex_a=True), dict(groups=4), dict(dt_rank=48)):
+                        if kw.get("order") == 2 and K != 2:
+                            continue
+                        ok = N <= 16 and (K <= 2 or kw.get("order") == 3)
+                        if ok:
+                            binding.plan(2, 3000, 256, N, K, in_dtype=dt, seg_len=seg, **kw)
+                        else:
+                            with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+                                binding.plan(2, 3000, 256, N, K, in_dtype=dt, seg_len=seg, **kw)
