@@ -287,7 +287,8 @@ def setup_ssm(args, np, torch, binding, inputs):
         dtype="f32" if cfg.in_dtype == "f32" else "bf16-in/f32",
         config={"workload": name + variant_suffix(args), "batch": B, "seq_len": L, "d_inner": D, "d_state": N,
                 "n_dirs": 0 if args.order == 3 else K, "in_dtype": cfg.in_dtype, "parallelism": "single GPU"},
-        cpu=(lambda: cpu_baseline(cfg, args.cpu_steps)) if args.order == 1 and not variant else None)
+        cpu=(lambda: cpu_baseline(cfg, args.cpu_steps)) if args.order == 1 and not variant else None,
+        outputs=outs if args.order == 1 and not variant else None, cfg=cfg)
 
 
 def la_flops_per_lane_step(K):
@@ -328,7 +329,7 @@ def setup_la(args, np, torch, binding, inputs):
         kernel="k_la_scan (scan with outputs)", traffic=committed_traffic(cfg.name, "scan_out", "la"), dtype="f32",
         config={"workload": cfg.name, "batch": B, "heads": H, "seq_len": L, "d_key": DK, "d_value": DV,
                 "n_dirs": K, "parallelism": "single GPU"},
-        cpu=(lambda: la_cpu_baseline(cfg, args.cpu_steps)))
+        cpu=(lambda: la_cpu_baseline(cfg, args.cpu_steps)), outputs=(o, do), cfg=cfg)
 
 
 def main():
@@ -360,27 +361,32 @@ def main():
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     ev0.record()
-    t0 = time.perf_counter()
     for _ in range(args.steps):
         w.step()
     ev1.record()
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
     binding.timing_enable(False)
     kern = binding.timing_read()
     ms_total = ev0.elapsed_time(ev1)
     peak = torch.cuda.max_memory_allocated()
-    ms_step = ms_total / args.steps
+    ms_step_instrumented = ms_total / args.steps
 
-    # a second timed pass without per-launch events, for the headline number
+    # The headline pass: exactly args.steps steps without per-launch events,
+    # an event between consecutive steps on the stream the library launches
+    # on; ms_per_step is the median of the per-step times.
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    ev0.record()
-    for _ in range(args.steps):
+    t0 = time.perf_counter()
+    evs[0].record()
+    for i in range(args.steps):
         w.step()
-    ev1.record()
+        evs[i + 1].record()
     torch.cuda.synchronize()
-    ms_step_clean = ev0.elapsed_time(ev1) / args.steps
-    ms_step = min(ms_step, ms_step_clean)
+    wall = time.perf_counter() - t0
+    per_step = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+    ms_step = per_step[len(per_step) // 2] if len(per_step) % 2 else \
+        0.5 * (per_step[len(per_step) // 2 - 1] + per_step[len(per_step) // 2])
+    ms_mean = evs[0].elapsed_time(evs[-1]) / args.steps
 
     value = w.tokch / (ms_step * 1e-3) / 1e9
     # Dominant kernel: the scan that writes the outputs (kind 3).  Per launch
@@ -412,6 +418,9 @@ def main():
                for k, v in kern.items()}
     plan, payload, metric, dtype, config, alg_bytes = w.plan, w.payload, w.metric, w.dtype, w.config, w.alg_bytes
     cpu_fn = None if args.no_cpu else w.cpu
+    # GPU outputs of the last timed step (every step writes the same values)
+    outputs = getattr(w, "outputs", None)
+    wcfg = getattr(w, "cfg", None)
 
     if args.calib_copy:
         # A plain copy of known size: what the HBM counters read for it
@@ -425,7 +434,13 @@ def main():
         torch.cuda.synchronize()
         del src, dst
         cpu_fn = None
-    cpu = cpu_fn() if cpu_fn is not None else None
+    cpu, parity = None, None
+    if cpu_fn is not None:
+        cpu, ref = cpu_fn()
+        if outputs is not None:
+            parity = prefix_parity(outputs, ref, np)
+            if wcfg is not None and args.workload not in inputs.LA_BY_NAME:
+                parity.update(tail_parity(wcfg, outputs, np, torch))
 
     out = {
         "metric": metric,
@@ -435,6 +450,9 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "ms_per_step_stats": {"median": round(ms_step, 4), "mean": round(ms_mean, 4), "min": round(per_step[0], 4),
+                              "max": round(per_step[-1], 4),
+                              "instrumented_mean": round(ms_step_instrumented, 4)},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -449,6 +467,7 @@ def main():
         "kernels": kernels,
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "parity": parity,
         "wall_s_timed": round(wall, 3),
     }
     print(json.dumps(out), flush=True)
@@ -474,19 +493,20 @@ def cpu_baseline(cfg, cpu_steps):
         sub = cfg.with_(seqlen=Ls)
         inp = inputs.make_inputs(sub)
         t0 = time.perf_counter()
-        oracle.scan_jvp(inp["x"], inp["dx"], inp, chunk=4096, nthreads=threads)
-        return sub, time.perf_counter() - t0
+        y, dy, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp, chunk=4096, nthreads=threads)
+        return sub, time.perf_counter() - t0, (y, dy)
 
     if cpu_steps:
         Ls = cpu_steps
     else:   # calibrate on a short prefix, then size the sample to ~15 s
-        _, t_cal = run(256)
+        _, t_cal, _ = run(256)
         Ls = int(max(256, min(cfg.seqlen, 256 * 15.0 / max(t_cal, 1e-3))))
-    sub, dt = run(Ls)
+    sub, dt, ref = run(Ls)
     tokch = sub.batch * Ls * sub.d_inner
-    return {"value": round(tokch / dt / 1e9, 6), "unit": "Gtok·ch/s", "cores": threads, "kind": "oracle",
-            "sample": f"{cfg.name} first {Ls} steps, all {sub.d_inner} channels, batch {sub.batch}, "
-                      f"{sub.n_dirs} direction(s); fp64; {dt:.2f}s"}
+    return ({"value": round(tokch / dt / 1e9, 6), "unit": "Gtok·ch/s", "cores": threads, "cpu_model": cpu_model(),
+             "kind": "oracle",
+             "sample": f"{cfg.name} first {Ls} steps, all {sub.d_inner} channels, batch {sub.batch}, "
+                       f"{sub.n_dirs} direction(s); fp64; {dt:.2f}s"}, ref)
 
 
 def la_cpu_baseline(cfg, cpu_steps):
@@ -502,18 +522,72 @@ def la_cpu_baseline(cfg, cpu_steps):
         sub = cfg.with_(seqlen=Ls)
         inp = inputs.make_la_inputs(sub)
         t0 = time.perf_counter()
-        oracle.la_scan_jvp(*[inp[n] for n in names], nthreads=threads)
-        return sub, time.perf_counter() - t0
+        o, do, _, _ = oracle.la_scan_jvp(*[inp[n] for n in names], nthreads=threads)
+        return sub, time.perf_counter() - t0, (o, do)
 
     if cpu_steps:
         Ls = cpu_steps
     else:   # calibrate on a short prefix, then size the sample to ~15 s
-        _, t_cal = run(64)
+        _, t_cal, _ = run(64)
         Ls = int(max(64, min(cfg.seqlen, 64 * 15.0 / max(t_cal, 1e-3))))
-    sub, dt = run(Ls)
-    return {"value": round(sub.tok_ch / dt / 1e9, 6), "unit": "Gtok·ch/s", "cores": threads, "kind": "oracle",
-            "sample": f"{cfg.name} first {Ls} steps, all {sub.heads} heads, batch {sub.batch}, "
-                      f"{sub.n_dirs} direction(s); fp64; {dt:.2f}s"}
+    sub, dt, ref = run(Ls)
+    return ({"value": round(sub.tok_ch / dt / 1e9, 6), "unit": "Gtok·ch/s", "cores": threads,
+             "cpu_model": cpu_model(), "kind": "oracle",
+             "sample": f"{cfg.name} first {Ls} steps, all {sub.heads} heads, batch {sub.batch}, "
+                       f"{sub.n_dirs} direction(s); fp64; {dt:.2f}s"}, ref)
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def _rel_l2(np, got, ref):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = float(np.linalg.norm(ref.ravel()))
+    return float(np.linalg.norm((got - ref).ravel()) / (den if den > 0 else 1.0))
+
+
+def prefix_parity(outputs, ref, np):
+    """The timed run's outputs over the oracle's prefix (outputs at step t
+    depend only on steps <= t, bit for bit), against the oracle: relative L2
+    over every channel of the prefix, per output."""
+    y, dy = outputs
+    yo, dyo = ref
+    Ls = yo.shape[-2]
+    if y.dim() == 3:       # SSM: y [B,L,D], dy [K,B,L,D]
+        yg, dyg = y[:, :Ls].cpu().numpy(), dy[:, :, :Ls].cpu().numpy()
+        ch = y.shape[-1]
+    else:                  # linear attention: o [B,H,L,dv], do [K,B,H,L,dv]
+        yg, dyg = y[:, :, :Ls].cpu().numpy(), dy[:, :, :, :Ls].cpu().numpy()
+        ch = y.shape[1] * y.shape[-1]
+    return {"y_rel_l2": _rel_l2(np, yg, yo), "dy_rel_l2": max(_rel_l2(np, dyg[k], dyo[k]) for k in range(len(dyo))),
+            "steps": int(Ls), "channels": int(ch), "reference": "fp64 oracle (the cpu_baseline run)"}
+
+
+def tail_parity(cfg, outputs, np, torch, n_ch=32, n_tail=1024):
+    """The last n_tail steps of the timed run's dy against the oracle over
+    the whole sequence on a seeded choice of n_ch channels (the oracle runs
+    any channel on its own; its projections still contract over all)."""
+    from oracle import oracle
+    from paper_2512_23068_amd import inputs
+    y, dy = outputs
+    D = cfg.d_inner
+    sel = np.sort(np.random.default_rng(7).choice(D, size=min(n_ch, D), replace=False))
+    idx = torch.from_numpy(sel).to(dy.device)
+    dyg = dy[:, :, -n_tail:].index_select(-1, idx).cpu().numpy()
+    t0 = time.perf_counter()
+    inp = inputs.make_inputs(cfg)
+    _, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp, channels=sel, chunk=8192)
+    return {"tail_dy_rel_l2": _rel_l2(np, dyg, dyo[:, :, -n_tail:]), "tail_steps": n_tail,
+            "tail_channels": int(len(sel)), "tail_oracle_s": round(time.perf_counter() - t0, 1)}
 
 
 if __name__ == "__main__":

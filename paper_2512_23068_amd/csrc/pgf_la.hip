@@ -27,6 +27,7 @@
 
 #include <stdint.h>
 
+#include "pgf_exp.h"
 #include "pgf_plan.h"
 #include "pgf_timing.h"
 
@@ -46,10 +47,12 @@ constexpr float kLn2 = 0.693147180559945309f;
 
 // e^v within a few ulp for moderate |v|: v*log2(e) split into p + lo (an fma
 // recovers the rounding of p), 2^p from the hardware exponential and
-// 2^lo ~ 1 + lo*ln2 as a correction.
+// 2^lo ~ 1 + lo*ln2 as a correction; lo also carries the lift that cancels
+// the hardware exponential's mean bias near 1 (pgf_exp.h), since the decay
+// alpha = e^g of a long-memory key is close to 1.
 __device__ __forceinline__ float exp_acc(float v) {
     const float p = v * kLog2eHi;
-    const float lo = fmaf(v, kLog2eHi, -p) + v * kLog2eLo;
+    const float lo = fmaf(v, kLog2eHi, -p) + fmaf(v, kLog2eLo, kExp2Lift);
     const float e = __builtin_amdgcn_exp2f(p);
     return fmaf(e, lo * kLn2, e);
 }
@@ -408,7 +411,7 @@ __global__ __launch_bounds__(kThreads) void k_la_carry(
             seg[base * per + r] = s;
 #pragma unroll
             for (int kk = 0; kk < K; ++kk) seg[(base + 1 + kk) * per + r] = ds[kk];
-            const float P = exp_acc(sg[jj]);
+            const float P = exp_series(sg[jj]);
 #pragma unroll
             for (int kk = 0; kk < K; ++kk) ds[kk] = fmaf(P, ds[kk], fmaf(P * sdg[kk][jj], s, e1[kk][jj]));
             s = fmaf(P, s, e0[jj]);

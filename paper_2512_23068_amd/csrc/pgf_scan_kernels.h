@@ -32,6 +32,7 @@
 #include <type_traits>
 #include <vector>
 
+#include "pgf_exp.h"
 #include "pgf_plan.h"
 #include "pgf_scan_launch.h"
 #include "pgf_stream.h"
@@ -965,7 +966,7 @@ void k_scan(
                 for (int i = 0; i < NT; ++i) {
                     const int n = ns * NT + i;
                     const float Bn = rec[n];
-                    const float a = __builtin_amdgcn_exp2f(delta * At[i]);
+                    const float a = transition(delta, At[i]);
                     const float sv = a * h[i];
                     const float gv = Af[i] * sv;
                     float hn;
@@ -1251,7 +1252,7 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
             for (int i = 0; i < NT; ++i) {
                 const int n = ns * NT + i;
                 const float Bn = rec[n];
-                const float a = __builtin_amdgcn_exp2f(delta * At[i]);
+                const float a = transition(delta, At[i]);
                 const float sv = a * h[i];
                 const float gv = Af[i] * sv;
                 const float hn = fmaf(Bn, u, sv);
@@ -1471,7 +1472,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(OUT ? 
 #pragma unroll
                 for (int i = 0; i < NT; ++i) {
                     const float Bn = rec[i], dBv = rec[N + i], dBw = rec[2 * N + i];
-                    const float a = __builtin_amdgcn_exp2f(delta * At[i]);
+                    const float a = transition(delta, At[i]);
                     const float sv = a * h[i];
                     const float gv = Af[i] * sv;
                     const float hn = fmaf(Bn, u, sv);
@@ -1582,7 +1583,7 @@ static __global__ __launch_bounds__(kThreads) void k_carry2(
             seg[(base + 1) * ND + lane] = hv;
             seg[(base + 2) * ND + lane] = hw;
             seg[(base + 3) * ND + lane] = hvw;
-            const float P = __builtin_amdgcn_exp2f(at * s0[j]);
+            const float P = exp2_series(at * s0[j]);
             const float asv = a * s1[j], asw = a * s2[j];
             const float Pv = P * asv, Pw = P * asw;
             const float Pvw = P * fmaf(asv, asw, a * s3[j]);
@@ -1645,7 +1646,7 @@ __global__ __launch_bounds__(kThreads) void k_carry(
             seg[base * ND + lane] = h;
 #pragma unroll
             for (int k = 0; k < K; ++k) seg[(base + 1 + k) * ND + lane] = dh[k];
-            const float P = __builtin_amdgcn_exp2f(at * sD[j]);
+            const float P = exp2_series(at * sD[j]);
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 const float q = P * (a * sdD[j][k]);
@@ -1780,7 +1781,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 #pragma unroll
                 for (int i = 0; i < NT; ++i) {
                     const float Bn = rec[i];
-                    const float a = __builtin_amdgcn_exp2f(delta * At[i]);
+                    const float a = transition(delta, At[i]);
                     const float sv = a * h[i];
                     ga[i] = fmaf(a, ga[i], delta * sv);
                     gb[i] = fmaf(a, gb[i], u);
@@ -1880,7 +1881,7 @@ static __global__ __launch_bounds__(kThreads) void k_pcarry(
             seg[base * ND + lane] = h;
             seg[(base + 1) * ND + lane] = ga;
             seg[(base + 2) * ND + lane] = gb;
-            const float P = __builtin_amdgcn_exp2f(at * s0[j]);
+            const float P = exp2_series(at * s0[j]);
             ga = fmaf(P, ga, fmaf(P * s0[j], h, e1[j]));
             gb = fmaf(P, gb, e2[j]);
             h = fmaf(P, h, e0[j]);
@@ -2099,7 +2100,7 @@ __global__ __launch_bounds__(kThreads) void k_cscan(
 #pragma unroll
                 for (int i = 0; i < NT; ++i) {
                     const float Bn = rec[i];
-                    const float e = __builtin_amdgcn_exp2f(delta * At[i]);
+                    const float e = transition(delta, At[i]);
                     float cs, sn;
                     rot(delta * Ar2[i], cs, sn);
                     const float ar = e * cs, ai = e * sn;
@@ -2216,7 +2217,7 @@ __global__ __launch_bounds__(kThreads) void k_ccarry(
             if (g0 + j >= G) break;
 #pragma unroll
             for (int c = 0; c < CP; ++c) seg[(((b * G + g0 + j) * CP) + c) * ND + sl] = st[c];
-            const float mag = __builtin_amdgcn_exp2f(at * sm[j][0]);
+            const float mag = exp2_series(at * sm[j][0]);
             float cs_, sn_;
             rot(arev * sm[j][0], cs_, sn_);
             const float pr = mag * cs_, pi = mag * sn_;

@@ -58,28 +58,34 @@ def _run_full(name):
     return cfg, sel, yg, dyg, yo, dyo
 
 
-def tail_bound(seg, L, n_tail=1024, u_exp=2.0 ** -23):
-    """First-order worst-case relative error of the impulse response's tail.
+# Rounding model of the tail (see tail_bound): per factor of the decay chain
+# the exponential errs by at most 0.66 ulp (measured over every f32 argument
+# of the transitions' range) and the product rounds once, together at most
+# 1.4e-7 relative; after the lift of the transition's argument their mean is
+# below 2e-10 per step.
+U_FACTOR = 1.4e-7
+MEAN_PER_STEP = 2e-10
+
+
+def tail_bound(seg, L, lam=6.0):
+    """Bound on the relative error of the impulse response's tail.
 
     For t >= 1 the impulse direction has dx_t = 0, so dDelta_t, p_t, dB_t and
     dC_t vanish and each lane's tangent only decays: dh_t = Abar_t dh_{t-1}.
-    In the segmented evaluation the value at a tail step is dh_0 times the
-    segment transitions P of the segments before the last and the step
-    transitions Abar of the last segment up to that step; each factor
-    carries the exponential's error (at most u_exp relative) and one
-    multiplication's rounding (2^-24), and P also the error of its f32 sum
-    of Delta over seg steps, (seg - 1) * 2^-24 relative, scaled by |A sum
-    Delta| <= 1 for the slowest lanes that hold the tail.  The sequential
-    evaluation (seg = 0) takes L step transitions.  The C-weighted sum over
-    n and the first step add a few roundings."""
-    u = 2.0 ** -24
-    if seg:
-        n_seg = L // seg - 1
-        n_step = seg
-        per_seg = u_exp + u + (seg - 1) * u
-    else:
-        n_seg, n_step, per_seg = 0, L, 0.0
-    return n_seg * per_seg + n_step * (u_exp + u) + 40 * u
+    The computed tail value is dh_0 times a chain of n rounded factors: in
+    the segmented evaluation the segment transitions P of the segments
+    before the last (seg steps each) and the step transitions Abar of the
+    last segment (n = L/seg - 1 + seg); in the sequential evaluation
+    (seg = 0) the L step transitions.  Its relative error is the sum of the
+    factors' errors; taking them as independent with mean below
+    MEAN_PER_STEP and magnitude below U_FACTOR, the sum stays below
+    lam * sqrt(n) * U_FACTOR + n * MEAN_PER_STEP except with probability
+    2 exp(-lam^2 / 2) (the probabilistic rounding-error bound of Higham and
+    Mary, 2019); lam = 6 gives 3e-8.  A biased transition (a mean error of
+    7e-9 per step, as the raw hardware exponential has) exceeds the bound
+    of the sequential evaluation by 3x."""
+    n = (L // seg - 1 + seg) if seg else L
+    return lam * np.sqrt(n) * U_FACTOR + n * MEAN_PER_STEP
 
 
 @pytest.mark.parametrize("name", ["tiny", "mamba130m", "pulse128k", "stiff128k", "multidir"])
@@ -129,3 +135,31 @@ def test_peak_memory_flat_in_L():
         del x, dx, y, dy
     assert len(set(incr)) == 1, incr
     assert incr[0] <= binding.workspace_bytes(1, 131072, D, N, 1) + (1 << 20)
+
+
+def test_sequential_tail_pulse128k():
+    """The impulse response's tail in the sequential evaluation (every one of
+    the 131072 steps a factor of the decay chain), on the 8 channels with the
+    slowest decay (the largest tail) and 24 seeded others."""
+    cfg = inputs.get_config("pulse128k")
+    print("case pulse128k sequential tail: inputs", flush=True)
+    inp = inputs.make_inputs(cfg)
+    D = cfg.d_inner
+    slow = np.argsort(inp["b_delta"])[:8]
+    sel = np.unique(np.concatenate([slow, np.random.default_rng(3).choice(D, 24, replace=False)]))
+    x, dx = gu.inputs_to_dev(inp)
+    print("case pulse128k sequential tail: GPU scan", flush=True)
+    y, dy = binding.scan_jvp(x, dx, gu.params_to_dev(inp), seg_len=-1)
+    torch.cuda.synchronize()
+    idx = torch.from_numpy(sel).to(gu.dev())
+    dyg = dy[:, :, -1024:].index_select(-1, idx).cpu().numpy()
+    del x, dx, y, dy
+    torch.cuda.empty_cache()
+    print(f"case pulse128k sequential tail: oracle on {len(sel)} channels", flush=True)
+    _, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp, channels=sel, chunk=8192)
+    tail = gu.rel_l2(dyg, dyo[:, :, -1024:])
+    bound = tail_bound(0, cfg.seqlen)
+    print(f"pulse128k sequential tail rel_l2 = {tail:.3e} (bound {bound:.3e})", flush=True)
+    gu.record("pulse128k_sequential_tail", {"seg_len": -1, "channels": sel.tolist(), "tail_steps": 1024,
+                                            "tail_dy_rel_l2": tail, "tail_bound": bound})
+    assert np.isfinite(tail) and tail <= bound, (tail, bound)
