@@ -73,6 +73,8 @@ extern "C" {
 #define PGF_ERR_UNSUPPORTED   -2   /* shape outside what the kernels are built for          */
 #define PGF_ERR_WORKSPACE     -3   /* workspace NULL or smaller than pgf_workspace_bytes    */
 #define PGF_ERR_HIP           -4   /* a HIP launch or runtime call failed                   */
+#define PGF_ERR_SCRATCH       -5   /* pgf_scan_jvp_noalloc: the call needs more than
+                                      PGF_SCRATCH_BYTES of workspace                       */
 
 /* dtype of x and dx. */
 #define PGF_F32   0
@@ -194,6 +196,29 @@ int pgf_plan(const pgf_params *p, pgf_plan_info *info);
  * them.  Returns PGF_OK or an error code; see the conventions above. */
 int pgf_scan_jvp(const void *x, const void *dx, const pgf_params *p,
                  float *y, float *dy, void *stream);
+
+/* For callers that cannot allocate device memory or create streams (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): pgf_scan_jvp with its workspace taken from a static device
+ * array of the library, PGF_SCRATCH_BYTES per GPU it runs on, held until
+ * the process ends.  Arguments and outputs as pgf_scan_jvp, except:
+ *   - p->workspace and p->workspace_bytes are not read;
+ *   - with chunk_segs = 0 the host blocks are sized so that the workspace
+ *     fits the scratch array; a call that cannot fit it (its state alone,
+ *     or an explicit chunk_segs too large) returns PGF_ERR_SCRATCH before
+ *     anything is launched;
+ *   - every host block runs in order on `stream` (no helper stream), and
+ *     the call records no timing events;
+ *   - the first call on a device looks up that device's array
+ *     (hipGetSymbolAddress); no call allocates, frees or creates anything.
+ * Outputs equal pgf_scan_jvp's bit for bit (results do not depend on the
+ * host-block size).  Every call on one GPU uses the same array, which keeps
+ * the last call's contents (each call writes every part of it before
+ * reading it): calls that overlap in time on one GPU race, from any stream
+ * or thread. */
+#define PGF_SCRATCH_BYTES ((size_t)256 << 20)
+int pgf_scan_jvp_noalloc(const void *x, const void *dx, const pgf_params *p,
+                         float *y, float *dy, void *stream);
 
 /* Second-order flow (App. G, the Hessian flow): along the two input
  * directions v = dx[0] and w = dx[1], the primal, both first-order flows and

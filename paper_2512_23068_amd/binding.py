@@ -61,7 +61,8 @@ class PgfPlanInfo(ctypes.Structure):
     ]
 
 
-EXPORTED = ("pgf_workspace_bytes", "pgf_plan", "pgf_scan_jvp", "pgf_scan_jvp2", "pgf_param_grads",
+EXPORTED = ("pgf_workspace_bytes", "pgf_plan", "pgf_scan_jvp", "pgf_scan_jvp_noalloc", "pgf_scan_jvp2",
+            "pgf_param_grads",
             "pgf_la_workspace_bytes", "pgf_la_plan", "pgf_la_scan_jvp", "pgf_status_string", "pgf_timing_enable",
             "pgf_timing_read")
 
@@ -84,6 +85,9 @@ def lib():
     L.pgf_scan_jvp.restype = ctypes.c_int
     L.pgf_scan_jvp.argtypes = [ctypes.c_void_p, ctypes.c_void_p, P, ctypes.c_void_p, ctypes.c_void_p,
                                ctypes.c_void_p]
+    L.pgf_scan_jvp_noalloc.restype = ctypes.c_int
+    L.pgf_scan_jvp_noalloc.argtypes = [ctypes.c_void_p, ctypes.c_void_p, P, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p]
     L.pgf_scan_jvp2.restype = ctypes.c_int
     L.pgf_scan_jvp2.argtypes = [ctypes.c_void_p, ctypes.c_void_p, P, ctypes.c_void_p, ctypes.c_void_p,
                                 ctypes.c_void_p, ctypes.c_void_p]
@@ -341,6 +345,49 @@ def scan_jvp(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_i
     """
     return _scan(x, dx, params, 1, h_in, dh_in, None, return_state, seg_len, chunk_segs, workspace, out, stream,
                  drive, act)
+
+
+def scan_jvp_noalloc(x: torch.Tensor, dx: torch.Tensor, params: dict, out, *, h_in=None, dh_in=None, seg_len=0,
+                     chunk_segs=0, stream=None, drive="euler", act="identity"):
+    """scan_jvp through pgf_scan_jvp_noalloc: the library takes its workspace
+    from a static per-GPU array (PGF_SCRATCH_BYTES) instead of the caller.
+
+    out = (y [B,L,D], dy [K,B,L,D]) float32 on the device, required; with
+    parameters and states already contiguous float32 on the device the
+    binding allocates nothing either.  Returns out.  Calls that overlap on
+    one GPU race (they share the array)."""
+    if not (isinstance(x, torch.Tensor) and isinstance(dx, torch.Tensor) and x.is_cuda and dx.is_cuda):
+        raise ValueError("x and dx must be device tensors")
+    if out is None:
+        raise ValueError("out: the caller provides y and dy")
+    with torch.cuda.device(x.device), _on_stream(stream, x.device):
+        L_ = lib()
+        if x.dtype not in (torch.float32, torch.bfloat16) or dx.dtype != x.dtype:
+            raise ValueError("x and dx must both be float32 or both bfloat16")
+        if x.dim() != 3 or dx.dim() != 4 or tuple(dx.shape[1:]) != tuple(x.shape) or dx.device != x.device:
+            raise ValueError(f"shapes: x [B,L,D], dx [K,B,L,D]; got {tuple(x.shape)}, {tuple(dx.shape)}")
+        if not (x.is_contiguous() and dx.is_contiguous()):
+            raise ValueError("x and dx must be contiguous")
+        B, L, D = x.shape
+        K = dx.shape[0]
+        dev = x.device
+        pr = make_params(B, L, D, params["A"].shape[1], K, "bf16" if x.dtype == torch.bfloat16 else "f32", seg_len,
+                         chunk_segs, 1, drive, act)
+        keep = []
+        N = _model_params(pr, params, D, dev, keep)
+        D_res = _dev_param(params.get("D_res"), (D,), dev, "D_res")
+        keep.append(D_res)
+        pr.D_res = None if D_res is None else D_res.data_ptr()
+        if params.get("A_im") is not None:
+            raise ValueError("scan_jvp_noalloc: real transitions only")
+        h_in = _dev_param(h_in, (B, D, N), dev, "h_in")
+        dh_in = _dev_param(dh_in, (K, B, D, N), dev, "dh_in")
+        pr.h_in = None if h_in is None else h_in.data_ptr()
+        pr.dh_in = None if dh_in is None else dh_in.data_ptr()
+        y, dy = _outputs(out, ((B, L, D), (K, B, L, D)), ("y", "dy"), dev)
+        st = torch.cuda.current_stream(dev).cuda_stream
+        _check(L_.pgf_scan_jvp_noalloc(_ptr(x), _ptr(dx), ctypes.byref(pr), _ptr(y), _ptr(dy), ctypes.c_void_p(st)))
+        return y, dy
 
 
 def scan_jvp2(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_in=None, d2h_in=None,

@@ -55,7 +55,7 @@ bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
 
 }  // namespace
 
-int make_plan(const pgf_params *p, Plan *plan) {
+int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
     if (!p || !plan) return PGF_ERR_INVALID_ARG;
     if (p->order < 0 || p->order > 3) return PGF_ERR_INVALID_ARG;
     const int order = p->order == 0 ? 1 : p->order;
@@ -153,7 +153,7 @@ int make_plan(const pgf_params *p, Plan *plan) {
         const size_t per_seg = (size_t)B * q.comp * (size_t)(N * D + D) * sizeof(float) +
                                (size_t)(1 + q.ksplit) * B * seg * q.R * sizeof(float) +
                                (size_t)(1 + K) * B * seg * (size_t)(rank ? q.rc + D : 0) * sizeof(float);
-        const size_t wcap = rank ? kLowRankWorkspaceCap : kWorkspaceCap;
+        const size_t wcap = ws_cap ? ws_cap : (rank ? kLowRankWorkspaceCap : kWorkspaceCap);
         const int64_t cap = std::max<int64_t>(1, (int64_t)(wcap / per_seg));
         const int64_t period = kResidentBlocks / gcd64(nblk, kResidentBlocks);
         const int64_t want = (3 * kResidentBlocks + nblk - 1) / nblk;
@@ -326,6 +326,9 @@ extern "C" const char *pgf_status_string(int s) {
         case PGF_ERR_UNSUPPORTED: return "PGF_ERR_UNSUPPORTED: shape not supported (N in {4,8,16,32,64}, K in {1,2,4,8})";
         case PGF_ERR_WORKSPACE: return "PGF_ERR_WORKSPACE: workspace missing or smaller than pgf_workspace_bytes()";
         case PGF_ERR_HIP: return "PGF_ERR_HIP: a HIP runtime call or kernel launch failed";
+        case PGF_ERR_SCRATCH:
+            return "PGF_ERR_SCRATCH: the call needs more workspace than the static scratch of "
+                   "pgf_scan_jvp_noalloc (PGF_SCRATCH_BYTES)";
         default: return "PGF: unknown status";
     }
 }

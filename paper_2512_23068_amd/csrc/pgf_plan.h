@@ -54,11 +54,15 @@ struct Plan {
     int R;               // floats per step in bc: groups * 2N(1+KP)
     int ksplit;          // channel splits S of the projections (1 up to 2048 channels)
     int64_t dchunk;      // channels per split, a multiple of 32
+    int noalloc;         // 1: run every host block in order on the caller's stream
+                         // (no helper stream) and record no timing events
     Layout ws;
 };
 
-// Validates the size fields and fills *plan.  Returns PGF_OK or an error.
-int make_plan(const pgf_params *p, Plan *plan);
+// Validates the size fields and fills *plan.  ws_cap bounds the workspace
+// that the default host-block size may take (0: the library's caps); an
+// explicit chunk_segs is not bounded.  Returns PGF_OK or an error.
+int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap = 0);
 
 // Decaying linear attention.  Workspace sections (256-byte aligned):
 //   state [(1+K)][BH][DK][DV]      state carried between host blocks (the

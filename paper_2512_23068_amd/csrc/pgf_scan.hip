@@ -4,25 +4,69 @@
 
 #include <stdint.h>
 
+#include <mutex>
+
 #include "pgf_plan.h"
 #include "pgf_scan_launch.h"
 
+// Workspace of pgf_scan_jvp_noalloc: a static device array, one per GPU the
+// library runs on, alive until the process ends.  In host code `scratch` is
+// a host-side stand-in, never a device address: the device address comes
+// from hipGetSymbolAddress (scratch_address below).
+static __device__ __align__(256) unsigned char scratch[PGF_SCRATCH_BYTES];
+
 namespace pgf {
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[kMaxDevices] = {};
+
+// The device address of this device's scratch array, looked up once per
+// device (on the first call made with it current).  nullptr on failure.
+void *scratch_address() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        g_scratch[dev] = ptr;
+    }
+    return g_scratch[dev];
+}
 
 bool overlap(const void *a, size_t na, const void *b, size_t nb) {
     const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
     return na && nb && pa < pb + nb && pb < pa + na;
 }
 
+// noalloc: the workspace is this device's static scratch array (p->workspace
+// is not read), host blocks are sized to fit it, and the call creates no
+// stream or event.
 int scan_common(const void *x, const void *dx, const pgf_params *p, float *y, float *dy, float *d2y,
-                void *stream, int order) {
+                void *stream, int order, bool noalloc = false) {
     Plan q;
-    const int rc = make_plan(p, &q);
+    const int rc = make_plan(p, &q, noalloc ? (size_t)PGF_SCRATCH_BYTES : 0);
     if (rc != PGF_OK) return rc;
     if (q.order != order) return PGF_ERR_INVALID_ARG;
     if (!p->A || !p->b_delta || !p->W_B || !p->W_C) return PGF_ERR_INVALID_ARG;
     if (q.rank ? (!p->W_dx || !p->W_dt) : !p->w_delta) return PGF_ERR_INVALID_ARG;
+    pgf_params pw = *p;
+    if (noalloc) {
+        if (q.ws.total > (size_t)PGF_SCRATCH_BYTES) return PGF_ERR_SCRATCH;
+        q.noalloc = 1;
+        pw.workspace = scratch_address();
+        pw.workspace_bytes = PGF_SCRATCH_BYTES;
+        if (!pw.workspace) return PGF_ERR_HIP;
+    }
+    p = &pw;
     if (!p->workspace || p->workspace_bytes < q.ws.total || ((uintptr_t)p->workspace & 255))
         return PGF_ERR_WORKSPACE;
     const size_t esz = q.in_bf16 ? 2 : 4;
@@ -95,6 +139,11 @@ extern "C" int pgf_param_grads(const void *x, const float *gy, const pgf_params 
 
 extern "C" int pgf_scan_jvp(const void *x, const void *dx, const pgf_params *p, float *y, float *dy, void *stream) {
     return pgf::scan_common(x, dx, p, y, dy, nullptr, stream, 1);
+}
+
+extern "C" int pgf_scan_jvp_noalloc(const void *x, const void *dx, const pgf_params *p, float *y, float *dy,
+                                    void *stream) {
+    return pgf::scan_common(x, dx, p, y, dy, nullptr, stream, 1, true);
 }
 
 extern "C" int pgf_scan_jvp2(const void *x, const void *dx, const pgf_params *p, float *y, float *dy, float *d2y,

@@ -2320,7 +2320,7 @@ struct Launcher {
         float *part = (float *)(ws + q.ws.part);
         const int64_t pstride = (int64_t)(q.ws.bc_half / sizeof(float));
         {
-            Timed tm(0, ps);
+            Timed tm(0, ps, !q.noalloc);
             if (q.groups > 1)
                 hipLaunchKernelGGL((k_proj<NC, InT, true>), grid, dim3(kThreads), 0, ps, x, dx, p.W_B, p.W_C, p.b_B,
                                    p.b_C, dst, q.B, q.L, q.D, (int)q.KP, t0, len, q.chunk_len, (int)q.N, S,
@@ -2332,7 +2332,7 @@ struct Launcher {
         }
         if (S > 1) {
             const int64_t n = q.B * q.chunk_len * q.R;
-            Timed tm(0, ps);
+            Timed tm(0, ps, !q.noalloc);
             hipLaunchKernelGGL(k_psum, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, ps, dst,
                                (const float *)part, pstride, S, n);
         }
@@ -2358,7 +2358,7 @@ struct Launcher {
     bool lowrank_rc(int64_t t0, int64_t len) {
         if (dry) return q.K == 1 || q.K == 2;
         {
-            Timed tm(0, st);
+            Timed tm(0, st, !q.noalloc);
             hipLaunchKernelGGL((k_lowx<RC, InT>),
                                dim3((unsigned)((len + kProjTM - 1) / kProjTM), (unsigned)(1 + q.K), (unsigned)q.B),
                                dim3(kThreads), 0, st, x, dx, p.W_dx, lrw(), q.B, q.L, q.D, q.rank, t0, len,
@@ -2366,7 +2366,7 @@ struct Launcher {
         }
         const int64_t ncol = (q.D + kLowCols - 1) / kLowCols;
         const dim3 grid((unsigned)(ncol * ((len + kLowRows - 1) / kLowRows)), (unsigned)q.B);
-        Timed tm(0, st);
+        Timed tm(0, st, !q.noalloc);
         if (q.K == 1)
             hipLaunchKernelGGL((k_lowdt<RC, 1>), grid, dim3(kThreads), 0, st, (const float *)lrw(), p.W_dt,
                                p.b_delta, dtw(), q.B, q.D, q.rank, len, q.chunk_len);
@@ -2398,7 +2398,7 @@ struct Launcher {
         const Variant vr{p.D_res, p.activation, q.groups, q.D / q.groups, dtw(), q.B * q.chunk_len * q.D};
         if (q.seg == 0) {
             // Sequential evaluation: one segment per block, state in place.
-            Timed tm(3, st);
+            Timed tm(3, st, !q.noalloc);
             hipLaunchKernelGGL((scan_kernel<NT, NS, K, true, InT, VAR>()), dim3(gx, 1, (unsigned)q.B), dim3(kThreads),
                                0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(), state(), ND, (int64_t)0, q.B * ND, y,
                                dy, state(), (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len,
@@ -2407,7 +2407,7 @@ struct Launcher {
         }
         const int G = (int)((len + q.seg - 1) / q.seg);
         {
-            Timed tm(1, st);
+            Timed tm(1, st, !q.noalloc);
             hipLaunchKernelGGL((scan_kernel<NT, NS, K, false, InT, VAR>()), dim3(gx, (unsigned)G, (unsigned)q.B),
                                dim3(kThreads), 0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(),
                                (const float *)nullptr, (int64_t)0, (int64_t)0, (int64_t)0, y, dy, (float *)nullptr,
@@ -2415,12 +2415,12 @@ struct Launcher {
         }
         {
             const int64_t lanes = q.B * ND;
-            Timed tm(2, st);
+            Timed tm(2, st, !q.noalloc);
             hipLaunchKernelGGL((k_carry<K>), dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0,
                                st, p.A, agg_h(), agg_s(), state(), q.B, q.D, q.N, G);
         }
         {
-            Timed tm(3, st);
+            Timed tm(3, st, !q.noalloc);
             hipLaunchKernelGGL((scan_kernel<NT, NS, K, true, InT, VAR>()), dim3(gx, (unsigned)G, (unsigned)q.B),
                                dim3(kThreads), 0, st, x, dx, p.A, p.w_delta, p.b_delta, bcw(), seg_in(),
                                (int64_t)G * (1 + K) * ND, (int64_t)(1 + K) * ND, ND, y, dy, (float *)nullptr,
@@ -2498,7 +2498,7 @@ struct Launcher {
         const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
         const int64_t ND = q.N * q.D;
         if (q.seg == 0) {
-            Timed tm(3, st);
+            Timed tm(3, st, !q.noalloc);
             hipLaunchKernelGGL((k_scan2<NT, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, dx, p.A,
                                p.w_delta, p.b_delta, bcw(), state(), ND, (int64_t)0, q.B * ND, y, dy, d2y, state(),
                                (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, len, 1);
@@ -2506,7 +2506,7 @@ struct Launcher {
         }
         const int G = (int)((len + q.seg - 1) / q.seg);
         {
-            Timed tm(1, st);
+            Timed tm(1, st, !q.noalloc);
             hipLaunchKernelGGL((k_scan2<NT, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
                                x, dx, p.A, p.w_delta, p.b_delta, bcw(), (const float *)nullptr, (int64_t)0, (int64_t)0,
                                (int64_t)0, y, dy, d2y, (float *)nullptr, agg_h(), agg_s(), q.B, q.L, q.D, t0, len,
@@ -2514,12 +2514,12 @@ struct Launcher {
         }
         {
             const int64_t lanes = q.B * ND;
-            Timed tm(2, st);
+            Timed tm(2, st, !q.noalloc);
             hipLaunchKernelGGL(k_carry2, dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
                                p.A, agg_h(), agg_s(), state(), q.B, q.D, q.N, G);
         }
         {
-            Timed tm(3, st);
+            Timed tm(3, st, !q.noalloc);
             hipLaunchKernelGGL((k_scan2<NT, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
                                x, dx, p.A, p.w_delta, p.b_delta, bcw(), seg_in(), (int64_t)G * 4 * ND, (int64_t)4 * ND,
                                ND, y, dy, d2y, (float *)nullptr, (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0,
@@ -2535,7 +2535,7 @@ struct Launcher {
         const int64_t ND = q.N * q.D;
         constexpr int CP = 2 * (1 + K);
         if (q.seg == 0) {
-            Timed tm(3, st);
+            Timed tm(3, st, !q.noalloc);
             hipLaunchKernelGGL((k_cscan<NT, K, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, dx,
                                p.A, p.A_im, p.w_delta, p.b_delta, bcw(), (const float *)state(), ND, (int64_t)0,
                                q.B * ND, y, dy, state(), (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len,
@@ -2544,7 +2544,7 @@ struct Launcher {
         }
         const int G = (int)((len + q.seg - 1) / q.seg);
         {
-            Timed tm(1, st);
+            Timed tm(1, st, !q.noalloc);
             hipLaunchKernelGGL((k_cscan<NT, K, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0,
                                st, x, dx, p.A, p.A_im, p.w_delta, p.b_delta, bcw(), (const float *)nullptr,
                                (int64_t)0, (int64_t)0, (int64_t)0, y, dy, (float *)nullptr, agg_h(), agg_s(), q.B,
@@ -2552,12 +2552,12 @@ struct Launcher {
         }
         {
             const int64_t lanes = q.B * ND;
-            Timed tm(2, st);
+            Timed tm(2, st, !q.noalloc);
             hipLaunchKernelGGL((k_ccarry<K>), dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0,
                                st, p.A, p.A_im, agg_h(), (const float *)agg_s(), state(), q.B, q.D, q.N, G);
         }
         {
-            Timed tm(3, st);
+            Timed tm(3, st, !q.noalloc);
             hipLaunchKernelGGL((k_cscan<NT, K, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0,
                                st, x, dx, p.A, p.A_im, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(),
                                (int64_t)G * CP * ND, (int64_t)CP * ND, ND, y, dy, (float *)nullptr, (float *)nullptr,
@@ -2582,7 +2582,7 @@ struct Launcher {
         const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
         const int64_t ND = q.N * q.D;
         if (q.seg == 0) {
-            Timed tm(3, st);
+            Timed tm(3, st, !q.noalloc);
             hipLaunchKernelGGL((k_pscan<NT, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, gy, p.A,
                                p.w_delta, p.b_delta, bcw(), (const float *)state(), ND, (int64_t)0, q.B * ND, y,
                                state(), gacc(), kSeqChunk, (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len,
@@ -2591,7 +2591,7 @@ struct Launcher {
         }
         const int G = (int)((len + q.seg - 1) / q.seg);
         {
-            Timed tm(1, st);
+            Timed tm(1, st, !q.noalloc);
             hipLaunchKernelGGL((k_pscan<NT, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
                                x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)nullptr, (int64_t)0,
                                (int64_t)0, (int64_t)0, y, (float *)nullptr, (float *)nullptr, (int64_t)0, agg_h(),
@@ -2600,19 +2600,19 @@ struct Launcher {
         }
         const int64_t lanes = q.B * ND;
         {
-            Timed tm(2, st);
+            Timed tm(2, st, !q.noalloc);
             hipLaunchKernelGGL(k_pcarry, dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
                                p.A, agg_h(), agg_s(), state(), q.B, q.D, q.N, G);
         }
         {
-            Timed tm(3, st);
+            Timed tm(3, st, !q.noalloc);
             hipLaunchKernelGGL((k_pscan<NT, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
                                x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(), (int64_t)G * 3 * ND,
                                (int64_t)3 * ND, ND, y, (float *)nullptr, seg_in(), (int64_t)0, (float *)nullptr,
                                (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
         }
         {
-            Timed tm(2, st);
+            Timed tm(2, st, !q.noalloc);
             hipLaunchKernelGGL(k_gsum, dim3((unsigned)((3 * lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
                                (const float *)seg_in(), gacc(), q.B, ND, G);
         }
@@ -2668,7 +2668,7 @@ struct Launcher {
         float *d2h_out = q.order == 2 ? p.d2h_out : nullptr;
         const int64_t nacc = 3 * q.B * q.N * q.D;
         {
-            Timed tm(4, st);
+            Timed tm(4, st, !q.noalloc);
             hipLaunchKernelGGL(k_state_import, dim3(gs), dim3(kThreads), 0, st, p.h_in, p.dh_in, d2h_in, state(), q.B,
                                q.D, q.N, (int)q.K, q.comp, q.cplx);
             if (q.order == 3)
@@ -2680,7 +2680,7 @@ struct Launcher {
         // stream: it starts once everything enqueued before block c's scans
         // (block c-1's scans, the last readers of that buffer) is done, and
         // block c+1's scans wait for it.  Without a helper it runs in order.
-        Helper *hp = q.n_chunks > 1 ? helper() : nullptr;
+        Helper *hp = q.n_chunks > 1 && !q.noalloc ? helper() : nullptr;
         std::unique_lock<std::mutex> lk;
         if (hp) lk = std::unique_lock<std::mutex>(hp->mu);
         const hipStream_t ps = hp ? hp->side : st;
@@ -2704,13 +2704,13 @@ struct Launcher {
             if (hp && c + 1 < q.n_chunks) (void)hipStreamWaitEvent(st, hp->join, 0);
         }
         if (q.order == 3) {
-            Timed tm(4, st);
+            Timed tm(4, st, !q.noalloc);
             const int64_t nd3 = 3 * q.N * q.D;
             hipLaunchKernelGGL(k_gout, dim3((unsigned)((nd3 + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
                                (const float *)gacc(), gA, gB, gC, q.B, q.D, q.N);
         }
         if (p.h_out || p.dh_out || d2h_out) {
-            Timed tm(4, st);
+            Timed tm(4, st, !q.noalloc);
             hipLaunchKernelGGL(k_state_export, dim3(gs), dim3(kThreads), 0, st, state(), p.h_out, p.dh_out, d2h_out,
                                q.B, q.D, q.N, (int)q.K, q.comp, q.cplx);
         }

@@ -40,7 +40,8 @@ hipEvent_t take_event(Registry &r) {
 
 }  // namespace
 
-Timed::Timed(int kind, hipStream_t st) : kind_(kind), st_(st) {
+Timed::Timed(int kind, hipStream_t st, bool on) : kind_(kind), st_(st) {
+    if (!on) return;
     Registry &r = registry();
     std::lock_guard<std::mutex> lk(r.mu);
     if (!r.on) return;

@@ -10,7 +10,9 @@ namespace pgf {
 
 class Timed {
 public:
-    Timed(int kind, hipStream_t st);
+    // on = false: records nothing whatever pgf_timing_enable says (calls
+    // that may not create events).
+    Timed(int kind, hipStream_t st, bool on = true);
     ~Timed();
     Timed(const Timed &) = delete;
     Timed &operator=(const Timed &) = delete;

@@ -28,7 +28,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for code in (0, -1, -2, -3, -4):
+    for code in (0, -1, -2, -3, -4, -5):
         assert binding.status_string(code).startswith("PGF_")
     assert "unknown" in binding.status_string(7)
 
