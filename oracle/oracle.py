@@ -40,19 +40,24 @@ from scipy.special import expit
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "pgf_oracle.c")
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_DEFAULT_LIB = os.path.join(_HERE, "liboracle.so")
+# PGF_ORACLE_LIB selects another build of the same source (the sanitized
+# build of the tests).
+_LIB_PATH = os.environ.get("PGF_ORACLE_LIB") or _DEFAULT_LIB
 _lib = None
+FLAGS = ["-O2", "-fno-fast-math", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall", "-Wextra"]
 
 
-def build(verbose: bool = False) -> str:
-    """Compile the C core into oracle/liboracle.so (always recompiles)."""
-    cmd = ["gcc", "-O2", "-fno-fast-math", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
-           "-std=c11", "-Wall", "-Wextra", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
+def build(verbose: bool = False, out: str | None = None, extra: tuple = ()) -> str:
+    """Compile the C core into oracle/liboracle.so, or `out` with `extra`
+    compiler flags appended (always recompiles)."""
+    out = out or _DEFAULT_LIB
+    cmd = ["gcc", *FLAGS, *extra, "-o", out + ".tmp", _SRC, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
-    os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
-    return _LIB_PATH
+    os.replace(out + ".tmp", out)
+    return out
 
 
 def declare(lib):

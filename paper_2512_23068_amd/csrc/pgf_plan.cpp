@@ -15,8 +15,6 @@
 
 #include <algorithm>
 
-#include "pgf_scan_launch.h"
-
 namespace pgf {
 
 namespace {
@@ -283,39 +281,6 @@ extern "C" int pgf_la_plan(const pgf_la_params *p, pgf_plan_info *info) {
     info->chunk_len = q.chunk_len;
     info->n_chunks = q.n_chunks;
     info->workspace_bytes = q.total;
-    return PGF_OK;
-}
-
-namespace {
-
-// The plan, and whether the kernel tables cover it (host only).
-int plan_checked(const pgf_params *p, pgf::Plan *q) {
-    const int rc = pgf::make_plan(p, q);
-    if (rc != PGF_OK) return rc;
-    const bool ok = q->in_bf16 ? pgf::launch_supported<uint16_t>(*q, *p) : pgf::launch_supported<float>(*q, *p);
-    return ok ? PGF_OK : PGF_ERR_UNSUPPORTED;
-}
-
-}  // namespace
-
-extern "C" size_t pgf_workspace_bytes(const pgf_params *p) {
-    pgf::Plan q;
-    if (plan_checked(p, &q) != PGF_OK) return 0;
-    return q.ws.total;
-}
-
-extern "C" int pgf_plan(const pgf_params *p, pgf_plan_info *info) {
-    if (!info) return PGF_ERR_INVALID_ARG;
-    pgf::Plan q;
-    const int rc = plan_checked(p, &q);
-    if (rc != PGF_OK) return rc;
-    info->n_per_thread = q.nt;
-    info->n_split = q.ns;
-    info->seg_len = q.seg;
-    info->chunk_segs = q.chunk_segs;
-    info->chunk_len = q.chunk_len;
-    info->n_chunks = q.n_chunks;
-    info->workspace_bytes = q.ws.total;
     return PGF_OK;
 }
 

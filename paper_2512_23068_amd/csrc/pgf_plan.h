@@ -1,6 +1,7 @@
 // Host-side planning of a libpgf call: argument checks, tiling choice and
-// workspace layout.  No device access; shared by the launch code and by the
-// host-only entry points (pgf_workspace_bytes, pgf_plan).
+// workspace layout.  Plain C++ with no device access (the sanitizer tests
+// build it with g++); shared by the launch code and by the host-only entry
+// points (pgf_workspace_bytes, pgf_plan, pgf_la_*).
 #pragma once
 
 #include <stddef.h>

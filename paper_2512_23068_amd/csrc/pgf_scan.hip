@@ -132,6 +132,41 @@ int param_common(const void *x, const float *gy, const pgf_params *p, float *y, 
 }  // namespace
 }  // namespace pgf
 
+namespace pgf {
+namespace {
+
+// The plan, and whether the kernel tables cover it (host only).
+int plan_checked(const pgf_params *p, pgf::Plan *q) {
+    const int rc = pgf::make_plan(p, q);
+    if (rc != PGF_OK) return rc;
+    const bool ok = q->in_bf16 ? pgf::launch_supported<uint16_t>(*q, *p) : pgf::launch_supported<float>(*q, *p);
+    return ok ? PGF_OK : PGF_ERR_UNSUPPORTED;
+}
+
+}  // namespace
+}  // namespace pgf
+
+extern "C" size_t pgf_workspace_bytes(const pgf_params *p) {
+    pgf::Plan q;
+    if (pgf::plan_checked(p, &q) != PGF_OK) return 0;
+    return q.ws.total;
+}
+
+extern "C" int pgf_plan(const pgf_params *p, pgf_plan_info *info) {
+    if (!info) return PGF_ERR_INVALID_ARG;
+    pgf::Plan q;
+    const int rc = pgf::plan_checked(p, &q);
+    if (rc != PGF_OK) return rc;
+    info->n_per_thread = q.nt;
+    info->n_split = q.ns;
+    info->seg_len = q.seg;
+    info->chunk_segs = q.chunk_segs;
+    info->chunk_len = q.chunk_len;
+    info->n_chunks = q.n_chunks;
+    info->workspace_bytes = q.ws.total;
+    return PGF_OK;
+}
+
 extern "C" int pgf_param_grads(const void *x, const float *gy, const pgf_params *p, float *y, float *grad_A,
                                float *grad_B, float *grad_C, void *stream) {
     return pgf::param_common(x, gy, p, y, grad_A, grad_B, grad_C, stream);
