@@ -70,7 +70,7 @@ def declare(lib):
     lib.pgf_oracle_core2.restype = ctypes.c_int
     lib.pgf_oracle_core2.argtypes = [i64] * 4 + [dp] * 22 + [ctypes.c_int]
     lib.pgf_oracle_param.restype = ctypes.c_int
-    lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 13 + [ctypes.c_int]
+    lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 13 + [ctypes.c_int, ctypes.c_int]
     lib.pgf_oracle_la.restype = ctypes.c_int
     lib.pgf_oracle_la.argtypes = [i64] * 6 + [dp] * 12 + [ctypes.c_int]
     lib.pgf_oracle_core_cplx.restype = ctypes.c_int
@@ -385,11 +385,13 @@ def scan_jvp2(x, dxv, dxw, params, state=None, channels=None, chunk=None, nthrea
 
 # ------------------------------------------------------------------ parameter flows
 
-def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None):
+def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None, drive="euler"):
     """Parameter-sensitivity flows (see pgf_oracle_param).  Shapes: A [D,N];
     x, delta, gy [B,L,D]; Bm, Cm [B,L,N]; state = (h, GammaA, GammaB), each
-    [B,D,N] (zero when None).  Returns y [B,L,D], (GA, GB, GC) each [B,D,N]
-    (this call's contributions per batch row) and the exit state tuple."""
+    [B,D,N] (zero when None); drive "euler" or "zoh" (the zero-order-hold
+    drive, whose A-dependence enters GammaA).  Returns y [B,L,D], (GA, GB,
+    GC) each [B,D,N] (this call's contributions per batch row) and the exit
+    state tuple."""
     lib = _load()
     A = _f64(A)
     x, delta, gy, Bm, Cm = (_f64(a) for a in (x, delta, gy, Bm, Cm))
@@ -406,21 +408,22 @@ def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None):
     y = np.empty((B, L, D))
     G = [np.zeros((B, D, N)) for _ in range(3)]
     rc = lib.pgf_oracle_param(B, L, D, N, _dp(A), _dp(x), _dp(delta), _dp(gy), _dp(Bm), _dp(Cm),
-                              *[_dp(s_) for s_ in st], _dp(y), *[_dp(g) for g in G],
+                              *[_dp(s_) for s_ in st], _dp(y), *[_dp(g) for g in G], DRIVES[drive],
                               _threads() if nthreads is None else nthreads)
     if rc != 0:
         raise RuntimeError("pgf_oracle_param failed")
     return y, tuple(G), tuple(st)
 
 
-def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=None):
+def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=None, drive="euler"):
     """Primal output and online parameter gradients of the full model over
     L-chunks (App. E, Alg. 2).  x, gy [B,L,D]; params as scan_jvp; channels:
     optional 1-D index array of the channels d to compute (the projections
     still use every channel; state and outputs cover only those).
 
     Returns (y [B,L,Dsel], (G_A, G_B, G_C) each [Dsel,N] summed over the
-    batch, exit state (h, GammaA, GammaB) each [B,Dsel,N]).  G_A = dl/dA;
+    batch, exit state (h, GammaA, GammaB) each [B,Dsel,N]).  drive: "euler"
+    or "zoh" (see core_param).  G_A = dl/dA;
     G_B and G_C are the gradients with respect to per-lane offsets of B and
     C, so that dl/db_B = G_B.sum(0) and dl/db_C = G_C.sum(0)."""
     B, L, D = np.shape(x)
@@ -443,7 +446,7 @@ def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=N
         xs = np.ascontiguousarray(xc[..., sel])
         delta, _ = discretize(xs, xs[None], w, bd)
         gs = np.ascontiguousarray(_f64(gy[:, t0:t1])[..., sel])
-        yc, G, st = core_param(As, xs, delta, gs, Bm, Cm, st, nthreads)
+        yc, G, st = core_param(As, xs, delta, gs, Bm, Cm, st, nthreads, drive)
         y[:, t0:t1] = yc
         for i in range(3):
             tot[i] += G[i]

@@ -241,18 +241,45 @@ int pgf_oracle_core2(int64_t B, int64_t L, int64_t D, int64_t N,
  *   GC     += gy*h'                             dy/dC = h' (outer product)
  *
  * GammaA and GammaB use the state before the step (h), h' the state after.
+ *
+ * drive = 1 takes the zero-order-hold drive b = e*B*x with
+ * e = expm1(Delta*A)/A (= Delta at A = 0), as pgf_oracle_core does.  The
+ * drive then depends on A (the appendix's "A via ZOH" case), and
+ *   GammaA' = Abar*GammaA + Delta*Abar*h + (de/dA)*B*x
+ *   GammaB' = Abar*GammaB + e*x
+ *   h'      = Abar*h + e*B*x
+ * with de/dA from zoh_coef_dA.
  * Shapes (double, row-major): A [D,N]; x, delta, gy [B,L,D];
  * Bm, Cm [B,L,N]; h, gA, gB [B,D,N] (entry state in, exit state out);
  * y [B,L,D] (written); GA, GB, GC [B,D,N] (added to, per batch row).
  * Returns 0, or -1 on a bad argument.
  */
+
+/* d/dA of e(A) = expm1(Delta*A)/A: (Delta*exp(Delta*A) - e)/A.  The closed
+ * form cancels as Delta*A -> 0 (both terms tend to Delta), so below
+ * |Delta*A| = 1e-3 the Taylor series Delta^2 * sum_m (m+1)/(m+2)! (Delta*A)^m
+ * is taken instead (e = Delta * sum_k z^k/(k+1)!, differentiated term by
+ * term), to m = 8: the omitted terms are below 1e-28 relative. */
+static double zoh_coef_dA(double dl, double a)
+{
+    const double z = dl * a;
+    if (fabs(z) >= 1e-3) return (dl * exp(z) - expm1(z) / a) / a;
+    double s = 0.0, zm = 1.0, fact = 2.0;   /* fact = (m+2)! */
+    for (int m = 0; m <= 8; ++m) {
+        s += (double)(m + 1) / fact * zm;
+        zm *= z;
+        fact *= (double)(m + 3);
+    }
+    return dl * dl * s;
+}
+
 int pgf_oracle_param(int64_t B, int64_t L, int64_t D, int64_t N,
                      const double *A, const double *x, const double *delta, const double *gy,
                      const double *Bm, const double *Cm,
                      double *h, double *gA, double *gB,
-                     double *y, double *GA, double *GB, double *GC, int nthreads)
+                     double *y, double *GA, double *GB, double *GC, int drive, int nthreads)
 {
-    if (B < 0 || L < 0 || D < 0 || N <= 0) return -1;
+    if (B < 0 || L < 0 || D < 0 || N <= 0 || drive < 0 || drive > 1) return -1;
     if (!A || !h || !gA || !gB || !GA || !GB || !GC) return -1;
     if (L > 0 && (!x || !delta || !gy || !Bm || !Cm || !y)) return -1;
     const int64_t lanes = B * D;
@@ -272,11 +299,15 @@ int pgf_oracle_param(int64_t B, int64_t L, int64_t D, int64_t N,
             double yt = 0.0;
             for (int64_t n = 0; n < N; ++n) {
                 const int64_t i = (b * D + d) * N + n;
-                const double abar = exp(dl * A[d * N + n]);
+                const double a = A[d * N + n];
+                const double abar = exp(dl * a);
+                /* drive coefficient e and its derivative in A */
+                const double ec = drive ? (a != 0.0 ? expm1(dl * a) / a : dl) : dl;
+                const double ea = drive ? zoh_coef_dA(dl, a) : 0.0;
                 const double hprev = h[i];
-                const double ga = abar * gA[i] + dl * abar * hprev;
-                const double gb = abar * gB[i] + dl * xt;
-                const double hnew = abar * hprev + dl * Bm[btn + n] * xt;
+                const double ga = abar * gA[i] + dl * abar * hprev + ea * Bm[btn + n] * xt;
+                const double gb = abar * gB[i] + ec * xt;
+                const double hnew = abar * hprev + ec * Bm[btn + n] * xt;
                 h[i] = hnew; gA[i] = ga; gB[i] = gb;
                 const double Ct = Cm[btn + n];
                 yt += Ct * hnew;

@@ -112,29 +112,79 @@ def test_full_workload_channels(name):
         assert mag > 0 and np.isfinite(tail) and tail <= rec["tail_bound"], rec
 
 
-def test_peak_memory_flat_in_L():
-    """Peak allocated bytes minus the IO payload (x, dx, y, dy) do not depend
-    on L (Sec. 4.3: only the O(1) tile is differentiation overhead)."""
-    cfg = inputs.get_config("pulse128k")
+def _flat_case(kind):
+    """(call(L) -> outputs, payload bytes(L), workspace bytes) of one entry
+    point at a benchmark shape, on random device inputs."""
+    dev = gu.dev()
+    if kind == "la_scan_jvp":
+        B, H, DK, DV = 1, 32, 64, 64
+
+        def call(L):
+            ts = [torch.randn(B, H, L, d, device=dev) * s for d, s in ((DK, 0.1), (DK, 0.1), (DV, 1.0))]
+            ts.append(-torch.rand(B, H, L, DK, device=dev) * 0.05)
+            ts += [torch.randn(1, *t.shape, device=dev) * 0.1 for t in ts]
+            return ts, (lambda: binding.la_scan_jvp(*ts))
+        return call, binding.la_plan(B, H, 8192, DK, DV, 1)["workspace_bytes"]
+    name = "stiff128k" if kind == "scan_jvp_bf16" else "pulse128k"
+    cfg = inputs.get_config(name)
     D, N = cfg.d_inner, cfg.d_state
-    prm = gu.params_to_dev(inputs.make_params(cfg))
-    incr = []
+    base = inputs.make_params(cfg)
+    K = 2 if kind == "scan_jvp2" else 1
+    dt = torch.bfloat16 if kind == "scan_jvp_bf16" else torch.float32
+    lr = 48 if kind == "low_rank" else 0
+    prm = inputs.variant_params({k: base[k] for k in ("A", "w_delta", "b_delta", "W_B", "W_C")}, cfg, lowrank=lr)
+    prm = gu.params_to_dev(prm)
+    order = {"scan_jvp2": 2, "param_grads": 3}.get(kind, 1)
+    ws = binding.plan(1, 8192, D, N, K, "bf16" if dt == torch.bfloat16 else "f32", order=order,
+                      dt_rank=lr)["workspace_bytes"]
+
+    def call(L):
+        x = torch.randn(1, L, D, device=dev).to(dt)
+        if kind == "param_grads":
+            gy = torch.randn(1, L, D, device=dev)
+            return [x, gy], (lambda: binding.param_grads(x, gy, prm))
+        dx = torch.randn(K, 1, L, D, device=dev).to(dt)
+        fn = binding.scan_jvp2 if kind == "scan_jvp2" else binding.scan_jvp
+        return [x, dx], (lambda: fn(x, dx, prm))
+    return call, ws
+
+
+@pytest.mark.parametrize("kind", ["scan_jvp", "scan_jvp_bf16", "scan_jvp2", "param_grads", "low_rank",
+                                  "la_scan_jvp"])
+def test_peak_memory_flat_in_L(kind):
+    """Peak allocated bytes minus the IO payload (inputs and outputs) do not
+    depend on L (Sec. 4.3: only the O(1) tile is differentiation overhead),
+    for every entry point at a benchmark shape (pulse128k; stiff128k with
+    bf16 inputs; rwkv128k for linear attention); and the device's free
+    memory (hipMemGetInfo) drops by no more than what torch reserved, so the
+    library allocates nothing outside torch."""
+    call, ws = _flat_case(kind)
+    ins, fn = call(131072)          # warm up at the longest sequence: every kernel loaded
+    fn()
+    torch.cuda.synchronize()
+    del ins, fn
+    incr, outside = [], []
     for L in (8192, 16384, 32768, 65536, 131072):
         torch.cuda.empty_cache()
-        x = torch.randn(1, L, D, device=gu.dev(), dtype=torch.float32)
-        dx = torch.randn(1, 1, L, D, device=gu.dev(), dtype=torch.float32)
+        ins, fn = call(L)
         torch.cuda.synchronize()
         base = torch.cuda.memory_allocated()
+        free0, res0 = torch.cuda.mem_get_info()[0], torch.cuda.memory_reserved()
         torch.cuda.reset_peak_memory_stats()
-        y, dy = binding.scan_jvp(x, dx, prm)
+        outs = fn()
         torch.cuda.synchronize()
         peak = torch.cuda.max_memory_allocated()
-        outs = y.numel() * 4 + dy.numel() * 4
-        incr.append(peak - base - outs)
-        print(f"L={L}: peak-minus-payload increment {incr[-1]} bytes", flush=True)
-        del x, dx, y, dy
+        free1, res1 = torch.cuda.mem_get_info()[0], torch.cuda.memory_reserved()
+        out_bytes = sum(t.numel() * t.element_size() for t in outs)
+        incr.append(peak - base - out_bytes)
+        outside.append((free0 - free1) - (res1 - res0))
+        print(f"{kind} L={L}: peak-minus-payload {incr[-1]} bytes, outside torch {outside[-1]}", flush=True)
+        del ins, fn, outs
+    gu.record(f"flat_vram_{kind}", {"L": [8192, 16384, 32768, 65536, 131072], "peak_minus_payload": incr,
+                                    "outside_torch": outside, "workspace_bytes": ws})
     assert len(set(incr)) == 1, incr
-    assert incr[0] <= binding.workspace_bytes(1, 131072, D, N, 1) + (1 << 20)
+    assert incr[0] <= ws + (4 << 20), (incr[0], ws)
+    assert all(o <= 0 for o in outside), outside
 
 
 def test_sequential_tail_pulse128k():

@@ -16,18 +16,32 @@ PIN_TESTS = [
     lambda: pins.test_time_invariant_closed_form(),
     lambda: pins.test_one_step_adjoint_is_the_outer_product(),
     lambda: pins.test_segment_composition_closed_forms(),
+    lambda: pins.test_zoh_reverse_mode_autograd("normal"),
+    lambda: pins.test_zoh_reverse_mode_autograd("small_steps"),
+    lambda: pins.test_zoh_central_differences_along_A(False),
+    lambda: pins.test_zoh_central_differences_along_A(True),
 ]
 
 C_MUTANTS = {
-    "GammaA without its drive": ("const double ga = abar * gA[i] + dl * abar * hprev;",
-                                 "const double ga = abar * gA[i];"),
-    "GammaA drive without Abar": ("const double ga = abar * gA[i] + dl * abar * hprev;",
-                                  "const double ga = abar * gA[i] + dl * hprev;"),
-    "GammaA drive from the new state": ("const double ga = abar * gA[i] + dl * abar * hprev;",
-                                        "const double ga = abar * gA[i] + dl * (abar * hprev + dl * Bm[btn + n] * xt);"),
-    "GammaB drive carries B": ("const double gb = abar * gB[i] + dl * xt;",
-                               "const double gb = abar * gB[i] + dl * Bm[btn + n] * xt;"),
-    "GammaB without decay": ("const double gb = abar * gB[i] + dl * xt;", "const double gb = gB[i] + dl * xt;"),
+    "GammaA without its drive": ("const double ga = abar * gA[i] + dl * abar * hprev + ea * Bm[btn + n] * xt;",
+                                 "const double ga = abar * gA[i] + ea * Bm[btn + n] * xt;"),
+    "GammaA drive without Abar": ("const double ga = abar * gA[i] + dl * abar * hprev + ea * Bm[btn + n] * xt;",
+                                  "const double ga = abar * gA[i] + dl * hprev + ea * Bm[btn + n] * xt;"),
+    "GammaA drive from the new state": (
+        "const double ga = abar * gA[i] + dl * abar * hprev + ea * Bm[btn + n] * xt;",
+        "const double ga = abar * gA[i] + dl * (abar * hprev + ec * Bm[btn + n] * xt) + ea * Bm[btn + n] * xt;"),
+    "GammaA without the ZOH drive's A-derivative": (
+        "const double ga = abar * gA[i] + dl * abar * hprev + ea * Bm[btn + n] * xt;",
+        "const double ga = abar * gA[i] + dl * abar * hprev;"),
+    "ZOH de/dA series coefficient (m+2) for (m+1)": ("s += (double)(m + 1) / fact * zm;",
+                                                      "s += (double)(m + 2) / fact * zm;"),
+    "ZOH de/dA closed form without the 1/A": ("if (fabs(z) >= 1e-3) return (dl * exp(z) - expm1(z) / a) / a;",
+                                              "if (fabs(z) >= 1e-3) return dl * exp(z) - expm1(z) / a;"),
+    "GammaB drive carries B": ("const double gb = abar * gB[i] + ec * xt;",
+                               "const double gb = abar * gB[i] + ec * Bm[btn + n] * xt;"),
+    "GammaB ZOH drive taken as Delta": ("const double gb = abar * gB[i] + ec * xt;",
+                                        "const double gb = abar * gB[i] + dl * xt;"),
+    "GammaB without decay": ("const double gb = abar * gB[i] + ec * xt;", "const double gb = gB[i] + ec * xt;"),
     "G_C from the old state": ("GC[i] += g * hnew;", "GC[i] += g * hprev;"),
     "G_A without C": ("GA[i] += g * Ct * ga;", "GA[i] += g * ga;"),
     "G_B from GammaA": ("GB[i] += g * Ct * gb;", "GB[i] += g * Ct * ga;"),

@@ -27,9 +27,10 @@ def problem(seed, B=2, L=14, D=3, N=4, stiff=False):
     return p, x, gy
 
 
-def _torch_loss(p, x, gy, A, beta_B, beta_C):
+def _torch_loss(p, x, gy, A, beta_B, beta_C, drive="euler"):
     """l = sum gy*y of the selective scan as a plain torch loop, with the
-    per-lane offsets beta_B, beta_C [D,N] added to B_t and C_t."""
+    per-lane offsets beta_B, beta_C [D,N] added to B_t and C_t; drive "zoh"
+    takes b = expm1(Delta A)/A * B x (A != 0 everywhere here)."""
     xt = torch.tensor(x)
     z = xt * torch.tensor(p["w_delta"]) + torch.tensor(p["b_delta"])
     delta = torch.logaddexp(z, torch.zeros((), dtype=torch.float64))
@@ -42,7 +43,8 @@ def _torch_loss(p, x, gy, A, beta_B, beta_C):
         dl = delta[:, t, :, None]
         Bt = Bm[:, t, None, :] + beta_B
         Ct = Cm[:, t, None, :] + beta_C
-        h = torch.exp(dl * A) * h + dl * Bt * xt[:, t, :, None]
+        e = torch.expm1(dl * A) / A if drive == "zoh" else dl
+        h = torch.exp(dl * A) * h + e * Bt * xt[:, t, :, None]
         loss = loss + (torch.tensor(gy[:, t]) * (h * Ct).sum(-1)).sum()
     return loss
 
@@ -165,3 +167,69 @@ def test_chunked_equals_whole():
         assert relerr(b, a) < 1e-14
     for a, b in zip(st, st2):
         assert relerr(b, a) < 1e-15
+
+
+# ---------------------------------------------------------------- zero-order-hold drive
+# App. E's "A via ZOH" case: the drive e(A) B x with e = expm1(Delta A)/A
+# depends on A, so GammaA gains the term (de/dA) B x.
+
+def small_step_problem(seed, B=1, L=30, D=3, N=4):
+    """Delta ~ 1.2e-4: |Delta A| < 1e-3, where the oracle takes de/dA from
+    its series."""
+    p, x, gy = problem(seed, B=B, L=L, D=D, N=N)
+    p["b_delta"] = np.full(D, -9.0)
+    p["w_delta"] = p["w_delta"] * 0.1
+    return p, x, gy
+
+
+@pytest.mark.parametrize("case", ["normal", "stiff", "small_steps"])
+def test_zoh_reverse_mode_autograd(case):
+    if case == "small_steps":
+        p, x, gy = small_step_problem(60)
+    else:
+        p, x, gy = problem(61, stiff=case == "stiff")
+    _, (GA, GB, GC), _ = oracle.param_grads(x, gy, p, drive="zoh")
+    A = torch.tensor(p["A"], requires_grad=True)
+    bB = torch.zeros(p["A"].shape, dtype=torch.float64, requires_grad=True)
+    bC = torch.zeros(p["A"].shape, dtype=torch.float64, requires_grad=True)
+    _torch_loss(p, x, gy, A, bB, bC, drive="zoh").backward()
+    assert relerr(GA, A.grad.numpy()) < 1e-10
+    assert relerr(GB, bB.grad.numpy()) < 1e-12
+    assert relerr(GC, bC.grad.numpy()) < 1e-12
+    # and the Euler flows differ (the drive's A-dependence is not negligible)
+    _, (GA_e, _, _), _ = oracle.param_grads(x, gy, p)
+    assert relerr(GA_e, GA) > 1e-6
+
+
+def _loss_zoh(p, x, gy):
+    y, _, _, _ = oracle.scan_jvp(x, x[None] * 0.0, p, drive="zoh")
+    return float((gy * y).sum())
+
+
+@pytest.mark.parametrize("small", [False, True])
+def test_zoh_central_differences_along_A(small):
+    """<G_A, dA> against central differences of the separately pinned ZOH
+    primal, with one column of A exactly 0 (the A = 0 limit of the drive)."""
+    p, x, gy = small_step_problem(62) if small else problem(62, L=18)
+    p["A"][:, 1] = 0.0
+    _, (GA, _, _), _ = oracle.param_grads(x, gy, p, drive="zoh")
+    dA = np.random.default_rng(63).standard_normal(p["A"].shape)
+    eps = 1e-6 if not small else 1e-3
+    fd = (_loss_zoh(dict(p, A=p["A"] + eps * dA), x, gy) - _loss_zoh(dict(p, A=p["A"] - eps * dA), x, gy)) / (2 * eps)
+    assert abs(fd - (GA * dA).sum()) < 1e-7 * max(1.0, abs(fd)), (fd, (GA * dA).sum())
+
+
+def test_zoh_segment_composition_closed_forms():
+    """The carry's composition is the same as with the Euler drive: the
+    drive's A-dependence is inside the zero-start end state GA0."""
+    p, x, gy = problem(64, L=17)
+    g = np.random.default_rng(65)
+    ent = tuple(g.standard_normal((2, 3, 4)) for _ in range(3))
+    _, _, z = oracle.param_grads(x, gy, p, drive="zoh")
+    _, _, e = oracle.param_grads(x, gy, p, state=ent, drive="zoh")
+    delta, _ = oracle.discretize(x, x[None], p["w_delta"], p["b_delta"])
+    S = delta.sum(1)[:, :, None]
+    P = np.exp(p["A"][None] * S)
+    assert relerr(e[0], P * ent[0] + z[0]) < 1e-13
+    assert relerr(e[1], P * ent[1] + S * P * ent[0] + z[1]) < 1e-13
+    assert relerr(e[2], P * ent[2] + z[2]) < 1e-13
