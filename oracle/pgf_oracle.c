@@ -299,11 +299,11 @@ int pgf_oracle_param(int64_t B, int64_t L, int64_t D, int64_t N,
             double yt = 0.0;
             for (int64_t n = 0; n < N; ++n) {
                 const int64_t i = (b * D + d) * N + n;
-                const double a = A[d * N + n];
-                const double abar = exp(dl * a);
+                const double an = A[d * N + n];
+                const double abar = exp(dl * an);
                 /* drive coefficient e and its derivative in A */
-                const double ec = drive ? (a != 0.0 ? expm1(dl * a) / a : dl) : dl;
-                const double ea = drive ? zoh_coef_dA(dl, a) : 0.0;
+                const double ec = drive ? (an != 0.0 ? expm1(dl * an) / an : dl) : dl;
+                const double ea = drive ? zoh_coef_dA(dl, an) : 0.0;
                 const double hprev = h[i];
                 const double ga = abar * gA[i] + dl * abar * hprev + ea * Bm[btn + n] * xt;
                 const double gb = abar * gB[i] + ec * xt;
