@@ -222,9 +222,11 @@ def setup_ssm(args, np, torch, binding, inputs):
     cfg = inputs.get_config(args.workload)
     variant = args.drive != "euler" or args.act != "identity" or args.dres or args.complex or args.groups > 1 or \
         args.lowrank > 0
-    if variant and args.order != 1:
-        print("bench.py: --drive/--act/--dres/--complex/--groups/--lowrank apply to the first order only",
-              file=sys.stderr)
+    param_zoh = args.order == 3 and args.drive == "zoh" and not (args.act != "identity" or args.dres or args.complex
+                                                                 or args.groups > 1 or args.lowrank > 0)
+    if variant and args.order != 1 and not param_zoh:
+        print("bench.py: --act/--dres/--complex/--groups/--lowrank apply to the first order only, --drive to the "
+              "first order and the parameter flows", file=sys.stderr)
         sys.exit(2)
     if args.order == 2:
         # two independent N(0,1) directions on the same workload shape
@@ -265,7 +267,7 @@ def setup_ssm(args, np, torch, binding, inputs):
     if args.order == 3:
         def step():
             binding.param_grads(x, gy, params, grads=grads, workspace=ws, out=y, seg_len=args.seg_len,
-                                chunk_segs=args.chunk_segs)
+                                chunk_segs=args.chunk_segs, drive=args.drive)
     else:
         fn = binding.scan_jvp2 if args.order == 2 else binding.scan_jvp
         vkw = dict(drive=args.drive, act=args.act) if args.order == 1 else {}

@@ -403,7 +403,8 @@ def scan_jvp2(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_
 
 
 def param_grads(x: torch.Tensor, gy: torch.Tensor, params: dict, *, h_in=None, gamma_in=None, grads=None,
-                return_state=False, seg_len=0, chunk_segs=0, workspace=None, out=None, stream=None):
+                return_state=False, seg_len=0, chunk_segs=0, workspace=None, out=None, stream=None,
+                drive="euler"):
     """Primal scan with the parameter-sensitivity flows and online gradient
     accumulation against the adjoint signal gy = dl/dy, on the GPU.
 
@@ -414,7 +415,8 @@ def param_grads(x: torch.Tensor, gy: torch.Tensor, params: dict, *, h_in=None, g
     Returns (y [B,L,D], grad_A, grad_B, grad_C), plus (h_out [B,D,N],
     gamma_out [2,B,D,N]) when return_state.  grad_B and grad_C are the
     gradients of per-lane offsets of B and C; their sums over d are
-    dl/db_B and dl/db_C.  Asynchronous on the current stream.
+    dl/db_B and dl/db_C.  drive: "euler" or "zoh" (the zero-order-hold drive,
+    whose derivative in A enters dl/dA).  Asynchronous on the current stream.
     """
     if not (isinstance(x, torch.Tensor) and isinstance(gy, torch.Tensor) and x.is_cuda and gy.is_cuda):
         raise ValueError("x and gy must be device tensors")
@@ -422,10 +424,11 @@ def param_grads(x: torch.Tensor, gy: torch.Tensor, params: dict, *, h_in=None, g
         raise ValueError("x and gy must be on the same device")
     with torch.cuda.device(x.device), _on_stream(stream, x.device):
         return _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len, chunk_segs, workspace,
-                               out)
+                               out, drive)
 
 
-def _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len, chunk_segs, workspace, out):
+def _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len, chunk_segs, workspace, out,
+                    drive):
     L_ = lib()
     if x.dtype not in (torch.float32, torch.bfloat16) or gy.dtype != torch.float32:
         raise ValueError("x must be float32 or bfloat16 and gy float32")
@@ -436,7 +439,7 @@ def _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len,
     B, L, D = x.shape
     dev = x.device
     pr = make_params(B, L, D, params["A"].shape[1], 2, "bf16" if x.dtype == torch.bfloat16 else "f32", seg_len,
-                     chunk_segs, 3)
+                     chunk_segs, 3, drive)
     keep = []
     N = _model_params(pr, params, D, dev, keep)
     h_in = _dev_param(h_in, (B, D, N), dev, "h_in")

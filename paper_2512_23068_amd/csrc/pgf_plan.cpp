@@ -75,7 +75,9 @@ int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
     if (p->drive < 0 || p->drive > 1 || p->activation < 0 || p->activation > 1) return PGF_ERR_INVALID_ARG;
     const int var = (p->drive == PGF_DRIVE_ZOH ? 1 : 0) |
                     ((p->activation != PGF_ACT_IDENTITY || p->D_res) ? 2 : 0);
-    if (var && order != 1) return PGF_ERR_UNSUPPORTED;
+    // the variants belong to the first order; the parameter flows also take
+    // the ZOH drive
+    if (var && order != 1 && !(order == 3 && var == 1)) return PGF_ERR_UNSUPPORTED;
     if (var && (K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
     const int cplx = p->A_im ? 1 : 0;
     if (cplx && (order != 1 || var || K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;

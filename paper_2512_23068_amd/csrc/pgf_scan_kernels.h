@@ -189,6 +189,24 @@ __device__ __forceinline__ float zoh_coef(float delta, float a_n, float inv_a, f
     return fabsf(z) < 0.25f ? delta * ph : (abar - 1.0f) * inv_a;
 }
 
+// The derivative in A of the ZOH drive coefficient e = (Abar - 1)/A of one
+// lane (the parameter flows' GammaA with the ZOH drive): (Delta Abar - e)/A.
+// For |z| < 1/4, z = Delta*A, it is Delta^2 psi(z) with psi(z) = (e^z -
+// phi(z))/z = sum_m (m+1)/(m+2)! z^m summed to z^6 (the first omitted term is
+// below 2e-9 relative); otherwise (Delta Abar - e) * (1/A), where the
+// subtraction loses less than 3 bits.  A = 0 takes the first branch
+// (Delta^2 / 2).
+__device__ __forceinline__ float zoh_coef_dA(float delta, float a_n, float inv_a, float abar, float e) {
+    const float z = delta * a_n;
+    float ps = fmaf(z, 1.0f / 5760.0f, 1.0f / 840.0f);
+    ps = fmaf(z, ps, 1.0f / 144.0f);
+    ps = fmaf(z, ps, 1.0f / 30.0f);
+    ps = fmaf(z, ps, 0.125f);
+    ps = fmaf(z, ps, 1.0f / 3.0f);
+    ps = fmaf(z, ps, 0.5f);
+    return fabsf(z) < 0.25f ? (delta * delta) * ps : fmaf(delta, abar, -e) * inv_a;
+}
+
 // SiLU and its derivative at v: s = sigmoid(v) and 1 - s from one
 // e = exp(-|v|) (no cancellation on either side), silu = v s,
 // silu' = s + v s (1 - s).
@@ -1667,6 +1685,9 @@ __global__ __launch_bounds__(kThreads) void k_carry(
 //   GA' = Abar GA + Delta Abar h     (dh/dA; the Euler drive has no A)
 //   GB' = Abar GB + Delta x          (dh/d offset of B)
 //   h'  = Abar h + Delta B x,        y = sum_n C h'
+// With ZOH the drive is e B x, e = (Abar - 1)/A, which depends on A:
+//   GA' = Abar GA + Delta Abar h + (de/dA) B x,  GB' = Abar GB + e x,
+//   h'  = Abar h + e B x.
 // and the rescan (OUT) accumulates, per lane, over its segment
 //   gradA += gy C GA',  gradB += gy C GB',  gradC += gy h'.
 // Records are [B(N) | C(N)].  OUT=false: zero-start segment aggregates
@@ -1674,17 +1695,16 @@ __global__ __launch_bounds__(kThreads) void k_carry(
 // component 0).  OUT=true: scan from the entry state in init (as k_scan) and
 // write y; the three gradient sums go to gout at the same place as the
 // entry state (the entry slot is read before it is overwritten, by the same
-// thread), or, when gflush > 0 (sequential evaluation: gout is the running
-// sum of the call, and end_state receives the state), are added to gout
-// every gflush steps of the sequence and at the end of the block, so that
-// the additions happen in the same order for every host block size (blocks
-// start at multiples of gflush).
-template <int NT, bool OUT, typename InT>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_pscan(
+// thread), or are added to gout when gadd is set (sequential evaluation:
+// gout is the running sum of the call, and end_state receives the state;
+// the launcher runs one launch per kSeqChunk steps, so the additions happen
+// in the same order for every host block size).
+template <int NT, bool OUT, typename InT, bool ZOH = false>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 2 : 3))) void k_pscan(
     const InT *__restrict__ x, const float *__restrict__ gy, const float *__restrict__ A,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *init, int64_t ibs, int64_t igs, int64_t ics,
-    float *__restrict__ y, float *end_state, float *gout, int64_t gflush,
+    float *__restrict__ y, float *end_state, float *gout, int gadd,
     float *__restrict__ agg_h, float *__restrict__ agg_s,
     int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
     constexpr int N = NT;
@@ -1701,9 +1721,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     const int64_t te = ts + S < len ? ts + S : len;
     if (ts >= te) return;
 
-    float At[NT];
+    float At[NT], Af[NT], Ai[NT];
 #pragma unroll
-    for (int i = 0; i < NT; ++i) At[i] = A[d * N + i] * kLog2e;
+    for (int i = 0; i < NT; ++i) {
+        At[i] = A[d * N + i] * kLog2e;
+        if constexpr (ZOH) {
+            Af[i] = A[d * N + i];
+            Ai[i] = 1.0f / Af[i];
+        }
+    }
     const float w = w_delta[d], bd = b_delta[d];
 
     float h[NT], ga[NT], gb[NT];
@@ -1743,22 +1769,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
         if constexpr (!OUT) {   // (the output pass is slower with it)
             asm volatile("" ::"v"(pf));
             pf = touch_records(rec0, tb + TT, tb + 2 * TT, te, R, R);
-        } else {
-            // wave-uniform: tb is the same for every lane (gflush is a
-            // multiple of TT)
-            if (gflush && tb != ts && tb % gflush == 0) {
-                if (active) {
-                    float *ob = gout + b * ibs + d;
-#pragma unroll
-                    for (int i = 0; i < NT; ++i) {
-                        ob[i * D] += sA[i];
-                        ob[ics + i * D] += sB[i];
-                        ob[2 * ics + i * D] += sC[i];
-                    }
-                }
-#pragma unroll
-                for (int i = 0; i < NT; ++i) sA[i] = sB[i] = sC[i] = 0.0f;
-            }
         }
 #pragma unroll
         for (int j = 0; j < TT; ++j) {
@@ -1783,9 +1793,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
                     const float Bn = rec[i];
                     const float a = transition(delta, At[i]);
                     const float sv = a * h[i];
-                    ga[i] = fmaf(a, ga[i], delta * sv);
-                    gb[i] = fmaf(a, gb[i], u);
-                    h[i] = fmaf(Bn, u, sv);
+                    if constexpr (ZOH) {
+                        const float e = zoh_coef(delta, Af[i], Ai[i], a);
+                        const float ea = zoh_coef_dA(delta, Af[i], Ai[i], a, e);
+                        const float Bx = Bn * xv;
+                        ga[i] = fmaf(a, ga[i], fmaf(delta, sv, ea * Bx));
+                        gb[i] = fmaf(a, gb[i], e * xv);
+                        h[i] = fmaf(e, Bx, sv);
+                    } else {
+                        ga[i] = fmaf(a, ga[i], delta * sv);
+                        gb[i] = fmaf(a, gb[i], u);
+                        h[i] = fmaf(Bn, u, sv);
+                    }
                     if constexpr (OUT) {
                         const float Cn = rec[N + i];
                         const float gC = gc[j] * Cn;
@@ -1819,7 +1838,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
             }
         }
         float *ob = gout + b * ibs + g * igs + d;
-        if (gflush) {
+        if (gadd) {
 #pragma unroll
             for (int i = 0; i < NT; ++i) {
                 ob[i * D] += sA[i];
@@ -2576,26 +2595,30 @@ struct Launcher {
     }
 
     // Parameter flows: one thread per channel with all N <= 16 states.
-    template <int NT>
+    template <int NT, bool ZOH>
     void pscans(int64_t t0, int64_t len) {
         if (dry) return;
         const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
         const int64_t ND = q.N * q.D;
         if (q.seg == 0) {
-            Timed tm(3, st, !q.noalloc);
-            hipLaunchKernelGGL((k_pscan<NT, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, gy, p.A,
-                               p.w_delta, p.b_delta, bcw(), (const float *)state(), ND, (int64_t)0, q.B * ND, y,
-                               state(), gacc(), kSeqChunk, (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len,
-                               q.chunk_len, len, 1);
+            // One launch per kSeqChunk steps (a host block is a whole number
+            // of them), each adding its gradient partials to the running sums.
+            for (int64_t u0 = 0; u0 < len; u0 += kSeqChunk) {
+                const int64_t ul = len - u0 < kSeqChunk ? len - u0 : kSeqChunk;
+                Timed tm(3, st, !q.noalloc);
+                hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x,
+                                   gy, p.A, p.w_delta, p.b_delta, (const float *)(bcw() + u0 * q.R),
+                                   (const float *)state(), ND, (int64_t)0, q.B * ND, y, state(), gacc(), 1,
+                                   (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0 + u0, ul, q.chunk_len, ul, 1);
+            }
             return;
         }
         const int G = (int)((len + q.seg - 1) / q.seg);
         {
             Timed tm(1, st, !q.noalloc);
-            hipLaunchKernelGGL((k_pscan<NT, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
+            hipLaunchKernelGGL((k_pscan<NT, false, InT, ZOH>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
                                x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)nullptr, (int64_t)0,
-                               (int64_t)0, (int64_t)0, y, (float *)nullptr, (float *)nullptr, (int64_t)0, agg_h(),
-                               agg_s(),
+                               (int64_t)0, (int64_t)0, y, (float *)nullptr, (float *)nullptr, 0, agg_h(), agg_s(),
                                q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
         }
         const int64_t lanes = q.B * ND;
@@ -2606,9 +2629,9 @@ struct Launcher {
         }
         {
             Timed tm(3, st, !q.noalloc);
-            hipLaunchKernelGGL((k_pscan<NT, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
+            hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
                                x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(), (int64_t)G * 3 * ND,
-                               (int64_t)3 * ND, ND, y, (float *)nullptr, seg_in(), (int64_t)0, (float *)nullptr,
+                               (int64_t)3 * ND, ND, y, (float *)nullptr, seg_in(), 0, (float *)nullptr,
                                (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
         }
         {
@@ -2624,11 +2647,12 @@ struct Launcher {
             return q.K == 1 ? cscan_block<1>(t0, len) : (q.K == 2 ? cscan_block<2>(t0, len) : false);
         }
         if (q.order == 3) {
-            if (q.ns != 1) return false;
+            if (q.ns != 1 || (q.var & ~kZoh)) return false;
+            const bool zoh = (q.var & kZoh) != 0;
             switch (q.nt) {
-                case 4: pscans<4>(t0, len); return true;
-                case 8: pscans<8>(t0, len); return true;
-                case 16: pscans<16>(t0, len); return true;
+                case 4: zoh ? pscans<4, true>(t0, len) : pscans<4, false>(t0, len); return true;
+                case 8: zoh ? pscans<8, true>(t0, len) : pscans<8, false>(t0, len); return true;
+                case 16: zoh ? pscans<16, true>(t0, len) : pscans<16, false>(t0, len); return true;
                 default: return false;
             }
         }

@@ -288,6 +288,13 @@ def test_low_rank_plans_and_bad_fields():
         assert _call(q) == -1, field
 
 
+def test_parameter_flows_take_only_the_zoh_variant():
+    binding.plan(1, 100, 256, 16, 1, order=3, drive="zoh")
+    for kw in (dict(act="silu"), dict(complex_a=True), dict(groups=4), dict(dt_rank=16)):
+        with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+            binding.plan(1, 100, 256, 16, 1, order=3, **kw)
+
+
 def test_support_matrix_has_kernels():
     """pgf_plan succeeds only when the launch sequence has a kernel for every
     step (a host-side dry run of the dispatch, the same check the entry
@@ -301,7 +308,7 @@ def test_support_matrix_has_kernels():
                     assert p["n_per_thread"] * p["n_split"] == N
                     # follow-on paths: one thread per channel, N <= 16, K <= 2
                     for kw in (dict(order=2), dict(order=3), dict(drive="zoh"), dict(act="silu"),
-                               dict(complex_a=True), dict(groups=4), dict(dt_rank=48)):
+                               dict(complex_a=True), dict(groups=4), dict(dt_rank=48), dict(order=3, drive="zoh")):
                         if kw.get("order") == 2 and K != 2:
                             continue
                         ok = N <= 16 and (K <= 2 or kw.get("order") == 3)

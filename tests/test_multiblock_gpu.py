@@ -149,21 +149,22 @@ def test_sequential_multiblock_second_order():
     assert e <= gu.TOL, e
 
 
-def test_sequential_multiblock_param_grads():
+@pytest.mark.parametrize("drive", ["euler", "zoh"])
+def test_sequential_multiblock_param_grads(drive):
     inp = gu.custom("mamba130m", batch=1, seqlen=L_MB, d_inner=64)
     inp["gy"] = inputs.make_adjoint(inp["cfg"])
-    print("case multiblock parameter flows", flush=True)
-    _plan_blocks(1, 64, 16, 1, order=3)
+    print(f"case multiblock parameter flows {drive}", flush=True)
+    _plan_blocks(1, 64, 16, 1, order=3, drive=drive)
     x, _ = gu.inputs_to_dev(inp)
     gy = torch.from_numpy(inp["gy"]).to(gu.dev())
     prm = gu.params_to_dev(inp)
     runs = []
     for cs in CHUNK_SEGS:
-        runs.append(binding.param_grads(x, gy, prm, seg_len=-1, chunk_segs=cs, return_state=True))
+        runs.append(binding.param_grads(x, gy, prm, seg_len=-1, chunk_segs=cs, return_state=True, drive=drive))
         torch.cuda.synchronize()
     _equal_all(runs, "parameter flows")
     y, gA, gB, gC = runs[0][:4]
-    yo, (GA, GB, GC), _ = oracle.param_grads(inp["x"], inp["gy"], inp)
+    yo, (GA, GB, GC), _ = oracle.param_grads(inp["x"], inp["gy"], inp, drive=drive)
     errs = [gu.rel_l2(a.cpu().numpy(), b) for a, b in ((y, yo), (gA, GA), (gB, GB), (gC, GC))]
     print(f"multiblock param rel_l2 y={errs[0]:.3e} gA={errs[1]:.3e} gB={errs[2]:.3e} gC={errs[3]:.3e}", flush=True)
     assert max(errs) <= gu.TOL, errs

@@ -34,7 +34,8 @@ def _check(inp, what, channels=None, **kw):
     print(f"case {what}", flush=True)
     y, gA, gB, gC = _run(inp, **kw)[:4]
     yo, (GA, GB, GC), _ = oracle.param_grads(inp["x"], inp["gy"], inp, channels=channels,
-                                             chunk=None if channels is None else 8192)
+                                             chunk=None if channels is None else 8192,
+                                             drive=kw.get("drive", "euler"))
     if channels is not None:
         idx = torch.from_numpy(np.asarray(channels)).to(gu.dev())
         y = y.index_select(-1, idx)
@@ -142,3 +143,39 @@ def test_argument_checks():
     with pytest.raises(ValueError, match="grads"):
         binding.param_grads(x, gy, gu.params_to_dev(inp), grads=(torch.zeros(16, 16, device=gu.dev()),) * 2
                             + (torch.zeros(16, 8, device=gu.dev()),))
+
+
+# ------------------------------------------------------------ zero-order-hold drive
+# GammaA gains the drive's derivative in A: (Delta Abar - e)/A * B x, from a
+# series for |Delta A| < 1/4 and from the closed form above.
+
+@pytest.mark.parametrize("N,seg", [(16, 0), (8, -1), (4, 64), (16, -1)])
+def test_param_grads_zoh_parity(N, seg):
+    inp = _case("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N)
+    _check(inp, f"param zoh N={N} seg={seg}", seg_len=seg, drive="zoh")
+
+
+def test_param_grads_zoh_small_steps_and_stiff():
+    """Delta A on both sides of the series / closed-form switch: pulse128k's
+    Delta in [1e-4, 1e-2] (series) and the stiff bf16 workload."""
+    _check(_case("pulse128k", seqlen=2000, d_inner=64), "param zoh small steps", drive="zoh")
+    _check(_case("stiff128k", seqlen=1500, d_inner=64), "param zoh stiff bf16", drive="zoh")
+
+
+def test_param_grads_zoh_block_invariance_and_handoff():
+    inp = _case("mamba130m", batch=2, seqlen=1000, d_inner=48)
+    ref = _run(inp, seg_len=64, chunk_segs=1, return_state=True, drive="zoh")
+    for cs in (3, 0):
+        got = _run(inp, seg_len=64, chunk_segs=cs, return_state=True, drive="zoh")
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), cs
+    # the Euler flows differ: the drive's A-dependence reached the gradient
+    eul = _run(inp, seg_len=64, chunk_segs=1)
+    assert not torch.equal(eul[1], ref[1]) and torch.equal(eul[2], eul[2])
+
+
+def test_param_grads_zoh_full_size_sampled_channels():
+    inp = _case("pulse128k")
+    g = np.random.default_rng(6)
+    ch = np.unique(np.concatenate([[0, 1535], g.choice(np.arange(1, 1535), 4, replace=False)]))
+    _check(inp, "param zoh pulse128k full", channels=ch, drive="zoh")
