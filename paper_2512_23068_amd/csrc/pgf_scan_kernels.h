@@ -1094,7 +1094,13 @@ void k_scan(
 //   s_rec  the TT step records (B, dB_k, C, dC_k), read by every channel;
 //   s_sc   per (t, d): Delta, u = Delta*x, dDelta_k, p_k = dDelta_k*x +
 //          Delta*dx_k, each computed once per channel instead of once per
-//          thread sharing it.
+//          thread sharing it.  With K >= 4 directions (FOLD) the row is
+//          Delta, u, q = sigma*w*x + Delta (= du/dx), sw = sigma*w and dx_k:
+//          since dDelta_k = sw dx_k and p_k = q dx_k, the tangent's input
+//          terms are dx_k * c with c = sw*g + B*q shared by the directions,
+//          dh_k = (Abar dh_k + dx_k c) + dB_k u: three operations per
+//          direction and lane instead of four, and 4 + K scalars per (t, d)
+//          instead of 2 + 2K.
 // Every tile runs all TT steps: the slots of a short last tile hold
 // Delta = u = dDelta_k = p_k = 0, so Abar = 1 and the drive is zero, which
 // leaves h and dh_k exactly unchanged; only their output stores are
@@ -1113,7 +1119,8 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
     constexpr int R = 2 * N * (1 + K);
     constexpr int DPB = kThreads / NS;       // channels per block
     constexpr int TT = 8;                    // steps per tile
-    constexpr int SCW = 2 + 2 * K;           // Delta, u, dDelta_k, p_k
+    constexpr bool FOLD = K >= 4;            // the direction-shared form above
+    constexpr int SCW = FOLD ? 4 + K : 2 + 2 * K;   // per-(t, d) scalars
     constexpr int SCP = (SCW + 3) / 4 * 4;   // 16-byte rows: 128-bit reads
     constexpr int RV4 = (TT * R / 4 + kThreads - 1) / kThreads;  // record float4s per thread
     constexpr int TQ = (TT * DPB + kThreads - 1) / kThreads;     // (t, d) tasks per thread
@@ -1229,11 +1236,18 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
             float *o = &s_sc[tt][j][0];
             o[0] = delta;
             o[1] = delta * xq[i];
+            if constexpr (FOLD) {
+                o[2] = fmaf(sw, xq[i], delta);
+                o[3] = sw;
 #pragma unroll
-            for (int k = 0; k < K; ++k) {
-                const float ddl = sw * dxq[i][k];
-                o[2 + k] = ddl;
-                o[2 + K + k] = fmaf(ddl, xq[i], delta * dxq[i][k]);
+                for (int k = 0; k < K; ++k) o[4 + k] = live ? dxq[i][k] : 0.0f;
+            } else {
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    const float ddl = sw * dxq[i][k];
+                    o[2 + k] = ddl;
+                    o[2 + K + k] = fmaf(ddl, xq[i], delta * dxq[i][k]);
+                }
             }
         }
     };
@@ -1251,16 +1265,27 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
             const int64_t t = tb + tt;
             const float *sc = &s_sc[tt][dl][0];
             const float delta = sc[0], u = sc[1];
-            float dD[K], pk[K];
+            float dD[K], pk[K];     // FOLD: pk unused, dD holds dx_k
+            float qv = 0.0f, swv = 0.0f;
+            if constexpr (FOLD) {
+                qv = sc[2];
+                swv = sc[3];
 #pragma unroll
-            for (int k = 0; k < K; ++k) {
-                dD[k] = sc[2 + k];
-                pk[k] = sc[2 + K + k];
+                for (int k = 0; k < K; ++k) dD[k] = sc[4 + k];
+            } else {
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    dD[k] = sc[2 + k];
+                    pk[k] = sc[2 + K + k];
+                }
             }
             if constexpr (!OUT) {
                 sD += delta;
 #pragma unroll
-                for (int k = 0; k < K; ++k) sdD[k] += dD[k];
+                for (int k = 0; k < K; ++k) {
+                    if constexpr (FOLD) sdD[k] = fmaf(swv, dD[k], sdD[k]);
+                    else sdD[k] += dD[k];
+                }
             }
             const float *rec = s_rec + tt * R;
             float yv = 0.0f, dyv[K];
@@ -1279,13 +1304,24 @@ __global__ __launch_bounds__(kThreads) void k_scan_sh(
                 // dh itself keeps each dh_k in one register across steps (the
                 // form a dh + (...) ends in a temporary, which this loop then
                 // copied back on every step).
+                if constexpr (FOLD) {
+                    const float c = fmaf(swv, gv, Bn * qv);
 #pragma unroll
-                for (int k = 0; k < K; ++k) {
-                    const float dBn = rec[(1 + k) * N + n];
-                    float v = a * dh[k][i];
-                    v = fmaf(gv, dD[k], v);
-                    v = fmaf(Bn, pk[k], v);
-                    dh[k][i] = fmaf(dBn, u, v);
+                    for (int k = 0; k < K; ++k) {
+                        const float dBn = rec[(1 + k) * N + n];
+                        float v = a * dh[k][i];
+                        v = fmaf(dD[k], c, v);
+                        dh[k][i] = fmaf(dBn, u, v);
+                    }
+                } else {
+#pragma unroll
+                    for (int k = 0; k < K; ++k) {
+                        const float dBn = rec[(1 + k) * N + n];
+                        float v = a * dh[k][i];
+                        v = fmaf(gv, dD[k], v);
+                        v = fmaf(Bn, pk[k], v);
+                        dh[k][i] = fmaf(dBn, u, v);
+                    }
                 }
                 h[i] = hn;
                 if constexpr (OUT) {
