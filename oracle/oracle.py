@@ -70,7 +70,7 @@ def declare(lib):
     lib.pgf_oracle_core2.restype = ctypes.c_int
     lib.pgf_oracle_core2.argtypes = [i64] * 4 + [dp] * 22 + [ctypes.c_int]
     lib.pgf_oracle_param.restype = ctypes.c_int
-    lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 13 + [ctypes.c_int, ctypes.c_int]
+    lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 14 + [ctypes.c_int, dp, ctypes.c_int, ctypes.c_int]
     lib.pgf_oracle_la.restype = ctypes.c_int
     lib.pgf_oracle_la.argtypes = [i64] * 6 + [dp] * 12 + [ctypes.c_int]
     lib.pgf_oracle_core_cplx.restype = ctypes.c_int
@@ -385,13 +385,18 @@ def scan_jvp2(x, dxv, dxw, params, state=None, channels=None, chunk=None, nthrea
 
 # ------------------------------------------------------------------ parameter flows
 
-def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None, drive="euler"):
+ACTIVATIONS = {"identity": 0, "silu": 1}
+
+
+def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None, drive="euler", act="identity", D_res=None):
     """Parameter-sensitivity flows (see pgf_oracle_param).  Shapes: A [D,N];
     x, delta, gy [B,L,D]; Bm, Cm [B,L,N]; state = (h, GammaA, GammaB), each
     [B,D,N] (zero when None); drive "euler" or "zoh" (the zero-order-hold
-    drive, whose A-dependence enters GammaA).  Returns y [B,L,D], (GA, GB,
-    GC) each [B,D,N] (this call's contributions per batch row) and the exit
-    state tuple."""
+    drive, whose A-dependence enters GammaA); act "identity" or "silu" and
+    D_res [D] or None: the output map y = act(sum_n C h + D_res x).
+    Returns y [B,L,D], (GA, GB, GC) each [B,D,N] (this call's contributions
+    per batch row), plus GD [B,D] (dl/dD_res per batch row) when D_res is
+    given, and the exit state tuple."""
     lib = _load()
     A = _f64(A)
     x, delta, gy, Bm, Cm = (_f64(a) for a in (x, delta, gy, Bm, Cm))
@@ -407,15 +412,22 @@ def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None, drive="euler"
         assert s_.shape == (B, D, N)
     y = np.empty((B, L, D))
     G = [np.zeros((B, D, N)) for _ in range(3)]
+    Dr = None if D_res is None else _f64(D_res)
+    GD = None if D_res is None else np.zeros((B, D))
+    null = ctypes.POINTER(ctypes.c_double)()
     rc = lib.pgf_oracle_param(B, L, D, N, _dp(A), _dp(x), _dp(delta), _dp(gy), _dp(Bm), _dp(Cm),
-                              *[_dp(s_) for s_ in st], _dp(y), *[_dp(g) for g in G], DRIVES[drive],
-                              _threads() if nthreads is None else nthreads)
+                              *[_dp(s_) for s_ in st], _dp(y), *[_dp(g) for g in G],
+                              null if Dr is None else _dp(Dr), ACTIVATIONS[act], null if GD is None else _dp(GD),
+                              DRIVES[drive], _threads() if nthreads is None else nthreads)
     if rc != 0:
         raise RuntimeError("pgf_oracle_param failed")
+    if GD is not None:
+        G.append(GD)
     return y, tuple(G), tuple(st)
 
 
-def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=None, drive="euler"):
+def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=None, drive="euler",
+                act="identity"):
     """Primal output and online parameter gradients of the full model over
     L-chunks (App. E, Alg. 2).  x, gy [B,L,D]; params as scan_jvp; channels:
     optional 1-D index array of the channels d to compute (the projections
@@ -425,7 +437,9 @@ def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=N
     batch, exit state (h, GammaA, GammaB) each [B,Dsel,N]).  drive: "euler"
     or "zoh" (see core_param).  G_A = dl/dA;
     G_B and G_C are the gradients with respect to per-lane offsets of B and
-    C, so that dl/db_B = G_B.sum(0) and dl/db_C = G_C.sum(0)."""
+    C, so that dl/db_B = G_B.sum(0) and dl/db_C = G_C.sum(0).  act and
+    params["D_res"] (if present) set the output map y = act(C h + D_res x);
+    with D_res the gradient tuple gains G_D = dl/dD_res [Dsel]."""
     B, L, D = np.shape(x)
     A = _f64(params["A"])
     N = A.shape[1]
@@ -434,8 +448,10 @@ def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=N
     w = _f64(params["w_delta"])[sel]
     bd = _f64(params["b_delta"])[sel]
     As = A[sel]
+    Dr = params.get("D_res")
+    Dr = None if Dr is None else _f64(Dr)[sel]
     y = np.empty((B, L, Ds))
-    tot = [np.zeros((B, Ds, N)) for _ in range(3)]
+    tot = [np.zeros((B, Ds, N)) for _ in range(3)] + ([] if Dr is None else [np.zeros((B, Ds))])
     st = state
     step = max(1, L if not chunk else int(chunk))
     for t0 in range(0, L, step):
@@ -446,9 +462,9 @@ def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=N
         xs = np.ascontiguousarray(xc[..., sel])
         delta, _ = discretize(xs, xs[None], w, bd)
         gs = np.ascontiguousarray(_f64(gy[:, t0:t1])[..., sel])
-        yc, G, st = core_param(As, xs, delta, gs, Bm, Cm, st, nthreads, drive)
+        yc, G, st = core_param(As, xs, delta, gs, Bm, Cm, st, nthreads, drive, act, Dr)
         y[:, t0:t1] = yc
-        for i in range(3):
+        for i in range(len(tot)):
             tot[i] += G[i]
     if st is None:
         st = tuple(np.zeros((B, Ds, N)) for _ in range(3))

@@ -249,10 +249,17 @@ int pgf_oracle_core2(int64_t B, int64_t L, int64_t D, int64_t N,
  *   GammaB' = Abar*GammaB + e*x
  *   h'      = Abar*h + e*B*x
  * with de/dA from zoh_coef_dA.
+ *
+ * The output map y = act(y_hat), y_hat = sum_n C*h' + D_res*x (Sec. 3, the
+ * map Alg. 2's G_C update differentiates through sigma'): act = 0 identity,
+ * 1 SiLU (v*sigmoid(v)); D_res [D] or NULL (= 0).  The adjoint then reaches
+ * the state through w = gy*act'(y_hat), so every accumulation above takes w
+ * in place of gy, and GD[b,d] += w*x accumulates dl/dD_res (GD may be NULL
+ * when D_res is).
  * Shapes (double, row-major): A [D,N]; x, delta, gy [B,L,D];
  * Bm, Cm [B,L,N]; h, gA, gB [B,D,N] (entry state in, exit state out);
- * y [B,L,D] (written); GA, GB, GC [B,D,N] (added to, per batch row).
- * Returns 0, or -1 on a bad argument.
+ * y [B,L,D] (written); GA, GB, GC [B,D,N] and GD [B,D] (added to, per batch
+ * row).  Returns 0, or -1 on a bad argument.
  */
 
 /* d/dA of e(A) = expm1(Delta*A)/A: (Delta*exp(Delta*A) - e)/A.  The closed
@@ -277,10 +284,11 @@ int pgf_oracle_param(int64_t B, int64_t L, int64_t D, int64_t N,
                      const double *A, const double *x, const double *delta, const double *gy,
                      const double *Bm, const double *Cm,
                      double *h, double *gA, double *gB,
-                     double *y, double *GA, double *GB, double *GC, int drive, int nthreads)
+                     double *y, double *GA, double *GB, double *GC,
+                     const double *D_res, int act, double *GD, int drive, int nthreads)
 {
-    if (B < 0 || L < 0 || D < 0 || N <= 0 || drive < 0 || drive > 1) return -1;
-    if (!A || !h || !gA || !gB || !GA || !GB || !GC) return -1;
+    if (B < 0 || L < 0 || D < 0 || N <= 0 || drive < 0 || drive > 1 || act < 0 || act > 1) return -1;
+    if (!A || !h || !gA || !gB || !GA || !GB || !GC || (D_res && !GD)) return -1;
     if (L > 0 && (!x || !delta || !gy || !Bm || !Cm || !y)) return -1;
     const int64_t lanes = B * D;
 #ifdef _OPENMP
@@ -295,8 +303,9 @@ int pgf_oracle_param(int64_t B, int64_t L, int64_t D, int64_t N,
         for (int64_t t = 0; t < L; ++t) {
             const int64_t btd = (b * L + t) * D + d;
             const int64_t btn = (b * L + t) * N;
-            const double xt = x[btd], dl = delta[btd], g = gy[btd];
-            double yt = 0.0;
+            const double xt = x[btd], dl = delta[btd];
+            /* the flows of this step (the state after it) */
+            double yhat = 0.0;
             for (int64_t n = 0; n < N; ++n) {
                 const int64_t i = (b * D + d) * N + n;
                 const double an = A[d * N + n];
@@ -309,13 +318,26 @@ int pgf_oracle_param(int64_t B, int64_t L, int64_t D, int64_t N,
                 const double gb = abar * gB[i] + ec * xt;
                 const double hnew = abar * hprev + ec * Bm[btn + n] * xt;
                 h[i] = hnew; gA[i] = ga; gB[i] = gb;
-                const double Ct = Cm[btn + n];
-                yt += Ct * hnew;
-                GA[i] += g * Ct * ga;
-                GB[i] += g * Ct * gb;
-                GC[i] += g * hnew;
+                yhat += Cm[btn + n] * hnew;
+            }
+            /* the output map and the adjoint it passes to the state */
+            if (D_res) yhat += D_res[d] * xt;
+            double yt = yhat, slope = 1.0;
+            if (act == 1) {
+                const double sg = 1.0 / (1.0 + exp(-yhat));
+                yt = yhat * sg;
+                slope = sg + yhat * sg * (1.0 - sg);
             }
             y[btd] = yt;
+            const double w = gy[btd] * slope;
+            for (int64_t n = 0; n < N; ++n) {
+                const int64_t i = (b * D + d) * N + n;
+                const double Ct = Cm[btn + n];
+                GA[i] += w * Ct * gA[i];
+                GB[i] += w * Ct * gB[i];
+                GC[i] += w * h[i];
+            }
+            if (D_res) GD[b * D + d] += w * xt;
         }
     }
     return 0;

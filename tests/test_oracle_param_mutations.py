@@ -20,6 +20,10 @@ PIN_TESTS = [
     lambda: pins.test_zoh_reverse_mode_autograd("small_steps"),
     lambda: pins.test_zoh_central_differences_along_A(False),
     lambda: pins.test_zoh_central_differences_along_A(True),
+    lambda: pins.test_output_map_reverse_mode_autograd("silu", "euler", False),
+    lambda: pins.test_output_map_identity_residual_closed_form(),
+    lambda: pins.test_output_map_central_differences(),
+    lambda: pins.test_output_map_one_step_adjoint(),
 ]
 
 C_MUTANTS = {
@@ -42,9 +46,17 @@ C_MUTANTS = {
     "GammaB ZOH drive taken as Delta": ("const double gb = abar * gB[i] + ec * xt;",
                                         "const double gb = abar * gB[i] + dl * xt;"),
     "GammaB without decay": ("const double gb = abar * gB[i] + ec * xt;", "const double gb = gB[i] + ec * xt;"),
-    "G_C from the old state": ("GC[i] += g * hnew;", "GC[i] += g * hprev;"),
-    "G_A without C": ("GA[i] += g * Ct * ga;", "GA[i] += g * ga;"),
-    "G_B from GammaA": ("GB[i] += g * Ct * gb;", "GB[i] += g * Ct * ga;"),
+    "G_C from the state's B-flow": ("GC[i] += w * h[i];", "GC[i] += w * gB[i];"),
+    "G_C against the raw adjoint": ("GC[i] += w * h[i];", "GC[i] += gy[btd] * h[i];"),
+    "G_A without C": ("GA[i] += w * Ct * gA[i];", "GA[i] += w * gA[i];"),
+    "G_B from GammaA": ("GB[i] += w * Ct * gB[i];", "GB[i] += w * Ct * gA[i];"),
+    "output map without the residual": ("if (D_res) yhat += D_res[d] * xt;", "(void)0;"),
+    "adjoint without act'": ("const double w = gy[btd] * slope;", "const double w = gy[btd];"),
+    "SiLU slope without its second term": ("slope = sg + yhat * sg * (1.0 - sg);", "slope = sg;"),
+    "SiLU slope with sigma' as sg^2": ("slope = sg + yhat * sg * (1.0 - sg);", "slope = sg + yhat * sg * sg;"),
+    "G_D from the output": ("if (D_res) GD[b * D + d] += w * xt;", "if (D_res) GD[b * D + d] += w * yt;"),
+    "G_D against the raw adjoint": ("if (D_res) GD[b * D + d] += w * xt;",
+                                    "if (D_res) GD[b * D + d] += gy[btd] * xt;"),
 }
 
 

@@ -27,10 +27,11 @@ def problem(seed, B=2, L=14, D=3, N=4, stiff=False):
     return p, x, gy
 
 
-def _torch_loss(p, x, gy, A, beta_B, beta_C, drive="euler"):
+def _torch_loss(p, x, gy, A, beta_B, beta_C, drive="euler", act="identity", D_res=None):
     """l = sum gy*y of the selective scan as a plain torch loop, with the
     per-lane offsets beta_B, beta_C [D,N] added to B_t and C_t; drive "zoh"
-    takes b = expm1(Delta A)/A * B x (A != 0 everywhere here)."""
+    takes b = expm1(Delta A)/A * B x (A != 0 everywhere here); act "silu"
+    and D_res [D] (a tensor) give y = silu(C h + D_res x)."""
     xt = torch.tensor(x)
     z = xt * torch.tensor(p["w_delta"]) + torch.tensor(p["b_delta"])
     delta = torch.logaddexp(z, torch.zeros((), dtype=torch.float64))
@@ -45,7 +46,12 @@ def _torch_loss(p, x, gy, A, beta_B, beta_C, drive="euler"):
         Ct = Cm[:, t, None, :] + beta_C
         e = torch.expm1(dl * A) / A if drive == "zoh" else dl
         h = torch.exp(dl * A) * h + e * Bt * xt[:, t, :, None]
-        loss = loss + (torch.tensor(gy[:, t]) * (h * Ct).sum(-1)).sum()
+        yt = (h * Ct).sum(-1)
+        if D_res is not None:
+            yt = yt + D_res * xt[:, t]
+        if act == "silu":
+            yt = torch.nn.functional.silu(yt)
+        loss = loss + (torch.tensor(gy[:, t]) * yt).sum()
     return loss
 
 
@@ -233,3 +239,82 @@ def test_zoh_segment_composition_closed_forms():
     assert relerr(e[0], P * ent[0] + z[0]) < 1e-13
     assert relerr(e[1], P * ent[1] + S * P * ent[0] + z[1]) < 1e-13
     assert relerr(e[2], P * ent[2] + z[2]) < 1e-13
+
+
+# ---------------------------------------------------------------- output map
+# y = act(C h + D_res x): the adjoint reaches the state through act' (the
+# sigma' factor of App. E's G_C update), and D_res gains dl/dD_res = sum gy act' x.
+
+@pytest.mark.parametrize("act,drive,stiff", [("silu", "euler", False), ("silu", "zoh", True),
+                                             ("identity", "euler", False)])
+def test_output_map_reverse_mode_autograd(act, drive, stiff):
+    p, x, gy = problem(70, stiff=stiff)
+    p["D_res"] = np.random.default_rng(71).standard_normal(p["A"].shape[0])
+    y, (GA, GB, GC, GD), _ = oracle.param_grads(x, gy, p, drive=drive, act=act)
+    A = torch.tensor(p["A"], requires_grad=True)
+    bB = torch.zeros(p["A"].shape, dtype=torch.float64, requires_grad=True)
+    bC = torch.zeros(p["A"].shape, dtype=torch.float64, requires_grad=True)
+    Dr = torch.tensor(p["D_res"], requires_grad=True)
+    _torch_loss(p, x, gy, A, bB, bC, drive=drive, act=act, D_res=Dr).backward()
+    tolA = 1e-10 if drive == "zoh" else 1e-12
+    assert relerr(GA, A.grad.numpy()) < tolA
+    assert relerr(GB, bB.grad.numpy()) < 1e-12
+    assert relerr(GC, bC.grad.numpy()) < 1e-12
+    assert relerr(GD, Dr.grad.numpy()) < 1e-12
+    # the primal is the first-order oracle's, output map included
+    y1, _, _, _ = oracle.scan_jvp(x, np.zeros((1,) + x.shape), p, drive=drive, act=act)
+    assert relerr(y, y1) < 1e-14
+
+
+def test_output_map_identity_residual_closed_form():
+    """With the identity map, y = C h + D_res x: the flows of A, B, C are
+    those without D_res, and dl/dD_res[d] = sum_{b,t} gy x."""
+    p, x, gy = problem(72)
+    _, G0, _ = oracle.param_grads(x, gy, p)
+    p["D_res"] = np.random.default_rng(73).standard_normal(p["A"].shape[0])
+    _, G, _ = oracle.param_grads(x, gy, p)
+    for a, b in zip(G0, G[:3]):
+        assert relerr(b, a) < 1e-15
+    assert relerr(G[3], (gy * x).sum((0, 1))) < 1e-14
+
+
+def _loss_map(p, x, gy, act):
+    y, _, _, _ = oracle.scan_jvp(x, x[None] * 0.0, p, act=act)
+    return float((gy * y).sum())
+
+
+def test_output_map_central_differences():
+    """<G, dP> along A, b_C and D_res against central differences of the
+    separately pinned first-order primal with the SiLU map."""
+    p, x, gy = problem(74, L=18)
+    p["D_res"] = np.random.default_rng(75).standard_normal(p["A"].shape[0])
+    _, (GA, GB, GC, GD), _ = oracle.param_grads(x, gy, p, act="silu")
+    g = np.random.default_rng(76)
+    eps = 1e-6
+    for key, G in (("A", GA), ("b_B", GB.sum(0)), ("b_C", GC.sum(0)), ("D_res", GD)):
+        dP = g.standard_normal(p[key].shape)
+        fd = (_loss_map(dict(p, **{key: p[key] + eps * dP}), x, gy, "silu")
+              - _loss_map(dict(p, **{key: p[key] - eps * dP}), x, gy, "silu")) / (2 * eps)
+        assert abs(fd - (G * dP).sum()) < 1e-7 * max(1.0, abs(fd)), (key, fd, (G * dP).sum())
+
+
+def test_output_map_one_step_adjoint():
+    """An adjoint at one (b, t0, d): G_C[d] = gy * silu'(yhat) * h_t0 and
+    G_D[d] = gy * silu'(yhat) * x, with yhat from the first-order primal
+    (identity map) at that step: the sigma' factor of the G_C update."""
+    p, x, _ = problem(77, B=2, L=20)
+    p["D_res"] = np.random.default_rng(78).standard_normal(3)
+    t0, b, d = 9, 0, 1
+    gy = np.zeros_like(x)
+    gy[b, t0, d] = -0.8
+    _, (GA, GB, GC, GD), _ = oracle.param_grads(x, gy, p, act="silu")
+    yh, _, h, _ = oracle.scan_jvp(x[:, :t0 + 1], np.zeros((1,) + x[:, :t0 + 1].shape), p)
+    v = yh[b, t0, d]
+    sg = 1.0 / (1.0 + np.exp(-v))
+    w = -0.8 * (sg + v * sg * (1.0 - sg))
+    ref = np.zeros_like(GC)
+    ref[d] = w * h[b, d]
+    assert relerr(GC, ref) < 1e-14
+    refD = np.zeros(3)
+    refD[d] = w * x[b, t0, d]
+    assert relerr(GD, refD) < 1e-14
