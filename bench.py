@@ -40,7 +40,7 @@ def parse():
                     help="2: second-order flow (two directions, pgf_scan_jvp2); "
                          "3: parameter flows with gradient accumulation (pgf_param_grads)")
     ap.add_argument("--drive", default="euler", choices=("euler", "zoh"), help="input drive (first order)")
-    ap.add_argument("--act", default="identity", choices=("identity", "silu"), help="output activation (first order)")
+    ap.add_argument("--act", default="identity", choices=("identity", "silu"), help="output activation (first order and parameter flows)")
     ap.add_argument("--dres", action="store_true", help="add a residual weight D_res ~ N(0,1) to the output map")
     ap.add_argument("--groups", type=int, default=1,
                     help="channel groups with their own B and C (first order; D/groups a multiple of 64)")
@@ -222,10 +222,9 @@ def setup_ssm(args, np, torch, binding, inputs):
     cfg = inputs.get_config(args.workload)
     variant = args.drive != "euler" or args.act != "identity" or args.dres or args.complex or args.groups > 1 or \
         args.lowrank > 0
-    param_zoh = args.order == 3 and args.drive == "zoh" and not (args.act != "identity" or args.dres or args.complex
-                                                                 or args.groups > 1 or args.lowrank > 0)
-    if variant and args.order != 1 and not param_zoh:
-        print("bench.py: --act/--dres/--complex/--groups/--lowrank apply to the first order only, --drive to the "
+    param_variant = args.order == 3 and not (args.complex or args.groups > 1 or args.lowrank > 0)
+    if variant and args.order != 1 and not param_variant:
+        print("bench.py: --complex/--groups/--lowrank apply to the first order only, --drive/--act/--dres to the "
               "first order and the parameter flows", file=sys.stderr)
         sys.exit(2)
     if args.order == 2:
@@ -249,8 +248,9 @@ def setup_ssm(args, np, torch, binding, inputs):
     y = torch.empty((B, L, D), device=dev)
     if args.order == 3:
         gy = torch.from_numpy(inputs.make_adjoint(cfg)).to(dev)
-        grads = tuple(torch.zeros((D, N), device=dev) for _ in range(3))
-        payload = x.numel() * s_in + gy.numel() * 4 + y.numel() * 4 + 3 * D * N * 4
+        grads = tuple(torch.zeros((D, N), device=dev) for _ in range(3)) + \
+            ((torch.zeros(D, device=dev),) if args.dres else ())
+        payload = x.numel() * s_in + gy.numel() * 4 + y.numel() * 4 + sum(g.numel() * 4 for g in grads)
     else:
         dx = torch.from_numpy(inp["dx"]).to(dev).to(tdt)
         payload = x.numel() * s_in + dx.numel() * s_in + (x.numel() + dx.numel()) * 4
@@ -267,7 +267,7 @@ def setup_ssm(args, np, torch, binding, inputs):
     if args.order == 3:
         def step():
             binding.param_grads(x, gy, params, grads=grads, workspace=ws, out=y, seg_len=args.seg_len,
-                                chunk_segs=args.chunk_segs, drive=args.drive)
+                                chunk_segs=args.chunk_segs, drive=args.drive, act=args.act)
     else:
         fn = binding.scan_jvp2 if args.order == 2 else binding.scan_jvp
         vkw = dict(drive=args.drive, act=args.act) if args.order == 1 else {}
@@ -284,7 +284,10 @@ def setup_ssm(args, np, torch, binding, inputs):
     return Workload(
         step=step, tokch=tokch, alg_bytes=alg_bytes,
         flops=tokch * N * (cplx_flops_per_lane_step(K) if args.complex else scan_flops_per_lane_step(K, args.order)),
-        payload=payload, plan=plan, metric=METRIC[args.order], kernel="k_scan (scan with outputs)",
+        payload=payload, plan=plan, metric=METRIC[args.order],
+        kernel={1: "k_scan/k_scan_sh (scan with outputs)", 2: "k_scan2 (scan with outputs)",
+                3: "k_pscan (rescan with outputs and gradient sums)"}[args.order]
+        if not args.complex else "k_cscan (scan with outputs)",
         traffic=None if variant else committed_traffic(name, "scan_out", args.order),
         dtype="f32" if cfg.in_dtype == "f32" else "bf16-in/f32",
         config={"workload": name + variant_suffix(args), "batch": B, "seq_len": L, "d_inner": D, "d_state": N,

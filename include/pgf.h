@@ -163,6 +163,9 @@ typedef struct pgf_params {
      * f32, and may reach 2 GiB. */
     int32_t dt_rank;
     const float *W_dx, *W_dt;
+    /* Parameter flows with D_res set: dl/dD_res, device [D] f32, ADDED to
+     * (like grad_A); not read otherwise. */
+    float *grad_D_res;
 } pgf_params;
 
 /* How a call is tiled (host-side planning; no device access). */
@@ -259,6 +262,14 @@ int pgf_scan_jvp2(const void *x, const void *dx, const pgf_params *p,
  *   grad_A, grad_B, grad_C : device, [D,N] f32, ADDED to (the caller zeroes
  *            them before the first call of a sequence)
  *   stream : a hipStream_t (NULL = the default stream)
+ * Output map (Sec. 3; p->activation, p->D_res as in pgf_scan_jvp): with
+ * y = act(yhat), yhat = sum_n C_t[n]*h' + D_res*x, the adjoint reaches the
+ * state through w = gy*act'(yhat) (the sigma' factor of Alg. 2's G_C
+ * update), so gy is replaced by w in the three sums above, and
+ *   p->grad_D_res[d] += w*x              = dl/dD_res
+ * (grad_D_res is required when D_res is set).  The ZOH drive
+ * (p->drive) adds (de/dA)*B_t[n]*x to GammaA' with e = (Abar - 1)/A, and
+ * takes e in place of Delta in the other drives.
  * p->order must be 3.  State hand-off: h_in/h_out as in pgf_scan_jvp;
  * dh_in/dh_out hold [GammaA; GammaB] as [2,B,D,N].  Chaining calls through
  * the state and adding into the same gradients gives the gradients of the

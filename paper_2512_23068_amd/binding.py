@@ -40,6 +40,7 @@ class PgfParams(ctypes.Structure):
         ("d2h_in", _c_f), ("d2h_out", _c_f),
         ("drive", ctypes.c_int32), ("activation", ctypes.c_int32), ("D_res", _c_f), ("A_im", _c_f),
         ("n_groups", ctypes.c_int32), ("dt_rank", ctypes.c_int32), ("W_dx", _c_f), ("W_dt", _c_f),
+        ("grad_D_res", _c_f),
     ]
 
 
@@ -404,7 +405,7 @@ def scan_jvp2(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_
 
 def param_grads(x: torch.Tensor, gy: torch.Tensor, params: dict, *, h_in=None, gamma_in=None, grads=None,
                 return_state=False, seg_len=0, chunk_segs=0, workspace=None, out=None, stream=None,
-                drive="euler"):
+                drive="euler", act="identity"):
     """Primal scan with the parameter-sensitivity flows and online gradient
     accumulation against the adjoint signal gy = dl/dy, on the GPU.
 
@@ -416,7 +417,10 @@ def param_grads(x: torch.Tensor, gy: torch.Tensor, params: dict, *, h_in=None, g
     gamma_out [2,B,D,N]) when return_state.  grad_B and grad_C are the
     gradients of per-lane offsets of B and C; their sums over d are
     dl/db_B and dl/db_C.  drive: "euler" or "zoh" (the zero-order-hold drive,
-    whose derivative in A enters dl/dA).  Asynchronous on the current stream.
+    whose derivative in A enters dl/dA).  act ("identity" or "silu") and
+    params["D_res"] (optional [D]) set the output map y = act(C h + D_res x);
+    with D_res the gradients gain a fourth, grad_D_res [D] (grads then holds
+    four tensors when given).  Asynchronous on the current stream.
     """
     if not (isinstance(x, torch.Tensor) and isinstance(gy, torch.Tensor) and x.is_cuda and gy.is_cuda):
         raise ValueError("x and gy must be device tensors")
@@ -424,11 +428,11 @@ def param_grads(x: torch.Tensor, gy: torch.Tensor, params: dict, *, h_in=None, g
         raise ValueError("x and gy must be on the same device")
     with torch.cuda.device(x.device), _on_stream(stream, x.device):
         return _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len, chunk_segs, workspace,
-                               out, drive)
+                               out, drive, act)
 
 
 def _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len, chunk_segs, workspace, out,
-                    drive):
+                    drive, act):
     L_ = lib()
     if x.dtype not in (torch.float32, torch.bfloat16) or gy.dtype != torch.float32:
         raise ValueError("x must be float32 or bfloat16 and gy float32")
@@ -439,9 +443,15 @@ def _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len,
     B, L, D = x.shape
     dev = x.device
     pr = make_params(B, L, D, params["A"].shape[1], 2, "bf16" if x.dtype == torch.bfloat16 else "f32", seg_len,
-                     chunk_segs, 3, drive)
+                     chunk_segs, 3, drive, act)
     keep = []
     N = _model_params(pr, params, D, dev, keep)
+    if params.get("A_im") is not None:
+        raise ValueError("param_grads: real transitions only")
+    D_res = _dev_param(params.get("D_res"), (D,), dev, "D_res")
+    keep.append(D_res)
+    pr.D_res = None if D_res is None else D_res.data_ptr()
+    shapes = [(D, N)] * 3 + ([(D,)] if D_res is not None else [])
     h_in = _dev_param(h_in, (B, D, N), dev, "h_in")
     gamma_in = _dev_param(gamma_in, (2, B, D, N), dev, "gamma_in")
     pr.h_in = None if h_in is None else h_in.data_ptr()
@@ -453,12 +463,15 @@ def _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len,
         pr.h_out, pr.dh_out = h_out.data_ptr(), g_out.data_ptr()
         states = (h_out, g_out)
     if grads is None:
-        grads = tuple(torch.zeros((D, N), device=dev, dtype=torch.float32) for _ in range(3))
+        grads = tuple(torch.zeros(sh, device=dev, dtype=torch.float32) for sh in shapes)
     else:
         grads = tuple(grads)
-        if len(grads) != 3 or not all(isinstance(g, torch.Tensor) and g.dtype == torch.float32 and g.device == dev
-                                      and tuple(g.shape) == (D, N) and g.is_contiguous() for g in grads):
-            raise ValueError(f"grads: three contiguous float32 tensors of shape [D,N] = [{D},{N}] on {dev}")
+        if len(grads) != len(shapes) or not all(
+                isinstance(g, torch.Tensor) and g.dtype == torch.float32 and g.device == dev
+                and tuple(g.shape) == sh and g.is_contiguous() for g, sh in zip(grads, shapes)):
+            raise ValueError(f"grads: {len(shapes)} contiguous float32 tensors of shapes {shapes} on {dev}")
+    if len(grads) == 4:
+        pr.grad_D_res = grads[3].data_ptr()
     y, = _outputs(out, ((B, L, D),), ("y",), dev)
     workspace = _workspace(L_, pr, workspace, dev)
     st = torch.cuda.current_stream(dev).cuda_stream

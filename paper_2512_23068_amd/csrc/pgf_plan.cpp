@@ -76,8 +76,8 @@ int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
     const int var = (p->drive == PGF_DRIVE_ZOH ? 1 : 0) |
                     ((p->activation != PGF_ACT_IDENTITY || p->D_res) ? 2 : 0);
     // the variants belong to the first order; the parameter flows also take
-    // the ZOH drive
-    if (var && order != 1 && !(order == 3 && var == 1)) return PGF_ERR_UNSUPPORTED;
+    // the ZOH drive and the output map
+    if (var && order == 2) return PGF_ERR_UNSUPPORTED;
     if (var && (K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
     const int cplx = p->A_im ? 1 : 0;
     if (cplx && (order != 1 || var || K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
@@ -186,7 +186,7 @@ int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
         w.agg_h = w.agg_s = off;
     }
     w.gacc = off;
-    if (order == 3) off = align256(off + 3 * (size_t)B * N * D * f);
+    if (order == 3) off = align256(off + (3 * (size_t)B * N * D + (size_t)B * D) * f);
     w.lr = off;
     if (rank) off = align256(off + (size_t)(1 + K) * B * q.chunk_len * q.rc * f);
     w.dt = off;

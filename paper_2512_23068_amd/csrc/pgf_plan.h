@@ -26,8 +26,9 @@ constexpr int64_t kSeqChunk = 4096;
 //                                    then (in place) the true state
 //                                    entering each segment
 //   agg_s   [B][G][(1+K)][D]         segment sums of Delta and dDelta_k
-//   gacc    [3][B][N][D]             parameter flows only: running gradient
-//                                    sums (A, B offset, C offset) of the call
+//   gacc    [3][B][N][D] + [B][D]    parameter flows only: running gradient
+//                                    sums (A, B offset, C offset) of the call,
+//                                    then those of the residual weight D_res
 //   lr      [(1+K)][B][Tc][RC]       low rank only: x W_dx and dx_k W_dx, the
 //                                    rank padded to RC (zero columns)
 //   dt      [(1+K)][B][Tc][D]        low rank only: Delta and dDelta_k

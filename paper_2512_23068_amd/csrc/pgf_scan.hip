@@ -102,25 +102,30 @@ int param_common(const void *x, const float *gy, const pgf_params *p, float *y, 
     if (q.order != 3) return PGF_ERR_INVALID_ARG;
     if (!p->A || !p->w_delta || !p->b_delta || !p->W_B || !p->W_C) return PGF_ERR_INVALID_ARG;
     if (!gA || !gB || !gC) return PGF_ERR_INVALID_ARG;
+    // the residual weight's gradient, when there is a residual weight
+    const float *gD = p->D_res ? p->grad_D_res : nullptr;
+    if (p->D_res && !gD) return PGF_ERR_INVALID_ARG;
     if (!p->workspace || p->workspace_bytes < q.ws.total || ((uintptr_t)p->workspace & 255))
         return PGF_ERR_WORKSPACE;
     const size_t esz = q.in_bf16 ? 2 : 4;
     const size_t nx = (size_t)q.B * q.L * q.D;
     const size_t bx = nx * esz, bg = nx * 4, by = nx * 4, bw = q.ws.total;
-    const size_t bp = (size_t)q.N * q.D * 4;
-    const float *grads[3] = {gA, gB, gC};
-    for (int i = 0; i < 3; ++i) {
-        for (int j = i + 1; j < 3; ++j)
-            if (overlap(grads[i], bp, grads[j], bp)) return PGF_ERR_INVALID_ARG;
-        if (overlap(grads[i], bp, p->workspace, bw)) return PGF_ERR_INVALID_ARG;
+    const int ng = gD ? 4 : 3;
+    const float *grads[4] = {gA, gB, gC, gD};
+    const size_t bp[4] = {(size_t)q.N * q.D * 4, (size_t)q.N * q.D * 4, (size_t)q.N * q.D * 4, (size_t)q.D * 4};
+    for (int i = 0; i < ng; ++i) {
+        for (int j = i + 1; j < ng; ++j)
+            if (overlap(grads[i], bp[i], grads[j], bp[j])) return PGF_ERR_INVALID_ARG;
+        if (overlap(grads[i], bp[i], p->workspace, bw)) return PGF_ERR_INVALID_ARG;
     }
     if (q.L > 0) {
         if (!x || !gy || !y) return PGF_ERR_INVALID_ARG;
         if (overlap(y, by, x, bx) || overlap(y, by, gy, bg) || overlap(y, by, p->workspace, bw) ||
             overlap(p->workspace, bw, x, bx) || overlap(p->workspace, bw, gy, bg))
             return PGF_ERR_INVALID_ARG;
-        for (int i = 0; i < 3; ++i)
-            if (overlap(grads[i], bp, x, bx) || overlap(grads[i], bp, gy, bg) || overlap(grads[i], bp, y, by))
+        for (int i = 0; i < ng; ++i)
+            if (overlap(grads[i], bp[i], x, bx) || overlap(grads[i], bp[i], gy, bg) ||
+                overlap(grads[i], bp[i], y, by))
                 return PGF_ERR_INVALID_ARG;
     }
     (void)hipGetLastError();

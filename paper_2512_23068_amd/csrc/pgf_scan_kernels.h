@@ -1735,17 +1735,25 @@ __global__ __launch_bounds__(kThreads) void k_carry(
 // gout is the running sum of the call, and end_state receives the state;
 // the launcher runs one launch per kSeqChunk steps, so the additions happen
 // in the same order for every host block size).
-template <int NT, bool OUT, typename InT, bool ZOH = false>
+// MAP (output pass only): the output map y = act(yhat), yhat = sum_n C h' +
+// D_res x.  The adjoint then reaches the state through w = gy act'(yhat):
+// the three sums take w in place of gy (App. E's sigma' factor of the G_C
+// update), and w x, summed over the segment, is the partial of dl/dD_res,
+// stored (or with gadd added) at gdr[b gdr_bs + g gdr_gs + d].
+template <int NT, bool OUT, typename InT, bool ZOH = false, bool MAP = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 2 : 3))) void k_pscan(
     const InT *__restrict__ x, const float *__restrict__ gy, const float *__restrict__ A,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *init, int64_t ibs, int64_t igs, int64_t ics,
     float *__restrict__ y, float *end_state, float *gout, int gadd,
     float *__restrict__ agg_h, float *__restrict__ agg_s,
-    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G,
+    const float *__restrict__ D_res, int act, float *gdr, int64_t gdr_bs, int64_t gdr_gs) {
+    static_assert(OUT || !MAP, "the output map belongs to the output pass");
     constexpr int N = NT;
     constexpr int R = 2 * N;          // B, C
-    constexpr int TT = OUT && NT >= 16 ? 4 : 8;   // prefetch depth, bounded by the VGPR budget
+    // prefetch depth, bounded by the VGPR budget
+    constexpr int TT = OUT && NT >= 16 ? (MAP ? 2 : 4) : 8;
 
     const int tid = threadIdx.x;
     const int64_t d_raw = (int64_t)blockIdx.x * kThreads + tid;
@@ -1767,6 +1775,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 
         }
     }
     const float w = w_delta[d], bd = b_delta[d];
+    float Dr = 0.0f, sDr = 0.0f;
+    if constexpr (MAP) Dr = D_res ? D_res[d] : 0.0f;
 
     float h[NT], ga[NT], gb[NT];
     float sA[NT], sB[NT], sC[NT];
@@ -1843,11 +1853,32 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 
                     }
                     if constexpr (OUT) {
                         const float Cn = rec[N + i];
-                        const float gC = gc[j] * Cn;
                         yv = fmaf(Cn, h[i], yv);
+                        if constexpr (!MAP) {
+                            const float gC = gc[j] * Cn;
+                            sA[i] = fmaf(gC, ga[i], sA[i]);
+                            sB[i] = fmaf(gC, gb[i], sB[i]);
+                            sC[i] = fmaf(gc[j], h[i], sC[i]);
+                        }
+                    }
+                }
+                if constexpr (MAP) {
+                    // the output map, then the sums against w = gy act'(yhat)
+                    yv = fmaf(Dr, xv, yv);
+                    float wv = gc[j];
+                    if (act == PGF_ACT_SILU) {
+                        float f, df;
+                        silu_and_slope(yv, f, df);
+                        yv = f;
+                        wv *= df;
+                    }
+                    sDr = fmaf(wv, xv, sDr);
+#pragma unroll
+                    for (int i = 0; i < NT; ++i) {
+                        const float gC = wv * rec[N + i];
                         sA[i] = fmaf(gC, ga[i], sA[i]);
                         sB[i] = fmaf(gC, gb[i], sB[i]);
-                        sC[i] = fmaf(gc[j], h[i], sC[i]);
+                        sC[i] = fmaf(wv, h[i], sC[i]);
                     }
                 }
                 if constexpr (OUT) {
@@ -1872,6 +1903,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 
                 eb[ics + i * D] = ga[i];
                 eb[2 * ics + i * D] = gb[i];
             }
+        }
+        if constexpr (MAP) {
+            float *dr = gdr + b * gdr_bs + g * gdr_gs + d;
+            *dr = gadd ? *dr + sDr : sDr;
         }
         float *ob = gout + b * ibs + g * igs + d;
         if (gadd) {
@@ -1950,11 +1985,21 @@ static __global__ __launch_bounds__(kThreads) void k_pcarry(
 // Adds the block's per-segment gradient partials part [B][G][3][N][D] to the
 // running sums acc [3][B][N][D] (the state layout), one segment after the
 // other in order, so the sums do not depend on how the call is split into
-// host blocks.
+// host blocks.  With dpart (the output map's residual weight), the partials
+// of dl/dD_res at dpart[(b G + g) 3 D + d] go the same way to the sums
+// acc[3 B N D + b D + d].
 static __global__ __launch_bounds__(kThreads) void k_gsum(
-    const float *__restrict__ part, float *__restrict__ acc, int64_t Bsz, int64_t ND, int G) {
+    const float *__restrict__ part, float *__restrict__ acc, int64_t Bsz, int64_t ND, int G,
+    const float *__restrict__ dpart, int64_t D) {
     constexpr int GB = 16;
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (dpart && idx >= 3 * Bsz * ND && idx < 3 * Bsz * ND + Bsz * D) {
+        const int64_t j = idx - 3 * Bsz * ND, b = j / D, d = j % D;
+        float s = acc[idx];
+        for (int g = 0; g < G; ++g) s += dpart[(b * G + g) * 3 * D + d];
+        acc[idx] = s;
+        return;
+    }
     if (idx >= 3 * Bsz * ND) return;
     const int64_t c = idx / (Bsz * ND), b = (idx / ND) % Bsz, r = idx % ND;
     float s = acc[idx];
@@ -1979,12 +2024,20 @@ static __global__ __launch_bounds__(kThreads) void k_fill0(float *__restrict__ p
     if (i < n) p[i] = 0.0f;
 }
 
-// grad_c[d][n] += sum over b (in order) of acc[c][b][n][d], c = A, B, C.
+// grad_c[d][n] += sum over b (in order) of acc[c][b][n][d], c = A, B, C, and
+// (gD not NULL) gD[d] += sum over b of acc[3 B N D + b D + d].
 static __global__ __launch_bounds__(kThreads) void k_gout(
     const float *__restrict__ acc, float *__restrict__ gA, float *__restrict__ gB, float *__restrict__ gC,
-    int64_t Bsz, int64_t D, int64_t N) {
+    float *__restrict__ gD, int64_t Bsz, int64_t D, int64_t N) {
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int64_t ND = N * D;
+    if (gD && idx >= 3 * ND && idx < 3 * ND + D) {
+        const int64_t d = idx - 3 * ND;
+        float s = 0.0f;
+        for (int64_t b = 0; b < Bsz; ++b) s += acc[3 * Bsz * ND + b * D + d];
+        gD[d] += s;
+        return;
+    }
     if (idx >= 3 * ND) return;
     const int64_t c = idx / ND, r = idx % ND;
     const int64_t d = r % D, n = r / D;
@@ -2631,7 +2684,9 @@ struct Launcher {
     }
 
     // Parameter flows: one thread per channel with all N <= 16 states.
-    template <int NT, bool ZOH>
+    // MAP: the output map (activation, residual weight) with the partials
+    // of dl/dD_res, summed into gacc's [B][D] tail.
+    template <int NT, bool ZOH, bool MAP>
     void pscans(int64_t t0, int64_t len) {
         if (dry) return;
         const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
@@ -2642,10 +2697,11 @@ struct Launcher {
             for (int64_t u0 = 0; u0 < len; u0 += kSeqChunk) {
                 const int64_t ul = len - u0 < kSeqChunk ? len - u0 : kSeqChunk;
                 Timed tm(3, st, !q.noalloc);
-                hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x,
-                                   gy, p.A, p.w_delta, p.b_delta, (const float *)(bcw() + u0 * q.R),
+                hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH, MAP>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0,
+                                   st, x, gy, p.A, p.w_delta, p.b_delta, (const float *)(bcw() + u0 * q.R),
                                    (const float *)state(), ND, (int64_t)0, q.B * ND, y, state(), gacc(), 1,
-                                   (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0 + u0, ul, q.chunk_len, ul, 1);
+                                   (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0 + u0, ul, q.chunk_len, ul, 1,
+                                   p.D_res, (int)p.activation, gacc() + 3 * q.B * ND, q.D, (int64_t)0);
             }
             return;
         }
@@ -2655,7 +2711,8 @@ struct Launcher {
             hipLaunchKernelGGL((k_pscan<NT, false, InT, ZOH>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
                                x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)nullptr, (int64_t)0,
                                (int64_t)0, (int64_t)0, y, (float *)nullptr, (float *)nullptr, 0, agg_h(), agg_s(),
-                               q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+                               q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G, (const float *)nullptr, 0,
+                               (float *)nullptr, (int64_t)0, (int64_t)0);
         }
         const int64_t lanes = q.B * ND;
         {
@@ -2663,17 +2720,33 @@ struct Launcher {
             hipLaunchKernelGGL(k_pcarry, dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
                                p.A, agg_h(), agg_s(), state(), q.B, q.D, q.N, G);
         }
+        // The rescan leaves the partials of dl/dD_res in component 1 of
+        // agg_s (the carry has consumed the segment sums; only component 0
+        // holds them in the parameter flows).
+        float *dpart = MAP ? agg_s() + q.D : nullptr;
         {
             Timed tm(3, st, !q.noalloc);
-            hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
-                               x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(), (int64_t)G * 3 * ND,
-                               (int64_t)3 * ND, ND, y, (float *)nullptr, seg_in(), 0, (float *)nullptr,
-                               (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+            hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH, MAP>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads),
+                               0, st, x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(),
+                               (int64_t)G * 3 * ND, (int64_t)3 * ND, ND, y, (float *)nullptr, seg_in(), 0,
+                               (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg,
+                               G, p.D_res, (int)p.activation, dpart, (int64_t)G * 3 * q.D, (int64_t)3 * q.D);
         }
         {
             Timed tm(2, st, !q.noalloc);
-            hipLaunchKernelGGL(k_gsum, dim3((unsigned)((3 * lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
-                               (const float *)seg_in(), gacc(), q.B, ND, G);
+            const int64_t n = 3 * lanes + (MAP ? q.B * q.D : 0);
+            hipLaunchKernelGGL(k_gsum, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
+                               (const float *)seg_in(), gacc(), q.B, ND, G, (const float *)dpart, q.D);
+        }
+    }
+
+    template <bool ZOH, bool MAP>
+    bool pscan_block(int64_t t0, int64_t len) {
+        switch (q.nt) {
+            case 4: pscans<4, ZOH, MAP>(t0, len); return true;
+            case 8: pscans<8, ZOH, MAP>(t0, len); return true;
+            case 16: pscans<16, ZOH, MAP>(t0, len); return true;
+            default: return false;
         }
     }
 
@@ -2683,13 +2756,12 @@ struct Launcher {
             return q.K == 1 ? cscan_block<1>(t0, len) : (q.K == 2 ? cscan_block<2>(t0, len) : false);
         }
         if (q.order == 3) {
-            if (q.ns != 1 || (q.var & ~kZoh)) return false;
-            const bool zoh = (q.var & kZoh) != 0;
-            switch (q.nt) {
-                case 4: zoh ? pscans<4, true>(t0, len) : pscans<4, false>(t0, len); return true;
-                case 8: zoh ? pscans<8, true>(t0, len) : pscans<8, false>(t0, len); return true;
-                case 16: zoh ? pscans<16, true>(t0, len) : pscans<16, false>(t0, len); return true;
-                default: return false;
+            if (q.ns != 1 || (q.var & ~(kZoh | kOutMap))) return false;
+            switch (q.var) {
+                case 0: return pscan_block<false, false>(t0, len);
+                case kZoh: return pscan_block<true, false>(t0, len);
+                case kOutMap: return pscan_block<false, true>(t0, len);
+                default: return pscan_block<true, true>(t0, len);
             }
         }
         if (q.order == 2) {
@@ -2726,7 +2798,7 @@ struct Launcher {
         const unsigned gs = (unsigned)((lanes_all + kThreads - 1) / kThreads);
         const float *d2h_in = q.order == 2 ? p.d2h_in : nullptr;
         float *d2h_out = q.order == 2 ? p.d2h_out : nullptr;
-        const int64_t nacc = 3 * q.B * q.N * q.D;
+        const int64_t nacc = 3 * q.B * q.N * q.D + q.B * q.D;   // gacc with its [B][D] tail
         {
             Timed tm(4, st, !q.noalloc);
             hipLaunchKernelGGL(k_state_import, dim3(gs), dim3(kThreads), 0, st, p.h_in, p.dh_in, d2h_in, state(), q.B,
@@ -2765,9 +2837,10 @@ struct Launcher {
         }
         if (q.order == 3) {
             Timed tm(4, st, !q.noalloc);
-            const int64_t nd3 = 3 * q.N * q.D;
+            float *gD = (q.var & kOutMap) && p.D_res ? p.grad_D_res : nullptr;
+            const int64_t nd3 = 3 * q.N * q.D + (gD ? q.D : 0);
             hipLaunchKernelGGL(k_gout, dim3((unsigned)((nd3 + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
-                               (const float *)gacc(), gA, gB, gC, q.B, q.D, q.N);
+                               (const float *)gacc(), gA, gB, gC, gD, q.B, q.D, q.N);
         }
         if (p.h_out || p.dh_out || d2h_out) {
             Timed tm(4, st, !q.noalloc);

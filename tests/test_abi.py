@@ -288,11 +288,16 @@ def test_low_rank_plans_and_bad_fields():
         assert _call(q) == -1, field
 
 
-def test_parameter_flows_take_only_the_zoh_variant():
-    binding.plan(1, 100, 256, 16, 1, order=3, drive="zoh")
-    for kw in (dict(act="silu"), dict(complex_a=True), dict(groups=4), dict(dt_rank=16)):
+def test_parameter_flows_take_the_zoh_drive_and_the_output_map_only():
+    for kw in (dict(drive="zoh"), dict(act="silu"), dict(drive="zoh", act="silu")):
+        binding.plan(1, 100, 256, 16, 1, order=3, **kw)
+    for kw in (dict(complex_a=True), dict(groups=4), dict(dt_rank=16)):
         with pytest.raises(RuntimeError, match="UNSUPPORTED"):
             binding.plan(1, 100, 256, 16, 1, order=3, **kw)
+    # the second order takes no variant
+    for kw in (dict(drive="zoh"), dict(act="silu")):
+        with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+            binding.plan(1, 100, 256, 16, 2, order=2, **kw)
 
 
 def test_support_matrix_has_kernels():
@@ -308,7 +313,8 @@ def test_support_matrix_has_kernels():
                     assert p["n_per_thread"] * p["n_split"] == N
                     # follow-on paths: one thread per channel, N <= 16, K <= 2
                     for kw in (dict(order=2), dict(order=3), dict(drive="zoh"), dict(act="silu"),
-                               dict(complex_a=True), dict(groups=4), dict(dt_rank=48), dict(order=3, drive="zoh")):
+                               dict(complex_a=True), dict(groups=4), dict(dt_rank=48), dict(order=3, drive="zoh"),
+                               dict(order=3, act="silu"), dict(order=3, drive="zoh", act="silu")):
                         if kw.get("order") == 2 and K != 2:
                             continue
                         ok = N <= 16 and (K <= 2 or kw.get("order") == 3)

@@ -149,25 +149,31 @@ def test_sequential_multiblock_second_order():
     assert e <= gu.TOL, e
 
 
-@pytest.mark.parametrize("drive", ["euler", "zoh"])
-def test_sequential_multiblock_param_grads(drive):
+@pytest.mark.parametrize("drive,omap", [("euler", False), ("zoh", False), ("euler", True), ("zoh", True)])
+def test_sequential_multiblock_param_grads(drive, omap):
+    """omap: SiLU output map with a residual weight (its gradient too)."""
     inp = gu.custom("mamba130m", batch=1, seqlen=L_MB, d_inner=64)
     inp["gy"] = inputs.make_adjoint(inp["cfg"])
-    print(f"case multiblock parameter flows {drive}", flush=True)
-    _plan_blocks(1, 64, 16, 1, order=3, drive=drive)
+    act = "silu" if omap else "identity"
+    if omap:
+        inp["D_res"] = np.random.default_rng(15).standard_normal(64).astype(np.float32)
+    print(f"case multiblock parameter flows {drive} act={act}", flush=True)
+    _plan_blocks(1, 64, 16, 1, order=3, drive=drive, act=act)
     x, _ = gu.inputs_to_dev(inp)
     gy = torch.from_numpy(inp["gy"]).to(gu.dev())
     prm = gu.params_to_dev(inp)
     runs = []
     for cs in CHUNK_SEGS:
-        runs.append(binding.param_grads(x, gy, prm, seg_len=-1, chunk_segs=cs, return_state=True, drive=drive))
+        runs.append(binding.param_grads(x, gy, prm, seg_len=-1, chunk_segs=cs, return_state=True, drive=drive,
+                                        act=act))
         torch.cuda.synchronize()
     _equal_all(runs, "parameter flows")
-    y, gA, gB, gC = runs[0][:4]
-    yo, (GA, GB, GC), _ = oracle.param_grads(inp["x"], inp["gy"], inp, drive=drive)
-    errs = [gu.rel_l2(a.cpu().numpy(), b) for a, b in ((y, yo), (gA, GA), (gB, GB), (gC, GC))]
-    print(f"multiblock param rel_l2 y={errs[0]:.3e} gA={errs[1]:.3e} gB={errs[2]:.3e} gC={errs[3]:.3e}", flush=True)
-    assert max(errs) <= gu.TOL, errs
+    ng = 4 if omap else 3
+    got = runs[0][:1 + ng]
+    yo, G, _ = oracle.param_grads(inp["x"], inp["gy"], inp, drive=drive, act=act)
+    errs = [gu.rel_l2(a.cpu().numpy(), b) for a, b in zip(got, (yo,) + tuple(G))]
+    print("multiblock param rel_l2 " + " ".join(f"{e:.3e}" for e in errs), flush=True)
+    assert len(errs) == 1 + ng and max(errs) <= gu.TOL, errs
 
 
 def test_sequential_multiblock_linear_attention():

@@ -31,18 +31,22 @@ def _run(inp, **kw):
 
 
 def _check(inp, what, channels=None, **kw):
+    """y and every gradient (dl/dD_res too when inp has D_res) against the
+    oracle, optionally on sampled channels only."""
     print(f"case {what}", flush=True)
-    y, gA, gB, gC = _run(inp, **kw)[:4]
-    yo, (GA, GB, GC), _ = oracle.param_grads(inp["x"], inp["gy"], inp, channels=channels,
-                                             chunk=None if channels is None else 8192,
-                                             drive=kw.get("drive", "euler"))
+    ng = 4 if inp.get("D_res") is not None else 3
+    got = list(_run(inp, **kw)[:1 + ng])
+    yo, G, _ = oracle.param_grads(inp["x"], inp["gy"], inp, channels=channels,
+                                  chunk=None if channels is None else 8192,
+                                  drive=kw.get("drive", "euler"), act=kw.get("act", "identity"))
+    assert len(G) == ng
     if channels is not None:
         idx = torch.from_numpy(np.asarray(channels)).to(gu.dev())
-        y = y.index_select(-1, idx)
-        gA, gB, gC = (g.index_select(0, idx) for g in (gA, gB, gC))
-    errs = [gu.rel_l2(a.cpu().numpy(), b) for a, b in ((y, yo), (gA, GA), (gB, GB), (gC, GC))]
-    print(f"{what} rel_l2 y={errs[0]:.3e} gA={errs[1]:.3e} gB={errs[2]:.3e} gC={errs[3]:.3e}", flush=True)
-    for a in (y, gA, gB, gC):
+        got = [got[0].index_select(-1, idx)] + [g.index_select(0, idx) for g in got[1:]]
+    errs = [gu.rel_l2(a.cpu().numpy(), b) for a, b in zip(got, (yo,) + tuple(G))]
+    names = ("y", "gA", "gB", "gC", "gD")
+    print(f"{what} rel_l2 " + " ".join(f"{n}={e:.3e}" for n, e in zip(names, errs)), flush=True)
+    for a in got:
         assert torch.all(torch.isfinite(a))
     assert max(errs) <= gu.TOL, (what, errs)
 
@@ -179,3 +183,99 @@ def test_param_grads_zoh_full_size_sampled_channels():
     g = np.random.default_rng(6)
     ch = np.unique(np.concatenate([[0, 1535], g.choice(np.arange(1, 1535), 4, replace=False)]))
     _check(inp, "param zoh pulse128k full", channels=ch, drive="zoh")
+
+
+# ------------------------------------------------------------ output map
+# y = act(sum_n C h + D_res x): the sums take w = gy act'(yhat) in place of
+# gy, and dl/dD_res = sum w x is returned as a fourth gradient.
+
+def _with_dres(inp, seed=17):
+    inp["D_res"] = np.random.default_rng(seed).standard_normal(inp["x"].shape[-1]).astype(np.float32)
+    return inp
+
+
+@pytest.mark.parametrize("act,dres,drive,N,seg", [
+    ("silu", True, "euler", 16, 0), ("silu", False, "euler", 8, -1), ("identity", True, "zoh", 16, 64),
+    ("silu", True, "zoh", 4, -1), ("silu", True, "euler", 16, -1), ("silu", True, "zoh", 16, 0)])
+def test_param_grads_output_map_parity(act, dres, drive, N, seg):
+    inp = _case("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N)
+    if dres:
+        _with_dres(inp)
+    _check(inp, f"param map act={act} dres={dres} {drive} N={N} seg={seg}", seg_len=seg, drive=drive, act=act)
+
+
+def test_param_grads_output_map_bf16_stiff():
+    _check(_with_dres(_case("stiff128k", seqlen=1500, d_inner=64)), "param map stiff bf16", act="silu")
+
+
+def test_param_grads_output_map_primal_and_blocks():
+    """y equals pgf_scan_jvp's with the same output map bit for bit; every
+    output (dl/dD_res included) is bit-identical for every host block size;
+    a split call chained through the state, adding into the same four
+    buffers, matches one call up to the rounding of the additions."""
+    inp = _with_dres(_case("mamba130m", batch=2, seqlen=1000, d_inner=48))
+    for seg in (64, -1):
+        y = _run(inp, seg_len=seg, chunk_segs=4, act="silu")[0]
+        y1, _ = gu.run(inp, seg_len=seg, chunk_segs=4, act="silu")
+        assert torch.equal(y, y1), seg
+    ref = _run(inp, seg_len=64, chunk_segs=1, return_state=True, act="silu")
+    assert len(ref) == 7
+    for cs in (3, 0):
+        got = _run(inp, seg_len=64, chunk_segs=cs, return_state=True, act="silu")
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), cs
+    x, _ = gu.inputs_to_dev(inp)
+    gy = torch.from_numpy(inp["gy"]).to(gu.dev())
+    prm = gu.params_to_dev(inp)
+    s = 384
+    a = binding.param_grads(x[:, :s], gy[:, :s], prm, seg_len=64, return_state=True, act="silu")
+    b = binding.param_grads(x[:, s:], gy[:, s:], prm, seg_len=64, h_in=a[5], gamma_in=a[6], grads=a[1:5],
+                            return_state=True, act="silu")
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat([a[0], b[0]], 1), ref[0])
+    assert torch.equal(b[5], ref[5]) and torch.equal(b[6], ref[6])
+    for i in (1, 2, 3, 4):
+        assert gu.rel_l2(b[i].cpu().numpy(), ref[i].cpu().numpy()) < 1e-6, i
+
+
+def test_param_grads_output_map_identity_residual():
+    """Identity map with D_res: the flows of A, B, C are those without the
+    residual weight bit for bit (only y changes), and dl/dD_res equals
+    sum over b and t of gy x (the closed form), to rounding."""
+    inp = _case("mamba130m", batch=2, seqlen=800, d_inner=64)
+    base = _run(inp, seg_len=128)
+    got = _run(_with_dres(inp), seg_len=128)
+    for i in (1, 2, 3):
+        assert torch.equal(got[i], base[i]), i
+    ref = (inp["gy"].astype(np.float64) * inp["x"].astype(np.float64)).sum((0, 1))
+    assert gu.rel_l2(got[4].cpu().numpy(), ref) < 1e-6
+
+
+def test_param_grads_output_map_full_size_sampled_channels():
+    inp = _with_dres(_case("pulse128k"))
+    g = np.random.default_rng(7)
+    ch = np.unique(np.concatenate([[0, 1535], g.choice(np.arange(1, 1535), 4, replace=False)]))
+    _check(inp, "param map pulse128k full", channels=ch, act="silu")
+
+
+def test_param_grads_output_map_argument_checks():
+    inp = _with_dres(_case("tiny", seqlen=64))
+    x, _ = gu.inputs_to_dev(inp)
+    gy = torch.zeros_like(x)
+    prm = gu.params_to_dev(inp)
+    D, N = inp["A"].shape
+    with pytest.raises(ValueError, match="grads"):   # three buffers where D_res needs four
+        binding.param_grads(x, gy, prm, grads=tuple(torch.zeros(D, N, device=gu.dev()) for _ in range(3)))
+    # through the C-ABI: D_res set and grad_D_res NULL
+    pr = binding.make_params(1, 64, D, N, 1, order=3, act="silu")
+    keep = []
+    binding._model_params(pr, prm, D, gu.dev(), keep)
+    pr.D_res = prm["D_res"].data_ptr()
+    ws = torch.empty(binding.workspace_bytes(1, 64, D, N, 1, order=3, act="silu"), dtype=torch.uint8,
+                     device=gu.dev())
+    pr.workspace, pr.workspace_bytes = ws.data_ptr(), ws.numel()
+    y = torch.empty_like(x)
+    g3 = [torch.zeros(D, N, device=gu.dev()) for _ in range(3)]
+    rc = binding.lib().pgf_param_grads(x.data_ptr(), gy.data_ptr(), ctypes.byref(pr), y.data_ptr(),
+                                       *[g.data_ptr() for g in g3], None)
+    assert rc == -1   # PGF_ERR_INVALID_ARG
