@@ -279,3 +279,13 @@ def test_param_grads_output_map_argument_checks():
     rc = binding.lib().pgf_param_grads(x.data_ptr(), gy.data_ptr(), ctypes.byref(pr), y.data_ptr(),
                                        *[g.data_ptr() for g in g3], None)
     assert rc == -1   # PGF_ERR_INVALID_ARG
+
+
+def test_param_grads_zoh_zero_eigenvalues():
+    """Columns of A exactly 0 with the ZOH drive: e and de/dA take their
+    limits Delta and Delta^2/2 (the closed forms' 1/A must not leak)."""
+    inp = _case("mamba130m", batch=1, seqlen=1000, d_inner=64)
+    inp["A"] = inp["A"].copy()
+    inp["A"][:, [0, 9]] = 0.0
+    for seg in (64, -1):
+        _check(inp, f"param zoh zero eigenvalues seg={seg}", seg_len=seg, drive="zoh")

@@ -81,3 +81,43 @@ def test_variant_limits():
         binding.plan(1, 100, 64, 32, 1, act="silu")
     with pytest.raises(RuntimeError, match="UNSUPPORTED"):
         binding.plan(1, 100, 64, 16, 2, order=2, drive="zoh")
+
+
+# ------------------------------------------------------------ degenerate cases
+
+@pytest.mark.parametrize("seg", [0, -1])
+def test_zoh_zero_eigenvalues(seg):
+    """Columns of A exactly 0: the ZOH coefficient takes its limit e = Delta
+    (the series branch; the closed form's 1/A is infinite and must not leak
+    into the result), and those lanes integrate without decay."""
+    inp = gu.custom("mamba130m", batch=1, seqlen=1200, d_inner=64, n_dirs=2)
+    inp["A"] = inp["A"].copy()
+    inp["A"][:, [0, 5]] = 0.0
+    inp["A"][7, :] = 0.0            # and one channel with every eigenvalue 0
+    _check(inp, f"zoh zero eigenvalues seg={seg}", drive="zoh", seg_len=seg)
+
+
+@pytest.mark.parametrize("seg", [64, -1])
+def test_vanishing_step_keeps_the_state(seg):
+    """A channel whose step size underflows (softplus(-200) is 0 in f32):
+    Abar = 1 and no drive, so its state and tangent state leave the call
+    exactly as they entered, for both drives; the others match the oracle."""
+    inp = gu.custom("mamba130m", batch=1, seqlen=700, d_inner=64, n_dirs=1)
+    inp["b_delta"] = inp["b_delta"].copy()
+    inp["w_delta"] = inp["w_delta"].copy()
+    inp["b_delta"][3] = -200.0
+    inp["w_delta"][3] = 0.0
+    g = np.random.default_rng(8)
+    h0 = torch.from_numpy(g.standard_normal((1, 64, 16)).astype(np.float32)).to(gu.dev())
+    dh0 = torch.from_numpy(g.standard_normal((1, 1, 64, 16)).astype(np.float32)).to(gu.dev())
+    x, dx = gu.inputs_to_dev(inp)
+    prm = gu.params_to_dev(inp)
+    for drive in ("euler", "zoh"):
+        print(f"case vanishing step {drive} seg={seg}", flush=True)
+        y, dy, h, dh = binding.scan_jvp(x, dx, prm, h_in=h0, dh_in=dh0, seg_len=seg, drive=drive,
+                                        return_state=True)
+        torch.cuda.synchronize()
+        assert torch.equal(h[:, 3], h0[:, 3]) and torch.equal(dh[:, :, 3], dh0[:, :, 3]), drive
+        yo, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp, h_in=h0.cpu().numpy(), dh_in=dh0.cpu().numpy(),
+                                        drive=drive)
+        gu.assert_close(y.cpu().numpy(), dy.cpu().numpy(), yo, dyo, what=f"vanishing step {drive}")
