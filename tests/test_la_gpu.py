@@ -65,6 +65,20 @@ def test_la_wide_values_and_constant_decay():
     _check(inp, "la retnet decay")
 
 
+@pytest.mark.parametrize("seg", [0, -1])
+def test_la_degenerate_decays(seg):
+    """No decay (g = 0: the linear transformer, every segment transition 1,
+    the state only grows) and a decay that underflows (g = -200: alpha is 0
+    in f32, so S_t = k_t v_t^T and o_t = (q_t . k_t) v_t) in two heads of
+    one call, with tangents of g zero in the first and N(0,1) in the
+    second."""
+    inp = _case(heads=2, seqlen=1100, d_key=32)
+    inp["g"][:, 0] = 0.0
+    inp["dg"][:, :, 0] = 0.0
+    inp["g"][:, 1] = -200.0
+    _check(inp, f"la degenerate decays seg={seg}", seg_len=seg)
+
+
 def test_la_full_size_sampled_heads():
     """rwkv128k (B=1, H=32, L=131072, dk=dv=64) in the default plan; heads are
     independent, so the oracle runs on two of them."""
