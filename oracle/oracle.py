@@ -70,7 +70,7 @@ def declare(lib):
     lib.pgf_oracle_core2.restype = ctypes.c_int
     lib.pgf_oracle_core2.argtypes = [i64] * 4 + [dp] * 22 + [ctypes.c_int]
     lib.pgf_oracle_param.restype = ctypes.c_int
-    lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 14 + [ctypes.c_int, dp, ctypes.c_int, ctypes.c_int]
+    lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 14 + [ctypes.c_int] + [dp] * 6 + [ctypes.c_int, ctypes.c_int]
     lib.pgf_oracle_la.restype = ctypes.c_int
     lib.pgf_oracle_la.argtypes = [i64] * 6 + [dp] * 12 + [ctypes.c_int]
     lib.pgf_oracle_core_cplx.restype = ctypes.c_int
@@ -388,15 +388,20 @@ def scan_jvp2(x, dxv, dxw, params, state=None, channels=None, chunk=None, nthrea
 ACTIVATIONS = {"identity": 0, "silu": 1}
 
 
-def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None, drive="euler", act="identity", D_res=None):
+def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None, drive="euler", act="identity", D_res=None,
+               sig=None):
     """Parameter-sensitivity flows (see pgf_oracle_param).  Shapes: A [D,N];
     x, delta, gy [B,L,D]; Bm, Cm [B,L,N]; state = (h, GammaA, GammaB), each
     [B,D,N] (zero when None); drive "euler" or "zoh" (the zero-order-hold
     drive, whose A-dependence enters GammaA); act "identity" or "silu" and
     D_res [D] or None: the output map y = act(sum_n C h + D_res x).
+    sig [B,L,D] (sigmoid of the step size's pre-activation) adds the flows
+    of w_delta and b_delta: the state tuple then has five entries (h,
+    GammaA, GammaB, Gamma_w, Gamma_s).
     Returns y [B,L,D], (GA, GB, GC) each [B,D,N] (this call's contributions
     per batch row), plus GD [B,D] (dl/dD_res per batch row) when D_res is
-    given, and the exit state tuple."""
+    given, plus GW, GS [B,D] (dl/dw_delta, dl/db_delta) when sig is, and the
+    exit state tuple."""
     lib = _load()
     A = _f64(A)
     x, delta, gy, Bm, Cm = (_f64(a) for a in (x, delta, gy, Bm, Cm))
@@ -404,10 +409,12 @@ def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None, drive="euler"
     N = A.shape[1]
     assert delta.shape == (B, L, D) and gy.shape == (B, L, D)
     assert Bm.shape == (B, L, N) and Cm.shape == (B, L, N)
+    ns = 3 if sig is None else 5
     if state is None:
-        st = [np.zeros((B, D, N)) for _ in range(3)]
+        st = [np.zeros((B, D, N)) for _ in range(ns)]
     else:
         st = [np.array(s, dtype=np.float64, copy=True, order="C") for s in state]
+    assert len(st) == ns
     for s_ in st:
         assert s_.shape == (B, D, N)
     y = np.empty((B, L, D))
@@ -415,19 +422,26 @@ def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None, drive="euler"
     Dr = None if D_res is None else _f64(D_res)
     GD = None if D_res is None else np.zeros((B, D))
     null = ctypes.POINTER(ctypes.c_double)()
+    sg = None if sig is None else _f64(sig)
+    GWS = None if sig is None else [np.zeros((B, D)), np.zeros((B, D))]
+    if sg is not None:
+        assert sg.shape == (B, L, D)
+    dres = [null if Dr is None else _dp(Dr), ACTIVATIONS[act], null if GD is None else _dp(GD)]
+    dlt = [null] * 5 if sg is None else [_dp(sg), _dp(st[3]), _dp(st[4]), _dp(GWS[0]), _dp(GWS[1])]
     rc = lib.pgf_oracle_param(B, L, D, N, _dp(A), _dp(x), _dp(delta), _dp(gy), _dp(Bm), _dp(Cm),
-                              *[_dp(s_) for s_ in st], _dp(y), *[_dp(g) for g in G],
-                              null if Dr is None else _dp(Dr), ACTIVATIONS[act], null if GD is None else _dp(GD),
+                              *[_dp(s_) for s_ in st[:3]], _dp(y), *[_dp(g) for g in G], *dres, *dlt,
                               DRIVES[drive], _threads() if nthreads is None else nthreads)
     if rc != 0:
         raise RuntimeError("pgf_oracle_param failed")
     if GD is not None:
         G.append(GD)
+    if GWS is not None:
+        G.extend(GWS)
     return y, tuple(G), tuple(st)
 
 
 def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=None, drive="euler",
-                act="identity"):
+                act="identity", delta_params=False):
     """Primal output and online parameter gradients of the full model over
     L-chunks (App. E, Alg. 2).  x, gy [B,L,D]; params as scan_jvp; channels:
     optional 1-D index array of the channels d to compute (the projections
@@ -439,7 +453,10 @@ def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=N
     G_B and G_C are the gradients with respect to per-lane offsets of B and
     C, so that dl/db_B = G_B.sum(0) and dl/db_C = G_C.sum(0).  act and
     params["D_res"] (if present) set the output map y = act(C h + D_res x);
-    with D_res the gradient tuple gains G_D = dl/dD_res [Dsel]."""
+    with D_res the gradient tuple gains G_D = dl/dD_res [Dsel].  With
+    delta_params it then gains dl/dw_delta and dl/db_delta [Dsel] (the
+    step size's parameters), and the state holds Gamma_w and Gamma_s after
+    GammaB."""
     B, L, D = np.shape(x)
     A = _f64(params["A"])
     N = A.shape[1]
@@ -451,7 +468,8 @@ def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=N
     Dr = params.get("D_res")
     Dr = None if Dr is None else _f64(Dr)[sel]
     y = np.empty((B, L, Ds))
-    tot = [np.zeros((B, Ds, N)) for _ in range(3)] + ([] if Dr is None else [np.zeros((B, Ds))])
+    tot = [np.zeros((B, Ds, N)) for _ in range(3)] + ([] if Dr is None else [np.zeros((B, Ds))]) + \
+        ([np.zeros((B, Ds)), np.zeros((B, Ds))] if delta_params else [])
     st = state
     step = max(1, L if not chunk else int(chunk))
     for t0 in range(0, L, step):
@@ -461,13 +479,14 @@ def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=N
                                params.get("b_C"))
         xs = np.ascontiguousarray(xc[..., sel])
         delta, _ = discretize(xs, xs[None], w, bd)
+        sig = expit(xs * w + bd) if delta_params else None
         gs = np.ascontiguousarray(_f64(gy[:, t0:t1])[..., sel])
-        yc, G, st = core_param(As, xs, delta, gs, Bm, Cm, st, nthreads, drive, act, Dr)
+        yc, G, st = core_param(As, xs, delta, gs, Bm, Cm, st, nthreads, drive, act, Dr, sig)
         y[:, t0:t1] = yc
         for i in range(len(tot)):
             tot[i] += G[i]
     if st is None:
-        st = tuple(np.zeros((B, Ds, N)) for _ in range(3))
+        st = tuple(np.zeros((B, Ds, N)) for _ in range(5 if delta_params else 3))
     return y, tuple(g.sum(0) for g in tot), st
 
 

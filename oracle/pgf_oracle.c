@@ -259,7 +259,19 @@ int pgf_oracle_core2(int64_t B, int64_t L, int64_t D, int64_t N,
  * Shapes (double, row-major): A [D,N]; x, delta, gy [B,L,D];
  * Bm, Cm [B,L,N]; h, gA, gB [B,D,N] (entry state in, exit state out);
  * y [B,L,D] (written); GA, GB, GC [B,D,N] and GD [B,D] (added to, per batch
- * row).  Returns 0, or -1 on a bad argument.
+ * row).
+ *
+ * The step-size parameters (Sec. 3: Delta = softplus(w_delta x + b_delta)),
+ * when sig [B,L,D] = sigmoid(w_delta x + b_delta) is given: dDelta/db_delta
+ * = sig and dDelta/dw_delta = sig*x, and the state moves with Delta by
+ * dh'/dDelta = A*Abar*h + Abar^z*B*x (z = 1 with ZOH, whose drive
+ * coefficient has derivative Abar in Delta; z = 0 with Euler), so per lane
+ *   Gamma_w' = Abar*Gamma_w + sig*x*(dh'/dDelta)   (gW, dh/dw_delta)
+ *   Gamma_s' = Abar*Gamma_s + sig*(dh'/dDelta)     (gS, dh/db_delta)
+ * and, per channel, GW[b,d] += w*sum_n C*Gamma_w', GS[b,d] += w*sum_n
+ * C*Gamma_s' (dl/dw_delta, dl/db_delta).  gW, gS [B,D,N] carry the state
+ * like h; GW, GS [B,D] are added to.  All four may be NULL when sig is.
+ * Returns 0, or -1 on a bad argument.
  */
 
 /* d/dA of e(A) = expm1(Delta*A)/A: (Delta*exp(Delta*A) - e)/A.  The closed
@@ -285,10 +297,12 @@ int pgf_oracle_param(int64_t B, int64_t L, int64_t D, int64_t N,
                      const double *Bm, const double *Cm,
                      double *h, double *gA, double *gB,
                      double *y, double *GA, double *GB, double *GC,
-                     const double *D_res, int act, double *GD, int drive, int nthreads)
+                     const double *D_res, int act, double *GD,
+                     const double *sig, double *gW, double *gS, double *GW, double *GS, int drive, int nthreads)
 {
     if (B < 0 || L < 0 || D < 0 || N <= 0 || drive < 0 || drive > 1 || act < 0 || act > 1) return -1;
     if (!A || !h || !gA || !gB || !GA || !GB || !GC || (D_res && !GD)) return -1;
+    if (sig && (!gW || !gS || !GW || !GS)) return -1;
     if (L > 0 && (!x || !delta || !gy || !Bm || !Cm || !y)) return -1;
     const int64_t lanes = B * D;
 #ifdef _OPENMP
@@ -317,6 +331,12 @@ int pgf_oracle_param(int64_t B, int64_t L, int64_t D, int64_t N,
                 const double ga = abar * gA[i] + dl * abar * hprev + ea * Bm[btn + n] * xt;
                 const double gb = abar * gB[i] + ec * xt;
                 const double hnew = abar * hprev + ec * Bm[btn + n] * xt;
+                if (sig) {
+                    /* the state's derivative in Delta, then the two flows */
+                    const double hd = an * abar * hprev + (drive ? abar : 1.0) * Bm[btn + n] * xt;
+                    gW[i] = abar * gW[i] + sig[btd] * xt * hd;
+                    gS[i] = abar * gS[i] + sig[btd] * hd;
+                }
                 h[i] = hnew; gA[i] = ga; gB[i] = gb;
                 yhat += Cm[btn + n] * hnew;
             }
@@ -338,6 +358,16 @@ int pgf_oracle_param(int64_t B, int64_t L, int64_t D, int64_t N,
                 GC[i] += w * h[i];
             }
             if (D_res) GD[b * D + d] += w * xt;
+            if (sig) {
+                double cw = 0.0, cs = 0.0;
+                for (int64_t n = 0; n < N; ++n) {
+                    const int64_t i = (b * D + d) * N + n;
+                    cw += Cm[btn + n] * gW[i];
+                    cs += Cm[btn + n] * gS[i];
+                }
+                GW[b * D + d] += w * cw;
+                GS[b * D + d] += w * cs;
+            }
         }
     }
     return 0;

@@ -24,6 +24,11 @@ PIN_TESTS = [
     lambda: pins.test_output_map_identity_residual_closed_form(),
     lambda: pins.test_output_map_central_differences(),
     lambda: pins.test_output_map_one_step_adjoint(),
+    lambda: pins.test_step_size_reverse_mode_autograd("euler", "identity", False),
+    lambda: pins.test_step_size_reverse_mode_autograd("zoh", "silu", False),
+    lambda: pins.test_step_size_central_differences(),
+    lambda: pins.test_step_size_segment_composition_and_chunks(),
+    lambda: pins.test_step_size_one_step_adjoint(),
 ]
 
 C_MUTANTS = {
@@ -57,6 +62,21 @@ C_MUTANTS = {
     "G_D from the output": ("if (D_res) GD[b * D + d] += w * xt;", "if (D_res) GD[b * D + d] += w * yt;"),
     "G_D against the raw adjoint": ("if (D_res) GD[b * D + d] += w * xt;",
                                     "if (D_res) GD[b * D + d] += gy[btd] * xt;"),
+    "dh/dDelta without the transition's term": (
+        "const double hd = an * abar * hprev + (drive ? abar : 1.0) * Bm[btn + n] * xt;",
+        "const double hd = (drive ? abar : 1.0) * Bm[btn + n] * xt;"),
+    "dh/dDelta with the ZOH drive's derivative taken as 1": (
+        "const double hd = an * abar * hprev + (drive ? abar : 1.0) * Bm[btn + n] * xt;",
+        "const double hd = an * abar * hprev + Bm[btn + n] * xt;"),
+    "dh/dDelta from the new state": (
+        "const double hd = an * abar * hprev + (drive ? abar : 1.0) * Bm[btn + n] * xt;",
+        "const double hd = an * hnew + (drive ? abar : 1.0) * Bm[btn + n] * xt;"),
+    "Gamma_w without x": ("gW[i] = abar * gW[i] + sig[btd] * xt * hd;", "gW[i] = abar * gW[i] + sig[btd] * hd;"),
+    "Gamma_w without decay": ("gW[i] = abar * gW[i] + sig[btd] * xt * hd;", "gW[i] = gW[i] + sig[btd] * xt * hd;"),
+    "Gamma_s without sigma": ("gS[i] = abar * gS[i] + sig[btd] * hd;", "gS[i] = abar * gS[i] + hd;"),
+    "G_w without C": ("cw += Cm[btn + n] * gW[i];", "cw += gW[i];"),
+    "G_s from Gamma_w": ("cs += Cm[btn + n] * gS[i];", "cs += Cm[btn + n] * gW[i];"),
+    "G_w against the raw adjoint": ("GW[b * D + d] += w * cw;", "GW[b * D + d] += gy[btd] * cw;"),
 }
 
 

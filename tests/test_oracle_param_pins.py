@@ -27,13 +27,17 @@ def problem(seed, B=2, L=14, D=3, N=4, stiff=False):
     return p, x, gy
 
 
-def _torch_loss(p, x, gy, A, beta_B, beta_C, drive="euler", act="identity", D_res=None):
+def _torch_loss(p, x, gy, A, beta_B, beta_C, drive="euler", act="identity", D_res=None, w_delta=None,
+                b_delta=None):
     """l = sum gy*y of the selective scan as a plain torch loop, with the
     per-lane offsets beta_B, beta_C [D,N] added to B_t and C_t; drive "zoh"
     takes b = expm1(Delta A)/A * B x (A != 0 everywhere here); act "silu"
-    and D_res [D] (a tensor) give y = silu(C h + D_res x)."""
+    and D_res [D] (a tensor) give y = silu(C h + D_res x); w_delta, b_delta
+    (tensors) replace the step size's parameters of p."""
     xt = torch.tensor(x)
-    z = xt * torch.tensor(p["w_delta"]) + torch.tensor(p["b_delta"])
+    w_delta = torch.tensor(p["w_delta"]) if w_delta is None else w_delta
+    b_delta = torch.tensor(p["b_delta"]) if b_delta is None else b_delta
+    z = xt * w_delta + b_delta
     delta = torch.logaddexp(z, torch.zeros((), dtype=torch.float64))
     Bm = xt @ torch.tensor(p["W_B"]) + torch.tensor(p["b_B"])
     Cm = xt @ torch.tensor(p["W_C"]) + torch.tensor(p["b_C"])
@@ -318,3 +322,91 @@ def test_output_map_one_step_adjoint():
     refD = np.zeros(3)
     refD[d] = w * x[b, t0, d]
     assert relerr(GD, refD) < 1e-14
+
+
+# ---------------------------------------------------------------- step-size parameters
+# Delta = softplus(w_delta x + b_delta): the flows Gamma_w = dh/dw_delta and
+# Gamma_s = dh/db_delta, driven by dh'/dDelta times sigma*x and sigma.
+
+@pytest.mark.parametrize("drive,act,stiff", [("euler", "identity", False), ("zoh", "identity", True),
+                                             ("euler", "silu", False), ("zoh", "silu", False)])
+def test_step_size_reverse_mode_autograd(drive, act, stiff):
+    p, x, gy = problem(80, stiff=stiff)
+    if act == "silu":
+        p["D_res"] = np.random.default_rng(81).standard_normal(p["A"].shape[0])
+    y, G, _ = oracle.param_grads(x, gy, p, drive=drive, act=act, delta_params=True)
+    GW, GS = G[-2], G[-1]
+    A = torch.tensor(p["A"], requires_grad=True)
+    zero = lambda: torch.zeros(p["A"].shape, dtype=torch.float64, requires_grad=True)
+    bB, bC = zero(), zero()
+    w = torch.tensor(p["w_delta"], requires_grad=True)
+    b = torch.tensor(p["b_delta"], requires_grad=True)
+    Dr = None if act != "silu" else torch.tensor(p["D_res"])
+    _torch_loss(p, x, gy, A, bB, bC, drive=drive, act=act, D_res=Dr, w_delta=w, b_delta=b).backward()
+    assert relerr(GW, w.grad.numpy()) < 1e-11
+    assert relerr(GS, b.grad.numpy()) < 1e-11
+    # the other gradients and the primal do not change with the extra flows
+    y0, G0, _ = oracle.param_grads(x, gy, p, drive=drive, act=act)
+    assert np.array_equal(y, y0) and all(np.array_equal(a, c) for a, c in zip(G0, G[:len(G0)]))
+    assert relerr(G[0], A.grad.numpy()) < (1e-10 if drive == "zoh" else 1e-12)
+
+
+def test_step_size_central_differences():
+    """<G_w, dw> and <G_s, db> against central differences of the separately
+    pinned first-order primal (ZOH drive, SiLU map, residual weight)."""
+    p, x, gy = problem(82, L=18)
+    p["D_res"] = np.random.default_rng(83).standard_normal(p["A"].shape[0])
+    _, G, _ = oracle.param_grads(x, gy, p, drive="zoh", act="silu", delta_params=True)
+
+    def loss(q):
+        y, _, _, _ = oracle.scan_jvp(x, x[None] * 0.0, q, drive="zoh", act="silu")
+        return float((gy * y).sum())
+
+    g = np.random.default_rng(84)
+    eps = 1e-6
+    for key, Gk in (("w_delta", G[-2]), ("b_delta", G[-1])):
+        dP = g.standard_normal(p[key].shape)
+        fd = (loss(dict(p, **{key: p[key] + eps * dP})) - loss(dict(p, **{key: p[key] - eps * dP}))) / (2 * eps)
+        assert abs(fd - (Gk * dP).sum()) < 1e-7 * max(1.0, abs(fd)), (key, fd, (Gk * dP).sum())
+
+
+def test_step_size_segment_composition_and_chunks():
+    """Over a block with S = sum Delta, P = exp(A S), the step-size flows'
+    exit state from entry (h, .., Gamma_w, Gamma_s) is P Gamma + P A S_theta h
+    + Gamma0 (Gamma0 from a zero start, S_theta = sum sigma x for w and
+    sum sigma for b): the carry the GPU uses.  Chunked evaluation equals one
+    pass."""
+    p, x, gy = problem(85, L=17)
+    g = np.random.default_rng(86)
+    ent = tuple(g.standard_normal((2, 3, 4)) for _ in range(5))
+    _, _, z = oracle.param_grads(x, gy, p, delta_params=True)
+    _, _, e = oracle.param_grads(x, gy, p, state=ent, delta_params=True)
+    delta, _ = oracle.discretize(x, x[None], p["w_delta"], p["b_delta"])
+    sg = 1.0 / (1.0 + np.exp(-(x * p["w_delta"] + p["b_delta"])))
+    S = delta.sum(1)[:, :, None]
+    P = np.exp(p["A"][None] * S)
+    Sw = (sg * x).sum(1)[:, :, None]
+    Ss = sg.sum(1)[:, :, None]
+    assert relerr(e[3], P * ent[3] + P * p["A"][None] * Sw * ent[0] + z[3]) < 1e-13
+    assert relerr(e[4], P * ent[4] + P * p["A"][None] * Ss * ent[0] + z[4]) < 1e-13
+    y, G, st = oracle.param_grads(x, gy, p, delta_params=True)
+    y2, G2, st2 = oracle.param_grads(x, gy, p, chunk=5, delta_params=True)
+    assert relerr(y2, y) < 1e-15
+    for a, b in zip(G + st, G2 + st2):
+        assert relerr(b, a) < 1e-13
+
+
+def test_step_size_one_step_adjoint():
+    """An adjoint at one (b, t0, d) and a single step: from a zero state,
+    h_1 = Delta B x, so dh_1/dDelta = B x and G_s = gy sigma sum_n C B x,
+    G_w = G_s x (Euler drive, identity map)."""
+    p, x, _ = problem(87, B=1, L=1)
+    gy = np.zeros_like(x)
+    gy[0, 0, 2] = 1.3
+    _, G, _ = oracle.param_grads(x, gy, p, delta_params=True)
+    Bm, Cm, _, _ = oracle.project(x, x[None], p["W_B"], p["W_C"], p["b_B"], p["b_C"])
+    xv = x[0, 0, 2]
+    sg = 1.0 / (1.0 + np.exp(-(xv * p["w_delta"][2] + p["b_delta"][2])))
+    ref_s = 1.3 * sg * (Cm[0, 0] * Bm[0, 0]).sum() * xv
+    assert abs(G[-1][2] - ref_s) < 1e-14 * abs(ref_s) and abs(G[-2][2] - ref_s * xv) < 1e-14 * abs(ref_s * xv)
+    assert np.all(G[-1][[0, 1]] == 0) and np.all(G[-2][[0, 1]] == 0)
