@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--drive", default="euler", choices=("euler", "zoh"), help="input drive (first order)")
     ap.add_argument("--act", default="identity", choices=("identity", "silu"), help="output activation (first order and parameter flows)")
     ap.add_argument("--dres", action="store_true", help="add a residual weight D_res ~ N(0,1) to the output map")
+    ap.add_argument("--delta-params", action="store_true",
+                    help="parameter flows (--order 3): also the flows of w_delta and b_delta")
     ap.add_argument("--groups", type=int, default=1,
                     help="channel groups with their own B and C (first order; D/groups a multiple of 64)")
     ap.add_argument("--complex", action="store_true",
@@ -221,8 +223,11 @@ class Workload:
 def setup_ssm(args, np, torch, binding, inputs):
     cfg = inputs.get_config(args.workload)
     variant = args.drive != "euler" or args.act != "identity" or args.dres or args.complex or args.groups > 1 or \
-        args.lowrank > 0
+        args.lowrank > 0 or args.delta_params
     param_variant = args.order == 3 and not (args.complex or args.groups > 1 or args.lowrank > 0)
+    if args.delta_params and args.order != 3:
+        print("bench.py: --delta-params belongs to the parameter flows (--order 3)", file=sys.stderr)
+        sys.exit(2)
     if variant and args.order != 1 and not param_variant:
         print("bench.py: --complex/--groups/--lowrank apply to the first order only, --drive/--act/--dres to the "
               "first order and the parameter flows", file=sys.stderr)
@@ -249,7 +254,8 @@ def setup_ssm(args, np, torch, binding, inputs):
     if args.order == 3:
         gy = torch.from_numpy(inputs.make_adjoint(cfg)).to(dev)
         grads = tuple(torch.zeros((D, N), device=dev) for _ in range(3)) + \
-            ((torch.zeros(D, device=dev),) if args.dres else ())
+            ((torch.zeros(D, device=dev),) if args.dres else ()) + \
+            ((torch.zeros(D, device=dev), torch.zeros(D, device=dev)) if args.delta_params else ())
         payload = x.numel() * s_in + gy.numel() * 4 + y.numel() * 4 + sum(g.numel() * 4 for g in grads)
     else:
         dx = torch.from_numpy(inp["dx"]).to(dev).to(tdt)
@@ -261,13 +267,15 @@ def setup_ssm(args, np, torch, binding, inputs):
             payload += x.numel() * 4
     del inp
     plan = binding.plan(B, L, D, N, K, cfg.in_dtype, args.seg_len, args.chunk_segs, args.order, args.drive, args.act,
-                        complex_a=args.complex, groups=args.groups, dt_rank=args.lowrank)
+                        complex_a=args.complex, groups=args.groups, dt_rank=args.lowrank,
+                        delta_flows=args.delta_params)
     ws = torch.empty(plan["workspace_bytes"], device=dev, dtype=torch.uint8)
 
     if args.order == 3:
         def step():
             binding.param_grads(x, gy, params, grads=grads, workspace=ws, out=y, seg_len=args.seg_len,
-                                chunk_segs=args.chunk_segs, drive=args.drive, act=args.act)
+                                chunk_segs=args.chunk_segs, drive=args.drive, act=args.act,
+                                delta_params=args.delta_params)
     else:
         fn = binding.scan_jvp2 if args.order == 2 else binding.scan_jvp
         vkw = dict(drive=args.drive, act=args.act) if args.order == 1 else {}
@@ -481,7 +489,8 @@ def main():
 def variant_suffix(args):
     parts = ([args.drive] if args.drive != "euler" else []) + ([args.act] if args.act != "identity" else []) + \
         (["dres"] if args.dres else []) + (["s4dlin"] if args.complex else []) + \
-        ([f"g{args.groups}"] if args.groups > 1 else []) + ([f"lr{args.lowrank}"] if args.lowrank > 0 else [])
+        ([f"g{args.groups}"] if args.groups > 1 else []) + ([f"lr{args.lowrank}"] if args.lowrank > 0 else []) + \
+        (["dparams"] if getattr(args, "delta_params", False) else [])
     return "".join("-" + p for p in parts)
 
 

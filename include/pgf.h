@@ -166,6 +166,13 @@ typedef struct pgf_params {
     /* Parameter flows with D_res set: dl/dD_res, device [D] f32, ADDED to
      * (like grad_A); not read otherwise. */
     float *grad_D_res;
+    /* Parameter flows only (read by the planning calls too): 1 to also carry
+     * the flows of the step size's parameters w_delta and b_delta (see
+     * pgf_param_grads), 0 not to.  With it, grad_w_delta and grad_b_delta
+     * (device, [D] f32, ADDED to) receive dl/dw_delta and dl/db_delta, and
+     * dh_in/dh_out hold four planes. */
+    int32_t delta_flows;
+    float *grad_w_delta, *grad_b_delta;
 } pgf_params;
 
 /* How a call is tiled (host-side planning; no device access). */
@@ -270,8 +277,20 @@ int pgf_scan_jvp2(const void *x, const void *dx, const pgf_params *p,
  * (grad_D_res is required when D_res is set).  The ZOH drive
  * (p->drive) adds (de/dA)*B_t[n]*x to GammaA' with e = (Abar - 1)/A, and
  * takes e in place of Delta in the other drives.
+ * Step-size parameters (p->delta_flows = 1; Sec. 3, Delta = softplus(z),
+ * z = w_delta*x + b_delta, sigma = sigmoid(z) = dDelta/db_delta and
+ * sigma*x = dDelta/dw_delta): the state moves with Delta by
+ *   hd = A*Abar*h + Abar^z*B_t[n]*x  (z = 1 with ZOH, 0 with Euler),
+ * so two more flows per lane run beside the others,
+ *   Gamma_w' = Abar*Gamma_w + sigma*x*hd,  Gamma_s' = Abar*Gamma_s + sigma*hd,
+ * and per channel
+ *   grad_w_delta[d] += w*sum_n C_t[n]*Gamma_w',
+ *   grad_b_delta[d] += w*sum_n C_t[n]*Gamma_s'
+ * (w = gy*act'(yhat), or gy).  dh_in/dh_out then hold
+ * [GammaA; GammaB; Gamma_w; Gamma_s] as [4,B,D,N].
  * p->order must be 3.  State hand-off: h_in/h_out as in pgf_scan_jvp;
- * dh_in/dh_out hold [GammaA; GammaB] as [2,B,D,N].  Chaining calls through
+ * dh_in/dh_out hold [GammaA; GammaB] as [2,B,D,N] (four planes with
+ * delta_flows).  Chaining calls through
  * the state and adding into the same gradients gives the gradients of the
  * whole sequence (up to the rounding of the additions).  y must not overlap
  * x or gy; the gradients must not overlap any other array or each other;

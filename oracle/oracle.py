@@ -70,7 +70,7 @@ def declare(lib):
     lib.pgf_oracle_core2.restype = ctypes.c_int
     lib.pgf_oracle_core2.argtypes = [i64] * 4 + [dp] * 22 + [ctypes.c_int]
     lib.pgf_oracle_param.restype = ctypes.c_int
-    lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 14 + [ctypes.c_int] + [dp] * 6 + [ctypes.c_int, ctypes.c_int]
+    lib.pgf_oracle_param.argtypes = [i64] * 4 + [dp] * 14 + [ctypes.c_int] + [dp] * 8 + [ctypes.c_int, ctypes.c_int]
     lib.pgf_oracle_la.restype = ctypes.c_int
     lib.pgf_oracle_la.argtypes = [i64] * 6 + [dp] * 12 + [ctypes.c_int]
     lib.pgf_oracle_core_cplx.restype = ctypes.c_int
@@ -389,7 +389,7 @@ ACTIVATIONS = {"identity": 0, "silu": 1}
 
 
 def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None, drive="euler", act="identity", D_res=None,
-               sig=None):
+               sig=None, scale=None):
     """Parameter-sensitivity flows (see pgf_oracle_param).  Shapes: A [D,N];
     x, delta, gy [B,L,D]; Bm, Cm [B,L,N]; state = (h, GammaA, GammaB), each
     [B,D,N] (zero when None); drive "euler" or "zoh" (the zero-order-hold
@@ -401,7 +401,8 @@ def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None, drive="euler"
     Returns y [B,L,D], (GA, GB, GC) each [B,D,N] (this call's contributions
     per batch row), plus GD [B,D] (dl/dD_res per batch row) when D_res is
     given, plus GW, GS [B,D] (dl/dw_delta, dl/db_delta) when sig is, and the
-    exit state tuple."""
+    exit state tuple.  scale: a pair of [B,D] arrays that receive (added to)
+    the sums of the absolute values of the terms of GW and GS."""
     lib = _load()
     A = _f64(A)
     x, delta, gy, Bm, Cm = (_f64(a) for a in (x, delta, gy, Bm, Cm))
@@ -428,6 +429,9 @@ def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None, drive="euler"
         assert sg.shape == (B, L, D)
     dres = [null if Dr is None else _dp(Dr), ACTIVATIONS[act], null if GD is None else _dp(GD)]
     dlt = [null] * 5 if sg is None else [_dp(sg), _dp(st[3]), _dp(st[4]), _dp(GWS[0]), _dp(GWS[1])]
+    if scale is not None:
+        assert sg is not None and all(a.shape == (B, D) and a.dtype == np.float64 for a in scale)
+    dlt += [null, null] if scale is None else [_dp(scale[0]), _dp(scale[1])]
     rc = lib.pgf_oracle_param(B, L, D, N, _dp(A), _dp(x), _dp(delta), _dp(gy), _dp(Bm), _dp(Cm),
                               *[_dp(s_) for s_ in st[:3]], _dp(y), *[_dp(g) for g in G], *dres, *dlt,
                               DRIVES[drive], _threads() if nthreads is None else nthreads)
@@ -441,7 +445,7 @@ def core_param(A, x, delta, gy, Bm, Cm, state=None, nthreads=None, drive="euler"
 
 
 def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=None, drive="euler",
-                act="identity", delta_params=False):
+                act="identity", delta_params=False, return_scale=False):
     """Primal output and online parameter gradients of the full model over
     L-chunks (App. E, Alg. 2).  x, gy [B,L,D]; params as scan_jvp; channels:
     optional 1-D index array of the channels d to compute (the projections
@@ -456,7 +460,9 @@ def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=N
     with D_res the gradient tuple gains G_D = dl/dD_res [Dsel].  With
     delta_params it then gains dl/dw_delta and dl/db_delta [Dsel] (the
     step size's parameters), and the state holds Gamma_w and Gamma_s after
-    GammaB."""
+    GammaB.  return_scale (with delta_params) appends the summation scales
+    of those two gradients, sum over b and t of the absolute values of
+    their terms [Dsel] each."""
     B, L, D = np.shape(x)
     A = _f64(params["A"])
     N = A.shape[1]
@@ -470,6 +476,7 @@ def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=N
     y = np.empty((B, L, Ds))
     tot = [np.zeros((B, Ds, N)) for _ in range(3)] + ([] if Dr is None else [np.zeros((B, Ds))]) + \
         ([np.zeros((B, Ds)), np.zeros((B, Ds))] if delta_params else [])
+    scale = [np.zeros((B, Ds)), np.zeros((B, Ds))] if return_scale else None
     st = state
     step = max(1, L if not chunk else int(chunk))
     for t0 in range(0, L, step):
@@ -481,12 +488,14 @@ def param_grads(x, gy, params, state=None, chunk=None, channels=None, nthreads=N
         delta, _ = discretize(xs, xs[None], w, bd)
         sig = expit(xs * w + bd) if delta_params else None
         gs = np.ascontiguousarray(_f64(gy[:, t0:t1])[..., sel])
-        yc, G, st = core_param(As, xs, delta, gs, Bm, Cm, st, nthreads, drive, act, Dr, sig)
+        yc, G, st = core_param(As, xs, delta, gs, Bm, Cm, st, nthreads, drive, act, Dr, sig, scale)
         y[:, t0:t1] = yc
         for i in range(len(tot)):
             tot[i] += G[i]
     if st is None:
         st = tuple(np.zeros((B, Ds, N)) for _ in range(5 if delta_params else 3))
+    if return_scale:
+        return y, tuple(g.sum(0) for g in tot), st, tuple(s_.sum(0) for s_ in scale)
     return y, tuple(g.sum(0) for g in tot), st
 
 

@@ -271,6 +271,9 @@ int pgf_oracle_core2(int64_t B, int64_t L, int64_t D, int64_t N,
  * and, per channel, GW[b,d] += w*sum_n C*Gamma_w', GS[b,d] += w*sum_n
  * C*Gamma_s' (dl/dw_delta, dl/db_delta).  gW, gS [B,D,N] carry the state
  * like h; GW, GS [B,D] are added to.  All four may be NULL when sig is.
+ * GWa, GSa [B,D] (optional, added to) receive the sums of the absolute
+ * values of those terms, the scale of the summation's condition (the
+ * error of a sum of terms of both signs is bounded relative to it).
  * Returns 0, or -1 on a bad argument.
  */
 
@@ -298,7 +301,8 @@ int pgf_oracle_param(int64_t B, int64_t L, int64_t D, int64_t N,
                      double *h, double *gA, double *gB,
                      double *y, double *GA, double *GB, double *GC,
                      const double *D_res, int act, double *GD,
-                     const double *sig, double *gW, double *gS, double *GW, double *GS, int drive, int nthreads)
+                     const double *sig, double *gW, double *gS, double *GW, double *GS,
+                     double *GWa, double *GSa, int drive, int nthreads)
 {
     if (B < 0 || L < 0 || D < 0 || N <= 0 || drive < 0 || drive > 1 || act < 0 || act > 1) return -1;
     if (!A || !h || !gA || !gB || !GA || !GB || !GC || (D_res && !GD)) return -1;
@@ -367,6 +371,8 @@ int pgf_oracle_param(int64_t B, int64_t L, int64_t D, int64_t N,
                 }
                 GW[b * D + d] += w * cw;
                 GS[b * D + d] += w * cs;
+                if (GWa) GWa[b * D + d] += fabs(w * cw);
+                if (GSa) GSa[b * D + d] += fabs(w * cs);
             }
         }
     }

@@ -40,7 +40,7 @@ class PgfParams(ctypes.Structure):
         ("d2h_in", _c_f), ("d2h_out", _c_f),
         ("drive", ctypes.c_int32), ("activation", ctypes.c_int32), ("D_res", _c_f), ("A_im", _c_f),
         ("n_groups", ctypes.c_int32), ("dt_rank", ctypes.c_int32), ("W_dx", _c_f), ("W_dt", _c_f),
-        ("grad_D_res", _c_f),
+        ("grad_D_res", _c_f), ("delta_flows", ctypes.c_int32), ("grad_w_delta", _c_f), ("grad_b_delta", _c_f),
     ]
 
 
@@ -122,27 +122,29 @@ def _check(code: int):
 
 
 def make_params(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1, drive="euler",
-                act="identity") -> PgfParams:
+                act="identity", delta_flows=False) -> PgfParams:
     p = PgfParams()
     p.batch, p.seqlen, p.d_inner, p.d_state, p.n_dirs = int(B), int(L), int(D), int(N), int(K)
     p.in_dtype = PGF_BF16 if in_dtype in ("bf16", torch.bfloat16) else PGF_F32
     p.seg_len, p.chunk_segs, p.order = int(seg_len), int(chunk_segs), int(order)
     p.drive, p.activation = DRIVES[drive], ACTIVATIONS[act]
+    p.delta_flows = 1 if delta_flows else 0
     return p
 
 
 def workspace_bytes(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1, drive="euler",
-                    act="identity") -> int:
+                    act="identity", delta_flows=False) -> int:
     return int(lib().pgf_workspace_bytes(ctypes.byref(make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs,
-                                                                  order, drive, act))))
+                                                                  order, drive, act, delta_flows))))
 
 
 def plan(B, L, D, N, K, in_dtype="f32", seg_len=0, chunk_segs=0, order=1, drive="euler", act="identity",
-         complex_a=False, groups=1, dt_rank=0) -> dict:
+         complex_a=False, groups=1, dt_rank=0, delta_flows=False) -> dict:
     """The tiling a call would use (complex_a: with a complex transition;
-    the planner only tests A_im for NULL, the pointer is never read)."""
+    the planner only tests A_im for NULL, the pointer is never read;
+    delta_flows: the parameter flows of the step size's parameters)."""
     info = PgfPlanInfo()
-    pr = make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs, order, drive, act)
+    pr = make_params(B, L, D, N, K, in_dtype, seg_len, chunk_segs, order, drive, act, delta_flows)
     pr.n_groups = int(groups)
     pr.dt_rank = int(dt_rank)
     if complex_a:
@@ -405,14 +407,15 @@ def scan_jvp2(x: torch.Tensor, dx: torch.Tensor, params: dict, *, h_in=None, dh_
 
 def param_grads(x: torch.Tensor, gy: torch.Tensor, params: dict, *, h_in=None, gamma_in=None, grads=None,
                 return_state=False, seg_len=0, chunk_segs=0, workspace=None, out=None, stream=None,
-                drive="euler", act="identity"):
+                drive="euler", act="identity", delta_params=False):
     """Primal scan with the parameter-sensitivity flows and online gradient
     accumulation against the adjoint signal gy = dl/dy, on the GPU.
 
     x [B,L,D] float32 or bfloat16 and gy [B,L,D] float32, CUDA tensors.
     grads: optional (grad_A, grad_B, grad_C), each [D,N] float32 on the
     device, which are ADDED to in place (zeros are allocated when None).
-    gamma_in: optional [2,B,D,N] entry state of the flows (dh/dA, dh/dB).
+    gamma_in: optional [2,B,D,N] entry state of the flows (dh/dA, dh/dB;
+    [4,B,D,N] with dh/dw_delta and dh/db_delta when delta_params).
     Returns (y [B,L,D], grad_A, grad_B, grad_C), plus (h_out [B,D,N],
     gamma_out [2,B,D,N]) when return_state.  grad_B and grad_C are the
     gradients of per-lane offsets of B and C; their sums over d are
@@ -420,7 +423,9 @@ def param_grads(x: torch.Tensor, gy: torch.Tensor, params: dict, *, h_in=None, g
     whose derivative in A enters dl/dA).  act ("identity" or "silu") and
     params["D_res"] (optional [D]) set the output map y = act(C h + D_res x);
     with D_res the gradients gain a fourth, grad_D_res [D] (grads then holds
-    four tensors when given).  Asynchronous on the current stream.
+    four tensors when given).  delta_params adds the flows of the step
+    size's parameters: the gradients then end with grad_w_delta and
+    grad_b_delta [D].  Asynchronous on the current stream.
     """
     if not (isinstance(x, torch.Tensor) and isinstance(gy, torch.Tensor) and x.is_cuda and gy.is_cuda):
         raise ValueError("x and gy must be device tensors")
@@ -428,11 +433,11 @@ def param_grads(x: torch.Tensor, gy: torch.Tensor, params: dict, *, h_in=None, g
         raise ValueError("x and gy must be on the same device")
     with torch.cuda.device(x.device), _on_stream(stream, x.device):
         return _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len, chunk_segs, workspace,
-                               out, drive, act)
+                               out, drive, act, delta_params)
 
 
 def _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len, chunk_segs, workspace, out,
-                    drive, act):
+                    drive, act, delta_params):
     L_ = lib()
     if x.dtype not in (torch.float32, torch.bfloat16) or gy.dtype != torch.float32:
         raise ValueError("x must be float32 or bfloat16 and gy float32")
@@ -443,7 +448,7 @@ def _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len,
     B, L, D = x.shape
     dev = x.device
     pr = make_params(B, L, D, params["A"].shape[1], 2, "bf16" if x.dtype == torch.bfloat16 else "f32", seg_len,
-                     chunk_segs, 3, drive, act)
+                     chunk_segs, 3, drive, act, delta_params)
     keep = []
     N = _model_params(pr, params, D, dev, keep)
     if params.get("A_im") is not None:
@@ -451,15 +456,16 @@ def _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len,
     D_res = _dev_param(params.get("D_res"), (D,), dev, "D_res")
     keep.append(D_res)
     pr.D_res = None if D_res is None else D_res.data_ptr()
-    shapes = [(D, N)] * 3 + ([(D,)] if D_res is not None else [])
+    shapes = [(D, N)] * 3 + ([(D,)] if D_res is not None else []) + ([(D,), (D,)] if delta_params else [])
+    ng = 4 if delta_params else 2     # planes of gamma_in / gamma_out
     h_in = _dev_param(h_in, (B, D, N), dev, "h_in")
-    gamma_in = _dev_param(gamma_in, (2, B, D, N), dev, "gamma_in")
+    gamma_in = _dev_param(gamma_in, (ng, B, D, N), dev, "gamma_in")
     pr.h_in = None if h_in is None else h_in.data_ptr()
     pr.dh_in = None if gamma_in is None else gamma_in.data_ptr()
     states = ()
     if return_state:
         h_out = torch.empty((B, D, N), device=dev, dtype=torch.float32)
-        g_out = torch.empty((2, B, D, N), device=dev, dtype=torch.float32)
+        g_out = torch.empty((ng, B, D, N), device=dev, dtype=torch.float32)
         pr.h_out, pr.dh_out = h_out.data_ptr(), g_out.data_ptr()
         states = (h_out, g_out)
     if grads is None:
@@ -470,8 +476,10 @@ def _param_grads_on(x, gy, params, h_in, gamma_in, grads, return_state, seg_len,
                 isinstance(g, torch.Tensor) and g.dtype == torch.float32 and g.device == dev
                 and tuple(g.shape) == sh and g.is_contiguous() for g, sh in zip(grads, shapes)):
             raise ValueError(f"grads: {len(shapes)} contiguous float32 tensors of shapes {shapes} on {dev}")
-    if len(grads) == 4:
+    if D_res is not None:
         pr.grad_D_res = grads[3].data_ptr()
+    if delta_params:
+        pr.grad_w_delta, pr.grad_b_delta = grads[-2].data_ptr(), grads[-1].data_ptr()
     y, = _outputs(out, ((B, L, D),), ("y",), dev)
     workspace = _workspace(L_, pr, workspace, dev)
     st = torch.cuda.current_stream(dev).cuda_stream

@@ -60,7 +60,9 @@ int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
     // The parameter flows carry two sensitivity states (dh/dA, dh/dB) and
     // need no tangent projections; n_dirs is not read.
     const int64_t B = p->batch, L = p->seqlen, D = p->d_inner, N = p->d_state;
-    const int64_t K = order == 3 ? 2 : p->n_dirs;
+    if (p->delta_flows < 0 || p->delta_flows > 1) return PGF_ERR_INVALID_ARG;
+    if (p->delta_flows && order != 3) return PGF_ERR_INVALID_ARG;
+    const int64_t K = order == 3 ? (p->delta_flows ? 4 : 2) : p->n_dirs;
     if (B < 1 || L < 0 || D < 1 || N < 1 || K < 1) return PGF_ERR_INVALID_ARG;
     if (p->in_dtype != PGF_F32 && p->in_dtype != PGF_BF16) return PGF_ERR_INVALID_ARG;
     if (!(N == 4 || N == 8 || N == 16 || N == 32 || N == 64)) return PGF_ERR_UNSUPPORTED;
@@ -78,7 +80,7 @@ int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
     // the variants belong to the first order; the parameter flows also take
     // the ZOH drive and the output map
     if (var && order == 2) return PGF_ERR_UNSUPPORTED;
-    if (var && (K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
+    if (var && ((order != 3 && K > 2) || N > 16)) return PGF_ERR_UNSUPPORTED;
     const int cplx = p->A_im ? 1 : 0;
     if (cplx && (order != 1 || var || K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
     if (p->n_groups < 0) return PGF_ERR_INVALID_ARG;
@@ -107,7 +109,8 @@ int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
     q.comp = (int)((1 + K + (order == 2 ? 1 : 0)) * (cplx ? 2 : 1));
     q.in_bf16 = p->in_dtype == PGF_BF16;
     // Registers per thread grow as nt*(3+K); keep them near 128.
-    q.nt = (int)std::min<int64_t>(N, K >= 8 ? 4 : (K >= 4 ? 8 : 16));
+    // (the parameter flows hold all N <= 16 lanes in one thread)
+    q.nt = (int)(order == 3 ? N : std::min<int64_t>(N, K >= 8 ? 4 : (K >= 4 ? 8 : 16)));
     q.ns = (int)(N / q.nt);
     q.R = (int)(groups * 2 * N * (1 + q.KP));
     // Wide f32 channel sums are cut into splits of at most about 2048
@@ -186,7 +189,7 @@ int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
         w.agg_h = w.agg_s = off;
     }
     w.gacc = off;
-    if (order == 3) off = align256(off + (3 * (size_t)B * N * D + (size_t)B * D) * f);
+    if (order == 3) off = align256(off + (3 * (size_t)B * N * D + 3 * (size_t)B * D) * f);
     w.lr = off;
     if (rank) off = align256(off + (size_t)(1 + K) * B * q.chunk_len * q.rc * f);
     w.dt = off;

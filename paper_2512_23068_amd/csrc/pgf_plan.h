@@ -26,14 +26,16 @@ constexpr int64_t kSeqChunk = 4096;
 //                                    then (in place) the true state
 //                                    entering each segment
 //   agg_s   [B][G][(1+K)][D]         segment sums of Delta and dDelta_k
-//   gacc    [3][B][N][D] + [B][D]    parameter flows only: running gradient
+//   gacc    [3][B][N][D] + [3][B][D] parameter flows only: running gradient
 //                                    sums (A, B offset, C offset) of the call,
-//                                    then those of the residual weight D_res
+//                                    then the per-channel ones (D_res,
+//                                    w_delta, b_delta)
 //   lr      [(1+K)][B][Tc][RC]       low rank only: x W_dx and dx_k W_dx, the
 //                                    rank padded to RC (zero columns)
 //   dt      [(1+K)][B][Tc][D]        low rank only: Delta and dDelta_k
-// In the parameter flows K = 2 (the states dh/dA and dh/dB) and agg_h also
-// receives each segment's gradient partials after its rescan.
+// In the parameter flows K = 2 (the states dh/dA and dh/dB; 4 with the
+// step size's dh/dw_delta and dh/db_delta) and agg_h also receives each
+// segment's gradient partials after its rescan.
 struct Layout {
     size_t state, bc, bc_half, part, agg_h, agg_s, gacc, lr, dt, total;   // bc_half: bytes of one bc buffer
 };

@@ -102,17 +102,23 @@ int param_common(const void *x, const float *gy, const pgf_params *p, float *y, 
     if (q.order != 3) return PGF_ERR_INVALID_ARG;
     if (!p->A || !p->w_delta || !p->b_delta || !p->W_B || !p->W_C) return PGF_ERR_INVALID_ARG;
     if (!gA || !gB || !gC) return PGF_ERR_INVALID_ARG;
-    // the residual weight's gradient, when there is a residual weight
+    // the residual weight's gradient, when there is a residual weight, and
+    // the step size's, with its flows
     const float *gD = p->D_res ? p->grad_D_res : nullptr;
     if (p->D_res && !gD) return PGF_ERR_INVALID_ARG;
+    const bool dlt = q.K == 4;
+    if (dlt && (!p->grad_w_delta || !p->grad_b_delta)) return PGF_ERR_INVALID_ARG;
     if (!p->workspace || p->workspace_bytes < q.ws.total || ((uintptr_t)p->workspace & 255))
         return PGF_ERR_WORKSPACE;
     const size_t esz = q.in_bf16 ? 2 : 4;
     const size_t nx = (size_t)q.B * q.L * q.D;
     const size_t bx = nx * esz, bg = nx * 4, by = nx * 4, bw = q.ws.total;
-    const int ng = gD ? 4 : 3;
-    const float *grads[4] = {gA, gB, gC, gD};
-    const size_t bp[4] = {(size_t)q.N * q.D * 4, (size_t)q.N * q.D * 4, (size_t)q.N * q.D * 4, (size_t)q.D * 4};
+    const float *grads[6] = {gA, gB, gC, gD, dlt ? p->grad_w_delta : nullptr, dlt ? p->grad_b_delta : nullptr};
+    int ng = 3;
+    for (int i = 3; i < 6; ++i)   // the per-channel gradients given, packed after the [D,N] ones
+        if (grads[i]) grads[ng++] = grads[i];
+    const size_t bnd = (size_t)q.N * q.D * 4, bd = (size_t)q.D * 4;
+    const size_t bp[6] = {bnd, bnd, bnd, bd, bd, bd};
     for (int i = 0; i < ng; ++i) {
         for (int j = i + 1; j < ng; ++j)
             if (overlap(grads[i], bp[i], grads[j], bp[j])) return PGF_ERR_INVALID_ARG;

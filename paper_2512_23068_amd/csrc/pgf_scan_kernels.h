@@ -111,6 +111,25 @@ __device__ __forceinline__ void discretize(float xv, float w, float bd, float &d
     sw = (z >= 0.0f ? r : e * r) * w;
 }
 
+// Also returns sig = sigmoid(z) = dDelta/db (the parameter flows of the step
+// size need it apart from w).
+__device__ __forceinline__ void discretize_sig(float xv, float w, float bd, float &delta, float &sw, float &sig) {
+    const float z = fmaf(xv, w, bd);
+    const float e = exp_nonpos(-fabsf(z));
+    const float sv = e * __builtin_amdgcn_rcpf(2.0f + e);
+    const float q = sv * sv;
+    float poly = fmaf(q, 1.0f / 13.0f, 1.0f / 11.0f);
+    poly = fmaf(q, poly, 1.0f / 9.0f);
+    poly = fmaf(q, poly, 1.0f / 7.0f);
+    poly = fmaf(q, poly, 1.0f / 5.0f);
+    poly = fmaf(q, poly, 1.0f / 3.0f);
+    poly = fmaf(q, poly, 1.0f);
+    delta = fmaxf(z, 0.0f) + 2.0f * sv * poly;
+    const float r = __builtin_amdgcn_rcpf(1.0f + e);
+    sig = z >= 0.0f ? r : e * r;
+    sw = sig * w;
+}
+
 // Also returns s2 = softplus''(z) * w^2 = sigmoid(z)(1 - sigmoid(z)) w^2,
 // which is e/(1+e)^2 * w^2 on both sides of z = 0.
 __device__ __forceinline__ void discretize2(float xv, float w, float bd, float &delta, float &sw, float &s2) {
@@ -1738,22 +1757,36 @@ __global__ __launch_bounds__(kThreads) void k_carry(
 // MAP (output pass only): the output map y = act(yhat), yhat = sum_n C h' +
 // D_res x.  The adjoint then reaches the state through w = gy act'(yhat):
 // the three sums take w in place of gy (App. E's sigma' factor of the G_C
-// update), and w x, summed over the segment, is the partial of dl/dD_res,
-// stored (or with gadd added) at gdr[b gdr_bs + g gdr_gs + d].
-template <int NT, bool OUT, typename InT, bool ZOH = false, bool MAP = false>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 2 : 3))) void k_pscan(
+// update), and w x, summed over the segment, is the partial of dl/dD_res.
+// DLT: two more planes per lane, the flows of the step size's parameters
+// (Delta = softplus(w_delta x + b_delta), sigma = dDelta/db_delta):
+//   hd = A Abar h + Abar^z B x           (dh'/dDelta; z = 1 with ZOH)
+//   Gw' = Abar Gw + sigma x hd,   Gs' = Abar Gs + sigma hd,
+// the aggregate pass also sums sigma x and sigma over the segment (agg_s
+// components 1 and 2), and the output pass accumulates per channel
+// w sum_n C Gw' and w sum_n C Gs'.  The per-channel partials of the output
+// pass (D_res, then w_delta, then b_delta) are stored, or with gadd added,
+// at gch[b gch_bs + g gch_gs + c gch_cs + d], c = 0, 1, 2.
+template <int NT, bool OUT, typename InT, bool ZOH = false, bool MAP = false, bool DLT = false>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH || DLT ? 2 : 3))) void k_pscan(
     const InT *__restrict__ x, const float *__restrict__ gy, const float *__restrict__ A,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *init, int64_t ibs, int64_t igs, int64_t ics,
     float *__restrict__ y, float *end_state, float *gout, int gadd,
     float *__restrict__ agg_h, float *__restrict__ agg_s,
     int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G,
-    const float *__restrict__ D_res, int act, float *gdr, int64_t gdr_bs, int64_t gdr_gs) {
+    const float *__restrict__ D_res, int act, float *gch, int64_t gch_bs, int64_t gch_gs, int64_t gch_cs) {
     static_assert(OUT || !MAP, "the output map belongs to the output pass");
     constexpr int N = NT;
     constexpr int R = 2 * N;          // B, C
+    constexpr int CP = DLT ? 5 : 3;   // state planes per lane
+    constexpr int NW = DLT ? NT : 1;
+    // With both the ZOH drive and the step size's flows the exponent scale
+    // A log2(e) is formed per step (the same product, so the same bits)
+    // instead of held, to stay within the registers.
+    constexpr bool ATF = ZOH && DLT;
     // prefetch depth, bounded by the VGPR budget
-    constexpr int TT = OUT && NT >= 16 ? (MAP ? 2 : 4) : 8;
+    constexpr int TT = OUT && NT >= 16 ? (MAP || DLT ? 2 : 4) : 8;
 
     const int tid = threadIdx.x;
     const int64_t d_raw = (int64_t)blockIdx.x * kThreads + tid;
@@ -1765,20 +1798,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 
     const int64_t te = ts + S < len ? ts + S : len;
     if (ts >= te) return;
 
-    float At[NT], Af[NT], Ai[NT];
+    float At[ATF ? 1 : NT], Af[NT], Ai[NT];
 #pragma unroll
     for (int i = 0; i < NT; ++i) {
-        At[i] = A[d * N + i] * kLog2e;
-        if constexpr (ZOH) {
-            Af[i] = A[d * N + i];
-            Ai[i] = 1.0f / Af[i];
-        }
+        if constexpr (!ATF) At[i] = A[d * N + i] * kLog2e;
+        if constexpr (ZOH || DLT) Af[i] = A[d * N + i];
+        if constexpr (ZOH) Ai[i] = 1.0f / Af[i];
     }
     const float w = w_delta[d], bd = b_delta[d];
     float Dr = 0.0f, sDr = 0.0f;
     if constexpr (MAP) Dr = D_res ? D_res[d] : 0.0f;
 
-    float h[NT], ga[NT], gb[NT];
+    float h[NT], ga[NT], gb[NT], gw[NW], gs[NW];
     float sA[NT], sB[NT], sC[NT];
     if constexpr (OUT) {
         const float *ib = init + b * ibs + g * igs + d;
@@ -1787,13 +1818,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 
             h[i] = ib[i * D];
             ga[i] = ib[ics + i * D];
             gb[i] = ib[2 * ics + i * D];
+            if constexpr (DLT) {
+                gw[i] = ib[3 * ics + i * D];
+                gs[i] = ib[4 * ics + i * D];
+            }
             sA[i] = sB[i] = sC[i] = 0.0f;
         }
     } else {
 #pragma unroll
         for (int i = 0; i < NT; ++i) h[i] = ga[i] = gb[i] = 0.0f;
+#pragma unroll
+        for (int i = 0; i < NW; ++i) gw[i] = gs[i] = 0.0f;
     }
     float sD = 0.0f;
+    float sSx = 0.0f, sS = 0.0f;   // aggregate pass, DLT: sums of sigma x and sigma
+    float sW = 0.0f, sG = 0.0f;    // output pass, DLT: the per-channel accumulations
 
     const InT *Xb = x + (b * L + t0) * D;
     const float *Gb = gy + (b * L + t0) * D;
@@ -1828,25 +1867,46 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 
             const int64_t t = tb + j;
             if (t < te) {
                 const float xv = xc[j];
-                float delta, sw;
-                discretize(xv, w, bd, delta, sw);
+                float delta, sw, sig = 0.0f;
+                if constexpr (DLT) discretize_sig(xv, w, bd, delta, sw, sig);
+                else discretize(xv, w, bd, delta, sw);
                 const float u = delta * xv;
-                if constexpr (!OUT) sD += delta;
+                const float sgx = sig * xv;
+                if constexpr (!OUT) {
+                    sD += delta;
+                    if constexpr (DLT) {
+                        sSx += sgx;
+                        sS += sig;
+                    }
+                }
                 const float *rec = rec0 + t * R;
-                float yv = 0.0f;
+                float yv = 0.0f, cw = 0.0f, cs = 0.0f;
 #pragma unroll
                 for (int i = 0; i < NT; ++i) {
                     const float Bn = rec[i];
-                    const float a = transition(delta, At[i]);
+                    float at;
+                    if constexpr (ATF) at = Af[i] * kLog2e;
+                    else at = At[i];
+                    const float a = transition(delta, at);
                     const float sv = a * h[i];
                     if constexpr (ZOH) {
                         const float e = zoh_coef(delta, Af[i], Ai[i], a);
                         const float ea = zoh_coef_dA(delta, Af[i], Ai[i], a, e);
                         const float Bx = Bn * xv;
+                        if constexpr (DLT) {
+                            const float hd = fmaf(Af[i], sv, a * Bx);
+                            gw[i] = fmaf(a, gw[i], sgx * hd);
+                            gs[i] = fmaf(a, gs[i], sig * hd);
+                        }
                         ga[i] = fmaf(a, ga[i], fmaf(delta, sv, ea * Bx));
                         gb[i] = fmaf(a, gb[i], e * xv);
                         h[i] = fmaf(e, Bx, sv);
                     } else {
+                        if constexpr (DLT) {
+                            const float hd = fmaf(Af[i], sv, Bn * xv);
+                            gw[i] = fmaf(a, gw[i], sgx * hd);
+                            gs[i] = fmaf(a, gs[i], sig * hd);
+                        }
                         ga[i] = fmaf(a, ga[i], delta * sv);
                         gb[i] = fmaf(a, gb[i], u);
                         h[i] = fmaf(Bn, u, sv);
@@ -1854,6 +1914,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 
                     if constexpr (OUT) {
                         const float Cn = rec[N + i];
                         yv = fmaf(Cn, h[i], yv);
+                        if constexpr (DLT) {
+                            cw = fmaf(Cn, gw[i], cw);
+                            cs = fmaf(Cn, gs[i], cs);
+                        }
                         if constexpr (!MAP) {
                             const float gC = gc[j] * Cn;
                             sA[i] = fmaf(gC, ga[i], sA[i]);
@@ -1861,6 +1925,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 
                             sC[i] = fmaf(gc[j], h[i], sC[i]);
                         }
                     }
+                }
+                if constexpr (OUT && DLT && !MAP) {
+                    sW = fmaf(gc[j], cw, sW);
+                    sG = fmaf(gc[j], cs, sG);
                 }
                 if constexpr (MAP) {
                     // the output map, then the sums against w = gy act'(yhat)
@@ -1873,6 +1941,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 
                         wv *= df;
                     }
                     sDr = fmaf(wv, xv, sDr);
+                    if constexpr (DLT) {
+                        sW = fmaf(wv, cw, sW);
+                        sG = fmaf(wv, cs, sG);
+                    }
 #pragma unroll
                     for (int i = 0; i < NT; ++i) {
                         const float gC = wv * rec[N + i];
@@ -1902,11 +1974,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 
                 eb[i * D] = h[i];
                 eb[ics + i * D] = ga[i];
                 eb[2 * ics + i * D] = gb[i];
+                if constexpr (DLT) {
+                    eb[3 * ics + i * D] = gw[i];
+                    eb[4 * ics + i * D] = gs[i];
+                }
             }
         }
-        if constexpr (MAP) {
-            float *dr = gdr + b * gdr_bs + g * gdr_gs + d;
-            *dr = gadd ? *dr + sDr : sDr;
+        float *pc = gch + b * gch_bs + g * gch_gs + d;
+        if constexpr (MAP) pc[0] = gadd ? pc[0] + sDr : sDr;
+        if constexpr (DLT) {
+            pc[gch_cs] = gadd ? pc[gch_cs] + sW : sW;
+            pc[2 * gch_cs] = gadd ? pc[2 * gch_cs] + sG : sG;
         }
         float *ob = gout + b * ibs + g * igs + d;
         if (gadd) {
@@ -1925,25 +2003,40 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ? 
             }
         }
     } else {
-        const int64_t base = (b * G + g) * 3;
+        const int64_t base = (b * G + g) * CP;
 #pragma unroll
         for (int i = 0; i < NT; ++i) {
             agg_h[(base * N + i) * D + d] = h[i];
             agg_h[((base + 1) * N + i) * D + d] = ga[i];
             agg_h[((base + 2) * N + i) * D + d] = gb[i];
+            if constexpr (DLT) {
+                agg_h[((base + 3) * N + i) * D + d] = gw[i];
+                agg_h[((base + 4) * N + i) * D + d] = gs[i];
+            }
         }
         agg_s[base * D + d] = sD;
+        if constexpr (DLT) {
+            agg_s[(base + 1) * D + d] = sSx;
+            agg_s[(base + 2) * D + d] = sS;
+        }
     }
 }
 
 // Carry of the parameter flows: a segment maps its entry state to
 //   h' = P h + h0,  GA' = P GA + S P h + GA0,  GB' = P GB + GB0,
-// P = exp(A S), S = the segment's sum of Delta (dP/dA = S P).  Same layout
-// and in-place convention as k_carry.
-static __global__ __launch_bounds__(kThreads) void k_pcarry(
+// P = exp(A S), S = the segment's sum of Delta (dP/dA = S P).  DLT: the
+// step size's flows go the same way with dP/dtheta = P A S_theta, S_theta
+// the segment's sum of dDelta/dtheta (sigma x for w_delta, sigma for
+// b_delta; agg_s components 1 and 2):
+//   Gw' = P Gw + P A S_w h + Gw0,  Gs' = P Gs + P A S_s h + Gs0.
+// Same layout (CP planes per segment) and in-place convention as k_carry.
+template <bool DLT>
+__global__ __launch_bounds__(kThreads) void k_pcarry(
     const float *__restrict__ A, float *__restrict__ seg, const float *__restrict__ agg_s,
     float *__restrict__ state, int64_t Bsz, int64_t D, int64_t N, int G) {
     constexpr int GB = 16;
+    constexpr int CP = DLT ? 5 : 3;
+    constexpr int NX = DLT ? GB : 1;
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int64_t ND = N * D;
     if (idx >= Bsz * ND) return;
@@ -1953,25 +2046,44 @@ static __global__ __launch_bounds__(kThreads) void k_pcarry(
     const int64_t cs = Bsz * ND;
     const int64_t lane = n * D + d;
     float h = state[b * ND + lane], ga = state[cs + b * ND + lane], gb = state[2 * cs + b * ND + lane];
+    float gw = 0.0f, gs = 0.0f;
+    if constexpr (DLT) {
+        gw = state[3 * cs + b * ND + lane];
+        gs = state[4 * cs + b * ND + lane];
+    }
     for (int g0 = 0; g0 < G; g0 += GB) {
         float e0[GB], e1[GB], e2[GB], s0[GB];
+        float e3[NX], e4[NX], s1[NX], s2[NX];
 #pragma unroll
         for (int j = 0; j < GB; ++j) {
             const int g = g0 + j < G ? g0 + j : G - 1;
-            const int64_t base = (b * G + g) * 3;
+            const int64_t base = (b * G + g) * CP;
             e0[j] = seg[base * ND + lane];
             e1[j] = seg[(base + 1) * ND + lane];
             e2[j] = seg[(base + 2) * ND + lane];
             s0[j] = agg_s[base * D + d];
+            if constexpr (DLT) {
+                e3[j] = seg[(base + 3) * ND + lane];
+                e4[j] = seg[(base + 4) * ND + lane];
+                s1[j] = agg_s[(base + 1) * D + d];
+                s2[j] = agg_s[(base + 2) * D + d];
+            }
         }
 #pragma unroll
         for (int j = 0; j < GB; ++j) {
             if (g0 + j >= G) break;
-            const int64_t base = (b * G + g0 + j) * 3;
+            const int64_t base = (b * G + g0 + j) * CP;
             seg[base * ND + lane] = h;
             seg[(base + 1) * ND + lane] = ga;
             seg[(base + 2) * ND + lane] = gb;
             const float P = exp2_series(at * s0[j]);
+            if constexpr (DLT) {
+                seg[(base + 3) * ND + lane] = gw;
+                seg[(base + 4) * ND + lane] = gs;
+                const float PA = P * a;
+                gw = fmaf(P, gw, fmaf(PA * s1[j], h, e3[j]));
+                gs = fmaf(P, gs, fmaf(PA * s2[j], h, e4[j]));
+            }
             ga = fmaf(P, ga, fmaf(P * s0[j], h, e1[j]));
             gb = fmaf(P, gb, e2[j]);
             h = fmaf(P, h, e0[j]);
@@ -1980,27 +2092,33 @@ static __global__ __launch_bounds__(kThreads) void k_pcarry(
     state[b * ND + lane] = h;
     state[cs + b * ND + lane] = ga;
     state[2 * cs + b * ND + lane] = gb;
+    if constexpr (DLT) {
+        state[3 * cs + b * ND + lane] = gw;
+        state[4 * cs + b * ND + lane] = gs;
+    }
 }
 
-// Adds the block's per-segment gradient partials part [B][G][3][N][D] to the
-// running sums acc [3][B][N][D] (the state layout), one segment after the
-// other in order, so the sums do not depend on how the call is split into
-// host blocks.  With dpart (the output map's residual weight), the partials
-// of dl/dD_res at dpart[(b G + g) 3 D + d] go the same way to the sums
-// acc[3 B N D + b D + d].
+// Adds the block's per-segment gradient partials part [B][G][CP][N][D] (the
+// first three planes) to the running sums acc [3][B][N][D] (the state
+// layout), one segment after the other in order, so the sums do not depend
+// on how the call is split into host blocks.  The per-channel partials c
+// (bit c of cmask: 0 D_res, 1 w_delta, 2 b_delta), at
+// chp[((b G + g) CP + c) D + d], go the same way to the sums
+// acc[3 B N D + c B D + b D + d].
 static __global__ __launch_bounds__(kThreads) void k_gsum(
-    const float *__restrict__ part, float *__restrict__ acc, int64_t Bsz, int64_t ND, int G,
-    const float *__restrict__ dpart, int64_t D) {
+    const float *__restrict__ part, float *__restrict__ acc, int64_t Bsz, int64_t ND, int G, int CP,
+    const float *__restrict__ chp, int cmask, int64_t D) {
     constexpr int GB = 16;
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (dpart && idx >= 3 * Bsz * ND && idx < 3 * Bsz * ND + Bsz * D) {
-        const int64_t j = idx - 3 * Bsz * ND, b = j / D, d = j % D;
+    const int64_t n3 = 3 * Bsz * ND;
+    if (idx >= n3) {
+        const int64_t j = idx - n3, c = j / (Bsz * D), b = (j / D) % Bsz, d = j % D;
+        if (c >= 3 || !((cmask >> c) & 1)) return;
         float s = acc[idx];
-        for (int g = 0; g < G; ++g) s += dpart[(b * G + g) * 3 * D + d];
+        for (int g = 0; g < G; ++g) s += chp[((b * G + g) * CP + c) * D + d];
         acc[idx] = s;
         return;
     }
-    if (idx >= 3 * Bsz * ND) return;
     const int64_t c = idx / (Bsz * ND), b = (idx / ND) % Bsz, r = idx % ND;
     float s = acc[idx];
     for (int g0 = 0; g0 < G; g0 += GB) {
@@ -2008,7 +2126,7 @@ static __global__ __launch_bounds__(kThreads) void k_gsum(
 #pragma unroll
         for (int j = 0; j < GB; ++j) {
             const int g = g0 + j < G ? g0 + j : G - 1;
-            v[j] = part[((b * G + g) * 3 + c) * ND + r];
+            v[j] = part[((b * G + g) * CP + c) * ND + r];
         }
 #pragma unroll
         for (int j = 0; j < GB; ++j) {
@@ -2025,20 +2143,22 @@ static __global__ __launch_bounds__(kThreads) void k_fill0(float *__restrict__ p
 }
 
 // grad_c[d][n] += sum over b (in order) of acc[c][b][n][d], c = A, B, C, and
-// (gD not NULL) gD[d] += sum over b of acc[3 B N D + b D + d].
+// for each per-channel gradient c given (0 gD, 1 gW, 2 gS; NULL = not
+// wanted) out_c[d] += sum over b of acc[3 B N D + c B D + b D + d].
 static __global__ __launch_bounds__(kThreads) void k_gout(
     const float *__restrict__ acc, float *__restrict__ gA, float *__restrict__ gB, float *__restrict__ gC,
-    float *__restrict__ gD, int64_t Bsz, int64_t D, int64_t N) {
+    float *__restrict__ gD, float *__restrict__ gW, float *__restrict__ gS, int64_t Bsz, int64_t D, int64_t N) {
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int64_t ND = N * D;
-    if (gD && idx >= 3 * ND && idx < 3 * ND + D) {
-        const int64_t d = idx - 3 * ND;
+    if (idx >= 3 * ND) {
+        const int64_t c = (idx - 3 * ND) / D, d = (idx - 3 * ND) % D;
+        float *out = c == 0 ? gD : (c == 1 ? gW : (c == 2 ? gS : nullptr));
+        if (!out) return;
         float s = 0.0f;
-        for (int64_t b = 0; b < Bsz; ++b) s += acc[3 * Bsz * ND + b * D + d];
-        gD[d] += s;
+        for (int64_t b = 0; b < Bsz; ++b) s += acc[3 * Bsz * ND + c * Bsz * D + b * D + d];
+        out[d] += s;
         return;
     }
-    if (idx >= 3 * ND) return;
     const int64_t c = idx / ND, r = idx % ND;
     const int64_t d = r % D, n = r / D;
     float s = 0.0f;
@@ -2685,10 +2805,14 @@ struct Launcher {
 
     // Parameter flows: one thread per channel with all N <= 16 states.
     // MAP: the output map (activation, residual weight) with the partials
-    // of dl/dD_res, summed into gacc's [B][D] tail.
-    template <int NT, bool ZOH, bool MAP>
+    // of dl/dD_res; DLT: the step size's flows with the partials of
+    // dl/dw_delta and dl/db_delta.  The per-channel sums go to gacc's
+    // [3][B][D] tail.
+    template <int NT, bool ZOH, bool MAP, bool DLT>
     void pscans(int64_t t0, int64_t len) {
         if (dry) return;
+        constexpr int CP = DLT ? 5 : 3;
+        constexpr int cmask = (MAP ? 1 : 0) | (DLT ? 6 : 0);
         const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
         const int64_t ND = q.N * q.D;
         if (q.seg == 0) {
@@ -2697,56 +2821,65 @@ struct Launcher {
             for (int64_t u0 = 0; u0 < len; u0 += kSeqChunk) {
                 const int64_t ul = len - u0 < kSeqChunk ? len - u0 : kSeqChunk;
                 Timed tm(3, st, !q.noalloc);
-                hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH, MAP>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0,
-                                   st, x, gy, p.A, p.w_delta, p.b_delta, (const float *)(bcw() + u0 * q.R),
+                hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH, MAP, DLT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads),
+                                   0, st, x, gy, p.A, p.w_delta, p.b_delta, (const float *)(bcw() + u0 * q.R),
                                    (const float *)state(), ND, (int64_t)0, q.B * ND, y, state(), gacc(), 1,
                                    (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0 + u0, ul, q.chunk_len, ul, 1,
-                                   p.D_res, (int)p.activation, gacc() + 3 * q.B * ND, q.D, (int64_t)0);
+                                   p.D_res, (int)p.activation, gacc() + 3 * q.B * ND, q.D, (int64_t)0, q.B * q.D);
             }
             return;
         }
         const int G = (int)((len + q.seg - 1) / q.seg);
         {
             Timed tm(1, st, !q.noalloc);
-            hipLaunchKernelGGL((k_pscan<NT, false, InT, ZOH>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
-                               x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)nullptr, (int64_t)0,
-                               (int64_t)0, (int64_t)0, y, (float *)nullptr, (float *)nullptr, 0, agg_h(), agg_s(),
-                               q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G, (const float *)nullptr, 0,
-                               (float *)nullptr, (int64_t)0, (int64_t)0);
+            hipLaunchKernelGGL((k_pscan<NT, false, InT, ZOH, false, DLT>), dim3(gx, (unsigned)G, (unsigned)q.B),
+                               dim3(kThreads), 0, st, x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)nullptr,
+                               (int64_t)0, (int64_t)0, (int64_t)0, y, (float *)nullptr, (float *)nullptr, 0, agg_h(),
+                               agg_s(), q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G,
+                               (const float *)nullptr, 0, (float *)nullptr, (int64_t)0, (int64_t)0, (int64_t)0);
         }
         const int64_t lanes = q.B * ND;
         {
             Timed tm(2, st, !q.noalloc);
-            hipLaunchKernelGGL(k_pcarry, dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
-                               p.A, agg_h(), agg_s(), state(), q.B, q.D, q.N, G);
+            hipLaunchKernelGGL(k_pcarry<DLT>, dim3((unsigned)((lanes + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                               st, p.A, agg_h(), agg_s(), state(), q.B, q.D, q.N, G);
         }
-        // The rescan leaves the partials of dl/dD_res in component 1 of
-        // agg_s (the carry has consumed the segment sums; only component 0
-        // holds them in the parameter flows).
-        float *dpart = MAP ? agg_s() + q.D : nullptr;
+        // The rescan leaves its per-channel partials in components 1..3 of
+        // agg_s (the carry has consumed what the aggregate pass left there).
+        float *chp = agg_s() + q.D;
         {
             Timed tm(3, st, !q.noalloc);
-            hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH, MAP>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads),
-                               0, st, x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(),
-                               (int64_t)G * 3 * ND, (int64_t)3 * ND, ND, y, (float *)nullptr, seg_in(), 0,
+            hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH, MAP, DLT>), dim3(gx, (unsigned)G, (unsigned)q.B),
+                               dim3(kThreads), 0, st, x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(),
+                               (int64_t)G * CP * ND, (int64_t)CP * ND, ND, y, (float *)nullptr, seg_in(), 0,
                                (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg,
-                               G, p.D_res, (int)p.activation, dpart, (int64_t)G * 3 * q.D, (int64_t)3 * q.D);
+                               G, p.D_res, (int)p.activation, chp, (int64_t)G * CP * q.D, (int64_t)CP * q.D, q.D);
         }
         {
             Timed tm(2, st, !q.noalloc);
-            const int64_t n = 3 * lanes + (MAP ? q.B * q.D : 0);
+            const int64_t n = 3 * lanes + (cmask ? 3 * q.B * q.D : 0);
             hipLaunchKernelGGL(k_gsum, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
-                               (const float *)seg_in(), gacc(), q.B, ND, G, (const float *)dpart, q.D);
+                               (const float *)seg_in(), gacc(), q.B, ND, G, CP, (const float *)chp, cmask, q.D);
         }
     }
 
-    template <bool ZOH, bool MAP>
+    template <bool ZOH, bool MAP, bool DLT>
     bool pscan_block(int64_t t0, int64_t len) {
         switch (q.nt) {
-            case 4: pscans<4, ZOH, MAP>(t0, len); return true;
-            case 8: pscans<8, ZOH, MAP>(t0, len); return true;
-            case 16: pscans<16, ZOH, MAP>(t0, len); return true;
+            case 4: pscans<4, ZOH, MAP, DLT>(t0, len); return true;
+            case 8: pscans<8, ZOH, MAP, DLT>(t0, len); return true;
+            case 16: pscans<16, ZOH, MAP, DLT>(t0, len); return true;
             default: return false;
+        }
+    }
+
+    template <bool DLT>
+    bool pscan_var(int64_t t0, int64_t len) {
+        switch (q.var) {
+            case 0: return pscan_block<false, false, DLT>(t0, len);
+            case kZoh: return pscan_block<true, false, DLT>(t0, len);
+            case kOutMap: return pscan_block<false, true, DLT>(t0, len);
+            default: return pscan_block<true, true, DLT>(t0, len);
         }
     }
 
@@ -2756,13 +2889,8 @@ struct Launcher {
             return q.K == 1 ? cscan_block<1>(t0, len) : (q.K == 2 ? cscan_block<2>(t0, len) : false);
         }
         if (q.order == 3) {
-            if (q.ns != 1 || (q.var & ~(kZoh | kOutMap))) return false;
-            switch (q.var) {
-                case 0: return pscan_block<false, false>(t0, len);
-                case kZoh: return pscan_block<true, false>(t0, len);
-                case kOutMap: return pscan_block<false, true>(t0, len);
-                default: return pscan_block<true, true>(t0, len);
-            }
+            if (q.ns != 1 || (q.var & ~(kZoh | kOutMap)) || (q.K != 2 && q.K != 4)) return false;
+            return q.K == 4 ? pscan_var<true>(t0, len) : pscan_var<false>(t0, len);
         }
         if (q.order == 2) {
             if (q.ns != 1) return false;
@@ -2798,7 +2926,7 @@ struct Launcher {
         const unsigned gs = (unsigned)((lanes_all + kThreads - 1) / kThreads);
         const float *d2h_in = q.order == 2 ? p.d2h_in : nullptr;
         float *d2h_out = q.order == 2 ? p.d2h_out : nullptr;
-        const int64_t nacc = 3 * q.B * q.N * q.D + q.B * q.D;   // gacc with its [B][D] tail
+        const int64_t nacc = 3 * q.B * q.N * q.D + 3 * q.B * q.D;   // gacc with its [3][B][D] tail
         {
             Timed tm(4, st, !q.noalloc);
             hipLaunchKernelGGL(k_state_import, dim3(gs), dim3(kThreads), 0, st, p.h_in, p.dh_in, d2h_in, state(), q.B,
@@ -2838,9 +2966,11 @@ struct Launcher {
         if (q.order == 3) {
             Timed tm(4, st, !q.noalloc);
             float *gD = (q.var & kOutMap) && p.D_res ? p.grad_D_res : nullptr;
-            const int64_t nd3 = 3 * q.N * q.D + (gD ? q.D : 0);
+            float *gW = q.K == 4 ? p.grad_w_delta : nullptr;
+            float *gS = q.K == 4 ? p.grad_b_delta : nullptr;
+            const int64_t nd3 = 3 * q.N * q.D + 3 * q.D;
             hipLaunchKernelGGL(k_gout, dim3((unsigned)((nd3 + kThreads - 1) / kThreads)), dim3(kThreads), 0, st,
-                               (const float *)gacc(), gA, gB, gC, gD, q.B, q.D, q.N);
+                               (const float *)gacc(), gA, gB, gC, gD, gW, gS, q.B, q.D, q.N);
         }
         if (p.h_out || p.dh_out || d2h_out) {
             Timed tm(4, st, !q.noalloc);

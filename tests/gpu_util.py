@@ -56,6 +56,17 @@ def rel_l2(got, ref):
     return float(np.linalg.norm((got - ref).ravel()) / (den if den > 0 else 1.0))
 
 
+def sum_error(got, ref, scale):
+    """||got - ref|| / ||scale|| in fp64, for accumulated sums whose terms
+    take both signs: scale holds, per output, the sum of the absolute values
+    of its terms (the condition of the summation), so that the measure does
+    not grow where the terms cancel."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.linalg.norm(np.asarray(scale, dtype=np.float64).ravel())
+    return float(np.linalg.norm((got - ref).ravel()) / (den if den > 0 else 1.0))
+
+
 def assert_close(y, dy, yo, dyo, tol=TOL, what=""):
     ey = rel_l2(y, yo)
     edys = [rel_l2(dy[k], dyo[k]) for k in range(dyo.shape[0])]

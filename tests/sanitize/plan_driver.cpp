@@ -34,6 +34,12 @@ static void check_layout(const pgf::Plan &q) {
     CHECK(q.n_chunks * q.chunk_len >= q.L);
     CHECK(q.L == 0 || (q.n_chunks - 1) * q.chunk_len < q.L);
     CHECK(q.chunk_len * q.D <= (int64_t(1) << 30));
+    if (q.order == 3) {
+        // one thread per channel with every lane, five state planes with the
+        // step size's flows, and room for the [3][B][N][D] + [3][B][D] sums
+        CHECK(q.ns == 1 && (q.K == 2 || q.K == 4) && q.comp == 1 + q.K);
+        CHECK(w.lr - w.gacc >= (size_t)(3 * q.B * q.N * q.D + 3 * q.B * q.D) * sizeof(float));
+    }
 }
 
 int main() {
@@ -48,7 +54,7 @@ int main() {
                 for (int64_t D : Ds)
                     for (int seg : segs)
                         for (int dt = 0; dt < 3; ++dt)
-                            for (int var = 0; var < 6; ++var) {
+                            for (int var = 0; var < 8; ++var) {
                                 pgf_params p;
                                 memset(&p, 0, sizeof(p));
                                 p.batch = (D == 77) ? 3 : 1;
@@ -64,6 +70,9 @@ int main() {
                                 p.A_im = var == 3 ? (const float *)16 : nullptr;   // tested for NULL only
                                 p.n_groups = var == 4 ? 2 : 0;
                                 p.dt_rank = (var == 5) ? 48 : 0;
+                                // the step size's parameter flows, alone and with the ZOH drive
+                                p.delta_flows = var >= 6 ? 1 : 0;
+                                if (var == 7) p.drive = 1;
                                 pgf::Plan q;
                                 const int rc = pgf::make_plan(&p, &q);
                                 CHECK(rc == PGF_OK || rc == PGF_ERR_INVALID_ARG || rc == PGF_ERR_UNSUPPORTED);

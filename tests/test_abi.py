@@ -300,6 +300,24 @@ def test_parameter_flows_take_the_zoh_drive_and_the_output_map_only():
             binding.plan(1, 100, 256, 16, 2, order=2, **kw)
 
 
+def test_step_size_flows_plan():
+    """delta_flows belongs to the parameter flows: every drive and output map
+    with it has kernels (the planner's dry run), the workspace grows by the
+    two extra state planes, and the other orders reject the flag."""
+    base = binding.workspace_bytes(1, 4096, 256, 16, 1, order=3, seg_len=64)
+    for kw in (dict(), dict(drive="zoh"), dict(act="silu"), dict(drive="zoh", act="silu")):
+        for seg in (0, -1, 64):
+            for N in (4, 8, 16):
+                p = binding.plan(2, 3000, 256, N, 1, order=3, seg_len=seg, delta_flows=True, **kw)
+                assert p["n_per_thread"] == N and p["n_split"] == 1
+    assert binding.workspace_bytes(1, 4096, 256, 16, 1, order=3, seg_len=64, delta_flows=True) > base
+    for order in (1, 2):
+        with pytest.raises(RuntimeError, match="INVALID_ARG"):
+            binding.plan(1, 100, 64, 16, 2, order=order, delta_flows=True)
+    with pytest.raises(RuntimeError, match="UNSUPPORTED"):
+        binding.plan(1, 100, 64, 32, 1, order=3, delta_flows=True)
+
+
 def test_support_matrix_has_kernels():
     """pgf_plan succeeds only when the launch sequence has a kernel for every
     step (a host-side dry run of the dispatch, the same check the entry

@@ -149,28 +149,30 @@ def test_sequential_multiblock_second_order():
     assert e <= gu.TOL, e
 
 
-@pytest.mark.parametrize("drive,omap", [("euler", False), ("zoh", False), ("euler", True), ("zoh", True)])
-def test_sequential_multiblock_param_grads(drive, omap):
-    """omap: SiLU output map with a residual weight (its gradient too)."""
+@pytest.mark.parametrize("drive,omap,dlt", [("euler", False, False), ("zoh", False, False), ("euler", True, False),
+                                            ("zoh", True, False), ("euler", False, True), ("zoh", True, True)])
+def test_sequential_multiblock_param_grads(drive, omap, dlt):
+    """omap: SiLU output map with a residual weight (its gradient too);
+    dlt: the flows of the step size's parameters."""
     inp = gu.custom("mamba130m", batch=1, seqlen=L_MB, d_inner=64)
     inp["gy"] = inputs.make_adjoint(inp["cfg"])
     act = "silu" if omap else "identity"
     if omap:
         inp["D_res"] = np.random.default_rng(15).standard_normal(64).astype(np.float32)
     print(f"case multiblock parameter flows {drive} act={act}", flush=True)
-    _plan_blocks(1, 64, 16, 1, order=3, drive=drive, act=act)
+    _plan_blocks(1, 64, 16, 1, order=3, drive=drive, act=act, delta_flows=dlt)
     x, _ = gu.inputs_to_dev(inp)
     gy = torch.from_numpy(inp["gy"]).to(gu.dev())
     prm = gu.params_to_dev(inp)
     runs = []
     for cs in CHUNK_SEGS:
         runs.append(binding.param_grads(x, gy, prm, seg_len=-1, chunk_segs=cs, return_state=True, drive=drive,
-                                        act=act))
+                                        act=act, delta_params=dlt))
         torch.cuda.synchronize()
     _equal_all(runs, "parameter flows")
-    ng = 4 if omap else 3
+    ng = (4 if omap else 3) + (2 if dlt else 0)
     got = runs[0][:1 + ng]
-    yo, G, _ = oracle.param_grads(inp["x"], inp["gy"], inp, drive=drive, act=act)
+    yo, G, _ = oracle.param_grads(inp["x"], inp["gy"], inp, drive=drive, act=act, delta_params=dlt)
     errs = [gu.rel_l2(a.cpu().numpy(), b) for a, b in zip(got, (yo,) + tuple(G))]
     print("multiblock param rel_l2 " + " ".join(f"{e:.3e}" for e in errs), flush=True)
     assert len(errs) == 1 + ng and max(errs) <= gu.TOL, errs

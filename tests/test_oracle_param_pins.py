@@ -410,3 +410,21 @@ def test_step_size_one_step_adjoint():
     ref_s = 1.3 * sg * (Cm[0, 0] * Bm[0, 0]).sum() * xv
     assert abs(G[-1][2] - ref_s) < 1e-14 * abs(ref_s) and abs(G[-2][2] - ref_s * xv) < 1e-14 * abs(ref_s * xv)
     assert np.all(G[-1][[0, 1]] == 0) and np.all(G[-2][[0, 1]] == 0)
+
+
+
+def test_step_size_summation_scale():
+    """The scale returned beside dl/dw_delta and dl/db_delta is the sum of
+    the absolute values of their terms: at least |G|, equal to it for a
+    single nonzero adjoint, and additive over the batch."""
+    p, x, gy = problem(88)
+    _, G, _, sc = oracle.param_grads(x, gy, p, delta_params=True, return_scale=True)
+    assert np.all(sc[0] >= np.abs(G[-2]) - 1e-15) and np.all(sc[1] >= np.abs(G[-1]) - 1e-15)
+    assert np.all(sc[0] > np.abs(G[-2])) and np.all(sc[1] > np.abs(G[-1]))
+    one = np.zeros_like(gy)
+    one[1, 7, 0] = -2.0
+    _, G1, _, sc1 = oracle.param_grads(x, one, p, delta_params=True, return_scale=True)
+    assert sc1[0][0] == abs(G1[-2][0]) and sc1[1][0] == abs(G1[-1][0])
+    _, _, _, sa = oracle.param_grads(x[:1], gy[:1], p, delta_params=True, return_scale=True)
+    _, _, _, sb = oracle.param_grads(x[1:], gy[1:], p, delta_params=True, return_scale=True)
+    assert relerr(sa[0] + sb[0], sc[0]) < 1e-15 and relerr(sa[1] + sb[1], sc[1]) < 1e-15

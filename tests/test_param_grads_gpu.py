@@ -30,21 +30,32 @@ def _run(inp, **kw):
     return out
 
 
-def _check(inp, what, channels=None, **kw):
+def _check(inp, what, channels=None, scaled=False, **kw):
     """y and every gradient (dl/dD_res too when inp has D_res) against the
-    oracle, optionally on sampled channels only."""
+    oracle, optionally on sampled channels only.  scaled: measure the step
+    size's gradients against the sums of the absolute values of their terms
+    (see gpu_util.sum_error) instead of their own norms."""
     print(f"case {what}", flush=True)
-    ng = 4 if inp.get("D_res") is not None else 3
+    dlt = kw.get("delta_params", False)
+    ng = (4 if inp.get("D_res") is not None else 3) + (2 if dlt else 0)
     got = list(_run(inp, **kw)[:1 + ng])
-    yo, G, _ = oracle.param_grads(inp["x"], inp["gy"], inp, channels=channels,
-                                  chunk=None if channels is None else 8192,
-                                  drive=kw.get("drive", "euler"), act=kw.get("act", "identity"))
+    out = oracle.param_grads(inp["x"], inp["gy"], inp, channels=channels, chunk=None if channels is None else 8192,
+                             drive=kw.get("drive", "euler"), act=kw.get("act", "identity"), delta_params=dlt,
+                             return_scale=dlt and scaled)
+    yo, G = out[0], out[1]
     assert len(G) == ng
     if channels is not None:
         idx = torch.from_numpy(np.asarray(channels)).to(gu.dev())
         got = [got[0].index_select(-1, idx)] + [g.index_select(0, idx) for g in got[1:]]
     errs = [gu.rel_l2(a.cpu().numpy(), b) for a, b in zip(got, (yo,) + tuple(G))]
-    names = ("y", "gA", "gB", "gC", "gD")
+    if dlt and scaled:
+        # dl/dw_delta and dl/db_delta are sums of terms of both signs over
+        # every step: over long sequences their error is measured against the
+        # sum of the terms' absolute values (the plain measure is printed too)
+        plain = errs[-2:]
+        errs[-2:] = [gu.sum_error(got[-2 + i].cpu().numpy(), G[-2 + i], out[3][i]) for i in range(2)]
+        print(f"{what} plain rel_l2 gW={plain[0]:.3e} gS={plain[1]:.3e}", flush=True)
+    names = ("y", "gA", "gB", "gC") + (("gD",) if inp.get("D_res") is not None else ()) + ("gW", "gS")
     print(f"{what} rel_l2 " + " ".join(f"{n}={e:.3e}" for n, e in zip(names, errs)), flush=True)
     for a in got:
         assert torch.all(torch.isfinite(a))
@@ -289,3 +300,102 @@ def test_param_grads_zoh_zero_eigenvalues():
     inp["A"][:, [0, 9]] = 0.0
     for seg in (64, -1):
         _check(inp, f"param zoh zero eigenvalues seg={seg}", seg_len=seg, drive="zoh")
+
+
+
+# ------------------------------------------------------------ step-size parameters
+# delta_params: the flows of w_delta and b_delta (Delta = softplus(w x + b))
+# beside the others, with dl/dw_delta and dl/db_delta per channel.
+
+@pytest.mark.parametrize("drive,act,dres,N,seg", [
+    ("euler", "identity", False, 16, 0), ("euler", "identity", False, 8, -1), ("zoh", "identity", False, 16, 64),
+    ("euler", "silu", True, 16, -1), ("zoh", "silu", True, 16, 0), ("zoh", "silu", True, 4, -1)])
+def test_param_grads_step_size_parity(drive, act, dres, N, seg):
+    inp = _case("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N)
+    if dres:
+        _with_dres(inp)
+    _check(inp, f"param step size {drive} act={act} dres={dres} N={N} seg={seg}", seg_len=seg, drive=drive,
+           act=act, delta_params=True)
+
+
+def test_param_grads_step_size_bf16_stiff():
+    _check(_case("stiff128k", seqlen=1500, d_inner=64), "param step size stiff bf16", delta_params=True)
+
+
+def test_param_grads_step_size_leaves_the_rest_unchanged():
+    """The other outputs are the same bits with and without the step size's
+    flows (the same arithmetic runs for them)."""
+    inp = _with_dres(_case("mamba130m", batch=2, seqlen=900, d_inner=64))
+    for drive, seg in (("euler", 64), ("zoh", -1)):
+        a = _run(inp, seg_len=seg, drive=drive, act="silu", return_state=True)
+        b = _run(inp, seg_len=seg, drive=drive, act="silu", return_state=True, delta_params=True)
+        for i in range(5):
+            assert torch.equal(a[i], b[i]), (drive, i)
+        assert torch.equal(a[5], b[7]) and torch.equal(a[6], b[8][:2]), drive
+
+
+def test_param_grads_step_size_blocks_and_handoff():
+    inp = _case("mamba130m", batch=2, seqlen=1000, d_inner=48)
+    ref = _run(inp, seg_len=64, chunk_segs=1, return_state=True, delta_params=True)
+    assert len(ref) == 8 and tuple(ref[7].shape) == (4, 2, 48, 16)
+    for cs in (3, 0):
+        got = _run(inp, seg_len=64, chunk_segs=cs, return_state=True, delta_params=True)
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), cs
+    x, _ = gu.inputs_to_dev(inp)
+    gy = torch.from_numpy(inp["gy"]).to(gu.dev())
+    prm = gu.params_to_dev(inp)
+    s = 384
+    a = binding.param_grads(x[:, :s], gy[:, :s], prm, seg_len=64, return_state=True, delta_params=True)
+    b = binding.param_grads(x[:, s:], gy[:, s:], prm, seg_len=64, h_in=a[6], gamma_in=a[7], grads=a[1:6],
+                            return_state=True, delta_params=True)
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat([a[0], b[0]], 1), ref[0])
+    assert torch.equal(b[6], ref[6]) and torch.equal(b[7], ref[7])
+    for i in range(1, 6):
+        assert gu.rel_l2(b[i].cpu().numpy(), ref[i].cpu().numpy()) < 1e-6, i
+    # the entry state of all five planes against the oracle
+    g = np.random.default_rng(19)
+    st = [g.standard_normal((2, 48, 16)).astype(np.float32) for _ in range(5)]
+    got = _run(inp, h_in=torch.from_numpy(st[0]), gamma_in=torch.from_numpy(np.stack(st[1:])), return_state=True,
+               delta_params=True)
+    yo, G, so = oracle.param_grads(inp["x"], inp["gy"], inp, state=tuple(st), delta_params=True)
+    for i, (gt, rf) in enumerate(zip(got[:6], (yo,) + tuple(G))):
+        assert gu.rel_l2(gt.cpu().numpy(), rf) < gu.TOL, i
+    assert gu.rel_l2(got[6].cpu().numpy(), so[0]) < gu.TOL
+    for k in range(4):
+        assert gu.rel_l2(got[7][k].cpu().numpy(), so[1 + k]) < gu.TOL, k
+
+
+def test_param_grads_step_size_full_size_sampled_channels():
+    inp = _with_dres(_case("pulse128k"))
+    g = np.random.default_rng(8)
+    ch = np.unique(np.concatenate([[0, 1535], g.choice(np.arange(1, 1535), 4, replace=False)]))
+    _check(inp, "param step size pulse128k full", channels=ch, act="silu", delta_params=True, scaled=True)
+
+
+def test_param_grads_step_size_argument_checks():
+    inp = _case("tiny", seqlen=64)
+    x, _ = gu.inputs_to_dev(inp)
+    gy = torch.zeros_like(x)
+    prm = gu.params_to_dev(inp)
+    D, N = inp["A"].shape
+    with pytest.raises(ValueError, match="grads"):   # three buffers where five are needed
+        binding.param_grads(x, gy, prm, grads=tuple(torch.zeros(D, N, device=gu.dev()) for _ in range(3)),
+                            delta_params=True)
+    with pytest.raises(RuntimeError, match="INVALID_ARG"):   # the flag belongs to the parameter flows
+        binding.plan(1, 64, D, N, 1, order=1, delta_flows=True)
+    # through the C-ABI: the flag set and grad_b_delta NULL
+    pr = binding.make_params(1, 64, D, N, 1, order=3, delta_flows=True)
+    keep = []
+    binding._model_params(pr, prm, D, gu.dev(), keep)
+    ws = torch.empty(binding.workspace_bytes(1, 64, D, N, 1, order=3, delta_flows=True), dtype=torch.uint8,
+                     device=gu.dev())
+    pr.workspace, pr.workspace_bytes = ws.data_ptr(), ws.numel()
+    gw = torch.zeros(D, device=gu.dev())
+    pr.grad_w_delta = gw.data_ptr()
+    y = torch.empty_like(x)
+    g3 = [torch.zeros(D, N, device=gu.dev()) for _ in range(3)]
+    rc = binding.lib().pgf_param_grads(x.data_ptr(), gy.data_ptr(), ctypes.byref(pr), y.data_ptr(),
+                                       *[g.data_ptr() for g in g3], None)
+    assert rc == -1   # PGF_ERR_INVALID_ARG
