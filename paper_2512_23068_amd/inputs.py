@@ -271,6 +271,8 @@ def _la_rows(cfg: LaConfig, field: int, shape_tail, threads: int) -> np.ndarray:
     """N(0,1) draws [B,H,L,*tail] for one field, block-seeded per (b, h)."""
     B, H, L = cfg.batch, cfg.heads, cfg.seqlen
     out = np.empty((B, H, L) + tuple(shape_tail), dtype=np.float32)
+    if L == 0:
+        return out
     for b in range(B):
         for h in range(H):
             _normal_rows(out[b, h].reshape(L, -1), cfg.index, 200 + field, b * H + h, threads)

@@ -45,3 +45,12 @@ def test_bf16_workload_values_are_bf16():
     cfg = inputs.get_config("stiff128k").with_(seqlen=64, d_inner=128)
     x = inputs.make_x(cfg)
     assert np.array_equal(x, inputs.bf16_bits_to_f32(inputs.round_to_bf16_bits(x)).reshape(x.shape))
+
+
+def test_empty_sequences():
+    """Every generator gives empty arrays of the right shapes for L = 0."""
+    ssm = inputs.make_inputs(inputs.get_config("mamba130m").with_(seqlen=0, d_inner=8, n_dirs=2))
+    assert ssm["x"].shape == (1, 0, 8) and ssm["dx"].shape == (2, 1, 0, 8)
+    assert inputs.make_adjoint(inputs.get_config("mamba130m").with_(seqlen=0, d_inner=8)).shape == (1, 0, 8)
+    la = inputs.make_la_inputs(inputs.LA_BY_NAME["la_tiny"].with_(seqlen=0, n_dirs=2))
+    assert la["q"].shape == (1, 2, 0, 16) and la["dv"].shape == (2, 1, 2, 0, 64)
