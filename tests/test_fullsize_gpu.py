@@ -213,3 +213,37 @@ def test_sequential_tail_pulse128k():
     gu.record("pulse128k_sequential_tail", {"seg_len": -1, "channels": sel.tolist(), "tail_steps": 1024,
                                             "tail_dy_rel_l2": tail, "tail_bound": bound})
     assert np.isfinite(tail) and tail <= bound, (tail, bound)
+
+
+@pytest.mark.parametrize("seg", [0, -1])
+def test_ghost_pulse_full_size(seg):
+    """The ghost pulse at the paper's depth: pulse128k's model and sizes
+    (L = 131072, D = 1536) with a single micro-perturbation dx = 1e-3 in one
+    channel at t0 = 100000 and zero elsewhere.  Before t0 the tangent output
+    is exactly zero in every channel (no background leakage); from t0 on
+    every channel responds (the projections spread the pulse), and sampled
+    channels, the perturbed one among them, match the oracle over the rest
+    of the sequence."""
+    t0, dp = 100000, 5
+    inp = gu.custom("pulse128k")
+    inp["dx"] = np.zeros_like(inp["dx"])
+    inp["dx"][0, 0, t0, dp] = 1e-3
+    print(f"case ghost pulse seg={seg}", flush=True)
+    x, dx = gu.inputs_to_dev(inp)
+    y, dy = binding.scan_jvp(x, dx, gu.params_to_dev(inp), seg_len=seg)
+    torch.cuda.synchronize()
+    leak = float(dy[:, :, :t0].abs().max())
+    reach = bool(torch.all(dy[0, 0, t0:].abs().sum(0) > 0))
+    ch = np.unique(np.concatenate([[0, dp, 1535], _channels(1536, 2, seed=17)]))
+    yo, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp, channels=ch, chunk=8192)
+    idx = torch.from_numpy(ch).to(gu.dev())
+    dys = dy.index_select(-1, idx)[:, :, t0:].cpu().numpy()
+    e = gu.rel_l2(dys, dyo[:, :, t0:])
+    print(f"ghost pulse seg={seg}: leak {leak:.1e}, every channel responds {reach}, rel_l2 dy after t0 {e:.3e} "
+          f"on {len(ch)} channels", flush=True)
+    if seg == 0:
+        gu.record("ghost_pulse_t100000", {"t0": t0, "channel": dp, "magnitude": 1e-3, "leak_max_abs": leak,
+                                          "every_channel_responds": reach, "dy_rel_l2_after_t0": e,
+                                          "channels_compared": len(ch)})
+    assert leak == 0.0 and reach
+    assert e <= gu.TOL, e
