@@ -42,6 +42,10 @@ def parse():
     ap.add_argument("--drive", default="euler", choices=("euler", "zoh"), help="input drive (first order)")
     ap.add_argument("--act", default="identity", choices=("identity", "silu"), help="output activation (first order and parameter flows)")
     ap.add_argument("--dres", action="store_true", help="add a residual weight D_res ~ N(0,1) to the output map")
+    for name in ("batch", "seqlen", "d-inner", "d-state", "n-dirs"):
+        ap.add_argument(f"--{name}", type=int, default=0,
+                        help=f"override the workload's {name} (0 = the workload's own; the line's workload "
+                             f"name then says so)")
     ap.add_argument("--delta-params", action="store_true",
                     help="parameter flows (--order 3): also the flows of w_delta and b_delta")
     ap.add_argument("--groups", type=int, default=1,
@@ -220,10 +224,19 @@ class Workload:
         self.__dict__.update(kw)
 
 
+def size_overrides(args):
+    """The size fields given on the command line, as ScanConfig keywords."""
+    return {k: getattr(args, k) for k in ("batch", "seqlen", "d_inner", "d_state", "n_dirs")
+            if getattr(args, k, 0)}
+
+
 def setup_ssm(args, np, torch, binding, inputs):
     cfg = inputs.get_config(args.workload)
+    over = size_overrides(args)
+    if over:
+        cfg = cfg.with_(**over)
     variant = args.drive != "euler" or args.act != "identity" or args.dres or args.complex or args.groups > 1 or \
-        args.lowrank > 0 or args.delta_params
+        args.lowrank > 0 or args.delta_params or bool(over)
     param_variant = args.order == 3 and not (args.complex or args.groups > 1 or args.lowrank > 0)
     if args.delta_params and args.order != 3:
         print("bench.py: --delta-params belongs to the parameter flows (--order 3)", file=sys.stderr)
@@ -313,8 +326,9 @@ def la_flops_per_lane_step(K):
 
 def setup_la(args, np, torch, binding, inputs):
     cfg = inputs.LA_BY_NAME[args.workload]
-    if args.order != 1 or args.drive != "euler" or args.act != "identity" or args.dres:
-        print("bench.py: the linear-attention workloads take no --order/--drive/--act/--dres", file=sys.stderr)
+    if args.order != 1 or args.drive != "euler" or args.act != "identity" or args.dres or size_overrides(args):
+        print("bench.py: the linear-attention workloads take no --order/--drive/--act/--dres or size overrides",
+              file=sys.stderr)
         sys.exit(2)
     B, H, L, DK, DV, K = cfg.batch, cfg.heads, cfg.seqlen, cfg.d_key, cfg.d_value, cfg.n_dirs
     dev = torch.device("cuda:0")
@@ -490,7 +504,8 @@ def variant_suffix(args):
     parts = ([args.drive] if args.drive != "euler" else []) + ([args.act] if args.act != "identity" else []) + \
         (["dres"] if args.dres else []) + (["s4dlin"] if args.complex else []) + \
         ([f"g{args.groups}"] if args.groups > 1 else []) + ([f"lr{args.lowrank}"] if args.lowrank > 0 else []) + \
-        (["dparams"] if getattr(args, "delta_params", False) else [])
+        (["dparams"] if getattr(args, "delta_params", False) else []) + \
+        [f"{k}{v}" for k, v in size_overrides(args).items()]
     return "".join("-" + p for p in parts)
 
 

@@ -247,3 +247,34 @@ def test_ghost_pulse_full_size(seg):
                                           "channels_compared": len(ch)})
     assert leak == 0.0 and reach
     assert e <= gu.TOL, e
+
+
+def test_length_invariance():
+    """The relative error against the oracle does not grow with L (App. B):
+    the mamba130m recipe (dx ~ N(0,1)) at L = 2^10 .. 2^17 in the default
+    plan, on 16 sampled channels; the fitted slope of the error in log2 L
+    is recorded, and the error at the longest L stays within 3x of the
+    shortest and below the bar."""
+    Ls = [2 ** k for k in range(10, 18)]
+    ch = _channels(1536, 2, seed=23)
+    idx = torch.from_numpy(ch).to(gu.dev())
+    base = gu.custom("mamba130m", seqlen=Ls[-1])
+    prm = gu.params_to_dev(base)
+    x_all, dx_all = gu.inputs_to_dev(base)
+    yo, dyo, _, _ = oracle.scan_jvp(base["x"], base["dx"], base, channels=ch, chunk=8192)
+    ey, edy = [], []
+    for L in Ls:
+        print(f"case length invariance L={L}", flush=True)
+        y, dy = binding.scan_jvp(x_all[:, :L].contiguous(), dx_all[:, :, :L].contiguous(), prm)
+        torch.cuda.synchronize()
+        # the oracle is causal: its first L steps are the L-step call's outputs
+        ey.append(gu.rel_l2(y.index_select(-1, idx).cpu().numpy(), yo[:, :L]))
+        edy.append(gu.rel_l2(dy.index_select(-1, idx).cpu().numpy(), dyo[:, :, :L]))
+    slope_y = float(np.polyfit(np.log2(Ls), ey, 1)[0])
+    slope_dy = float(np.polyfit(np.log2(Ls), edy, 1)[0])
+    print("L", Ls, "\nrel_l2 y", [f"{e:.2e}" for e in ey], "\nrel_l2 dy", [f"{e:.2e}" for e in edy],
+          f"\nslope per doubling of L: y {slope_y:.2e}, dy {slope_dy:.2e}", flush=True)
+    gu.record("length_invariance", {"L": Ls, "y_rel_l2": ey, "dy_rel_l2": edy, "slope_per_doubling_y": slope_y,
+                                    "slope_per_doubling_dy": slope_dy, "channels_compared": len(ch)})
+    assert max(ey + edy) <= gu.TOL
+    assert ey[-1] <= 3 * ey[0] and edy[-1] <= 3 * edy[0], (ey, edy)
