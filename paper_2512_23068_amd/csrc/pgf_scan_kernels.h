@@ -2108,25 +2108,29 @@ __global__ __launch_bounds__(kThreads) void k_pcarry(
 static __global__ __launch_bounds__(kThreads) void k_gsum(
     const float *__restrict__ part, float *__restrict__ acc, int64_t Bsz, int64_t ND, int G, int CP,
     const float *__restrict__ chp, int cmask, int64_t D) {
-    constexpr int GB = 16;
+    constexpr int GB = 32;   // loads in flight per thread: the sums are latency bound
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     const int64_t n3 = 3 * Bsz * ND;
+    // a lane-plane sum (part, stride ND) or a per-channel one (chp, stride D)
+    const float *src;
+    int64_t stride;
     if (idx >= n3) {
         const int64_t j = idx - n3, c = j / (Bsz * D), b = (j / D) % Bsz, d = j % D;
         if (c >= 3 || !((cmask >> c) & 1)) return;
-        float s = acc[idx];
-        for (int g = 0; g < G; ++g) s += chp[((b * G + g) * CP + c) * D + d];
-        acc[idx] = s;
-        return;
+        src = chp + (b * G * CP + c) * D + d;
+        stride = CP * D;
+    } else {
+        const int64_t c = idx / (Bsz * ND), b = (idx / ND) % Bsz, r = idx % ND;
+        src = part + (b * G * CP + c) * ND + r;
+        stride = CP * ND;
     }
-    const int64_t c = idx / (Bsz * ND), b = (idx / ND) % Bsz, r = idx % ND;
     float s = acc[idx];
     for (int g0 = 0; g0 < G; g0 += GB) {
         float v[GB];
 #pragma unroll
         for (int j = 0; j < GB; ++j) {
             const int g = g0 + j < G ? g0 + j : G - 1;
-            v[j] = part[((b * G + g) * CP + c) * ND + r];
+            v[j] = src[g * stride];
         }
 #pragma unroll
         for (int j = 0; j < GB; ++j) {
