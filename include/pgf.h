@@ -125,9 +125,10 @@ typedef struct pgf_params {
      * not written). */
     const float *d2h_in;
     float *d2h_out;
-    /* Model variants of the first-order scan (Sec. 3 output map, the
-     * appendix's zero-order-hold drive); zero for the others.  With any of
-     * them set, pgf_scan_jvp supports N <= 16 and K <= 2.
+    /* Model variants of the first-order scan and of the parameter flows
+     * (Sec. 3 output map, the appendix's zero-order-hold drive); zero for
+     * the second order.  With any of them set, pgf_scan_jvp supports
+     * N <= 16 and K <= 2 (pgf_param_grads: N <= 16, as always).
      *   drive      : PGF_DRIVE_EULER or PGF_DRIVE_ZOH
      *   activation : PGF_ACT_IDENTITY or PGF_ACT_SILU
      *   D_res      : device, [D] f32 residual weight, or NULL (= 0)
