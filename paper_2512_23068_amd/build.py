@@ -56,5 +56,21 @@ def build(verbose: bool = False) -> str:
     return OUT
 
 
+CALLER_SRC = os.path.join(ROOT, "tests", "native", "pgf_c_caller.cpp")
+CALLER = os.path.join(ROOT, "tests", "native", "pgf_c_caller")
+
+
+def build_caller() -> str:
+    """Compiles the plain C-ABI caller used by the tests (host code only),
+    linked against the in-tree libpgf.so."""
+    tmp = CALLER + ".tmp"
+    cmd = [hipcc(), "-O2", "-std=c++17", "--offload-arch=gfx950", "-I", os.path.join(ROOT, "include"), CALLER_SRC,
+           "-o", tmp, "-L", _HERE, "-lpgf", "-Wl,-rpath,$ORIGIN/../../paper_2512_23068_amd"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, CALLER)
+    return CALLER
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_caller())
