@@ -1746,11 +1746,12 @@ __global__ __launch_bounds__(kThreads) void k_carry(
 // and the rescan (OUT) accumulates, per lane, over its segment
 //   gradA += gy C GA',  gradB += gy C GB',  gradC += gy h'.
 // Records are [B(N) | C(N)].  OUT=false: zero-start segment aggregates
-// (end state in agg_h [B][G][3][N][D], sum of Delta in agg_s [B][G][3][D],
-// component 0).  OUT=true: scan from the entry state in init (as k_scan) and
-// write y; the three gradient sums go to gout at the same place as the
-// entry state (the entry slot is read before it is overwritten, by the same
-// thread), or are added to gout when gadd is set (sequential evaluation:
+// (end state in agg_h [B][G][CP][N][D], sum of Delta in agg_s
+// [B][G][CP][D], component 0; CP = 3 planes, 5 with DLT below).  OUT=true:
+// scan from the entry state in init (as k_scan) and write y; the three
+// per-lane gradient sums go to gout at the same place as the first three
+// planes of the entry state (the entry slot is read before it is
+// overwritten, by the same thread), or are added to gout when gadd is set (sequential evaluation:
 // gout is the running sum of the call, and end_state receives the state;
 // the launcher runs one launch per kSeqChunk steps, so the additions happen
 // in the same order for every host block size).
