@@ -1522,7 +1522,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(OUT ? 
         wc[j] = load_in(Wb, o);
     }
     float pf = 0.0f;     // records of the next tile, touched (touch_records)
-    for (int64_t tb = ts; tb < te; tb += TT) {
+    // Whole tiles run without per-step checks, a segment's last tile
+    // guarded (as in k_scan); the aggregate pass over bf16 rows keeps the
+    // check on every step, which measured faster there.
+    auto tile = [&](const int64_t tb, auto guard) {
+        constexpr bool GUARD = decltype(guard)::value;
         float xn[TT], vn[TT], wn[TT];
         if constexpr (std::is_same<InT, float>::value) {   // (slower with bf16 rows)
             asm volatile("" ::"v"(pf));
@@ -1539,7 +1543,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(OUT ? 
 #pragma unroll
         for (int j = 0; j < TT; ++j) {
             const int64_t t = tb + j;
-            if (t < te) {
+            if (!GUARD || t < te) {
                 const float xv = xc[j], vv = vc[j], wv = wc[j];
                 float delta, sw, s2;
                 discretize2(xv, w, bd, delta, sw, s2);
@@ -1600,6 +1604,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(OUT ? 
             vc[j] = vn[j];
             wc[j] = wn[j];
         }
+    };
+    if constexpr (OUT || std::is_same<InT, float>::value) {
+        int64_t tb = ts;
+        for (; tb + TT < te; tb += TT) tile(tb, std::false_type{});
+        tile(tb, std::true_type{});
+    } else {
+        for (int64_t tb = ts; tb < te; tb += TT) tile(tb, std::true_type{});
     }
 
     if (!active) return;
