@@ -303,7 +303,7 @@ def setup_ssm(args, np, torch, binding, inputs):
         alg_bytes = tokch * ((1 + K) * (s_in + 4) + (4 if args.order == 2 else 0))
     name = cfg.name + SUFFIX[args.order]
     return Workload(
-        step=step, tokch=tokch, alg_bytes=alg_bytes,
+        step=step, tokch=tokch, alg_bytes=alg_bytes, lane_steps=tokch * N,
         flops=tokch * N * (cplx_flops_per_lane_step(K) if args.complex else scan_flops_per_lane_step(K, args.order)),
         payload=payload, plan=plan, metric=METRIC[args.order],
         kernel={1: "k_scan/k_scan_sh (scan with outputs)", 2: "k_scan2 (scan with outputs)",
@@ -351,7 +351,7 @@ def setup_la(args, np, torch, binding, inputs):
     # read v, dv_k and the key-side q, k, g and tangents once, write o, do_k
     alg_bytes = tokch * 4 * (2 * (1 + K)) + B * H * L * DK * 4 * (3 + 3 * K)
     return Workload(
-        step=step, tokch=tokch, alg_bytes=alg_bytes, flops=tokch * DK * la_flops_per_lane_step(K),
+        step=step, tokch=tokch, alg_bytes=alg_bytes, lane_steps=tokch * DK, flops=tokch * DK * la_flops_per_lane_step(K),
         payload=payload, plan=plan, metric="decaying linear attention primal+JVP Gtok·ch/s",
         kernel="k_la_scan (scan with outputs)", traffic=committed_traffic(cfg.name, "scan_out", "la"), dtype="f32",
         config={"workload": cfg.name, "batch": B, "heads": H, "seq_len": L, "d_key": DK, "d_value": DV,
@@ -444,6 +444,7 @@ def main():
     kernels = {k: {"ms_per_step": round(v[0] / args.steps, 4), "launches_per_step": v[1] / args.steps}
                for k, v in kern.items()}
     plan, payload, metric, dtype, config, alg_bytes = w.plan, w.payload, w.metric, w.dtype, w.config, w.alg_bytes
+    lane_steps = w.lane_steps
     cpu_fn = None if args.no_cpu else w.cpu
     # GPU outputs of the last timed step (every step writes the same values)
     outputs = getattr(w, "outputs", None)
@@ -488,6 +489,9 @@ def main():
         "config": config,
         "hbm_gbs_path": round(alg_bytes / (ms_step * 1e-3) / 1e9, 1),
         "hbm_frac_path": round(alg_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        # state lanes advanced per second (a lane is one (b, d, n) of the
+        # recurrence, one (b, h, key, value) entry for linear attention)
+        "lane_steps_g_per_s": round(lane_steps / (ms_step * 1e-3) / 1e9, 1),
         "vram": {"peak_bytes": int(peak), "payload_bytes": int(payload), "workspace_bytes": plan["workspace_bytes"],
                  "peak_minus_payload": int(peak - payload)},
         "plan": plan,
