@@ -20,6 +20,9 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, vendor figure
 FP32_VECTOR_PEAK_TFLOPS = 157.3  # MI355X fp32 vector, vendor figure
+# The same units without packed FP32 (the kernels are built without it): 256
+# CUs x 4 SIMDs x 16 lanes per cycle x 2 flops per fma x 2.4 GHz.
+FP32_UNPACKED_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
 
 
 def parse():
@@ -434,6 +437,8 @@ def main():
         "peak": FP32_VECTOR_PEAK_TFLOPS,
         "unit": "TFLOP/s",
         "frac": round(tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
+        "peak_unpacked": round(FP32_UNPACKED_PEAK_TFLOPS, 2),
+        "frac_unpacked": round(tflops / FP32_UNPACKED_PEAK_TFLOPS, 4),
         "traffic": w.traffic,
         "hbm_achieved_gbs": round(hbm_gbs, 1),
         "hbm_frac": round(hbm_gbs / HBM_PEAK_GBS, 4),

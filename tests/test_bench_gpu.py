@@ -44,6 +44,7 @@ def test_bench_line_fields_and_parity():
     assert rf["bound"] in ("hbm", "mfma", "alu") and rf["unit"] in ("GB/s", "TFLOP/s")
     assert rf["peak"] > 0 and rf["achieved"] > 0
     assert rf["frac"] == pytest.approx(rf["achieved"] / rf["peak"], rel=1e-2, abs=1e-4)
+    assert rf["peak_unpacked"] == pytest.approx(78.64, abs=0.01) and rf["frac_unpacked"] >= rf["frac"]
     cb = d["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["cores"] >= 1 and cb["value"] > 0 and cb["sample"]
     par = d["parity"]
