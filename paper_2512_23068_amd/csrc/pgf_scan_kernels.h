@@ -193,19 +193,20 @@ struct Variant {
 };
 
 // The ZOH drive coefficient e = (Abar - 1)/A of one lane, z = Delta*A,
-// Abar = exp(z) as computed by the caller.  For |z| < 1/4, e = Delta * phi(z) with
-// phi(z) = expm1(z)/z = sum_k z^k/(k+1)! summed to z^6 (the first omitted
-// term is below 2e-9 relative); otherwise (Abar - 1) * (1/A), where the
-// subtraction loses less than 3 bits.  A = 0 takes the first branch (e = Delta).
+// Abar = exp(z) as computed by the caller.  For |z| < 1/16, e = Delta * phi(z)
+// with phi(z) = expm1(z)/z = sum_k z^k/(k+1)! summed to z^4 (the first
+// omitted term, z^5/720, is below 2e-9 relative); otherwise (Abar - 1) *
+// (1/A), where the subtraction loses at most 4 bits, so that Abar's rounding
+// costs e at most ~1e-6 relative (at |z| = 1/16; the same bound as the
+// step's other f32 roundings over a segment).  A = 0 takes the first branch
+// (e = Delta).
 __device__ __forceinline__ float zoh_coef(float delta, float a_n, float inv_a, float abar) {
     const float z = delta * a_n;
-    float ph = fmaf(z, 1.0f / 5040.0f, 1.0f / 720.0f);
-    ph = fmaf(z, ph, 1.0f / 120.0f);
-    ph = fmaf(z, ph, 1.0f / 24.0f);
+    float ph = fmaf(z, 1.0f / 120.0f, 1.0f / 24.0f);
     ph = fmaf(z, ph, 1.0f / 6.0f);
     ph = fmaf(z, ph, 0.5f);
     ph = fmaf(z, ph, 1.0f);
-    return fabsf(z) < 0.25f ? delta * ph : (abar - 1.0f) * inv_a;
+    return fabsf(z) < 0.0625f ? delta * ph : (abar - 1.0f) * inv_a;
 }
 
 // The derivative in A of the ZOH drive coefficient e = (Abar - 1)/A of one
@@ -1017,15 +1018,18 @@ void k_scan(
                     const float gv = Af[i] * sv;
                     float hn;
                     if constexpr ((VAR & kZoh) != 0) {
-                        // b = e B x, db_k = Abar dDelta_k B x + e (dB_k x + B dx_k)
+                        // b = e B x, db_k = Abar dDelta_k B x + e (dB_k x + B dx_k);
+                        // with the transition's term A Abar h dDelta_k the
+                        // dDelta_k terms share the factor Abar B x + g.
                         const float e = zoh_coef(delta, Af[i], Ai[i], a);
                         const float Bx = Bn * xv;
                         hn = fmaf(e, Bx, sv);
+                        const float r = fmaf(a, Bx, gv);
 #pragma unroll
                         for (int k = 0; k < K; ++k) {
                             const float dBn = rec[(1 + k) * N + n];
-                            const float jk = fmaf(a * dD[k], Bx, e * fmaf(dBn, xv, Bn * dxc[k][j]));
-                            dh[k][i] = fmaf(a, dh[k][i], fmaf(gv, dD[k], jk));
+                            const float jk = e * fmaf(dBn, xv, Bn * dxc[k][j]);
+                            dh[k][i] = fmaf(a, dh[k][i], fmaf(dD[k], r, jk));
                         }
                     } else {
                         hn = fmaf(Bn, u, sv);
