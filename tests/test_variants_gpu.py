@@ -121,3 +121,30 @@ def test_vanishing_step_keeps_the_state(seg):
         yo, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp, h_in=h0.cpu().numpy(), dh_in=dh0.cpu().numpy(),
                                         drive=drive)
         gu.assert_close(y.cpu().numpy(), dy.cpu().numpy(), yo, dyo, what=f"vanishing step {drive}")
+
+
+def test_zoh_coefficient_across_the_switch():
+    """One step from a zero state leaves h = e B x per lane: with Delta = 0.1
+    in every channel and |A| log-spaced over 1e-4 ... 160 (1024 lanes), z =
+    Delta*A runs over 1e-5 ... 16 through both branches of the coefficient
+    and its switch; every lane's h and dh match the oracle's within 2e-6
+    relative (e's own error is below ~1e-6 on either side of the switch)."""
+    inp = gu.custom("mamba130m", batch=1, seqlen=1, d_inner=64, d_state=16, dx_kind="normal")
+    D, N = 64, 16
+    inp["A"] = (-np.logspace(-4.0, 2.2, D * N)).reshape(D, N).astype(np.float32)
+    inp["w_delta"] = np.zeros(D, np.float32)
+    inp["b_delta"] = np.full(D, np.log(np.expm1(0.1)), np.float32)
+    # positive inputs and weights: B, dB and the drive are sums without
+    # cancellation, so h / (B x) isolates e
+    inp["x"] = (np.abs(inp["x"]) + 0.5).astype(np.float32)
+    inp["dx"] = (np.abs(inp["dx"]) + 0.5).astype(np.float32)
+    for w in ("W_B", "W_C"):
+        inp[w] = np.full((D, N), 1.0 / D, np.float32)
+    print("case zoh coefficient sweep", flush=True)
+    _, _, h, dh = gu.run(inp, drive="zoh", return_state=True)
+    _, _, ho, dho = oracle.scan_jvp(inp["x"], inp["dx"], inp, drive="zoh")
+    for got, ref in ((h, ho), (dh, dho)):
+        got = got.cpu().numpy().astype(np.float64)
+        rel = np.abs(got - ref) / np.maximum(np.abs(ref), 1e-30)
+        print(f"zoh coefficient sweep: max rel err {rel.max():.3e}", flush=True)
+        assert np.all(np.isfinite(got)) and rel.max() <= 2e-6, rel.max()
