@@ -542,7 +542,7 @@ def cpu_baseline(cfg, cpu_steps):
     sub, dt, ref = run(Ls)
     tokch = sub.batch * Ls * sub.d_inner
     return ({"value": round(tokch / dt / 1e9, 6), "unit": "Gtok·ch/s", "cores": threads, "cpu_model": cpu_model(),
-             "kind": "oracle",
+             "kind": "oracle", "lane_steps_g_per_s": round(tokch * sub.d_state / dt / 1e9, 6),
              "sample": f"{cfg.name} first {Ls} steps, all {sub.d_inner} channels, batch {sub.batch}, "
                        f"{sub.n_dirs} direction(s); fp64; {dt:.2f}s"}, ref)
 
@@ -571,6 +571,7 @@ def la_cpu_baseline(cfg, cpu_steps):
     sub, dt, ref = run(Ls)
     return ({"value": round(sub.tok_ch / dt / 1e9, 6), "unit": "Gtok·ch/s", "cores": threads,
              "cpu_model": cpu_model(), "kind": "oracle",
+             "lane_steps_g_per_s": round(sub.tok_ch * sub.d_key / dt / 1e9, 6),
              "sample": f"{cfg.name} first {Ls} steps, all {sub.heads} heads, batch {sub.batch}, "
                        f"{sub.n_dirs} direction(s); fp64; {dt:.2f}s"}, ref)
 

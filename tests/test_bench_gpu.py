@@ -47,6 +47,7 @@ def test_bench_line_fields_and_parity():
     assert rf["peak_unpacked"] == pytest.approx(78.64, abs=0.01) and rf["frac_unpacked"] >= rf["frac"]
     cb = d["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["cores"] >= 1 and cb["value"] > 0 and cb["sample"]
+    assert cb["lane_steps_g_per_s"] == pytest.approx(cb["value"] * N, rel=1e-3, abs=2e-6)
     par = d["parity"]
     assert par["y_rel_l2"] <= 1e-5 and par["dy_rel_l2"] <= 1e-5, par
     assert par["channels"] == D and 0 < par["steps"] <= L
