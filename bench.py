@@ -102,7 +102,7 @@ LA_SRC = "paper_2512_23068_amd/csrc/pgf_la.hip"
 TRAFFIC_SECTIONS = {
     1: ("helpers", "variants", "k_proj", "k_scan", "k_scan_sh", "k_carry", "state in/out", "dispatch"),
     2: ("helpers", "k_proj", "k_scan2", "state in/out", "dispatch"),
-    3: ("helpers", "k_proj", "parameter flows", "state in/out", "dispatch"),
+    3: ("helpers", "variants", "k_proj", "parameter flows", "state in/out", "dispatch"),
 }
 
 
