@@ -43,7 +43,7 @@ def _first_order_case(i):
     return base, cfg, kw, extra
 
 
-@pytest.mark.parametrize("i", range(32))
+@pytest.mark.parametrize("i", range(96))
 def test_random_first_order(i):
     base, cfg, kw, extra = _first_order_case(i)
     print(f"case first order #{i}: {base} {cfg} {kw} {extra}", flush=True)
@@ -68,7 +68,7 @@ def test_random_first_order(i):
         assert e <= gu.TOL, (i, e)
 
 
-@pytest.mark.parametrize("i", range(12))
+@pytest.mark.parametrize("i", range(40))
 def test_random_parameter_flows(i):
     r = np.random.default_rng([4244, i])
     N = int(r.choice([4, 8, 16]))
@@ -99,7 +99,7 @@ def test_random_parameter_flows(i):
         assert gu.rel_l2(gam[k].cpu().numpy(), so[1 + k]) <= gu.TOL, (i, k)
 
 
-@pytest.mark.parametrize("i", range(6))
+@pytest.mark.parametrize("i", range(20))
 def test_random_second_order(i):
     r = np.random.default_rng([4245, i])
     cfg = dict(batch=int(r.integers(1, 4)), seqlen=_length(r, i), d_inner=int(r.integers(1, 301)),
@@ -116,7 +116,7 @@ def test_random_second_order(i):
         assert gu.rel_l2(d2y.cpu().numpy(), yvwo) <= gu.TOL
 
 
-@pytest.mark.parametrize("i", range(8))
+@pytest.mark.parametrize("i", range(24))
 def test_random_linear_attention(i):
     r = np.random.default_rng([4246, i])
     dk = int(r.choice([16, 32, 64]))
