@@ -2254,7 +2254,7 @@ __device__ __forceinline__ void rot(float rev, float &c, float &s) {
 }
 
 template <int NT, int K, bool OUT, typename InT>
-__global__ __launch_bounds__(kThreads) void k_cscan(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(!OUT && K >= 2 ? 2 : 1))) void k_cscan(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A, const float *__restrict__ Aim,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *init, int64_t ibs, int64_t igs, int64_t ics, float *__restrict__ y, float *__restrict__ dy,
