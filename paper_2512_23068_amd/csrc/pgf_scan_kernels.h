@@ -856,9 +856,13 @@ __global__ __launch_bounds__(kThreads) void k_lowdt(
 // entry state at init[b*ibs + g*igs + c*ics + n*D + d] and write y, dy; if
 // end_state is set (sequential evaluation) the exit state is stored there
 // with the same indexing (g = 0).
+// Occupancy: one direction, f32 rows and the Euler drive fit four waves
+// per SIMD; two directions are held to three (a few registers spill outside
+// the step loop), except the ZOH aggregate pass, which spills inside it.
 template <int NT, int NS, int K, bool OUT, typename InT, int VAR = 0>
 __global__ __launch_bounds__(kThreads)
-__attribute__((amdgpu_waves_per_eu(K == 1 && (VAR & kZoh) == 0 && std::is_same<InT, float>::value ? 4 : 1)))
+__attribute__((amdgpu_waves_per_eu(K == 1 && (VAR & kZoh) == 0 && std::is_same<InT, float>::value ? 4
+                                   : (K == 2 && NS == 1 && (OUT || (VAR & kZoh) == 0) ? 3 : 1))))
 void k_scan(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
