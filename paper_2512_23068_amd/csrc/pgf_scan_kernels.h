@@ -1460,11 +1460,13 @@ constexpr auto scan_kernel() {
 // with Abar_v = A Abar dv, Abar_vw = A Abar (A dv dw + dvw) and
 // b_vw = B q + dBv pw + dBw pv,  q = dvw x + dv xw + dw xv,
 // pv = dv x + Delta xv, pw = dw x + Delta xw.  Layouts and grid as k_scan
-// with 4 state components (h, hv, hw, hvw).  The output pass is held to
-// three waves per SIMD (168 VGPRs, no spills; 204 and two waves otherwise);
-// the aggregate pass would spill there.
+// with 4 state components (h, hv, hw, hvw).  The output pass and the
+// aggregate pass over bf16 rows are held to three waves per SIMD (168 and
+// 152 VGPRs, no spills); the f32 aggregate pass spills there (slower) and
+// keeps two.
 template <int NT, bool OUT, typename InT>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(OUT ? 3 : 1))) void k_scan2(
+__global__ __launch_bounds__(kThreads)
+__attribute__((amdgpu_waves_per_eu(OUT || !std::is_same<InT, float>::value ? 3 : 1))) void k_scan2(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *__restrict__ init, int64_t ibs, int64_t igs, int64_t ics,
