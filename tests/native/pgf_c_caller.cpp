@@ -1,12 +1,15 @@
 // A caller of libpgf through its C ABI alone (no Python, no torch): reads a
 // problem from raw float32 files, runs pgf_scan_jvp on a stream of its own
-// and writes y and dy back.  Used by tests/test_c_caller_gpu.py, which writes
-// the inputs and compares the outputs with the fp64 oracle.
+// with a workspace it allocates, then pgf_scan_jvp_noalloc (no workspace) on
+// the same stream, and writes both results back.  Used by
+// tests/test_c_caller_gpu.py, which writes the inputs, compares the outputs
+// with the fp64 oracle and the two calls with each other.
 //
 //   pgf_c_caller DIR
 //   DIR/sizes.txt : B L D N K
 //   DIR/{x,dx,A,w_delta,b_delta,W_B,W_C}.bin : row-major float32 arrays
-//   writes DIR/y.bin [B,L,D] and DIR/dy.bin [K,B,L,D]
+//   writes DIR/y.bin [B,L,D], DIR/dy.bin [K,B,L,D] (pgf_scan_jvp) and
+//   DIR/y_noalloc.bin, DIR/dy_noalloc.bin (pgf_scan_jvp_noalloc)
 #include <hip/hip_runtime_api.h>
 
 #include <cstdio>
@@ -112,6 +115,20 @@ int main(int argc, char **argv) {
     hip_ok(hipMemcpy(hdy.data(), dy, nx * K * sizeof(float), hipMemcpyDeviceToHost), "hipMemcpy D2H");
     write_f32(dir + "/y.bin", hy);
     write_f32(dir + "/dy.bin", hdy);
+
+    // the allocation-free entry point on the same stream, into cleared outputs
+    hip_ok(hipMemsetAsync(y, 0, nx * sizeof(float), st), "hipMemsetAsync");
+    hip_ok(hipMemsetAsync(dy, 0, nx * K * sizeof(float), st), "hipMemsetAsync");
+    p.workspace = nullptr;
+    p.workspace_bytes = 0;
+    rc = pgf_scan_jvp_noalloc(x, dx, &p, y, dy, st);
+    std::printf("pgf_scan_jvp_noalloc: %s\n", pgf_status_string(rc));
+    if (rc != PGF_OK) return 4;
+    hip_ok(hipStreamSynchronize(st), "hipStreamSynchronize");
+    hip_ok(hipMemcpy(hy.data(), y, nx * sizeof(float), hipMemcpyDeviceToHost), "hipMemcpy D2H");
+    hip_ok(hipMemcpy(hdy.data(), dy, nx * K * sizeof(float), hipMemcpyDeviceToHost), "hipMemcpy D2H");
+    write_f32(dir + "/y_noalloc.bin", hy);
+    write_f32(dir + "/dy_noalloc.bin", hdy);
 
     for (void *ptr : {(void *)x, (void *)dx, (void *)A, (void *)w, (void *)b, (void *)WB, (void *)WC, (void *)y,
                       (void *)dy, wsp})

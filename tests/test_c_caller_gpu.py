@@ -1,7 +1,8 @@
 """The library from a plain C++ caller (tests/native/pgf_c_caller.cpp): no
 Python and no torch in the process that calls it, buffers from hipMalloc,
 a stream from hipStreamCreate.  The caller runs as a child process on files
-this test writes; its outputs are compared with the fp64 oracle."""
+this test writes; its outputs are compared with the fp64 oracle, and the
+allocation-free entry point's with pgf_scan_jvp's bit for bit."""
 import os
 import subprocess
 
@@ -36,3 +37,7 @@ def test_plain_c_caller(tmp_path, L, N, K):
     dy = np.fromfile(tmp_path / "dy.bin", dtype=np.float32).reshape(inp["dx"].shape)
     yo, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp)
     gu.assert_close(y, dy, yo, dyo, what=f"C caller L={L} N={N} K={K}")
+    assert "pgf_scan_jvp_noalloc: PGF_OK" in r.stdout
+    y_na = np.fromfile(tmp_path / "y_noalloc.bin", dtype=np.float32).reshape(inp["x"].shape)
+    dy_na = np.fromfile(tmp_path / "dy_noalloc.bin", dtype=np.float32).reshape(inp["dx"].shape)
+    assert np.array_equal(y_na, y) and np.array_equal(dy_na, dy)
