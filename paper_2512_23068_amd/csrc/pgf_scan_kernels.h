@@ -1149,8 +1149,11 @@ void k_scan(
 // leaves h and dh_k exactly unchanged; only their output stores are
 // skipped.  With no early exit the loop keeps the state in place (an exit
 // inside the loop made the compiler copy the state on every step).
+// The output pass with one or two directions, or four in pairs of threads,
+// is held to three waves per SIMD (168 VGPRs; N = 64 at pulse128k sizes
+// 5.16 -> 4.13 ms per pass); wider ones spill there and keep two.
 template <int NT, int NS, int K, bool OUT, typename InT>
-__global__ __launch_bounds__(kThreads) void k_scan_sh(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(OUT && (K <= 2 || (K == 4 && NS == 2)) ? 3 : 1))) void k_scan_sh(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *__restrict__ init, int64_t ibs, int64_t igs, int64_t ics,
