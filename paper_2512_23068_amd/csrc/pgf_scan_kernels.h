@@ -2220,6 +2220,9 @@ static __global__ __launch_bounds__(kThreads) void k_gout(
 //   s = Abar h,  h' = s + B u,  g = A s,
 //   dh'_k = Abar dh_k + g dDelta_k + (B p_k + dB_k u)     (drive real)
 //   y = sum_n C Re(h'),  dy_k = sum_n dC_k Re(h') + C Re(dh'_k)
+// and, with MAP (output pass only), the output map of Sec. 3 on that real
+// read-out as in k_scan: y = act(yhat + D_res x), dy_k = act'(yhat + D_res
+// x) (dyhat_k + D_res dx_k).
 // The angle is reduced in revolutions and its sine and cosine evaluated to
 // about one ulp (rot); the hardware sine and cosine were not accurate enough
 // for long sequences.  Layouts as k_scan with the state split into planes:
@@ -2262,13 +2265,14 @@ __device__ __forceinline__ void rot(float rev, float &c, float &s) {
     c = sg * cp;
 }
 
-template <int NT, int K, bool OUT, typename InT>
+template <int NT, int K, bool OUT, typename InT, bool MAP = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(!OUT && K >= 2 ? 2 : 1))) void k_cscan(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A, const float *__restrict__ Aim,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *init, int64_t ibs, int64_t igs, int64_t ics, float *__restrict__ y, float *__restrict__ dy,
     float *end_state, float *__restrict__ agg_h, float *__restrict__ agg_s, int64_t Bsz, int64_t L, int64_t D,
-    int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
+    int64_t t0, int64_t len, int64_t Tc, int64_t S, int G, const float *__restrict__ D_res, int act) {
+    static_assert(OUT || !MAP, "the aggregate pass writes no outputs");
     constexpr int N = NT;
     constexpr int R = 2 * N * (1 + K);
     constexpr int TT = 8;
@@ -2293,6 +2297,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(!OUT &
         Ar2[i] = Ai[i] * kInv2Pi;
     }
     const float w = w_delta[d], bd = b_delta[d];
+    float Dr = 0.0f;
+    if constexpr (MAP) Dr = D_res ? D_res[d] : 0.0f;
 
     float hr[NT], hi[NT], dr[K][NT], di[K][NT];
     if constexpr (OUT) {
@@ -2403,6 +2409,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(!OUT &
                     }
                 }
                 if constexpr (OUT) {
+                    if constexpr (MAP) {
+                        yv = fmaf(Dr, xv, yv);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) dyv[k] = fmaf(Dr, dxc[k][j], dyv[k]);
+                        if (act == PGF_ACT_SILU) {
+                            float f, df;
+                            silu_and_slope(yv, f, df);
+                            yv = f;
+#pragma unroll
+                            for (int k = 0; k < K; ++k) dyv[k] *= df;
+                        }
+                    }
                     if (active) {
                         store_out(Yb, (uint32_t)t * Du + du, yv);
 #pragma unroll
@@ -2807,12 +2825,14 @@ struct Launcher {
         const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
         const int64_t ND = q.N * q.D;
         constexpr int CP = 2 * (1 + K);
+        // the output pass with the output map when the call asks for one
+        auto kout = (q.var & 2) ? &k_cscan<NT, K, true, InT, true> : &k_cscan<NT, K, true, InT, false>;
         if (q.seg == 0) {
             Timed tm(3, st, !q.noalloc);
-            hipLaunchKernelGGL((k_cscan<NT, K, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, dx,
+            hipLaunchKernelGGL(kout, dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, dx,
                                p.A, p.A_im, p.w_delta, p.b_delta, bcw(), (const float *)state(), ND, (int64_t)0,
                                q.B * ND, y, dy, state(), (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len,
-                               q.chunk_len, len, 1);
+                               q.chunk_len, len, 1, p.D_res, p.activation);
             return;
         }
         const int G = (int)((len + q.seg - 1) / q.seg);
@@ -2821,7 +2841,7 @@ struct Launcher {
             hipLaunchKernelGGL((k_cscan<NT, K, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0,
                                st, x, dx, p.A, p.A_im, p.w_delta, p.b_delta, bcw(), (const float *)nullptr,
                                (int64_t)0, (int64_t)0, (int64_t)0, y, dy, (float *)nullptr, agg_h(), agg_s(), q.B,
-                               q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+                               q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G, (const float *)nullptr, 0);
         }
         {
             const int64_t lanes = q.B * ND;
@@ -2831,10 +2851,11 @@ struct Launcher {
         }
         {
             Timed tm(3, st, !q.noalloc);
-            hipLaunchKernelGGL((k_cscan<NT, K, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0,
+            hipLaunchKernelGGL(kout, dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0,
                                st, x, dx, p.A, p.A_im, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(),
                                (int64_t)G * CP * ND, (int64_t)CP * ND, ND, y, dy, (float *)nullptr, (float *)nullptr,
-                               (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G);
+                               (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G, p.D_res,
+                               p.activation);
         }
     }
 

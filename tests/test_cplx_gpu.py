@@ -89,3 +89,39 @@ def test_cplx_limits():
     inp = _with_im(gu.custom("tiny", seqlen=64))
     with pytest.raises(RuntimeError, match="UNSUPPORTED"):
         gu.run(inp, drive="zoh")
+
+
+def _with_dres(inp, seed=11):
+    inp["D_res"] = np.random.default_rng(seed).standard_normal(inp["x"].shape[-1]).astype(np.float32)
+    return inp
+
+
+def _check_map(inp, what, act, **kw):
+    print(f"case {what}", flush=True)
+    y, dy = gu.run(inp, act=act, **kw)
+    yo, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp, act=act)
+    gu.assert_close(y.cpu().numpy(), dy.cpu().numpy(), yo, dyo, what=what)
+
+
+@pytest.mark.parametrize("K,seg,act", [(1, 0, "silu"), (2, 0, "silu"), (2, -1, "silu"), (1, 64, "identity")])
+def test_cplx_with_output_map(K, seg, act):
+    """Sec. 3's general output map on the complex state, y = act(Re(C h) +
+    D_res x), with its tangent."""
+    inp = _with_dres(_with_im(gu.custom("mamba130m", batch=2, seqlen=1100, d_inner=70, n_dirs=K)))
+    _check_map(inp, f"complex + output map K={K} seg={seg} act={act}", act, seg_len=seg)
+
+
+def test_cplx_with_output_map_s4dlin_stiff_and_blocks():
+    _check_map(_with_dres(_with_im(gu.custom("mamba130m", seqlen=3000, d_inner=64), "s4dlin")),
+               "complex s4d-lin + silu + D_res", "silu")
+    _check_map(_with_dres(_with_im(gu.custom("stiff128k", seqlen=1500, d_inner=64))),
+               "complex stiff bf16 + silu + D_res", "silu")
+    inp = _with_dres(_with_im(gu.custom("mamba130m", batch=2, seqlen=1000, d_inner=48, n_dirs=2)))
+    ref = gu.run(inp, act="silu", seg_len=64, chunk_segs=1, return_state=True)
+    for cs in (3, 0):
+        got = gu.run(inp, act="silu", seg_len=64, chunk_segs=cs, return_state=True)
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), cs
+    # the map leaves the state untouched: the same exit state as without it
+    plain = gu.run({k: v for k, v in inp.items() if k != "D_res"}, seg_len=64, return_state=True)
+    assert torch.equal(plain[2], ref[2]) and torch.equal(plain[3], ref[3])

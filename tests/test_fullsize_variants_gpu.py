@@ -37,6 +37,7 @@ VARIANTS = {
     "zoh": (dict(), dict(drive="zoh")),
     "silu_dres": (dict(dres=True), dict(act="silu")),
     "s4dlin": (dict(complex_a=True), dict()),
+    "s4dlin_silu_dres": (dict(complex_a=True, dres=True), dict(act="silu")),
     "groups4": (dict(groups=4), dict()),
     "lowrank48": (dict(lowrank=48), dict()),
 }

@@ -40,6 +40,8 @@ def _first_order_case(i):
             extra = dict(lowrank=int(r.integers(1, 65)))
         elif v == 3:
             extra = dict(complex=True)
+            if r.integers(0, 2):
+                extra.update(act="silu", dres=True)
     return base, cfg, kw, extra
 
 
