@@ -74,7 +74,7 @@ def declare(lib):
     lib.pgf_oracle_la.restype = ctypes.c_int
     lib.pgf_oracle_la.argtypes = [i64] * 6 + [dp] * 12 + [ctypes.c_int]
     lib.pgf_oracle_core_cplx.restype = ctypes.c_int
-    lib.pgf_oracle_core_cplx.argtypes = [i64] * 5 + [dp] * 16 + [ctypes.c_int]
+    lib.pgf_oracle_core_cplx.argtypes = [i64] * 5 + [dp] * 16 + [ctypes.c_int, ctypes.c_int]
     return lib
 
 
@@ -169,11 +169,11 @@ def project(x, dx, W_B, W_C, b_B=None, b_C=None):
     return Bm, Cm, dx @ WB, dx @ WC
 
 
-def core_cplx(A, Aim, x, dx, delta, ddelta, Bm, Cm, dBm, dCm, h=None, dh=None, nthreads=None):
+def core_cplx(A, Aim, x, dx, delta, ddelta, Bm, Cm, dBm, dCm, h=None, dh=None, nthreads=None, drive="euler"):
     """The recurrence with a complex diagonal transition A + i*Aim (see
-    pgf_oracle_core_cplx).  h [B,D,N] and dh [K,B,D,N] are complex (zero
-    when None).  Returns (y, dy, h_out, dh_out); y and dy are the real
-    read-out sum_n C Re(h)."""
+    pgf_oracle_core_cplx), Euler or zero-order-hold drive.  h [B,D,N] and
+    dh [K,B,D,N] are complex (zero when None).  Returns (y, dy, h_out,
+    dh_out); y and dy are the real read-out sum_n C Re(h)."""
     lib = _load()
     A, Aim = _f64(A), _f64(Aim)
     x, dx, delta, ddelta = _f64(x), _f64(dx), _f64(delta), _f64(ddelta)
@@ -187,7 +187,7 @@ def core_cplx(A, Aim, x, dx, delta, ddelta, Bm, Cm, dBm, dCm, h=None, dh=None, n
     dy = np.empty((K, B, L, D))
     rc = lib.pgf_oracle_core_cplx(B, L, D, N, K, _dp(A), _dp(Aim), _dp(x), _dp(dx), _dp(delta), _dp(ddelta),
                                   _dp(Bm), _dp(Cm), _dp(dBm), _dp(dCm), *[_dp(p) for p in parts], _dp(y), _dp(dy),
-                                  _threads() if nthreads is None else nthreads)
+                                  DRIVES[drive], _threads() if nthreads is None else nthreads)
     if rc != 0:
         raise RuntimeError("pgf_oracle_core_cplx failed")
     return y, dy, parts[0] + 1j * parts[1], parts[2] + 1j * parts[3]
@@ -269,8 +269,6 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
     h = np.array(h, copy=True)
     dh = np.array(dh, copy=True)
     if cplx:
-        if drive != "euler":
-            raise ValueError("the complex transition takes the Euler drive")
         Ais = _f64(params["A_im"])[sel]
         h = np.asarray(h, complex)
         dh = np.asarray(dh, complex)
@@ -300,7 +298,7 @@ def scan_jvp(x, dx, params, h_in=None, dh_in=None, channels=None, chunk=None, nt
             args = (As[m], xs[..., m], dxs[..., m], delta[..., m], ddelta[..., m], Bm[..., cols], Cm[..., cols],
                     dBm[..., cols], dCm[..., cols], h[:, m], dh[:, :, m], nthreads)
             if cplx:
-                yg, dyg, hg, dhg = core_cplx(args[0], Ais[m], *args[1:])
+                yg, dyg, hg, dhg = core_cplx(args[0], Ais[m], *args[1:], drive=drive)
             else:
                 yg, dyg, hg, dhg = core(*args, drive)
             yc[..., m], dyc[..., m] = yg, dyg

@@ -449,13 +449,16 @@ int pgf_oracle_la(int64_t B, int64_t H, int64_t L, int64_t DK, int64_t DV, int64
 /*
  * Complex diagonal transition (Sec. 3: the state lives in C^{D x N}; the
  * read-out takes the real part, y = Re(C h)).  A = A_re + i A_im per lane;
- * B, C and Delta are real as in pgf_oracle_core (Euler drive).  The tangent
- * is the derivative along the real input direction, so it obeys the same
- * complex recurrence as the state:
+ * B, C and Delta are real as in pgf_oracle_core.  The drive coefficient is
+ * e = Delta (Euler, drive = 0) or e = (exp(Delta*A) - 1)/A (zero-order
+ * hold, drive = 1; complex, = Delta at A = 0), whose derivative in Delta is
+ * Abar (1 for the Euler drive).  The tangent is the derivative along the
+ * real input direction, so it obeys the same complex recurrence as the
+ * state:
  *
  *   Abar  = exp(Delta*A)                           (complex)
- *   h'    = Abar*h + Delta*B*x
- *   dh'_k = Abar*dh_k + Abar*A*dDelta_k*h + dDelta_k*B*x + Delta*dB_k*x + Delta*B*dx_k
+ *   h'    = Abar*h + e*B*x
+ *   dh'_k = Abar*dh_k + Abar*A*dDelta_k*h + (de/dDelta)*dDelta_k*B*x + e*dB_k*x + e*B*dx_k
  *   y     = sum_n C*Re(h'),   dy_k = sum_n dC_k*Re(h') + C*Re(dh'_k)
  *
  * Shapes as pgf_oracle_core plus Aim [D,N]; the state is split into real
@@ -464,14 +467,24 @@ int pgf_oracle_la(int64_t B, int64_t H, int64_t L, int64_t DK, int64_t DV, int64
  */
 #include <complex.h>
 
+/* exp(z) - 1 for complex z without cancellation near 0: with z = u + i v,
+ * exp(z) - 1 = (expm1(u) cos v - 2 sin^2(v/2)) + i exp(u) sin v. */
+static double complex cexpm1_(double complex z)
+{
+    const double u = creal(z), v = cimag(z);
+    const double sh = sin(0.5 * v);
+    return (expm1(u) * cos(v) - 2.0 * sh * sh) + I * (exp(u) * sin(v));
+}
+
 int pgf_oracle_core_cplx(int64_t B, int64_t L, int64_t D, int64_t N, int64_t K,
                          const double *A, const double *Aim, const double *x, const double *dx,
                          const double *delta, const double *ddelta,
                          const double *Bm, const double *Cm, const double *dBm, const double *dCm,
                          double *h_re, double *h_im, double *dh_re, double *dh_im,
-                         double *y, double *dy, int nthreads)
+                         double *y, double *dy, int drive, int nthreads)
 {
     if (B < 0 || L < 0 || D < 0 || N <= 0 || K <= 0) return -1;
+    if (drive != 0 && drive != 1) return -1;
     if (!A || !Aim || !h_re || !h_im || !dh_re || !dh_im) return -1;
     if (L > 0 && (!x || !dx || !delta || !ddelta || !Bm || !Cm || !dBm || !dCm || !y || !dy)) return -1;
     const int64_t lanes = B * D;
@@ -494,16 +507,18 @@ int pgf_oracle_core_cplx(int64_t B, int64_t L, int64_t D, int64_t N, int64_t K,
                 const int64_t i = (b * D + d) * N + n;
                 const double complex a = A[d * N + n] + I * Aim[d * N + n];
                 const double complex abar = cexp(dl * a);
+                const double complex ec = drive ? (a != 0.0 ? cexpm1_(dl * a) / a : (double complex)dl) : dl;
+                const double complex de = drive ? abar : 1.0;   /* de/dDelta */
                 const double complex hprev = h_re[i] + I * h_im[i];
-                const double complex hnew = abar * hprev + dl * Bm[btn + n] * xt;
+                const double complex hnew = abar * hprev + ec * Bm[btn + n] * xt;
                 for (int64_t kk = 0; kk < K; ++kk) {
                     const int64_t kbtd = ((kk * B + b) * L + t) * D + d;
                     const int64_t kbtn = ((kk * B + b) * L + t) * N + n;
                     const int64_t ki = ((kk * B + b) * D + d) * N + n;
                     const double ddl = ddelta[kbtd], dxt = dx[kbtd];
                     const double complex dhprev = dh_re[ki] + I * dh_im[ki];
-                    const double complex dhnew = abar * dhprev + abar * a * ddl * hprev + ddl * Bm[btn + n] * xt +
-                                                 dl * dBm[kbtn] * xt + dl * Bm[btn + n] * dxt;
+                    const double complex dhnew = abar * dhprev + abar * a * ddl * hprev + de * ddl * Bm[btn + n] * xt +
+                                                 ec * dBm[kbtn] * xt + ec * Bm[btn + n] * dxt;
                     dh_re[ki] = creal(dhnew);
                     dh_im[ki] = cimag(dhnew);
                     dy[kbtd] += dCm[kbtn] * creal(hnew) + Cm[btn + n] * creal(dhnew);

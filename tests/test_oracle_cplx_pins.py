@@ -2,7 +2,9 @@
 y = Re(C h)) against the real oracle at A_im = 0, the closed-form impulse
 response of a damped oscillator, forward-mode autograd of an independent
 complex torch loop, central differences, conjugation symmetry and the
-segment composition; planted mistakes are caught."""
+segment composition; with the zero-order-hold drive, the real ZOH oracle
+at A_im = 0, the exact solution of the oscillator ODE for a held input,
+autograd and central differences; planted mistakes are caught."""
 import ctypes
 import os
 import subprocess
@@ -48,7 +50,7 @@ def test_damped_oscillator_impulse_response():
     assert relerr(y[0], ref) < 1e-13
 
 
-def _torch_model(p, xt):
+def _torch_model(p, xt, drive="euler"):
     f64 = dict(dtype=torch.float64)
     z = xt * torch.tensor(p["w_delta"], **f64) + torch.tensor(p["b_delta"], **f64)
     delta = torch.logaddexp(z, torch.zeros((), **f64))
@@ -60,7 +62,8 @@ def _torch_model(p, xt):
     ys = []
     for t in range(L):
         dl = delta[:, t, :, None]
-        h = torch.exp(dl * A) * h + dl * Bm[:, t, None, :] * xt[:, t, :, None]
+        e = dl if drive == "euler" else torch.expm1(dl * A) / A   # ZOH: (exp(dl A) - 1) / A
+        h = torch.exp(dl * A) * h + e * Bm[:, t, None, :] * xt[:, t, :, None]
         ys.append((h.real * Cm[:, t, None, :]).sum(-1))
     return torch.stack(ys, 1)
 
@@ -74,6 +77,49 @@ def test_forward_mode_autograd(stiff):
     for k in range(dx.shape[0]):
         _, jv = torch.func.jvp(f, (torch.tensor(x),), (torch.tensor(dx[k]),))
         assert relerr(dy[k], jv.numpy()) < 1e-11, k
+
+
+@pytest.mark.parametrize("stiff", [False, True])
+def test_zoh_forward_mode_autograd(stiff):
+    p, x, dx = problem(92 + stiff, stiff=stiff)
+    y, dy, _, _ = oracle.scan_jvp(x, dx, p, drive="zoh")
+    f = lambda xt: _torch_model(p, xt, "zoh")
+    assert relerr(y, f(torch.tensor(x)).numpy()) < 1e-12
+    for k in range(dx.shape[0]):
+        _, jv = torch.func.jvp(f, (torch.tensor(x),), (torch.tensor(dx[k]),))
+        assert relerr(dy[k], jv.numpy()) < 1e-11, k
+
+
+def test_zoh_real_limit_and_central_differences():
+    p, x, dx = problem(94, L=20, K=1)
+    a = oracle.scan_jvp(x, dx, dict(p, A_im=np.zeros_like(p["A"])), drive="zoh")
+    b = oracle.scan_jvp(x, dx, {k: v for k, v in p.items() if k != "A_im"}, drive="zoh")
+    for u, w in zip(a, b):
+        assert relerr(np.real(u), w) < 1e-14 and np.abs(np.imag(u)).max() == 0
+    _, dy, _, _ = oracle.scan_jvp(x, dx, p, drive="zoh")
+    eps = 1e-6
+    yp, _, _, _ = oracle.scan_jvp(x + eps * dx[0], dx, p, drive="zoh")
+    ym, _, _, _ = oracle.scan_jvp(x - eps * dx[0], dx, p, drive="zoh")
+    assert relerr(dy[0], (yp - ym) / (2 * eps)) < 1e-8
+
+
+def test_zoh_is_exact_for_a_held_oscillator_input():
+    """Constant Delta, B, C and a constant input c: zero-order hold gives the
+    exact solution of the damped oscillator dh/ds = A h + B c (A complex) at
+    s = t*Delta, h(s) = (exp(A s) - 1) / A * B c, for every step count t."""
+    g = np.random.default_rng(95)
+    D, N, L = 3, 5, 30
+    p = dict(A=-g.uniform(0.05, 2, (D, N)), A_im=g.uniform(-6, 6, (D, N)), w_delta=np.zeros(D),
+             b_delta=g.uniform(-2, 1, D), W_B=np.zeros((D, N)), W_C=np.zeros((D, N)),
+             b_B=g.standard_normal(N), b_C=g.standard_normal(N))
+    c = g.standard_normal(D)
+    x = np.broadcast_to(c, (1, L, D)).copy()
+    y, _, _, _ = oracle.scan_jvp(x, np.zeros((1, 1, L, D)), p, drive="zoh")
+    dl = np.log1p(np.exp(p["b_delta"]))
+    A = (p["A"] + 1j * p["A_im"])[None]
+    t = np.arange(1, L + 1)[:, None, None]
+    h = np.expm1(A * t * dl[None, :, None]) / A * p["b_B"] * c[None, :, None]
+    assert relerr(y[0], (h.real * p["b_C"]).sum(-1)) < 1e-12
 
 
 def test_central_differences():
@@ -114,7 +160,8 @@ def test_segment_composition_closed_forms():
 
 
 PIN_TESTS = [test_damped_oscillator_impulse_response, lambda: test_forward_mode_autograd(False),
-             test_segment_composition_closed_forms]
+             test_segment_composition_closed_forms, lambda: test_zoh_forward_mode_autograd(False),
+             test_zoh_is_exact_for_a_held_oscillator_input]
 
 C_MUTANTS = {
     "imaginary part dropped from exp": ("const double complex abar = cexp(dl * a);",
@@ -124,6 +171,10 @@ C_MUTANTS = {
     "read-out of Im(h)": ("yt += Cm[btn + n] * creal(hnew);", "yt += Cm[btn + n] * cimag(hnew);"),
     "tangent read-out drops C*Re(dh)": ("dy[kbtd] += dCm[kbtn] * creal(hnew) + Cm[btn + n] * creal(dhnew);",
                                         "dy[kbtd] += dCm[kbtn] * creal(hnew);"),
+    "ZOH coefficient from the real part of A": ("cexpm1_(dl * a) / a", "cexpm1_(dl * creal(a)) / creal(a)"),
+    "ZOH coefficient without the sin^2 term": ("(expm1(u) * cos(v) - 2.0 * sh * sh)", "(expm1(u) * cos(v))"),
+    "ZOH tangent drive without Abar": ("const double complex de = drive ? abar : 1.0;",
+                                       "const double complex de = 1.0;"),
 }
 
 
