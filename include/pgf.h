@@ -142,8 +142,9 @@ typedef struct pgf_params {
      * the output is y = sum_n C Re(h) and dy_k = sum_n dC_k Re(h) + C Re(dh_k),
      * and with the output map above y = act(sum_n C Re(h) + D_res x) (Sec.
      * 3's general form); h_in/h_out are [B,D,N] and dh_in/dh_out [K,B,D,N]
-     * complex (interleaved real, imaginary f32).  First order only, Euler
-     * drive, N <= 16, K <= 2. */
+     * complex (interleaved real, imaginary f32).  Either drive: with the
+     * zero-order hold the drive coefficient is the complex (Abar - 1) / A.
+     * First order only, N <= 16, K <= 2. */
     const float *A_im;
     /* Channel groups with their own B and C (Mamba-style grouped
      * projections), 0 or 1 = one group.  With G > 1 groups, W_B and W_C are

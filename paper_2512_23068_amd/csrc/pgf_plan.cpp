@@ -82,9 +82,9 @@ int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
     if (var && order == 2) return PGF_ERR_UNSUPPORTED;
     if (var && ((order != 3 && K > 2) || N > 16)) return PGF_ERR_UNSUPPORTED;
     const int cplx = p->A_im ? 1 : 0;
-    // the complex transition takes the Euler drive; the output map is applied
+    // the complex transition takes either drive; the output map is applied
     // to its real read-out
-    if (cplx && (order != 1 || (var & 1) || K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
+    if (cplx && (order != 1 || K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
     if (p->n_groups < 0) return PGF_ERR_INVALID_ARG;
     const int64_t groups = p->n_groups > 1 ? p->n_groups : 1;
     if (groups > 1) {

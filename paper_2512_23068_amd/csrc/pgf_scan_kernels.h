@@ -2214,11 +2214,14 @@ static __global__ __launch_bounds__(kThreads) void k_gout(
 
 // ---------------------------------------------------------------- complex
 // Complex diagonal transition A = A_re + i A_im (Sec. 3: state in C^{DxN},
-// read-out y = sum_n C Re(h)), Euler drive, one thread per channel with all
-// NT = N lanes.  Per lane and step, with Abar = exp(Delta A_re) (cos th +
-// i sin th), th = Delta A_im:
+// read-out y = sum_n C Re(h)), one thread per channel with all NT = N lanes.
+// Per lane and step, with Abar = exp(Delta A_re) (cos th + i sin th),
+// th = Delta A_im:
 //   s = Abar h,  h' = s + B u,  g = A s,
-//   dh'_k = Abar dh_k + g dDelta_k + (B p_k + dB_k u)     (drive real)
+//   dh'_k = Abar dh_k + g dDelta_k + (B p_k + dB_k u)     (Euler: drive real)
+// or with ZOH the complex drive coefficient e = (Abar - 1)/A (zoh_coef_c):
+//   h' = s + e B x,  dh'_k = Abar dh_k + (g + Abar B x) dDelta_k + e (dB_k x + B dx_k)
+// and in both cases
 //   y = sum_n C Re(h'),  dy_k = sum_n dC_k Re(h') + C Re(dh'_k)
 // and, with MAP (output pass only), the output map of Sec. 3 on that real
 // read-out as in k_scan: y = act(yhat + D_res x), dy_k = act'(yhat + D_res
@@ -2265,8 +2268,31 @@ __device__ __forceinline__ void rot(float rev, float &c, float &s) {
     c = sg * cp;
 }
 
-template <int NT, int K, bool OUT, typename InT, bool MAP = false>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(!OUT && K >= 2 ? 2 : 1))) void k_cscan(
+// The ZOH drive coefficient of a complex lane, e = (Abar - 1)/A = Delta
+// phi(z), z = Delta*A, Abar = exp(z) = abr + i abi as computed by the caller:
+// for |z| < 1/16 the series phi(z) = sum_k z^k/(k+1)! to z^4 (first omitted
+// term below 2e-9 relative), otherwise Delta (Abar - 1) / z, where the
+// subtraction loses at most 4 bits.  z = 0 takes the series (e = Delta).
+__device__ __forceinline__ void zoh_coef_c(float delta, float a_re, float a_im, float abr, float abi, float &er,
+                                           float &ei) {
+    const float zr = delta * a_re, zi = delta * a_im;
+    const float m2 = fmaf(zr, zr, zi * zi);
+    float pr = fmaf(zr, 1.0f / 120.0f, 1.0f / 24.0f), pi = zi * (1.0f / 120.0f);
+    float qr = fmaf(pr, zr, fmaf(-pi, zi, 1.0f / 6.0f)), qi = fmaf(pr, zi, pi * zr);
+    pr = fmaf(qr, zr, fmaf(-qi, zi, 0.5f));
+    pi = fmaf(qr, zi, qi * zr);
+    qr = fmaf(pr, zr, fmaf(-pi, zi, 1.0f));
+    qi = fmaf(pr, zi, pi * zr);
+    const float ur = abr - 1.0f;
+    const float sc = delta * __builtin_amdgcn_rcpf(m2);
+    const float lr = fmaf(ur, zr, abi * zi) * sc, li = fmaf(abi, zr, -ur * zi) * sc;
+    const bool small = m2 < 1.0f / 256.0f;
+    er = small ? delta * qr : lr;
+    ei = small ? delta * qi : li;
+}
+
+template <int NT, int K, bool OUT, typename InT, bool MAP = false, bool ZOH = false>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(!OUT && (K >= 2 || ZOH) ? 2 : 1))) void k_cscan(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A, const float *__restrict__ Aim,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *init, int64_t ibs, int64_t igs, int64_t ics, float *__restrict__ y, float *__restrict__ dy,
@@ -2387,17 +2413,39 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(!OUT &
                     const float si = fmaf(ar, hi[i], ai * hr[i]);
                     const float gr = fmaf(Ar[i], sr, -Ai[i] * si);
                     const float gi = fmaf(Ar[i], si, Ai[i] * sr);
-                    const float hrn = fmaf(Bn, u, sr);
+                    float hrn;
+                    if constexpr (ZOH) {
+                        // b = e B x (e complex), db_k = Abar dDelta_k B x + e (dB_k x + B dx_k);
+                        // with the transition's term g dDelta_k the dDelta_k terms
+                        // share the factor Abar B x + g.
+                        float ecr, eci;
+                        zoh_coef_c(delta, Ar[i], Ai[i], ar, ai, ecr, eci);
+                        const float Bx = Bn * xv;
+                        hrn = fmaf(ecr, Bx, sr);
+                        const float rr = fmaf(ar, Bx, gr), ri = fmaf(ai, Bx, gi);
 #pragma unroll
-                    for (int k = 0; k < K; ++k) {
-                        const float dBn = rec[(1 + k) * N + i];
-                        const float tr = fmaf(ar, dr[k][i], -ai * di[k][i]);
-                        const float ti = fmaf(ar, di[k][i], ai * dr[k][i]);
-                        dr[k][i] = fmaf(gr, dD[k], tr) + fmaf(Bn, pk[k], dBn * u);
-                        di[k][i] = fmaf(gi, dD[k], ti);
+                        for (int k = 0; k < K; ++k) {
+                            const float dBn = rec[(1 + k) * N + i];
+                            const float tr = fmaf(ar, dr[k][i], -ai * di[k][i]);
+                            const float ti = fmaf(ar, di[k][i], ai * dr[k][i]);
+                            const float jk = fmaf(dBn, xv, Bn * dxc[k][j]);
+                            dr[k][i] = fmaf(rr, dD[k], fmaf(ecr, jk, tr));
+                            di[k][i] = fmaf(ri, dD[k], fmaf(eci, jk, ti));
+                        }
+                        hi[i] = fmaf(eci, Bx, si);
+                    } else {
+                        hrn = fmaf(Bn, u, sr);
+#pragma unroll
+                        for (int k = 0; k < K; ++k) {
+                            const float dBn = rec[(1 + k) * N + i];
+                            const float tr = fmaf(ar, dr[k][i], -ai * di[k][i]);
+                            const float ti = fmaf(ar, di[k][i], ai * dr[k][i]);
+                            dr[k][i] = fmaf(gr, dD[k], tr) + fmaf(Bn, pk[k], dBn * u);
+                            di[k][i] = fmaf(gi, dD[k], ti);
+                        }
+                        hi[i] = si;
                     }
                     hr[i] = hrn;
-                    hi[i] = si;
                     if constexpr (OUT) {
                         const float Cn = rec[(1 + K) * N + i];
                         yv = fmaf(Cn, hrn, yv);
@@ -2825,8 +2873,12 @@ struct Launcher {
         const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
         const int64_t ND = q.N * q.D;
         constexpr int CP = 2 * (1 + K);
-        // the output pass with the output map when the call asks for one
-        auto kout = (q.var & 2) ? &k_cscan<NT, K, true, InT, true> : &k_cscan<NT, K, true, InT, false>;
+        // the passes of the call's drive, the output pass with its output map
+        auto kout = (q.var & 1) ? ((q.var & 2) ? &k_cscan<NT, K, true, InT, true, true>
+                                               : &k_cscan<NT, K, true, InT, false, true>)
+                                : ((q.var & 2) ? &k_cscan<NT, K, true, InT, true, false>
+                                               : &k_cscan<NT, K, true, InT, false, false>);
+        auto kagg = (q.var & 1) ? &k_cscan<NT, K, false, InT, false, true> : &k_cscan<NT, K, false, InT, false, false>;
         if (q.seg == 0) {
             Timed tm(3, st, !q.noalloc);
             hipLaunchKernelGGL(kout, dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, dx,
@@ -2838,7 +2890,7 @@ struct Launcher {
         const int G = (int)((len + q.seg - 1) / q.seg);
         {
             Timed tm(1, st, !q.noalloc);
-            hipLaunchKernelGGL((k_cscan<NT, K, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0,
+            hipLaunchKernelGGL(kagg, dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0,
                                st, x, dx, p.A, p.A_im, p.w_delta, p.b_delta, bcw(), (const float *)nullptr,
                                (int64_t)0, (int64_t)0, (int64_t)0, y, dy, (float *)nullptr, agg_h(), agg_s(), q.B,
                                q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G, (const float *)nullptr, 0);

@@ -226,16 +226,17 @@ def test_complex_transition_plans():
     p.A_im = 1 << 30                      # any non-NULL pointer selects the complex state
     cplx = binding.lib().pgf_workspace_bytes(ctypes.byref(p))
     assert cplx > base
-    for kw in (dict(n_dirs=4), dict(order=2, n_dirs=2), dict(drive=1), dict(d_state=32)):
+    for kw in (dict(n_dirs=4), dict(order=2, n_dirs=2), dict(d_state=32)):
         q = binding.make_params(1, 1000, 64, 16, 1)
         q.A_im = 1 << 30
         for k, v in kw.items():
             setattr(q, k, v)
         assert binding.lib().pgf_workspace_bytes(ctypes.byref(q)) == 0, kw
-    # the output map applies to the real read-out
-    q = binding.make_params(1, 1000, 64, 16, 2, act="silu")
-    q.A_im = 1 << 30
-    assert binding.lib().pgf_workspace_bytes(ctypes.byref(q)) > 0
+    # either drive, and the output map on the real read-out
+    for kw in (dict(act="silu"), dict(drive="zoh"), dict(drive="zoh", act="silu")):
+        q = binding.make_params(1, 1000, 64, 16, 2, **kw)
+        q.A_im = 1 << 30
+        assert binding.lib().pgf_workspace_bytes(ctypes.byref(q)) > 0, kw
 
 
 def test_group_plans():
@@ -335,7 +336,8 @@ def test_support_matrix_has_kernels():
                     assert p["n_per_thread"] * p["n_split"] == N
                     # follow-on paths: one thread per channel, N <= 16, K <= 2
                     for kw in (dict(order=2), dict(order=3), dict(drive="zoh"), dict(act="silu"),
-                               dict(complex_a=True), dict(complex_a=True, act="silu"), dict(groups=4),
+                               dict(complex_a=True), dict(complex_a=True, act="silu"),
+                               dict(complex_a=True, drive="zoh"), dict(groups=4),
                                dict(dt_rank=48), dict(order=3, drive="zoh"),
                                dict(order=3, act="silu"), dict(order=3, drive="zoh", act="silu")):
                         if kw.get("order") == 2 and K != 2:

@@ -2,7 +2,8 @@
 the GPU against the fp64 oracle: several state sizes, one and two
 directions, the segmented and sequential evaluations, an S4D-Lin style
 spectrum and a stiff bf16 case; the real limit; bit-identical results for
-every host block size and split calls chained through the complex state."""
+every host block size and split calls chained through the complex state;
+the output map on the real read-out and the zero-order-hold drive."""
 import numpy as np
 import pytest
 import torch
@@ -86,7 +87,7 @@ def test_cplx_limits():
     inp = _with_im(gu.custom("tiny", seqlen=64, n_dirs=4))
     with pytest.raises(RuntimeError, match="UNSUPPORTED"):
         gu.run(inp)
-    inp = _with_im(gu.custom("tiny", seqlen=64))
+    inp = _with_im(gu.custom("tiny", seqlen=64, d_state=32))
     with pytest.raises(RuntimeError, match="UNSUPPORTED"):
         gu.run(inp, drive="zoh")
 
@@ -125,3 +126,36 @@ def test_cplx_with_output_map_s4dlin_stiff_and_blocks():
     # the map leaves the state untouched: the same exit state as without it
     plain = gu.run({k: v for k, v in inp.items() if k != "D_res"}, seg_len=64, return_state=True)
     assert torch.equal(plain[2], ref[2]) and torch.equal(plain[3], ref[3])
+
+
+@pytest.mark.parametrize("N,K,seg", [(16, 1, 0), (16, 2, 0), (8, 1, -1), (4, 2, 64), (16, 1, -1)])
+def test_cplx_zoh_parity(N, K, seg):
+    """The zero-order-hold drive with the complex transition (S4D's
+    discretisation): e = (exp(Delta A) - 1)/A complex, both branches of its
+    evaluation (small and large |Delta A|)."""
+    inp = _with_im(gu.custom("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N, n_dirs=K))
+    print(f"case complex zoh N={N} K={K} seg={seg}", flush=True)
+    y, dy = gu.run(inp, drive="zoh", seg_len=seg)
+    yo, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp, drive="zoh")
+    gu.assert_close(y.cpu().numpy(), dy.cpu().numpy(), yo, dyo, what=f"complex zoh N={N} K={K} seg={seg}")
+
+
+def test_cplx_zoh_s4dlin_stiff_map_and_blocks():
+    for inp, what, act in ((_with_im(gu.custom("pulse128k", seqlen=3000, d_inner=64, dx_kind="normal"), "s4dlin"),
+                            "complex zoh s4d-lin small steps", "identity"),
+                           (_with_im(gu.custom("stiff128k", seqlen=1500, d_inner=64)), "complex zoh stiff bf16",
+                            "identity"),
+                           (_with_dres(_with_im(gu.custom("mamba130m", seqlen=1200, d_inner=64, n_dirs=2))),
+                            "complex zoh + silu + D_res", "silu")):
+        print(f"case {what}", flush=True)
+        y, dy = gu.run(inp, drive="zoh", act=act)
+        yo, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp, drive="zoh", act=act)
+        gu.assert_close(y.cpu().numpy(), dy.cpu().numpy(), yo, dyo, what=what)
+    inp = _with_im(gu.custom("mamba130m", batch=2, seqlen=1000, d_inner=48, n_dirs=2))
+    ref = gu.run(inp, drive="zoh", seg_len=64, chunk_segs=1, return_state=True)
+    for cs in (3, 0):
+        got = gu.run(inp, drive="zoh", seg_len=64, chunk_segs=cs, return_state=True)
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), cs
+    _, _, ho, dho = oracle.scan_jvp(inp["x"], inp["dx"], inp, drive="zoh")
+    assert gu.rel_l2(ref[2].cpu().numpy(), ho) <= gu.TOL and gu.rel_l2(ref[3].cpu().numpy(), dho) <= gu.TOL

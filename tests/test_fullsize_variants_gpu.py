@@ -38,6 +38,7 @@ VARIANTS = {
     "silu_dres": (dict(dres=True), dict(act="silu")),
     "s4dlin": (dict(complex_a=True), dict()),
     "s4dlin_silu_dres": (dict(complex_a=True, dres=True), dict(act="silu")),
+    "s4dlin_zoh": (dict(complex_a=True), dict(drive="zoh")),
     "groups4": (dict(groups=4), dict()),
     "lowrank48": (dict(lowrank=48), dict()),
 }

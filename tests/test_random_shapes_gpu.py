@@ -42,6 +42,8 @@ def _first_order_case(i):
             extra = dict(complex=True)
             if r.integers(0, 2):
                 extra.update(act="silu", dres=True)
+            if r.integers(0, 2):
+                extra.update(drive="zoh")
     return base, cfg, kw, extra
 
 
