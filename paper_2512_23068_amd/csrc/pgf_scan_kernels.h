@@ -2291,8 +2291,11 @@ __device__ __forceinline__ void zoh_coef_c(float delta, float a_re, float a_im, 
     ei = small ? delta * qi : li;
 }
 
+// Occupancy: with one direction and N = 16 both passes are held to three
+// waves per SIMD (168 VGPRs), except the ZOH aggregate pass, which measured
+// faster at two; two directions and the other ZOH passes run two.
 template <int NT, int K, bool OUT, typename InT, bool MAP = false, bool ZOH = false>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(!OUT && (K >= 2 || ZOH) ? 2 : 1))) void k_cscan(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 16 && K == 1 ? (ZOH && !OUT ? 2 : 3) : (K >= 2 || ZOH ? 2 : 1)))) void k_cscan(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A, const float *__restrict__ Aim,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *init, int64_t ibs, int64_t igs, int64_t ics, float *__restrict__ y, float *__restrict__ dy,
@@ -2314,13 +2317,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(!OUT &
     const int64_t te = ts + S < len ? ts + S : len;
     if (ts >= te) return;
 
-    float Ar[NT], Ai[NT], At[NT], Ar2[NT];
+    // Only A itself is held per lane; the step's scale factors of the
+    // exponent (Delta log2 e) and of the angle in revolutions (Delta / 2 pi)
+    // are formed once per step for all lanes.
+    float Ar[NT], Ai[NT];
 #pragma unroll
     for (int i = 0; i < NT; ++i) {
         Ar[i] = A[d * N + i];
         Ai[i] = Aim[d * N + i];
-        At[i] = Ar[i] * kLog2e;
-        Ar2[i] = Ai[i] * kInv2Pi;
     }
     const float w = w_delta[d], bd = b_delta[d];
     float Dr = 0.0f;
@@ -2387,6 +2391,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(!OUT &
                 float delta, sw;
                 discretize(xv, w, bd, delta, sw);
                 const float u = delta * xv;
+                const float dl2 = delta * kLog2e, drev = delta * kInv2Pi;
                 float dD[K], pk[K];
 #pragma unroll
                 for (int k = 0; k < K; ++k) {
@@ -2405,9 +2410,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(!OUT &
 #pragma unroll
                 for (int i = 0; i < NT; ++i) {
                     const float Bn = rec[i];
-                    const float e = transition(delta, At[i]);
+                    const float e = transition(dl2, Ar[i]);
                     float cs, sn;
-                    rot(delta * Ar2[i], cs, sn);
+                    rot(drev * Ai[i], cs, sn);
                     const float ar = e * cs, ai = e * sn;
                     const float sr = fmaf(ar, hr[i], -ai * hi[i]);
                     const float si = fmaf(ar, hi[i], ai * hr[i]);
@@ -2461,19 +2466,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(!OUT &
                         yv = fmaf(Dr, xv, yv);
 #pragma unroll
                         for (int k = 0; k < K; ++k) dyv[k] = fmaf(Dr, dxc[k][j], dyv[k]);
-                        if (act == PGF_ACT_SILU) {
-                            float f, df;
-                            silu_and_slope(yv, f, df);
-                            yv = f;
+                        // selected, not branched on (see the stores below)
+                        float f, df;
+                        silu_and_slope(yv, f, df);
+                        const bool on = act == PGF_ACT_SILU;
+                        yv = on ? f : yv;
 #pragma unroll
-                            for (int k = 0; k < K; ++k) dyv[k] *= df;
-                        }
+                        for (int k = 0; k < K; ++k) dyv[k] *= on ? df : 1.0f;
                     }
-                    if (active) {
-                        store_out(Yb, (uint32_t)t * Du + du, yv);
+                    // A thread past D computes channel D-1 exactly and stores
+                    // the same bits there, so the step has no branch: a branch
+                    // here cut the step into two blocks, and values held across
+                    // the cut took up to twice the registers.
+                    store_out(Yb, (uint32_t)t * Du + du, yv);
 #pragma unroll
-                        for (int k = 0; k < K; ++k) store_out(DYb + k * dxs, (uint32_t)t * Du + du, dyv[k]);
-                    }
+                    for (int k = 0; k < K; ++k) store_out(DYb + k * dxs, (uint32_t)t * Du + du, dyv[k]);
                 }
             }
         }
