@@ -2291,24 +2291,29 @@ __device__ __forceinline__ void zoh_coef_c(float delta, float a_re, float a_im, 
     ei = small ? delta * qi : li;
 }
 
-// Occupancy: with one direction and N = 16 both passes are held to three
-// waves per SIMD (168 VGPRs), except the ZOH aggregate pass, which measured
-// faster at two; two directions and the other ZOH passes run two.
-template <int NT, int K, bool OUT, typename InT, bool MAP = false, bool ZOH = false>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 16 && K == 1 ? (ZOH && !OUT ? 2 : 3) : (K >= 2 || ZOH ? 2 : 1)))) void k_cscan(
+// Occupancy: with one direction and 16 lanes per thread both passes are held
+// to three waves per SIMD (168 VGPRs), except the ZOH aggregate pass, which
+// measured faster at two; two directions and the other ZOH passes run two.
+// NS >= 2 threads share a channel (N = 32, 64): each holds NT = 16 of its
+// lanes and the partial outputs are summed over the NS threads (group_sum,
+// the same bits in each), so every thread of the channel stores the same
+// value.
+template <int NT, int K, bool OUT, typename InT, bool MAP = false, bool ZOH = false, int NS = 1>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 16 && K == 1 && NS == 1 ? (ZOH && !OUT ? 2 : 3) : (K >= 2 || ZOH || NS > 1 ? 2 : 1)))) void k_cscan(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A, const float *__restrict__ Aim,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *init, int64_t ibs, int64_t igs, int64_t ics, float *__restrict__ y, float *__restrict__ dy,
     float *end_state, float *__restrict__ agg_h, float *__restrict__ agg_s, int64_t Bsz, int64_t L, int64_t D,
     int64_t t0, int64_t len, int64_t Tc, int64_t S, int G, const float *__restrict__ D_res, int act) {
     static_assert(OUT || !MAP, "the aggregate pass writes no outputs");
-    constexpr int N = NT;
+    constexpr int N = NT * NS;
     constexpr int R = 2 * N * (1 + K);
     constexpr int TT = 8;
     constexpr int CP = 2 * (1 + K);   // state planes
 
     const int tid = threadIdx.x;
-    const int64_t d_raw = (int64_t)blockIdx.x * kThreads + tid;
+    const int ns = tid % NS;          // this thread's lanes: n = ns NT + i
+    const int64_t d_raw = (int64_t)blockIdx.x * (kThreads / NS) + tid / NS;
     const bool active = d_raw < D;
     const int64_t d = active ? d_raw : D - 1;
     const int g = blockIdx.y;
@@ -2323,8 +2328,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
     float Ar[NT], Ai[NT];
 #pragma unroll
     for (int i = 0; i < NT; ++i) {
-        Ar[i] = A[d * N + i];
-        Ai[i] = Aim[d * N + i];
+        Ar[i] = A[d * N + ns * NT + i];
+        Ai[i] = Aim[d * N + ns * NT + i];
     }
     const float w = w_delta[d], bd = b_delta[d];
     float Dr = 0.0f;
@@ -2332,7 +2337,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
 
     float hr[NT], hi[NT], dr[K][NT], di[K][NT];
     if constexpr (OUT) {
-        const float *ib = init + b * ibs + g * igs + d;
+        const float *ib = init + b * ibs + g * igs + (int64_t)ns * NT * D + d;
 #pragma unroll
         for (int i = 0; i < NT; ++i) {
             hr[i] = ib[i * D];
@@ -2403,7 +2408,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
 #pragma unroll
                     for (int k = 0; k < K; ++k) sdD[k] += dD[k];
                 }
-                const float *rec = rec0 + t * R;
+                const float *rec = rec0 + t * R + ns * NT;   // this thread's lanes
                 float yv = 0.0f, dyv[K];
 #pragma unroll
                 for (int k = 0; k < K; ++k) dyv[k] = 0.0f;
@@ -2462,6 +2467,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
                     }
                 }
                 if constexpr (OUT) {
+                    yv = group_sum<NS>(yv);
+#pragma unroll
+                    for (int k = 0; k < K; ++k) dyv[k] = group_sum<NS>(dyv[k]);
                     if constexpr (MAP) {
                         yv = fmaf(Dr, xv, yv);
 #pragma unroll
@@ -2495,7 +2503,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
     if (!active) return;
     if constexpr (OUT) {
         if (end_state) {
-            float *eb = end_state + b * ibs + d;
+            float *eb = end_state + b * ibs + (int64_t)ns * NT * D + d;
 #pragma unroll
             for (int i = 0; i < NT; ++i) {
                 eb[i * D] = hr[i];
@@ -2511,14 +2519,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
         const int64_t base = (b * G + g) * CP;
 #pragma unroll
         for (int i = 0; i < NT; ++i) {
-            agg_h[(base * N + i) * D + d] = hr[i];
-            agg_h[((base + 1) * N + i) * D + d] = hi[i];
+            const int n = ns * NT + i;
+            agg_h[(base * N + n) * D + d] = hr[i];
+            agg_h[((base + 1) * N + n) * D + d] = hi[i];
 #pragma unroll
             for (int k = 0; k < K; ++k) {
-                agg_h[((base + 2 + 2 * k) * N + i) * D + d] = dr[k][i];
-                agg_h[((base + 3 + 2 * k) * N + i) * D + d] = di[k][i];
+                agg_h[((base + 2 + 2 * k) * N + n) * D + d] = dr[k][i];
+                agg_h[((base + 3 + 2 * k) * N + n) * D + d] = di[k][i];
             }
         }
+        if (ns != 0) return;   // the per-channel sums once
         const int64_t sbase = (b * G + g) * (1 + K);
         agg_s[sbase * D + d] = sD;
 #pragma unroll
@@ -2873,19 +2883,22 @@ struct Launcher {
         }
     }
 
-    // Complex transition: one thread per channel with all N <= 16 lanes.
-    template <int NT, int K>
+    // Complex transition: NS threads per channel with NT lanes each
+    // (N <= 16: one thread with all lanes; N = 32, 64: 16 lanes per thread).
+    template <int NT, int NS, int K>
     void cscans(int64_t t0, int64_t len) {
         if (dry) return;
-        const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
+        constexpr int DPB = kThreads / NS;   // channels per block
+        const unsigned gx = (unsigned)((q.D + DPB - 1) / DPB);
         const int64_t ND = q.N * q.D;
         constexpr int CP = 2 * (1 + K);
         // the passes of the call's drive, the output pass with its output map
-        auto kout = (q.var & 1) ? ((q.var & 2) ? &k_cscan<NT, K, true, InT, true, true>
-                                               : &k_cscan<NT, K, true, InT, false, true>)
-                                : ((q.var & 2) ? &k_cscan<NT, K, true, InT, true, false>
-                                               : &k_cscan<NT, K, true, InT, false, false>);
-        auto kagg = (q.var & 1) ? &k_cscan<NT, K, false, InT, false, true> : &k_cscan<NT, K, false, InT, false, false>;
+        auto kout = (q.var & 1) ? ((q.var & 2) ? &k_cscan<NT, K, true, InT, true, true, NS>
+                                               : &k_cscan<NT, K, true, InT, false, true, NS>)
+                                : ((q.var & 2) ? &k_cscan<NT, K, true, InT, true, false, NS>
+                                               : &k_cscan<NT, K, true, InT, false, false, NS>);
+        auto kagg = (q.var & 1) ? &k_cscan<NT, K, false, InT, false, true, NS>
+                                : &k_cscan<NT, K, false, InT, false, false, NS>;
         if (q.seg == 0) {
             Timed tm(3, st, !q.noalloc);
             hipLaunchKernelGGL(kout, dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, dx,
@@ -2920,10 +2933,12 @@ struct Launcher {
 
     template <int K>
     bool cscan_block(int64_t t0, int64_t len) {
-        switch (q.nt) {
-            case 4: cscans<4, K>(t0, len); return true;
-            case 8: cscans<8, K>(t0, len); return true;
-            case 16: cscans<16, K>(t0, len); return true;
+        switch (q.nt * 8 + q.ns) {
+            case 4 * 8 + 1: cscans<4, 1, K>(t0, len); return true;
+            case 8 * 8 + 1: cscans<8, 1, K>(t0, len); return true;
+            case 16 * 8 + 1: cscans<16, 1, K>(t0, len); return true;
+            case 16 * 8 + 2: cscans<16, 2, K>(t0, len); return true;
+            case 16 * 8 + 4: cscans<16, 4, K>(t0, len); return true;
             default: return false;
         }
     }
@@ -3010,7 +3025,6 @@ struct Launcher {
 
     bool scan_block(int64_t t0, int64_t len) {
         if (q.cplx) {
-            if (q.ns != 1) return false;
             return q.K == 1 ? cscan_block<1>(t0, len) : (q.K == 2 ? cscan_block<2>(t0, len) : false);
         }
         if (q.order == 3) {

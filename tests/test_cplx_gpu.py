@@ -33,7 +33,8 @@ def _check(inp, what, **kw):
     gu.assert_close(y.cpu().numpy(), dy.cpu().numpy(), yo, dyo, what=what)
 
 
-@pytest.mark.parametrize("N,K,seg", [(16, 1, 0), (16, 2, 0), (8, 1, -1), (4, 2, 64), (16, 1, -1)])
+@pytest.mark.parametrize("N,K,seg", [(16, 1, 0), (16, 2, 0), (8, 1, -1), (4, 2, 64), (16, 1, -1),
+                                     (32, 1, 0), (32, 2, -1), (64, 1, 64), (64, 2, 0)])
 def test_cplx_parity(N, K, seg):
     inp = _with_im(gu.custom("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N, n_dirs=K))
     _check(inp, f"complex N={N} K={K} seg={seg}", seg_len=seg)
@@ -72,11 +73,12 @@ def test_cplx_block_invariance_and_handoff():
     assert torch.equal(b[2], ref[2]) and torch.equal(b[3], ref[3])
 
 
-def test_cplx_entry_state_matches_oracle():
-    inp = _with_im(gu.custom("mamba130m", batch=1, seqlen=600, d_inner=40))
+@pytest.mark.parametrize("N", [16, 64])
+def test_cplx_entry_state_matches_oracle(N):
+    inp = _with_im(gu.custom("mamba130m", batch=1, seqlen=600, d_inner=40, d_state=N))
     r = np.random.default_rng(4)
-    h0 = (r.standard_normal((1, 40, 16)) + 1j * r.standard_normal((1, 40, 16))).astype(np.complex64)
-    dh0 = (r.standard_normal((1, 1, 40, 16)) + 1j * r.standard_normal((1, 1, 40, 16))).astype(np.complex64)
+    h0 = (r.standard_normal((1, 40, N)) + 1j * r.standard_normal((1, 40, N))).astype(np.complex64)
+    dh0 = (r.standard_normal((1, 1, 40, N)) + 1j * r.standard_normal((1, 1, 40, N))).astype(np.complex64)
     y, dy, h, dh = gu.run(inp, h_in=torch.from_numpy(h0), dh_in=torch.from_numpy(dh0), return_state=True)
     yo, dyo, ho, dho = oracle.scan_jvp(inp["x"], inp["dx"], inp, h_in=h0, dh_in=dh0)
     for got, ref in ((y, yo), (dy, dyo), (h, ho), (dh, dho)):
@@ -87,9 +89,9 @@ def test_cplx_limits():
     inp = _with_im(gu.custom("tiny", seqlen=64, n_dirs=4))
     with pytest.raises(RuntimeError, match="UNSUPPORTED"):
         gu.run(inp)
-    inp = _with_im(gu.custom("tiny", seqlen=64, d_state=32))
+    inp = _with_im(gu.custom("tiny", seqlen=64, n_dirs=2))
     with pytest.raises(RuntimeError, match="UNSUPPORTED"):
-        gu.run(inp, drive="zoh")
+        binding.plan(1, 64, 16, 16, 2, order=2, complex_a=True)
 
 
 def _with_dres(inp, seed=11):
@@ -128,7 +130,8 @@ def test_cplx_with_output_map_s4dlin_stiff_and_blocks():
     assert torch.equal(plain[2], ref[2]) and torch.equal(plain[3], ref[3])
 
 
-@pytest.mark.parametrize("N,K,seg", [(16, 1, 0), (16, 2, 0), (8, 1, -1), (4, 2, 64), (16, 1, -1)])
+@pytest.mark.parametrize("N,K,seg", [(16, 1, 0), (16, 2, 0), (8, 1, -1), (4, 2, 64), (16, 1, -1),
+                                     (32, 1, 64), (64, 2, -1)])
 def test_cplx_zoh_parity(N, K, seg):
     """The zero-order-hold drive with the complex transition (S4D's
     discretisation): e = (exp(Delta A) - 1)/A complex, both branches of its
@@ -159,3 +162,52 @@ def test_cplx_zoh_s4dlin_stiff_map_and_blocks():
             assert torch.equal(a, b), cs
     _, _, ho, dho = oracle.scan_jvp(inp["x"], inp["dx"], inp, drive="zoh")
     assert gu.rel_l2(ref[2].cpu().numpy(), ho) <= gu.TOL and gu.rel_l2(ref[3].cpu().numpy(), dho) <= gu.TOL
+
+
+@pytest.mark.parametrize("N", [32, 64])
+def test_cplx_wide_state_map_zoh_and_blocks(N):
+    """N = 32 and 64 (16 lanes per thread, the partial outputs summed over
+    the threads of a channel): either drive with the output map, and
+    bit-identical results and exit states for every host block size."""
+    base = gu.custom("mamba130m", batch=2, seqlen=1300, d_inner=72, d_state=N, n_dirs=2)
+    for drive in ("euler", "zoh"):
+        inp = _with_dres(_with_im(dict(base)))
+        what = f"complex N={N} {drive} + silu + D_res"
+        print(f"case {what}", flush=True)
+        y, dy = gu.run(inp, drive=drive, act="silu")
+        yo, dyo, _, _ = oracle.scan_jvp(inp["x"], inp["dx"], inp, drive=drive, act="silu")
+        gu.assert_close(y.cpu().numpy(), dy.cpu().numpy(), yo, dyo, what=what)
+    inp = _with_im(dict(base))
+    ref = gu.run(inp, drive="zoh", seg_len=64, chunk_segs=1, return_state=True)
+    for cs in (4, 0):
+        got = gu.run(inp, drive="zoh", seg_len=64, chunk_segs=cs, return_state=True)
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), (N, cs)
+    _, _, ho, dho = oracle.scan_jvp(inp["x"], inp["dx"], inp, drive="zoh")
+    assert gu.rel_l2(ref[2].cpu().numpy(), ho) <= gu.TOL and gu.rel_l2(ref[3].cpu().numpy(), dho) <= gu.TOL
+
+
+@pytest.mark.parametrize("drive", ["euler", "zoh"])
+def test_cplx_wide_state_is_the_sum_of_its_halves(drive):
+    """The lanes of a channel do not interact, and with the identity map y
+    and dy are sums over them: N = 32 on two threads per channel equals the
+    two N = 16 halves of its S4D-Lin spectrum on the one-thread path, added
+    (outputs) and stacked (exit states), to rounding.  The halves' own
+    errors against the oracle are printed: the upper half rotates up to
+    twice as fast per step, and its phase error in f32 is the larger one."""
+    full = _with_im(gu.custom("mamba130m", batch=2, seqlen=1300, d_inner=72, d_state=32, n_dirs=2), "s4dlin")
+    y, dy, h, dh = gu.run(full, drive=drive, seg_len=64, return_state=True)
+    parts = []
+    for lo in (0, 16):
+        half = gu.custom("mamba130m", batch=2, seqlen=1300, d_inner=72, d_state=16, n_dirs=2)
+        for k in ("A", "A_im", "W_B", "W_C"):
+            half[k] = np.ascontiguousarray(full[k][:, lo:lo + 16])
+        half["x"], half["dx"] = full["x"], full["dx"]
+        parts.append(gu.run(half, drive=drive, seg_len=64, return_state=True))
+        yo, dyo, _, _ = oracle.scan_jvp(half["x"], half["dx"], half, drive=drive)
+        print(f"half n in [{lo}, {lo + 16}) {drive}: rel_l2 y={gu.rel_l2(parts[-1][0].cpu().numpy(), yo):.3e} "
+              f"dy={gu.rel_l2(parts[-1][1].cpu().numpy(), dyo):.3e}", flush=True)
+    checks = ((y, parts[0][0] + parts[1][0]), (dy, parts[0][1] + parts[1][1]),
+              (h, torch.cat([parts[0][2], parts[1][2]], -1)), (dh, torch.cat([parts[0][3], parts[1][3]], -1)))
+    for got, want in checks:
+        assert gu.rel_l2(got.cpu().numpy(), want.cpu().numpy()) < 1e-6
