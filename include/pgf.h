@@ -144,7 +144,7 @@ typedef struct pgf_params {
      * 3's general form); h_in/h_out are [B,D,N] and dh_in/dh_out [K,B,D,N]
      * complex (interleaved real, imaginary f32).  Either drive: with the
      * zero-order hold the drive coefficient is the complex (Abar - 1) / A.
-     * First order only, K <= 2, N up to 64. */
+     * First order only (every N and K of it). */
     const float *A_im;
     /* Channel groups with their own B and C (Mamba-style grouped
      * projections), 0 or 1 = one group.  With G > 1 groups, W_B and W_C are

@@ -81,10 +81,10 @@ int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
     // the ZOH drive and the output map
     if (var && order == 2) return PGF_ERR_UNSUPPORTED;
     const int cplx = p->A_im ? 1 : 0;
-    if (var && ((order != 3 && K > 2) || (N > 16 && !cplx))) return PGF_ERR_UNSUPPORTED;
-    // the complex transition takes either drive and N up to 64 (16 lanes
-    // per thread); the output map is applied to its real read-out
-    if (cplx && (order != 1 || K > 2)) return PGF_ERR_UNSUPPORTED;
+    if (var && !cplx && ((order != 3 && K > 2) || N > 16)) return PGF_ERR_UNSUPPORTED;
+    // the complex transition takes either drive, every N and K of the real
+    // first order; the output map is applied to its real read-out
+    if (cplx && order != 1) return PGF_ERR_UNSUPPORTED;
     if (p->n_groups < 0) return PGF_ERR_INVALID_ARG;
     const int64_t groups = p->n_groups > 1 ? p->n_groups : 1;
     if (groups > 1) {

@@ -2299,7 +2299,7 @@ __device__ __forceinline__ void zoh_coef_c(float delta, float a_re, float a_im, 
 // the same bits in each), so every thread of the channel stores the same
 // value.
 template <int NT, int K, bool OUT, typename InT, bool MAP = false, bool ZOH = false, int NS = 1>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 16 && K == 1 && NS == 1 ? (ZOH && !OUT ? 2 : 3) : (K >= 2 || ZOH || NS > 1 ? 2 : 1)))) void k_cscan(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 16 && K == 1 && NS == 1 ? (ZOH && !OUT ? 2 : 3) : (K <= 2 && (K == 2 || ZOH || NS > 1) ? 2 : 1)))) void k_cscan(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A, const float *__restrict__ Aim,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *init, int64_t ibs, int64_t igs, int64_t ics, float *__restrict__ y, float *__restrict__ dy,
@@ -2308,7 +2308,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 
     static_assert(OUT || !MAP, "the aggregate pass writes no outputs");
     constexpr int N = NT * NS;
     constexpr int R = 2 * N * (1 + K);
-    constexpr int TT = 8;
+    constexpr int TT = K >= 8 ? 2 : (K >= 4 ? 4 : 8);   // prefetched steps: K+1 inputs each
     constexpr int CP = 2 * (1 + K);   // state planes
 
     const int tid = threadIdx.x;
@@ -2931,15 +2931,38 @@ struct Launcher {
         }
     }
 
+    // The planner's tilings: 16 lanes per thread for K <= 2, 8 for K = 4,
+    // 4 for K = 8 (fewer when N is smaller).
     template <int K>
     bool cscan_block(int64_t t0, int64_t len) {
-        switch (q.nt * 8 + q.ns) {
-            case 4 * 8 + 1: cscans<4, 1, K>(t0, len); return true;
-            case 8 * 8 + 1: cscans<8, 1, K>(t0, len); return true;
-            case 16 * 8 + 1: cscans<16, 1, K>(t0, len); return true;
-            case 16 * 8 + 2: cscans<16, 2, K>(t0, len); return true;
-            case 16 * 8 + 4: cscans<16, 4, K>(t0, len); return true;
-            default: return false;
+        const int code = q.nt * 32 + q.ns;
+        if constexpr (K <= 2) {
+            switch (code) {
+                case 4 * 32 + 1: cscans<4, 1, K>(t0, len); return true;
+                case 8 * 32 + 1: cscans<8, 1, K>(t0, len); return true;
+                case 16 * 32 + 1: cscans<16, 1, K>(t0, len); return true;
+                case 16 * 32 + 2: cscans<16, 2, K>(t0, len); return true;
+                case 16 * 32 + 4: cscans<16, 4, K>(t0, len); return true;
+                default: return false;
+            }
+        } else if constexpr (K == 4) {
+            switch (code) {
+                case 4 * 32 + 1: cscans<4, 1, K>(t0, len); return true;
+                case 8 * 32 + 1: cscans<8, 1, K>(t0, len); return true;
+                case 8 * 32 + 2: cscans<8, 2, K>(t0, len); return true;
+                case 8 * 32 + 4: cscans<8, 4, K>(t0, len); return true;
+                case 8 * 32 + 8: cscans<8, 8, K>(t0, len); return true;
+                default: return false;
+            }
+        } else {
+            switch (code) {
+                case 4 * 32 + 1: cscans<4, 1, K>(t0, len); return true;
+                case 4 * 32 + 2: cscans<4, 2, K>(t0, len); return true;
+                case 4 * 32 + 4: cscans<4, 4, K>(t0, len); return true;
+                case 4 * 32 + 8: cscans<4, 8, K>(t0, len); return true;
+                case 4 * 32 + 16: cscans<4, 16, K>(t0, len); return true;
+                default: return false;
+            }
         }
     }
 
@@ -3025,7 +3048,13 @@ struct Launcher {
 
     bool scan_block(int64_t t0, int64_t len) {
         if (q.cplx) {
-            return q.K == 1 ? cscan_block<1>(t0, len) : (q.K == 2 ? cscan_block<2>(t0, len) : false);
+            switch (q.K) {
+                case 1: return cscan_block<1>(t0, len);
+                case 2: return cscan_block<2>(t0, len);
+                case 4: return cscan_block<4>(t0, len);
+                case 8: return cscan_block<8>(t0, len);
+                default: return false;
+            }
         }
         if (q.order == 3) {
             if (q.ns != 1 || (q.var & ~(kZoh | kOutMap)) || (q.K != 2 && q.K != 4)) return false;

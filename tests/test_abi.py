@@ -226,16 +226,17 @@ def test_complex_transition_plans():
     p.A_im = 1 << 30                      # any non-NULL pointer selects the complex state
     cplx = binding.lib().pgf_workspace_bytes(ctypes.byref(p))
     assert cplx > base
-    for kw in (dict(n_dirs=4), dict(order=2, n_dirs=2), dict(order=3)):
+    for kw in (dict(order=2, n_dirs=2), dict(order=3)):
         q = binding.make_params(1, 1000, 64, 16, 1)
         q.A_im = 1 << 30
         for k, v in kw.items():
             setattr(q, k, v)
         assert binding.lib().pgf_workspace_bytes(ctypes.byref(q)) == 0, kw
-    # either drive, and the output map on the real read-out, N up to 64
-    for N in (16, 32, 64):
+    # either drive, and the output map on the real read-out, N up to 64,
+    # up to eight directions
+    for N, K in ((16, 2), (32, 1), (64, 2), (16, 4), (64, 8)):
         for kw in (dict(act="silu"), dict(drive="zoh"), dict(drive="zoh", act="silu")):
-            q = binding.make_params(1, 1000, 64, N, 2, **kw)
+            q = binding.make_params(1, 1000, 64, N, K, **kw)
             q.A_im = 1 << 30
             assert binding.lib().pgf_workspace_bytes(ctypes.byref(q)) > 0, (N, kw)
 
@@ -336,7 +337,7 @@ def test_support_matrix_has_kernels():
                     p = binding.plan(2, 3000, 256, N, K, in_dtype=dt, seg_len=seg)
                     assert p["n_per_thread"] * p["n_split"] == N
                     # follow-on paths: one thread per channel, N <= 16, K <= 2
-                    # (the complex state: N <= 64, 16 lanes per thread)
+                    # (the complex state: every N and K of the first order)
                     for kw in (dict(order=2), dict(order=3), dict(drive="zoh"), dict(act="silu"),
                                dict(complex_a=True), dict(complex_a=True, act="silu"),
                                dict(complex_a=True, drive="zoh"), dict(groups=4),
@@ -344,8 +345,8 @@ def test_support_matrix_has_kernels():
                                dict(order=3, act="silu"), dict(order=3, drive="zoh", act="silu")):
                         if kw.get("order") == 2 and K != 2:
                             continue
-                        ok = (N <= 16 or (kw.get("complex_a") and "order" not in kw)) and \
-                            (K <= 2 or kw.get("order") == 3)
+                        ok = (kw.get("complex_a") and "order" not in kw) or \
+                            (N <= 16 and (K <= 2 or kw.get("order") == 3))
                         if ok:
                             binding.plan(2, 3000, 256, N, K, in_dtype=dt, seg_len=seg, **kw)
                         else:

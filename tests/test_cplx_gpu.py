@@ -34,7 +34,8 @@ def _check(inp, what, **kw):
 
 
 @pytest.mark.parametrize("N,K,seg", [(16, 1, 0), (16, 2, 0), (8, 1, -1), (4, 2, 64), (16, 1, -1),
-                                     (32, 1, 0), (32, 2, -1), (64, 1, 64), (64, 2, 0)])
+                                     (32, 1, 0), (32, 2, -1), (64, 1, 64), (64, 2, 0),
+                                     (16, 4, 0), (64, 4, -1), (4, 4, 64), (16, 8, 64), (64, 8, 0), (4, 8, -1)])
 def test_cplx_parity(N, K, seg):
     inp = _with_im(gu.custom("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N, n_dirs=K))
     _check(inp, f"complex N={N} K={K} seg={seg}", seg_len=seg)
@@ -86,9 +87,8 @@ def test_cplx_entry_state_matches_oracle(N):
 
 
 def test_cplx_limits():
-    inp = _with_im(gu.custom("tiny", seqlen=64, n_dirs=4))
     with pytest.raises(RuntimeError, match="UNSUPPORTED"):
-        gu.run(inp)
+        binding.plan(1, 64, 16, 16, 1, order=3, complex_a=True)
     inp = _with_im(gu.custom("tiny", seqlen=64, n_dirs=2))
     with pytest.raises(RuntimeError, match="UNSUPPORTED"):
         binding.plan(1, 64, 16, 16, 2, order=2, complex_a=True)
@@ -131,7 +131,7 @@ def test_cplx_with_output_map_s4dlin_stiff_and_blocks():
 
 
 @pytest.mark.parametrize("N,K,seg", [(16, 1, 0), (16, 2, 0), (8, 1, -1), (4, 2, 64), (16, 1, -1),
-                                     (32, 1, 64), (64, 2, -1)])
+                                     (32, 1, 64), (64, 2, -1), (8, 4, 64), (32, 8, -1)])
 def test_cplx_zoh_parity(N, K, seg):
     """The zero-order-hold drive with the complex transition (S4D's
     discretisation): e = (exp(Delta A) - 1)/A complex, both branches of its

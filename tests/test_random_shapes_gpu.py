@@ -44,8 +44,9 @@ def _first_order_case(i):
                 extra.update(act="silu", dres=True)
             if r.integers(0, 2):
                 extra.update(drive="zoh")
-    elif K <= 2 and i % 8 == 5:
-        # the complex state with 16 lanes per thread (N = 32, 64)
+    elif i % 8 == 5:
+        # the complex state with several threads per channel (N = 32, 64, or
+        # four and eight directions)
         extra = dict(complex=True, drive="zoh" if i % 16 == 5 else "euler")
     return base, cfg, kw, extra
 
