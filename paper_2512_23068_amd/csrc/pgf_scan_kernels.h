@@ -2214,7 +2214,8 @@ static __global__ __launch_bounds__(kThreads) void k_gout(
 
 // ---------------------------------------------------------------- complex
 // Complex diagonal transition A = A_re + i A_im (Sec. 3: state in C^{DxN},
-// read-out y = sum_n C Re(h)), one thread per channel with all NT = N lanes.
+// read-out y = sum_n C Re(h)), NS threads per channel with NT = N/NS lanes
+// each (one thread with all lanes up to N = 16 and K = 2).
 // Per lane and step, with Abar = exp(Delta A_re) (cos th + i sin th),
 // th = Delta A_im:
 //   s = Abar h,  h' = s + B u,  g = A s,
