@@ -73,7 +73,7 @@ int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
     if ((double)K * B * (double)L * D > 9.0e18 / 16) return PGF_ERR_UNSUPPORTED;
 
     if (order == 2 && K != 2) return PGF_ERR_INVALID_ARG;
-    if (order >= 2 && N > 16) return PGF_ERR_UNSUPPORTED;
+    if (order == 2 && N > 16) return PGF_ERR_UNSUPPORTED;
     if (p->drive < 0 || p->drive > 1 || p->activation < 0 || p->activation > 1) return PGF_ERR_INVALID_ARG;
     const int var = (p->drive == PGF_DRIVE_ZOH ? 1 : 0) |
                     ((p->activation != PGF_ACT_IDENTITY || p->D_res) ? 2 : 0);
@@ -81,7 +81,7 @@ int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
     // the ZOH drive and the output map
     if (var && order == 2) return PGF_ERR_UNSUPPORTED;
     const int cplx = p->A_im ? 1 : 0;
-    if (var && !cplx && ((order != 3 && K > 2) || N > 16)) return PGF_ERR_UNSUPPORTED;
+    if (var && !cplx && order != 3 && (K > 2 || N > 16)) return PGF_ERR_UNSUPPORTED;
     // the complex transition takes either drive, every N and K of the real
     // first order; the output map is applied to its real read-out
     if (cplx && order != 1) return PGF_ERR_UNSUPPORTED;
@@ -111,8 +111,9 @@ int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
     q.comp = (int)((1 + K + (order == 2 ? 1 : 0)) * (cplx ? 2 : 1));
     q.in_bf16 = p->in_dtype == PGF_BF16;
     // Registers per thread grow as nt*(3+K); keep them near 128.
-    // (the parameter flows hold all N <= 16 lanes in one thread)
-    q.nt = (int)(order == 3 ? N : std::min<int64_t>(N, K >= 8 ? 4 : (K >= 4 ? 8 : 16)));
+    // (the parameter flows: up to 16 lanes per thread, N = 32 and 64 on
+    // two and four threads)
+    q.nt = (int)(order == 3 ? std::min<int64_t>(N, 16) : std::min<int64_t>(N, K >= 8 ? 4 : (K >= 4 ? 8 : 16)));
     q.ns = (int)(N / q.nt);
     q.R = (int)(groups * 2 * N * (1 + q.KP));
     // Wide f32 channel sums are cut into splits of at most about 2048

@@ -1808,7 +1808,11 @@ __global__ __launch_bounds__(kThreads) void k_carry(
 // w sum_n C Gw' and w sum_n C Gs'.  The per-channel partials of the output
 // pass (D_res, then w_delta, then b_delta) are stored, or with gadd added,
 // at gch[b gch_bs + g gch_gs + c gch_cs + d], c = 0, 1, 2.
-template <int NT, bool OUT, typename InT, bool ZOH = false, bool MAP = false, bool DLT = false>
+// NS >= 2 threads share a channel (N = 32, 64) with NT = 16 of its lanes
+// each; the per-channel sums (y, and the step size's C Gw, C Gs) are summed
+// over them (group_sum, the same bits in each) and the per-channel partials
+// are written by the first of them.
+template <int NT, bool OUT, typename InT, bool ZOH = false, bool MAP = false, bool DLT = false, int NS = 1>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH || DLT ? 2 : 3))) void k_pscan(
     const InT *__restrict__ x, const float *__restrict__ gy, const float *__restrict__ A,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
@@ -1818,7 +1822,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ||
     int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G,
     const float *__restrict__ D_res, int act, float *gch, int64_t gch_bs, int64_t gch_gs, int64_t gch_cs) {
     static_assert(OUT || !MAP, "the output map belongs to the output pass");
-    constexpr int N = NT;
+    constexpr int N = NT * NS;
     constexpr int R = 2 * N;          // B, C
     constexpr int CP = DLT ? 5 : 3;   // state planes per lane
     constexpr int NW = DLT ? NT : 1;
@@ -1830,7 +1834,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ||
     constexpr int TT = OUT && NT >= 16 ? (MAP || DLT ? 2 : 4) : 8;
 
     const int tid = threadIdx.x;
-    const int64_t d_raw = (int64_t)blockIdx.x * kThreads + tid;
+    const int ns = tid % NS;          // this thread's lanes: n = ns NT + i
+    const int64_t d_raw = (int64_t)blockIdx.x * (kThreads / NS) + tid / NS;
     const bool active = d_raw < D;
     const int64_t d = active ? d_raw : D - 1;
     const int g = blockIdx.y;
@@ -1842,8 +1847,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ||
     float At[ATF ? 1 : NT], Af[NT], Ai[NT];
 #pragma unroll
     for (int i = 0; i < NT; ++i) {
-        if constexpr (!ATF) At[i] = A[d * N + i] * kLog2e;
-        if constexpr (ZOH || DLT) Af[i] = A[d * N + i];
+        if constexpr (!ATF) At[i] = A[d * N + ns * NT + i] * kLog2e;
+        if constexpr (ZOH || DLT) Af[i] = A[d * N + ns * NT + i];
         if constexpr (ZOH) Ai[i] = 1.0f / Af[i];
     }
     const float w = w_delta[d], bd = b_delta[d];
@@ -1853,7 +1858,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ||
     float h[NT], ga[NT], gb[NT], gw[NW], gs[NW];
     float sA[NT], sB[NT], sC[NT];
     if constexpr (OUT) {
-        const float *ib = init + b * ibs + g * igs + d;
+        const float *ib = init + b * ibs + g * igs + (int64_t)ns * NT * D + d;
 #pragma unroll
         for (int i = 0; i < NT; ++i) {
             h[i] = ib[i * D];
@@ -1920,7 +1925,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ||
                         sS += sig;
                     }
                 }
-                const float *rec = rec0 + t * R;
+                const float *rec = rec0 + t * R + ns * NT;   // this thread's lanes
                 float yv = 0.0f, cw = 0.0f, cs = 0.0f;
 #pragma unroll
                 for (int i = 0; i < NT; ++i) {
@@ -1967,6 +1972,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ||
                         }
                     }
                 }
+                if constexpr (OUT && NS > 1) {
+                    yv = group_sum<NS>(yv);
+                    if constexpr (DLT) {
+                        cw = group_sum<NS>(cw);
+                        cs = group_sum<NS>(cs);
+                    }
+                }
                 if constexpr (OUT && DLT && !MAP) {
                     sW = fmaf(gc[j], cw, sW);
                     sG = fmaf(gc[j], cs, sG);
@@ -2009,7 +2021,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ||
     if (!active) return;
     if constexpr (OUT) {
         if (end_state) {
-            float *eb = end_state + b * ibs + d;
+            float *eb = end_state + b * ibs + (int64_t)ns * NT * D + d;
 #pragma unroll
             for (int i = 0; i < NT; ++i) {
                 eb[i * D] = h[i];
@@ -2021,13 +2033,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ||
                 }
             }
         }
-        float *pc = gch + b * gch_bs + g * gch_gs + d;
-        if constexpr (MAP) pc[0] = gadd ? pc[0] + sDr : sDr;
-        if constexpr (DLT) {
-            pc[gch_cs] = gadd ? pc[gch_cs] + sW : sW;
-            pc[2 * gch_cs] = gadd ? pc[2 * gch_cs] + sG : sG;
+        if (ns == 0) {
+            float *pc = gch + b * gch_bs + g * gch_gs + d;
+            if constexpr (MAP) pc[0] = gadd ? pc[0] + sDr : sDr;
+            if constexpr (DLT) {
+                pc[gch_cs] = gadd ? pc[gch_cs] + sW : sW;
+                pc[2 * gch_cs] = gadd ? pc[2 * gch_cs] + sG : sG;
+            }
         }
-        float *ob = gout + b * ibs + g * igs + d;
+        float *ob = gout + b * ibs + g * igs + (int64_t)ns * NT * D + d;
         if (gadd) {
 #pragma unroll
             for (int i = 0; i < NT; ++i) {
@@ -2047,14 +2061,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH ||
         const int64_t base = (b * G + g) * CP;
 #pragma unroll
         for (int i = 0; i < NT; ++i) {
-            agg_h[(base * N + i) * D + d] = h[i];
-            agg_h[((base + 1) * N + i) * D + d] = ga[i];
-            agg_h[((base + 2) * N + i) * D + d] = gb[i];
+            const int n = ns * NT + i;
+            agg_h[(base * N + n) * D + d] = h[i];
+            agg_h[((base + 1) * N + n) * D + d] = ga[i];
+            agg_h[((base + 2) * N + n) * D + d] = gb[i];
             if constexpr (DLT) {
-                agg_h[((base + 3) * N + i) * D + d] = gw[i];
-                agg_h[((base + 4) * N + i) * D + d] = gs[i];
+                agg_h[((base + 3) * N + n) * D + d] = gw[i];
+                agg_h[((base + 4) * N + n) * D + d] = gs[i];
             }
         }
+        if (ns != 0) return;   // the per-channel sums once
         agg_s[base * D + d] = sD;
         if constexpr (DLT) {
             agg_s[(base + 1) * D + d] = sSx;
@@ -2972,12 +2988,12 @@ struct Launcher {
     // of dl/dD_res; DLT: the step size's flows with the partials of
     // dl/dw_delta and dl/db_delta.  The per-channel sums go to gacc's
     // [3][B][D] tail.
-    template <int NT, bool ZOH, bool MAP, bool DLT>
+    template <int NT, int NS, bool ZOH, bool MAP, bool DLT>
     void pscans(int64_t t0, int64_t len) {
         if (dry) return;
         constexpr int CP = DLT ? 5 : 3;
         constexpr int cmask = (MAP ? 1 : 0) | (DLT ? 6 : 0);
-        const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
+        const unsigned gx = (unsigned)((q.D + kThreads / NS - 1) / (kThreads / NS));
         const int64_t ND = q.N * q.D;
         if (q.seg == 0) {
             // One launch per kSeqChunk steps (a host block is a whole number
@@ -2985,7 +3001,7 @@ struct Launcher {
             for (int64_t u0 = 0; u0 < len; u0 += kSeqChunk) {
                 const int64_t ul = len - u0 < kSeqChunk ? len - u0 : kSeqChunk;
                 Timed tm(3, st, !q.noalloc);
-                hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH, MAP, DLT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads),
+                hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH, MAP, DLT, NS>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads),
                                    0, st, x, gy, p.A, p.w_delta, p.b_delta, (const float *)(bcw() + u0 * q.R),
                                    (const float *)state(), ND, (int64_t)0, q.B * ND, y, state(), gacc(), 1,
                                    (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0 + u0, ul, q.chunk_len, ul, 1,
@@ -2996,7 +3012,7 @@ struct Launcher {
         const int G = (int)((len + q.seg - 1) / q.seg);
         {
             Timed tm(1, st, !q.noalloc);
-            hipLaunchKernelGGL((k_pscan<NT, false, InT, ZOH, false, DLT>), dim3(gx, (unsigned)G, (unsigned)q.B),
+            hipLaunchKernelGGL((k_pscan<NT, false, InT, ZOH, false, DLT, NS>), dim3(gx, (unsigned)G, (unsigned)q.B),
                                dim3(kThreads), 0, st, x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)nullptr,
                                (int64_t)0, (int64_t)0, (int64_t)0, y, (float *)nullptr, (float *)nullptr, 0, agg_h(),
                                agg_s(), q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg, G,
@@ -3013,7 +3029,7 @@ struct Launcher {
         float *chp = agg_s() + q.D;
         {
             Timed tm(3, st, !q.noalloc);
-            hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH, MAP, DLT>), dim3(gx, (unsigned)G, (unsigned)q.B),
+            hipLaunchKernelGGL((k_pscan<NT, true, InT, ZOH, MAP, DLT, NS>), dim3(gx, (unsigned)G, (unsigned)q.B),
                                dim3(kThreads), 0, st, x, gy, p.A, p.w_delta, p.b_delta, bcw(), (const float *)seg_in(),
                                (int64_t)G * CP * ND, (int64_t)CP * ND, ND, y, (float *)nullptr, seg_in(), 0,
                                (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, (int64_t)q.seg,
@@ -3029,10 +3045,12 @@ struct Launcher {
 
     template <bool ZOH, bool MAP, bool DLT>
     bool pscan_block(int64_t t0, int64_t len) {
-        switch (q.nt) {
-            case 4: pscans<4, ZOH, MAP, DLT>(t0, len); return true;
-            case 8: pscans<8, ZOH, MAP, DLT>(t0, len); return true;
-            case 16: pscans<16, ZOH, MAP, DLT>(t0, len); return true;
+        switch (q.nt * 32 + q.ns) {
+            case 4 * 32 + 1: pscans<4, 1, ZOH, MAP, DLT>(t0, len); return true;
+            case 8 * 32 + 1: pscans<8, 1, ZOH, MAP, DLT>(t0, len); return true;
+            case 16 * 32 + 1: pscans<16, 1, ZOH, MAP, DLT>(t0, len); return true;
+            case 16 * 32 + 2: pscans<16, 2, ZOH, MAP, DLT>(t0, len); return true;
+            case 16 * 32 + 4: pscans<16, 4, ZOH, MAP, DLT>(t0, len); return true;
             default: return false;
         }
     }
@@ -3058,7 +3076,7 @@ struct Launcher {
             }
         }
         if (q.order == 3) {
-            if (q.ns != 1 || (q.var & ~(kZoh | kOutMap)) || (q.K != 2 && q.K != 4)) return false;
+            if ((q.var & ~(kZoh | kOutMap)) || (q.K != 2 && q.K != 4)) return false;
             return q.K == 4 ? pscan_var<true>(t0, len) : pscan_var<false>(t0, len);
         }
         if (q.order == 2) {

@@ -35,9 +35,9 @@ static void check_layout(const pgf::Plan &q) {
     CHECK(q.L == 0 || (q.n_chunks - 1) * q.chunk_len < q.L);
     CHECK(q.chunk_len * q.D <= (int64_t(1) << 30));
     if (q.order == 3) {
-        // one thread per channel with every lane, five state planes with the
+        // up to 16 lanes per thread (N = 32, 64 on two, four), five planes with the
         // step size's flows, and room for the [3][B][N][D] + [3][B][D] sums
-        CHECK(q.ns == 1 && (q.K == 2 || q.K == 4) && q.comp == 1 + q.K);
+        CHECK(q.nt * q.ns == q.N && q.nt <= 16 && (q.K == 2 || q.K == 4) && q.comp == 1 + q.K);
         CHECK(w.lr - w.gacc >= (size_t)(3 * q.B * q.N * q.D + 3 * q.B * q.D) * sizeof(float));
     }
 }

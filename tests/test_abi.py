@@ -155,8 +155,8 @@ def test_parameter_flow_plans():
     p8 = binding.plan(1, 131072, 1536, 16, 8, order=3)
     assert p1 == p8 and p1["n_per_thread"] == 16
     assert len({binding.workspace_bytes(1, L, 1536, 16, 1, order=3) for L in (1, 8192, 131072)}) == 1
-    with pytest.raises(RuntimeError, match="UNSUPPORTED"):
-        binding.plan(1, 100, 16, 64, 1, order=3)
+    p64 = binding.plan(1, 100, 16, 64, 1, order=3)       # four threads per channel
+    assert p64["n_per_thread"] == 16 and p64["n_split"] == 4
     with pytest.raises(RuntimeError, match="INVALID_ARG"):
         binding.plan(1, 100, 16, 16, 1, order=4)
     p = _valid_params()
@@ -321,8 +321,9 @@ def test_step_size_flows_plan():
     for order in (1, 2):
         with pytest.raises(RuntimeError, match="INVALID_ARG"):
             binding.plan(1, 100, 64, 16, 2, order=order, delta_flows=True)
-    with pytest.raises(RuntimeError, match="UNSUPPORTED"):
-        binding.plan(1, 100, 64, 32, 1, order=3, delta_flows=True)
+    for N in (32, 64):   # 16 lanes per thread, two and four threads per channel
+        p = binding.plan(1, 100, 64, N, 1, order=3, delta_flows=True)
+        assert p["n_per_thread"] == 16 and p["n_split"] == N // 16
 
 
 def test_support_matrix_has_kernels():
@@ -345,8 +346,8 @@ def test_support_matrix_has_kernels():
                                dict(order=3, act="silu"), dict(order=3, drive="zoh", act="silu")):
                         if kw.get("order") == 2 and K != 2:
                             continue
-                        ok = (kw.get("complex_a") and "order" not in kw) or \
-                            (N <= 16 and (K <= 2 or kw.get("order") == 3))
+                        ok = (kw.get("complex_a") and "order" not in kw) or kw.get("order") == 3 or \
+                            (N <= 16 and K <= 2)
                         if ok:
                             binding.plan(2, 3000, 256, N, K, in_dtype=dt, seg_len=seg, **kw)
                         else:

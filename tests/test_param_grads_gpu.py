@@ -75,7 +75,7 @@ def _check(inp, what, channels=None, scaled=False, record=None, **kw):
     assert max(errs) <= gu.TOL, (what, errs)
 
 
-@pytest.mark.parametrize("N,seg", [(16, 0), (8, 0), (4, 0), (16, -1), (16, 64)])
+@pytest.mark.parametrize("N,seg", [(16, 0), (8, 0), (4, 0), (16, -1), (16, 64), (32, 0), (64, 64), (32, -1)])
 def test_param_grads_parity(N, seg):
     inp = _case("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N)
     _check(inp, f"param N={N} seg={seg}", seg_len=seg)
@@ -161,7 +161,7 @@ def test_zero_adjoint_gives_zero_gradients():
 def test_argument_checks():
     inp = _case("tiny", seqlen=64)
     with pytest.raises(RuntimeError, match="UNSUPPORTED"):
-        binding.plan(1, 64, 16, 32, 1, order=3)
+        binding.plan(1, 64, 16, 32, 1, order=3, complex_a=True)
     pr = binding.make_params(1, 64, 16, 16, 1, order=1)
     lib = binding.lib()
     assert lib.pgf_param_grads(None, None, ctypes.byref(pr), None, None, None, None, None) == -1
@@ -178,7 +178,7 @@ def test_argument_checks():
 # GammaA gains the drive's derivative in A: (Delta Abar - e)/A * B x, from a
 # series for |Delta A| < 1/4 and from the closed form above.
 
-@pytest.mark.parametrize("N,seg", [(16, 0), (8, -1), (4, 64), (16, -1)])
+@pytest.mark.parametrize("N,seg", [(16, 0), (8, -1), (4, 64), (16, -1), (64, -1), (32, 64)])
 def test_param_grads_zoh_parity(N, seg):
     inp = _case("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N)
     _check(inp, f"param zoh N={N} seg={seg}", seg_len=seg, drive="zoh")
@@ -221,7 +221,8 @@ def _with_dres(inp, seed=17):
 
 @pytest.mark.parametrize("act,dres,drive,N,seg", [
     ("silu", True, "euler", 16, 0), ("silu", False, "euler", 8, -1), ("identity", True, "zoh", 16, 64),
-    ("silu", True, "zoh", 4, -1), ("silu", True, "euler", 16, -1), ("silu", True, "zoh", 16, 0)])
+    ("silu", True, "zoh", 4, -1), ("silu", True, "euler", 16, -1), ("silu", True, "zoh", 16, 0),
+    ("silu", True, "euler", 64, 0), ("silu", True, "zoh", 32, -1)])
 def test_param_grads_output_map_parity(act, dres, drive, N, seg):
     inp = _case("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N)
     if dres:
@@ -323,7 +324,8 @@ def test_param_grads_zoh_zero_eigenvalues():
 
 @pytest.mark.parametrize("drive,act,dres,N,seg", [
     ("euler", "identity", False, 16, 0), ("euler", "identity", False, 8, -1), ("zoh", "identity", False, 16, 64),
-    ("euler", "silu", True, 16, -1), ("zoh", "silu", True, 16, 0), ("zoh", "silu", True, 4, -1)])
+    ("euler", "silu", True, 16, -1), ("zoh", "silu", True, 16, 0), ("zoh", "silu", True, 4, -1),
+    ("euler", "identity", False, 64, 64), ("zoh", "silu", True, 32, 0), ("euler", "silu", True, 64, -1)])
 def test_param_grads_step_size_parity(drive, act, dres, N, seg):
     inp = _case("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N)
     if dres:
