@@ -1813,7 +1813,7 @@ __global__ __launch_bounds__(kThreads) void k_carry(
 // over them (group_sum, the same bits in each) and the per-channel partials
 // are written by the first of them.
 template <int NT, bool OUT, typename InT, bool ZOH = false, bool MAP = false, bool DLT = false, int NS = 1>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH || DLT ? 2 : 3))) void k_pscan(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ZOH || DLT || NS > 1 ? 2 : 3))) void k_pscan(
     const InT *__restrict__ x, const float *__restrict__ gy, const float *__restrict__ A,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *init, int64_t ibs, int64_t igs, int64_t ics,
