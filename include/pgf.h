@@ -107,7 +107,7 @@ typedef struct pgf_params {
     /* Which flows a call carries; read by the planning calls too.
      *   0 or 1: first order (pgf_scan_jvp).
      *   2: second order (pgf_scan_jvp2; needs n_dirs == 2 and N <= 16).
-     *   3: parameter flows (pgf_param_grads; N <= 16; n_dirs is not read). */
+     *   3: parameter flows (pgf_param_grads; any N; n_dirs is not read). */
     int32_t order;
     /* Model parameters (device, f32).  b_B / b_C may be NULL (= 0). */
     const float *A, *w_delta, *b_delta, *W_B, *W_C, *b_B, *b_C;
@@ -128,7 +128,8 @@ typedef struct pgf_params {
     /* Model variants of the first-order scan and of the parameter flows
      * (Sec. 3 output map, the appendix's zero-order-hold drive); zero for
      * the second order.  With any of them set, pgf_scan_jvp supports
-     * N <= 16 and K <= 2 (pgf_param_grads: N <= 16, as always).
+     * N <= 16 and K <= 2 for a real A (every N and K for a complex A;
+     * pgf_param_grads: every N).
      *   drive      : PGF_DRIVE_EULER or PGF_DRIVE_ZOH
      *   activation : PGF_ACT_IDENTITY or PGF_ACT_SILU
      *   D_res      : device, [D] f32 residual weight, or NULL (= 0)
