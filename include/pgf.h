@@ -106,7 +106,7 @@ typedef struct pgf_params {
     int32_t chunk_segs;
     /* Which flows a call carries; read by the planning calls too.
      *   0 or 1: first order (pgf_scan_jvp).
-     *   2: second order (pgf_scan_jvp2; needs n_dirs == 2 and N <= 16).
+     *   2: second order (pgf_scan_jvp2; needs n_dirs == 2; any N).
      *   3: parameter flows (pgf_param_grads; any N; n_dirs is not read). */
     int32_t order;
     /* Model parameters (device, f32).  b_B / b_C may be NULL (= 0). */

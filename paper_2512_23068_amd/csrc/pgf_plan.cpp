@@ -73,7 +73,6 @@ int make_plan(const pgf_params *p, Plan *plan, size_t ws_cap) {
     if ((double)K * B * (double)L * D > 9.0e18 / 16) return PGF_ERR_UNSUPPORTED;
 
     if (order == 2 && K != 2) return PGF_ERR_INVALID_ARG;
-    if (order == 2 && N > 16) return PGF_ERR_UNSUPPORTED;
     if (p->drive < 0 || p->drive > 1 || p->activation < 0 || p->activation > 1) return PGF_ERR_INVALID_ARG;
     const int var = (p->drive == PGF_DRIVE_ZOH ? 1 : 0) |
                     ((p->activation != PGF_ACT_IDENTITY || p->D_res) ? 2 : 0);

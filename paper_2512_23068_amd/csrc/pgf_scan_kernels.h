@@ -1467,21 +1467,22 @@ constexpr auto scan_kernel() {
 // aggregate pass over bf16 rows are held to three waves per SIMD (168 and
 // 152 VGPRs, no spills); the f32 aggregate pass spills there (slower) and
 // keeps two.
-template <int NT, bool OUT, typename InT>
+template <int NT, bool OUT, typename InT, int NS = 1>
 __global__ __launch_bounds__(kThreads)
-__attribute__((amdgpu_waves_per_eu(OUT || !std::is_same<InT, float>::value ? 3 : 1))) void k_scan2(
+__attribute__((amdgpu_waves_per_eu(NS > 1 ? 2 : (OUT || !std::is_same<InT, float>::value ? 3 : 1)))) void k_scan2(
     const InT *__restrict__ x, const InT *__restrict__ dx, const float *__restrict__ A,
     const float *__restrict__ w_delta, const float *__restrict__ b_delta, const float *__restrict__ bc,
     const float *__restrict__ init, int64_t ibs, int64_t igs, int64_t ics,
     float *__restrict__ y, float *__restrict__ dy, float *__restrict__ d2y, float *__restrict__ end_state,
     float *__restrict__ agg_h, float *__restrict__ agg_s,
     int64_t Bsz, int64_t L, int64_t D, int64_t t0, int64_t len, int64_t Tc, int64_t S, int G) {
-    constexpr int N = NT;
+    constexpr int N = NT * NS;   // NS threads per channel, NT lanes each
     constexpr int R = 6 * N;          // B, dBv, dBw, C, dCv, dCw
     constexpr int TT = NT >= 16 ? 4 : 8;   // prefetch depth, bounded by the VGPR budget
 
     const int tid = threadIdx.x;
-    const int64_t d_raw = (int64_t)blockIdx.x * kThreads + tid;
+    const int ns = tid % NS;
+    const int64_t d_raw = (int64_t)blockIdx.x * (kThreads / NS) + tid / NS;
     const bool active = d_raw < D;
     const int64_t d = active ? d_raw : D - 1;
     const int g = blockIdx.y;
@@ -1493,14 +1494,14 @@ __attribute__((amdgpu_waves_per_eu(OUT || !std::is_same<InT, float>::value ? 3 :
     float Af[NT], At[NT];
 #pragma unroll
     for (int i = 0; i < NT; ++i) {
-        Af[i] = A[d * N + i];
+        Af[i] = A[d * N + ns * NT + i];
         At[i] = Af[i] * kLog2e;
     }
     const float w = w_delta[d], bd = b_delta[d];
 
     float h[NT], hv[NT], hw[NT], hvw[NT];
     if constexpr (OUT) {
-        const float *ib = init + b * ibs + g * igs + d;
+        const float *ib = init + b * ibs + g * igs + (int64_t)ns * NT * D + d;
 #pragma unroll
         for (int i = 0; i < NT; ++i) {
             h[i] = ib[i * D];
@@ -1573,7 +1574,7 @@ __attribute__((amdgpu_waves_per_eu(OUT || !std::is_same<InT, float>::value ? 3 :
                     sDw += dw;
                     sDvw += dvw;
                 }
-                const float *rec = rec0 + t * R;
+                const float *rec = rec0 + t * R + ns * NT;
                 float yv = 0.0f, y1 = 0.0f, y2 = 0.0f, y3 = 0.0f;
 #pragma unroll
                 for (int i = 0; i < NT; ++i) {
@@ -1601,6 +1602,10 @@ __attribute__((amdgpu_waves_per_eu(OUT || !std::is_same<InT, float>::value ? 3 :
                     }
                 }
                 if constexpr (OUT) {
+                    yv = group_sum<NS>(yv);
+                    y1 = group_sum<NS>(y1);
+                    y2 = group_sum<NS>(y2);
+                    y3 = group_sum<NS>(y3);
                     if (active) {
                         const uint32_t o = (uint32_t)t * Du + du;
                         store_out(Yb, o, yv);
@@ -1629,7 +1634,7 @@ __attribute__((amdgpu_waves_per_eu(OUT || !std::is_same<InT, float>::value ? 3 :
     if (!active) return;
     if constexpr (OUT) {
         if (end_state) {
-            float *eb = end_state + b * ibs + d;
+            float *eb = end_state + b * ibs + (int64_t)ns * NT * D + d;
 #pragma unroll
             for (int i = 0; i < NT; ++i) {
                 eb[i * D] = h[i];
@@ -1642,11 +1647,13 @@ __attribute__((amdgpu_waves_per_eu(OUT || !std::is_same<InT, float>::value ? 3 :
         const int64_t base = (b * G + g) * 4;
 #pragma unroll
         for (int i = 0; i < NT; ++i) {
-            agg_h[(base * N + i) * D + d] = h[i];
-            agg_h[((base + 1) * N + i) * D + d] = hv[i];
-            agg_h[((base + 2) * N + i) * D + d] = hw[i];
-            agg_h[((base + 3) * N + i) * D + d] = hvw[i];
+            const int n = ns * NT + i;
+            agg_h[(base * N + n) * D + d] = h[i];
+            agg_h[((base + 1) * N + n) * D + d] = hv[i];
+            agg_h[((base + 2) * N + n) * D + d] = hw[i];
+            agg_h[((base + 3) * N + n) * D + d] = hvw[i];
         }
+        if (ns != 0) return;   // the per-channel sums once
         agg_s[base * D + d] = sD;
         agg_s[(base + 1) * D + d] = sDv;
         agg_s[(base + 2) * D + d] = sDw;
@@ -2864,15 +2871,15 @@ struct Launcher {
         }
     }
 
-    // Second order: one thread per channel with all N <= 16 states.
-    template <int NT>
+    // Second order: NS threads per channel with NT <= 16 states each.
+    template <int NT, int NS>
     void scans2(int64_t t0, int64_t len) {
         if (dry) return;
-        const unsigned gx = (unsigned)((q.D + kThreads - 1) / kThreads);
+        const unsigned gx = (unsigned)((q.D + kThreads / NS - 1) / (kThreads / NS));
         const int64_t ND = q.N * q.D;
         if (q.seg == 0) {
             Timed tm(3, st, !q.noalloc);
-            hipLaunchKernelGGL((k_scan2<NT, true, InT>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, dx, p.A,
+            hipLaunchKernelGGL((k_scan2<NT, true, InT, NS>), dim3(gx, 1, (unsigned)q.B), dim3(kThreads), 0, st, x, dx, p.A,
                                p.w_delta, p.b_delta, bcw(), state(), ND, (int64_t)0, q.B * ND, y, dy, d2y, state(),
                                (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0, len, q.chunk_len, len, 1);
             return;
@@ -2880,7 +2887,7 @@ struct Launcher {
         const int G = (int)((len + q.seg - 1) / q.seg);
         {
             Timed tm(1, st, !q.noalloc);
-            hipLaunchKernelGGL((k_scan2<NT, false, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
+            hipLaunchKernelGGL((k_scan2<NT, false, InT, NS>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
                                x, dx, p.A, p.w_delta, p.b_delta, bcw(), (const float *)nullptr, (int64_t)0, (int64_t)0,
                                (int64_t)0, y, dy, d2y, (float *)nullptr, agg_h(), agg_s(), q.B, q.L, q.D, t0, len,
                                q.chunk_len, (int64_t)q.seg, G);
@@ -2893,7 +2900,7 @@ struct Launcher {
         }
         {
             Timed tm(3, st, !q.noalloc);
-            hipLaunchKernelGGL((k_scan2<NT, true, InT>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
+            hipLaunchKernelGGL((k_scan2<NT, true, InT, NS>), dim3(gx, (unsigned)G, (unsigned)q.B), dim3(kThreads), 0, st,
                                x, dx, p.A, p.w_delta, p.b_delta, bcw(), seg_in(), (int64_t)G * 4 * ND, (int64_t)4 * ND,
                                ND, y, dy, d2y, (float *)nullptr, (float *)nullptr, (float *)nullptr, q.B, q.L, q.D, t0,
                                len, q.chunk_len, (int64_t)q.seg, G);
@@ -3080,11 +3087,12 @@ struct Launcher {
             return q.K == 4 ? pscan_var<true>(t0, len) : pscan_var<false>(t0, len);
         }
         if (q.order == 2) {
-            if (q.ns != 1) return false;
-            switch (q.nt) {
-                case 4: scans2<4>(t0, len); return true;
-                case 8: scans2<8>(t0, len); return true;
-                case 16: scans2<16>(t0, len); return true;
+            switch (q.nt * 32 + q.ns) {
+                case 4 * 32 + 1: scans2<4, 1>(t0, len); return true;
+                case 8 * 32 + 1: scans2<8, 1>(t0, len); return true;
+                case 16 * 32 + 1: scans2<16, 1>(t0, len); return true;
+                case 16 * 32 + 2: scans2<16, 2>(t0, len); return true;
+                case 16 * 32 + 4: scans2<16, 4>(t0, len); return true;
                 default: return false;
             }
         }

@@ -346,7 +346,7 @@ def test_support_matrix_has_kernels():
                                dict(order=3, act="silu"), dict(order=3, drive="zoh", act="silu")):
                         if kw.get("order") == 2 and K != 2:
                             continue
-                        ok = (kw.get("complex_a") and "order" not in kw) or kw.get("order") == 3 or \
+                        ok = (kw.get("complex_a") and "order" not in kw) or kw.get("order") in (2, 3) or \
                             (N <= 16 and K <= 2)
                         if ok:
                             binding.plan(2, 3000, 256, N, K, in_dtype=dt, seg_len=seg, **kw)

@@ -33,7 +33,7 @@ def _check2(inp, what, **kw):
     assert np.all(np.isfinite(d2y.cpu().numpy())) and e <= gu.TOL, (what, e)
 
 
-@pytest.mark.parametrize("N,seg", [(16, 0), (8, 0), (4, 0), (16, -1), (16, 64)])
+@pytest.mark.parametrize("N,seg", [(16, 0), (8, 0), (4, 0), (16, -1), (16, 64), (32, 0), (64, 64), (32, -1)])
 def test_second_order_parity(N, seg):
     inp = gu.custom("mamba130m", batch=2, seqlen=1100, d_inner=70, d_state=N, n_dirs=2)
     _check2(inp, f"order2 N={N} seg={seg}", seg_len=seg)
@@ -99,9 +99,9 @@ def test_second_order_argument_checks():
     with pytest.raises(ValueError, match="two directions"):
         x, dx = gu.inputs_to_dev(inp)
         binding.scan_jvp2(x, dx[:1], gu.params_to_dev(inp))
-    # order 2 with N = 32 is not built; order mismatches are refused
+    # order 2 takes no variant; order mismatches are refused
     with pytest.raises(RuntimeError, match="UNSUPPORTED"):
-        binding.plan(1, 64, 16, 32, 2, order=2)
+        binding.plan(1, 64, 16, 32, 2, order=2, drive="zoh")
     with pytest.raises(RuntimeError, match="INVALID_ARG"):
         binding.plan(1, 64, 16, 16, 1, order=2)
     pr = binding.make_params(1, 64, 16, 16, 2, order=1)
